@@ -1,0 +1,331 @@
+"""CPU oracle for one binary upper-case-lower-case EinSum.
+
+TEST INFRASTRUCTURE, NOT PART OF THE PRODUCT.  Only ``tests/``,
+``__graft_entry__.smoke()`` and the CPU-baseline leg of ``bench.py`` may import
+this package.  It shares no code with the HIP library
+(``paper_2603_08957_amd``) and never imports it.
+
+The arithmetic lives in ``tre_oracle.c`` (plain C, fp64, single-threaded);
+this module only marshals numpy arrays through ctypes, plus two relational
+helpers written out in numpy:
+
+* :func:`restrict` -- the selections of Sec. 5 (Eq. "eqn_tr": sigma over the
+  promoted labels) used to evaluate only a sample of output keys exactly;
+* :func:`stack_rows` -- the re-composition of Sec. 6 (the STACK aggregate) for
+  the case where a promoted label's tile size grows, which the GNN chain with
+  per-vertex vectors needs between its two EinSums.
+
+Paper: Tang et al., "Automated Tensor-Relational Decomposition for
+Large-Scale Sparse Tensor Computation", PVLDB 19(6), 2026.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "tre_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+
+ERRORS = {
+    0: "OK",
+    1: "ARG",
+    2: "PARSE",
+    3: "SPLIT",
+    4: "SHAPE",
+    5: "UNSORTED",
+    6: "DUPKEY",
+    7: "KEYRANGE",
+    8: "NOMEM",
+}
+
+DTYPES = {"f32": 0, "bf16": 1, "f64": 2}
+
+
+class OracleError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        self.category = ERRORS.get(code, str(code))
+        super().__init__(f"oracle {where}: {self.category}")
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (plain C, -O2, no OpenMP)."""
+    if force or not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+        tmp = _LIB_PATH + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-std=c11", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build()
+        L = ctypes.CDLL(_LIB_PATH)
+        P = ctypes.c_void_p
+        i64 = ctypes.c_int64
+        L.orc_plan_size.restype = i64
+        L.orc_plan_make.argtypes = [ctypes.c_char_p, ctypes.c_char_p, P, P, P]
+        L.orc_plan_make.restype = ctypes.c_int
+        L.orc_plan_desc.argtypes = [P, P, P, P, P, P]
+        L.orc_plan_desc.restype = None
+        L.orc_check_keys.argtypes = [P, ctypes.c_int, P, i64]
+        L.orc_check_keys.restype = ctypes.c_int
+        L.orc_expand.argtypes = [P, ctypes.c_int, P, i64, P, ctypes.c_int, P, P, P, i64]
+        L.orc_expand.restype = i64
+        L.orc_keys_from_coo.argtypes = [P, ctypes.c_int, P, i64, P, P]
+        L.orc_keys_from_coo.restype = ctypes.c_int
+        L.orc_join.argtypes = [P, P, i64, P, i64, P, P, P, P]
+        L.orc_join.restype = ctypes.c_int
+        L.orc_eval.argtypes = [P, P, P, i64, P, P, i64, P, i64, P, P, P]
+        L.orc_eval.restype = ctypes.c_int
+        L.orc_free.argtypes = [P]
+        L.orc_free.restype = None
+        L.orc_f32_to_bf16.argtypes = [P, P, i64]
+        L.orc_f32_to_bf16.restype = None
+        _lib = L
+    return _lib
+
+
+def _ptr(a: np.ndarray | None):
+    if a is None:
+        return None
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+@dataclass
+class Plan:
+    """Parsed EinSum with its promoted labels and tile sizes (Sec. 4.2-4.3)."""
+
+    einsum: str
+    upper: str
+    extents: dict
+    tiles: dict
+
+    def __post_init__(self):
+        L = lib()
+        self._buf = np.zeros(int(L.orc_plan_size()), dtype=np.uint8)
+        ext = np.zeros(26, dtype=np.int64)
+        til = np.ones(26, dtype=np.int32)
+        for k, v in self.extents.items():
+            ext[ord(k) - 97] = v
+        for k, v in (self.tiles or {}).items():
+            til[ord(k) - 97] = v
+        rc = L.orc_plan_make(self.einsum.encode(), self.upper.encode(), _ptr(ext), _ptr(til), _ptr(self._buf))
+        if rc != 0:
+            raise OracleError(rc, "plan")
+        nl = np.zeros(3, np.int32)
+        nk = np.zeros(3, np.int32)
+        te = np.zeros(3, np.int64)
+        labs = np.zeros(78, np.int32)
+        klabs = np.zeros(78, np.int32)
+        L.orc_plan_desc(_ptr(self._buf), _ptr(nl), _ptr(nk), _ptr(te), _ptr(labs), _ptr(klabs))
+        self.n_labels = [int(x) for x in nl]
+        self.key_arity = [int(x) for x in nk]
+        self.tile_elems = [int(x) for x in te]
+        self.labels = ["".join(chr(97 + c) for c in labs[o * 26:o * 26 + nl[o]]) for o in range(3)]
+        self.key_labels = ["".join(chr(97 + c) for c in klabs[o * 26:o * 26 + nk[o]]) for o in range(3)]
+        up = set(self.upper)
+        self.tile_shape = []
+        for o in range(3):
+            shp = []
+            for c in self.labels[o]:
+                shp.append(int(self.tiles[c]) if c in up else int(self.extents[c]))
+            self.tile_shape.append(tuple(shp))
+
+    @property
+    def handle(self):
+        return _ptr(self._buf)
+
+
+def check_keys(plan: Plan, op: int, keys: np.ndarray) -> str:
+    keys = np.ascontiguousarray(keys, dtype=np.int32)
+    rc = lib().orc_check_keys(plan.handle, op, _ptr(keys), keys.shape[0])
+    return ERRORS[rc]
+
+
+def expand(plan: Plan, op: int, keys: np.ndarray, tiles: np.ndarray, dtype: str):
+    """Scalar COO of a relation: (coords [nnz, n_labels] int64, vals fp64, tuple ids)."""
+    L = lib()
+    keys = np.ascontiguousarray(keys, dtype=np.int32)
+    tiles = np.ascontiguousarray(tiles)
+    n = int(keys.shape[0])
+    nnz = L.orc_expand(plan.handle, op, _ptr(keys), n, _ptr(tiles), DTYPES[dtype], None, None, None, 0)
+    nl = plan.n_labels[op]
+    coords = np.zeros((max(nnz, 1), nl), dtype=np.int64)
+    vals = np.zeros(max(nnz, 1), dtype=np.float64)
+    tup = np.zeros(max(nnz, 1), dtype=np.int64)
+    got = L.orc_expand(plan.handle, op, _ptr(keys), n, _ptr(tiles), DTYPES[dtype], _ptr(coords), _ptr(vals),
+                       _ptr(tup), nnz)
+    assert got == nnz
+    return coords[:nnz], vals[:nnz], tup[:nnz]
+
+
+def keys_from_coo(plan: Plan, op: int, coords: np.ndarray) -> np.ndarray:
+    L = lib()
+    coords = np.ascontiguousarray(coords, dtype=np.int64)
+    n = ctypes.c_int64(0)
+    p = ctypes.c_void_p(0)
+    rc = L.orc_keys_from_coo(plan.handle, op, _ptr(coords), coords.shape[0], ctypes.byref(n), ctypes.byref(p))
+    if rc != 0:
+        raise OracleError(rc, "keys_from_coo")
+    r = plan.key_arity[op]
+    out = np.zeros((n.value, r), dtype=np.int32)
+    if n.value and r:
+        ctypes.memmove(_ptr(out), p, out.nbytes)
+    if p.value:
+        L.orc_free(p)
+    return out
+
+
+def join(plan: Plan, ukeys: np.ndarray, vkeys: np.ndarray):
+    """Key-level join + GROUP BY: (pairs [n_pairs, 2] int32 in (w_key, u, v)
+    order, output keys [n_w, r_W] int32 sorted)."""
+    L = lib()
+    ukeys = np.ascontiguousarray(ukeys, dtype=np.int32)
+    vkeys = np.ascontiguousarray(vkeys, dtype=np.int32)
+    np_ = ctypes.c_int64(0)
+    nw = ctypes.c_int64(0)
+    pp = ctypes.c_void_p(0)
+    pw = ctypes.c_void_p(0)
+    rc = L.orc_join(plan.handle, _ptr(ukeys), ukeys.shape[0], _ptr(vkeys), vkeys.shape[0], ctypes.byref(np_),
+                    ctypes.byref(pp), ctypes.byref(nw), ctypes.byref(pw))
+    if rc != 0:
+        raise OracleError(rc, "join")
+    pairs = np.zeros((np_.value, 2), dtype=np.int32)
+    rw = plan.key_arity[2]
+    wkeys = np.zeros((nw.value, rw), dtype=np.int32)
+    if np_.value:
+        ctypes.memmove(_ptr(pairs), pp, pairs.nbytes)
+    if nw.value and rw:
+        ctypes.memmove(_ptr(wkeys), pw, wkeys.nbytes)
+    for p in (pp, pw):
+        if p.value:
+            L.orc_free(p)
+    return pairs, wkeys
+
+
+def evaluate(plan: Plan, ucoo, uval, vcoo, vval, wkeys: np.ndarray):
+    """Value-level result on the listed output keys: (acc, mag, n_outside) with
+    acc/mag of shape [n_w, tile_elems(W)] in fp64."""
+    L = lib()
+    ucoo = np.ascontiguousarray(ucoo, dtype=np.int64)
+    vcoo = np.ascontiguousarray(vcoo, dtype=np.int64)
+    uval = np.ascontiguousarray(uval, dtype=np.float64)
+    vval = np.ascontiguousarray(vval, dtype=np.float64)
+    wkeys = np.ascontiguousarray(wkeys, dtype=np.int32)
+    nw = int(wkeys.shape[0])
+    tw = plan.tile_elems[2]
+    acc = np.zeros((nw, tw), dtype=np.float64)
+    mag = np.zeros((nw, tw), dtype=np.float64)
+    nout = ctypes.c_int64(0)
+    rc = L.orc_eval(plan.handle, _ptr(ucoo), _ptr(uval), ucoo.shape[0], _ptr(vcoo), _ptr(vval), vcoo.shape[0],
+                    _ptr(wkeys), nw, _ptr(acc), _ptr(mag), ctypes.byref(nout))
+    if rc != 0:
+        raise OracleError(rc, "eval")
+    return acc, mag, int(nout.value)
+
+
+def f32_to_bf16(x: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bits (uint16), round to nearest even."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    y = np.zeros(x.shape, dtype=np.uint16)
+    lib().orc_f32_to_bf16(_ptr(x), _ptr(y), x.size)
+    return y
+
+
+def bf16_to_f64(b: np.ndarray) -> np.ndarray:
+    return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+@dataclass
+class Result:
+    pairs: np.ndarray
+    wkeys: np.ndarray
+    acc: np.ndarray
+    mag: np.ndarray
+    n_outside: int
+
+
+def _coo_of(plan: Plan, op: int, rel: dict):
+    if "coo" in rel:
+        return rel["coo"][0], rel["coo"][1]
+    c, v, _ = expand(plan, op, rel["keys"], rel["tiles"], rel["dtype"])
+    return c, v
+
+
+def run(plan: Plan, U: dict, V: dict) -> Result:
+    """Full oracle evaluation of one EinSum over two relations.
+
+    A relation is a dict with ``keys`` ([n, r] int32) and either ``tiles`` +
+    ``dtype`` (expanded here) or ``coo`` = (coords, vals) over global
+    coordinates; for a COO relation without ``keys`` the key set is derived
+    from the entries."""
+    ukeys = U["keys"] if "keys" in U else keys_from_coo(plan, 0, U["coo"][0])
+    vkeys = V["keys"] if "keys" in V else keys_from_coo(plan, 1, V["coo"][0])
+    pairs, wkeys = join(plan, ukeys, vkeys)
+    uc, uv = _coo_of(plan, 0, U)
+    vc, vv = _coo_of(plan, 1, V)
+    acc, mag, nout = evaluate(plan, uc, uv, vc, vv, wkeys)
+    return Result(pairs, wkeys, acc, mag, nout)
+
+
+def restrict(plan: Plan, ukeys: np.ndarray, vkeys: np.ndarray, sample_wkeys: np.ndarray):
+    """Boolean masks over the U and V tuples that can contribute to the
+    sampled output keys (Sec. 5, Eq. "eqn_tr": W restricted to a set S of
+    promoted-label values only needs the tuples selected by sigma on S).
+
+    A U tuple is kept when its projection on W's promoted labels that U owns
+    is the projection of some key in S and its join key meets a kept V
+    tuple's; likewise for V.  Every pair whose output key is in S survives, so
+    evaluating the kept tuples gives the exact result on S."""
+    ukeys = np.asarray(ukeys, dtype=np.int32).reshape(len(ukeys), -1)
+    vkeys = np.asarray(vkeys, dtype=np.int32).reshape(len(vkeys), -1)
+    S = np.asarray(sample_wkeys, dtype=np.int32).reshape(len(sample_wkeys), -1)
+    kl = plan.key_labels
+
+    def proj_mask(keys, op):
+        cols_op, cols_w = [], []
+        for a, c in enumerate(kl[op]):
+            if c in kl[2]:
+                cols_op.append(a)
+                cols_w.append(kl[2].index(c))
+        if not cols_op:
+            return np.ones(len(keys), dtype=bool)
+        allowed = {tuple(r) for r in S[:, cols_w].tolist()}
+        return np.array([tuple(r) in allowed for r in keys[:, cols_op].tolist()], dtype=bool)
+
+    mu = proj_mask(ukeys, 0)
+    mv = proj_mask(vkeys, 1)
+    ju = [a for a, c in enumerate(kl[0]) if c in kl[1]]
+    jv = [kl[1].index(kl[0][a]) for a in ju]
+    if ju:
+        ku = {tuple(r) for r in ukeys[mu][:, ju].tolist()}
+        mv &= np.array([tuple(r) in ku for r in vkeys[:, jv].tolist()], dtype=bool)
+        kv = {tuple(r) for r in vkeys[mv][:, jv].tolist()}
+        mu &= np.array([tuple(r) in kv for r in ukeys[:, ju].tolist()], dtype=bool)
+    return mu, mv
+
+
+def stack_rows(keys: np.ndarray, tiles: np.ndarray, group: int):
+    """Re-compose a relation keyed by one promoted label with tile size 1 (one
+    row per key) into a relation with tile size ``group`` along that label:
+    new key = key // group, the row lands at position key % group, and rows
+    that are absent stay zero (the STACK aggregate of Sec. 6, grouped by the
+    new key)."""
+    keys = np.asarray(keys).reshape(-1)
+    rows = np.asarray(tiles).reshape(len(keys), -1)
+    nk = keys // group
+    uk, inv = np.unique(nk, return_inverse=True)
+    out = np.zeros((len(uk), group, rows.shape[1]), dtype=rows.dtype)
+    out[inv, keys % group] = rows
+    return uk.reshape(-1, 1).astype(np.int32), out.reshape(len(uk), -1)
