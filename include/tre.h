@@ -1,0 +1,211 @@
+/*
+ * tre.h -- C ABI of the tensor-relational EinSum library for AMD Instinct
+ * MI355X (gfx950).
+ *
+ * One call evaluates one binary EinSum whose operands are tensor relations
+ * (Tang et al., "Automated Tensor-Relational Decomposition for Large-Scale
+ * Sparse Tensor Computation", PVLDB 19(6), 2026):
+ *
+ *   - Sec. 3, Eq. "Einsum": W[lW] = sum over labels not in W of U[lU] * V[lV].
+ *   - Sec. 4.2: a relation stores one tuple per key of its promoted
+ *     (upper-case) labels; each tuple holds a dense tile over the demoted
+ *     (lower-case) labels.  Here a promoted label l may also carry a tile size
+ *     t_l: the global index is t_l * L + l', L is the tuple attribute and l'
+ *     indexes the tile (t_l = 1 is the paper's plain promoted label).
+ *   - Sec. 5, Eq. "eqn-TRA" and its SQL form
+ *         SELECT upper(W), SUM(K(valU, valV)) FROM U NATURAL JOIN V
+ *         GROUP BY upper(W)
+ *     is what tre_join + tre_contract compute: (1) a join on the promoted
+ *     labels the operands share, (2) the kernel K -- the EinSum restricted to
+ *     the tile labels -- on every matched tile pair, (3) a sum of the partial
+ *     tiles grouped by W's promoted labels.
+ *
+ * Conventions for every entry point:
+ *   - Device pointers are HIP device memory owned by the caller; the library
+ *     allocates no device memory in tre_join / tre_contract / tre_execute and
+ *     uses only the caller's workspace.  Host pointers are marked "host".
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *   - Keys: int32, row-major [n x r], r = number of promoted labels of the
+ *     operand, attributes in the order the labels appear in the operand's
+ *     string; rows strictly increasing in lexicographic order; attribute of
+ *     label l in [0, extent_l / t_l).  A relation with r = 0 holds at most one
+ *     tuple and its key pointer is ignored.
+ *   - Tiles: [n x tile_elems] contiguous, each tile row-major over ALL the
+ *     operand's labels in string order, with extent t_l for a promoted label
+ *     and the full extent for a demoted one.  Inputs are fp32 or bf16 (raw
+ *     bits, uint16); W tiles are always fp32.
+ *   - Output order: W keys sorted lexicographically; the pair list in order of
+ *     (W key, u index, v index), u/v being positions in the caller's arrays.
+ *   - Errors are returned as tre_status; the library never aborts and never
+ *     prints.  tre_last_error() gives a thread-local detail string.
+ */
+#ifndef TRE_H
+#define TRE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    TRE_OK = 0,
+    TRE_E_ARG = 1,        /* null pointer, negative size, bad option */
+    TRE_E_PARSE = 2,      /* malformed EinSum string */
+    TRE_E_SPLIT = 3,      /* promoted-label set names a label not in the EinSum */
+    TRE_E_SHAPE = 4,      /* extent < 1, tile not dividing extent, key space > 64 bits */
+    TRE_E_DTYPE = 5,      /* unsupported input dtype */
+    TRE_E_UNSORTED = 6,   /* keys not in increasing lexicographic order */
+    TRE_E_DUPKEY = 7,     /* repeated key (or r = 0 with more than one tuple) */
+    TRE_E_KEYRANGE = 8,   /* key attribute outside [0, extent / t) */
+    TRE_E_CAPACITY = 9,   /* caller buffer too small; required sizes are reported */
+    TRE_E_WORKSPACE = 10, /* workspace too small for this input */
+    TRE_E_DEVICE = 11,    /* a HIP runtime call failed */
+    TRE_E_STATE = 12      /* join result does not belong to this plan / workspace */
+} tre_status;
+
+typedef enum { TRE_F32 = 0, TRE_BF16 = 1 } tre_dtype;
+
+typedef struct tre_plan_s *tre_plan_t;
+
+typedef struct {
+    int32_t validate_keys;      /* nonzero: check key order, uniqueness and range on the device (default 1) */
+    int32_t max_pairs_per_unit; /* work-unit length cap; 0 = chosen from the pair count */
+    int32_t reserved[6];
+} tre_options;
+
+/* Static facts about a plan (host). */
+typedef struct {
+    int32_t key_arity[3];     /* r_U, r_V, r_W */
+    int64_t tile_elems[3];    /* elements per tile of U, V, W */
+    int32_t n_join;           /* promoted labels shared by U and V */
+    int32_t kernel_class;     /* 0 = MFMA tile GEMM, 1 = vector (scale / GEMV / dot) */
+    int64_t batch, m, n, k;   /* per-pair contraction: W[b,m,n] += sum_k U[b,m,k] V[b,k,n] */
+    int64_t flops_per_pair;   /* 2 * batch * m * n * k */
+    char key_labels[3][27];   /* promoted labels of U, V, W in key order (NUL-terminated) */
+    char roles[27];           /* per letter a..z: 'b','m','n','k','p' (pre-sum) or '.' unused */
+    int32_t group_needs_sort; /* 1 if pairs are radix-sorted by W key */
+    int32_t v_needs_sort;     /* 1 if V is radix-sorted by its join key */
+} tre_plan_info;
+
+/* Result of tre_join, consumed by tre_contract (host struct; the pair list,
+ * segments and packed output keys stay in the workspace). */
+typedef struct {
+    int64_t n_u, n_v;
+    int64_t n_pairs;          /* matched tile pairs */
+    int64_t n_w;              /* output tuples (distinct W keys) */
+    uint64_t internal[16];    /* workspace layout; do not modify */
+} tre_join_result;
+
+/* Optional per-phase device timings (milliseconds, hipEvent based). */
+typedef struct {
+    float join_ms;            /* key packing, validation, sort, join, group-by */
+    float contract_ms;        /* work units and tile contraction */
+    float reduce_ms;          /* segmented sum of split segments */
+    float total_ms;
+    int64_t n_units;
+    int64_t n_split_segments;
+} tre_timing;
+
+/* tre_plan -- parse and classify one binary EinSum (host only, no device work).
+ *   einsum : host string "lhs0,lhs1->out" of lower-case letters; exactly two
+ *            inputs; no label repeated within an operand; every output label
+ *            appears in an input (Sec. 3 general form).
+ *   upper  : host string, the promoted labels (Sec. 4.3 upper case); may be "".
+ *   extent : host [26], indexed by letter - 'a'; >= 1 for used labels.
+ *   tile   : host [26]; for a promoted label 1 <= t <= extent and extent % t == 0;
+ *            ignored for demoted labels (their tile extent is the full extent).
+ *   in_dtype : TRE_F32 or TRE_BF16 for both inputs; accumulation and W are fp32.
+ *   opt    : host, may be NULL for defaults.
+ *   out    : receives a host-owned, immutable plan; thread-safe to share. */
+tre_status tre_plan(const char *einsum, const char *upper, const int64_t *extent, const int32_t *tile,
+                    tre_dtype in_dtype, const tre_options *opt, tre_plan_t *out);
+
+tre_status tre_plan_get_info(tre_plan_t plan, tre_plan_info *info);
+
+void tre_plan_destroy(tre_plan_t plan);
+
+/* Upper bound on the workspace needed for n_u and n_v input tuples and at most
+ * max_pairs matched pairs (bytes, a multiple of 256). */
+size_t tre_workspace_bytes(tre_plan_t plan, int64_t n_u, int64_t n_v, int64_t max_pairs);
+
+/* Largest pair count a workspace of ws_bytes can hold for n_u, n_v. */
+int64_t tre_workspace_max_pairs(tre_plan_t plan, int64_t n_u, int64_t n_v, size_t ws_bytes);
+
+/* tre_join -- step (1) of Sec. 5 plus the GROUP BY keys: validate keys
+ * (optional), sort V by join key if its key order does not start with the
+ * join labels, build the matched pair list on the device (binary-search
+ * counts, scan, load-balanced expansion), sort pairs by W key (stable LSD
+ * radix) and run-length encode them into output keys and segments.
+ *   u_keys, v_keys : device, as in the conventions above.
+ *   ws, ws_bytes   : device workspace (256-byte aligned); must stay untouched
+ *                    until the matching tre_contract has completed.
+ *   out            : host; receives n_pairs and n_w.
+ * Synchronizes the stream (twice) to read the pair and key counts.
+ * TRE_E_WORKSPACE (out->n_pairs set) if the pairs do not fit; key errors are
+ * reported as TRE_E_UNSORTED / TRE_E_DUPKEY / TRE_E_KEYRANGE. */
+tre_status tre_join(tre_plan_t plan, const int32_t *u_keys, int64_t n_u, const int32_t *v_keys, int64_t n_v,
+                    void *ws, size_t ws_bytes, void *stream, tre_join_result *out, tre_timing *timing);
+
+/* tre_contract -- steps (2) and (3) of Sec. 5: contract every matched tile
+ * pair and sum the results per output key.  Pairs of one output key are
+ * processed together (split into bounded work units when long); a unit
+ * accumulates in registers; split keys are summed by an atomic-free
+ * fixed-order segmented reduction, so results are run-to-run deterministic.
+ *   u_tiles, v_tiles : device tiles of the same arrays given to tre_join.
+ *   w_keys  : device [w_cap x r_W] int32 (may be NULL when r_W = 0).
+ *   w_tiles : device [w_cap x tile_elems(W)] fp32.
+ *   pairs_out : device [pair_cap x 2] int32 (u, v) or NULL.
+ * TRE_E_CAPACITY if w_cap < n_w or (pairs_out and pair_cap < n_pairs).
+ * Asynchronous on the stream unless timing is non-NULL (then it waits). */
+tre_status tre_contract(tre_plan_t plan, const tre_join_result *jr, const void *u_tiles, const void *v_tiles,
+                        int32_t *w_keys, int64_t w_cap, float *w_tiles, int32_t *pairs_out, int64_t pair_cap,
+                        void *stream, tre_timing *timing);
+
+/* tre_execute -- tre_join followed by tre_contract.  n_w / n_pairs (host) are
+ * always written when the join succeeded, also with TRE_E_CAPACITY. */
+tre_status tre_execute(tre_plan_t plan, const int32_t *u_keys, int64_t n_u, const void *u_tiles,
+                       const int32_t *v_keys, int64_t n_v, const void *v_tiles, int32_t *w_keys, float *w_tiles,
+                       int64_t w_cap, int64_t *n_w, int32_t *pairs_out, int64_t pair_cap, int64_t *n_pairs,
+                       void *ws, size_t ws_bytes, void *stream, tre_timing *timing);
+
+/* --- chain glue between two EinSums (Sec. 6, repartition) --------------- */
+
+/* Round fp32 to bf16 (nearest even; NaN stays NaN).  x, y device, n elements. */
+tre_status tre_cast_f32_bf16(const float *x, uint16_t *y, int64_t n, void *stream);
+
+/* Re-compose a relation keyed by ONE promoted label from tile size t_in to
+ * t_out = group * t_in along that label (the STACK aggregate of Sec. 6 where
+ * the new promoted set equals the old one):
+ *   keys     : device [n] int32 sorted increasing (arity 1).
+ *   tiles    : device [n x row_elems] of elem_bytes-wide elements; a tile is
+ *              t_in rows along the label times the remaining elements.
+ *   out_keys : device [out_cap] int32 = distinct key / group.
+ *   out_tiles: device [out_cap x group*row_elems]; absent rows are zero.
+ *   ws       : device workspace of at least tre_stack_workspace_bytes(n).
+ *   n_out    : host; synchronizes to read it.  TRE_E_CAPACITY if out_cap is short. */
+size_t tre_stack_workspace_bytes(int64_t n);
+tre_status tre_stack_rows(const int32_t *keys, int64_t n, const void *tiles, int64_t row_elems, int32_t group,
+                          int32_t elem_bytes, int32_t *out_keys, void *out_tiles, int64_t out_cap, int64_t *n_out,
+                          void *ws, size_t ws_bytes, void *stream);
+
+/* --- input preparation --------------------------------------------------- */
+
+/* Materialise tiles from scalar entries: tiles[slot[e] * tile_elems + offset[e]]
+ * = value[e] after zero-filling n_tiles tiles.  slot/offset device int64,
+ * value device (elem_bytes = 2 for bf16 bits or 4 for fp32).  Entries must
+ * address distinct positions (else the last writer is unspecified). */
+tre_status tre_tiles_from_entries(const int64_t *slot, const int64_t *offset, const void *value, int64_t n_entries,
+                                  int32_t elem_bytes, void *tiles, int64_t n_tiles, int64_t tile_elems, void *stream);
+
+/* --- errors -------------------------------------------------------------- */
+const char *tre_status_str(tre_status s);
+const char *tre_last_error(void);
+const char *tre_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TRE_H */

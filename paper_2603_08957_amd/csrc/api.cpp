@@ -1,0 +1,288 @@
+// C-ABI entry points: argument checks, workspace layout, phase ordering,
+// the two count read-backs of the join, capacity checks and timing.
+#include <algorithm>
+#include <cstring>
+
+#include "tre_internal.h"
+
+using namespace tre;
+
+namespace {
+
+constexpr uint64_t kMagic = 0x7472655f6a6f696eull;  // "tre_join"
+constexpr int kTargetWorkgroups = 1024;              // 4 per CU on 256 CUs
+
+tre_status dev_fail(hipError_t e, const char* where) {
+    set_error(std::string(where) + ": " + hipGetErrorString(e));
+    return TRE_E_DEVICE;
+}
+
+struct Timer {
+    bool on = false;
+    hipEvent_t ev[4] = {};
+    int n = 0;
+    explicit Timer(bool enable) : on(enable) {
+        if (on)
+            for (auto& e : ev)
+                if (hipEventCreate(&e) != hipSuccess) on = false;
+    }
+    ~Timer() {
+        for (auto& e : ev)
+            if (e) (void)hipEventDestroy(e);
+    }
+    void mark(hipStream_t s) {
+        if (on && n < 4) (void)hipEventRecord(ev[n++], s);
+    }
+    float between(int a, int b) {
+        float ms = 0.f;
+        if (on && b < n) {
+            (void)hipEventSynchronize(ev[b]);
+            (void)hipEventElapsedTime(&ms, ev[a], ev[b]);
+        }
+        return ms;
+    }
+};
+
+tre_status key_error(int32_t flags) {
+    if (flags & 4) return TRE_E_KEYRANGE;
+    if (flags & 1) return TRE_E_UNSORTED;
+    if (flags & 2) return TRE_E_DUPKEY;
+    return TRE_OK;
+}
+
+int64_t blocks_per_unit(const Plan& p) {
+    if (p.kclass == KC_GEMM) {
+        const int64_t M = p.swap ? p.nN : p.nM, N = p.swap ? p.nM : p.nN;
+        return p.nB * ((M + 63) / 64) * ((N + 63) / 64);
+    }
+    return (p.tile_elems[2] + 255) / 256;
+}
+
+int64_t choose_unit(const Plan& p, const Layout& L, int64_t n_pairs, int64_t n_w) {
+    const int64_t bpu = blocks_per_unit(p);
+    int64_t pu;
+    if (p.opt.max_pairs_per_unit > 0) {
+        pu = p.opt.max_pairs_per_unit;
+    } else if (n_w * bpu >= kTargetWorkgroups) {
+        pu = std::max<int64_t>(n_pairs, 1);  // enough output blocks: one unit per key
+    } else {
+        pu = std::max<int64_t>(4, (n_pairs * bpu + kTargetWorkgroups - 1) / kTargetWorkgroups);
+    }
+    // partial tiles of split keys must fit: at most 2 * n_pairs / pu of them
+    const int64_t need = (2 * n_pairs + L.part_cap - 2) / std::max<int64_t>(L.part_cap - 1, 1);
+    return std::max<int64_t>(pu, std::max<int64_t>(need, 1));
+}
+
+}  // namespace
+
+extern "C" {
+
+tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const int32_t* v_keys, int64_t n_v,
+                    void* ws, size_t ws_bytes, void* stream, tre_join_result* out, tre_timing* timing) {
+    if (!plan || !out || n_u < 0 || n_v < 0 || !ws) {
+        set_error("tre_join: null plan/out/workspace or negative size");
+        return TRE_E_ARG;
+    }
+    const Plan& p = plan->p;
+    std::memset(out, 0, sizeof(*out));
+    out->n_u = n_u;
+    out->n_v = n_v;
+    if ((p.nk[0] > 0 && n_u > 0 && !u_keys) || (p.nk[1] > 0 && n_v > 0 && !v_keys)) {
+        set_error("tre_join: null key array");
+        return TRE_E_ARG;
+    }
+    if (reinterpret_cast<uintptr_t>(ws) % 256) {
+        set_error("tre_join: workspace must be 256-byte aligned");
+        return TRE_E_ARG;
+    }
+    if ((p.nk[0] == 0 && n_u > 1) || (p.nk[1] == 0 && n_v > 1)) {
+        set_error("tre_join: a relation without promoted labels holds at most one tuple");
+        return TRE_E_DUPKEY;
+    }
+    if (n_u >= INT32_MAX || n_v >= INT32_MAX) {
+        set_error("tre_join: more than 2^31 - 1 tuples");
+        return TRE_E_SHAPE;
+    }
+    const int64_t max_pairs = tre_workspace_max_pairs(plan, n_u, n_v, ws_bytes);
+    if (max_pairs < 0) {
+        set_error("tre_join: workspace smaller than tre_workspace_bytes(plan, n_u, n_v, 0)");
+        return TRE_E_WORKSPACE;
+    }
+    const Layout L = make_layout(p, n_u, n_v, max_pairs);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    char* w = reinterpret_cast<char*>(ws);
+    Timer tm(timing != nullptr);
+    tm.mark(s);
+    hipError_t e = launch_fill_zero(w + L.hdr, sizeof(WsHeader), s);
+    if (e != hipSuccess) return dev_fail(e, "header");
+    WsHeader* hdr = reinterpret_cast<WsHeader*>(w + L.hdr);
+    if (p.opt.validate_keys) {
+        if ((e = launch_validate(u_keys, n_u, p.nk[0], p.radix[0], &hdr->err_u, s)) != hipSuccess)
+            return dev_fail(e, "validate U");
+        if ((e = launch_validate(v_keys, n_v, p.nk[1], p.radix[1], &hdr->err_v, s)) != hipSuccess)
+            return dev_fail(e, "validate V");
+    }
+    WsHeader h{};
+    if (n_u > 0 && n_v > 0) {
+        if ((e = launch_join(p, L, w, u_keys, v_keys, s, 0)) != hipSuccess) return dev_fail(e, "join");
+    }
+    if ((e = hipMemcpyAsync(&h, hdr, sizeof(h), hipMemcpyDeviceToHost, s)) != hipSuccess)
+        return dev_fail(e, "count read-back");
+    if ((e = hipStreamSynchronize(s)) != hipSuccess) return dev_fail(e, "join sync");
+    tre_status ks = key_error(h.err_u);
+    if (ks == TRE_OK) ks = key_error(h.err_v);
+    if (ks != TRE_OK) {
+        set_error(std::string("tre_join: invalid keys in ") + (key_error(h.err_u) != TRE_OK ? "U" : "V"));
+        return ks;
+    }
+    const int64_t n_pairs = (n_u > 0 && n_v > 0) ? h.n_pairs : 0;
+    out->n_pairs = n_pairs;
+    if (n_pairs > max_pairs) {
+        set_error("tre_join: workspace too small for the matched pairs (see n_pairs)");
+        return TRE_E_WORKSPACE;
+    }
+    if (n_pairs >= INT32_MAX) {
+        set_error("tre_join: more than 2^31 - 1 pairs");
+        return TRE_E_SHAPE;
+    }
+    int64_t n_w = 0;
+    if (n_pairs > 0) {
+        if ((e = launch_group(p, L, w, u_keys, v_keys, n_pairs, s, 0)) != hipSuccess) return dev_fail(e, "group");
+        if ((e = hipMemcpyAsync(&h, hdr, sizeof(h), hipMemcpyDeviceToHost, s)) != hipSuccess)
+            return dev_fail(e, "key read-back");
+        if ((e = hipStreamSynchronize(s)) != hipSuccess) return dev_fail(e, "group sync");
+        n_w = h.n_w;
+    }
+    tm.mark(s);
+    out->n_w = n_w;
+    out->internal[0] = kMagic;
+    out->internal[1] = reinterpret_cast<uint64_t>(plan);
+    out->internal[2] = reinterpret_cast<uint64_t>(ws);
+    out->internal[3] = uint64_t(ws_bytes);
+    out->internal[4] = uint64_t(max_pairs);
+    if (timing) {
+        std::memset(timing, 0, sizeof(*timing));
+        timing->join_ms = tm.between(0, 1);
+        timing->total_ms = timing->join_ms;
+    }
+    return TRE_OK;
+}
+
+tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* u_tiles, const void* v_tiles,
+                        int32_t* w_keys, int64_t w_cap, float* w_tiles, int32_t* pairs_out, int64_t pair_cap,
+                        void* stream, tre_timing* timing) {
+    if (!plan || !jr) {
+        set_error("tre_contract: null plan or join result");
+        return TRE_E_ARG;
+    }
+    if (jr->internal[0] != kMagic || jr->internal[1] != reinterpret_cast<uint64_t>(plan)) {
+        set_error("tre_contract: join result was not produced by tre_join with this plan");
+        return TRE_E_STATE;
+    }
+    const Plan& p = plan->p;
+    const int64_t n_pairs = jr->n_pairs, n_w = jr->n_w;
+    if (w_cap < n_w || (pairs_out && pair_cap < n_pairs)) {
+        set_error("tre_contract: output capacity below n_w / n_pairs");
+        return TRE_E_CAPACITY;
+    }
+    if (n_pairs == 0) return TRE_OK;
+    if (!u_tiles || !v_tiles || !w_tiles || (p.nk[2] > 0 && !w_keys)) {
+        set_error("tre_contract: null tile or key buffer");
+        return TRE_E_ARG;
+    }
+    char* w = reinterpret_cast<char*>(jr->internal[2]);
+    const Layout L = make_layout(p, jr->n_u, jr->n_v, int64_t(jr->internal[4]));
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    Timer tm(timing != nullptr);
+    tm.mark(s);
+    const int64_t p_unit = choose_unit(p, L, n_pairs, n_w);
+    hipError_t e;
+    if ((e = launch_tables(p, reinterpret_cast<int32_t*>(w + L.tables), s)) != hipSuccess) return dev_fail(e, "tables");
+    if ((e = launch_units(p, L, w, n_pairs, n_w, p_unit, s)) != hipSuccess) return dev_fail(e, "units");
+    const int64_t unit_bound = n_w + n_pairs / p_unit + 1;
+    if ((e = launch_contract(p, L, w, u_tiles, v_tiles, w_tiles, n_pairs, n_w, unit_bound, s)) != hipSuccess)
+        return dev_fail(e, "contract");
+    tm.mark(s);
+    if (p_unit < n_pairs) {
+        const int64_t split_bound = std::min<int64_t>(n_w, n_pairs / (p_unit + 1) + 1);
+        if ((e = launch_reduce(p, L, w, w_tiles, split_bound, s)) != hipSuccess) return dev_fail(e, "reduce");
+    }
+    if ((e = launch_write_outputs(p, L, w, w_keys, pairs_out, n_pairs, n_w, s)) != hipSuccess)
+        return dev_fail(e, "outputs");
+    tm.mark(s);
+    if (timing) {
+        timing->contract_ms = tm.between(0, 1);
+        timing->reduce_ms = tm.between(1, 2);
+        timing->total_ms += tm.between(0, 2);
+        WsHeader h{};
+        if (hipMemcpy(&h, w + L.hdr, sizeof(h), hipMemcpyDeviceToHost) == hipSuccess) {
+            timing->n_units = h.n_units;
+            timing->n_split_segments = h.n_split;
+        }
+    }
+    return TRE_OK;
+}
+
+tre_status tre_execute(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const void* u_tiles,
+                       const int32_t* v_keys, int64_t n_v, const void* v_tiles, int32_t* w_keys, float* w_tiles,
+                       int64_t w_cap, int64_t* n_w, int32_t* pairs_out, int64_t pair_cap, int64_t* n_pairs,
+                       void* ws, size_t ws_bytes, void* stream, tre_timing* timing) {
+    tre_join_result jr;
+    tre_status st = tre_join(plan, u_keys, n_u, v_keys, n_v, ws, ws_bytes, stream, &jr, timing);
+    if (n_pairs) *n_pairs = jr.n_pairs;
+    if (n_w) *n_w = jr.n_w;
+    if (st != TRE_OK) return st;
+    return tre_contract(plan, &jr, u_tiles, v_tiles, w_keys, w_cap, w_tiles, pairs_out, pair_cap, stream, timing);
+}
+
+tre_status tre_cast_f32_bf16(const float* x, uint16_t* y, int64_t n, void* stream) {
+    if (n < 0 || (n > 0 && (!x || !y))) return TRE_E_ARG;
+    hipError_t e = launch_cast_bf16(x, y, n, reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TRE_OK : dev_fail(e, "cast");
+}
+
+size_t tre_stack_workspace_bytes(int64_t n) { return n < 0 ? 0 : stack_ws_bytes(n); }
+
+tre_status tre_stack_rows(const int32_t* keys, int64_t n, const void* tiles, int64_t row_elems, int32_t group,
+                          int32_t elem_bytes, int32_t* out_keys, void* out_tiles, int64_t out_cap, int64_t* n_out,
+                          void* ws, size_t ws_bytes, void* stream) {
+    if (n < 0 || row_elems < 1 || group < 1 || (elem_bytes != 2 && elem_bytes != 4) || !n_out || !ws ||
+        (n > 0 && (!keys || !tiles))) {
+        set_error("tre_stack_rows: bad argument");
+        return TRE_E_ARG;
+    }
+    if (ws_bytes < stack_ws_bytes(n)) return TRE_E_WORKSPACE;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    char* w = reinterpret_cast<char*>(ws);
+    *n_out = 0;
+    if (n == 0) return TRE_OK;
+    hipError_t e = launch_stack(keys, n, tiles, row_elems, group, elem_bytes, nullptr, nullptr, 0, w, s, 0);
+    if (e != hipSuccess) return dev_fail(e, "stack count");
+    int64_t cnt = 0;
+    const size_t cnt_off = (sizeof(int32_t) * size_t(n + 1) + 255) / 256 * 256;
+    if ((e = hipMemcpyAsync(&cnt, w + cnt_off, sizeof(cnt), hipMemcpyDeviceToHost, s)) != hipSuccess)
+        return dev_fail(e, "stack read-back");
+    if ((e = hipStreamSynchronize(s)) != hipSuccess) return dev_fail(e, "stack sync");
+    *n_out = cnt;
+    if (cnt > out_cap || !out_keys || !out_tiles) {
+        set_error("tre_stack_rows: output capacity below the number of stacked keys");
+        return TRE_E_CAPACITY;
+    }
+    e = launch_stack(keys, n, tiles, row_elems, group, elem_bytes, out_keys, out_tiles, cnt, w, s, 1);
+    return e == hipSuccess ? TRE_OK : dev_fail(e, "stack");
+}
+
+tre_status tre_tiles_from_entries(const int64_t* slot, const int64_t* offset, const void* value, int64_t n_entries,
+                                  int32_t elem_bytes, void* tiles, int64_t n_tiles, int64_t tile_elems,
+                                  void* stream) {
+    if (n_entries < 0 || n_tiles < 0 || tile_elems < 1 || (elem_bytes != 2 && elem_bytes != 4) ||
+        (n_entries > 0 && (!slot || !offset || !value)) || (n_tiles > 0 && !tiles)) {
+        set_error("tre_tiles_from_entries: bad argument");
+        return TRE_E_ARG;
+    }
+    hipError_t e = launch_tiles_from_entries(slot, offset, value, n_entries, elem_bytes, tiles, n_tiles, tile_elems,
+                                             reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TRE_OK : dev_fail(e, "tiles_from_entries");
+}
+
+}  // extern "C"

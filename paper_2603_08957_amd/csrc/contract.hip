@@ -1,0 +1,482 @@
+// Steps (2) and (3) of the tensor-relational EinSum (Sec. 5): the kernel K on
+// every matched tile pair and the sum of the results per output key.
+//
+// Pairs arrive sorted by output key; a segment is the run of pairs of one
+// key.  Segments are cut into work units of at most P pairs.  A workgroup
+// owns one (unit, output block) and accumulates Sum_{pairs in unit} K(U, V)
+// in registers, so no per-pair partial tile ever reaches memory.  A segment
+// that fits one unit is written straight to W; the units of a longer segment
+// write partial tiles that k_reduce sums in unit order (atomic-free, hence
+// deterministic).
+//
+// K is the EinSum over the tile labels, W[b,m,n] += sum_k A[b,m,k] B[b,k,n];
+// element offsets inside a tile come from per-role tables, so any label
+// order / layout of the operand tiles is accepted.
+//   KC_GEMM: 64x64 output block per 256-thread workgroup (2x2 waves of one
+//            32x32 MFMA tile each), 32-deep K chunks staged in LDS;
+//            fp32 -> v_mfma_f32_32x32x2_f32, bf16 -> v_mfma_f32_32x32x16_bf16.
+//   KC_VEC : one output element per thread, fp32 FMA (scale, GEMV, dot).
+#include "tre_internal.h"
+
+namespace tre {
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int kThreads = 256;
+
+__device__ inline float ld_f(const float* p) { return *p; }
+__device__ inline float ld_f(const uint16_t* p) { return __uint_as_float(uint32_t(*p) << 16); }
+
+// ---------------------------------------------------------------- tables
+
+struct TableSet {
+    Dims d[T_COUNT];
+    int64_t off[T_COUNT];
+};
+
+__global__ void k_tables(TableSet ts, int32_t* __restrict__ out) {
+    const int t = blockIdx.y;
+    const Dims& d = ts.d[t];
+    int64_t cnt = 1;
+    for (int i = 0; i < d.n; i++) cnt *= d.size[i];
+    for (int64_t x = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; x < cnt; x += int64_t(gridDim.x) * blockDim.x) {
+        int64_t rem = x, o = 0;
+        for (int i = d.n - 1; i >= 0; i--) {
+            o += (rem % d.size[i]) * d.stride[i];
+            rem /= d.size[i];
+        }
+        out[ts.off[t] + x] = int32_t(o);
+    }
+}
+
+// ----------------------------------------------------------------- units
+
+__global__ void k_seg_units(const int32_t* __restrict__ seg_start, int64_t n_w, int64_t p_unit,
+                            int32_t* __restrict__ nunits, int32_t* __restrict__ nparts, int32_t* __restrict__ nsplit) {
+    const int64_t s = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (s > n_w) return;
+    if (s == n_w) {
+        nunits[s] = 0;
+        nparts[s] = 0;
+        nsplit[s] = 0;
+        return;
+    }
+    const int64_t len = seg_start[s + 1] - seg_start[s];
+    const int64_t u = (len + p_unit - 1) / p_unit;
+    nunits[s] = int32_t(u);
+    nparts[s] = u > 1 ? int32_t(u) : 0;
+    nsplit[s] = u > 1 ? 1 : 0;
+}
+
+__global__ void k_fill_units(const int32_t* __restrict__ seg_start, int64_t n_w, int64_t p_unit,
+                             const int32_t* __restrict__ uoff, const int32_t* __restrict__ poff,
+                             const int32_t* __restrict__ soff, Unit* __restrict__ units, int32_t* __restrict__ split,
+                             WsHeader* hdr) {
+    const int64_t s = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (s > n_w) return;
+    if (s == n_w) {
+        hdr->n_units = uoff[n_w];
+        hdr->n_parts = poff[n_w];
+        hdr->n_split = soff[n_w];
+        return;
+    }
+    const int32_t a = seg_start[s], b = seg_start[s + 1];
+    const int32_t nu = uoff[s + 1] - uoff[s];
+    for (int32_t j = 0; j < nu; j++) {
+        Unit u;
+        u.seg = int32_t(s);
+        u.p0 = a + int32_t(j * p_unit);
+        u.p1 = int32_t(min<int64_t>(int64_t(a) + (j + 1) * p_unit, b));
+        u.slot = nu > 1 ? poff[s] + j : -1;
+        units[uoff[s] + j] = u;
+    }
+    if (nu > 1) split[soff[s]] = int32_t(s);
+}
+
+// ------------------------------------------------------------------ GEMM
+
+struct GemmArgs {
+    const void* A;
+    const void* B;
+    const int32_t* pa;
+    const int32_t* pb;
+    int64_t a_elems, b_elems, w_elems;
+    const int32_t *tAM, *tAK, *tBK, *tBN, *tWM, *tWN, *tAB, *tBB, *tWB;
+    int32_t M, N, K, nB, mblocks, nblocks;
+    int32_t vec_a, vec_b;
+    const Unit* units;
+    const WsHeader* hdr;
+    float* W;
+    float* partials;
+};
+
+constexpr int kBM = 64, kBN = 64, kBK = 32;
+
+template <typename T>
+struct LdsPitch;
+template <>
+struct LdsPitch<float> {
+    static constexpr int kfast = kBK + 1;   // [row][k]
+    static constexpr int rfast = kBM + 1;   // [k][row]
+};
+template <>
+struct LdsPitch<uint16_t> {
+    static constexpr int kfast = kBK + 8;   // keeps 16-byte row alignment for 8-wide reads
+    static constexpr int rfast = kBM + 2;
+};
+
+// 8 consecutive elements from a 16-byte aligned address.
+__device__ inline void load8(float* v, const float* src) {
+    const uint4 a = reinterpret_cast<const uint4*>(src)[0], b = reinterpret_cast<const uint4*>(src)[1];
+    __builtin_memcpy(v, &a, 16);
+    __builtin_memcpy(v + 4, &b, 16);
+}
+__device__ inline void load8(uint16_t* v, const uint16_t* src) {
+    const uint4 a = *reinterpret_cast<const uint4*>(src);
+    __builtin_memcpy(v, &a, 16);
+}
+
+// Stage a 64 x 32 (rows x k) chunk of one operand into LDS.
+//   KF: the operand's unit-stride dim is k (LDS [row][k]); else rows ([k][row]).
+template <typename T, bool KF>
+__device__ inline void stage(T* __restrict__ lds, const T* __restrict__ base, const int32_t* __restrict__ tR,
+                             const int32_t* __restrict__ tK, int r0, int R, int k0, int K, bool vec) {
+    const int t = threadIdx.x;
+    if (KF) {
+        const int r = t >> 2, ks = (t & 3) * 8;
+        const int gr = r0 + r, gk = k0 + ks;
+        T v[8];
+        if (vec && gr < R && gk + 8 <= K) {
+            load8(v, base + tR[gr] + tK[gk]);
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; j++) v[j] = (gr < R && gk + j < K) ? base[tR[gr] + tK[gk + j]] : T(0);
+        }
+#pragma unroll
+        for (int j = 0; j < 8; j++) lds[r * LdsPitch<T>::kfast + ks + j] = v[j];
+    } else {
+        const int k = t >> 3, rs = (t & 7) * 8;
+        const int gk = k0 + k, gr = r0 + rs;
+        T v[8];
+        if (vec && gk < K && gr + 8 <= R) {
+            load8(v, base + tK[gk] + tR[gr]);
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; j++) v[j] = (gk < K && gr + j < R) ? base[tK[gk] + tR[gr + j]] : T(0);
+        }
+#pragma unroll
+        for (int j = 0; j < 8; j++) lds[k * LdsPitch<T>::rfast + rs + j] = v[j];
+    }
+}
+
+template <typename T, bool KF>
+__device__ inline T lds_at(const T* lds, int row, int k) {
+    return KF ? lds[row * LdsPitch<T>::kfast + k] : lds[k * LdsPitch<T>::rfast + row];
+}
+
+template <bool KF>
+__device__ inline bf16x8 frag_bf16(const uint16_t* lds, int row, int k) {
+    u16x8 v;
+    if (KF) {
+        v = *reinterpret_cast<const u16x8*>(lds + row * LdsPitch<uint16_t>::kfast + k);
+    } else {
+#pragma unroll
+        for (int j = 0; j < 8; j++) v[j] = lds[(k + j) * LdsPitch<uint16_t>::rfast + row];
+    }
+    return __builtin_bit_cast(bf16x8, v);
+}
+
+template <typename T, bool AK, bool BK>
+__global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs g) {
+    const int unit_id = blockIdx.x;
+    if (unit_id >= g.hdr->n_units) return;
+    const Unit un = g.units[unit_id];
+    int y = blockIdx.y;
+    const int nblk = y % g.nblocks;
+    y /= g.nblocks;
+    const int mblk = y % g.mblocks;
+    const int b = y / g.mblocks;
+    const int m0 = mblk * kBM, n0 = nblk * kBN;
+
+    __shared__ __attribute__((aligned(16))) T As[AK ? kBM * LdsPitch<T>::kfast : kBK * LdsPitch<T>::rfast];
+    __shared__ __attribute__((aligned(16))) T Bs[BK ? kBN * LdsPitch<T>::kfast : kBK * LdsPitch<T>::rfast];
+
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int wm = w >> 1, wn = w & 1;
+    floatx16 acc;
+#pragma unroll
+    for (int r = 0; r < 16; r++) acc[r] = 0.f;
+
+    const T* Ag = reinterpret_cast<const T*>(g.A);
+    const T* Bg = reinterpret_cast<const T*>(g.B);
+    const int32_t offAB = g.tAB[b], offBB = g.tBB[b];
+    for (int p = un.p0; p < un.p1; p++) {
+        const T* Ab = Ag + int64_t(g.pa[p]) * g.a_elems + offAB;
+        const T* Bb = Bg + int64_t(g.pb[p]) * g.b_elems + offBB;
+        for (int k0 = 0; k0 < g.K; k0 += kBK) {
+            stage<T, AK>(As, Ab, g.tAM, g.tAK, m0, g.M, k0, g.K, g.vec_a);
+            stage<T, BK>(Bs, Bb, g.tBN, g.tBK, n0, g.N, k0, g.K, g.vec_b);
+            __syncthreads();
+            const int row = lane & 31, half = lane >> 5;
+            if constexpr (sizeof(T) == 4) {
+#pragma unroll
+                for (int ks = 0; ks < kBK; ks += 2) {
+                    float a = lds_at<T, AK>(As, wm * 32 + row, ks + half);
+                    float bb = lds_at<T, BK>(Bs, wn * 32 + row, ks + half);
+                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, bb, acc, 0, 0, 0);
+                }
+            } else {
+#pragma unroll
+                for (int ks = 0; ks < kBK; ks += 16) {
+                    bf16x8 a = frag_bf16<AK>(reinterpret_cast<const uint16_t*>(As), wm * 32 + row, ks + half * 8);
+                    bf16x8 bb = frag_bf16<BK>(reinterpret_cast<const uint16_t*>(Bs), wn * 32 + row, ks + half * 8);
+                    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bb, acc, 0, 0, 0);
+                }
+            }
+            __syncthreads();
+        }
+    }
+    float* out = un.slot < 0 ? g.W + int64_t(un.seg) * g.w_elems : g.partials + int64_t(un.slot) * g.w_elems;
+    out += g.tWB[b];
+    const int n = n0 + wn * 32 + (lane & 31);
+#pragma unroll
+    for (int r = 0; r < 16; r++) {
+        const int m = m0 + wm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        if (m < g.M && n < g.N) out[g.tWM[m] + g.tWN[n]] = acc[r];
+    }
+}
+
+// ------------------------------------------------------------------- VEC
+
+struct VecArgs {
+    const void* U;
+    const void* V;
+    const int32_t* pu;
+    const int32_t* pv;
+    int64_t u_elems, v_elems, w_elems;
+    const int32_t *tEU, *tEV, *tKU, *tKV;
+    int32_t K;
+    const Unit* units;
+    const WsHeader* hdr;
+    float* W;
+    float* partials;
+};
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_vec(VecArgs a) {
+    const int unit_id = blockIdx.x;
+    if (unit_id >= a.hdr->n_units) return;
+    const int64_t e = int64_t(blockIdx.y) * kThreads + threadIdx.x;
+    if (e >= a.w_elems) return;
+    const Unit un = a.units[unit_id];
+    const T* U = reinterpret_cast<const T*>(a.U);
+    const T* V = reinterpret_cast<const T*>(a.V);
+    const int32_t eu = a.tEU[e], ev = a.tEV[e];
+    float acc = 0.f;
+    for (int p = un.p0; p < un.p1; p++) {
+        const T* ub = U + int64_t(a.pu[p]) * a.u_elems + eu;
+        const T* vb = V + int64_t(a.pv[p]) * a.v_elems + ev;
+        for (int k = 0; k < a.K; k++) acc = fmaf(ld_f(ub + a.tKU[k]), ld_f(vb + a.tKV[k]), acc);
+    }
+    float* out = un.slot < 0 ? a.W + int64_t(un.seg) * a.w_elems : a.partials + int64_t(un.slot) * a.w_elems;
+    out[e] = acc;
+}
+
+// ---------------------------------------------------------------- reduce
+
+__global__ __launch_bounds__(kThreads) void k_reduce(const int32_t* __restrict__ split, const WsHeader* hdr,
+                                                     const int32_t* __restrict__ poff, const float* __restrict__ parts,
+                                                     float* __restrict__ W, int64_t w_elems) {
+    const int64_t x = blockIdx.x;
+    if (x >= hdr->n_split) return;
+    const int32_t s = split[x];
+    const int32_t first = poff[s], cnt = poff[s + 1] - poff[s];
+    for (int64_t e = int64_t(blockIdx.y) * kThreads + threadIdx.x; e < w_elems; e += int64_t(gridDim.y) * kThreads) {
+        float acc = 0.f;
+        for (int j = 0; j < cnt; j++) acc += parts[int64_t(first + j) * w_elems + e];
+        W[int64_t(s) * w_elems + e] = acc;
+    }
+}
+
+// ----------------------------------------------------------- outputs
+
+struct Unpack {
+    int32_t n;
+    int32_t bits[26];
+};
+
+__global__ void k_write_keys(const uint64_t* __restrict__ seg_key, int64_t n_w, Unpack up, int32_t* __restrict__ out) {
+    const int64_t s = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (s >= n_w) return;
+    uint64_t k = seg_key[s];
+    for (int c = up.n - 1; c >= 0; c--) {
+        const int b = up.bits[c];
+        out[s * up.n + c] = int32_t(b ? (k & ((uint64_t(1) << b) - 1)) : 0);
+        k = b < 64 ? (k >> b) : 0;
+    }
+}
+
+__global__ void k_write_pairs(const int32_t* __restrict__ pu, const int32_t* __restrict__ pv, int64_t n,
+                              int32_t* __restrict__ out) {
+    const int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (p >= n) return;
+    out[2 * p] = pu[p];
+    out[2 * p + 1] = pv[p];
+}
+
+inline unsigned blocks_for(int64_t n) { return unsigned((n + kThreads - 1) / kThreads); }
+
+template <typename T>
+hipError_t gemm_dispatch(const Plan& p, const GemmArgs& g, dim3 grid, hipStream_t s) {
+    if (p.a_kfast && p.b_kfast) k_gemm<T, true, true><<<grid, kThreads, 0, s>>>(g);
+    else if (p.a_kfast) k_gemm<T, true, false><<<grid, kThreads, 0, s>>>(g);
+    else if (p.b_kfast) k_gemm<T, false, true><<<grid, kThreads, 0, s>>>(g);
+    else k_gemm<T, false, false><<<grid, kThreads, 0, s>>>(g);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_tables(const Plan& p, int32_t* tables, hipStream_t s) {
+    TableSet ts{};
+    int64_t mx = 1;
+    for (int t = 0; t < T_COUNT; t++) {
+        ts.d[t] = p.dims[t];
+        ts.off[t] = p.table_off[t];
+        mx = std::max<int64_t>(mx, p.dims[t].count());
+    }
+    const unsigned gx = unsigned(std::min<int64_t>((mx + kThreads - 1) / kThreads, 1024));
+    k_tables<<<dim3(gx, T_COUNT), kThreads, 0, s>>>(ts, tables);
+    return hipGetLastError();
+}
+
+hipError_t launch_units(const Plan& p, const Layout& L, char* ws, int64_t n_pairs, int64_t n_w, int64_t p_unit,
+                        hipStream_t s) {
+    (void)p;
+    (void)n_pairs;
+    WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
+    int32_t* seg_start = reinterpret_cast<int32_t*>(ws + L.seg_start);
+    int32_t* nunits = reinterpret_cast<int32_t*>(ws + L.seg_units);
+    int32_t* nparts = reinterpret_cast<int32_t*>(ws + L.part_off);
+    int32_t* nsplit = reinterpret_cast<int32_t*>(ws + L.flags);
+    int32_t* tmp = reinterpret_cast<int32_t*>(ws + L.scan_tmp);
+    hipError_t e;
+    k_seg_units<<<blocks_for(n_w + 1), kThreads, 0, s>>>(seg_start, n_w, p_unit, nunits, nparts, nsplit);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = scan_exclusive_i32(nunits, nunits, n_w + 1, tmp, s)) != hipSuccess) return e;
+    if ((e = scan_exclusive_i32(nparts, nparts, n_w + 1, tmp, s)) != hipSuccess) return e;
+    if ((e = scan_exclusive_i32(nsplit, nsplit, n_w + 1, tmp, s)) != hipSuccess) return e;
+    k_fill_units<<<blocks_for(n_w + 1), kThreads, 0, s>>>(seg_start, n_w, p_unit, nunits, nparts, nsplit,
+                                                          reinterpret_cast<Unit*>(ws + L.unit_desc),
+                                                          reinterpret_cast<int32_t*>(ws + L.split_list), hdr);
+    return hipGetLastError();
+}
+
+hipError_t launch_contract(const Plan& p, const Layout& L, char* ws, const void* u_tiles, const void* v_tiles,
+                           float* w_tiles, int64_t n_pairs, int64_t n_w, int64_t unit_bound, hipStream_t s) {
+    (void)n_pairs;
+    (void)n_w;
+    if (unit_bound <= 0) return hipSuccess;
+    const int32_t* tb = reinterpret_cast<const int32_t*>(ws + L.tables);
+    const int32_t* pu = reinterpret_cast<const int32_t*>(ws + L.pu);
+    const int32_t* pv = reinterpret_cast<const int32_t*>(ws + L.pv);
+    const Unit* units = reinterpret_cast<const Unit*>(ws + L.unit_desc);
+    const WsHeader* hdr = reinterpret_cast<const WsHeader*>(ws + L.hdr);
+    float* parts = reinterpret_cast<float*>(ws + L.partials);
+    if (p.kclass == KC_GEMM) {
+        GemmArgs g{};
+        g.A = p.swap ? v_tiles : u_tiles;
+        g.B = p.swap ? u_tiles : v_tiles;
+        g.pa = p.swap ? pv : pu;
+        g.pb = p.swap ? pu : pv;
+        g.a_elems = p.tile_elems[p.swap ? 1 : 0];
+        g.b_elems = p.tile_elems[p.swap ? 0 : 1];
+        g.w_elems = p.tile_elems[2];
+        g.tAM = tb + p.table_off[T_AM];
+        g.tAK = tb + p.table_off[T_AK];
+        g.tBK = tb + p.table_off[T_BK];
+        g.tBN = tb + p.table_off[T_BN];
+        g.tWM = tb + p.table_off[T_WM];
+        g.tWN = tb + p.table_off[T_WN];
+        g.tAB = tb + p.table_off[T_AB];
+        g.tBB = tb + p.table_off[T_BB];
+        g.tWB = tb + p.table_off[T_WB];
+        g.M = int32_t(p.swap ? p.nN : p.nM);
+        g.N = int32_t(p.swap ? p.nM : p.nN);
+        g.K = int32_t(p.nK);
+        g.nB = int32_t(p.nB);
+        g.mblocks = (g.M + kBM - 1) / kBM;
+        g.nblocks = (g.N + kBN - 1) / kBN;
+        g.vec_a = p.vec_a;
+        g.vec_b = p.vec_b;
+        g.units = units;
+        g.hdr = hdr;
+        g.W = w_tiles;
+        g.partials = parts;
+        const int64_t gy = int64_t(g.nB) * g.mblocks * g.nblocks;
+        if (gy > 65535) return hipErrorInvalidConfiguration;
+        dim3 grid{unsigned(unit_bound), unsigned(gy), 1u};
+        return p.dtype == TRE_BF16 ? gemm_dispatch<uint16_t>(p, g, grid, s) : gemm_dispatch<float>(p, g, grid, s);
+    }
+    VecArgs a{};
+    a.U = u_tiles;
+    a.V = v_tiles;
+    a.pu = pu;
+    a.pv = pv;
+    a.u_elems = p.tile_elems[0];
+    a.v_elems = p.tile_elems[1];
+    a.w_elems = p.tile_elems[2];
+    a.tEU = tb + p.table_off[T_EU];
+    a.tEV = tb + p.table_off[T_EV];
+    a.tKU = tb + p.table_off[T_KU];
+    a.tKV = tb + p.table_off[T_KV];
+    a.K = int32_t(p.nK);
+    a.units = units;
+    a.hdr = hdr;
+    a.W = w_tiles;
+    a.partials = parts;
+    const int64_t gy = (p.tile_elems[2] + kThreads - 1) / kThreads;
+    if (gy > 65535) return hipErrorInvalidConfiguration;
+    dim3 grid{unsigned(unit_bound), unsigned(gy), 1u};
+    if (p.dtype == TRE_BF16) k_vec<uint16_t><<<grid, kThreads, 0, s>>>(a);
+    else k_vec<float><<<grid, kThreads, 0, s>>>(a);
+    return hipGetLastError();
+}
+
+hipError_t launch_reduce(const Plan& p, const Layout& L, char* ws, float* w_tiles, int64_t split_bound,
+                         hipStream_t s) {
+    if (split_bound <= 0) return hipSuccess;
+    const int64_t we = p.tile_elems[2];
+    const unsigned gy = unsigned(std::min<int64_t>((we + kThreads - 1) / kThreads, 65535));
+    k_reduce<<<dim3(unsigned(split_bound), gy), kThreads, 0, s>>>(
+        reinterpret_cast<const int32_t*>(ws + L.split_list), reinterpret_cast<const WsHeader*>(ws + L.hdr),
+        reinterpret_cast<const int32_t*>(ws + L.part_off), reinterpret_cast<const float*>(ws + L.partials), w_tiles,
+        we);
+    return hipGetLastError();
+}
+
+hipError_t launch_write_outputs(const Plan& p, const Layout& L, char* ws, int32_t* w_keys, int32_t* pairs_out,
+                                int64_t n_pairs, int64_t n_w, hipStream_t s) {
+    if (w_keys && p.nk[2] > 0 && n_w > 0) {
+        Unpack up{};
+        up.n = p.nk[2];
+        for (int c = 0; c < p.nk[2]; c++) up.bits[c] = p.w_bits[c];
+        k_write_keys<<<blocks_for(n_w), kThreads, 0, s>>>(reinterpret_cast<const uint64_t*>(ws + L.seg_key), n_w, up,
+                                                           w_keys);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (pairs_out && n_pairs > 0) {
+        k_write_pairs<<<blocks_for(n_pairs), kThreads, 0, s>>>(reinterpret_cast<const int32_t*>(ws + L.pu),
+                                                                reinterpret_cast<const int32_t*>(ws + L.pv), n_pairs,
+                                                                pairs_out);
+        return hipGetLastError();
+    }
+    return hipSuccess;
+}
+
+}  // namespace tre

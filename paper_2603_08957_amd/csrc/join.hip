@@ -1,0 +1,281 @@
+// Step (1) of the tensor-relational EinSum (Sec. 5): the natural join of two
+// relations on their shared promoted labels, and the GROUP BY keys.
+//
+//   stage 0  validate keys (optional), pack V's join key (join labels in V's
+//            key order, most significant first) and radix-sort V by it when
+//            V's key order does not start with the join labels; for every U
+//            tuple binary-search the run of equal join keys in V, then an
+//            exclusive scan of the run lengths gives each U tuple its first
+//            pair index and the total pair count.
+//   stage 1  load-balanced expansion: pair p finds its U tuple by a binary
+//            search over the scanned counts, so hub tuples with long runs
+//            are spread over many threads; pairs come out in (u, v) order.
+//            Each pair gets its packed W key; a stable radix sort by W key
+//            (skipped when W's keys are a prefix of U's) gives the canonical
+//            (w_key, u, v) order; run-length encoding gives the output keys
+//            and segment offsets.
+#include "tre_internal.h"
+
+namespace tre {
+
+namespace {
+
+constexpr int kThreads = 256;
+
+struct KeyDesc {
+    int32_t n;
+    int32_t pos[26];
+    int32_t bits[26];
+};
+
+struct WDesc {
+    int32_t n;
+    int32_t src[26];
+    int32_t pos[26];
+    int32_t bits[26];
+};
+
+struct Radix {
+    int32_t r[26];
+};
+
+inline unsigned blocks_for(int64_t n) { return unsigned((n + kThreads - 1) / kThreads); }
+
+__device__ inline uint64_t pack_row(const int32_t* row, const KeyDesc& d) {
+    uint64_t k = 0;
+    for (int i = 0; i < d.n; i++) k = (k << d.bits[i]) | uint64_t(uint32_t(row[d.pos[i]]));
+    return k;
+}
+
+__global__ void k_validate(const int32_t* __restrict__ keys, int64_t n, int r, Radix rad, int32_t* err) {
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    int flags = 0;
+    const int32_t* row = keys + i * r;
+    for (int a = 0; a < r; a++)
+        if (row[a] < 0 || row[a] >= rad.r[a]) flags |= 4;
+    if (i > 0) {
+        const int32_t* prev = row - r;
+        int c = 0;
+        for (int a = 0; a < r && c == 0; a++) c = (prev[a] < row[a]) ? -1 : (prev[a] > row[a] ? 1 : 0);
+        if (c == 0) flags |= 2;
+        if (c > 0) flags |= 1;
+    }
+    if (flags) atomicOr(err, flags);
+}
+
+__global__ void k_pack_join(const int32_t* __restrict__ keys, int64_t n, int r, KeyDesc d, uint64_t* __restrict__ out,
+                            uint32_t* __restrict__ perm) {
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    out[i] = pack_row(keys + i * r, d);
+    if (perm) perm[i] = uint32_t(i);
+}
+
+// Run of V tuples whose join key equals U tuple u's: [lo, lo + cnt).
+__global__ void k_count(const int32_t* __restrict__ ukeys, int64_t n_u, int ru, KeyDesc du,
+                        const uint64_t* __restrict__ vjk, int64_t n_v, int has_join, int64_t* __restrict__ cnt,
+                        int64_t* __restrict__ lo) {
+    const int64_t u = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (u > n_u) return;
+    if (u == n_u) {
+        cnt[u] = 0;
+        return;
+    }
+    if (!has_join) {
+        cnt[u] = n_v;
+        lo[u] = 0;
+        return;
+    }
+    const uint64_t key = pack_row(ukeys + u * ru, du);
+    int64_t a = 0, b = n_v;
+    while (a < b) {
+        int64_t m = (a + b) >> 1;
+        if (vjk[m] < key) a = m + 1; else b = m;
+    }
+    int64_t c = a, e = n_v;
+    while (c < e) {
+        int64_t m = (c + e) >> 1;
+        if (vjk[m] <= key) c = m + 1; else e = m;
+    }
+    lo[u] = a;
+    cnt[u] = c - a;
+}
+
+__global__ void k_store_count(const int64_t* __restrict__ off, int64_t n_u, WsHeader* hdr) {
+    hdr->n_pairs = off[n_u];
+}
+
+__device__ inline uint64_t pack_w(const int32_t* urow, const int32_t* vrow, const WDesc& d) {
+    uint64_t k = 0;
+    for (int i = 0; i < d.n; i++) {
+        int32_t f = d.src[i] == 0 ? urow[d.pos[i]] : vrow[d.pos[i]];
+        k = (k << d.bits[i]) | uint64_t(uint32_t(f));
+    }
+    return k;
+}
+
+__global__ void k_expand(const int64_t* __restrict__ off, const int64_t* __restrict__ lo, int64_t n_u, int64_t n_pairs,
+                         const uint32_t* __restrict__ vperm, const int32_t* __restrict__ ukeys, int ru,
+                         const int32_t* __restrict__ vkeys, int rv, WDesc wd, int32_t* __restrict__ pu,
+                         int32_t* __restrict__ pv, uint64_t* __restrict__ wk, uint32_t* __restrict__ pidx) {
+    const int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (p >= n_pairs) return;
+    // largest u with off[u] <= p
+    int64_t a = 0, b = n_u - 1;
+    while (a < b) {
+        int64_t m = (a + b + 1) >> 1;
+        if (off[m] <= p) a = m; else b = m - 1;
+    }
+    const int64_t u = a;
+    const int64_t vs = lo[u] + (p - off[u]);
+    const int64_t v = vperm ? int64_t(vperm[vs]) : vs;
+    pu[p] = int32_t(u);
+    pv[p] = int32_t(v);
+    wk[p] = pack_w(ukeys + u * ru, vkeys + v * rv, wd);
+    if (pidx) pidx[p] = uint32_t(p);
+}
+
+__global__ void k_gather_pairs(const uint32_t* __restrict__ idx, const int32_t* __restrict__ pu_in,
+                               const int32_t* __restrict__ pv_in, int32_t* __restrict__ pu, int32_t* __restrict__ pv,
+                               int64_t n) {
+    const int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (p >= n) return;
+    const uint32_t s = idx[p];
+    pu[p] = pu_in[s];
+    pv[p] = pv_in[s];
+}
+
+__global__ void k_heads(const uint64_t* __restrict__ wk, int64_t n, int32_t* __restrict__ flags) {
+    const int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (p > n) return;
+    flags[p] = (p < n && (p == 0 || wk[p] != wk[p - 1])) ? 1 : 0;
+}
+
+__global__ void k_compact(const uint64_t* __restrict__ wk, int64_t n, const int32_t* __restrict__ seg_of,
+                          int32_t* __restrict__ seg_start, uint64_t* __restrict__ seg_key, WsHeader* hdr) {
+    const int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (p > n) return;
+    if (p == n) {
+        seg_start[seg_of[n]] = int32_t(n);
+        hdr->n_w = seg_of[n];
+        return;
+    }
+    if (p == 0 || wk[p] != wk[p - 1]) {
+        const int32_t s = seg_of[p];
+        seg_start[s] = int32_t(p);
+        seg_key[s] = wk[p];
+    }
+}
+
+KeyDesc desc_u(const Plan& p) {
+    KeyDesc d{};
+    d.n = p.n_join;
+    for (int i = 0; i < p.n_join; i++) {
+        d.pos[i] = p.join_pos_u[i];
+        d.bits[i] = p.join_bits[i];
+    }
+    return d;
+}
+
+KeyDesc desc_v(const Plan& p) {
+    KeyDesc d{};
+    d.n = p.n_join;
+    for (int i = 0; i < p.n_join; i++) {
+        d.pos[i] = p.join_pos_v[i];
+        d.bits[i] = p.join_bits[i];
+    }
+    return d;
+}
+
+}  // namespace
+
+hipError_t launch_validate(const int32_t* keys, int64_t n, int r, const int32_t* radix, int32_t* err_flag,
+                           hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    Radix rad{};
+    for (int a = 0; a < r; a++) rad.r[a] = radix[a];
+    if (r == 0) return hipSuccess;  // at most one tuple; checked on the host
+    k_validate<<<blocks_for(n), kThreads, 0, s>>>(keys, n, r, rad, err_flag);
+    return hipGetLastError();
+}
+
+hipError_t launch_join(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
+                       hipStream_t s, int stage) {
+    WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
+    uint64_t* vjk = reinterpret_cast<uint64_t*>(ws + L.vjk);
+    uint32_t* vperm = p.v_needs_sort ? reinterpret_cast<uint32_t*>(ws + L.vperm) : nullptr;
+    int64_t* cnt = reinterpret_cast<int64_t*>(ws + L.ucnt);
+    int64_t* lo = reinterpret_cast<int64_t*>(ws + L.ulo);
+    int64_t* tmp = reinterpret_cast<int64_t*>(ws + L.scan_tmp);
+    int64_t* hist = reinterpret_cast<int64_t*>(ws + L.hist);
+    const int64_t n_u = L.n_u, n_v = L.n_v;
+    hipError_t e = hipSuccess;
+    if (stage == 0) {
+        if (p.n_join > 0 && n_v > 0) {
+            k_pack_join<<<blocks_for(n_v), kThreads, 0, s>>>(v_keys, n_v, p.nk[1], desc_v(p), vjk, vperm);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+            if (p.v_needs_sort) {
+                e = radix_sort_u64(vjk, vperm, reinterpret_cast<uint64_t*>(ws + L.vjk_alt),
+                                   reinterpret_cast<uint32_t*>(ws + L.vperm_alt), n_v, p.join_total_bits, hist, tmp,
+                                   s);
+                if (e != hipSuccess) return e;
+            }
+        }
+        k_count<<<blocks_for(n_u + 1), kThreads, 0, s>>>(u_keys, n_u, p.nk[0], desc_u(p), vjk, n_v, p.n_join > 0,
+                                                          cnt, lo);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = scan_exclusive_i64(cnt, cnt, n_u + 1, tmp, s)) != hipSuccess) return e;
+        k_store_count<<<1, 1, 0, s>>>(cnt, n_u, hdr);
+        return hipGetLastError();
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
+                        int64_t n_pairs, hipStream_t s, int stage) {
+    (void)stage;
+    WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
+    int64_t* off = reinterpret_cast<int64_t*>(ws + L.ucnt);
+    int64_t* lo = reinterpret_cast<int64_t*>(ws + L.ulo);
+    uint32_t* vperm = p.v_needs_sort ? reinterpret_cast<uint32_t*>(ws + L.vperm) : nullptr;
+    int32_t* pu = reinterpret_cast<int32_t*>(ws + L.pu);
+    int32_t* pv = reinterpret_cast<int32_t*>(ws + L.pv);
+    uint64_t* wk = reinterpret_cast<uint64_t*>(ws + L.wk);
+    int64_t* tmp = reinterpret_cast<int64_t*>(ws + L.scan_tmp);
+    int64_t* hist = reinterpret_cast<int64_t*>(ws + L.hist);
+    int32_t* flags = reinterpret_cast<int32_t*>(ws + L.flags);
+    int32_t* seg_start = reinterpret_cast<int32_t*>(ws + L.seg_start);
+    uint64_t* seg_key = reinterpret_cast<uint64_t*>(ws + L.seg_key);
+    WDesc wd{};
+    wd.n = p.nk[2];
+    for (int c = 0; c < p.nk[2]; c++) {
+        wd.src[c] = p.w_src[c];
+        wd.pos[c] = p.w_pos[c];
+        wd.bits[c] = p.w_bits[c];
+    }
+    hipError_t e;
+    const bool sort = p.group_needs_sort && n_pairs > 1 && p.w_total_bits > 0;
+    int32_t* epu = sort ? reinterpret_cast<int32_t*>(ws + L.pu_alt) : pu;
+    int32_t* epv = sort ? reinterpret_cast<int32_t*>(ws + L.pv_alt) : pv;
+    uint32_t* pidx = sort ? reinterpret_cast<uint32_t*>(ws + L.pidx) : nullptr;
+    if (n_pairs > 0) {
+        k_expand<<<blocks_for(n_pairs), kThreads, 0, s>>>(off, lo, L.n_u, n_pairs, vperm, u_keys, p.nk[0], v_keys,
+                                                           p.nk[1], wd, epu, epv, wk, pidx);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    if (sort) {
+        e = radix_sort_u64(wk, pidx, reinterpret_cast<uint64_t*>(ws + L.wk_alt),
+                           reinterpret_cast<uint32_t*>(ws + L.pidx_alt), n_pairs, p.w_total_bits, hist, tmp, s);
+        if (e != hipSuccess) return e;
+        k_gather_pairs<<<blocks_for(n_pairs), kThreads, 0, s>>>(pidx, epu, epv, pu, pv, n_pairs);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    k_heads<<<blocks_for(n_pairs + 1), kThreads, 0, s>>>(wk, n_pairs, flags);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = scan_exclusive_i32(flags, flags, n_pairs + 1, reinterpret_cast<int32_t*>(tmp), s)) != hipSuccess) return e;
+    k_compact<<<blocks_for(n_pairs + 1), kThreads, 0, s>>>(wk, n_pairs, flags, seg_start, seg_key, hdr);
+    return hipGetLastError();
+}
+
+}  // namespace tre

@@ -1,0 +1,158 @@
+// Internal declarations shared by the host planner and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+
+#include "../../include/tre.h"
+
+namespace tre {
+
+constexpr int kMaxDims = 8;
+
+// Row-major index decomposition: index x over sizes (last fastest) maps to
+// sum_i coord_i(x) * stride_i.  Used to build per-role offset tables.
+struct Dims {
+    int32_t n = 0;
+    int32_t size[kMaxDims] = {};
+    int32_t stride[kMaxDims] = {};
+    int64_t count() const {
+        int64_t c = 1;
+        for (int i = 0; i < n; i++) c *= size[i];
+        return c;
+    }
+};
+
+// Offset tables (int32 element offsets inside one tile).
+//   GEMM: A/B are the two operands as the MFMA kernel sees them (A = U unless
+//   the plan swaps), W the output tile.
+//   VEC : EU/EV map a W-tile element (in W memory order) to the U / V offset
+//   of its non-contracted part; KU/KV map the contracted index.
+enum TableId { T_AM, T_AK, T_BK, T_BN, T_WM, T_WN, T_AB, T_BB, T_WB, T_EU, T_EV, T_KU, T_KV, T_COUNT };
+
+enum KernelClass { KC_GEMM = 0, KC_VEC = 1 };
+
+struct Plan {
+    std::string einsum;
+    tre_dtype dtype = TRE_F32;
+    tre_options opt{};
+    // parsed labels
+    int nl[3] = {0, 0, 0};
+    int lab[3][26] = {};
+    bool up[26] = {};
+    bool used[26] = {};
+    int64_t ext[26] = {};
+    int64_t tsz[26] = {};  // extent of the label inside a tile
+    int nk[3] = {0, 0, 0};
+    int klab[3][26] = {};
+    int64_t tile_elems[3] = {1, 1, 1};
+    int32_t radix[3][26] = {};  // per key attribute: extent / t
+    // join key: join labels in V's key order, packed most significant first
+    int n_join = 0;
+    int join_pos_u[26] = {}, join_pos_v[26] = {}, join_bits[26] = {};
+    int join_total_bits = 0;
+    bool v_needs_sort = false;
+    // W key: attributes in W key order, each from U (0) or V (1)
+    int w_src[26] = {}, w_pos[26] = {}, w_bits[26] = {};
+    int w_total_bits = 0;
+    bool group_needs_sort = false;
+    // tile roles
+    char role[26] = {};
+    int64_t nB = 1, nM = 1, nN = 1, nK = 1;
+    KernelClass kclass = KC_VEC;
+    bool swap = false;     // GEMM: A operand is V
+    bool a_kfast = false;  // GEMM: A's unit-stride dim is a K dim
+    bool b_kfast = false;
+    bool vec_a = false;    // GEMM: 8-wide vector loads legal along A's fast dim
+    bool vec_b = false;
+    Dims dims[T_COUNT];
+    int64_t table_off[T_COUNT] = {};
+    int64_t table_total = 0;
+};
+
+// Workspace layout (byte offsets from the workspace base).
+struct Layout {
+    int64_t n_u = 0, n_v = 0, max_pairs = 0;
+    int64_t part_cap = 0;  // partial tiles
+    size_t hdr, vjk, vjk_alt, vperm, vperm_alt, ucnt, ulo, scan_tmp, pu, pv, pu_alt, pv_alt, wk, wk_alt, pidx,
+        pidx_alt, hist, flags, seg_start, seg_key, unit_desc, seg_units, part_off, split_list, tables, partials;
+    size_t total = 0;
+};
+
+// Header at the start of the workspace (device memory).
+struct WsHeader {
+    int32_t err_u;       // bit 0 unsorted, bit 1 duplicate, bit 2 range
+    int32_t err_v;
+    int32_t pad0[2];
+    int64_t n_pairs;
+    int64_t n_w;
+    int64_t n_units;
+    int64_t n_split;
+    int64_t n_parts;
+    int64_t pad1[9];
+};
+
+// Work unit: a run of pairs [p0, p1) of one segment; slot >= 0 means the
+// unit writes a partial tile that the segmented reduction sums.
+struct Unit {
+    int32_t seg;
+    int32_t p0;
+    int32_t p1;
+    int32_t slot;
+};
+
+Layout make_layout(const Plan& p, int64_t n_u, int64_t n_v, int64_t max_pairs);
+
+// ----- launchers (defined in the .hip files) -----
+// scan.hip
+size_t scan_tmp_elems(int64_t n);
+hipError_t scan_exclusive_i64(const int64_t* in, int64_t* out, int64_t n, int64_t* tmp, hipStream_t s);
+hipError_t scan_exclusive_i32(const int32_t* in, int32_t* out, int64_t n, int32_t* tmp, hipStream_t s);
+
+// sort.hip: stable LSD radix sort of (uint64 key, uint32 payload) over the
+// low `bits` bits; result lands in keys/vals (alt buffers are scratch).
+int64_t radix_hist_elems(int64_t n);
+hipError_t radix_sort_u64(uint64_t* keys, uint32_t* vals, uint64_t* keys_alt, uint32_t* vals_alt, int64_t n,
+                          int bits, int64_t* hist, int64_t* scan_tmp, hipStream_t s);
+
+// join.hip
+hipError_t launch_validate(const int32_t* keys, int64_t n, int r, const int32_t* radix, int32_t* err_flag,
+                           hipStream_t s);
+hipError_t launch_join(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
+                       hipStream_t s, int stage);
+hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
+                        int64_t n_pairs, hipStream_t s, int stage);
+
+// contract.hip
+hipError_t launch_tables(const Plan& p, int32_t* tables, hipStream_t s);
+hipError_t launch_units(const Plan& p, const Layout& L, char* ws, int64_t n_pairs, int64_t n_w, int64_t p_unit,
+                        hipStream_t s);
+hipError_t launch_contract(const Plan& p, const Layout& L, char* ws, const void* u_tiles, const void* v_tiles,
+                           float* w_tiles, int64_t n_pairs, int64_t n_w, int64_t unit_bound, hipStream_t s);
+hipError_t launch_reduce(const Plan& p, const Layout& L, char* ws, float* w_tiles, int64_t split_bound,
+                         hipStream_t s);
+hipError_t launch_write_outputs(const Plan& p, const Layout& L, char* ws, int32_t* w_keys, int32_t* pairs_out,
+                                int64_t n_pairs, int64_t n_w, hipStream_t s);
+
+// glue.hip
+hipError_t launch_cast_bf16(const float* x, uint16_t* y, int64_t n, hipStream_t s);
+hipError_t launch_tiles_from_entries(const int64_t* slot, const int64_t* off, const void* val, int64_t n,
+                                     int elem_bytes, void* tiles, int64_t n_tiles, int64_t tile_elems,
+                                     hipStream_t s);
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_stack(const int32_t* keys, int64_t n, const void* tiles, int64_t row_elems, int32_t group,
+                        int32_t elem_bytes, int32_t* out_keys, void* out_tiles, int64_t n_out, char* ws,
+                        hipStream_t s, int stage);
+size_t stack_ws_bytes(int64_t n);
+
+void set_error(const std::string& msg);
+
+}  // namespace tre
+
+// Opaque plan handle of the C ABI.
+struct tre_plan_s {
+    tre::Plan p;
+};

@@ -1,0 +1,272 @@
+"""ctypes binding of ``libtre.so`` (the C ABI declared in ``include/tre.h``).
+
+Argument marshalling only: torch supplies device memory and the stream, and
+every step of the path runs in the library's HIP kernels.  There is no CPU
+fallback; a missing library raises at load time.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtre.so")
+
+STATUS = {
+    0: "TRE_OK", 1: "TRE_E_ARG", 2: "TRE_E_PARSE", 3: "TRE_E_SPLIT", 4: "TRE_E_SHAPE", 5: "TRE_E_DTYPE",
+    6: "TRE_E_UNSORTED", 7: "TRE_E_DUPKEY", 8: "TRE_E_KEYRANGE", 9: "TRE_E_CAPACITY", 10: "TRE_E_WORKSPACE",
+    11: "TRE_E_DEVICE", 12: "TRE_E_STATE",
+}
+DTYPE = {"f32": 0, "bf16": 1}
+
+# every symbol include/tre.h declares
+EXPORTS = [
+    "tre_plan", "tre_plan_get_info", "tre_plan_destroy", "tre_workspace_bytes", "tre_workspace_max_pairs",
+    "tre_join", "tre_contract", "tre_execute", "tre_cast_f32_bf16", "tre_stack_workspace_bytes", "tre_stack_rows",
+    "tre_tiles_from_entries", "tre_status_str", "tre_last_error", "tre_version",
+]
+
+
+class TreError(RuntimeError):
+    def __init__(self, code: int, where: str, detail: str = ""):
+        self.code = code
+        self.status = STATUS.get(code, str(code))
+        super().__init__(f"{where}: {self.status}" + (f" ({detail})" if detail else ""))
+
+
+class Options(ctypes.Structure):
+    _fields_ = [("validate_keys", ctypes.c_int32), ("max_pairs_per_unit", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 6)]
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("key_arity", ctypes.c_int32 * 3), ("tile_elems", ctypes.c_int64 * 3), ("n_join", ctypes.c_int32),
+                ("kernel_class", ctypes.c_int32), ("batch", ctypes.c_int64), ("m", ctypes.c_int64),
+                ("n", ctypes.c_int64), ("k", ctypes.c_int64), ("flops_per_pair", ctypes.c_int64),
+                ("key_labels", (ctypes.c_char * 27) * 3), ("roles", ctypes.c_char * 27),
+                ("group_needs_sort", ctypes.c_int32), ("v_needs_sort", ctypes.c_int32)]
+
+
+class JoinResult(ctypes.Structure):
+    _fields_ = [("n_u", ctypes.c_int64), ("n_v", ctypes.c_int64), ("n_pairs", ctypes.c_int64), ("n_w", ctypes.c_int64),
+                ("internal", ctypes.c_uint64 * 16)]
+
+
+class Timing(ctypes.Structure):
+    _fields_ = [("join_ms", ctypes.c_float), ("contract_ms", ctypes.c_float), ("reduce_ms", ctypes.c_float),
+                ("total_ms", ctypes.c_float), ("n_units", ctypes.c_int64), ("n_split_segments", ctypes.c_int64)]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
+_lib = None
+
+
+def lib():
+    """Load libtre.so; raises if it has not been built (no fallback path)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2603_08957_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+        L.tre_plan.argtypes = [ctypes.c_char_p, ctypes.c_char_p, P, P, ctypes.c_int, P, P]
+        L.tre_plan_get_info.argtypes = [P, P]
+        L.tre_plan_destroy.argtypes = [P]
+        L.tre_plan_destroy.restype = None
+        L.tre_workspace_bytes.argtypes = [P, i64, i64, i64]
+        L.tre_workspace_bytes.restype = sz
+        L.tre_workspace_max_pairs.argtypes = [P, i64, i64, sz]
+        L.tre_workspace_max_pairs.restype = i64
+        L.tre_join.argtypes = [P, P, i64, P, i64, P, sz, P, P, P]
+        L.tre_contract.argtypes = [P, P, P, P, P, i64, P, P, i64, P, P]
+        L.tre_execute.argtypes = [P, P, i64, P, P, i64, P, P, P, i64, P, P, i64, P, P, sz, P, P]
+        L.tre_cast_f32_bf16.argtypes = [P, P, i64, P]
+        L.tre_stack_workspace_bytes.argtypes = [i64]
+        L.tre_stack_workspace_bytes.restype = sz
+        L.tre_stack_rows.argtypes = [P, i64, P, i64, i32, i32, P, P, i64, P, P, sz, P]
+        L.tre_tiles_from_entries.argtypes = [P, P, P, i64, i32, P, i64, i64, P]
+        L.tre_status_str.restype = ctypes.c_char_p
+        L.tre_last_error.restype = ctypes.c_char_p
+        L.tre_version.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _check(rc: int, where: str):
+    if rc != 0:
+        raise TreError(rc, where, lib().tre_last_error().decode())
+
+
+def _ptr(t):
+    """Device pointer of a torch tensor (or None)."""
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    import torch
+
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class Plan:
+    """A parsed, classified binary EinSum (host object, see tre_plan)."""
+
+    def __init__(self, einsum: str, upper: str, extents: dict, tiles: dict, dtype: str = "f32",
+                 validate: bool = True, max_pairs_per_unit: int = 0):
+        L = lib()
+        ext = np.zeros(26, dtype=np.int64)
+        til = np.ones(26, dtype=np.int32)
+        for k, v in extents.items():
+            ext[ord(k) - 97] = v
+        for k, v in (tiles or {}).items():
+            til[ord(k) - 97] = v
+        opt = Options(int(validate), int(max_pairs_per_unit))
+        h = ctypes.c_void_p(0)
+        rc = L.tre_plan(einsum.encode(), upper.encode(), ext.ctypes.data_as(ctypes.c_void_p),
+                        til.ctypes.data_as(ctypes.c_void_p), DTYPE[dtype], ctypes.byref(opt), ctypes.byref(h))
+        _check(rc, "tre_plan")
+        self._h = h
+        self.einsum, self.upper, self.dtype = einsum, upper, dtype
+        info = PlanInfo()
+        _check(L.tre_plan_get_info(h, ctypes.byref(info)), "tre_plan_get_info")
+        self.key_arity = list(info.key_arity)
+        self.tile_elems = list(info.tile_elems)
+        self.n_join = info.n_join
+        self.kernel_class = "gemm" if info.kernel_class == 0 else "vec"
+        self.bmnk = (info.batch, info.m, info.n, info.k)
+        self.flops_per_pair = info.flops_per_pair
+        self.key_labels = [bytes(info.key_labels[o]).split(b"\0")[0].decode() for o in range(3)]
+        self.roles = bytes(info.roles).split(b"\0")[0].decode()
+        self.group_needs_sort = bool(info.group_needs_sort)
+        self.v_needs_sort = bool(info.v_needs_sort)
+
+    @classmethod
+    def from_spec(cls, spec: dict, **kw):
+        return cls(spec["einsum"], spec["upper"], spec["extents"], spec["tiles"], spec["dtype"], **kw)
+
+    @property
+    def handle(self):
+        return self._h
+
+    def workspace_bytes(self, n_u: int, n_v: int, max_pairs: int) -> int:
+        return int(lib().tre_workspace_bytes(self._h, n_u, n_v, max_pairs))
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value and _lib is not None:
+            _lib.tre_plan_destroy(h)
+            self._h = None
+
+
+def alloc_workspace(nbytes: int, device="cuda"):
+    import torch
+
+    ws = torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+    assert ws.data_ptr() % 256 == 0
+    return ws
+
+
+def join(plan: Plan, u_keys, n_u: int, v_keys, n_v: int, ws, stream=None, timing: Timing | None = None) -> JoinResult:
+    jr = JoinResult()
+    rc = lib().tre_join(plan.handle, _ptr(u_keys), n_u, _ptr(v_keys), n_v, _ptr(ws), ws.numel(), _stream(stream),
+                        ctypes.byref(jr), ctypes.byref(timing) if timing is not None else None)
+    if rc != 0:
+        err = TreError(rc, "tre_join", lib().tre_last_error().decode())
+        err.join_result = jr
+        raise err
+    return jr
+
+
+def contract(plan: Plan, jr: JoinResult, u_tiles, v_tiles, w_keys, w_tiles, pairs_out=None, stream=None,
+             timing: Timing | None = None):
+    w_cap = w_tiles.shape[0] if w_tiles is not None else 0
+    pair_cap = pairs_out.shape[0] if pairs_out is not None else 0
+    rc = lib().tre_contract(plan.handle, ctypes.byref(jr), _ptr(u_tiles), _ptr(v_tiles), _ptr(w_keys), w_cap,
+                            _ptr(w_tiles), _ptr(pairs_out), pair_cap, _stream(stream),
+                            ctypes.byref(timing) if timing is not None else None)
+    _check(rc, "tre_contract")
+
+
+@dataclass
+class Output:
+    w_keys: object      # torch int32 [n_w, r_W]
+    w_tiles: object     # torch float32 [n_w, tile_elems(W)]
+    pairs: object       # torch int32 [n_pairs, 2] or None
+    n_pairs: int
+    n_w: int
+    timing: dict | None
+    ws: object
+
+
+def einsum(plan: Plan, u_keys, u_tiles, v_keys, v_tiles, want_pairs: bool = False, ws=None, stream=None,
+           timing: bool = False, pair_hint: int | None = None) -> Output:
+    """Join + contract with output buffers allocated by torch.  The workspace
+    is grown and the join repeated once if the pair list does not fit."""
+    import torch
+
+    n_u, n_v = int(u_tiles.shape[0]), int(v_tiles.shape[0])
+    dev = u_tiles.device
+    if ws is None:
+        hint = pair_hint if pair_hint is not None else max(n_u, n_v, 1) * 2
+        ws = alloc_workspace(plan.workspace_bytes(n_u, n_v, hint), dev)
+    tm = Timing() if timing else None
+    try:
+        jr = join(plan, u_keys, n_u, v_keys, n_v, ws, stream, tm)
+    except TreError as e:
+        if e.code != 10 or e.join_result.n_pairs <= 0:
+            raise
+        ws = alloc_workspace(plan.workspace_bytes(n_u, n_v, int(e.join_result.n_pairs)), dev)
+        jr = join(plan, u_keys, n_u, v_keys, n_v, ws, stream, tm)
+    n_w, n_p = int(jr.n_w), int(jr.n_pairs)
+    rw = plan.key_arity[2]
+    w_keys = torch.empty((n_w, rw), dtype=torch.int32, device=dev)
+    w_tiles = torch.empty((n_w, plan.tile_elems[2]), dtype=torch.float32, device=dev)
+    pairs = torch.empty((n_p, 2), dtype=torch.int32, device=dev) if want_pairs else None
+    contract(plan, jr, u_tiles, v_tiles, w_keys if rw > 0 else None, w_tiles, pairs, stream, tm)
+    return Output(w_keys, w_tiles, pairs, n_p, n_w, tm.as_dict() if tm is not None else None, ws)
+
+
+def cast_f32_bf16(x, out=None, stream=None):
+    import torch
+
+    y = out if out is not None else torch.empty(x.shape, dtype=torch.bfloat16, device=x.device)
+    _check(lib().tre_cast_f32_bf16(_ptr(x), _ptr(y), x.numel(), _stream(stream)), "tre_cast_f32_bf16")
+    return y
+
+
+def stack_rows(keys, tiles, group: int, stream=None):
+    """STACK re-composition (see tre_stack_rows); keys [n] or [n,1] int32."""
+    import torch
+
+    n = int(keys.shape[0])
+    row = int(tiles.numel() // max(n, 1)) if n else int(tiles.shape[1])
+    eb = tiles.element_size()
+    ws = alloc_workspace(int(lib().tre_stack_workspace_bytes(n)), tiles.device)
+    cap = n
+    out_keys = torch.empty((cap, 1), dtype=torch.int32, device=tiles.device)
+    out_tiles = torch.empty((cap, group * row), dtype=tiles.dtype, device=tiles.device)
+    n_out = ctypes.c_int64(0)
+    rc = lib().tre_stack_rows(_ptr(keys), n, _ptr(tiles), row, group, eb, _ptr(out_keys), _ptr(out_tiles), cap,
+                              ctypes.byref(n_out), _ptr(ws), ws.numel(), _stream(stream))
+    _check(rc, "tre_stack_rows")
+    k = int(n_out.value)
+    return out_keys[:k], out_tiles[:k]
+
+
+def tiles_from_entries(slot, offset, values, n_tiles: int, tile_elems: int, stream=None):
+    """Dense tiles [n_tiles, tile_elems] (dtype of ``values``) from scalar entries."""
+    import torch
+
+    tiles = torch.empty((n_tiles, tile_elems), dtype=values.dtype, device=values.device)
+    rc = lib().tre_tiles_from_entries(_ptr(slot), _ptr(offset), _ptr(values), int(values.numel()),
+                                      values.element_size(), _ptr(tiles), n_tiles, tile_elems, _stream(stream))
+    _check(rc, "tre_tiles_from_entries")
+    return tiles

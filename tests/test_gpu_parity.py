@@ -1,0 +1,260 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on the
+same seeded inputs.  Pair lists and key sets bit-exact; values within the
+mag-relative tolerance (1e-4 fp32, 1e-2 bf16 in / fp32 accumulate)."""
+import json
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import workloads
+from _parity import TOL, check, gpu_run, to_dev, value_error
+from test_oracle import random_plan, split_einsum
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "worked_example.json")
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+
+    assert torch.cuda.is_available(), "GPU test needs a GPU"
+    import paper_2603_08957_amd as tre
+
+    tre.lib()
+
+
+def orc_plan(orc, s):
+    return orc.Plan(s["einsum"], s["upper"], s["extents"], s["tiles"])
+
+
+@pytest.mark.parametrize("name", ["a_rows_times_cols", "b_columns_times_scalars", "c_outer_products"])
+def test_worked_example_gpu(orc, name):
+    g = json.load(open(GOLDEN))
+    d = g["decompositions"][name]
+    spec = workloads.spec(d["einsum"], d["upper"], {"i": 4, "j": 4, "k": 4}, d["tiles"], "f32")
+    U = {"keys": np.array(d["U_keys"], np.int32).reshape(len(d["U_keys"]), -1),
+         "tiles": np.array(d["U_tiles"], np.float32), "dtype": "f32"}
+    V = {"keys": np.array(d["V_keys"], np.int32).reshape(len(d["V_keys"]), -1),
+         "tiles": np.array(d["V_tiles"], np.float32), "dtype": "f32"}
+    say("worked example", name)
+    _, out = gpu_run(spec, U, V)
+    ref = orc.run(orc_plan(orc, spec), U, V)
+    check(out, ref, "f32")
+    assert out.pairs.cpu().numpy().tolist() == d["pairs"]
+    np.testing.assert_allclose(out.w_tiles.cpu().numpy(), np.array(d["W_tiles"]), rtol=1e-6, atol=1e-6)
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_random_plans_gpu(orc, seed):
+    rng = np.random.default_rng(1000 + seed)
+    e, upper, ext, til = random_plan(rng)
+    u_lab, v_lab, _ = split_einsum(e)
+    dtype = "bf16" if seed % 3 == 0 else "f32"
+    U = workloads.random_relation(rng, u_lab, upper, ext, til, dtype, keep=0.6, zero_frac=0.3)
+    V = workloads.random_relation(rng, v_lab, upper, ext, til, dtype, keep=0.6, zero_frac=0.3)
+    spec = workloads.spec(e, upper, ext, til, dtype)
+    say("random plan", seed, e, upper, til, len(U["keys"]), len(V["keys"]))
+    if len(U["keys"]) == 0 or len(V["keys"]) == 0:
+        _, out = gpu_run(spec, U, V)
+        assert out.n_pairs == 0 and out.n_w == 0
+        return
+    _, out = gpu_run(spec, U, V)
+    ref = orc.run(orc_plan(orc, spec), U, V)
+    check(out, ref, dtype)
+
+
+def _wider_plans():
+    """Plans with larger tiles so the MFMA class and ragged blocks are hit."""
+    return [
+        ("ij,jk->ik", "j", {"i": 100, "j": 96, "k": 70}, {"j": 32}),          # GEMM, ragged M/N
+        ("ij,jk->ki", "jk", {"i": 64, "j": 256, "k": 256}, {"j": 64, "k": 64}),  # GNN E1 form
+        ("ki,im->km", "k", {"k": 512, "i": 64, "m": 32}, {"k": 64}),            # GNN E2 form
+        ("ik,kn->in", "ik", {"i": 512, "k": 512, "n": 160}, {"i": 128, "k": 128}),
+        ("ijk,jr->ikr", "ijk", {"i": 64, "j": 64, "k": 64, "r": 24}, {"i": 16, "j": 16, "k": 16}),
+        ("ikr,kr->ir", "ik", {"i": 64, "k": 64, "r": 24}, {"i": 16, "k": 16}),
+        ("bij,bjk->bik", "j", {"b": 3, "i": 40, "j": 48, "k": 36}, {"j": 16}),  # batch role in a GEMM
+        ("ija,jkc->ik", "j", {"i": 33, "j": 40, "a": 3, "k": 20, "c": 2}, {"j": 8}),  # pre-sum labels
+        ("ij,kj->ik", "ik", {"i": 96, "j": 80, "k": 96}, {"i": 32, "k": 32}),   # K-fast B, cross product
+        ("ji,jk->ik", "", {"i": 70, "j": 90, "k": 50}, {}),                    # all demoted: one tuple each
+    ]
+
+
+@pytest.mark.parametrize("idx", range(10))
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_wider_plans_gpu(orc, idx, dtype):
+    e, upper, ext, til = _wider_plans()[idx]
+    rng = np.random.default_rng(42 + idx)
+    u_lab, v_lab, _ = split_einsum(e)
+    keep = 1.0 if not upper else 0.7
+    U = workloads.random_relation(rng, u_lab, upper, ext, til, dtype, keep=keep, zero_frac=0.1)
+    V = workloads.random_relation(rng, v_lab, upper, ext, til, dtype, keep=keep, zero_frac=0.1)
+    spec = workloads.spec(e, upper, ext, til, dtype)
+    say("wider plan", idx, dtype, e)
+    _, out = gpu_run(spec, U, V)
+    ref = orc.run(orc_plan(orc, spec), U, V)
+    check(out, ref, dtype)
+
+
+@pytest.mark.parametrize("pmax", [1, 2, 3, 7])
+def test_split_segments_gpu(orc, pmax):
+    """Forcing short work units splits every key's pairs; the segmented sum of
+    the partial tiles must give the same result."""
+    e, upper, ext, til = "ij,jk->ki", "jk", {"i": 64, "j": 512, "k": 256}, {"j": 64, "k": 64}
+    rng = np.random.default_rng(9)
+    U = workloads.random_relation(rng, "ij", upper, ext, til, "f32", keep=0.9)
+    V = workloads.random_relation(rng, "jk", upper, ext, til, "f32", keep=0.8)
+    spec = workloads.spec(e, upper, ext, til, "f32")
+    say("split", pmax)
+    _, out = gpu_run(spec, U, V, max_pairs_per_unit=pmax)
+    assert out.timing is None
+    ref = orc.run(orc_plan(orc, spec), U, V)
+    check(out, ref, "f32")
+
+
+@pytest.mark.parametrize("c", [1, 2, 3, 4, 5])
+def test_small_configs_gpu(orc, c):
+    """Scaled-down twins of the five workloads, every EinSum of each."""
+    w = workloads.config(c, "small")
+    say("small config", c)
+    if c in (1, 2, 5):
+        Y = w["Y"]
+        _, o1 = gpu_run(w["E1"], w["X"], Y)
+        r1 = orc.run(orc_plan(orc, w["E1"]), w["X"], {"keys": Y["keys"], "coo": Y["coo"]})
+        check(o1, r1, w["dtype"])
+        # E2 on its own, with a seeded T of the shape E1 produces
+        rng = np.random.default_rng(5)
+        t2 = w["tile_e2"]
+        nT = w["n"] // t2
+        T = {"keys": np.arange(nT, dtype=np.int32).reshape(-1, 1),
+             "tiles": rng.standard_normal((nT, t2 * w["emb"]), dtype=np.float32), "dtype": w["dtype"]}
+        if w["dtype"] == "bf16":
+            T["tiles"] = workloads.to_bf16_bits(T["tiles"])
+        _, o2 = gpu_run(w["E2"], T, w["Z"])
+        r2 = orc.run(orc_plan(orc, w["E2"]), T, w["Z"])
+        check(o2, r2, w["dtype"])
+    elif c == 3:
+        _, o = gpu_run(w["E"], w["A"], w["B"])
+        check(o, orc.run(orc_plan(orc, w["E"]), w["A"], w["B"]), "f32")
+    else:
+        _, o1 = gpu_run(w["E1"], w["T"], w["B"])
+        r1 = orc.run(orc_plan(orc, w["E1"]), w["T"], w["B"])
+        check(o1, r1, "f32")
+        rng = np.random.default_rng(6)
+        Wr = {"keys": r1.wkeys, "tiles": rng.standard_normal(r1.acc.shape, dtype=np.float32), "dtype": "f32"}
+        _, o2 = gpu_run(w["E2"], Wr, w["C"])
+        check(o2, orc.run(orc_plan(orc, w["E2"]), Wr, w["C"]), "f32")
+
+
+def test_determinism_gpu(orc):
+    """Atomic-free path: two runs give bit-identical tiles and pair lists."""
+    w = workloads.config(2, "small")
+    _, a = gpu_run(w["E1"], w["X"], w["Y"], max_pairs_per_unit=3)
+    _, b = gpu_run(w["E1"], w["X"], w["Y"], max_pairs_per_unit=3)
+    assert np.array_equal(a.pairs.cpu().numpy(), b.pairs.cpu().numpy())
+    assert np.array_equal(a.w_tiles.cpu().numpy().view(np.uint32), b.w_tiles.cpu().numpy().view(np.uint32))
+
+
+def test_key_errors_gpu():
+    import paper_2603_08957_amd as tre
+    import torch
+
+    plan = tre.Plan("ij,jk->ik", "jk", {"i": 4, "j": 8, "k": 8}, {"j": 2, "k": 2}, "f32")
+    uk = torch.arange(4, dtype=torch.int32).reshape(4, 1).cuda()
+    ut = torch.ones((4, 8), dtype=torch.float32).cuda()
+    good = np.array([[0, 1], [0, 3], [2, 0]], np.int32)
+    cases = {"TRE_E_UNSORTED": good[[0, 2, 1]], "TRE_E_DUPKEY": good[[0, 0, 1]],
+             "TRE_E_KEYRANGE": np.array([[0, 1], [0, 4]], np.int32)}
+    for status, vk in cases.items():
+        vkt = torch.from_numpy(vk).cuda()
+        vt = torch.ones((len(vk), 4), dtype=torch.float32).cuda()
+        with pytest.raises(tre.TreError) as ei:
+            tre.einsum(plan, uk, ut, vkt, vt)
+        assert ei.value.status == status
+    # validation off: a valid input still works and the call does not fault
+    plan2 = tre.Plan("ij,jk->ik", "jk", {"i": 4, "j": 8, "k": 8}, {"j": 2, "k": 2}, "f32", validate=False)
+    out = tre.einsum(plan2, uk, ut, torch.from_numpy(good).cuda(), torch.ones((3, 4)).cuda())
+    assert out.n_pairs == 3
+
+
+def test_capacity_and_workspace_errors_gpu():
+    import paper_2603_08957_amd as tre
+    import torch
+
+    plan = tre.Plan("ij,jk->ik", "j", {"i": 8, "j": 8, "k": 8}, {"j": 1}, "f32")
+    uk = torch.arange(8, dtype=torch.int32).reshape(8, 1).cuda()
+    ut = torch.ones((8, 8)).cuda()
+    # workspace for 0 pairs: join reports the required count
+    ws = tre.alloc_workspace(plan.workspace_bytes(8, 8, 0))
+    with pytest.raises(tre.TreError) as ei:
+        tre.join(plan, uk, 8, uk, 8, ws)
+    assert ei.value.status == "TRE_E_WORKSPACE" and ei.value.join_result.n_pairs == 8
+    ws = tre.alloc_workspace(plan.workspace_bytes(8, 8, 8))
+    jr = tre.join(plan, uk, 8, uk, 8, ws)
+    assert jr.n_pairs == 8 and jr.n_w == 1
+    small = torch.empty((0, 64)).cuda()
+    with pytest.raises(tre.TreError) as ei:
+        tre.contract(plan, jr, ut, ut, None, small)
+    assert ei.value.status == "TRE_E_CAPACITY"
+
+
+def test_empty_inputs_gpu():
+    import paper_2603_08957_amd as tre
+    import torch
+
+    plan = tre.Plan("ij,jk->ik", "j", {"i": 4, "j": 4, "k": 4}, {"j": 2}, "f32")
+    out = tre.einsum(plan, torch.zeros((0, 1), dtype=torch.int32).cuda(), torch.zeros((0, 8)).cuda(),
+                     torch.zeros((1, 1), dtype=torch.int32).cuda(), torch.ones((1, 8)).cuda(), want_pairs=True)
+    assert out.n_pairs == 0 and out.n_w == 0
+
+
+def test_cast_bf16_gpu(orc):
+    import paper_2603_08957_amd as tre
+    import torch
+
+    rng = np.random.default_rng(0)
+    x = (rng.standard_normal(100003) * 10.0 ** rng.integers(-20, 20, 100003)).astype(np.float32)
+    x[:6] = [0.0, -0.0, np.inf, -np.inf, np.nan, 1 + 2 ** -8]
+    y = tre.cast_f32_bf16(torch.from_numpy(x).cuda())
+    got = y.view(torch.int16).cpu().numpy().view(np.uint16)
+    ref = orc.f32_to_bf16(x)
+    assert np.array_equal(got[5:], ref[5:])
+    assert (got[4] & 0x7F80) == 0x7F80 and (got[4] & 0x7F)  # NaN stays NaN
+
+
+def test_stack_rows_gpu(orc):
+    import paper_2603_08957_amd as tre
+    import torch
+
+    rng = np.random.default_rng(3)
+    keys = np.sort(rng.choice(1000, size=300, replace=False)).astype(np.int32)
+    rows = rng.standard_normal((300, 12)).astype(np.float32)
+    k, t = tre.stack_rows(torch.from_numpy(keys).cuda(), torch.from_numpy(rows).cuda(), 16)
+    rk, rt = orc.stack_rows(keys, rows, 16)
+    assert np.array_equal(k.cpu().numpy(), rk)
+    assert np.array_equal(t.cpu().numpy(), rt)
+
+
+def test_tiles_from_entries_gpu(orc):
+    import paper_2603_08957_amd as tre
+    import torch
+
+    w = workloads.config(2, "small")
+    Y = w["Y"]
+    vals = torch.from_numpy(Y["values"].view(np.int16)).cuda().view(torch.bfloat16)
+    tiles = tre.tiles_from_entries(torch.from_numpy(Y["slot"]).cuda(), torch.from_numpy(Y["offset"]).cuda(), vals,
+                                   len(Y["keys"]), Y["tile_elems"])
+    assert np.array_equal(tiles.view(torch.int16).cpu().numpy().view(np.uint16), Y["tiles"])
+    p1 = orc_plan(orc, w["E1"])
+    c, v, _ = orc.expand(p1, 1, Y["keys"], tiles.view(torch.int16).cpu().numpy().view(np.uint16), "bf16")
+    got = sorted(zip(map(tuple, c.tolist()), v.tolist()))
+    ref = sorted(zip(map(tuple, Y["coo"][0].tolist()), Y["coo"][1].tolist()))
+    assert got == ref
