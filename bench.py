@@ -1,0 +1,412 @@
+"""Benchmark: one decomposed EinSum chain per step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+
+A step is one pass of the whole hot path over one batch of synthetic input
+that is already resident in HBM: for the default workload (the bf16 GNN
+message-passing chain (X.Y)^T.Z on a 262,144-vertex power-law graph with
+128x128 tiles) that is E1 = join X with Y on J + tile contraction + group by
+K, the fp32 -> bf16 cast of T, and E2 = cross product of T with Z + tile
+contraction.  Prints one JSON line:
+
+  value       effective tile GFLOP/s of the step = sum over EinSums of
+              (matched pairs x dense tile flops per pair) / step time
+  roofline    the dominant kernel (E1's tile contraction): algorithmic bytes
+              or flops per launch / its average launch time, measured with
+              HIP events on the launch stream inside the timed region
+  cpu_baseline the CPU oracle timed on a bounded sample of the same inputs
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}
+METRIC = "effective tile GFLOP/s + join/reduce HBM GB/s per EinSum, 1 MI355X"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def dev_rel(rel, torch):
+    keys = torch.from_numpy(np.ascontiguousarray(rel["keys"], dtype=np.int32)).cuda()
+    t = np.ascontiguousarray(rel["tiles"])
+    if rel["dtype"] == "bf16":
+        tiles = torch.from_numpy(t.view(np.int16)).cuda().view(torch.bfloat16)
+    else:
+        tiles = torch.from_numpy(t).cuda()
+    return keys, tiles
+
+
+class Stage:
+    """One binary EinSum with preallocated workspace and outputs."""
+
+    def __init__(self, tre, torch, spec, n_u, n_v, n_pairs, name):
+        self.tre, self.torch, self.name = tre, torch, name
+        self.plan = tre.Plan.from_spec(spec, validate=False)
+        self.spec = spec
+        self.ws = tre.alloc_workspace(self.plan.workspace_bytes(n_u, n_v, n_pairs))
+        self.n_u, self.n_v = n_u, n_v
+        self.w_keys = None
+        self.w_tiles = None
+        self.n_pairs = 0
+        self.n_w = 0
+        self.record = None  # a Timing to fill synchronously on the next run
+
+    def phase_report(self):
+        """Join / contract / reduce times of the last recorded run and their
+        algorithmic HBM rates: the join reads the int32 keys once and writes
+        the (u, v) pair list and the segment table once; the contraction
+        reads every input tuple once and writes every output tile once; the
+        reduction reads and writes partial tiles of split keys only."""
+        t = self.record
+        jb = 4 * (self.n_u * self.plan.key_arity[0] + self.n_v * self.plan.key_arity[1]) + 8 * self.n_pairs \
+            + 12 * self.n_w
+        rb = (t.n_partials + t.n_split_segments) * self.tile_bytes(2) if t.n_split_segments else 0
+        gbs = lambda b, ms: (b / (ms * 1e-3) / 1e9) if ms > 0 else None  # noqa: E731
+        return {"join_ms": t.join_ms, "join_alg_bytes": jb, "join_GBs": gbs(jb, t.join_ms),
+                "contract_ms": t.contract_ms, "contract_alg_bytes": self.alg_bytes(),
+                "contract_GBs": gbs(self.alg_bytes(), t.contract_ms),
+                "contract_TFLOPs": self.flops() / (t.contract_ms * 1e-3) / 1e12 if t.contract_ms > 0 else None,
+                "units_ms": t.units_ms, "reduce_ms": t.reduce_ms, "reduce_alg_bytes": rb,
+                "reduce_GBs": gbs(rb, t.reduce_ms) if rb else None, "n_units": t.n_units,
+                "n_split_segments": t.n_split_segments}
+
+    def run(self, uk, ut, vk, vt, timing=None):
+        tre = self.tre
+        if self.record is not None:
+            timing = self.record
+            timing.deferred = 0
+        jr = tre.join(self.plan, uk, self.n_u, vk, self.n_v, self.ws, timing=timing)
+        if self.w_tiles is None or self.w_tiles.shape[0] < jr.n_w:
+            self.w_keys = self.torch.empty((jr.n_w, max(self.plan.key_arity[2], 1)), dtype=self.torch.int32,
+                                           device="cuda")
+            self.w_tiles = self.torch.empty((jr.n_w, self.plan.tile_elems[2]), dtype=self.torch.float32,
+                                            device="cuda")
+        tre.contract(self.plan, jr, ut, vt, self.w_keys if self.plan.key_arity[2] else None,
+                     self.w_tiles[:jr.n_w], None, timing=timing)
+        self.n_pairs, self.n_w = int(jr.n_pairs), int(jr.n_w)
+        return self.w_keys[:jr.n_w], self.w_tiles[:jr.n_w]
+
+    def tile_bytes(self, op):
+        eb = 2 if self.spec["dtype"] == "bf16" else 4
+        return self.plan.tile_elems[op] * (4 if op == 2 else eb)
+
+    def flops(self):
+        return self.n_pairs * self.plan.flops_per_pair
+
+    def alg_bytes(self):
+        """Read every input tuple once, write every output tile once."""
+        return self.n_u * self.tile_bytes(0) + self.n_v * self.tile_bytes(1) + self.n_w * self.tile_bytes(2)
+
+
+# ------------------------------------------------------------ workloads
+
+class GnnChain:
+    """(X.Y)^T.Z: E1 'ij,jk->ki' over (X keyed J, Y keyed (J,K)), cast, E2 'ki,im->km'."""
+
+    def __init__(self, c, tre, torch):
+        import workloads
+
+        self.c = c
+        t0 = time.time()
+        w = workloads.config(c)
+        log(f"[bench] generated workload {c} in {time.time() - t0:.1f}s: {w['n_edges']} edges, "
+            f"{len(w['Y']['keys'])} Y tuples")
+        self.w = w
+        self.tre, self.torch = tre, torch
+        self.xk, self.xt = dev_rel(w["X"], torch)
+        Y = w["Y"]
+        self.yk = torch.from_numpy(Y["keys"]).cuda()
+        if w["tile_e1"] == 1:
+            self.yt = dev_rel({"keys": Y["keys"], "tiles": Y["tiles"], "dtype": w["dtype"]}, torch)[1]
+        else:
+            vals = Y["values"]
+            v = torch.from_numpy(vals.view(np.int16)).cuda().view(torch.bfloat16) if w["dtype"] == "bf16" \
+                else torch.from_numpy(vals).cuda()
+            self.yt = tre.tiles_from_entries(torch.from_numpy(Y["slot"]).cuda(), torch.from_numpy(Y["offset"]).cuda(),
+                                             v, len(Y["keys"]), Y["tile_elems"])
+            del v
+        self.zk, self.zt = dev_rel(w["Z"], torch)
+        nY = len(Y["keys"])
+        nX = len(w["X"]["keys"])
+        self.e1 = Stage(tre, torch, w["E1"], nX, nY, nY, "E1")
+        n_t = w["n"] // w["tile_e1"]
+        self.e2 = None
+        self.bf = w["dtype"] == "bf16"
+        self.stack = w["tile_e2"] // w["tile_e1"]
+        self.n_t2 = w["n"] // w["tile_e2"]
+        self.e2 = Stage(tre, torch, w["E2"], self.n_t2, 1, self.n_t2, "E2")
+        self.t_cast = None
+        self.n_t = n_t
+        torch.cuda.synchronize()
+
+    def step(self, timing=None):
+        tre, torch = self.tre, self.torch
+        tk, tt = self.e1.run(self.xk, self.xt, self.yk, self.yt, timing=timing)
+        if self.stack > 1:
+            tk, tt = tre.stack_rows(tk, tt, self.stack)
+        if self.bf:
+            if self.t_cast is None or self.t_cast.numel() < tt.numel():
+                self.t_cast = torch.empty(tt.numel(), dtype=torch.bfloat16, device="cuda")
+            tb = tre.cast_f32_bf16(tt, out=self.t_cast[:tt.numel()]).view(tt.shape)
+        else:
+            tb = tt
+        self.e2.n_u = int(tk.shape[0])
+        return self.e2.run(tk, tb, self.zk, self.zt)
+
+    def stages(self):
+        return [self.e1, self.e2]
+
+    def describe(self):
+        w = self.w
+        return {"workload": f"GNN chain (X.Y)^T.Z, {w['dtype']}: {w['n']} vertices, "
+                            f"{'power-law out-degree' if self.c != 1 else '8 out-edges per vertex'}, "
+                            f"embedding {w['emb']}, Z {w['emb']}x{w['z_out']}, E1 tiles {w['tile_e1']}, "
+                            f"E2 tiles {w['tile_e2']}",
+                "vertices": w["n"], "edges": w["n_edges"], "embedding": w["emb"], "tile_e1": w["tile_e1"],
+                "tile_e2": w["tile_e2"], "y_tuples": len(w["Y"]["keys"]),
+                "einsums": [w["E1"]["einsum"] + " upper " + w["E1"]["upper"],
+                            w["E2"]["einsum"] + " upper " + w["E2"]["upper"]]}
+
+    def oracle_sample(self, orc, n_keys_e1=4, n_keys_e2=64):
+        """Time the oracle on a bounded sample: n_keys_e1 output keys of E1 and
+        n_keys_e2 of E2 (seeded choice), restricted to the tuples that feed them."""
+        w = self.w
+        rng = np.random.default_rng(0)
+        p1 = orc.Plan(w["E1"]["einsum"], w["E1"]["upper"], w["E1"]["extents"], w["E1"]["tiles"])
+        Y = w["Y"]
+        all_k = np.unique(Y["keys"][:, 1])
+        S = np.sort(rng.choice(all_k, size=min(n_keys_e1, len(all_k)), replace=False)).reshape(-1, 1).astype(np.int32)
+        mu, mv = orc.restrict(p1, w["X"]["keys"], Y["keys"], S)
+        ykeep = mv[Y["slot"]]
+        t0 = time.perf_counter()
+        uc, uv, _ = orc.expand(p1, 0, w["X"]["keys"][mu], w["X"]["tiles"][mu], w["dtype"])
+        acc, mag, _ = orc.evaluate(p1, uc, uv, Y["coo"][0][ykeep], Y["coo"][1][ykeep], S)
+        t1 = time.perf_counter()
+        pairs1 = int(np.isin(Y["keys"][:, 1], S[:, 0]).sum())
+        flops1 = pairs1 * self.e1.plan.flops_per_pair
+        # E2 sample: synthetic T rows for the sampled keys (same shapes)
+        p2 = orc.Plan(w["E2"]["einsum"], w["E2"]["upper"], w["E2"]["extents"], w["E2"]["tiles"])
+        te = w["tile_e2"] * w["emb"]
+        S2 = np.sort(rng.choice(self.n_t2, size=min(n_keys_e2, self.n_t2), replace=False)).reshape(-1, 1)
+        T = rng.standard_normal((len(S2), te)).astype(np.float32)
+        t2 = time.perf_counter()
+        tc, tv, _ = orc.expand(p2, 0, S2.astype(np.int32), T, "f32")
+        zc, zv, _ = orc.expand(p2, 1, w["Z"]["keys"], w["Z"]["tiles"], w["dtype"])
+        orc.evaluate(p2, tc, tv, zc, zv, S2.astype(np.int32))
+        t3 = time.perf_counter()
+        flops2 = len(S2) * self.e2.plan.flops_per_pair
+        secs = (t1 - t0) + (t3 - t2)
+        return {"value": (flops1 + flops2) / secs / 1e9, "unit": "GFLOP/s", "cores": 1, "kind": "oracle",
+                "sample": f"E1 restricted to {len(S)} of {len(all_k)} output keys ({pairs1} tile pairs) + "
+                          f"E2 restricted to {len(S2)} of {self.n_t2} output keys; tile-flop-equivalent rate, "
+                          f"single-threaded fp64 C oracle, {secs:.1f} s",
+                "seconds": secs}
+
+
+class BlockSparse:
+    def __init__(self, c, tre, torch):
+        import workloads
+
+        w = workloads.config(c)
+        self.w, self.tre, self.torch = w, tre, torch
+        self.ak, self.at = dev_rel(w["A"], torch)
+        self.bk, self.bt = dev_rel(w["B"], torch)
+        n = len(w["A"]["keys"])
+        self.e = Stage(tre, torch, w["E"], n, len(w["B"]["keys"]), n, "E")
+
+    def step(self, timing=None):
+        return self.e.run(self.ak, self.at, self.bk, self.bt, timing=timing)
+
+    def stages(self):
+        return [self.e]
+
+    def describe(self):
+        w = self.w
+        return {"workload": f"block-sparse A.B, fp32: A {w['n']}x{w['n']} with 5% of {w['block']}x{w['block']} "
+                            f"blocks, B {w['n']}x{w['n_cols']}", "a_blocks": len(w["A"]["keys"])}
+
+    def oracle_sample(self, orc, n_keys=2):
+        w = self.w
+        p = orc.Plan(w["E"]["einsum"], w["E"]["upper"], w["E"]["extents"], w["E"]["tiles"])
+        S = np.unique(w["A"]["keys"][:, 0])[:n_keys].reshape(-1, 1).astype(np.int32)
+        mu, mv = orc.restrict(p, w["A"]["keys"], w["B"]["keys"], S)
+        t0 = time.perf_counter()
+        uc, uv, _ = orc.expand(p, 0, w["A"]["keys"][mu], w["A"]["tiles"][mu], "f32")
+        vc, vv, _ = orc.expand(p, 1, w["B"]["keys"][mv], w["B"]["tiles"][mv], "f32")
+        orc.evaluate(p, uc, uv, vc, vv, S)
+        secs = time.perf_counter() - t0
+        flops = int(mu.sum()) * self.e.plan.flops_per_pair
+        return {"value": flops / secs / 1e9, "unit": "GFLOP/s", "cores": 1, "kind": "oracle",
+                "sample": f"{n_keys} output keys ({int(mu.sum())} tile pairs), {secs:.1f} s", "seconds": secs}
+
+
+class ThreeWay:
+    def __init__(self, c, tre, torch):
+        import workloads
+
+        w = workloads.config(c)
+        self.w, self.tre, self.torch = w, tre, torch
+        self.tk, self.tt = dev_rel(w["T"], torch)
+        self.bk, self.bt = dev_rel(w["B"], torch)
+        self.ck, self.ct = dev_rel(w["C"], torch)
+        n = len(w["T"]["keys"])
+        self.e1 = Stage(tre, torch, w["E1"], n, len(w["B"]["keys"]), n, "E1")
+        self.e2 = Stage(tre, torch, w["E2"], n, len(w["C"]["keys"]), n, "E2")
+
+    def step(self, timing=None):
+        wk, wt = self.e1.run(self.tk, self.tt, self.bk, self.bt, timing=timing)
+        self.e2.n_u = int(wk.shape[0])
+        return self.e2.run(wk, wt, self.ck, self.ct)
+
+    def stages(self):
+        return [self.e1, self.e2]
+
+    def describe(self):
+        w = self.w
+        return {"workload": f"sparse 3-way A[i,r] = sum_jk T[i,j,k] B[j,r] C[k,r], fp32: T {w['n']}^3 as "
+                            f"{w['block']}^3 blocks (0.5% of blocks, 10% dense), r {w['r']}",
+                "t_blocks": len(w["T"]["keys"])}
+
+    def oracle_sample(self, orc, n_keys=1):
+        w = self.w
+        p = orc.Plan(w["E1"]["einsum"], w["E1"]["upper"], w["E1"]["extents"], w["E1"]["tiles"])
+        keys = w["T"]["keys"]
+        ik = np.unique(keys[:, [0, 2]], axis=0)[:64].astype(np.int32)
+        mu, mv = orc.restrict(p, keys, w["B"]["keys"], ik)
+        t0 = time.perf_counter()
+        uc, uv, _ = orc.expand(p, 0, keys[mu], w["T"]["tiles"][mu], "f32")
+        vc, vv, _ = orc.expand(p, 1, w["B"]["keys"][mv], w["B"]["tiles"][mv], "f32")
+        orc.evaluate(p, uc, uv, vc, vv, ik)
+        secs = time.perf_counter() - t0
+        flops = int(mu.sum()) * self.e1.plan.flops_per_pair
+        return {"value": flops / secs / 1e9, "unit": "GFLOP/s", "cores": 1, "kind": "oracle",
+                "sample": f"E1 restricted to 64 output keys ({int(mu.sum())} tile pairs), {secs:.1f} s",
+                "seconds": secs}
+
+
+def make_workload(c, tre, torch):
+    if c in (1, 2, 5):
+        return GnnChain(c, tre, torch)
+    if c == 3:
+        return BlockSparse(c, tre, torch)
+    if c == 4:
+        return ThreeWay(c, tre, torch)
+    raise SystemExit(f"unknown workload {c}")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default 2: bf16 GNN chain, 262,144 vertices)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (the path shards by output key "
+              f"across GPUs by design, but this build runs on a single MI355X)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    tre.lib()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    W = make_workload(args.config, tre, torch)
+    log("[bench] inputs resident; warming up")
+    for _ in range(args.warmup):
+        W.step()
+    torch.cuda.synchronize()
+    stages = W.stages()
+    dom = stages[0]
+    timings = []
+    log(f"[bench] timing {args.steps} steps")
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record()
+    for _ in range(args.steps):
+        tm = tre.Timing()
+        tm.deferred = 1
+        W.step(timing=tm)
+        timings.append(tm)
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = ev0.elapsed_time(ev1) / args.steps
+    for tm in timings:
+        tm.read()
+    contract_ms = float(np.mean([t.contract_ms for t in timings]))
+    units_ms = float(np.mean([t.units_ms for t in timings]))
+    reduce_ms = float(np.mean([t.reduce_ms for t in timings]))
+    # per-EinSum phase times (join / contract / reduce) from one extra pass
+    # with synchronous library timing, outside the timed region
+    for st in stages:
+        st.record = tre.Timing()
+    W.step()
+    torch.cuda.synchronize()
+    phases = {st.name: st.phase_report() for st in stages}
+    for st in stages:
+        st.record = None
+    flops = sum(st.flops() for st in stages)
+    value = flops / (ms_step * 1e-3) / 1e9
+    dtype = "bf16" if dom.spec["dtype"] == "bf16" else "f32"
+    alg = dom.alg_bytes()
+    dflops = dom.flops()
+    t_hbm = alg / (PEAK_HBM_GBS * 1e9)
+    t_mfma = dflops / (PEAK_TFLOPS[dtype] * 1e12)
+    if t_hbm >= t_mfma:
+        roof = {"bound": "hbm", "achieved": alg / (contract_ms * 1e-3) / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    else:
+        roof = {"bound": "mfma", "achieved": dflops / (contract_ms * 1e-3) / 1e12, "peak": PEAK_TFLOPS[dtype],
+                "unit": "TFLOP/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = None
+    roof["kernel"] = f"{dom.name} tile contraction ({dom.plan.kernel_class})"
+    roof["kernel_ms"] = contract_ms
+    roof["alg_bytes_per_launch"] = alg
+    roof["flops_per_launch"] = dflops
+    roof["mfma_tflops"] = dflops / (contract_ms * 1e-3) / 1e12
+    roof["mfma_frac"] = roof["mfma_tflops"] / PEAK_TFLOPS[dtype]
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+
+        oracle.build()
+        log("[bench] timing the CPU oracle on a bounded sample")
+        cpu = W.oracle_sample(oracle)
+    per_stage = []
+    for st in stages:
+        per_stage.append({"einsum": st.spec["einsum"], "upper": st.spec["upper"], "n_pairs": st.n_pairs,
+                          "n_w": st.n_w, "tile_gflop": st.flops() / 1e9, "alg_bytes": st.alg_bytes()})
+    out = {
+        "metric": METRIC, "value": value, "unit": "GFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": dtype, "data": "synthetic",
+        "config": W.describe(),
+        "roofline": roof, "cpu_baseline": cpu,
+        "timed_region": {"dominant_contract_ms": contract_ms, "dominant_units_ms": units_ms,
+                         "dominant_reduce_and_write_ms": reduce_ms, "wall_s": wall},
+        "phases": phases,
+        "einsums": per_stage,
+    }
+    if cpu is not None:
+        cpu.pop("seconds", None)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -98,14 +98,24 @@ typedef struct {
     uint64_t internal[16];    /* workspace layout; do not modify */
 } tre_join_result;
 
-/* Optional per-phase device timings (milliseconds, hipEvent based). */
+/* Optional per-phase device timings (milliseconds, hipEvent based).
+ * With `deferred` = 0 the call waits for its own events before returning.
+ * With `deferred` != 0 tre_contract only records events on the stream (no
+ * wait); tre_timing_read later waits for them, fills the millisecond fields
+ * and releases the events.  A struct with `pending` set must be read (or the
+ * events leak). */
 typedef struct {
-    float join_ms;            /* key packing, validation, sort, join, group-by */
-    float contract_ms;        /* work units and tile contraction */
-    float reduce_ms;          /* segmented sum of split segments */
+    float join_ms;            /* key validation, join, group-by (tre_join; always immediate) */
+    float units_ms;           /* offset tables and work units */
+    float contract_ms;        /* the tile-contraction kernel alone */
+    float reduce_ms;          /* segmented sum of split segments + key / pair write-out */
     float total_ms;
+    int32_t deferred;         /* in */
+    int32_t pending;          /* out: events recorded, not yet read */
     int64_t n_units;
     int64_t n_split_segments;
+    int64_t n_partials;       /* partial tiles written by units of split segments */
+    void *events[4];          /* library-owned while pending */
 } tre_timing;
 
 /* tre_plan -- parse and classify one binary EinSum (host only, no device work).
@@ -158,10 +168,13 @@ tre_status tre_join(tre_plan_t plan, const int32_t *u_keys, int64_t n_u, const i
  *   w_tiles : device [w_cap x tile_elems(W)] fp32.
  *   pairs_out : device [pair_cap x 2] int32 (u, v) or NULL.
  * TRE_E_CAPACITY if w_cap < n_w or (pairs_out and pair_cap < n_pairs).
- * Asynchronous on the stream unless timing is non-NULL (then it waits). */
+ * Asynchronous on the stream unless timing is non-NULL and not deferred. */
 tre_status tre_contract(tre_plan_t plan, const tre_join_result *jr, const void *u_tiles, const void *v_tiles,
                         int32_t *w_keys, int64_t w_cap, float *w_tiles, int32_t *pairs_out, int64_t pair_cap,
                         void *stream, tre_timing *timing);
+
+/* Wait for the events of a deferred tre_contract timing and fill its fields. */
+tre_status tre_timing_read(tre_timing *timing);
 
 /* tre_execute -- tre_join followed by tre_contract.  n_w / n_pairs (host) are
  * always written when the join succeeded, also with TRE_E_CAPACITY. */

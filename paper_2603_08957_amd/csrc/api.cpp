@@ -17,16 +17,20 @@ tre_status dev_fail(hipError_t e, const char* where) {
     return TRE_E_DEVICE;
 }
 
+// hipEvent timer.  In deferred mode the events are handed to the caller's
+// tre_timing and read later by tre_timing_read.
 struct Timer {
     bool on = false;
+    bool keep = false;
     hipEvent_t ev[4] = {};
     int n = 0;
-    explicit Timer(bool enable) : on(enable) {
+    explicit Timer(bool enable, bool deferred = false) : on(enable), keep(deferred) {
         if (on)
             for (auto& e : ev)
                 if (hipEventCreate(&e) != hipSuccess) on = false;
     }
     ~Timer() {
+        if (keep && on) return;
         for (auto& e : ev)
             if (e) (void)hipEventDestroy(e);
     }
@@ -42,6 +46,15 @@ struct Timer {
         return ms;
     }
 };
+
+float elapsed(void* a, void* b) {
+    float ms = 0.f;
+    if (a && b) {
+        (void)hipEventSynchronize(reinterpret_cast<hipEvent_t>(b));
+        (void)hipEventElapsedTime(&ms, reinterpret_cast<hipEvent_t>(a), reinterpret_cast<hipEvent_t>(b));
+    }
+    return ms;
+}
 
 tre_status key_error(int32_t flags) {
     if (flags & 4) return TRE_E_KEYRANGE;
@@ -161,7 +174,9 @@ tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const i
     out->internal[3] = uint64_t(ws_bytes);
     out->internal[4] = uint64_t(max_pairs);
     if (timing) {
+        const int32_t deferred = timing->deferred;
         std::memset(timing, 0, sizeof(*timing));
+        timing->deferred = deferred;
         timing->join_ms = tm.between(0, 1);
         timing->total_ms = timing->join_ms;
     }
@@ -193,12 +208,14 @@ tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* 
     char* w = reinterpret_cast<char*>(jr->internal[2]);
     const Layout L = make_layout(p, jr->n_u, jr->n_v, int64_t(jr->internal[4]));
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    Timer tm(timing != nullptr);
+    const bool deferred = timing && timing->deferred;
+    Timer tm(timing != nullptr, deferred);
     tm.mark(s);
     const int64_t p_unit = choose_unit(p, L, n_pairs, n_w);
     hipError_t e;
     if ((e = launch_tables(p, reinterpret_cast<int32_t*>(w + L.tables), s)) != hipSuccess) return dev_fail(e, "tables");
     if ((e = launch_units(p, L, w, n_pairs, n_w, p_unit, s)) != hipSuccess) return dev_fail(e, "units");
+    tm.mark(s);
     const int64_t unit_bound = n_w + n_pairs / p_unit + 1;
     if ((e = launch_contract(p, L, w, u_tiles, v_tiles, w_tiles, n_pairs, n_w, unit_bound, s)) != hipSuccess)
         return dev_fail(e, "contract");
@@ -211,15 +228,37 @@ tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* 
         return dev_fail(e, "outputs");
     tm.mark(s);
     if (timing) {
-        timing->contract_ms = tm.between(0, 1);
-        timing->reduce_ms = tm.between(1, 2);
-        timing->total_ms += tm.between(0, 2);
+        if (deferred && tm.on) {
+            for (int i = 0; i < 4; i++) timing->events[i] = reinterpret_cast<void*>(tm.ev[i]);
+            timing->pending = 1;
+        } else {
+            timing->units_ms = tm.between(0, 1);
+            timing->contract_ms = tm.between(1, 2);
+            timing->reduce_ms = tm.between(2, 3);
+            timing->total_ms += tm.between(0, 3);
+        }
         WsHeader h{};
-        if (hipMemcpy(&h, w + L.hdr, sizeof(h), hipMemcpyDeviceToHost) == hipSuccess) {
+        if (!deferred && hipMemcpy(&h, w + L.hdr, sizeof(h), hipMemcpyDeviceToHost) == hipSuccess) {
             timing->n_units = h.n_units;
             timing->n_split_segments = h.n_split;
+            timing->n_partials = h.n_parts;
         }
     }
+    return TRE_OK;
+}
+
+tre_status tre_timing_read(tre_timing* t) {
+    if (!t) return TRE_E_ARG;
+    if (!t->pending) return TRE_OK;
+    t->units_ms = elapsed(t->events[0], t->events[1]);
+    t->contract_ms = elapsed(t->events[1], t->events[2]);
+    t->reduce_ms = elapsed(t->events[2], t->events[3]);
+    t->total_ms += elapsed(t->events[0], t->events[3]);
+    for (auto& e : t->events) {
+        if (e) (void)hipEventDestroy(reinterpret_cast<hipEvent_t>(e));
+        e = nullptr;
+    }
+    t->pending = 0;
     return TRE_OK;
 }
 

@@ -25,7 +25,7 @@ DTYPE = {"f32": 0, "bf16": 1}
 # every symbol include/tre.h declares
 EXPORTS = [
     "tre_plan", "tre_plan_get_info", "tre_plan_destroy", "tre_workspace_bytes", "tre_workspace_max_pairs",
-    "tre_join", "tre_contract", "tre_execute", "tre_cast_f32_bf16", "tre_stack_workspace_bytes", "tre_stack_rows",
+    "tre_join", "tre_contract", "tre_execute", "tre_timing_read", "tre_cast_f32_bf16", "tre_stack_workspace_bytes", "tre_stack_rows",
     "tre_tiles_from_entries", "tre_status_str", "tre_last_error", "tre_version",
 ]
 
@@ -56,11 +56,18 @@ class JoinResult(ctypes.Structure):
 
 
 class Timing(ctypes.Structure):
-    _fields_ = [("join_ms", ctypes.c_float), ("contract_ms", ctypes.c_float), ("reduce_ms", ctypes.c_float),
-                ("total_ms", ctypes.c_float), ("n_units", ctypes.c_int64), ("n_split_segments", ctypes.c_int64)]
+    _fields_ = [("join_ms", ctypes.c_float), ("units_ms", ctypes.c_float), ("contract_ms", ctypes.c_float),
+                ("reduce_ms", ctypes.c_float), ("total_ms", ctypes.c_float), ("deferred", ctypes.c_int32),
+                ("pending", ctypes.c_int32), ("n_units", ctypes.c_int64), ("n_split_segments", ctypes.c_int64),
+                ("n_partials", ctypes.c_int64), ("events", ctypes.c_void_p * 4)]
+
+    def read(self):
+        """Wait for deferred events and fill the millisecond fields."""
+        _check(lib().tre_timing_read(ctypes.byref(self)), "tre_timing_read")
+        return self
 
     def as_dict(self):
-        return {k: getattr(self, k) for k, _ in self._fields_}
+        return {k: getattr(self, k) for k, _ in self._fields_ if k not in ("events", "deferred", "pending")}
 
 
 _lib = None
@@ -85,6 +92,7 @@ def lib():
         L.tre_join.argtypes = [P, P, i64, P, i64, P, sz, P, P, P]
         L.tre_contract.argtypes = [P, P, P, P, P, i64, P, P, i64, P, P]
         L.tre_execute.argtypes = [P, P, i64, P, P, i64, P, P, P, i64, P, P, i64, P, P, sz, P, P]
+        L.tre_timing_read.argtypes = [P]
         L.tre_cast_f32_bf16.argtypes = [P, P, i64, P]
         L.tre_stack_workspace_bytes.argtypes = [i64]
         L.tre_stack_workspace_bytes.restype = sz
