@@ -80,7 +80,7 @@ typedef struct {
     int32_t key_arity[3];     /* r_U, r_V, r_W */
     int64_t tile_elems[3];    /* elements per tile of U, V, W */
     int32_t n_join;           /* promoted labels shared by U and V */
-    int32_t kernel_class;     /* 0 = MFMA tile GEMM, 1 = vector (scale / GEMV / dot) */
+    int32_t kernel_class;     /* 0 = MFMA tile GEMM, 1 = vector (scale / GEMV / dot), 2 = bf16 MFMA GEMM, 128x128 blocks */
     int64_t batch, m, n, k;   /* per-pair contraction: W[b,m,n] += sum_k U[b,m,k] V[b,k,n] */
     int64_t flops_per_pair;   /* 2 * batch * m * n * k */
     char key_labels[3][27];   /* promoted labels of U, V, W in key order (NUL-terminated) */

@@ -66,6 +66,7 @@ tre_status key_error(int32_t flags) {
 int64_t blocks_per_unit(const Plan& p) {
     if (p.kclass == KC_GEMM) {
         const int64_t M = p.swap ? p.nN : p.nM, N = p.swap ? p.nM : p.nN;
+        if (p.fast) return (M / 128) * (N / 128);
         return p.nB * ((M + 63) / 64) * ((N + 63) / 64);
     }
     return (p.tile_elems[2] + 255) / 256;

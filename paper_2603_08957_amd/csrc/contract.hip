@@ -387,6 +387,7 @@ hipError_t launch_contract(const Plan& p, const Layout& L, char* ws, const void*
     const Unit* units = reinterpret_cast<const Unit*>(ws + L.unit_desc);
     const WsHeader* hdr = reinterpret_cast<const WsHeader*>(ws + L.hdr);
     float* parts = reinterpret_cast<float*>(ws + L.partials);
+    if (p.kclass == KC_GEMM && p.fast) return launch_gemm_fast(p, L, ws, u_tiles, v_tiles, w_tiles, unit_bound, s);
     if (p.kclass == KC_GEMM) {
         GemmArgs g{};
         g.A = p.swap ? v_tiles : u_tiles;

@@ -299,6 +299,31 @@ static tre_status classify(Plan& p) {
                   (p.a_kfast ? (runs_of_8(tAK) && all_mult_8(tAM)) : (runs_of_8(tAM) && all_mult_8(tAK)));
         p.vec_b = te_b && all_mult_8(tBB) &&
                   (p.b_kfast ? (runs_of_8(tBK) && all_mult_8(tBN)) : (runs_of_8(tBN) && all_mult_8(tBK)));
+        // Fast path: bf16, no batch, 128-multiple M/N, 64-multiple K, every
+        // operand a plain 2-D row-major matrix (one unit stride, one leading
+        // dimension) and W stored with N fastest.
+        auto affine = [](const std::vector<int32_t>& t, int64_t& s) {
+            s = t.size() > 1 ? t[1] - t[0] : 0;
+            for (size_t i = 0; i < t.size(); i++)
+                if (t[i] != int64_t(i) * s) return false;
+            return true;
+        };
+        auto tWM = host_table(p.dims[T_WM]), tWN = host_table(p.dims[T_WN]);
+        const int64_t M = p.swap ? p.nN : p.nM, N = p.swap ? p.nM : p.nN;
+        int64_t sAM, sAK, sBN, sBK, sWM, sWN;
+        bool ok = p.dtype == TRE_BF16 && p.nB == 1 && M % 128 == 0 && N % 128 == 0 && p.nK % 64 == 0 &&
+                  affine(tAM, sAM) && affine(tAK, sAK) && affine(tBN, sBN) && affine(tBK, sBK) &&
+                  affine(tWM, sWM) && affine(tWN, sWN) && sWN == 1 && sWM >= N;
+        if (ok) {
+            if (sAK == 1 && sAM >= p.nK) { p.fast_a_rowfast = false; p.fast_lda = sAM; }
+            else if (sAM == 1 && sAK >= M) { p.fast_a_rowfast = true; p.fast_lda = sAK; }
+            else ok = false;
+            if (sBK == 1 && sBN >= p.nK) { p.fast_b_rowfast = false; p.fast_ldb = sBN; }
+            else if (sBN == 1 && sBK >= N) { p.fast_b_rowfast = true; p.fast_ldb = sBK; }
+            else ok = false;
+            p.fast_ldw = sWM;
+        }
+        p.fast = ok;
     }
     return TRE_OK;
 }
@@ -407,7 +432,7 @@ tre_status tre_plan_get_info(tre_plan_t plan, tre_plan_info* info) {
         for (int a = 0; a < p.nk[o]; a++) info->key_labels[o][a] = char('a' + p.klab[o][a]);
     }
     info->n_join = p.n_join;
-    info->kernel_class = p.kclass;
+    info->kernel_class = (p.kclass == KC_GEMM && p.fast) ? 2 : p.kclass;
     info->batch = p.nB;
     info->m = p.nM;
     info->n = p.nN;

@@ -68,6 +68,11 @@ struct Plan {
     bool b_kfast = false;
     bool vec_a = false;    // GEMM: 8-wide vector loads legal along A's fast dim
     bool vec_b = false;
+    // bf16 fast path: A(m,k) = A[k*lda + m] if a_rowfast else A[m*lda + k];
+    // B(n,k) = B[k*ldb + n] if b_rowfast else B[n*ldb + k]; W(m,n) = W[m*ldw + n]
+    bool fast = false;
+    bool fast_a_rowfast = false, fast_b_rowfast = false;
+    int64_t fast_lda = 0, fast_ldb = 0, fast_ldw = 0;
     Dims dims[T_COUNT];
     int64_t table_off[T_COUNT] = {};
     int64_t table_total = 0;
@@ -132,6 +137,8 @@ hipError_t launch_units(const Plan& p, const Layout& L, char* ws, int64_t n_pair
                         hipStream_t s);
 hipError_t launch_contract(const Plan& p, const Layout& L, char* ws, const void* u_tiles, const void* v_tiles,
                            float* w_tiles, int64_t n_pairs, int64_t n_w, int64_t unit_bound, hipStream_t s);
+hipError_t launch_gemm_fast(const Plan& p, const Layout& L, char* ws, const void* u_tiles, const void* v_tiles,
+                            float* w_tiles, int64_t unit_bound, hipStream_t s);
 hipError_t launch_reduce(const Plan& p, const Layout& L, char* ws, float* w_tiles, int64_t split_bound,
                          hipStream_t s);
 hipError_t launch_write_outputs(const Plan& p, const Layout& L, char* ws, int32_t* w_keys, int32_t* pairs_out,

@@ -148,7 +148,7 @@ class Plan:
         self.key_arity = list(info.key_arity)
         self.tile_elems = list(info.tile_elems)
         self.n_join = info.n_join
-        self.kernel_class = "gemm" if info.kernel_class == 0 else "vec"
+        self.kernel_class = {0: "gemm", 1: "vec", 2: "gemm128"}[info.kernel_class]
         self.bmnk = (info.batch, info.m, info.n, info.k)
         self.flops_per_pair = info.flops_per_pair
         self.key_labels = [bytes(info.key_labels[o]).split(b"\0")[0].decode() for o in range(3)]

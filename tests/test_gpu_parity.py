@@ -104,6 +104,33 @@ def test_wider_plans_gpu(orc, idx, dtype):
     check(out, ref, dtype)
 
 
+FAST_PLANS = [
+    # (einsum, upper, extents, tiles): each hits one operand-layout variant of
+    # the bf16 128x128 kernel (A row- or k-contiguous, B row- or k-contiguous)
+    ("ij,jk->ki", "jk", {"i": 128, "j": 1024, "k": 1024}, {"j": 128, "k": 128}),
+    ("ki,im->km", "k", {"k": 2048, "i": 128, "m": 256}, {"k": 128}),
+    ("ik,jk->ij", "ij", {"i": 512, "j": 384, "k": 192}, {"i": 128, "j": 128}),
+    ("ki,kj->ij", "ij", {"i": 256, "j": 512, "k": 64}, {"i": 256, "j": 128}),
+]
+
+
+@pytest.mark.parametrize("idx", range(len(FAST_PLANS)))
+@pytest.mark.parametrize("pmax", [0, 3])
+def test_fast_path_gpu(orc, idx, pmax):
+    import paper_2603_08957_amd as tre
+
+    e, upper, ext, til = FAST_PLANS[idx]
+    assert tre.Plan(e, upper, ext, til, "bf16").kernel_class == "gemm128"
+    rng = np.random.default_rng(77 + idx)
+    u_lab, v_lab, _ = split_einsum(e)
+    U = workloads.random_relation(rng, u_lab, upper, ext, til, "bf16", keep=0.6, zero_frac=0.05)
+    V = workloads.random_relation(rng, v_lab, upper, ext, til, "bf16", keep=0.6, zero_frac=0.05)
+    spec = workloads.spec(e, upper, ext, til, "bf16")
+    say("fast path", idx, pmax, e, len(U["keys"]), len(V["keys"]))
+    _, out = gpu_run(spec, U, V, max_pairs_per_unit=pmax)
+    check(out, orc.run(orc_plan(orc, spec), U, V), "bf16")
+
+
 @pytest.mark.parametrize("pmax", [1, 2, 3, 7])
 def test_split_segments_gpu(orc, pmax):
     """Forcing short work units splits every key's pairs; the segmented sum of
