@@ -32,6 +32,7 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}
 METRIC = "effective tile GFLOP/s + join/reduce HBM GB/s per EinSum, 1 MI355X"
+PLAN_OPTIONS = {}  # extra tre_options for every EinSum (set from the command line)
 
 
 def log(*a):
@@ -53,7 +54,7 @@ class Stage:
 
     def __init__(self, tre, torch, spec, n_u, n_v, n_pairs, name):
         self.tre, self.torch, self.name = tre, torch, name
-        self.plan = tre.Plan.from_spec(spec, validate=False)
+        self.plan = tre.Plan.from_spec(spec, validate=False, **PLAN_OPTIONS)
         self.spec = spec
         self.ws = tre.alloc_workspace(self.plan.workspace_bytes(n_u, n_v, n_pairs))
         self.n_u, self.n_v = n_u, n_v
@@ -313,6 +314,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default 2: bf16 GNN chain, 262,144 vertices)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--u-ranges", type=int, default=0,
+                    help="tre_options.u_ranges for every EinSum (0 = library default, < 0 = off)")
+    ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
+                    help="first run one device copy of this many GiB (counter calibration under rocprofv3 --pmc)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (the path shards by output key "
@@ -325,6 +330,18 @@ def main():
 
     tre.lib()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.copy_calibration:
+        # one plain device copy of a known size: under rocprofv3 --pmc its
+        # FETCH_SIZE / WRITE_SIZE readings give the scale of those counters
+        n = int(args.copy_calibration * (1 << 30))
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy: {n} bytes read, {n} bytes written")
+        del src, dst
+    PLAN_OPTIONS["u_ranges"] = args.u_ranges
     W = make_workload(args.config, tre, torch)
     log("[bench] inputs resident; warming up")
     for _ in range(args.warmup):

@@ -72,7 +72,10 @@ typedef struct tre_plan_s *tre_plan_t;
 typedef struct {
     int32_t validate_keys;      /* nonzero: check key order, uniqueness and range on the device (default 1) */
     int32_t max_pairs_per_unit; /* work-unit length cap; 0 = chosen from the pair count */
-    int32_t reserved[6];
+    int32_t u_ranges;           /* bf16 128x128 path: cut every output key's pairs into this many ranges of
+                                   U tuple index and run range by range so concurrent workgroups share U
+                                   tiles in L2 (partials summed after); 0 = automatic, < 0 = never */
+    int32_t reserved[5];
 } tre_options;
 
 /* Static facts about a plan (host). */

@@ -72,6 +72,27 @@ int64_t blocks_per_unit(const Plan& p) {
     return (p.tile_elems[2] + 255) / 256;
 }
 
+// Number of U-index ranges for the bf16 128x128 path (0 or 1 = off).  Worth
+// it when the U tiles are reused by many keys (pairs per U tuple high) but do
+// not fit in one XCD's 4 MB L2: cutting every key's pairs into ranges of U and
+// dispatching range by range lets the workgroups resident at one time share
+// about 2 MB of U tiles, at the price of one partial tile per (key, range).
+int32_t choose_u_ranges(const Plan& p, const Layout& L, int64_t n_u, int64_t n_pairs, int64_t n_w) {
+    if (!(p.kclass == KC_GEMM && p.fast) || p.opt.u_ranges < 0 || n_u < 2 || n_w < 1) return 0;
+    int64_t R;
+    if (p.opt.u_ranges > 0) {
+        R = p.opt.u_ranges;
+    } else {
+        const int64_t u_bytes = n_u * p.tile_elems[0] * (p.dtype == TRE_BF16 ? 2 : 4);
+        const int64_t reuse = n_pairs / n_u;
+        if (u_bytes <= (int64_t(16) << 20) || reuse < 64 || n_w * blocks_per_unit(p) < kTargetWorkgroups) return 0;
+        R = (u_bytes + (int64_t(2) << 20) - 1) >> 21;
+    }
+    R = std::min<int64_t>({R, n_u, kMaxURanges});
+    while (R > 1 && R * n_w > L.part_cap) R /= 2;
+    return R > 1 ? int32_t(R) : 0;
+}
+
 int64_t choose_unit(const Plan& p, const Layout& L, int64_t n_pairs, int64_t n_w) {
     const int64_t bpu = blocks_per_unit(p);
     int64_t pu;
@@ -212,17 +233,20 @@ tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* 
     const bool deferred = timing && timing->deferred;
     Timer tm(timing != nullptr, deferred);
     tm.mark(s);
-    const int64_t p_unit = choose_unit(p, L, n_pairs, n_w);
+    const int32_t R = choose_u_ranges(p, L, jr->n_u, n_pairs, n_w);
+    const int64_t p_unit = R > 1 ? n_pairs : choose_unit(p, L, n_pairs, n_w);
     hipError_t e;
     if ((e = launch_tables(p, reinterpret_cast<int32_t*>(w + L.tables), s)) != hipSuccess) return dev_fail(e, "tables");
-    if ((e = launch_units(p, L, w, n_pairs, n_w, p_unit, s)) != hipSuccess) return dev_fail(e, "units");
+    if (R > 1) e = launch_range_units(p, L, w, n_w, jr->n_u, R, s);
+    else e = launch_units(p, L, w, n_pairs, n_w, p_unit, s);
+    if (e != hipSuccess) return dev_fail(e, "units");
     tm.mark(s);
-    const int64_t unit_bound = n_w + n_pairs / p_unit + 1;
+    const int64_t unit_bound = R > 1 ? int64_t(R) * n_w : n_w + n_pairs / p_unit + 1;
     if ((e = launch_contract(p, L, w, u_tiles, v_tiles, w_tiles, n_pairs, n_w, unit_bound, s)) != hipSuccess)
         return dev_fail(e, "contract");
     tm.mark(s);
-    if (p_unit < n_pairs) {
-        const int64_t split_bound = std::min<int64_t>(n_w, n_pairs / (p_unit + 1) + 1);
+    if (R > 1 || p_unit < n_pairs) {
+        const int64_t split_bound = R > 1 ? n_w : std::min<int64_t>(n_w, n_pairs / (p_unit + 1) + 1);
         if ((e = launch_reduce(p, L, w, w_tiles, split_bound, s)) != hipSuccess) return dev_fail(e, "reduce");
     }
     if ((e = launch_write_outputs(p, L, w, w_keys, pairs_out, n_pairs, n_w, s)) != hipSuccess)

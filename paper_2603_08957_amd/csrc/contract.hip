@@ -97,6 +97,44 @@ __global__ void k_fill_units(const int32_t* __restrict__ seg_start, int64_t n_w,
     if (nu > 1) split[soff[s]] = int32_t(s);
 }
 
+// U-range units (see launch_range_units): unit r * n_w + s covers the pairs of
+// key s with U index in [r * n_u / R, (r + 1) * n_u / R); within a key the
+// pairs are sorted by U index, so that is one contiguous run, found by binary
+// search.  Dispatch order is range-major, so workgroups running together use
+// the same slice of U.
+__global__ void k_range_units(const int32_t* __restrict__ seg_start, const int32_t* __restrict__ pu, int64_t n_w,
+                              int64_t n_u, int32_t R, Unit* __restrict__ units, int32_t* __restrict__ part_off,
+                              int32_t* __restrict__ split, WsHeader* hdr) {
+    const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (idx <= n_w) {
+        part_off[idx] = int32_t(idx * R);
+        if (idx < n_w) split[idx] = int32_t(idx);
+    }
+    if (idx == 0) {
+        hdr->n_units = int64_t(R) * n_w;
+        hdr->n_parts = int64_t(R) * n_w;
+        hdr->n_split = n_w;
+    }
+    if (idx >= int64_t(R) * n_w) return;
+    const int32_t r = int32_t(idx / n_w);
+    const int32_t s = int32_t(idx % n_w);
+    const int32_t lo = seg_start[s], hi = seg_start[s + 1];
+    auto lower = [&](int64_t key) {
+        int32_t a = lo, b = hi;
+        while (a < b) {
+            const int32_t m = (a + b) >> 1;
+            if (pu[m] < key) a = m + 1; else b = m;
+        }
+        return a;
+    };
+    Unit u;
+    u.seg = s;
+    u.p0 = lower(int64_t(r) * n_u / R);
+    u.p1 = r + 1 == R ? hi : lower(int64_t(r + 1) * n_u / R);
+    u.slot = s * R + r;
+    units[idx] = u;
+}
+
 // ------------------------------------------------------------------ GEMM
 
 struct GemmArgs {
@@ -373,6 +411,17 @@ hipError_t launch_units(const Plan& p, const Layout& L, char* ws, int64_t n_pair
     k_fill_units<<<blocks_for(n_w + 1), kThreads, 0, s>>>(seg_start, n_w, p_unit, nunits, nparts, nsplit,
                                                           reinterpret_cast<Unit*>(ws + L.unit_desc),
                                                           reinterpret_cast<int32_t*>(ws + L.split_list), hdr);
+    return hipGetLastError();
+}
+
+hipError_t launch_range_units(const Plan& p, const Layout& L, char* ws, int64_t n_w, int64_t n_u, int32_t R,
+                              hipStream_t s) {
+    (void)p;
+    const int64_t n = std::max<int64_t>(int64_t(R) * n_w, n_w + 1);
+    k_range_units<<<blocks_for(n), kThreads, 0, s>>>(
+        reinterpret_cast<const int32_t*>(ws + L.seg_start), reinterpret_cast<const int32_t*>(ws + L.pu), n_w, n_u, R,
+        reinterpret_cast<Unit*>(ws + L.unit_desc), reinterpret_cast<int32_t*>(ws + L.part_off),
+        reinterpret_cast<int32_t*>(ws + L.split_list), reinterpret_cast<WsHeader*>(ws + L.hdr));
     return hipGetLastError();
 }
 

@@ -4,13 +4,21 @@
 //
 // 256 threads = 4 waves in a 2x2 grid, each wave a 64x64 sub-block (2x2 MFMA
 // tiles, 64 fp32 accumulators per lane).  K advances in 64-deep chunks over
-// the concatenation of all pairs of the unit; each chunk of A and B is staged
-// in LDS as [row][k] (k contiguous, so every MFMA operand is one 16-byte LDS
-// read).  An operand whose unit stride runs along rows (M for A, N for B) is
-// transposed in registers on the way in: each thread loads four 16-byte row
-// segments (4 k x 8 rows) and writes eight 8-byte k-runs.  The next chunk's
-// global loads are issued before the current chunk's MFMAs, and LDS is
-// double-buffered, so one barrier per chunk suffices.  LDS: 2 x 2 x 18 KB.
+// the concatenation of all pairs of the unit.  Each chunk of A and B is
+// staged in LDS as [row][k]: 128-byte rows of eight 16-byte granules, granule
+// g of row r stored at g ^ ((r ^ (r >> 3)) & 7).  With that swizzle the MFMA
+// operand reads (one 16-byte read per lane, 16 or 8 consecutive rows per LDS
+// cycle), the plain copies and the transposing writes below are all free of
+// bank conflicts.
+//
+// An operand whose unit stride runs along rows (M for A, N for B) is
+// transposed in registers: a thread loads four 16-byte row segments (4 k x 8
+// rows) and writes eight 8-byte k-runs; half of each wavefront writes the
+// odd row of a row pair first so that both bank halves stay busy.
+//
+// Global loads run two chunks ahead in registers (two register sets used
+// alternately) and LDS is double-buffered, so one barrier per chunk suffices.
+// LDS: 2 buffers x 2 operands x 16 KB.
 #include "tre_internal.h"
 
 namespace tre {
@@ -21,12 +29,13 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kThreads = 256;
-constexpr int kB = 128;        // output block (rows and columns)
-constexpr int kKC = 64;        // K chunk
-constexpr int kPitch = kKC + 8;  // LDS row pitch in bf16 (144 bytes)
-constexpr int kBuf = kB * kPitch;  // one operand chunk in LDS (elements)
+constexpr int kB = 128;          // output block (rows and columns)
+constexpr int kKC = 64;          // K chunk
+constexpr int kRow = kKC;        // LDS row length in bf16 (128 bytes)
+constexpr int kBuf = kB * kRow;  // one operand chunk in LDS (elements)
 
 struct FastArgs {
     const uint16_t* A;
@@ -42,20 +51,29 @@ struct FastArgs {
     float* partials;
 };
 
+__device__ inline int swz(int r) { return (r ^ (r >> 3)) & 7; }
+
+// element offset in an LDS chunk of (row r, 16-byte granule g)
+__device__ inline int lds_off(int r, int g) { return r * kRow + ((g ^ swz(r)) << 3); }
+
+// Thread -> data maps.  Copy: row t/8 + 32j, granule t%8.  Transpose: row
+// block rb (8 rows) and k quad kb, chosen so that 8 consecutive lanes read
+// 128 contiguous bytes of one k row.
+__device__ inline int tr_rb(int t) { return (t & 7) | (((t >> 4) & 1) << 3); }
+__device__ inline int tr_kb(int t) { return ((t >> 3) & 1) | (((t >> 5) & 1) << 1) | ((t >> 6) << 2); }
+
 // Global -> registers for one 128 x 64 chunk of an operand whose element
 // (r, k) sits at base[r*ld + k] (ROWFAST = false) or base[k*ld + r] (true).
 template <bool ROWFAST>
 __device__ inline void load_chunk(u32x4 (&v)[4], const uint16_t* __restrict__ base, int64_t ld, int r0, int k0) {
     const int t = threadIdx.x;
     if (!ROWFAST) {
-        // 8 threads per row, 16 bytes each: rows r0 + 32*j + t/8
         const int r = t >> 3, kk = (t & 7) * 8;
 #pragma unroll
         for (int j = 0; j < 4; j++)
             v[j] = *reinterpret_cast<const u32x4*>(base + int64_t(r0 + 32 * j + r) * ld + k0 + kk);
     } else {
-        // a 4 (k) x 8 (row) block per thread: rb = t % 16 (8 rows), kb = t / 16 (4 k)
-        const int rb = t & 15, kb = t >> 4;
+        const int rb = tr_rb(t), kb = tr_kb(t);
 #pragma unroll
         for (int q = 0; q < 4; q++)
             v[q] = *reinterpret_cast<const u32x4*>(base + int64_t(k0 + kb * 4 + q) * ld + r0 + rb * 8);
@@ -70,31 +88,34 @@ template <bool ROWFAST>
 __device__ inline void store_chunk(uint16_t* __restrict__ lds, const u32x4 (&v)[4]) {
     const int t = threadIdx.x;
     if (!ROWFAST) {
-        const int r = t >> 3, kk = (t & 7) * 8;
+        const int r = t >> 3, g = t & 7;
 #pragma unroll
-        for (int j = 0; j < 4; j++) *reinterpret_cast<u32x4*>(lds + (32 * j + r) * kPitch + kk) = v[j];
+        for (int j = 0; j < 4; j++) *reinterpret_cast<u32x4*>(lds + lds_off(32 * j + r, g)) = v[j];
     } else {
-        const int rb = t & 15, kb = t >> 4;
-        const u32x4 w0 = v[0];
-        const u32x4 w1 = v[1];
-        const u32x4 w2 = v[2];
-        const u32x4 w3 = v[3];
-        // v[q] holds rows rb*8 .. rb*8+7 of k = kb*4 + q, two rows per dword
+        const int rb = tr_rb(t), kb = tr_kb(t);
+        const int g = kb >> 1, h = (kb & 1) * 4;
+        const bool odd_first = (t >> 4) & 1;
+        // v[q] holds rows rb*8 .. rb*8+7 of k = kb*4 + q, two rows per dword;
+        // piece e = the 4 k values of row rb*8 + e
 #pragma unroll
         for (int c = 0; c < 4; c++) {
-            uint2 even, odd;  // rows 2c and 2c+1, k = kb*4 .. kb*4+3
-            even.x = lo_pair(w0[c], w1[c]);
-            even.y = lo_pair(w2[c], w3[c]);
-            odd.x = hi_pair(w0[c], w1[c]);
-            odd.y = hi_pair(w2[c], w3[c]);
-            *reinterpret_cast<uint2*>(lds + (rb * 8 + 2 * c) * kPitch + kb * 4) = even;
-            *reinterpret_cast<uint2*>(lds + (rb * 8 + 2 * c + 1) * kPitch + kb * 4) = odd;
+            u32x2 even, odd;
+            even.x = lo_pair(v[0][c], v[1][c]);
+            even.y = lo_pair(v[2][c], v[3][c]);
+            odd.x = hi_pair(v[0][c], v[1][c]);
+            odd.y = hi_pair(v[2][c], v[3][c]);
+            const u32x2 first = odd_first ? odd : even;
+            const u32x2 second = odd_first ? even : odd;
+            const int r1 = rb * 8 + 2 * c + (odd_first ? 1 : 0);
+            const int r2 = rb * 8 + 2 * c + (odd_first ? 0 : 1);
+            *reinterpret_cast<u32x2*>(lds + lds_off(r1, g) + h) = first;
+            *reinterpret_cast<u32x2*>(lds + lds_off(r2, g) + h) = second;
         }
     }
 }
 
-__device__ inline bf16x8 frag(const uint16_t* lds, int row, int k) {
-    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(lds + row * kPitch + k));
+__device__ inline bf16x8 frag(const uint16_t* lds, int row, int g) {
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(lds + lds_off(row, g)));
 }
 
 template <bool AROW, bool BROW>
@@ -117,53 +138,70 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm_fast(FastArgs g) {
 #pragma unroll
             for (int r = 0; r < 16; r++) acc[i][j][r] = 0.f;
 
-    const int kc_per_pair = g.K / kKC;
-    const int total = (un.p1 - un.p0) * kc_per_pair;
-    u32x4 ra[4], rb[4];
-
-    {
-        const uint16_t* Ab = g.A + int64_t(g.pa[un.p0]) * g.a_elems;
-        const uint16_t* Bb = g.B + int64_t(g.pb[un.p0]) * g.b_elems;
-        load_chunk<AROW>(ra, Ab, g.lda, m0, 0);
-        load_chunk<BROW>(rb, Bb, g.ldb, n0, 0);
+    const int kc = g.K / kKC;
+    const int total = (un.p1 - un.p0) * kc;
+    float* out = un.slot < 0 ? g.W + int64_t(un.seg) * g.w_elems : g.partials + int64_t(un.slot) * g.w_elems;
+    if (total == 0) {
+        // an empty U range of a key: its partial tile is zero
+        for (int e = threadIdx.x; e < kB * kB; e += kThreads)
+            out[int64_t(m0 + e / kB) * g.ldw + n0 + e % kB] = 0.f;
+        return;
     }
-    store_chunk<AROW>(lds[0][0], ra);
-    store_chunk<BROW>(lds[0][1], rb);
+    // chunk c of the unit: pair p0 + c / kc, k offset (c % kc) * 64; indices
+    // past the end reload the last chunk so the load pattern stays uniform
+    auto src_a = [&](int c) {
+        c = min(c, total - 1);
+        return g.A + int64_t(g.pa[un.p0 + c / kc]) * g.a_elems;
+    };
+    auto src_b = [&](int c) {
+        c = min(c, total - 1);
+        return g.B + int64_t(g.pb[un.p0 + c / kc]) * g.b_elems;
+    };
+    auto koff = [&](int c) { return (min(c, total - 1) % kc) * kKC; };
+
+    u32x4 ra0[4], rb0[4], ra1[4], rb1[4];
+    load_chunk<AROW>(ra0, src_a(0), g.lda, m0, koff(0));
+    load_chunk<BROW>(rb0, src_b(0), g.ldb, n0, koff(0));
+    load_chunk<AROW>(ra1, src_a(1), g.lda, m0, koff(1));
+    load_chunk<BROW>(rb1, src_b(1), g.ldb, n0, koff(1));
+    store_chunk<AROW>(lds[0][0], ra0);
+    store_chunk<BROW>(lds[0][1], rb0);
     __syncthreads();
+
     const int row = lane & 31, half = lane >> 5;
-    for (int it = 0; it < total; it++) {
-        const int buf = it & 1;
-        if (it + 1 < total) {
-            const int nx = it + 1;
-            const int p = un.p0 + nx / kc_per_pair;
-            const int k0 = (nx % kc_per_pair) * kKC;
-            const uint16_t* Ab = g.A + int64_t(g.pa[p]) * g.a_elems;
-            const uint16_t* Bb = g.B + int64_t(g.pb[p]) * g.b_elems;
-            load_chunk<AROW>(ra, Ab, g.lda, m0, k0);
-            load_chunk<BROW>(rb, Bb, g.ldb, n0, k0);
-        }
-        const uint16_t* As = lds[buf][0];
-        const uint16_t* Bs = lds[buf][1];
+    auto compute = [&](const uint16_t* As, const uint16_t* Bs) {
 #pragma unroll
-        for (int ks = 0; ks < kKC; ks += 16) {
-            const int k = ks + half * 8;
-            bf16x8 a0 = frag(As, wm * 64 + row, k);
-            bf16x8 a1 = frag(As, wm * 64 + 32 + row, k);
-            bf16x8 b0 = frag(Bs, wn * 64 + row, k);
-            bf16x8 b1 = frag(Bs, wn * 64 + 32 + row, k);
+        for (int ks = 0; ks < kKC / 16; ks++) {
+            const int gr = ks * 2 + half;
+            bf16x8 a0 = frag(As, wm * 64 + row, gr);
+            bf16x8 a1 = frag(As, wm * 64 + 32 + row, gr);
+            bf16x8 b0 = frag(Bs, wn * 64 + row, gr);
+            bf16x8 b1 = frag(Bs, wn * 64 + 32 + row, gr);
             acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b0, acc[0][0], 0, 0, 0);
             acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b1, acc[0][1], 0, 0, 0);
             acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc[1][0], 0, 0, 0);
             acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, acc[1][1], 0, 0, 0);
         }
-        if (it + 1 < total) {
-            store_chunk<AROW>(lds[buf ^ 1][0], ra);
-            store_chunk<BROW>(lds[buf ^ 1][1], rb);
-        }
+    };
+
+    for (int it = 0; it < total; it += 2) {
+        // even chunk `it` in LDS buffer 0; chunk it+1 in ra1/rb1
+        load_chunk<AROW>(ra0, src_a(it + 2), g.lda, m0, koff(it + 2));
+        load_chunk<BROW>(rb0, src_b(it + 2), g.ldb, n0, koff(it + 2));
+        compute(lds[0][0], lds[0][1]);
+        store_chunk<AROW>(lds[1][0], ra1);
+        store_chunk<BROW>(lds[1][1], rb1);
+        __syncthreads();
+        if (it + 1 >= total) break;
+        // odd chunk it+1 in LDS buffer 1; chunk it+2 in ra0/rb0
+        load_chunk<AROW>(ra1, src_a(it + 3), g.lda, m0, koff(it + 3));
+        load_chunk<BROW>(rb1, src_b(it + 3), g.ldb, n0, koff(it + 3));
+        compute(lds[1][0], lds[1][1]);
+        store_chunk<AROW>(lds[0][0], ra0);
+        store_chunk<BROW>(lds[0][1], rb0);
         __syncthreads();
     }
 
-    float* out = un.slot < 0 ? g.W + int64_t(un.seg) * g.w_elems : g.partials + int64_t(un.slot) * g.w_elems;
 #pragma unroll
     for (int i = 0; i < 2; i++)
 #pragma unroll

@@ -341,8 +341,17 @@ Layout make_layout(const Plan& p, int64_t n_u, int64_t n_v, int64_t max_pairs) {
     int64_t cap = std::max<int64_t>(16, (int64_t(1) << 30) / wtile_bytes);
     cap = std::min<int64_t>(cap, 4096);
     cap = std::min<int64_t>(cap, P + 1);
+    if (p.kclass == KC_GEMM && p.fast) {
+        // U-range mode: up to kMaxURanges partial tiles per output key, at
+        // most 4 GiB of them
+        int64_t wspace = 1;
+        for (int c = 0; c < p.nk[2] && wspace < (int64_t(1) << 40); c++) wspace *= p.radix[2][c];
+        const int64_t n_w_max = std::min<int64_t>(P, wspace);
+        const int64_t range_cap = std::min<int64_t>(kMaxURanges * n_w_max, (int64_t(4) << 30) / wtile_bytes);
+        cap = std::max<int64_t>(cap, range_cap);
+    }
     L.part_cap = cap;
-    const int64_t units_max = 2 * P + 2;
+    const int64_t units_max = std::max<int64_t>(2 * P + 2, cap);
     size_t off = 0;
     auto take = [&](size_t bytes) {
         size_t o = off;

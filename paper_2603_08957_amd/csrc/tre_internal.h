@@ -12,6 +12,7 @@
 namespace tre {
 
 constexpr int kMaxDims = 8;
+constexpr int kMaxURanges = 64;
 
 // Row-major index decomposition: index x over sizes (last fastest) maps to
 // sum_i coord_i(x) * stride_i.  Used to build per-role offset tables.
@@ -135,6 +136,10 @@ hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t*
 hipError_t launch_tables(const Plan& p, int32_t* tables, hipStream_t s);
 hipError_t launch_units(const Plan& p, const Layout& L, char* ws, int64_t n_pairs, int64_t n_w, int64_t p_unit,
                         hipStream_t s);
+// U-range units: unit r * n_w + s holds the pairs of key s whose U index lies
+// in [r * n_u / R, (r + 1) * n_u / R); its partial tile is slot s * R + r.
+hipError_t launch_range_units(const Plan& p, const Layout& L, char* ws, int64_t n_w, int64_t n_u, int32_t R,
+                              hipStream_t s);
 hipError_t launch_contract(const Plan& p, const Layout& L, char* ws, const void* u_tiles, const void* v_tiles,
                            float* w_tiles, int64_t n_pairs, int64_t n_w, int64_t unit_bound, hipStream_t s);
 hipError_t launch_gemm_fast(const Plan& p, const Layout& L, char* ws, const void* u_tiles, const void* v_tiles,

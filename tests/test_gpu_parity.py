@@ -115,8 +115,10 @@ FAST_PLANS = [
 
 
 @pytest.mark.parametrize("idx", range(len(FAST_PLANS)))
-@pytest.mark.parametrize("pmax", [0, 3])
-def test_fast_path_gpu(orc, idx, pmax):
+@pytest.mark.parametrize("pmax,ur", [(0, -1), (3, -1), (0, 3), (0, 64)])
+def test_fast_path_gpu(orc, idx, pmax, ur):
+    """bf16 128x128 path, including U-range units (ur > 0: every key's pairs cut
+    into ur ranges of U index, empty ranges included, partials summed after)."""
     import paper_2603_08957_amd as tre
 
     e, upper, ext, til = FAST_PLANS[idx]
@@ -126,8 +128,8 @@ def test_fast_path_gpu(orc, idx, pmax):
     U = workloads.random_relation(rng, u_lab, upper, ext, til, "bf16", keep=0.6, zero_frac=0.05)
     V = workloads.random_relation(rng, v_lab, upper, ext, til, "bf16", keep=0.6, zero_frac=0.05)
     spec = workloads.spec(e, upper, ext, til, "bf16")
-    say("fast path", idx, pmax, e, len(U["keys"]), len(V["keys"]))
-    _, out = gpu_run(spec, U, V, max_pairs_per_unit=pmax)
+    say("fast path", idx, pmax, ur, e, len(U["keys"]), len(V["keys"]))
+    _, out = gpu_run(spec, U, V, max_pairs_per_unit=pmax, u_ranges=ur)
     check(out, orc.run(orc_plan(orc, spec), U, V), "bf16")
 
 
