@@ -1,0 +1,267 @@
+"""GPU parity at the full sizes of the five workloads, in the launch
+configuration the benchmark times.
+
+The oracle cannot evaluate every output at these sizes, so each test samples
+output keys (seeded), restricts the input relations to the tuples that feed
+them (selection on the promoted labels, Sec. 5) and compares:
+  * the pair list restricted to the sampled keys: bit-exact,
+  * the output key set: bit-exact against the oracle's key-level join where
+    that is cheap, else against closed forms,
+  * the sampled output tiles: mag-relative error within 1e-4 (fp32) / 1e-2
+    (bf16 inputs, fp32 accumulation).
+Chains are also checked end to end on sampled keys, each side computing its
+own intermediate (the GPU in fp32 then bf16 via its cast kernel, the oracle in
+fp64 rounded to fp32 then bf16)."""
+import gc
+import sys
+
+import numpy as np
+import pytest
+
+import workloads
+from _parity import TOL, value_error
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(autouse=True)
+def _free_gpu():
+    yield
+    import torch
+
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+def orc_plan(orc, s):
+    return orc.Plan(s["einsum"], s["upper"], s["extents"], s["tiles"])
+
+
+def split_einsum(e):
+    lhs, w = e.split("->")
+    u, v = lhs.split(",")
+    return u, v, w
+
+
+def w_keys_of_pairs(spec, ukeys, vkeys, pairs):
+    """Output key of every pair: W's promoted labels taken from U's key when U
+    has the label, else from V's."""
+    u, v, w = split_einsum(spec["einsum"])
+    up = spec["upper"]
+    uk = [c for c in u if c in up]
+    vk = [c for c in v if c in up]
+    cols = []
+    for c in [c for c in w if c in up]:
+        if c in uk:
+            cols.append(ukeys[pairs[:, 0], uk.index(c)])
+        else:
+            cols.append(vkeys[pairs[:, 1], vk.index(c)])
+    return np.stack(cols, axis=1) if cols else np.zeros((len(pairs), 0), np.int32)
+
+
+def rows_in(a, b):
+    """Boolean mask: rows of a that occur in b."""
+    if a.shape[1] == 0:
+        return np.ones(len(a), bool)
+    base = int(max(a.max(initial=0), b.max(initial=0))) + 1
+    enc = lambda x: (x.astype(np.int64) * (base ** np.arange(x.shape[1] - 1, -1, -1))).sum(axis=1)  # noqa: E731
+    return np.isin(enc(a), enc(b))
+
+
+def dev(a, bf16=False):
+    import torch
+
+    a = np.ascontiguousarray(a)
+    if bf16:
+        return torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
+    return torch.from_numpy(a).cuda()
+
+
+def sampled_check(orc, spec, U, V, out, S, u_tiles_host=True, pairs=None):
+    """Restrict U and V to the tuples feeding the sampled keys S, run the
+    oracle there and compare pairs and tiles of S."""
+    p = orc_plan(orc, spec)
+    mu, mv = orc.restrict(p, U["keys"], V["keys"], S)
+    iu, iv = np.nonzero(mu)[0], np.nonzero(mv)[0]
+
+    def sub(rel, idx, m):
+        r = {"keys": rel["keys"][idx]}
+        if "tiles" in rel:
+            r.update(tiles=rel["tiles"][idx], dtype=rel["dtype"])
+        else:  # scalar entries: keep those of kept tuples
+            keep = m[rel["slot"]]
+            r["coo"] = (rel["coo"][0][keep], rel["coo"][1][keep])
+        return r
+
+    su, sv = sub(U, iu, mu), sub(V, iv, mv)
+    ref_pairs, ref_keys = orc.join(p, su["keys"], sv["keys"])
+    ref_pairs = np.stack([iu[ref_pairs[:, 0]], iv[ref_pairs[:, 1]]], axis=1) if len(ref_pairs) else ref_pairs
+    in_s = rows_in(ref_keys, S)
+    assert in_s.sum() == len(S), "a sampled key has no pairs"
+    if pairs is not None:
+        wk = w_keys_of_pairs(spec, U["keys"], V["keys"], pairs)
+        got = pairs[rows_in(wk, S)]
+        rwk = w_keys_of_pairs(spec, U["keys"], V["keys"], ref_pairs)
+        assert np.array_equal(got, ref_pairs[rows_in(rwk, S)]), "pair list differs on the sampled keys"
+    uc, uv = orc._coo_of(p, 0, su)
+    vc, vv = orc._coo_of(p, 1, sv)
+    acc, mag, _ = orc.evaluate(p, uc, uv, vc, vv, S)
+    gk = out.w_keys.cpu().numpy().reshape(out.n_w, -1)
+    index = {tuple(r): i for i, r in enumerate(gk.tolist())}
+    rows = [index[tuple(r)] for r in S.tolist()]
+    got = out.w_tiles[rows].cpu().numpy()
+    worst, zeros_ok = value_error(got, acc, mag)
+    assert zeros_ok
+    assert worst <= TOL[spec["dtype"]], f"max mag-relative error {worst:.3e}"
+    return worst
+
+
+def pick(rng, keys, n):
+    idx = np.sort(rng.choice(len(keys), size=min(n, len(keys)), replace=False))
+    return np.ascontiguousarray(keys[idx])
+
+
+# ----------------------------------------------------------------- GNN
+
+def run_gnn(orc, c):
+    import paper_2603_08957_amd as tre
+    import torch
+
+    w = workloads.config(c)
+    Y = w["Y"]
+    bf = w["dtype"] == "bf16"
+    say(f"workload {c}: {w['n']} vertices, {w['n_edges']} edges, {len(Y['keys'])} Y tuples")
+    xk, xt = dev(w["X"]["keys"]), dev(w["X"]["tiles"], bf)
+    yk = dev(Y["keys"])
+    if "tiles" in Y:
+        yt = dev(Y["tiles"], bf)
+    else:
+        yt = tre.tiles_from_entries(dev(Y["slot"]), dev(Y["offset"]), dev(Y["values"], bf), len(Y["keys"]),
+                                    Y["tile_elems"])
+    p1 = tre.Plan.from_spec(w["E1"])
+    o1 = tre.einsum(p1, xk, xt, yk, yt, want_pairs=True, pair_hint=len(Y["keys"]) if w["tile_e1"] > 1 else w["n_edges"])
+    torch.cuda.synchronize()
+    del yt
+    torch.cuda.empty_cache()
+    # closed forms: one pair per Y tuple (X holds every J); keys = distinct K
+    assert o1.n_pairs == len(Y["keys"])
+    assert np.array_equal(o1.w_keys.cpu().numpy()[:, 0], np.unique(Y["keys"][:, 1]))
+    pairs = o1.pairs.cpu().numpy()
+    rng = np.random.default_rng(100 + c)
+    S1 = pick(rng, o1.w_keys.cpu().numpy(), 6)
+    say("E1 sampled", S1.ravel().tolist())
+    sampled_check(orc, w["E1"], w["X"], Y if "tiles" not in Y else {**Y, "tiles": Y["tiles"]}, o1, S1,
+                  pairs=pairs)
+    # glue and E2 on the GPU
+    tk, tt = o1.w_keys, o1.w_tiles
+    stack = w["tile_e2"] // w["tile_e1"]
+    if stack > 1:
+        tk, tt = tre.stack_rows(tk, tt, stack)
+    tb = tre.cast_f32_bf16(tt).view(tt.shape) if bf else tt
+    p2 = tre.Plan.from_spec(w["E2"])
+    o2 = tre.einsum(p2, tk, tb, dev(w["Z"]["keys"]), dev(w["Z"]["tiles"], bf), want_pairs=True)
+    assert o2.n_pairs == tk.shape[0] and o2.n_w == tk.shape[0]
+    assert np.array_equal(o2.pairs.cpu().numpy(), np.stack([np.arange(o2.n_pairs), np.zeros(o2.n_pairs)], 1))
+    # end to end on sampled E2 keys: the oracle computes the T rows they need
+    # itself (E1 restricted to those vertices), rounds fp64 -> fp32 -> bf16,
+    # stacks, and runs E2
+    S2 = pick(rng, o2.w_keys.cpu().numpy(), 4)
+    t2, t1 = w["tile_e2"], w["tile_e1"]
+    need = np.unique(np.concatenate([np.arange(k * t2 // t1, (k + 1) * t2 // t1) for k in S2[:, 0]]))
+    have = set(np.unique(Y["keys"][:, 1]).tolist())
+    need = np.array([k for k in need if k in have], dtype=np.int32).reshape(-1, 1)
+    op1 = orc_plan(orc, w["E1"])
+    mu, mv = orc.restrict(op1, w["X"]["keys"], Y["keys"], need)
+    keep = mv[Y["slot"]]
+    uc, uv, _ = orc.expand(op1, 0, w["X"]["keys"][mu], w["X"]["tiles"][mu], w["dtype"])
+    acc1, _, _ = orc.evaluate(op1, uc, uv, Y["coo"][0][keep], Y["coo"][1][keep], need)
+    t32 = acc1.astype(np.float32)
+    kk, tiles = need, t32
+    if stack > 1:
+        kk, tiles = orc.stack_rows(need[:, 0], t32, stack)
+    op2 = orc_plan(orc, w["E2"])
+    if bf:
+        Tin = {"keys": kk, "tiles": orc.f32_to_bf16(tiles), "dtype": "bf16"}
+    else:
+        Tin = {"keys": kk, "tiles": tiles, "dtype": "f32"}
+    r2 = orc.run(op2, Tin, w["Z"])
+    gk = o2.w_keys.cpu().numpy()
+    index = {int(k): i for i, k in enumerate(gk[:, 0])}
+    rk = {int(k): i for i, k in enumerate(r2.wkeys[:, 0])}
+    got = o2.w_tiles[[index[int(k)] for k in S2[:, 0]]].cpu().numpy()
+    acc = r2.acc[[rk[int(k)] for k in S2[:, 0]]]
+    mag = r2.mag[[rk[int(k)] for k in S2[:, 0]]]
+    worst, zeros_ok = value_error(got, acc, mag)
+    say(f"chain end-to-end on {len(S2)} keys: max mag-relative error {worst:.3e}")
+    assert zeros_ok and worst <= TOL[w["dtype"]]
+
+
+def test_gnn_chain_fp32_full(orc):
+    run_gnn(orc, 1)
+
+
+def test_gnn_chain_bf16_262k_full(orc):
+    run_gnn(orc, 2)
+
+
+def test_gnn_chain_bf16_1m_full(orc):
+    run_gnn(orc, 5)
+
+
+# --------------------------------------------------------- block sparse
+
+def test_block_sparse_full(orc):
+    import paper_2603_08957_amd as tre
+
+    w = workloads.config(3)
+    p = tre.Plan.from_spec(w["E"])
+    o = tre.einsum(p, dev(w["A"]["keys"]), dev(w["A"]["tiles"]), dev(w["B"]["keys"]), dev(w["B"]["tiles"]),
+                   want_pairs=True)
+    ref_pairs, ref_keys = orc.join(orc_plan(orc, w["E"]), w["A"]["keys"], w["B"]["keys"])
+    assert np.array_equal(o.pairs.cpu().numpy(), ref_pairs) and len(ref_pairs) == 819
+    assert np.array_equal(o.w_keys.cpu().numpy(), ref_keys)
+    rng = np.random.default_rng(103)
+    sampled_check(orc, w["E"], w["A"], w["B"], o, pick(rng, ref_keys, 4))
+
+
+# ------------------------------------------------------------ 3-way
+
+def test_sparse_three_way_full(orc):
+    import paper_2603_08957_amd as tre
+    import torch
+
+    w = workloads.config(4)
+    p1 = tre.Plan.from_spec(w["E1"])
+    o1 = tre.einsum(p1, dev(w["T"]["keys"]), dev(w["T"]["tiles"]), dev(w["B"]["keys"]), dev(w["B"]["tiles"]),
+                    want_pairs=True)
+    op1 = orc_plan(orc, w["E1"])
+    ref_pairs, ref_keys = orc.join(op1, w["T"]["keys"], w["B"]["keys"])
+    assert np.array_equal(o1.pairs.cpu().numpy(), ref_pairs) and len(ref_pairs) == len(w["T"]["keys"])
+    assert np.array_equal(o1.w_keys.cpu().numpy(), ref_keys)
+    rng = np.random.default_rng(104)
+    sampled_check(orc, w["E1"], w["T"], w["B"], o1, pick(rng, ref_keys, 24))
+    # E2 on the GPU's W, then end to end on sampled output rows I
+    p2 = tre.Plan.from_spec(w["E2"])
+    o2 = tre.einsum(p2, o1.w_keys, o1.w_tiles, dev(w["C"]["keys"]), dev(w["C"]["tiles"]), want_pairs=True)
+    torch.cuda.synchronize()
+    ref2_pairs, ref2_keys = orc.join(orc_plan(orc, w["E2"]), ref_keys, w["C"]["keys"])
+    assert np.array_equal(o2.pairs.cpu().numpy(), ref2_pairs)
+    assert np.array_equal(o2.w_keys.cpu().numpy(), ref2_keys)
+    S = pick(rng, ref2_keys, 3)
+    need = ref_keys[np.isin(ref_keys[:, 0], S[:, 0])]
+    mu, mv = orc.restrict(op1, w["T"]["keys"], w["B"]["keys"], need)
+    uc, uv, _ = orc.expand(op1, 0, w["T"]["keys"][mu], w["T"]["tiles"][mu], "f32")
+    vc, vv, _ = orc.expand(op1, 1, w["B"]["keys"][mv], w["B"]["tiles"][mv], "f32")
+    acc1, _, _ = orc.evaluate(op1, uc, uv, vc, vv, need)
+    r2 = orc.run(orc_plan(orc, w["E2"]), {"keys": need, "tiles": acc1, "dtype": "f64"}, w["C"])
+    gk = o2.w_keys.cpu().numpy()[:, 0]
+    rows = [int(np.nonzero(gk == k)[0][0]) for k in S[:, 0]]
+    rr = [int(np.nonzero(r2.wkeys[:, 0] == k)[0][0]) for k in S[:, 0]]
+    worst, zeros_ok = value_error(o2.w_tiles[rows].cpu().numpy(), r2.acc[rr], r2.mag[rr])
+    say(f"3-way end-to-end on {len(S)} rows: max mag-relative error {worst:.3e}")
+    assert zeros_ok and worst <= TOL["f32"]
