@@ -333,13 +333,13 @@ def main():
     if args.copy_calibration:
         # one plain device copy of a known size: under rocprofv3 --pmc its
         # FETCH_SIZE / WRITE_SIZE readings give the scale of those counters
-        n = int(args.copy_calibration * (1 << 30))
-        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        n = int(args.copy_calibration * (1 << 30)) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
-        dst.copy_(src)
+        torch.add(src, 1.0, out=dst)  # one elementwise kernel: reads 4n bytes, writes 4n bytes
         torch.cuda.synchronize()
-        log(f"[bench] calibration copy: {n} bytes read, {n} bytes written")
+        log(f"[bench] calibration copy: {4 * n} bytes read, {4 * n} bytes written")
         del src, dst
     PLAN_OPTIONS["u_ranges"] = args.u_ranges
     W = make_workload(args.config, tre, torch)
