@@ -155,14 +155,15 @@ class GnnChain:
     def step(self, timing=None):
         tre, torch = self.tre, self.torch
         tk, tt = self.e1.run(self.xk, self.xt, self.yk, self.yt, timing=timing)
-        if self.stack > 1:
-            tk, tt = tre.stack_rows(tk, tt, self.stack)
         if self.bf:
+            # cast first: the stack then moves half the bytes
             if self.t_cast is None or self.t_cast.numel() < tt.numel():
                 self.t_cast = torch.empty(tt.numel(), dtype=torch.bfloat16, device="cuda")
             tb = tre.cast_f32_bf16(tt, out=self.t_cast[:tt.numel()]).view(tt.shape)
         else:
             tb = tt
+        if self.stack > 1:
+            tk, tb = tre.stack_rows(tk, tb, self.stack)
         self.e2.n_u = int(tk.shape[0])
         return self.e2.run(tk, tb, self.zk, self.zt)
 

@@ -289,6 +289,14 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs g) {
 }
 
 // ------------------------------------------------------------------- VEC
+//
+// Vector class (scale, batched GEMV, dot): W[e] += sum_k U[eu(e) + ku(k)] *
+// V[ev(e) + kv(k)] per pair.  A thread owns EPT consecutive W elements, loaded
+// as one 16-byte vector when the plan shows the U offsets (and V's, or V is
+// the same scalar for the whole group) run contiguously in aligned groups; a
+// unit needing fewer than 256 threads shares its workgroup with other units.
+// The contracted-index tables sit in LDS; for K <= 2 the pair loop is unrolled
+// by four so four tiles are in flight per thread.
 
 struct VecArgs {
     const void* U;
@@ -298,30 +306,115 @@ struct VecArgs {
     int64_t u_elems, v_elems, w_elems;
     const int32_t *tEU, *tEV, *tKU, *tKV;
     int32_t K;
+    int32_t tpu;  // threads per unit (power of two when several units share a block)
+    int32_t upb;  // units per block
     const Unit* units;
     const WsHeader* hdr;
     float* W;
     float* partials;
 };
 
-template <typename T>
+constexpr int kVecMaxK = 2048;
+
+template <typename T, int EPT>
+__device__ inline void load_vec(const T* p, float (&x)[EPT]) {
+    if constexpr (EPT == 1) {
+        x[0] = ld_f(p);
+    } else if constexpr (sizeof(T) == 4 && EPT == 4) {
+        const float4 v = *reinterpret_cast<const float4*>(p);
+        x[0] = v.x; x[1] = v.y; x[2] = v.z; x[3] = v.w;
+    } else {
+        static_assert(sizeof(T) == 2 && EPT == 8, "unsupported vector width");
+        const uint4 v = *reinterpret_cast<const uint4*>(p);
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            x[2 * i] = __uint_as_float(w[i] << 16);
+            x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+        }
+    }
+}
+
+template <typename T, int EPT, bool VB, int PU>
 __global__ __launch_bounds__(kThreads) void k_vec(VecArgs a) {
-    const int unit_id = blockIdx.x;
-    if (unit_id >= a.hdr->n_units) return;
-    const int64_t e = int64_t(blockIdx.y) * kThreads + threadIdx.x;
-    if (e >= a.w_elems) return;
+    __shared__ int32_t sKU[kVecMaxK], sKV[kVecMaxK];
+    const bool lds_tables = a.K <= kVecMaxK;
+    if (lds_tables) {
+        for (int k = threadIdx.x; k < a.K; k += kThreads) {
+            sKU[k] = a.tKU[k];
+            sKV[k] = a.tKV[k];
+        }
+        __syncthreads();
+    }
+    const int64_t unit_id = int64_t(blockIdx.x) * a.upb + (a.upb > 1 ? threadIdx.x / a.tpu : 0);
+    const int64_t ti = a.upb > 1 ? threadIdx.x % a.tpu : int64_t(blockIdx.y) * kThreads + threadIdx.x;
+    const int64_t e0 = ti * EPT;
+    if (unit_id >= a.hdr->n_units || e0 >= a.w_elems) return;
     const Unit un = a.units[unit_id];
     const T* U = reinterpret_cast<const T*>(a.U);
     const T* V = reinterpret_cast<const T*>(a.V);
-    const int32_t eu = a.tEU[e], ev = a.tEV[e];
-    float acc = 0.f;
-    for (int p = un.p0; p < un.p1; p++) {
+    const int32_t eu = a.tEU[e0], ev = a.tEV[e0];
+    const int32_t* kU = lds_tables ? sKU : a.tKU;
+    const int32_t* kV = lds_tables ? sKV : a.tKV;
+    float acc[EPT];
+#pragma unroll
+    for (int i = 0; i < EPT; i++) acc[i] = 0.f;
+    auto pair_step = [&](const T* ub, const T* vb, int k) {
+        float x[EPT];
+        load_vec<T, EPT>(ub + kU[k], x);
+        if constexpr (VB) {
+            const float y = ld_f(vb + kV[k]);
+#pragma unroll
+            for (int i = 0; i < EPT; i++) acc[i] = fmaf(x[i], y, acc[i]);
+        } else {
+            float y[EPT];
+            load_vec<T, EPT>(vb + kV[k], y);
+#pragma unroll
+            for (int i = 0; i < EPT; i++) acc[i] = fmaf(x[i], y[i], acc[i]);
+        }
+    };
+    int p = un.p0;
+    if constexpr (PU > 1) {
+        for (; p + PU <= un.p1; p += PU) {
+            const T* ub[PU];
+            const T* vb[PU];
+#pragma unroll
+            for (int j = 0; j < PU; j++) {
+                ub[j] = U + int64_t(a.pu[p + j]) * a.u_elems + eu;
+                vb[j] = V + int64_t(a.pv[p + j]) * a.v_elems + ev;
+            }
+            for (int k = 0; k < a.K; k++)
+#pragma unroll
+                for (int j = 0; j < PU; j++) pair_step(ub[j], vb[j], k);
+        }
+    }
+    for (; p < un.p1; p++) {
         const T* ub = U + int64_t(a.pu[p]) * a.u_elems + eu;
         const T* vb = V + int64_t(a.pv[p]) * a.v_elems + ev;
-        for (int k = 0; k < a.K; k++) acc = fmaf(ld_f(ub + a.tKU[k]), ld_f(vb + a.tKV[k]), acc);
+#pragma unroll 4
+        for (int k = 0; k < a.K; k++) pair_step(ub, vb, k);
     }
     float* out = un.slot < 0 ? a.W + int64_t(un.seg) * a.w_elems : a.partials + int64_t(un.slot) * a.w_elems;
-    out[e] = acc;
+    if constexpr (EPT == 1) {
+        out[e0] = acc[0];
+    } else {
+#pragma unroll
+        for (int i = 0; i < EPT; i += 4)
+            *reinterpret_cast<float4*>(out + e0 + i) = make_float4(acc[i], acc[i + 1], acc[i + 2], acc[i + 3]);
+    }
+}
+
+template <typename T, int EPT>
+hipError_t vec_dispatch(const Plan& p, const VecArgs& a, dim3 grid, hipStream_t s) {
+    const bool pu4 = p.nK <= 2;
+    if (p.vec_vbcast) {
+        if (pu4) k_vec<T, EPT, true, 4><<<grid, kThreads, 0, s>>>(a);
+        else k_vec<T, EPT, true, 1><<<grid, kThreads, 0, s>>>(a);
+    } else {
+        if (pu4) k_vec<T, EPT, false, 4><<<grid, kThreads, 0, s>>>(a);
+        else k_vec<T, EPT, false, 1><<<grid, kThreads, 0, s>>>(a);
+    }
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------- reduce
@@ -489,12 +582,26 @@ hipError_t launch_contract(const Plan& p, const Layout& L, char* ws, const void*
     a.hdr = hdr;
     a.W = w_tiles;
     a.partials = parts;
-    const int64_t gy = (p.tile_elems[2] + kThreads - 1) / kThreads;
-    if (gy > 65535) return hipErrorInvalidConfiguration;
-    dim3 grid{unsigned(unit_bound), unsigned(gy), 1u};
-    if (p.dtype == TRE_BF16) k_vec<uint16_t><<<grid, kThreads, 0, s>>>(a);
-    else k_vec<float><<<grid, kThreads, 0, s>>>(a);
-    return hipGetLastError();
+    const int ept = p.vec_ept;
+    const int64_t threads = (p.tile_elems[2] + ept - 1) / ept;
+    dim3 grid;
+    if (threads <= kThreads / 2) {
+        int tpu = 1;
+        while (tpu < threads) tpu <<= 1;
+        a.tpu = tpu;
+        a.upb = kThreads / tpu;
+        grid = dim3{unsigned((unit_bound + a.upb - 1) / a.upb), 1u, 1u};
+    } else {
+        a.tpu = int32_t(threads);
+        a.upb = 1;
+        const int64_t gy = (threads + kThreads - 1) / kThreads;
+        if (gy > 65535) return hipErrorInvalidConfiguration;
+        grid = dim3{unsigned(unit_bound), unsigned(gy), 1u};
+    }
+    if (p.dtype == TRE_BF16) {
+        return ept == 8 ? vec_dispatch<uint16_t, 8>(p, a, grid, s) : vec_dispatch<uint16_t, 1>(p, a, grid, s);
+    }
+    return ept == 4 ? vec_dispatch<float, 4>(p, a, grid, s) : vec_dispatch<float, 1>(p, a, grid, s);
 }
 
 hipError_t launch_reduce(const Plan& p, const Layout& L, char* ws, float* w_tiles, int64_t split_bound,

@@ -69,20 +69,23 @@ __global__ void k_stack_count(const int32_t* __restrict__ excl, int64_t n, int64
     *n_out = excl[n];
 }
 
-template <typename T>
+// Copy every input row to its place in the stacked output, in copy units of
+// type C (16 bytes when rows allow it); row i lands in output tuple
+// excl[i] - (row i is not the first of its group) at row keys[i] % group.
+template <typename C>
 __global__ void k_stack_rows(const int32_t* __restrict__ keys, int64_t n, const int32_t* __restrict__ excl,
-                             const T* __restrict__ tiles, int64_t row_elems, int32_t group, int32_t* __restrict__ out_keys,
-                             T* __restrict__ out_tiles) {
-    // one workgroup per input row
-    const int64_t i = blockIdx.x;
-    if (i >= n) return;
-    const int32_t k = keys[i];
-    // output index of this key: heads carry excl + 1 semantics via the scan
-    const int32_t oi = excl[i] + ((i == 0 || keys[i] / group != keys[i - 1] / group) ? 0 : -1);
-    if (threadIdx.x == 0) out_keys[oi] = k / group;
-    const T* src = tiles + i * row_elems;
-    T* dst = out_tiles + (int64_t(oi) * group + (k % group)) * row_elems;
-    for (int64_t e = threadIdx.x; e < row_elems; e += kThreads) dst[e] = src[e];
+                             const C* __restrict__ src, int64_t row_units, int32_t group, int32_t* __restrict__ out_keys,
+                             C* __restrict__ dst) {
+    const int64_t total = n * row_units;
+    const int64_t stride = int64_t(gridDim.x) * kThreads;
+    for (int64_t c = int64_t(blockIdx.x) * kThreads + threadIdx.x; c < total; c += stride) {
+        const int64_t i = c / row_units, e = c - i * row_units;
+        const int32_t k = keys[i];
+        const bool head = i == 0 || keys[i - 1] / group != k / group;
+        const int32_t oi = excl[i] - (head ? 0 : 1);
+        if (e == 0 && head) out_keys[oi] = k / group;
+        dst[(int64_t(oi) * group + (k % group)) * row_units + e] = src[c];
+    }
 }
 
 }  // namespace
@@ -134,14 +137,22 @@ hipError_t launch_stack(const int32_t* keys, int64_t n, const void* tiles, int64
     e = launch_fill_zero(out_tiles, size_t(n_out) * size_t(group) * size_t(row_elems) * size_t(elem_bytes), s);
     if (e != hipSuccess) return e;
     if (n <= 0) return hipSuccess;
-    if (elem_bytes == 2)
-        k_stack_rows<uint16_t><<<unsigned(n), kThreads, 0, s>>>(keys, n, flags,
-                                                                 reinterpret_cast<const uint16_t*>(tiles), row_elems,
-                                                                 group, out_keys, reinterpret_cast<uint16_t*>(out_tiles));
+    const int64_t row_bytes = row_elems * elem_bytes;
+    const bool wide = row_bytes % 16 == 0 && reinterpret_cast<uintptr_t>(tiles) % 16 == 0 &&
+                      reinterpret_cast<uintptr_t>(out_tiles) % 16 == 0;
+    const int64_t units = wide ? row_bytes / 16 : row_elems;
+    const unsigned grid = unsigned(std::min<int64_t>((n * units + kThreads - 1) / kThreads, 65536));
+    if (wide)
+        k_stack_rows<uint4><<<grid, kThreads, 0, s>>>(keys, n, flags, reinterpret_cast<const uint4*>(tiles), units,
+                                                       group, out_keys, reinterpret_cast<uint4*>(out_tiles));
+    else if (elem_bytes == 2)
+        k_stack_rows<uint16_t><<<grid, kThreads, 0, s>>>(keys, n, flags, reinterpret_cast<const uint16_t*>(tiles),
+                                                          units, group, out_keys,
+                                                          reinterpret_cast<uint16_t*>(out_tiles));
     else
-        k_stack_rows<uint32_t><<<unsigned(n), kThreads, 0, s>>>(keys, n, flags,
-                                                                 reinterpret_cast<const uint32_t*>(tiles), row_elems,
-                                                                 group, out_keys, reinterpret_cast<uint32_t*>(out_tiles));
+        k_stack_rows<uint32_t><<<grid, kThreads, 0, s>>>(keys, n, flags, reinterpret_cast<const uint32_t*>(tiles),
+                                                          units, group, out_keys,
+                                                          reinterpret_cast<uint32_t*>(out_tiles));
     return hipGetLastError();
 }
 

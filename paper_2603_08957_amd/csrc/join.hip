@@ -7,13 +7,14 @@
 //            tuple binary-search the run of equal join keys in V, then an
 //            exclusive scan of the run lengths gives each U tuple its first
 //            pair index and the total pair count.
-//   stage 1  load-balanced expansion: pair p finds its U tuple by a binary
-//            search over the scanned counts, so hub tuples with long runs
-//            are spread over many threads; pairs come out in (u, v) order.
-//            Each pair gets its packed W key; a stable radix sort by W key
-//            (skipped when W's keys are a prefix of U's) gives the canonical
-//            (w_key, u, v) order; run-length encoding gives the output keys
-//            and segment offsets.
+//   stage 1  load-balanced expansion: a thread owns 8 consecutive pair
+//            indices, finds the U tuple of the first by binary search over
+//            the scanned counts and walks forward, so hub tuples with long
+//            runs are spread over many threads; pairs come out in (u, v)
+//            order.  Each pair gets its packed W key; a stable radix sort by
+//            W key (skipped when W's keys are a prefix of U's) carrying the
+//            packed (u, v) gives the canonical (w_key, u, v) order; run-length
+//            encoding gives the output keys and segment offsets.
 #include "tre_internal.h"
 
 namespace tre {
@@ -21,6 +22,7 @@ namespace tre {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kPairsPerThread = 8;
 
 struct KeyDesc {
     int32_t n;
@@ -115,35 +117,47 @@ __device__ inline uint64_t pack_w(const int32_t* urow, const int32_t* vrow, cons
     return k;
 }
 
+// Pairs [t*8, t*8 + 8) of the expansion.  Writes either the final (u, v)
+// arrays (no group sort) or packed (u << 32 | v) payloads for the sort.
 __global__ void k_expand(const int64_t* __restrict__ off, const int64_t* __restrict__ lo, int64_t n_u, int64_t n_pairs,
                          const uint32_t* __restrict__ vperm, const int32_t* __restrict__ ukeys, int ru,
                          const int32_t* __restrict__ vkeys, int rv, WDesc wd, int32_t* __restrict__ pu,
-                         int32_t* __restrict__ pv, uint64_t* __restrict__ wk, uint32_t* __restrict__ pidx) {
-    const int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (p >= n_pairs) return;
-    // largest u with off[u] <= p
+                         int32_t* __restrict__ pv, uint64_t* __restrict__ wk, uint64_t* __restrict__ uv) {
+    const int64_t p0 = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) * kPairsPerThread;
+    if (p0 >= n_pairs) return;
+    // largest u with off[u] <= p0
     int64_t a = 0, b = n_u - 1;
     while (a < b) {
         int64_t m = (a + b + 1) >> 1;
-        if (off[m] <= p) a = m; else b = m - 1;
+        if (off[m] <= p0) a = m; else b = m - 1;
     }
-    const int64_t u = a;
-    const int64_t vs = lo[u] + (p - off[u]);
-    const int64_t v = vperm ? int64_t(vperm[vs]) : vs;
-    pu[p] = int32_t(u);
-    pv[p] = int32_t(v);
-    wk[p] = pack_w(ukeys + u * ru, vkeys + v * rv, wd);
-    if (pidx) pidx[p] = uint32_t(p);
+    int64_t u = a;
+    int64_t next = off[u + 1];
+    const int64_t p1 = min<int64_t>(p0 + kPairsPerThread, n_pairs);
+    for (int64_t p = p0; p < p1; p++) {
+        while (p >= next) {
+            u++;
+            next = off[u + 1];
+        }
+        const int64_t vs = lo[u] + (p - off[u]);
+        const int64_t v = vperm ? int64_t(vperm[vs]) : vs;
+        wk[p] = pack_w(ukeys + u * ru, vkeys + v * rv, wd);
+        if (uv) {
+            uv[p] = (uint64_t(uint32_t(u)) << 32) | uint64_t(uint32_t(v));
+        } else {
+            pu[p] = int32_t(u);
+            pv[p] = int32_t(v);
+        }
+    }
 }
 
-__global__ void k_gather_pairs(const uint32_t* __restrict__ idx, const int32_t* __restrict__ pu_in,
-                               const int32_t* __restrict__ pv_in, int32_t* __restrict__ pu, int32_t* __restrict__ pv,
-                               int64_t n) {
+__global__ void k_split_pairs(const uint64_t* __restrict__ uv, int32_t* __restrict__ pu, int32_t* __restrict__ pv,
+                              int64_t n) {
     const int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (p >= n) return;
-    const uint32_t s = idx[p];
-    pu[p] = pu_in[s];
-    pv[p] = pv_in[s];
+    const uint64_t x = uv[p];
+    pu[p] = int32_t(x >> 32);
+    pv[p] = int32_t(x & 0xffffffffu);
 }
 
 __global__ void k_heads(const uint64_t* __restrict__ wk, int64_t n, int32_t* __restrict__ flags) {
@@ -192,44 +206,40 @@ KeyDesc desc_v(const Plan& p) {
 
 hipError_t launch_validate(const int32_t* keys, int64_t n, int r, const int32_t* radix, int32_t* err_flag,
                            hipStream_t s) {
-    if (n <= 0) return hipSuccess;
+    if (n <= 0 || r == 0) return hipSuccess;  // r == 0: at most one tuple, checked on the host
     Radix rad{};
     for (int a = 0; a < r; a++) rad.r[a] = radix[a];
-    if (r == 0) return hipSuccess;  // at most one tuple; checked on the host
     k_validate<<<blocks_for(n), kThreads, 0, s>>>(keys, n, r, rad, err_flag);
     return hipGetLastError();
 }
 
 hipError_t launch_join(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
                        hipStream_t s, int stage) {
+    if (stage != 0) return hipErrorInvalidValue;
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
     uint64_t* vjk = reinterpret_cast<uint64_t*>(ws + L.vjk);
     uint32_t* vperm = p.v_needs_sort ? reinterpret_cast<uint32_t*>(ws + L.vperm) : nullptr;
     int64_t* cnt = reinterpret_cast<int64_t*>(ws + L.ucnt);
     int64_t* lo = reinterpret_cast<int64_t*>(ws + L.ulo);
     int64_t* tmp = reinterpret_cast<int64_t*>(ws + L.scan_tmp);
-    int64_t* hist = reinterpret_cast<int64_t*>(ws + L.hist);
+    int32_t* hist = reinterpret_cast<int32_t*>(ws + L.hist);
     const int64_t n_u = L.n_u, n_v = L.n_v;
     hipError_t e = hipSuccess;
-    if (stage == 0) {
-        if (p.n_join > 0 && n_v > 0) {
-            k_pack_join<<<blocks_for(n_v), kThreads, 0, s>>>(v_keys, n_v, p.nk[1], desc_v(p), vjk, vperm);
-            if ((e = hipGetLastError()) != hipSuccess) return e;
-            if (p.v_needs_sort) {
-                e = radix_sort_u64(vjk, vperm, reinterpret_cast<uint64_t*>(ws + L.vjk_alt),
-                                   reinterpret_cast<uint32_t*>(ws + L.vperm_alt), n_v, p.join_total_bits, hist, tmp,
-                                   s);
-                if (e != hipSuccess) return e;
-            }
-        }
-        k_count<<<blocks_for(n_u + 1), kThreads, 0, s>>>(u_keys, n_u, p.nk[0], desc_u(p), vjk, n_v, p.n_join > 0,
-                                                          cnt, lo);
+    if (p.n_join > 0 && n_v > 0) {
+        k_pack_join<<<blocks_for(n_v), kThreads, 0, s>>>(v_keys, n_v, p.nk[1], desc_v(p), vjk, vperm);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        if ((e = scan_exclusive_i64(cnt, cnt, n_u + 1, tmp, s)) != hipSuccess) return e;
-        k_store_count<<<1, 1, 0, s>>>(cnt, n_u, hdr);
-        return hipGetLastError();
+        if (p.v_needs_sort) {
+            e = radix_sort_u64(vjk, vperm, reinterpret_cast<uint64_t*>(ws + L.vjk_alt),
+                               reinterpret_cast<uint32_t*>(ws + L.vperm_alt), n_v, p.join_total_bits, hist,
+                               reinterpret_cast<int32_t*>(tmp), s);
+            if (e != hipSuccess) return e;
+        }
     }
-    return hipErrorInvalidValue;
+    k_count<<<blocks_for(n_u + 1), kThreads, 0, s>>>(u_keys, n_u, p.nk[0], desc_u(p), vjk, n_v, p.n_join > 0, cnt, lo);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = scan_exclusive_i64(cnt, cnt, n_u + 1, tmp, s)) != hipSuccess) return e;
+    k_store_count<<<1, 1, 0, s>>>(cnt, n_u, hdr);
+    return hipGetLastError();
 }
 
 hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
@@ -242,8 +252,8 @@ hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t*
     int32_t* pu = reinterpret_cast<int32_t*>(ws + L.pu);
     int32_t* pv = reinterpret_cast<int32_t*>(ws + L.pv);
     uint64_t* wk = reinterpret_cast<uint64_t*>(ws + L.wk);
-    int64_t* tmp = reinterpret_cast<int64_t*>(ws + L.scan_tmp);
-    int64_t* hist = reinterpret_cast<int64_t*>(ws + L.hist);
+    int32_t* tmp = reinterpret_cast<int32_t*>(ws + L.scan_tmp);
+    int32_t* hist = reinterpret_cast<int32_t*>(ws + L.hist);
     int32_t* flags = reinterpret_cast<int32_t*>(ws + L.flags);
     int32_t* seg_start = reinterpret_cast<int32_t*>(ws + L.seg_start);
     uint64_t* seg_key = reinterpret_cast<uint64_t*>(ws + L.seg_key);
@@ -256,24 +266,23 @@ hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t*
     }
     hipError_t e;
     const bool sort = p.group_needs_sort && n_pairs > 1 && p.w_total_bits > 0;
-    int32_t* epu = sort ? reinterpret_cast<int32_t*>(ws + L.pu_alt) : pu;
-    int32_t* epv = sort ? reinterpret_cast<int32_t*>(ws + L.pv_alt) : pv;
-    uint32_t* pidx = sort ? reinterpret_cast<uint32_t*>(ws + L.pidx) : nullptr;
+    uint64_t* uv = sort ? reinterpret_cast<uint64_t*>(ws + L.pidx) : nullptr;
     if (n_pairs > 0) {
-        k_expand<<<blocks_for(n_pairs), kThreads, 0, s>>>(off, lo, L.n_u, n_pairs, vperm, u_keys, p.nk[0], v_keys,
-                                                           p.nk[1], wd, epu, epv, wk, pidx);
+        const int64_t threads = (n_pairs + kPairsPerThread - 1) / kPairsPerThread;
+        k_expand<<<blocks_for(threads), kThreads, 0, s>>>(off, lo, L.n_u, n_pairs, vperm, u_keys, p.nk[0], v_keys,
+                                                          p.nk[1], wd, pu, pv, wk, uv);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (sort) {
-        e = radix_sort_u64(wk, pidx, reinterpret_cast<uint64_t*>(ws + L.wk_alt),
-                           reinterpret_cast<uint32_t*>(ws + L.pidx_alt), n_pairs, p.w_total_bits, hist, tmp, s);
+        e = radix_sort_u64_pairs(wk, uv, reinterpret_cast<uint64_t*>(ws + L.wk_alt),
+                                 reinterpret_cast<uint64_t*>(ws + L.pidx_alt), n_pairs, p.w_total_bits, hist, tmp, s);
         if (e != hipSuccess) return e;
-        k_gather_pairs<<<blocks_for(n_pairs), kThreads, 0, s>>>(pidx, epu, epv, pu, pv, n_pairs);
+        k_split_pairs<<<blocks_for(n_pairs), kThreads, 0, s>>>(uv, pu, pv, n_pairs);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     k_heads<<<blocks_for(n_pairs + 1), kThreads, 0, s>>>(wk, n_pairs, flags);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = scan_exclusive_i32(flags, flags, n_pairs + 1, reinterpret_cast<int32_t*>(tmp), s)) != hipSuccess) return e;
+    if ((e = scan_exclusive_i32(flags, flags, n_pairs + 1, tmp, s)) != hipSuccess) return e;
     k_compact<<<blocks_for(n_pairs + 1), kThreads, 0, s>>>(wk, n_pairs, flags, seg_start, seg_key, hdr);
     return hipGetLastError();
 }

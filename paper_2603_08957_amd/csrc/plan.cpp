@@ -286,6 +286,38 @@ static tre_status classify(Plan& p) {
     }
     p.table_total = off;
 
+    // Vector class: EPT consecutive W elements per thread when U's offsets run
+    // contiguously in aligned groups of EPT and V's either do too or stay
+    // constant over each group (V broadcast); otherwise one element.
+    if (p.kclass == KC_VEC) {
+        auto tEU = host_table(p.dims[T_EU]), tEV = host_table(p.dims[T_EV]);
+        auto tKU = host_table(p.dims[T_KU]), tKV = host_table(p.dims[T_KV]);
+        const int ept = p.dtype == TRE_BF16 ? 8 : 4;
+        auto grouped = [&](const std::vector<int32_t>& t, bool& contiguous, bool& constant) {
+            contiguous = constant = t.size() % ept == 0;
+            for (size_t g = 0; g < t.size() && (contiguous || constant); g += ept) {
+                if (t[g] % ept) contiguous = false;
+                for (int j = 1; j < ept; j++) {
+                    if (t[g + j] != t[g] + j) contiguous = false;
+                    if (t[g + j] != t[g]) constant = false;
+                }
+            }
+        };
+        auto aligned = [&](const std::vector<int32_t>& t) {
+            for (int32_t x : t)
+                if (x % ept) return false;
+            return true;
+        };
+        bool u_cont, u_const, v_cont, v_const;
+        grouped(tEU, u_cont, u_const);
+        grouped(tEV, v_cont, v_const);
+        const bool u_ok = u_cont && p.tile_elems[0] % ept == 0 && aligned(tKU);
+        const bool v_vec = v_cont && p.tile_elems[1] % ept == 0 && aligned(tKV);
+        if (u_ok && p.tile_elems[2] % ept == 0 && (v_vec || v_const)) {
+            p.vec_ept = ept;
+            p.vec_vbcast = !v_vec;
+        }
+    }
     // GEMM staging: which dim of A / B has unit stride, and whether 8-wide
     // aligned vector loads along it are legal
     if (p.kclass == KC_GEMM) {
@@ -370,13 +402,13 @@ Layout make_layout(const Plan& p, int64_t n_u, int64_t n_v, int64_t max_pairs) {
     L.scan_tmp = take(sizeof(int64_t) * scan_tmp_elems(scan_n));
     L.pu = take(sizeof(int32_t) * size_t(P));
     L.pv = take(sizeof(int32_t) * size_t(P));
-    L.pu_alt = take(p.group_needs_sort ? sizeof(int32_t) * size_t(P) : 0);
-    L.pv_alt = take(p.group_needs_sort ? sizeof(int32_t) * size_t(P) : 0);
+    L.pu_alt = take(0);
+    L.pv_alt = take(0);
     L.wk = take(sizeof(uint64_t) * size_t(P));
     L.wk_alt = take(p.group_needs_sort ? sizeof(uint64_t) * size_t(P) : 0);
-    L.pidx = take(p.group_needs_sort ? sizeof(uint32_t) * size_t(P) : 0);
-    L.pidx_alt = take(p.group_needs_sort ? sizeof(uint32_t) * size_t(P) : 0);
-    L.hist = take(sizeof(int64_t) * size_t(radix_hist_elems(std::max<int64_t>(sort_n, 1))));
+    L.pidx = take(p.group_needs_sort ? sizeof(uint64_t) * size_t(P) : 0);      // packed (u, v) per pair
+    L.pidx_alt = take(p.group_needs_sort ? sizeof(uint64_t) * size_t(P) : 0);
+    L.hist = take(sizeof(int32_t) * size_t(radix_hist_elems(std::max<int64_t>(sort_n, 1))));
     L.flags = take(sizeof(int32_t) * size_t(P + 1));
     L.seg_start = take(sizeof(int32_t) * size_t(P + 1));
     L.seg_key = take(sizeof(uint64_t) * size_t(P));

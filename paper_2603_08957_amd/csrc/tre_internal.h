@@ -71,6 +71,10 @@ struct Plan {
     bool vec_b = false;
     // bf16 fast path: A(m,k) = A[k*lda + m] if a_rowfast else A[m*lda + k];
     // B(n,k) = B[k*ldb + n] if b_rowfast else B[n*ldb + k]; W(m,n) = W[m*ldw + n]
+    // vector class: W elements per thread (1, 4 for fp32, 8 for bf16) and
+    // whether V's element is the same for a whole group of them
+    int vec_ept = 1;
+    bool vec_vbcast = false;
     bool fast = false;
     bool fast_a_rowfast = false, fast_b_rowfast = false;
     int64_t fast_lda = 0, fast_ldb = 0, fast_ldw = 0;
@@ -122,7 +126,9 @@ hipError_t scan_exclusive_i32(const int32_t* in, int32_t* out, int64_t n, int32_
 // low `bits` bits; result lands in keys/vals (alt buffers are scratch).
 int64_t radix_hist_elems(int64_t n);
 hipError_t radix_sort_u64(uint64_t* keys, uint32_t* vals, uint64_t* keys_alt, uint32_t* vals_alt, int64_t n,
-                          int bits, int64_t* hist, int64_t* scan_tmp, hipStream_t s);
+                          int bits, int32_t* hist, int32_t* scan_tmp, hipStream_t s);
+hipError_t radix_sort_u64_pairs(uint64_t* keys, uint64_t* vals, uint64_t* keys_alt, uint64_t* vals_alt, int64_t n,
+                                int bits, int32_t* hist, int32_t* scan_tmp, hipStream_t s);
 
 // join.hip
 hipError_t launch_validate(const int32_t* keys, int64_t n, int r, const int32_t* radix, int32_t* err_flag,
