@@ -25,6 +25,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
 
@@ -426,6 +427,17 @@ __global__ __launch_bounds__(kThreads) void k_reduce(const int32_t* __restrict__
     if (x >= hdr->n_split) return;
     const int32_t s = split[x];
     const int32_t first = poff[s], cnt = poff[s + 1] - poff[s];
+    if (w_elems % 4 == 0) {
+        // 16-byte lanes; partials are read once, so they bypass L2 retention
+        const int64_t q = w_elems / 4;
+        for (int64_t e = int64_t(blockIdx.y) * kThreads + threadIdx.x; e < q; e += int64_t(gridDim.y) * kThreads) {
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+            for (int j = 0; j < cnt; j++)
+                acc += __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(parts) + int64_t(first + j) * q + e);
+            reinterpret_cast<f32x4*>(W)[int64_t(s) * q + e] = acc;
+        }
+        return;
+    }
     for (int64_t e = int64_t(blockIdx.y) * kThreads + threadIdx.x; e < w_elems; e += int64_t(gridDim.y) * kThreads) {
         float acc = 0.f;
         for (int j = 0; j < cnt; j++) acc += parts[int64_t(first + j) * w_elems + e];
@@ -529,7 +541,8 @@ hipError_t launch_contract(const Plan& p, const Layout& L, char* ws, const void*
     const Unit* units = reinterpret_cast<const Unit*>(ws + L.unit_desc);
     const WsHeader* hdr = reinterpret_cast<const WsHeader*>(ws + L.hdr);
     float* parts = reinterpret_cast<float*>(ws + L.partials);
-    if (p.kclass == KC_GEMM && p.fast) return launch_gemm_fast(p, L, ws, u_tiles, v_tiles, w_tiles, unit_bound, s);
+    if (p.kclass == KC_GEMM && p.fast)
+        return launch_gemm_fast(p, L, ws, u_tiles, v_tiles, w_tiles, n_pairs, unit_bound, s);
     if (p.kclass == KC_GEMM) {
         GemmArgs g{};
         g.A = p.swap ? v_tiles : u_tiles;
@@ -608,7 +621,8 @@ hipError_t launch_reduce(const Plan& p, const Layout& L, char* ws, float* w_tile
                          hipStream_t s) {
     if (split_bound <= 0) return hipSuccess;
     const int64_t we = p.tile_elems[2];
-    const unsigned gy = unsigned(std::min<int64_t>((we + kThreads - 1) / kThreads, 65535));
+    const int64_t lanes = we % 4 == 0 ? we / 4 : we;
+    const unsigned gy = unsigned(std::min<int64_t>((lanes + kThreads - 1) / kThreads, 65535));
     k_reduce<<<dim3(unsigned(split_bound), gy), kThreads, 0, s>>>(
         reinterpret_cast<const int32_t*>(ws + L.split_list), reinterpret_cast<const WsHeader*>(ws + L.hdr),
         reinterpret_cast<const int32_t*>(ws + L.part_off), reinterpret_cast<const float*>(ws + L.partials), w_tiles,

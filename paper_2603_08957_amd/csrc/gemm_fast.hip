@@ -64,20 +64,34 @@ __device__ inline int tr_kb(int t) { return ((t >> 3) & 1) | (((t >> 5) & 1) << 
 
 // Global -> registers for one 128 x 64 chunk of an operand whose element
 // (r, k) sits at base[r*ld + k] (ROWFAST = false) or base[k*ld + r] (true).
+// NT: the operand is streamed (each tile read by one workgroup once), so its
+// loads carry the non-temporal hint and do not push reused tiles out of L2.
+template <bool NT>
+__device__ inline u32x4 gload(const uint16_t* p) {
+    if constexpr (NT) return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    else return *reinterpret_cast<const u32x4*>(p);
+}
+
+// The per-lane part of the addresses is fixed for the whole unit: lane offset
+// `lo` and the step between a thread's four loads (32 rows when k is
+// contiguous, one k row when rows are); the per-chunk part is uniform.
 template <bool ROWFAST>
-__device__ inline void load_chunk(u32x4 (&v)[4], const uint16_t* __restrict__ base, int64_t ld, int r0, int k0) {
+__device__ inline int32_t lane_offset(int32_t ld) {
     const int t = threadIdx.x;
-    if (!ROWFAST) {
-        const int r = t >> 3, kk = (t & 7) * 8;
+    if (!ROWFAST) return (t >> 3) * ld + (t & 7) * 8;
+    return tr_kb(t) * 4 * ld + tr_rb(t) * 8;
+}
+
+template <bool ROWFAST>
+__device__ inline int64_t chunk_offset(int64_t ld, int r0, int k0) {
+    return ROWFAST ? int64_t(k0) * ld + r0 : int64_t(r0) * ld + k0;
+}
+
+template <bool ROWFAST, bool NT>
+__device__ inline void load_chunk(u32x4 (&v)[4], const uint16_t* __restrict__ base, int32_t lo, int32_t step) {
+    const uint16_t* p = base + lo;
 #pragma unroll
-        for (int j = 0; j < 4; j++)
-            v[j] = *reinterpret_cast<const u32x4*>(base + int64_t(r0 + 32 * j + r) * ld + k0 + kk);
-    } else {
-        const int rb = tr_rb(t), kb = tr_kb(t);
-#pragma unroll
-        for (int q = 0; q < 4; q++)
-            v[q] = *reinterpret_cast<const u32x4*>(base + int64_t(k0 + kb * 4 + q) * ld + r0 + rb * 8);
-    }
+    for (int j = 0; j < 4; j++) v[j] = gload<NT>(p + j * step);
 }
 
 __device__ inline uint32_t lo_pair(uint32_t x, uint32_t y) { return (x & 0xffffu) | (y << 16); }
@@ -118,7 +132,7 @@ __device__ inline bf16x8 frag(const uint16_t* lds, int row, int g) {
     return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(lds + lds_off(row, g)));
 }
 
-template <bool AROW, bool BROW>
+template <bool AROW, bool BROW, bool ANT, bool BNT>
 __global__ __launch_bounds__(kThreads, 2) void k_gemm_fast(FastArgs g) {
     const int unit_id = blockIdx.x;
     if (unit_id >= g.hdr->n_units) return;
@@ -149,21 +163,23 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm_fast(FastArgs g) {
     }
     // chunk c of the unit: pair p0 + c / kc, k offset (c % kc) * 64; indices
     // past the end reload the last chunk so the load pattern stays uniform
+    const int32_t lo_a = lane_offset<AROW>(int32_t(g.lda)), lo_b = lane_offset<BROW>(int32_t(g.ldb));
+    const int32_t st_a = AROW ? int32_t(g.lda) : 32 * int32_t(g.lda);
+    const int32_t st_b = BROW ? int32_t(g.ldb) : 32 * int32_t(g.ldb);
     auto src_a = [&](int c) {
         c = min(c, total - 1);
-        return g.A + int64_t(g.pa[un.p0 + c / kc]) * g.a_elems;
+        return g.A + int64_t(g.pa[un.p0 + c / kc]) * g.a_elems + chunk_offset<AROW>(g.lda, m0, (c % kc) * kKC);
     };
     auto src_b = [&](int c) {
         c = min(c, total - 1);
-        return g.B + int64_t(g.pb[un.p0 + c / kc]) * g.b_elems;
+        return g.B + int64_t(g.pb[un.p0 + c / kc]) * g.b_elems + chunk_offset<BROW>(g.ldb, n0, (c % kc) * kKC);
     };
-    auto koff = [&](int c) { return (min(c, total - 1) % kc) * kKC; };
 
     u32x4 ra0[4], rb0[4], ra1[4], rb1[4];
-    load_chunk<AROW>(ra0, src_a(0), g.lda, m0, koff(0));
-    load_chunk<BROW>(rb0, src_b(0), g.ldb, n0, koff(0));
-    load_chunk<AROW>(ra1, src_a(1), g.lda, m0, koff(1));
-    load_chunk<BROW>(rb1, src_b(1), g.ldb, n0, koff(1));
+    load_chunk<AROW, ANT>(ra0, src_a(0), lo_a, st_a);
+    load_chunk<BROW, BNT>(rb0, src_b(0), lo_b, st_b);
+    load_chunk<AROW, ANT>(ra1, src_a(1), lo_a, st_a);
+    load_chunk<BROW, BNT>(rb1, src_b(1), lo_b, st_b);
     store_chunk<AROW>(lds[0][0], ra0);
     store_chunk<BROW>(lds[0][1], rb0);
     __syncthreads();
@@ -186,16 +202,16 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm_fast(FastArgs g) {
 
     for (int it = 0; it < total; it += 2) {
         // even chunk `it` in LDS buffer 0; chunk it+1 in ra1/rb1
-        load_chunk<AROW>(ra0, src_a(it + 2), g.lda, m0, koff(it + 2));
-        load_chunk<BROW>(rb0, src_b(it + 2), g.ldb, n0, koff(it + 2));
+        load_chunk<AROW, ANT>(ra0, src_a(it + 2), lo_a, st_a);
+        load_chunk<BROW, BNT>(rb0, src_b(it + 2), lo_b, st_b);
         compute(lds[0][0], lds[0][1]);
         store_chunk<AROW>(lds[1][0], ra1);
         store_chunk<BROW>(lds[1][1], rb1);
         __syncthreads();
         if (it + 1 >= total) break;
         // odd chunk it+1 in LDS buffer 1; chunk it+2 in ra0/rb0
-        load_chunk<AROW>(ra1, src_a(it + 3), g.lda, m0, koff(it + 3));
-        load_chunk<BROW>(rb1, src_b(it + 3), g.ldb, n0, koff(it + 3));
+        load_chunk<AROW, ANT>(ra1, src_a(it + 3), lo_a, st_a);
+        load_chunk<BROW, BNT>(rb1, src_b(it + 3), lo_b, st_b);
         compute(lds[1][0], lds[1][1]);
         store_chunk<AROW>(lds[0][0], ra0);
         store_chunk<BROW>(lds[0][1], rb0);
@@ -218,7 +234,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm_fast(FastArgs g) {
 }  // namespace
 
 hipError_t launch_gemm_fast(const Plan& p, const Layout& L, char* ws, const void* u_tiles, const void* v_tiles,
-                            float* w_tiles, int64_t unit_bound, hipStream_t s) {
+                            float* w_tiles, int64_t n_pairs, int64_t unit_bound, hipStream_t s) {
     FastArgs g{};
     const int32_t* pu = reinterpret_cast<const int32_t*>(ws + L.pu);
     const int32_t* pv = reinterpret_cast<const int32_t*>(ws + L.pv);
@@ -242,10 +258,21 @@ hipError_t launch_gemm_fast(const Plan& p, const Layout& L, char* ws, const void
     const int64_t gy = (M / kB) * (N / kB);
     if (gy > 65535) return hipErrorInvalidConfiguration;
     dim3 grid{unsigned(unit_bound), unsigned(gy), 1u};
-    if (p.fast_a_rowfast && p.fast_b_rowfast) k_gemm_fast<true, true><<<grid, kThreads, 0, s>>>(g);
-    else if (p.fast_a_rowfast) k_gemm_fast<true, false><<<grid, kThreads, 0, s>>>(g);
-    else if (p.fast_b_rowfast) k_gemm_fast<false, true><<<grid, kThreads, 0, s>>>(g);
-    else k_gemm_fast<false, false><<<grid, kThreads, 0, s>>>(g);
+    // an operand whose tiles are each used by about one pair is streamed
+    const int64_t n_a = p.swap ? L.n_v : L.n_u, n_b = p.swap ? L.n_u : L.n_v;
+    const bool ant = 2 * n_a >= n_pairs, bnt = 2 * n_b >= n_pairs;
+    const int sel = (p.fast_a_rowfast ? 8 : 0) | (p.fast_b_rowfast ? 4 : 0) | (ant ? 2 : 0) | (bnt ? 1 : 0);
+#define TRE_FAST_CASE(X)                                                                                   \
+    case X:                                                                                                \
+        k_gemm_fast<bool(X & 8), bool(X & 4), bool(X & 2), bool(X & 1)><<<grid, kThreads, 0, s>>>(g); \
+        break;
+    switch (sel) {
+        TRE_FAST_CASE(0) TRE_FAST_CASE(1) TRE_FAST_CASE(2) TRE_FAST_CASE(3)
+        TRE_FAST_CASE(4) TRE_FAST_CASE(5) TRE_FAST_CASE(6) TRE_FAST_CASE(7)
+        TRE_FAST_CASE(8) TRE_FAST_CASE(9) TRE_FAST_CASE(10) TRE_FAST_CASE(11)
+        TRE_FAST_CASE(12) TRE_FAST_CASE(13) TRE_FAST_CASE(14) TRE_FAST_CASE(15)
+    }
+#undef TRE_FAST_CASE
     return hipGetLastError();
 }
 

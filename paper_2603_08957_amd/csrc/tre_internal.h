@@ -149,7 +149,7 @@ hipError_t launch_range_units(const Plan& p, const Layout& L, char* ws, int64_t 
 hipError_t launch_contract(const Plan& p, const Layout& L, char* ws, const void* u_tiles, const void* v_tiles,
                            float* w_tiles, int64_t n_pairs, int64_t n_w, int64_t unit_bound, hipStream_t s);
 hipError_t launch_gemm_fast(const Plan& p, const Layout& L, char* ws, const void* u_tiles, const void* v_tiles,
-                            float* w_tiles, int64_t unit_bound, hipStream_t s);
+                            float* w_tiles, int64_t n_pairs, int64_t unit_bound, hipStream_t s);
 hipError_t launch_reduce(const Plan& p, const Layout& L, char* ws, float* w_tiles, int64_t split_bound,
                          hipStream_t s);
 hipError_t launch_write_outputs(const Plan& p, const Layout& L, char* ws, int32_t* w_keys, int32_t* pairs_out,
