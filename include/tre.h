@@ -33,7 +33,8 @@
  *   - Tiles: [n x tile_elems] contiguous, each tile row-major over ALL the
  *     operand's labels in string order, with extent t_l for a promoted label
  *     and the full extent for a demoted one.  Inputs are fp32 or bf16 (raw
- *     bits, uint16); W tiles are always fp32.
+ *     bits, uint16); W tiles are always fp32.  Tile arrays start on a
+ *     16-byte boundary (TRE_E_ARG otherwise).
  *   - Output order: W keys sorted lexicographically; the pair list in order of
  *     (W key, u index, v index), u/v being positions in the caller's arrays.
  *   - Errors are returned as tre_status; the library never aborts and never

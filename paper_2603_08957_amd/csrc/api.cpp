@@ -75,8 +75,9 @@ int64_t blocks_per_unit(const Plan& p) {
 // Number of U-index ranges for the bf16 128x128 path (0 or 1 = off).  Worth
 // it when the U tiles are reused by many keys (pairs per U tuple high) but do
 // not fit in one XCD's 4 MB L2: cutting every key's pairs into ranges of U and
-// dispatching range by range lets the workgroups resident at one time share
-// a few MB of U tiles, at the price of one partial tile per (key, range).
+// dispatching range by range lets the workgroups resident on an XCD share
+// about 2 MB of U tiles, which stay in its L2 while the V tiles stream past,
+// at the price of one partial tile per (key, range).
 int32_t choose_u_ranges(const Plan& p, const Layout& L, int64_t n_u, int64_t n_pairs, int64_t n_w) {
     if (!(p.kclass == KC_GEMM && p.fast) || p.opt.u_ranges < 0 || n_u < 2 || n_w < 1) return 0;
     int64_t R;
@@ -86,9 +87,9 @@ int32_t choose_u_ranges(const Plan& p, const Layout& L, int64_t n_u, int64_t n_p
         const int64_t u_bytes = n_u * p.tile_elems[0] * (p.dtype == TRE_BF16 ? 2 : 4);
         const int64_t reuse = n_pairs / n_u;
         if (u_bytes <= (int64_t(16) << 20) || reuse < 64 || n_w * blocks_per_unit(p) < kTargetWorkgroups) return 0;
-        // ~8 MB of U per range: measured best on the 262,144-vertex chain
-        // (R = 4..8 within 1%; R = 32 loses to the extra partial traffic)
-        R = (u_bytes + (int64_t(8) << 20) - 1) >> 23;
+        // ~2 MB of U per range: measured best on the 262,144-vertex chain
+        // (4 MB ranges thrash the L2, 1 MB ranges pay for twice the partials)
+        R = (u_bytes + (int64_t(2) << 20) - 1) >> 21;
     }
     R = std::min<int64_t>({R, n_u, kMaxURanges});
     while (R > 1 && R * n_w > L.part_cap) R /= 2;
@@ -227,6 +228,11 @@ tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* 
     if (n_pairs == 0) return TRE_OK;
     if (!u_tiles || !v_tiles || !w_tiles || (p.nk[2] > 0 && !w_keys)) {
         set_error("tre_contract: null tile or key buffer");
+        return TRE_E_ARG;
+    }
+    if ((reinterpret_cast<uintptr_t>(u_tiles) | reinterpret_cast<uintptr_t>(v_tiles) |
+         reinterpret_cast<uintptr_t>(w_tiles)) & 15) {
+        set_error("tre_contract: tile arrays must be 16-byte aligned");
         return TRE_E_ARG;
     }
     char* w = reinterpret_cast<char*>(jr->internal[2]);

@@ -3,23 +3,36 @@
 // unit of A_p (128 x K) * B_p (K x 128) on v_mfma_f32_32x32x16_bf16.
 //
 // 256 threads = 4 waves in a 2x2 grid, each wave a 64x64 sub-block (2x2 MFMA
-// tiles, 64 fp32 accumulators per lane).  K advances in 64-deep chunks over
-// the concatenation of all pairs of the unit.  Each chunk of A and B is
-// staged in LDS as [row][k]: 128-byte rows of eight 16-byte granules, granule
-// g of row r stored at g ^ ((r ^ (r >> 3)) & 7).  With that swizzle the MFMA
-// operand reads (one 16-byte read per lane, 16 or 8 consecutive rows per LDS
-// cycle), the plain copies and the transposing writes below are all free of
-// bank conflicts.
+// tiles, 64 fp32 accumulators per lane).  K advances over the concatenation
+// of all pairs of the unit.
 //
-// An operand whose unit stride runs along rows (M for A, N for B) is
-// transposed in registers: a thread loads four 16-byte row segments (4 k x 8
-// rows) and writes eight 8-byte k-runs; half of each wavefront writes the
-// odd row of a row pair first so that both bank halves stay busy.
+// Global memory is copied straight into LDS by global_load_lds_dwordx4 (16
+// bytes per lane, lane l to LDS base + 16 l), so no registers hold staged
+// data and no VALU work transposes it.  Each operand has its own ring of LDS
+// stages, shaped by the direction of its unit stride so that every copy
+// instruction moves eight whole 128-byte lines:
+//   KFAST (k contiguous): a stage is a K = 64 chunk, [row][64 k] with
+//     128-byte rows, 16 KB, three stages; the 16-byte granule G of row r sits
+//     in slot G ^ ((r ^ (r >> 3)) & 7).  Read with ds_read_b128.
+//   RFAST (rows contiguous): a stage is a K = 32 chunk, [k][128 rows] with
+//     256-byte k-rows, 8 KB, four stages; granule g of k-row k sits in slot
+//     g ^ (4 (k & 3)).  Read with ds_read_b64_tr_b16, which hands each lane
+//     4 consecutive k of one row.
+// The swizzles are applied by choosing, per lane, which global granule goes
+// to the lane's fixed LDS slot; all reads are free of bank conflicts and
+// every global access covers whole contiguous row segments.  With one ring
+// of each kind a workgroup takes 80 KB of LDS (two per CU).
 //
-// Global loads run two chunks ahead in registers (two register sets used
-// alternately) and LDS is double-buffered, so one barrier per chunk suffices.
-// LDS: 2 buffers x 2 operands x 16 KB.
+// The main loop advances in ticks of K = 32: an RFAST ring is refilled every
+// tick three ticks ahead, a KFAST ring every second tick four ticks ahead,
+// so only the stage being computed on is ever read while the others fill.
+// The copies are issued from inline assembly (the compiler's own wait
+// insertion would drain every outstanding copy before the first LDS read);
+// the kernel waits for them explicitly (vmcnt) before each barrier and
+// drains them before it leaves the loop.
 #include "tre_internal.h"
+
+#include <type_traits>
 
 namespace tre {
 
@@ -28,14 +41,9 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kThreads = 256;
-constexpr int kB = 128;          // output block (rows and columns)
-constexpr int kKC = 64;          // K chunk
-constexpr int kRow = kKC;        // LDS row length in bf16 (128 bytes)
-constexpr int kBuf = kB * kRow;  // one operand chunk in LDS (elements)
+constexpr int kB = 128;  // output block (rows and columns)
 
 struct FastArgs {
     const uint16_t* A;
@@ -51,96 +59,163 @@ struct FastArgs {
     float* partials;
 };
 
-__device__ inline int swz(int r) { return (r ^ (r >> 3)) & 7; }
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+typedef __attribute__((address_space(3))) char lds_char;
+typedef __attribute__((address_space(4))) int32_t const_i32;
 
-// element offset in an LDS chunk of (row r, 16-byte granule g)
-__device__ inline int lds_off(int r, int g) { return r * kRow + ((g ^ swz(r)) << 3); }
+// s_waitcnt immediate: vmcnt(n) with expcnt and lgkmcnt left alone
+constexpr int vmcnt_only(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
-// Thread -> data maps.  Copy: row t/8 + 32j, granule t%8.  Transpose: row
-// block rb (8 rows) and k quad kb, chosen so that 8 consecutive lanes read
-// 128 contiguous bytes of one k row.
-__device__ inline int tr_rb(int t) { return (t & 7) | (((t >> 4) & 1) << 3); }
-__device__ inline int tr_kb(int t) { return ((t >> 3) & 1) | (((t >> 5) & 1) << 1) | ((t >> 6) << 2); }
+// ring geometry of one operand
+template <bool RF>
+struct Ring {
+    static constexpr int kK = RF ? 32 : 64;            // K per stage
+    static constexpr int kStageBytes = 128 * kK * 2;   // 8 or 16 KB
+    static constexpr int kStages = RF ? 4 : 3;
+    static constexpr int kBytes = kStages * kStageBytes;
+    static constexpr int kPerWave = kStageBytes / 1024 / 4;  // copy instructions per wave per refill
+};
 
-// Global -> registers for one 128 x 64 chunk of an operand whose element
-// (r, k) sits at base[r*ld + k] (ROWFAST = false) or base[k*ld + r] (true).
-// NT: the operand is streamed (each tile read by one workgroup once), so its
-// loads carry the non-temporal hint and do not push reused tiles out of L2.
+__device__ inline uint64_t uniform64(uint64_t x) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(x));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(uint32_t(x >> 32));
+    return (uint64_t(hi) << 32) | lo;
+}
+
 template <bool NT>
-__device__ inline u32x4 gload(const uint16_t* p) {
-    if constexpr (NT) return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
-    else return *reinterpret_cast<const u32x4*>(p);
+__device__ inline void dma16(uint32_t lds_addr, const void* base, uint32_t voff) {
+    const uint32_t m = __builtin_amdgcn_readfirstlane(lds_addr);
+    const uint64_t b = uniform64(reinterpret_cast<uint64_t>(base));
+    if constexpr (NT)
+        asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2 nt" ::"s"(m), "v"(voff), "s"(b) : "m0");
+    else
+        asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(m), "v"(voff), "s"(b) : "m0");
 }
 
-// The per-lane part of the addresses is fixed for the whole unit: lane offset
-// `lo` and the step between a thread's four loads (32 rows when k is
-// contiguous, one k row when rows are); the per-chunk part is uniform.
-template <bool ROWFAST>
-__device__ inline int32_t lane_offset(int32_t ld) {
-    const int t = threadIdx.x;
-    if (!ROWFAST) return (t >> 3) * ld + (t & 7) * 8;
-    return tr_kb(t) * 4 * ld + tr_rb(t) * 8;
+// Byte offset, from the stage's chunk origin, of the 16 bytes this lane
+// copies for copy instruction q of an operand with leading dimension ld
+// (elements); the copy lands at stage offset q * 1024 + 16 * lane.
+template <bool RF>
+__device__ inline uint32_t dma_src(int lane, int q, int64_t ld) {
+    if (!RF) {  // 8 rows x 128 B; row & 7 == lane >> 3, (row >> 3) & 7 == q & 7
+        const int row = 8 * q + (lane >> 3);
+        return uint32_t(row * ld * 2 + (((lane & 7) ^ (lane >> 3) ^ (q & 7)) << 4));
+    }
+    const int krow = 4 * q + (lane >> 4);  // 4 k-rows x 256 B; krow & 3 == lane >> 4
+    return uint32_t(krow * ld * 2 + (((lane & 15) ^ ((lane >> 4) << 2)) << 4));
 }
 
-template <bool ROWFAST>
-__device__ inline int64_t chunk_offset(int64_t ld, int r0, int k0) {
-    return ROWFAST ? int64_t(k0) * ld + r0 : int64_t(r0) * ld + k0;
+// Element offset inside a tile of the chunk origin (rows r0.., k0..).
+template <bool RF>
+__device__ inline int64_t dma_origin(int64_t ld, int r0, int k0) {
+    return RF ? int64_t(k0) * ld + r0 : int64_t(r0) * ld + k0;
 }
 
-template <bool ROWFAST, bool NT>
-__device__ inline void load_chunk(u32x4 (&v)[4], const uint16_t* __restrict__ base, int32_t lo, int32_t step) {
-    const uint16_t* p = base + lo;
+// Stage offsets of this lane's MFMA operand reads for the 32-row tile at row
+// rb (a multiple of 32), one per k-step of 16 inside a stage.  KFAST: the
+// 16-byte read of k-step s.  RFAST: the first of the two 8-byte transposing
+// reads (k 0..3 and 4..7 of the lane's eight; the second is 4 k-rows on).
+template <bool RF>
+__device__ inline void frag_offsets(int lane, int rb, uint32_t (&off)[4]) {
+    if (!RF) {
+        const int r = rb + (lane & 31);
+        const int x = (r ^ (r >> 3)) & 7, h = lane >> 5;
 #pragma unroll
-    for (int j = 0; j < 4; j++) v[j] = gload<NT>(p + j * step);
-}
-
-__device__ inline uint32_t lo_pair(uint32_t x, uint32_t y) { return (x & 0xffffu) | (y << 16); }
-__device__ inline uint32_t hi_pair(uint32_t x, uint32_t y) { return (x >> 16) | (y & 0xffff0000u); }
-
-// Registers -> LDS [row][k] for the chunk loaded by load_chunk.
-template <bool ROWFAST>
-__device__ inline void store_chunk(uint16_t* __restrict__ lds, const u32x4 (&v)[4]) {
-    const int t = threadIdx.x;
-    if (!ROWFAST) {
-        const int r = t >> 3, g = t & 7;
-#pragma unroll
-        for (int j = 0; j < 4; j++) *reinterpret_cast<u32x4*>(lds + lds_off(32 * j + r, g)) = v[j];
+        for (int s = 0; s < 4; s++) off[s] = uint32_t(r * 128 + (((2 * s + h) ^ x) << 4));
     } else {
-        const int rb = tr_rb(t), kb = tr_kb(t);
-        const int g = kb >> 1, h = (kb & 1) * 4;
-        const bool odd_first = (t >> 4) & 1;
-        // v[q] holds rows rb*8 .. rb*8+7 of k = kb*4 + q, two rows per dword;
-        // piece e = the 4 k values of row rb*8 + e
-#pragma unroll
-        for (int c = 0; c < 4; c++) {
-            u32x2 even, odd;
-            even.x = lo_pair(v[0][c], v[1][c]);
-            even.y = lo_pair(v[2][c], v[3][c]);
-            odd.x = hi_pair(v[0][c], v[1][c]);
-            odd.y = hi_pair(v[2][c], v[3][c]);
-            const u32x2 first = odd_first ? odd : even;
-            const u32x2 second = odd_first ? even : odd;
-            const int r1 = rb * 8 + 2 * c + (odd_first ? 1 : 0);
-            const int r2 = rb * 8 + 2 * c + (odd_first ? 0 : 1);
-            *reinterpret_cast<u32x2*>(lds + lds_off(r1, g) + h) = first;
-            *reinterpret_cast<u32x2*>(lds + lds_off(r2, g) + h) = second;
-        }
+        const int i = lane & 15, G = lane >> 4;
+        const int krow = 8 * (G >> 1) + (i >> 2);
+        const int gran = ((rb >> 3) ^ ((i >> 2) << 2)) + 2 * (G & 1) + ((i & 3) >> 1);
+        off[0] = uint32_t(krow * 256 + gran * 16 + 8 * (i & 1));
+        off[1] = off[0] + 16 * 256;
+        off[2] = off[3] = 0;
     }
 }
 
-__device__ inline bf16x8 frag(const uint16_t* lds, int row, int g) {
-    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(lds + lds_off(row, g)));
+template <bool RF>
+__device__ inline bf16x8 frag_read(const char* stage, uint32_t off) {
+    if (!RF) return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(stage + off));
+    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(stage + off));
+    const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(stage + off + 4 * 256));
+    const v4i16 both[2] = {lo, hi};
+    return __builtin_bit_cast(bf16x8, both);
 }
 
+// Copy cursor of one operand: walks the unit's pairs stage by stage; past
+// the end it copies the last stage again (never read).
+template <bool RF, bool NT>
+struct Cursor {
+    const uint16_t* base;  // operand tiles, offset to the block's chunk origin
+    const const_i32* idx;  // tile index of each pair of the unit
+    int64_t elems, step;   // tile elements; element step from one stage to the next
+    int np, per_pair;      // pairs; stages per pair
+    int ip = 0, ik = 0, stage = 0;
+    int32_t next = 0;
+    const uint16_t* cur = nullptr;
+    uint32_t src[Ring<RF>::kPerWave];
+
+    __device__ void init(const uint16_t* b, const const_i32* ix, int64_t e, int64_t ld, int K, int npairs, int lane,
+                         int w) {
+        base = b;
+        idx = ix;
+        elems = e;
+        step = RF ? int64_t(Ring<RF>::kK) * ld : Ring<RF>::kK;
+        np = npairs;
+        per_pair = K / Ring<RF>::kK;
+        cur = base + int64_t(idx[0]) * elems;
+        next = idx[min(1, np - 1)];
+#pragma unroll
+        for (int j = 0; j < Ring<RF>::kPerWave; j++) src[j] = dma_src<RF>(lane, Ring<RF>::kPerWave * w + j, ld);
+    }
+    __device__ void issue(uint32_t ring_lds, int w) {
+        const uint32_t l0 = ring_lds + stage * Ring<RF>::kStageBytes + Ring<RF>::kPerWave * w * 1024;
+#pragma unroll
+        for (int j = 0; j < Ring<RF>::kPerWave; j++) dma16<NT>(l0 + j * 1024, cur, src[j]);
+        stage = stage == Ring<RF>::kStages - 1 ? 0 : stage + 1;
+        if (++ik < per_pair) {
+            cur += step;
+            return;
+        }
+        ik = 0;
+        if (ip + 1 < np) {
+            ip++;
+            cur = base + int64_t(next) * elems;
+            next = idx[min(ip + 1, np - 1)];
+        } else {
+            cur -= (per_pair - 1) * step;
+        }
+    }
+};
+
+template <bool AROW, bool BROW>
+struct DmaShape {
+    using RA = Ring<AROW>;
+    using RB = Ring<BROW>;
+    static constexpr int kLds = RA::kBytes + RB::kBytes;
+    static constexpr int kOcc = 163840 / kLds;
+    // Copies still allowed in flight when a tick's data must have landed (see
+    // the schedule above): with one RFAST ring, the two previous ticks'
+    // copies; with two KFAST rings, the previous refill (even ticks) or the
+    // two previous refills (odd ticks, which need no new data).
+    static constexpr int kWait0 = (AROW || BROW) ? 8 : 8;
+    static constexpr int kWait1 = (AROW || BROW) ? 8 : 16;
+};
+
 template <bool AROW, bool BROW, bool ANT, bool BNT>
-__global__ __launch_bounds__(kThreads, 2) void k_gemm_fast(FastArgs g) {
+__global__ __launch_bounds__(kThreads, (DmaShape<AROW, BROW>::kOcc)) void k_gemm_dma(FastArgs g) {
+    using SH = DmaShape<AROW, BROW>;
+    using RA = Ring<AROW>;
+    using RB = Ring<BROW>;
     const int unit_id = blockIdx.x;
     if (unit_id >= g.hdr->n_units) return;
     const Unit un = g.units[unit_id];
     const int mblk = blockIdx.y / g.nblocks, nblk = blockIdx.y % g.nblocks;
     const int m0 = mblk * kB, n0 = nblk * kB;
 
-    __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][kBuf];  // [buffer][A/B]
+    __shared__ __attribute__((aligned(1024))) char lds[SH::kLds];
+    const uint32_t lds_a = uint32_t(reinterpret_cast<uintptr_t>((lds_char*)(lds)));
+    const uint32_t lds_b = lds_a + RA::kBytes;
 
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int wm = w >> 1, wn = w & 1;
@@ -152,71 +227,82 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm_fast(FastArgs g) {
 #pragma unroll
             for (int r = 0; r < 16; r++) acc[i][j][r] = 0.f;
 
-    const int kc = g.K / kKC;
-    const int total = (un.p1 - un.p0) * kc;
+    const int np = un.p1 - un.p0;
+    const int ticks = np * (g.K / 32);
     float* out = un.slot < 0 ? g.W + int64_t(un.seg) * g.w_elems : g.partials + int64_t(un.slot) * g.w_elems;
-    if (total == 0) {
-        // an empty U range of a key: its partial tile is zero
+    if (ticks == 0) {
         for (int e = threadIdx.x; e < kB * kB; e += kThreads)
             out[int64_t(m0 + e / kB) * g.ldw + n0 + e % kB] = 0.f;
         return;
     }
-    // chunk c of the unit: pair p0 + c / kc, k offset (c % kc) * 64; indices
-    // past the end reload the last chunk so the load pattern stays uniform
-    const int32_t lo_a = lane_offset<AROW>(int32_t(g.lda)), lo_b = lane_offset<BROW>(int32_t(g.ldb));
-    const int32_t st_a = AROW ? int32_t(g.lda) : 32 * int32_t(g.lda);
-    const int32_t st_b = BROW ? int32_t(g.ldb) : 32 * int32_t(g.ldb);
-    auto src_a = [&](int c) {
-        c = min(c, total - 1);
-        return g.A + int64_t(g.pa[un.p0 + c / kc]) * g.a_elems + chunk_offset<AROW>(g.lda, m0, (c % kc) * kKC);
-    };
-    auto src_b = [&](int c) {
-        c = min(c, total - 1);
-        return g.B + int64_t(g.pb[un.p0 + c / kc]) * g.b_elems + chunk_offset<BROW>(g.ldb, n0, (c % kc) * kKC);
-    };
+    // the pair list is read-only here; reading it through the constant
+    // address space keeps the (uniform) index loads on the scalar unit
+    Cursor<AROW, ANT> ca;
+    Cursor<BROW, BNT> cb;
+    ca.init(g.A + dma_origin<AROW>(g.lda, m0, 0), (const const_i32*)(g.pa + un.p0), g.a_elems, g.lda, g.K, np,
+            lane, w);
+    cb.init(g.B + dma_origin<BROW>(g.ldb, n0, 0), (const const_i32*)(g.pb + un.p0), g.b_elems, g.ldb, g.K, np,
+            lane, w);
 
-    u32x4 ra0[4], rb0[4], ra1[4], rb1[4];
-    load_chunk<AROW, ANT>(ra0, src_a(0), lo_a, st_a);
-    load_chunk<BROW, BNT>(rb0, src_b(0), lo_b, st_b);
-    load_chunk<AROW, ANT>(ra1, src_a(1), lo_a, st_a);
-    load_chunk<BROW, BNT>(rb1, src_b(1), lo_b, st_b);
-    store_chunk<AROW>(lds[0][0], ra0);
-    store_chunk<BROW>(lds[0][1], rb0);
-    __syncthreads();
-
-    const int row = lane & 31, half = lane >> 5;
-    auto compute = [&](const uint16_t* As, const uint16_t* Bs) {
+    uint32_t oa[2][4], ob[2][4];
 #pragma unroll
-        for (int ks = 0; ks < kKC / 16; ks++) {
-            const int gr = ks * 2 + half;
-            bf16x8 a0 = frag(As, wm * 64 + row, gr);
-            bf16x8 a1 = frag(As, wm * 64 + 32 + row, gr);
-            bf16x8 b0 = frag(Bs, wn * 64 + row, gr);
-            bf16x8 b1 = frag(Bs, wn * 64 + 32 + row, gr);
-            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b0, acc[0][0], 0, 0, 0);
-            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b1, acc[0][1], 0, 0, 0);
-            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc[1][0], 0, 0, 0);
-            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, acc[1][1], 0, 0, 0);
+    for (int t = 0; t < 2; t++) {
+        frag_offsets<AROW>(lane, wm * 64 + t * 32, oa[t]);
+        frag_offsets<BROW>(lane, wn * 64 + t * 32, ob[t]);
+    }
+
+    // refills of tick tau: KFAST rings on even ticks (stage tau / 2 + 2),
+    // then RFAST rings (stage tau + 3); the prologue runs ticks -4 .. -1
+    auto refill = [&](int tau_parity, bool rf_too) {
+        if (tau_parity == 0) {
+            if (!AROW) ca.issue(lds_a, w);
+            if (!BROW) cb.issue(lds_b, w);
+        }
+        if (rf_too) {
+            if (AROW) ca.issue(lds_a, w);
+            if (BROW) cb.issue(lds_b, w);
         }
     };
+    refill(0, false);  // tick -4
+    refill(1, true);   // tick -3
+    refill(0, true);   // tick -2
+    refill(1, true);   // tick -1
 
-    for (int it = 0; it < total; it += 2) {
-        // even chunk `it` in LDS buffer 0; chunk it+1 in ra1/rb1
-        load_chunk<AROW, ANT>(ra0, src_a(it + 2), lo_a, st_a);
-        load_chunk<BROW, BNT>(rb0, src_b(it + 2), lo_b, st_b);
-        compute(lds[0][0], lds[0][1]);
-        store_chunk<AROW>(lds[1][0], ra1);
-        store_chunk<BROW>(lds[1][1], rb1);
+    int sa = 0, sb = 0;  // ring stage being read
+    auto tick = [&](auto parity) {
+        constexpr int p = decltype(parity)::value;
+        __builtin_amdgcn_s_waitcnt(vmcnt_only(p == 0 ? SH::kWait0 : SH::kWait1));
         __syncthreads();
-        if (it + 1 >= total) break;
-        // odd chunk it+1 in LDS buffer 1; chunk it+2 in ra0/rb0
-        load_chunk<AROW, ANT>(ra1, src_a(it + 3), lo_a, st_a);
-        load_chunk<BROW, BNT>(rb1, src_b(it + 3), lo_b, st_b);
-        compute(lds[1][0], lds[1][1]);
-        store_chunk<AROW>(lds[0][0], ra0);
-        store_chunk<BROW>(lds[0][1], rb0);
-        __syncthreads();
+        refill(p, true);
+        const char* As = lds + sa * RA::kStageBytes;
+        const char* Bs = lds + RA::kBytes + sb * RB::kStageBytes;
+        bf16x8 a[2][2], b[2][2];
+#pragma unroll
+        for (int s = 0; s < 2; s++)
+#pragma unroll
+            for (int t = 0; t < 2; t++) {
+                a[s][t] = frag_read<AROW>(As, oa[t][AROW ? s : 2 * p + s]);
+                b[s][t] = frag_read<BROW>(Bs, ob[t][BROW ? s : 2 * p + s]);
+            }
+#pragma unroll
+        for (int s = 0; s < 2; s++) {
+            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s][0], b[s][0], acc[0][0], 0, 0, 0);
+            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s][0], b[s][1], acc[0][1], 0, 0, 0);
+            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s][1], b[s][0], acc[1][0], 0, 0, 0);
+            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s][1], b[s][1], acc[1][1], 0, 0, 0);
+        }
+        // advance the read stages: RFAST every tick, KFAST after odd ticks
+        if (AROW || p == 1) sa = sa == RA::kStages - 1 ? 0 : sa + 1;
+        if (BROW || p == 1) sb = sb == RB::kStages - 1 ? 0 : sb + 1;
+    };
+    // K is a multiple of 64, so a unit has an even number of ticks
+    for (int t = 0; t < ticks; t += 2) {
+        tick(std::integral_constant<int, 0>{});
+        tick(std::integral_constant<int, 1>{});
     }
+    // the copies issued past the end must land before the workgroup leaves
+    // (its LDS may be handed to another workgroup)
+    __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
 
 #pragma unroll
     for (int i = 0; i < 2; i++)
@@ -264,7 +350,7 @@ hipError_t launch_gemm_fast(const Plan& p, const Layout& L, char* ws, const void
     const int sel = (p.fast_a_rowfast ? 8 : 0) | (p.fast_b_rowfast ? 4 : 0) | (ant ? 2 : 0) | (bnt ? 1 : 0);
 #define TRE_FAST_CASE(X)                                                                                   \
     case X:                                                                                                \
-        k_gemm_fast<bool(X & 8), bool(X & 4), bool(X & 2), bool(X & 1)><<<grid, kThreads, 0, s>>>(g); \
+        k_gemm_dma<bool(X & 8), bool(X & 4), bool(X & 2), bool(X & 1)><<<grid, kThreads, 0, s>>>(g); \
         break;
     switch (sel) {
         TRE_FAST_CASE(0) TRE_FAST_CASE(1) TRE_FAST_CASE(2) TRE_FAST_CASE(3)

@@ -354,6 +354,8 @@ static tre_status classify(Plan& p) {
             else if (sBN == 1 && sBK >= N) { p.fast_b_rowfast = true; p.fast_ldb = sBK; }
             else ok = false;
             p.fast_ldw = sWM;
+            // 16-byte copies: rows must start on 16-byte boundaries
+            ok = ok && p.fast_lda % 8 == 0 && p.fast_ldb % 8 == 0;
         }
         p.fast = ok;
     }
