@@ -298,6 +298,33 @@ class ThreeWay:
                 "seconds": secs}
 
 
+# Counter-measured HBM traffic of the dominant kernel, kept in profiles/ with
+# the SHA-256 of the kernel source the counters were taken on.
+TRAFFIC_RECORDS = {2: "hbm_traffic_gemm128_gnn_chain_262144_bf16.md"}
+
+
+def traffic_record(config):
+    """HBM bytes per launch of the dominant kernel (FETCH_SIZE + WRITE_SIZE,
+    each scaled by a copy of known size), or None when no record exists for
+    this workload or the kernel source changed since it was taken."""
+    import hashlib
+
+    name = TRAFFIC_RECORDS.get(config)
+    if name is None or PLAN_OPTIONS.get("u_ranges", 0) != 0:
+        return None
+    path = os.path.join(ROOT, "profiles", name)
+    try:
+        text = open(path).read()
+        rec = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
+        src = open(os.path.join(ROOT, rec["kernel_source"]), "rb").read()
+    except (OSError, IndexError, KeyError, ValueError):
+        return None
+    if hashlib.sha256(src).hexdigest() != rec["kernel_source_sha256"]:
+        return None
+    return {"bytes": rec["traffic_bytes_per_launch"], "read_bytes": rec["read_bytes_per_launch"],
+            "write_bytes": rec["write_bytes_per_launch"], "source": "profiles/" + name}
+
+
 def make_workload(c, tre, torch):
     if c in (1, 2, 5):
         return GnnChain(c, tre, torch)
@@ -392,7 +419,10 @@ def main():
         roof = {"bound": "mfma", "achieved": dflops / (contract_ms * 1e-3) / 1e12, "peak": PEAK_TFLOPS[dtype],
                 "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
+    rec = traffic_record(args.config)
+    roof["traffic"] = rec["bytes"] if rec else None
+    if rec:
+        roof["traffic_detail"] = rec
     roof["kernel"] = f"{dom.name} tile contraction ({dom.plan.kernel_class})"
     roof["kernel_ms"] = contract_ms
     roof["alg_bytes_per_launch"] = alg

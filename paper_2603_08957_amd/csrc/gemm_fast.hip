@@ -52,7 +52,7 @@ struct FastArgs {
     const int32_t* pb;
     int64_t a_elems, b_elems, w_elems;
     int64_t lda, ldb, ldw;
-    int32_t K, nblocks;
+    int32_t K, mblocks, nblocks;
     const Unit* units;
     const WsHeader* hdr;
     float* W;
@@ -207,10 +207,15 @@ __global__ __launch_bounds__(kThreads, (DmaShape<AROW, BROW>::kOcc)) void k_gemm
     using SH = DmaShape<AROW, BROW>;
     using RA = Ring<AROW>;
     using RB = Ring<BROW>;
-    const int unit_id = blockIdx.x;
+    // Workgroup -> (unit, row block, column block).  Workgroups are dealt to
+    // the 8 XCDs round-robin; the column blocks of one (unit, row block) take
+    // consecutive slots of one XCD, so they share the A tile in its L2.
+    const int64_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
+    const int64_t grp = (slot / g.nblocks) * 8 + xcd;
+    const int nblk = int(slot % g.nblocks), mblk = int(grp % g.mblocks);
+    const int64_t unit_id = grp / g.mblocks;
     if (unit_id >= g.hdr->n_units) return;
     const Unit un = g.units[unit_id];
-    const int mblk = blockIdx.y / g.nblocks, nblk = blockIdx.y % g.nblocks;
     const int m0 = mblk * kB, n0 = nblk * kB;
 
     __shared__ __attribute__((aligned(1024))) char lds[SH::kLds];
@@ -336,14 +341,16 @@ hipError_t launch_gemm_fast(const Plan& p, const Layout& L, char* ws, const void
     g.ldw = p.fast_ldw;
     g.K = int32_t(p.nK);
     const int64_t M = p.swap ? p.nN : p.nM, N = p.swap ? p.nM : p.nN;
+    g.mblocks = int32_t(M / kB);
     g.nblocks = int32_t(N / kB);
     g.units = reinterpret_cast<const Unit*>(ws + L.unit_desc);
     g.hdr = reinterpret_cast<const WsHeader*>(ws + L.hdr);
     g.W = w_tiles;
     g.partials = reinterpret_cast<float*>(ws + L.partials);
-    const int64_t gy = (M / kB) * (N / kB);
-    if (gy > 65535) return hipErrorInvalidConfiguration;
-    dim3 grid{unsigned(unit_bound), unsigned(gy), 1u};
+    const int64_t groups = unit_bound * g.mblocks;
+    const int64_t blocks = (groups + 7) / 8 * 8 * g.nblocks;
+    if (blocks > int64_t(0x7fffffff)) return hipErrorInvalidConfiguration;
+    dim3 grid{unsigned(blocks), 1u, 1u};
     // an operand whose tiles are each used by about one pair is streamed
     const int64_t n_a = p.swap ? L.n_v : L.n_u, n_b = p.swap ? L.n_u : L.n_v;
     const bool ant = 2 * n_a >= n_pairs, bnt = 2 * n_b >= n_pairs;
