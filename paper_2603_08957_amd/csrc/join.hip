@@ -118,35 +118,50 @@ __device__ inline uint64_t pack_w(const int32_t* urow, const int32_t* vrow, cons
 }
 
 // Pairs [t*8, t*8 + 8) of the expansion.  Writes either the final (u, v)
-// arrays (no group sort) or packed (u << 32 | v) payloads for the sort.
-__global__ void k_expand(const int64_t* __restrict__ off, const int64_t* __restrict__ lo, int64_t n_u, int64_t n_pairs,
-                         const uint32_t* __restrict__ vperm, const int32_t* __restrict__ ukeys, int ru,
-                         const int32_t* __restrict__ vkeys, int rv, WDesc wd, int32_t* __restrict__ pu,
-                         int32_t* __restrict__ pv, uint64_t* __restrict__ wk, uint64_t* __restrict__ uv) {
-    const int64_t p0 = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) * kPairsPerThread;
-    if (p0 >= n_pairs) return;
-    // largest u with off[u] <= p0
-    int64_t a = 0, b = n_u - 1;
-    while (a < b) {
-        int64_t m = (a + b + 1) >> 1;
-        if (off[m] <= p0) a = m; else b = m - 1;
-    }
-    int64_t u = a;
-    int64_t next = off[u + 1];
-    const int64_t p1 = min<int64_t>(p0 + kPairsPerThread, n_pairs);
-    for (int64_t p = p0; p < p1; p++) {
-        while (p >= next) {
-            u++;
-            next = off[u + 1];
+// arrays (no group sort) or packed (u << 32 | v) payloads for the sort.  A
+// workgroup's 2048 pairs are staged in LDS and written out by consecutive
+// threads, so every store instruction covers consecutive pairs.
+__global__ __launch_bounds__(kThreads) void k_expand(const int64_t* __restrict__ off, const int64_t* __restrict__ lo,
+                                                     int64_t n_u, int64_t n_pairs, const uint32_t* __restrict__ vperm,
+                                                     const int32_t* __restrict__ ukeys, int ru,
+                                                     const int32_t* __restrict__ vkeys, int rv, WDesc wd,
+                                                     int32_t* __restrict__ pu, int32_t* __restrict__ pv,
+                                                     uint64_t* __restrict__ wk, uint64_t* __restrict__ uv) {
+    constexpr int kBlockPairs = kThreads * kPairsPerThread;
+    __shared__ uint64_t swk[kBlockPairs];
+    __shared__ uint64_t suv[kBlockPairs];
+    const int64_t b0 = int64_t(blockIdx.x) * kBlockPairs;
+    const int64_t p0 = b0 + int64_t(threadIdx.x) * kPairsPerThread;
+    if (p0 < n_pairs) {
+        // largest u with off[u] <= p0
+        int64_t a = 0, b = n_u - 1;
+        while (a < b) {
+            int64_t m = (a + b + 1) >> 1;
+            if (off[m] <= p0) a = m; else b = m - 1;
         }
-        const int64_t vs = lo[u] + (p - off[u]);
-        const int64_t v = vperm ? int64_t(vperm[vs]) : vs;
-        wk[p] = pack_w(ukeys + u * ru, vkeys + v * rv, wd);
+        int64_t u = a;
+        int64_t next = off[u + 1];
+        const int64_t p1 = min<int64_t>(p0 + kPairsPerThread, n_pairs);
+        for (int64_t p = p0; p < p1; p++) {
+            while (p >= next) {
+                u++;
+                next = off[u + 1];
+            }
+            const int64_t vs = lo[u] + (p - off[u]);
+            const int64_t v = vperm ? int64_t(vperm[vs]) : vs;
+            swk[p - b0] = pack_w(ukeys + u * ru, vkeys + v * rv, wd);
+            suv[p - b0] = (uint64_t(uint32_t(u)) << 32) | uint64_t(uint32_t(v));
+        }
+    }
+    __syncthreads();
+    const int cnt = int(min<int64_t>(kBlockPairs, n_pairs - b0));
+    for (int q = threadIdx.x; q < cnt; q += kThreads) {
+        wk[b0 + q] = swk[q];
         if (uv) {
-            uv[p] = (uint64_t(uint32_t(u)) << 32) | uint64_t(uint32_t(v));
+            uv[b0 + q] = suv[q];
         } else {
-            pu[p] = int32_t(u);
-            pv[p] = int32_t(v);
+            pu[b0 + q] = int32_t(suv[q] >> 32);
+            pv[b0 + q] = int32_t(suv[q] & 0xffffffffu);
         }
     }
 }

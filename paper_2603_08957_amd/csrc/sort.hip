@@ -1,14 +1,23 @@
 // Stable LSD radix sort of (uint64 key, payload) pairs over the low `bits`
-// bits of the key, with up to 11-bit digits (so a 20-bit key takes two
-// passes).  Payload: uint32 (a permutation) or uint64 (a packed pair).
+// bits of the key, in passes of at most 8-bit digits (a 20-bit key takes
+// three passes of 7 bits).  Payload: uint32 (a permutation) or uint64 (a
+// packed pair).
 //
 // Per pass: (1) every 256-thread workgroup counts the digits of its
-// 8192-item tile in LDS, (2) a device-wide exclusive scan over the digit-major
-// count matrix gives each (digit, tile) its output base, (3) each workgroup
-// walks its tile in 32 rounds of 256 items in index order and ranks every item
-// among equal digits with one wavefront ballot per digit bit (a 64-lane match
-// mask); wave totals meet in LDS.  Equal keys keep their input order, so the
-// result is deterministic.
+// 4096-item tile in LDS, (2) a device-wide exclusive scan over the
+// digit-major count matrix gives each (digit, tile) its output base, (3)
+// each workgroup ranks its tile locally and writes it out through LDS:
+//   - wave w owns the contiguous quarter [1024 w, 1024 w + 1024) of the tile
+//     and walks it in 16 rounds of 64 items; an item's rank among equal
+//     digits of its wave comes from one ballot per digit bit (a 64-lane
+//     match mask) plus a per-(wave, digit) counter in LDS,
+//   - after one barrier the counters become per-digit wave prefixes and a
+//     scan over the digits gives the tile-local start of every digit,
+//   - items are placed in LDS in their tile-local sorted position, and the
+//     workgroup copies the tile out in that order: each digit's run is one
+//     contiguous stretch of the output, so the stores are coalesced.
+// Equal digits keep their input order (wave, round, lane order is index
+// order), so the sort is stable and the result deterministic.
 #include "tre_internal.h"
 
 namespace tre {
@@ -16,14 +25,16 @@ namespace tre {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kIpt = 32;
-constexpr int kTile = kThreads * kIpt;
-constexpr int kMaxBits = 11;
-constexpr int kMaxRadix = 1 << kMaxBits;
+constexpr int kWaves = kThreads / 64;
+constexpr int kIpt = 16;
+constexpr int kTile = kThreads * kIpt;  // 4096 items
+constexpr int kPerWave = kTile / kWaves;
+constexpr int kMaxBits = 8;
+constexpr int kRadix = 1 << kMaxBits;
 
 __global__ __launch_bounds__(kThreads) void k_digit_hist(const uint64_t* __restrict__ keys, int64_t n, int shift,
                                                          int dbits, int32_t* __restrict__ hist, int64_t n_tiles) {
-    __shared__ int32_t cnt[kMaxRadix];
+    __shared__ int32_t cnt[kRadix];
     const int radix = 1 << dbits;
     for (int d = threadIdx.x; d < radix; d += kThreads) cnt[d] = 0;
     __syncthreads();
@@ -43,52 +54,95 @@ __global__ __launch_bounds__(kThreads) void k_digit_scatter(const uint64_t* __re
                                                             uint64_t* __restrict__ kout, VT* __restrict__ vout,
                                                             int64_t n, int shift, int dbits,
                                                             const int32_t* __restrict__ offs, int64_t n_tiles) {
-    __shared__ int32_t base[kMaxRadix];
-    __shared__ int32_t wcnt[kThreads / 64][kMaxRadix];
+    __shared__ uint64_t skey[kTile];
+    __shared__ VT sval[kTile];
+    __shared__ int32_t wcnt[kWaves][kRadix];  // per-(wave, digit) counts, then wave prefixes
+    __shared__ int32_t dstart[kRadix];        // tile-local start of each digit
+    __shared__ int32_t gbase[kRadix];         // output position of (digit, this tile)
+    __shared__ int32_t wsum[kWaves];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int radix = 1 << dbits;
-    for (int d = tid; d < radix; d += kThreads) {
-        base[d] = offs[int64_t(d) * n_tiles + blockIdx.x];
+    for (int d = tid; d < kRadix; d += kThreads)
 #pragma unroll
-        for (int i = 0; i < kThreads / 64; i++) wcnt[i][d] = 0;
-    }
+        for (int i = 0; i < kWaves; i++) wcnt[i][d] = 0;
     __syncthreads();
+
     const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     const uint64_t dmask = uint64_t(radix - 1);
     const int64_t tile0 = int64_t(blockIdx.x) * kTile;
+    const int64_t item0 = tile0 + int64_t(w) * kPerWave + lane;
+    uint64_t key[kIpt];
+    VT val[kIpt];
+    int32_t rank[kIpt];
+#pragma unroll
     for (int r = 0; r < kIpt; r++) {
-        const int64_t i = tile0 + int64_t(r) * kThreads + tid;
+        const int64_t i = item0 + int64_t(r) * 64;
         const bool valid = i < n;
-        const uint64_t key = valid ? kin[i] : 0ull;
-        const VT val = valid ? vin[i] : VT(0);
-        const int d = int((key >> shift) & dmask);
+        key[r] = valid ? kin[i] : 0ull;
+        val[r] = valid ? vin[i] : VT(0);
+    }
+    // ranks among equal digits inside this wave's quarter, in index order
+#pragma unroll
+    for (int r = 0; r < kIpt; r++) {
+        const bool valid = item0 + int64_t(r) * 64 < n;
+        const int d = int((key[r] >> shift) & dmask);
         uint64_t mask = __ballot(valid);
         for (int b = 0; b < dbits; b++) {
             const bool bit = (d >> b) & 1;
             const uint64_t bb = __ballot(bit);
             mask &= bit ? bb : ~bb;
         }
-        const int rank = __popcll(mask & lt);
-        if (valid && rank == 0) wcnt[w][d] = __popcll(mask);
-        __syncthreads();
-        if (valid) {
-            int32_t pre = 0;
-            for (int j = 0; j < w; j++) pre += wcnt[j][d];
-            const int64_t dest = int64_t(base[d]) + pre + rank;
-            kout[dest] = key;
-            vout[dest] = val;
-        }
-        __syncthreads();
-        for (int dd = tid; dd < radix; dd += kThreads) {
-            int32_t add = 0;
+        const int32_t before = valid ? wcnt[w][d] : 0;
+        rank[r] = before + __popcll(mask & lt);
+        // the lowest lane of each digit group advances the counter; every lane
+        // of the group has read it above (one wavefront, LDS order kept)
+        if (valid && (mask & lt) == 0) wcnt[w][d] = before + __popcll(mask);
+    }
+    __syncthreads();
+    // per digit: wave prefixes and the tile total; then tile-local starts
+    int32_t tot = 0;
+    if (tid < kRadix) {
 #pragma unroll
-            for (int j = 0; j < kThreads / 64; j++) {
-                add += wcnt[j][dd];
-                wcnt[j][dd] = 0;
-            }
-            base[dd] += add;
+        for (int i = 0; i < kWaves; i++) {
+            const int32_t c = wcnt[i][tid];
+            wcnt[i][tid] = tot;
+            tot += c;
         }
-        __syncthreads();
+        gbase[tid] = tid < radix ? offs[int64_t(tid) * n_tiles + blockIdx.x] : 0;
+    }
+    // exclusive scan of tot over the 256 digits (one digit per thread)
+    int32_t incl = tot;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int32_t y = __shfl_up(incl, o);
+        if (lane >= o) incl += y;
+    }
+    if (lane == 63) wsum[w] = incl;
+    __syncthreads();
+    int32_t carry = 0;
+    for (int i = 0; i < w; i++) carry += wsum[i];
+    if (tid < kRadix) dstart[tid] = carry + incl - tot;
+    __syncthreads();
+    // place every item at its tile-local sorted position
+#pragma unroll
+    for (int r = 0; r < kIpt; r++) {
+        if (item0 + int64_t(r) * 64 < n) {
+            const int d = int((key[r] >> shift) & dmask);
+            const int pos = dstart[d] + wcnt[w][d] + rank[r];
+            skey[pos] = key[r];
+            sval[pos] = val[r];
+        }
+    }
+    __syncthreads();
+    // copy out in sorted order: consecutive positions of one digit are
+    // consecutive output positions
+    const int cnt = int(min<int64_t>(kTile, n - tile0));
+    for (int q = tid; q < cnt; q += kThreads) {
+        const uint64_t k = skey[q];
+        const int d = int((k >> shift) & dmask);
+        const int64_t dest = int64_t(gbase[d]) + (q - dstart[d]);
+        kout[dest] = k;
+        vout[dest] = sval[q];
     }
 }
 
@@ -121,7 +175,7 @@ hipError_t sort_impl(uint64_t* keys, VT* vals, uint64_t* keys_alt, VT* vals_alt,
 
 }  // namespace
 
-int64_t radix_hist_elems(int64_t n) { return int64_t(kMaxRadix) * ((n + kTile - 1) / kTile) + 64; }
+int64_t radix_hist_elems(int64_t n) { return int64_t(kRadix) * ((n + kTile - 1) / kTile) + 64; }
 
 hipError_t radix_sort_u64(uint64_t* keys, uint32_t* vals, uint64_t* keys_alt, uint32_t* vals_alt, int64_t n,
                           int bits, int32_t* hist, int32_t* scan_tmp, hipStream_t s) {
