@@ -95,10 +95,21 @@ __global__ void k_count(const int32_t* __restrict__ ukeys, int64_t n_u, int ru, 
         int64_t m = (a + b) >> 1;
         if (vjk[m] < key) a = m + 1; else b = m;
     }
-    int64_t c = a, e = n_v;
-    while (c < e) {
-        int64_t m = (c + e) >> 1;
-        if (vjk[m] <= key) c = m + 1; else e = m;
+    // end of the run: gallop from its start (runs are short), then bisect
+    int64_t c = a;
+    if (a < n_v && vjk[a] == key) {
+        int64_t last = a, step = 1, probe = a + 1;
+        while (probe < n_v && vjk[probe] == key) {
+            last = probe;
+            step <<= 1;
+            probe = a + step;
+        }
+        int64_t x = last + 1, y = min(probe, n_v);
+        while (x < y) {
+            int64_t m = (x + y) >> 1;
+            if (vjk[m] == key) x = m + 1; else y = m;
+        }
+        c = x;
     }
     lo[u] = a;
     cnt[u] = c - a;
@@ -166,15 +177,6 @@ __global__ __launch_bounds__(kThreads) void k_expand(const int64_t* __restrict__
     }
 }
 
-__global__ void k_split_pairs(const uint64_t* __restrict__ uv, int32_t* __restrict__ pu, int32_t* __restrict__ pv,
-                              int64_t n) {
-    const int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (p >= n) return;
-    const uint64_t x = uv[p];
-    pu[p] = int32_t(x >> 32);
-    pv[p] = int32_t(x & 0xffffffffu);
-}
-
 __global__ void k_heads(const uint64_t* __restrict__ wk, int64_t n, int32_t* __restrict__ flags) {
     const int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (p > n) return;
@@ -234,6 +236,10 @@ hipError_t launch_join(const Plan& p, const Layout& L, char* ws, const int32_t* 
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
     uint64_t* vjk = reinterpret_cast<uint64_t*>(ws + L.vjk);
     uint32_t* vperm = p.v_needs_sort ? reinterpret_cast<uint32_t*>(ws + L.vperm) : nullptr;
+    // the sorted join keys end up in the alt buffer after an odd pass count
+    const uint64_t* vjk_sorted =
+        (p.v_needs_sort && radix_result_in_alt(L.n_v, p.join_total_bits)) ? reinterpret_cast<uint64_t*>(ws + L.vjk_alt)
+                                                                           : vjk;
     int64_t* cnt = reinterpret_cast<int64_t*>(ws + L.ucnt);
     int64_t* lo = reinterpret_cast<int64_t*>(ws + L.ulo);
     int64_t* tmp = reinterpret_cast<int64_t*>(ws + L.scan_tmp);
@@ -250,7 +256,8 @@ hipError_t launch_join(const Plan& p, const Layout& L, char* ws, const int32_t* 
             if (e != hipSuccess) return e;
         }
     }
-    k_count<<<blocks_for(n_u + 1), kThreads, 0, s>>>(u_keys, n_u, p.nk[0], desc_u(p), vjk, n_v, p.n_join > 0, cnt, lo);
+    k_count<<<blocks_for(n_u + 1), kThreads, 0, s>>>(u_keys, n_u, p.nk[0], desc_u(p), vjk_sorted, n_v, p.n_join > 0,
+                                                      cnt, lo);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = scan_exclusive_i64(cnt, cnt, n_u + 1, tmp, s)) != hipSuccess) return e;
     k_store_count<<<1, 1, 0, s>>>(cnt, n_u, hdr);
@@ -263,7 +270,9 @@ hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t*
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
     int64_t* off = reinterpret_cast<int64_t*>(ws + L.ucnt);
     int64_t* lo = reinterpret_cast<int64_t*>(ws + L.ulo);
-    uint32_t* vperm = p.v_needs_sort ? reinterpret_cast<uint32_t*>(ws + L.vperm) : nullptr;
+    uint32_t* vperm = nullptr;
+    if (p.v_needs_sort)
+        vperm = reinterpret_cast<uint32_t*>(ws + (radix_result_in_alt(L.n_v, p.join_total_bits) ? L.vperm_alt : L.vperm));
     int32_t* pu = reinterpret_cast<int32_t*>(ws + L.pu);
     int32_t* pv = reinterpret_cast<int32_t*>(ws + L.pv);
     uint64_t* wk = reinterpret_cast<uint64_t*>(ws + L.wk);
@@ -289,11 +298,12 @@ hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t*
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (sort) {
+        // the last pass writes the sorted (u, v) straight into pu / pv
         e = radix_sort_u64_pairs(wk, uv, reinterpret_cast<uint64_t*>(ws + L.wk_alt),
-                                 reinterpret_cast<uint64_t*>(ws + L.pidx_alt), n_pairs, p.w_total_bits, hist, tmp, s);
+                                 reinterpret_cast<uint64_t*>(ws + L.pidx_alt), n_pairs, p.w_total_bits, hist, tmp, pu,
+                                 pv, s);
         if (e != hipSuccess) return e;
-        k_split_pairs<<<blocks_for(n_pairs), kThreads, 0, s>>>(uv, pu, pv, n_pairs);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if (radix_result_in_alt(n_pairs, p.w_total_bits)) wk = reinterpret_cast<uint64_t*>(ws + L.wk_alt);
     }
     k_heads<<<blocks_for(n_pairs + 1), kThreads, 0, s>>>(wk, n_pairs, flags);
     if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -1,7 +1,9 @@
 // Stable LSD radix sort of (uint64 key, payload) pairs over the low `bits`
 // bits of the key, in passes of at most 8-bit digits (a 20-bit key takes
 // three passes of 7 bits).  Payload: uint32 (a permutation) or uint64 (a
-// packed pair).
+// packed pair, optionally split into two int32 arrays by the last pass).
+// Passes ping-pong between the two buffers; the result stays where the last
+// pass wrote it (radix_result_in_alt tells which).
 //
 // Per pass: (1) every 256-thread workgroup counts the digits of its
 // 4096-item tile in LDS, (2) a device-wide exclusive scan over the
@@ -31,6 +33,8 @@ constexpr int kTile = kThreads * kIpt;  // 4096 items
 constexpr int kPerWave = kTile / kWaves;
 constexpr int kMaxBits = 8;
 constexpr int kRadix = 1 << kMaxBits;
+constexpr int kDpt = kRadix / kThreads;  // digits per thread in the prefix step
+static_assert(kDpt >= 1 && kDpt * kThreads == kRadix, "radix must be a multiple of the workgroup size");
 
 __global__ __launch_bounds__(kThreads) void k_digit_hist(const uint64_t* __restrict__ keys, int64_t n, int shift,
                                                          int dbits, int32_t* __restrict__ hist, int64_t n_tiles) {
@@ -49,9 +53,12 @@ __global__ __launch_bounds__(kThreads) void k_digit_hist(const uint64_t* __restr
     for (int d = threadIdx.x; d < radix; d += kThreads) hist[int64_t(d) * n_tiles + blockIdx.x] = cnt[d];
 }
 
-template <typename VT>
+// SPLIT (uint64 payloads only): write the payload's high and low halves to
+// two int32 arrays instead of vout.
+template <typename VT, bool SPLIT>
 __global__ __launch_bounds__(kThreads) void k_digit_scatter(const uint64_t* __restrict__ kin, const VT* __restrict__ vin,
                                                             uint64_t* __restrict__ kout, VT* __restrict__ vout,
+                                                            int32_t* __restrict__ hi_out, int32_t* __restrict__ lo_out,
                                                             int64_t n, int shift, int dbits,
                                                             const int32_t* __restrict__ offs, int64_t n_tiles) {
     __shared__ uint64_t skey[kTile];
@@ -99,19 +106,26 @@ __global__ __launch_bounds__(kThreads) void k_digit_scatter(const uint64_t* __re
         if (valid && (mask & lt) == 0) wcnt[w][d] = before + __popcll(mask);
     }
     __syncthreads();
-    // per digit: wave prefixes and the tile total; then tile-local starts
-    int32_t tot = 0;
-    if (tid < kRadix) {
+    // per digit: wave prefixes and the tile total; then tile-local starts.
+    // Thread t owns the kDpt consecutive digits [kDpt t, kDpt t + kDpt).
+    int32_t tot[kDpt];
+    int32_t sum = 0;
+#pragma unroll
+    for (int j = 0; j < kDpt; j++) {
+        const int d = tid * kDpt + j;
+        int32_t acc = 0;
 #pragma unroll
         for (int i = 0; i < kWaves; i++) {
-            const int32_t c = wcnt[i][tid];
-            wcnt[i][tid] = tot;
-            tot += c;
+            const int32_t c = wcnt[i][d];
+            wcnt[i][d] = acc;
+            acc += c;
         }
-        gbase[tid] = tid < radix ? offs[int64_t(tid) * n_tiles + blockIdx.x] : 0;
+        tot[j] = acc;
+        sum += acc;
+        gbase[d] = d < radix ? offs[int64_t(d) * n_tiles + blockIdx.x] : 0;
     }
-    // exclusive scan of tot over the 256 digits (one digit per thread)
-    int32_t incl = tot;
+    // exclusive scan of the per-thread sums over the workgroup
+    int32_t incl = sum;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
         const int32_t y = __shfl_up(incl, o);
@@ -119,9 +133,13 @@ __global__ __launch_bounds__(kThreads) void k_digit_scatter(const uint64_t* __re
     }
     if (lane == 63) wsum[w] = incl;
     __syncthreads();
-    int32_t carry = 0;
-    for (int i = 0; i < w; i++) carry += wsum[i];
-    if (tid < kRadix) dstart[tid] = carry + incl - tot;
+    int32_t run = incl - sum;
+    for (int i = 0; i < w; i++) run += wsum[i];
+#pragma unroll
+    for (int j = 0; j < kDpt; j++) {
+        dstart[tid * kDpt + j] = run;
+        run += tot[j];
+    }
     __syncthreads();
     // place every item at its tile-local sorted position
 #pragma unroll
@@ -142,16 +160,23 @@ __global__ __launch_bounds__(kThreads) void k_digit_scatter(const uint64_t* __re
         const int d = int((k >> shift) & dmask);
         const int64_t dest = int64_t(gbase[d]) + (q - dstart[d]);
         kout[dest] = k;
-        vout[dest] = sval[q];
+        if constexpr (SPLIT) {
+            hi_out[dest] = int32_t(uint64_t(sval[q]) >> 32);
+            lo_out[dest] = int32_t(uint64_t(sval[q]) & 0xffffffffu);
+        } else {
+            vout[dest] = sval[q];
+        }
     }
 }
 
+int sort_passes(int bits) { return bits <= 0 ? 0 : (bits + kMaxBits - 1) / kMaxBits; }
+
 template <typename VT>
 hipError_t sort_impl(uint64_t* keys, VT* vals, uint64_t* keys_alt, VT* vals_alt, int64_t n, int bits, int32_t* hist,
-                     int32_t* scan_tmp, hipStream_t s) {
+                     int32_t* scan_tmp, int32_t* split_hi, int32_t* split_lo, hipStream_t s) {
     if (n <= 1 || bits <= 0) return hipSuccess;
     const int64_t nt = (n + kTile - 1) / kTile;
-    const int passes = (bits + kMaxBits - 1) / kMaxBits;
+    const int passes = sort_passes(bits);
     const int dbits = (bits + passes - 1) / passes;
     uint64_t *ki = keys, *ko = keys_alt;
     VT *vi = vals, *vo = vals_alt;
@@ -160,15 +185,14 @@ hipError_t sort_impl(uint64_t* keys, VT* vals, uint64_t* keys_alt, VT* vals_alt,
         k_digit_hist<<<dim3(unsigned(nt)), kThreads, 0, s>>>(ki, n, shift, dbits, hist, nt);
         hipError_t e = scan_exclusive_i32(hist, hist, (int64_t(1) << dbits) * nt, scan_tmp, s);
         if (e != hipSuccess) return e;
-        k_digit_scatter<VT><<<dim3(unsigned(nt)), kThreads, 0, s>>>(ki, vi, ko, vo, n, shift, dbits, hist, nt);
+        if (split_hi && p == passes - 1)
+            k_digit_scatter<VT, true><<<dim3(unsigned(nt)), kThreads, 0, s>>>(ki, vi, ko, vo, split_hi, split_lo, n,
+                                                                             shift, dbits, hist, nt);
+        else
+            k_digit_scatter<VT, false><<<dim3(unsigned(nt)), kThreads, 0, s>>>(ki, vi, ko, vo, nullptr, nullptr, n,
+                                                                              shift, dbits, hist, nt);
         std::swap(ki, ko);
         std::swap(vi, vo);
-    }
-    if (ki != keys) {
-        hipError_t e = hipMemcpyAsync(keys, ki, sizeof(uint64_t) * size_t(n), hipMemcpyDeviceToDevice, s);
-        if (e != hipSuccess) return e;
-        e = hipMemcpyAsync(vals, vi, sizeof(VT) * size_t(n), hipMemcpyDeviceToDevice, s);
-        if (e != hipSuccess) return e;
     }
     return hipGetLastError();
 }
@@ -177,14 +201,17 @@ hipError_t sort_impl(uint64_t* keys, VT* vals, uint64_t* keys_alt, VT* vals_alt,
 
 int64_t radix_hist_elems(int64_t n) { return int64_t(kRadix) * ((n + kTile - 1) / kTile) + 64; }
 
+bool radix_result_in_alt(int64_t n, int bits) { return n > 1 && (sort_passes(bits) & 1); }
+
 hipError_t radix_sort_u64(uint64_t* keys, uint32_t* vals, uint64_t* keys_alt, uint32_t* vals_alt, int64_t n,
                           int bits, int32_t* hist, int32_t* scan_tmp, hipStream_t s) {
-    return sort_impl<uint32_t>(keys, vals, keys_alt, vals_alt, n, bits, hist, scan_tmp, s);
+    return sort_impl<uint32_t>(keys, vals, keys_alt, vals_alt, n, bits, hist, scan_tmp, nullptr, nullptr, s);
 }
 
 hipError_t radix_sort_u64_pairs(uint64_t* keys, uint64_t* vals, uint64_t* keys_alt, uint64_t* vals_alt, int64_t n,
-                                int bits, int32_t* hist, int32_t* scan_tmp, hipStream_t s) {
-    return sort_impl<uint64_t>(keys, vals, keys_alt, vals_alt, n, bits, hist, scan_tmp, s);
+                                int bits, int32_t* hist, int32_t* scan_tmp, int32_t* split_hi, int32_t* split_lo,
+                                hipStream_t s) {
+    return sort_impl<uint64_t>(keys, vals, keys_alt, vals_alt, n, bits, hist, scan_tmp, split_hi, split_lo, s);
 }
 
 }  // namespace tre

@@ -122,13 +122,18 @@ size_t scan_tmp_elems(int64_t n);
 hipError_t scan_exclusive_i64(const int64_t* in, int64_t* out, int64_t n, int64_t* tmp, hipStream_t s);
 hipError_t scan_exclusive_i32(const int32_t* in, int32_t* out, int64_t n, int32_t* tmp, hipStream_t s);
 
-// sort.hip: stable LSD radix sort of (uint64 key, uint32 payload) over the
-// low `bits` bits; result lands in keys/vals (alt buffers are scratch).
+// sort.hip: stable LSD radix sort of (uint64 key, payload) over the low
+// `bits` bits.  The passes alternate between the primary and the alt
+// buffers; the sorted result is in the alt buffers iff
+// radix_result_in_alt(n, bits).  The pair variant can split the uint64
+// payload (hi, lo) into two int32 arrays instead (split_hi non-null).
 int64_t radix_hist_elems(int64_t n);
+bool radix_result_in_alt(int64_t n, int bits);
 hipError_t radix_sort_u64(uint64_t* keys, uint32_t* vals, uint64_t* keys_alt, uint32_t* vals_alt, int64_t n,
                           int bits, int32_t* hist, int32_t* scan_tmp, hipStream_t s);
 hipError_t radix_sort_u64_pairs(uint64_t* keys, uint64_t* vals, uint64_t* keys_alt, uint64_t* vals_alt, int64_t n,
-                                int bits, int32_t* hist, int32_t* scan_tmp, hipStream_t s);
+                                int bits, int32_t* hist, int32_t* scan_tmp, int32_t* split_hi, int32_t* split_lo,
+                                hipStream_t s);
 
 // join.hip
 hipError_t launch_validate(const int32_t* keys, int64_t n, int r, const int32_t* radix, int32_t* err_flag,
