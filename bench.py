@@ -310,7 +310,7 @@ def traffic_record(config):
     import hashlib
 
     name = TRAFFIC_RECORDS.get(config)
-    if name is None or PLAN_OPTIONS.get("u_ranges", 0) != 0:
+    if name is None or PLAN_OPTIONS.get("u_ranges", 0) != 0 or PLAN_OPTIONS.get("pace_windows", 0) != 0:
         return None
     path = os.path.join(ROOT, "profiles", name)
     try:
@@ -344,6 +344,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--u-ranges", type=int, default=0,
                     help="tre_options.u_ranges for every EinSum (0 = library default, < 0 = off)")
+    ap.add_argument("--pace-windows", type=int, default=0,
+                    help="tre_options.pace_windows for every EinSum (0 = library default, < 0 = off)")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="first run one device copy of this many GiB (counter calibration under rocprofv3 --pmc)")
     args = ap.parse_args()
@@ -370,6 +372,7 @@ def main():
         log(f"[bench] calibration copy: {4 * n} bytes read, {4 * n} bytes written")
         del src, dst
     PLAN_OPTIONS["u_ranges"] = args.u_ranges
+    PLAN_OPTIONS["pace_windows"] = args.pace_windows
     W = make_workload(args.config, tre, torch)
     log("[bench] inputs resident; warming up")
     for _ in range(args.warmup):

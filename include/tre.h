@@ -76,7 +76,13 @@ typedef struct {
     int32_t u_ranges;           /* bf16 128x128 path: cut every output key's pairs into this many ranges of
                                    U tuple index and run range by range so concurrent workgroups share U
                                    tiles in L2 (partials summed after); 0 = automatic, < 0 = never */
-    int32_t reserved[5];
+    int32_t pace_windows;       /* bf16 128x128 path with one 128x128 block per W tile: one persistent
+                                   workgroup per resident slot walks whole keys while the workgroups of each
+                                   XCD keep within a few windows of U tuple index of each other (the U
+                                   index range is cut into this many windows), so U tiles stay in L2 with
+                                   no partial tiles; 0 = automatic (preferred over u_ranges when both
+                                   apply), < 0 = never.  Results do not depend on it. */
+    int32_t reserved[4];
 } tre_options;
 
 /* Static facts about a plan (host). */

@@ -96,6 +96,33 @@ int32_t choose_u_ranges(const Plan& p, const Layout& L, int64_t n_u, int64_t n_p
     return R > 1 ? int32_t(R) : 0;
 }
 
+// Windows for the paced persistent kernel (0 = not used).  It applies where
+// U ranges would (U tiles reused by many keys and too big for one L2) when a W
+// tile is one 128x128 block, and is preferred there: it keeps U tiles in L2
+// without partial tiles.  `slots` = workgroups resident at once.
+int32_t choose_pacing(const Plan& p, int64_t n_u, int64_t n_pairs, int64_t n_w, int64_t slots) {
+    if (!(p.kclass == KC_GEMM && p.fast) || blocks_per_unit(p) != 1 || p.opt.pace_windows < 0 ||
+        p.opt.max_pairs_per_unit > 0 || n_u < 2 || n_w < 1 || slots <= 0)
+        return 0;
+    int64_t W;
+    if (p.opt.pace_windows > 0) {
+        W = p.opt.pace_windows;
+    } else {
+        if (p.opt.u_ranges != 0) return 0;  // an explicit U-range request wins
+        const int64_t u_bytes = n_u * p.tile_elems[0] * (p.dtype == TRE_BF16 ? 2 : 4);
+        const int64_t reuse = n_pairs / n_u;
+        if (u_bytes <= (int64_t(16) << 20) || reuse < 64 || n_w < slots) return 0;
+        // ~4 MB of U per window: measured best on the 262,144-vertex chain
+        // (2 MB windows wait more often, 8 MB windows miss L2)
+        W = (u_bytes + (int64_t(4) << 20) - 1) >> 22;
+    }
+    W = std::max<int64_t>(1, std::min<int64_t>({W, n_u, 256}));
+    const int64_t n_wg = std::min(n_w, slots);
+    const int64_t rounds = (n_w + n_wg - 1) / n_wg;
+    if (rounds * 8 * W > kPaceCounters) return 0;
+    return int32_t(W);
+}
+
 int64_t choose_unit(const Plan& p, const Layout& L, int64_t n_pairs, int64_t n_w) {
     const int64_t bpu = blocks_per_unit(p);
     int64_t pu;
@@ -241,8 +268,10 @@ tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* 
     const bool deferred = timing && timing->deferred;
     Timer tm(timing != nullptr, deferred);
     tm.mark(s);
-    const int32_t R = choose_u_ranges(p, L, jr->n_u, n_pairs, n_w);
-    const int64_t p_unit = R > 1 ? n_pairs : choose_unit(p, L, n_pairs, n_w);
+    const int64_t slots = (p.kclass == KC_GEMM && p.fast) ? gemm_paced_slots(p) : 0;
+    const int32_t pace = choose_pacing(p, jr->n_u, n_pairs, n_w, slots);
+    const int32_t R = pace ? 0 : choose_u_ranges(p, L, jr->n_u, n_pairs, n_w);
+    const int64_t p_unit = (R > 1 || pace) ? n_pairs : choose_unit(p, L, n_pairs, n_w);
     hipError_t e;
     if ((e = launch_tables(p, reinterpret_cast<int32_t*>(w + L.tables), s)) != hipSuccess) return dev_fail(e, "tables");
     if (R > 1) e = launch_range_units(p, L, w, n_w, jr->n_u, R, s);
@@ -250,8 +279,17 @@ tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* 
     if (e != hipSuccess) return dev_fail(e, "units");
     tm.mark(s);
     const int64_t unit_bound = R > 1 ? int64_t(R) * n_w : n_w + n_pairs / p_unit + 1;
-    if ((e = launch_contract(p, L, w, u_tiles, v_tiles, w_tiles, n_pairs, n_w, unit_bound, s)) != hipSuccess)
-        return dev_fail(e, "contract");
+    if (pace) {
+        // one unit per key; every workgroup of the grid is resident at once
+        const int64_t n_wg = std::min(n_w, slots);
+        const int64_t rounds = (n_w + n_wg - 1) / n_wg;
+        if ((e = launch_fill_zero(w + L.pace, sizeof(int32_t) * size_t(rounds * 8 * pace), s)) != hipSuccess)
+            return dev_fail(e, "pace");
+        e = launch_gemm_paced(p, L, w, u_tiles, v_tiles, w_tiles, n_pairs, n_wg, pace, s);
+    } else {
+        e = launch_contract(p, L, w, u_tiles, v_tiles, w_tiles, n_pairs, n_w, unit_bound, s);
+    }
+    if (e != hipSuccess) return dev_fail(e, "contract");
     tm.mark(s);
     if (R > 1 || p_unit < n_pairs) {
         const int64_t split_bound = R > 1 ? n_w : std::min<int64_t>(n_w, n_pairs / (p_unit + 1) + 1);

@@ -53,6 +53,8 @@ struct FastArgs {
     int64_t a_elems, b_elems, w_elems;
     int64_t lda, ldb, ldw;
     int32_t K, mblocks, nblocks;
+    const int32_t* ridx;  // pacing: U's tile index of each pair, and U's tile count
+    int64_t n_r;
     const Unit* units;
     const WsHeader* hdr;
     float* W;
@@ -202,23 +204,55 @@ struct DmaShape {
     static constexpr int kWait1 = (AROW || BROW) ? 8 : 16;
 };
 
-template <bool AROW, bool BROW, bool ANT, bool BNT>
-__global__ __launch_bounds__(kThreads, (DmaShape<AROW, BROW>::kOcc)) void k_gemm_dma(FastArgs g) {
+// Pacing hooks of run_unit: called by every thread at the first tick of
+// each pair and after the last one.  NoPace does nothing.
+struct NoPace {
+    __device__ void at_pair(int) {}
+    __device__ void at_end() {}
+};
+
+// Cooperative pacing for the persistent variant (below).  The reused
+// operand's index range is cut into `windows` windows; done[q] counts the
+// workgroups of this XCD and round that have moved past window q.  Before a
+// workgroup's pairs enter window w, it waits until `thr` peers are past
+// window w - 1 - ahead, so the workgroups sharing an L2 stay within a few
+// windows of each other.  The wait is bounded: after kMaxPolls polls it
+// goes on regardless, so pacing can only cost time, never correctness.
+struct Pace {
+    static constexpr int kMaxPolls = 4096;
+    int32_t* done;
+    const const_i32* ridx;  // reused operand's tile index of each pair of the unit
+    int64_t n_r;            // tiles of the reused operand
+    int windows, ahead, thr, cur;
+    __device__ int window_of(int32_t i) const { return int(int64_t(i) * windows / n_r); }
+    __device__ void pass_to(int w) {
+        for (int q = cur < 0 ? 0 : cur; q < w; q++) atomicAdd(done + q, 1);
+    }
+    __device__ void at_pair(int p) {
+        if (threadIdx.x != 0) return;
+        const int w = window_of(ridx[p]);
+        if (w == cur) return;
+        pass_to(w);
+        cur = w;
+        const int q = w - 1 - ahead;
+        if (q < 0) return;
+        for (int it = 0; it < kMaxPolls; it++) {
+            if (__hip_atomic_load(done + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= thr) break;
+            __builtin_amdgcn_s_sleep(2);
+        }
+    }
+    __device__ void at_end() {
+        if (threadIdx.x == 0) pass_to(windows);
+    }
+};
+
+// One work unit: sum over its pairs of A_p B_p into the 128x128 block
+// (m0, n0) of its output tile, written to W (whole key) or a partial slot.
+template <bool AROW, bool BROW, bool ANT, bool BNT, class Pacer>
+__device__ inline void run_unit(const FastArgs& g, const Unit& un, int m0, int n0, char* lds, Pacer& pc) {
     using SH = DmaShape<AROW, BROW>;
     using RA = Ring<AROW>;
     using RB = Ring<BROW>;
-    // Workgroup -> (unit, row block, column block).  Workgroups are dealt to
-    // the 8 XCDs round-robin; the column blocks of one (unit, row block) take
-    // consecutive slots of one XCD, so they share the A tile in its L2.
-    const int64_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
-    const int64_t grp = (slot / g.nblocks) * 8 + xcd;
-    const int nblk = int(slot % g.nblocks), mblk = int(grp % g.mblocks);
-    const int64_t unit_id = grp / g.mblocks;
-    if (unit_id >= g.hdr->n_units) return;
-    const Unit un = g.units[unit_id];
-    const int m0 = mblk * kB, n0 = nblk * kB;
-
-    __shared__ __attribute__((aligned(1024))) char lds[SH::kLds];
     const uint32_t lds_a = uint32_t(reinterpret_cast<uintptr_t>((lds_char*)(lds)));
     const uint32_t lds_b = lds_a + RA::kBytes;
 
@@ -233,11 +267,13 @@ __global__ __launch_bounds__(kThreads, (DmaShape<AROW, BROW>::kOcc)) void k_gemm
             for (int r = 0; r < 16; r++) acc[i][j][r] = 0.f;
 
     const int np = un.p1 - un.p0;
-    const int ticks = np * (g.K / 32);
+    const int tpp = g.K / 32;  // ticks per pair
+    const int ticks = np * tpp;
     float* out = un.slot < 0 ? g.W + int64_t(un.seg) * g.w_elems : g.partials + int64_t(un.slot) * g.w_elems;
     if (ticks == 0) {
         for (int e = threadIdx.x; e < kB * kB; e += kThreads)
             out[int64_t(m0 + e / kB) * g.ldw + n0 + e % kB] = 0.f;
+        pc.at_end();
         return;
     }
     // the pair list is read-only here; reading it through the constant
@@ -302,9 +338,11 @@ __global__ __launch_bounds__(kThreads, (DmaShape<AROW, BROW>::kOcc)) void k_gemm
     };
     // K is a multiple of 64, so a unit has an even number of ticks
     for (int t = 0; t < ticks; t += 2) {
+        if (t % tpp == 0) pc.at_pair(t / tpp);
         tick(std::integral_constant<int, 0>{});
         tick(std::integral_constant<int, 1>{});
     }
+    pc.at_end();
     // the copies issued past the end must land before the workgroup leaves
     // (its LDS may be handed to another workgroup)
     __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
@@ -322,10 +360,61 @@ __global__ __launch_bounds__(kThreads, (DmaShape<AROW, BROW>::kOcc)) void k_gemm
         }
 }
 
+template <bool AROW, bool BROW, bool ANT, bool BNT>
+__global__ __launch_bounds__(kThreads, (DmaShape<AROW, BROW>::kOcc)) void k_gemm_dma(FastArgs g) {
+    // Workgroup -> (unit, row block, column block).  Workgroups are dealt to
+    // the 8 XCDs round-robin; the column blocks of one (unit, row block) take
+    // consecutive slots of one XCD, so they share the A tile in its L2.
+    const int64_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
+    const int64_t grp = (slot / g.nblocks) * 8 + xcd;
+    const int nblk = int(slot % g.nblocks), mblk = int(grp % g.mblocks);
+    const int64_t unit_id = grp / g.mblocks;
+    if (unit_id >= g.hdr->n_units) return;
+    __shared__ __attribute__((aligned(1024))) char lds[DmaShape<AROW, BROW>::kLds];
+    NoPace pc;
+    run_unit<AROW, BROW, ANT, BNT>(g, g.units[unit_id], mblk * kB, nblk * kB, lds, pc);
+}
+
+// Persistent, paced variant for one 128x128 block per key (M = N = 128):
+// `n_wg` workgroups, all resident at once; workgroup b takes units b, b +
+// n_wg, b + 2 n_wg, ... (one per round).  Units of one round start together,
+// and pacing keeps the workgroups of an XCD within a few windows of the
+// reused operand, so its tiles stay in that XCD's L2 without cutting keys
+// into ranges (no partial tiles).  pace: rounds x 8 x windows counters,
+// zeroed by the host before the launch.
+template <bool AROW, bool BROW, bool ANT, bool BNT>
+__global__ __launch_bounds__(kThreads, (DmaShape<AROW, BROW>::kOcc)) void k_gemm_paced(FastArgs g, int32_t* pace,
+                                                                                      int32_t n_wg, int32_t windows,
+                                                                                      int32_t ahead, int32_t slack_div) {
+    __shared__ __attribute__((aligned(1024))) char lds[DmaShape<AROW, BROW>::kLds];
+    const int64_t n_units = g.hdr->n_units;
+    const int xcd = int(blockIdx.x % 8);
+    for (int64_t round = 0;; round++) {
+        const int64_t unit_id = blockIdx.x + round * n_wg;
+        if (unit_id >= n_units) break;
+        // workgroups of this XCD that have a unit in this round
+        const int64_t left = n_units - round * n_wg - xcd;
+        const int64_t active = min<int64_t>((left + 7) / 8, (n_wg - xcd + 7) / 8);
+        const Unit un = g.units[unit_id];
+        Pace pc;
+        pc.done = pace + (round * 8 + xcd) * windows;
+        pc.ridx = (const const_i32*)(g.ridx + un.p0);
+        pc.n_r = g.n_r;
+        pc.windows = windows;
+        pc.ahead = ahead;
+        pc.thr = int(max<int64_t>(active - active / slack_div, 1));
+        pc.cur = -1;
+        __syncthreads();  // the previous unit's LDS reads are done
+        run_unit<AROW, BROW, ANT, BNT>(g, un, 0, 0, lds, pc);
+    }
+}
+
 }  // namespace
 
-hipError_t launch_gemm_fast(const Plan& p, const Layout& L, char* ws, const void* u_tiles, const void* v_tiles,
-                            float* w_tiles, int64_t n_pairs, int64_t unit_bound, hipStream_t s) {
+namespace {
+
+FastArgs fast_args(const Plan& p, const Layout& L, char* ws, const void* u_tiles, const void* v_tiles,
+                   float* w_tiles) {
     FastArgs g{};
     const int32_t* pu = reinterpret_cast<const int32_t*>(ws + L.pu);
     const int32_t* pv = reinterpret_cast<const int32_t*>(ws + L.pv);
@@ -343,29 +432,76 @@ hipError_t launch_gemm_fast(const Plan& p, const Layout& L, char* ws, const void
     const int64_t M = p.swap ? p.nN : p.nM, N = p.swap ? p.nM : p.nN;
     g.mblocks = int32_t(M / kB);
     g.nblocks = int32_t(N / kB);
+    g.ridx = pu;
+    g.n_r = L.n_u;
     g.units = reinterpret_cast<const Unit*>(ws + L.unit_desc);
     g.hdr = reinterpret_cast<const WsHeader*>(ws + L.hdr);
     g.W = w_tiles;
     g.partials = reinterpret_cast<float*>(ws + L.partials);
+    return g;
+}
+
+// kernel variant: operand layouts, and which operand is streamed (each tile
+// used by about one pair, so its copies carry the non-temporal hint)
+int fast_variant(const Plan& p, const Layout& L, int64_t n_pairs) {
+    const int64_t n_a = p.swap ? L.n_v : L.n_u, n_b = p.swap ? L.n_u : L.n_v;
+    const bool ant = 2 * n_a >= n_pairs, bnt = 2 * n_b >= n_pairs;
+    return (p.fast_a_rowfast ? 8 : 0) | (p.fast_b_rowfast ? 4 : 0) | (ant ? 2 : 0) | (bnt ? 1 : 0);
+}
+
+}  // namespace
+
+hipError_t launch_gemm_fast(const Plan& p, const Layout& L, char* ws, const void* u_tiles, const void* v_tiles,
+                            float* w_tiles, int64_t n_pairs, int64_t unit_bound, hipStream_t s) {
+    const FastArgs g = fast_args(p, L, ws, u_tiles, v_tiles, w_tiles);
     const int64_t groups = unit_bound * g.mblocks;
     const int64_t blocks = (groups + 7) / 8 * 8 * g.nblocks;
     if (blocks > int64_t(0x7fffffff)) return hipErrorInvalidConfiguration;
     dim3 grid{unsigned(blocks), 1u, 1u};
-    // an operand whose tiles are each used by about one pair is streamed
-    const int64_t n_a = p.swap ? L.n_v : L.n_u, n_b = p.swap ? L.n_u : L.n_v;
-    const bool ant = 2 * n_a >= n_pairs, bnt = 2 * n_b >= n_pairs;
-    const int sel = (p.fast_a_rowfast ? 8 : 0) | (p.fast_b_rowfast ? 4 : 0) | (ant ? 2 : 0) | (bnt ? 1 : 0);
 #define TRE_FAST_CASE(X)                                                                                   \
     case X:                                                                                                \
         k_gemm_dma<bool(X & 8), bool(X & 4), bool(X & 2), bool(X & 1)><<<grid, kThreads, 0, s>>>(g); \
         break;
-    switch (sel) {
+    switch (fast_variant(p, L, n_pairs)) {
         TRE_FAST_CASE(0) TRE_FAST_CASE(1) TRE_FAST_CASE(2) TRE_FAST_CASE(3)
         TRE_FAST_CASE(4) TRE_FAST_CASE(5) TRE_FAST_CASE(6) TRE_FAST_CASE(7)
         TRE_FAST_CASE(8) TRE_FAST_CASE(9) TRE_FAST_CASE(10) TRE_FAST_CASE(11)
         TRE_FAST_CASE(12) TRE_FAST_CASE(13) TRE_FAST_CASE(14) TRE_FAST_CASE(15)
     }
 #undef TRE_FAST_CASE
+    return hipGetLastError();
+}
+
+int64_t gemm_paced_slots(const Plan& p) {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+        return 0;
+    const int occ = (p.fast_a_rowfast || p.fast_b_rowfast) ? 2 : 1;  // 80 / 64 KB vs 96 KB of LDS
+    return int64_t(cus) * occ;
+}
+
+hipError_t launch_gemm_paced(const Plan& p, const Layout& L, char* ws, const void* u_tiles, const void* v_tiles,
+                             float* w_tiles, int64_t n_pairs, int64_t n_wg, int32_t windows, hipStream_t s) {
+    const FastArgs g = fast_args(p, L, ws, u_tiles, v_tiles, w_tiles);
+    if (g.mblocks != 1 || g.nblocks != 1 || n_wg <= 0 || n_wg > int64_t(0x7fffffff)) return hipErrorInvalidValue;
+    int32_t* pace = reinterpret_cast<int32_t*>(ws + L.pace);
+    // a workgroup waits until 3/4 of its XCD's peers have left the window
+    // before the one it enters
+    constexpr int32_t kAhead = 0, kSlackDiv = 4;
+    dim3 grid{unsigned(n_wg), 1u, 1u};
+#define TRE_PACED_CASE(X)                                                                                      \
+    case X:                                                                                                    \
+        k_gemm_paced<bool(X & 8), bool(X & 4), bool(X & 2), bool(X & 1)><<<grid, kThreads, 0, s>>>(           \
+            g, pace, int32_t(n_wg), windows, kAhead, kSlackDiv);                                               \
+        break;
+    switch (fast_variant(p, L, n_pairs)) {
+        TRE_PACED_CASE(0) TRE_PACED_CASE(1) TRE_PACED_CASE(2) TRE_PACED_CASE(3)
+        TRE_PACED_CASE(4) TRE_PACED_CASE(5) TRE_PACED_CASE(6) TRE_PACED_CASE(7)
+        TRE_PACED_CASE(8) TRE_PACED_CASE(9) TRE_PACED_CASE(10) TRE_PACED_CASE(11)
+        TRE_PACED_CASE(12) TRE_PACED_CASE(13) TRE_PACED_CASE(14) TRE_PACED_CASE(15)
+    }
+#undef TRE_PACED_CASE
     return hipGetLastError();
 }
 

@@ -419,6 +419,7 @@ Layout make_layout(const Plan& p, int64_t n_u, int64_t n_v, int64_t max_pairs) {
     L.part_off = take(sizeof(int32_t) * size_t(P + 1));
     L.split_list = take(sizeof(int32_t) * size_t(P + 1));
     L.tables = take(sizeof(int32_t) * size_t(p.table_total));
+    L.pace = take((p.kclass == KC_GEMM && p.fast) ? sizeof(int32_t) * size_t(kPaceCounters) : 0);
     L.partials = take(sizeof(float) * size_t(cap) * size_t(p.tile_elems[2]));
     L.total = off;
     return L;

@@ -13,6 +13,7 @@ namespace tre {
 
 constexpr int kMaxDims = 8;
 constexpr int kMaxURanges = 64;
+constexpr int64_t kPaceCounters = int64_t(1) << 20;  // int32 pacing counters in the workspace
 
 // Row-major index decomposition: index x over sizes (last fastest) maps to
 // sum_i coord_i(x) * stride_i.  Used to build per-role offset tables.
@@ -88,7 +89,7 @@ struct Layout {
     int64_t n_u = 0, n_v = 0, max_pairs = 0;
     int64_t part_cap = 0;  // partial tiles
     size_t hdr, vjk, vjk_alt, vperm, vperm_alt, ucnt, ulo, scan_tmp, pu, pv, pu_alt, pv_alt, wk, wk_alt, pidx,
-        pidx_alt, hist, flags, seg_start, seg_key, unit_desc, seg_units, part_off, split_list, tables, partials;
+        pidx_alt, hist, flags, seg_start, seg_key, unit_desc, seg_units, part_off, split_list, tables, pace, partials;
     size_t total = 0;
 };
 
@@ -155,6 +156,12 @@ hipError_t launch_contract(const Plan& p, const Layout& L, char* ws, const void*
                            float* w_tiles, int64_t n_pairs, int64_t n_w, int64_t unit_bound, hipStream_t s);
 hipError_t launch_gemm_fast(const Plan& p, const Layout& L, char* ws, const void* u_tiles, const void* v_tiles,
                             float* w_tiles, int64_t n_pairs, int64_t unit_bound, hipStream_t s);
+// Persistent paced variant (one unit per key, one 128x128 block per W tile):
+// n_wg workgroups, all resident at once; pacing counters in L.pace, zeroed by
+// the caller (rounds x 8 x windows int32, rounds = ceil(n_units / n_wg)).
+int64_t gemm_paced_slots(const Plan& p);
+hipError_t launch_gemm_paced(const Plan& p, const Layout& L, char* ws, const void* u_tiles, const void* v_tiles,
+                             float* w_tiles, int64_t n_pairs, int64_t n_wg, int32_t windows, hipStream_t s);
 hipError_t launch_reduce(const Plan& p, const Layout& L, char* ws, float* w_tiles, int64_t split_bound,
                          hipStream_t s);
 hipError_t launch_write_outputs(const Plan& p, const Layout& L, char* ws, int32_t* w_keys, int32_t* pairs_out,

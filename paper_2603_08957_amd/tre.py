@@ -39,7 +39,8 @@ class TreError(RuntimeError):
 
 class Options(ctypes.Structure):
     _fields_ = [("validate_keys", ctypes.c_int32), ("max_pairs_per_unit", ctypes.c_int32),
-                ("u_ranges", ctypes.c_int32), ("reserved", ctypes.c_int32 * 5)]
+                ("u_ranges", ctypes.c_int32), ("pace_windows", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 4)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -128,7 +129,7 @@ class Plan:
     """A parsed, classified binary EinSum (host object, see tre_plan)."""
 
     def __init__(self, einsum: str, upper: str, extents: dict, tiles: dict, dtype: str = "f32",
-                 validate: bool = True, max_pairs_per_unit: int = 0, u_ranges: int = 0):
+                 validate: bool = True, max_pairs_per_unit: int = 0, u_ranges: int = 0, pace_windows: int = 0):
         L = lib()
         ext = np.zeros(26, dtype=np.int64)
         til = np.ones(26, dtype=np.int32)
@@ -136,7 +137,7 @@ class Plan:
             ext[ord(k) - 97] = v
         for k, v in (tiles or {}).items():
             til[ord(k) - 97] = v
-        opt = Options(int(validate), int(max_pairs_per_unit), int(u_ranges))
+        opt = Options(int(validate), int(max_pairs_per_unit), int(u_ranges), int(pace_windows))
         h = ctypes.c_void_p(0)
         rc = L.tre_plan(einsum.encode(), upper.encode(), ext.ctypes.data_as(ctypes.c_void_p),
                         til.ctypes.data_as(ctypes.c_void_p), DTYPE[dtype], ctypes.byref(opt), ctypes.byref(h))

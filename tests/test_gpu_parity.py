@@ -133,6 +133,26 @@ def test_fast_path_gpu(orc, idx, pmax, ur):
     check(out, orc.run(orc_plan(orc, spec), U, V), "bf16")
 
 
+@pytest.mark.parametrize("idx", [0, 2])
+@pytest.mark.parametrize("windows", [1, 3, 64])
+def test_paced_path_gpu(orc, idx, windows):
+    """Persistent paced bf16 kernel (one 128x128 block per W tile): whole keys
+    per workgroup, rounds of units, pacing over windows of U index; the result
+    must not depend on the window count."""
+    import paper_2603_08957_amd as tre
+
+    e, upper, ext, til = FAST_PLANS[idx]
+    rng = np.random.default_rng(177 + idx)
+    u_lab, v_lab, _ = split_einsum(e)
+    U = workloads.random_relation(rng, u_lab, upper, ext, til, "bf16", keep=0.6, zero_frac=0.05)
+    V = workloads.random_relation(rng, v_lab, upper, ext, til, "bf16", keep=0.6, zero_frac=0.05)
+    spec = workloads.spec(e, upper, ext, til, "bf16")
+    assert tre.Plan(e, upper, ext, til, "bf16").kernel_class == "gemm128"
+    say("paced path", idx, windows, e, len(U["keys"]), len(V["keys"]))
+    _, out = gpu_run(spec, U, V, pace_windows=windows)
+    check(out, orc.run(orc_plan(orc, spec), U, V), "bf16")
+
+
 @pytest.mark.parametrize("pmax", [1, 2, 3, 7])
 def test_split_segments_gpu(orc, pmax):
     """Forcing short work units splits every key's pairs; the segmented sum of
