@@ -181,7 +181,7 @@ class GnnChain:
                 "einsums": [w["E1"]["einsum"] + " upper " + w["E1"]["upper"],
                             w["E2"]["einsum"] + " upper " + w["E2"]["upper"]]}
 
-    def oracle_sample(self, orc, n_keys_e1=4, n_keys_e2=64):
+    def oracle_sample(self, orc, n_keys_e1=20, n_keys_e2=64):
         """Time the oracle on a bounded sample: n_keys_e1 output keys of E1 and
         n_keys_e2 of E2 (seeded choice), restricted to the tuples that feed them."""
         w = self.w
