@@ -1,0 +1,49 @@
+"""Host-side checks of bench.py: the one-GPU rule and the counter-traffic record."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+
+
+@pytest.fixture
+def bench(monkeypatch):
+    import bench as b
+
+    monkeypatch.setattr(b, "PLAN_OPTIONS", {"u_ranges": 0, "pace_windows": 0})
+    return b
+
+
+def test_traffic_record_matches_kernel_source(bench):
+    rec = bench.traffic_record(2)
+    assert rec is not None, "profile record should match the committed kernel source"
+    assert rec["bytes"] == rec["read_bytes"] + rec["write_bytes"]
+    # the record is for the default workload only, and only with default options
+    assert bench.traffic_record(3) is None
+    bench.PLAN_OPTIONS["u_ranges"] = 8
+    assert bench.traffic_record(2) is None
+
+
+def test_traffic_record_null_after_kernel_change(bench, tmp_path, monkeypatch):
+    name = bench.TRAFFIC_RECORDS[2]
+    text = open(os.path.join(ROOT, "profiles", name)).read()
+    rec = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
+    rec["kernel_source_sha256"] = "0" * 64
+    (tmp_path / "profiles").mkdir()
+    (tmp_path / "profiles" / name).write_text("```json\n" + json.dumps(rec) + "\n```\n")
+    src_dir = tmp_path / os.path.dirname(rec["kernel_source"])
+    src_dir.mkdir(parents=True)
+    (tmp_path / rec["kernel_source"]).write_bytes(open(os.path.join(ROOT, rec["kernel_source"]), "rb").read())
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.traffic_record(2) is None
