@@ -13,10 +13,13 @@
 // element offsets inside a tile come from per-role tables, so any label
 // order / layout of the operand tiles is accepted.
 //   KC_GEMM: 64x64 output block per 256-thread workgroup (2x2 waves of one
-//            32x32 MFMA tile each), 32-deep K chunks staged in LDS;
+//            32x32 MFMA tile each), 32-deep K chunks staged in LDS, the next
+//            two chunks' global loads in flight in registers;
 //            fp32 -> v_mfma_f32_32x32x2_f32, bf16 -> v_mfma_f32_32x32x16_bf16.
 //   KC_VEC : one output element per thread, fp32 FMA (scale, GEMV, dot).
 #include "tre_internal.h"
+
+#include <type_traits>
 
 namespace tre {
 
@@ -155,11 +158,14 @@ struct GemmArgs {
 
 constexpr int kBM = 64, kBN = 64, kBK = 32;
 
+// LDS row pitches (elements).  fp32 [row][k] rows of 36 floats are 16-byte
+// aligned and a 16-lane b128 read of 16 rows at one k offset hits 16
+// distinct 4-bank groups; [k][row] rows are padded by one element.
 template <typename T>
 struct LdsPitch;
 template <>
 struct LdsPitch<float> {
-    static constexpr int kfast = kBK + 1;   // [row][k]
+    static constexpr int kfast = kBK + 4;   // [row][k]
     static constexpr int rfast = kBM + 1;   // [k][row]
 };
 template <>
@@ -179,43 +185,54 @@ __device__ inline void load8(uint16_t* v, const uint16_t* src) {
     __builtin_memcpy(v, &a, 16);
 }
 
-// Stage a 64 x 32 (rows x k) chunk of one operand into LDS.
+// One thread's share (8 elements) of a 64 x 32 (rows x k) chunk of one
+// operand, held in registers between its global load and its LDS store so
+// the next chunk's loads overlap the current chunk's MFMAs.
 //   KF: the operand's unit-stride dim is k (LDS [row][k]); else rows ([k][row]).
 template <typename T, bool KF>
-__device__ inline void stage(T* __restrict__ lds, const T* __restrict__ base, const int32_t* __restrict__ tR,
-                             const int32_t* __restrict__ tK, int r0, int R, int k0, int K, bool vec) {
-    const int t = threadIdx.x;
-    if (KF) {
-        const int r = t >> 2, ks = (t & 3) * 8;
-        const int gr = r0 + r, gk = k0 + ks;
-        T v[8];
-        if (vec && gr < R && gk + 8 <= K) {
-            load8(v, base + tR[gr] + tK[gk]);
+struct Staged {
+    T v[8];
+    // tR: element offsets of the block's rows (local index, rows < nr valid);
+    // tK: offsets of the contracted index (both tables in LDS)
+    __device__ void load(const T* __restrict__ base, const int32_t* tR, const int32_t* tK, int nr, int k0, int K,
+                         bool vec) {
+        const int t = threadIdx.x;
+        if (KF) {
+            const int lr = t >> 2, gk = k0 + (t & 3) * 8;
+            if (vec && lr < nr && gk + 8 <= K) {
+                load8(v, base + tR[lr] + tK[gk]);
+            } else {
+#pragma unroll
+                for (int j = 0; j < 8; j++) v[j] = (lr < nr && gk + j < K) ? base[tR[lr] + tK[gk + j]] : T(0);
+            }
         } else {
+            const int gk = k0 + (t >> 3), lr = (t & 7) * 8;
+            if (vec && gk < K && lr + 8 <= nr) {
+                load8(v, base + tK[gk] + tR[lr]);
+            } else {
 #pragma unroll
-            for (int j = 0; j < 8; j++) v[j] = (gr < R && gk + j < K) ? base[tR[gr] + tK[gk + j]] : T(0);
+                for (int j = 0; j < 8; j++) v[j] = (gk < K && lr + j < nr) ? base[tK[gk] + tR[lr + j]] : T(0);
+            }
         }
-#pragma unroll
-        for (int j = 0; j < 8; j++) lds[r * LdsPitch<T>::kfast + ks + j] = v[j];
-    } else {
-        const int k = t >> 3, rs = (t & 7) * 8;
-        const int gk = k0 + k, gr = r0 + rs;
-        T v[8];
-        if (vec && gk < K && gr + 8 <= R) {
-            load8(v, base + tK[gk] + tR[gr]);
-        } else {
-#pragma unroll
-            for (int j = 0; j < 8; j++) v[j] = (gk < K && gr + j < R) ? base[tK[gk] + tR[gr + j]] : T(0);
-        }
-#pragma unroll
-        for (int j = 0; j < 8; j++) lds[k * LdsPitch<T>::rfast + rs + j] = v[j];
     }
-}
-
-template <typename T, bool KF>
-__device__ inline T lds_at(const T* lds, int row, int k) {
-    return KF ? lds[row * LdsPitch<T>::kfast + k] : lds[k * LdsPitch<T>::rfast + row];
-}
+    __device__ void store(T* __restrict__ lds) const {
+        const int t = threadIdx.x;
+        if (KF) {
+            T* d = lds + (t >> 2) * LdsPitch<T>::kfast + (t & 3) * 8;
+            if constexpr (sizeof(T) == 4) {
+                reinterpret_cast<f32x4*>(d)[0] = f32x4{v[0], v[1], v[2], v[3]};
+                reinterpret_cast<f32x4*>(d)[1] = f32x4{v[4], v[5], v[6], v[7]};
+            } else {
+#pragma unroll
+                for (int j = 0; j < 8; j++) d[j] = v[j];
+            }
+        } else {
+            T* d = lds + (t >> 3) * LdsPitch<T>::rfast + (t & 7) * 8;
+#pragma unroll
+            for (int j = 0; j < 8; j++) d[j] = v[j];
+        }
+    }
+};
 
 template <bool KF>
 __device__ inline bf16x8 frag_bf16(const uint16_t* lds, int row, int k) {
@@ -229,7 +246,20 @@ __device__ inline bf16x8 frag_bf16(const uint16_t* lds, int row, int k) {
     return __builtin_bit_cast(bf16x8, v);
 }
 
-template <typename T, bool AK, bool BK>
+// fp32 operand values of 4 consecutive MFMA k-steps (k = k4 .. k4 + 3) for
+// the lane's row: one 16-byte read from [row][k], four reads from [k][row].
+template <bool KF>
+__device__ inline f32x4 frag4_f32(const float* lds, int row, int k4) {
+    if (KF) return *reinterpret_cast<const f32x4*>(lds + row * LdsPitch<float>::kfast + k4);
+    f32x4 v;
+#pragma unroll
+    for (int j = 0; j < 4; j++) v[j] = lds[(k4 + j) * LdsPitch<float>::rfast + row];
+    return v;
+}
+
+// PF: load two chunks ahead (worth it for long units; short units keep the
+// registers and get more workgroups per CU instead).
+template <typename T, bool AK, bool BK, bool PF>
 __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs g) {
     const int unit_id = blockIdx.x;
     if (unit_id >= g.hdr->n_units) return;
@@ -241,8 +271,10 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs g) {
     const int b = y / g.mblocks;
     const int m0 = mblk * kBM, n0 = nblk * kBN;
 
-    __shared__ __attribute__((aligned(16))) T As[AK ? kBM * LdsPitch<T>::kfast : kBK * LdsPitch<T>::rfast];
-    __shared__ __attribute__((aligned(16))) T Bs[BK ? kBN * LdsPitch<T>::kfast : kBK * LdsPitch<T>::rfast];
+    constexpr int kAs = AK ? kBM * LdsPitch<T>::kfast : kBK * LdsPitch<T>::rfast;
+    constexpr int kBs = BK ? kBN * LdsPitch<T>::kfast : kBK * LdsPitch<T>::rfast;
+    __shared__ __attribute__((aligned(16))) T As[kAs];
+    __shared__ __attribute__((aligned(16))) T Bs[kBs];
 
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int wm = w >> 1, wn = w & 1;
@@ -250,34 +282,73 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs g) {
 #pragma unroll
     for (int r = 0; r < 16; r++) acc[r] = 0.f;
 
+    // offset tables of this block's rows and of the contracted index, copied
+    // to LDS once so the loads of the chunk loop depend on no global read
+    extern __shared__ int32_t tabs[];  // [kBM rows of A][kBN rows of B][K of A][K of B]
+    int32_t* sAM = tabs;
+    int32_t* sBN = tabs + kBM;
+    int32_t* sAK = tabs + kBM + kBN;
+    int32_t* sBK = sAK + g.K;
+    for (int i = threadIdx.x; i < kBM; i += kThreads) sAM[i] = m0 + i < g.M ? g.tAM[m0 + i] : 0;
+    for (int i = threadIdx.x; i < kBN; i += kThreads) sBN[i] = n0 + i < g.N ? g.tBN[n0 + i] : 0;
+    for (int i = threadIdx.x; i < g.K; i += kThreads) {
+        sAK[i] = g.tAK[i];
+        sBK[i] = g.tBK[i];
+    }
+    __syncthreads();
+    const int nra = min(kBM, g.M - m0), nrb = min(kBN, g.N - n0);
+
     const T* Ag = reinterpret_cast<const T*>(g.A);
     const T* Bg = reinterpret_cast<const T*>(g.B);
     const int32_t offAB = g.tAB[b], offBB = g.tBB[b];
-    for (int p = un.p0; p < un.p1; p++) {
-        const T* Ab = Ag + int64_t(g.pa[p]) * g.a_elems + offAB;
-        const T* Bb = Bg + int64_t(g.pb[p]) * g.b_elems + offBB;
-        for (int k0 = 0; k0 < g.K; k0 += kBK) {
-            stage<T, AK>(As, Ab, g.tAM, g.tAK, m0, g.M, k0, g.K, g.vec_a);
-            stage<T, BK>(Bs, Bb, g.tBN, g.tBK, n0, g.N, k0, g.K, g.vec_b);
-            __syncthreads();
-            const int row = lane & 31, half = lane >> 5;
-            if constexpr (sizeof(T) == 4) {
+    // chunk c of the unit: pair p0 + c / kcn, k offset (c % kcn) * kBK; with
+    // PF two chunks are loaded ahead into two register sets used alternately
+    // (the LDS tile stays single, so many workgroups fit on a CU)
+    const int kcn = (g.K + kBK - 1) / kBK;
+    const int total = (un.p1 - un.p0) * kcn;
+    Staged<T, AK> sa[PF ? 2 : 1];
+    Staged<T, BK> sb[PF ? 2 : 1];
+    auto load = [&](int c, auto slot) {
+        constexpr int q = decltype(slot)::value;
+        const int p = un.p0 + c / kcn, k0 = (c % kcn) * kBK;
+        sa[q].load(Ag + int64_t(g.pa[p]) * g.a_elems + offAB, sAM, sAK, nra, k0, g.K, g.vec_a);
+        sb[q].load(Bg + int64_t(g.pb[p]) * g.b_elems + offBB, sBN, sBK, nrb, k0, g.K, g.vec_b);
+    };
+    const int row = lane & 31, half = lane >> 5;
+    auto step = [&](int c, auto slot) {
+        constexpr int q = decltype(slot)::value;
+        if (!PF) load(c, slot);
+        sa[q].store(As);
+        sb[q].store(Bs);
+        __syncthreads();
+        if (PF && c + 2 < total) load(c + 2, slot);
+        if constexpr (sizeof(T) == 4) {
+            // k-steps are taken in the order k = 16 half + s (s = 0 .. 15) in
+            // both operands, so a lane's k run is contiguous
 #pragma unroll
-                for (int ks = 0; ks < kBK; ks += 2) {
-                    float a = lds_at<T, AK>(As, wm * 32 + row, ks + half);
-                    float bb = lds_at<T, BK>(Bs, wn * 32 + row, ks + half);
-                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, bb, acc, 0, 0, 0);
-                }
-            } else {
+            for (int s4 = 0; s4 < kBK / 2; s4 += 4) {
+                const f32x4 a = frag4_f32<AK>(As, wm * 32 + row, 16 * half + s4);
+                const f32x4 bb = frag4_f32<BK>(Bs, wn * 32 + row, 16 * half + s4);
 #pragma unroll
-                for (int ks = 0; ks < kBK; ks += 16) {
-                    bf16x8 a = frag_bf16<AK>(reinterpret_cast<const uint16_t*>(As), wm * 32 + row, ks + half * 8);
-                    bf16x8 bb = frag_bf16<BK>(reinterpret_cast<const uint16_t*>(Bs), wn * 32 + row, ks + half * 8);
-                    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bb, acc, 0, 0, 0);
-                }
+                for (int j = 0; j < 4; j++) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[j], bb[j], acc, 0, 0, 0);
             }
-            __syncthreads();
+        } else {
+#pragma unroll
+            for (int ks = 0; ks < kBK; ks += 16) {
+                bf16x8 a = frag_bf16<AK>(reinterpret_cast<const uint16_t*>(As), wm * 32 + row, ks + half * 8);
+                bf16x8 bb = frag_bf16<BK>(reinterpret_cast<const uint16_t*>(Bs), wn * 32 + row, ks + half * 8);
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bb, acc, 0, 0, 0);
+            }
         }
+        __syncthreads();
+    };
+    using S0 = std::integral_constant<int, 0>;
+    using S1 = std::integral_constant<int, PF ? 1 : 0>;
+    if (PF && total > 0) load(0, S0{});
+    if (PF && total > 1) load(1, S1{});
+    for (int c = 0; c < total; c += 2) {
+        step(c, S0{});
+        if (c + 1 < total) step(c + 1, S1{});
     }
     float* out = un.slot < 0 ? g.W + int64_t(un.seg) * g.w_elems : g.partials + int64_t(un.slot) * g.w_elems;
     out += g.tWB[b];
@@ -473,13 +544,24 @@ __global__ void k_write_pairs(const int32_t* __restrict__ pu, const int32_t* __r
 
 inline unsigned blocks_for(int64_t n) { return unsigned((n + kThreads - 1) / kThreads); }
 
-template <typename T>
+template <typename T, bool PF>
 hipError_t gemm_dispatch(const Plan& p, const GemmArgs& g, dim3 grid, hipStream_t s) {
-    if (p.a_kfast && p.b_kfast) k_gemm<T, true, true><<<grid, kThreads, 0, s>>>(g);
-    else if (p.a_kfast) k_gemm<T, true, false><<<grid, kThreads, 0, s>>>(g);
-    else if (p.b_kfast) k_gemm<T, false, true><<<grid, kThreads, 0, s>>>(g);
-    else k_gemm<T, false, false><<<grid, kThreads, 0, s>>>(g);
+    const size_t tab = sizeof(int32_t) * size_t(kBM + kBN + 2 * int64_t(g.K));
+    if (tab > 96 * 1024) return hipErrorInvalidConfiguration;
+    if (p.a_kfast && p.b_kfast) k_gemm<T, true, true, PF><<<grid, kThreads, tab, s>>>(g);
+    else if (p.a_kfast) k_gemm<T, true, false, PF><<<grid, kThreads, tab, s>>>(g);
+    else if (p.b_kfast) k_gemm<T, false, true, PF><<<grid, kThreads, tab, s>>>(g);
+    else k_gemm<T, false, false, PF><<<grid, kThreads, tab, s>>>(g);
     return hipGetLastError();
+}
+
+// Prefetch pays when units run many K chunks (pairs per unit x chunks per pair).
+template <typename T>
+hipError_t gemm_dispatch(const Plan& p, const GemmArgs& g, dim3 grid, int64_t n_pairs, int64_t n_units,
+                         hipStream_t s) {
+    const int64_t chunks = (p.nK + kBK - 1) / kBK;
+    const bool pf = n_pairs * chunks >= 4 * std::max<int64_t>(n_units, 1);
+    return pf ? gemm_dispatch<T, true>(p, g, grid, s) : gemm_dispatch<T, false>(p, g, grid, s);
 }
 
 }  // namespace
@@ -532,7 +614,6 @@ hipError_t launch_range_units(const Plan& p, const Layout& L, char* ws, int64_t 
 
 hipError_t launch_contract(const Plan& p, const Layout& L, char* ws, const void* u_tiles, const void* v_tiles,
                            float* w_tiles, int64_t n_pairs, int64_t n_w, int64_t unit_bound, hipStream_t s) {
-    (void)n_pairs;
     (void)n_w;
     if (unit_bound <= 0) return hipSuccess;
     const int32_t* tb = reinterpret_cast<const int32_t*>(ws + L.tables);
@@ -576,7 +657,8 @@ hipError_t launch_contract(const Plan& p, const Layout& L, char* ws, const void*
         const int64_t gy = int64_t(g.nB) * g.mblocks * g.nblocks;
         if (gy > 65535) return hipErrorInvalidConfiguration;
         dim3 grid{unsigned(unit_bound), unsigned(gy), 1u};
-        return p.dtype == TRE_BF16 ? gemm_dispatch<uint16_t>(p, g, grid, s) : gemm_dispatch<float>(p, g, grid, s);
+        return p.dtype == TRE_BF16 ? gemm_dispatch<uint16_t>(p, g, grid, n_pairs, unit_bound, s)
+                                   : gemm_dispatch<float>(p, g, grid, n_pairs, unit_bound, s);
     }
     VecArgs a{};
     a.U = u_tiles;
