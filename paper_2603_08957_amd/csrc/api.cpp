@@ -1,6 +1,7 @@
 // C-ABI entry points: argument checks, workspace layout, phase ordering,
 // the two count read-backs of the join, capacity checks and timing.
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 
 #include "tre_internal.h"
@@ -10,7 +11,7 @@ using namespace tre;
 namespace {
 
 constexpr uint64_t kMagic = 0x7472655f6a6f696eull;  // "tre_join"
-constexpr int kTargetWorkgroups = 1024;              // 4 per CU on 256 CUs
+constexpr int kTargetWorkgroups = 2048;              // 8 per CU on 256 CUs
 
 tre_status dev_fail(hipError_t e, const char* where) {
     set_error(std::string(where) + ": " + hipGetErrorString(e));
@@ -123,15 +124,26 @@ int32_t choose_pacing(const Plan& p, int64_t n_u, int64_t n_pairs, int64_t n_w, 
     return int32_t(W);
 }
 
+// Workgroups one unit occupies: its output blocks (GEMM), or its threads /
+// 256 for the vector class (several small units share a workgroup).
+double unit_workgroups(const Plan& p) {
+    if (p.kclass == KC_GEMM) return double(blocks_per_unit(p));
+    const int64_t threads = (p.tile_elems[2] + p.vec_ept - 1) / p.vec_ept;
+    if (threads > 128) return double((threads + 255) / 256);
+    int64_t t = 1;
+    while (t < threads) t <<= 1;
+    return double(t) / 256.0;
+}
+
 int64_t choose_unit(const Plan& p, const Layout& L, int64_t n_pairs, int64_t n_w) {
-    const int64_t bpu = blocks_per_unit(p);
+    const double uw = unit_workgroups(p);
     int64_t pu;
     if (p.opt.max_pairs_per_unit > 0) {
         pu = p.opt.max_pairs_per_unit;
-    } else if (n_w * bpu >= kTargetWorkgroups) {
+    } else if (double(n_w) * uw >= kTargetWorkgroups) {
         pu = std::max<int64_t>(n_pairs, 1);  // enough output blocks: one unit per key
     } else {
-        pu = std::max<int64_t>(4, (n_pairs * bpu + kTargetWorkgroups - 1) / kTargetWorkgroups);
+        pu = std::max<int64_t>(4, int64_t(std::ceil(double(n_pairs) * uw / kTargetWorkgroups)));
     }
     // partial tiles of split keys must fit: at most 2 * n_pairs / pu of them
     const int64_t need = (2 * n_pairs + L.part_cap - 2) / std::max<int64_t>(L.part_cap - 1, 1);
