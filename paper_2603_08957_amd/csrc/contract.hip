@@ -261,9 +261,8 @@ __device__ inline f32x4 frag4_f32(const float* lds, int row, int k4) {
 // registers and get more workgroups per CU instead).
 template <typename T, bool AK, bool BK, bool PF>
 __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs g) {
-    const int unit_id = blockIdx.x;
-    if (unit_id >= g.hdr->n_units) return;
-    const Unit un = g.units[unit_id];
+    const int64_t n_units = g.hdr->n_units;
+    if (blockIdx.x >= n_units) return;
     int y = blockIdx.y;
     const int nblk = y % g.nblocks;
     y /= g.nblocks;
@@ -301,62 +300,81 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs g) {
     const T* Ag = reinterpret_cast<const T*>(g.A);
     const T* Bg = reinterpret_cast<const T*>(g.B);
     const int32_t offAB = g.tAB[b], offBB = g.tBB[b];
-    // chunk c of the unit: pair p0 + c / kcn, k offset (c % kcn) * kBK; with
-    // PF two chunks are loaded ahead into two register sets used alternately
-    // (the LDS tile stays single, so many workgroups fit on a CU)
-    const int kcn = (g.K + kBK - 1) / kBK;
-    const int total = (un.p1 - un.p0) * kcn;
-    Staged<T, AK> sa[PF ? 2 : 1];
-    Staged<T, BK> sb[PF ? 2 : 1];
-    auto load = [&](int c, auto slot) {
-        constexpr int q = decltype(slot)::value;
-        const int p = un.p0 + c / kcn, k0 = (c % kcn) * kBK;
-        sa[q].load(Ag + int64_t(g.pa[p]) * g.a_elems + offAB, sAM, sAK, nra, k0, g.K, g.vec_a);
-        sb[q].load(Bg + int64_t(g.pb[p]) * g.b_elems + offBB, sBN, sBK, nrb, k0, g.K, g.vec_b);
-    };
-    const int row = lane & 31, half = lane >> 5;
-    auto step = [&](int c, auto slot) {
-        constexpr int q = decltype(slot)::value;
-        if (!PF) load(c, slot);
-        sa[q].store(As);
-        sb[q].store(Bs);
-        __syncthreads();
-        if (PF && c + 2 < total) load(c + 2, slot);
-        if constexpr (sizeof(T) == 4) {
-            // k-steps are taken in the order k = 16 half + s (s = 0 .. 15) in
-            // both operands, so a lane's k run is contiguous
-#pragma unroll
-            for (int s4 = 0; s4 < kBK / 2; s4 += 4) {
-                const f32x4 a = frag4_f32<AK>(As, wm * 32 + row, 16 * half + s4);
-                const f32x4 bb = frag4_f32<BK>(Bs, wn * 32 + row, 16 * half + s4);
-#pragma unroll
-                for (int j = 0; j < 4; j++) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[j], bb[j], acc, 0, 0, 0);
-            }
-        } else {
-#pragma unroll
-            for (int ks = 0; ks < kBK; ks += 16) {
-                bf16x8 a = frag_bf16<AK>(reinterpret_cast<const uint16_t*>(As), wm * 32 + row, ks + half * 8);
-                bf16x8 bb = frag_bf16<BK>(reinterpret_cast<const uint16_t*>(Bs), wn * 32 + row, ks + half * 8);
-                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bb, acc, 0, 0, 0);
-            }
-        }
-        __syncthreads();
-    };
-    using S0 = std::integral_constant<int, 0>;
-    using S1 = std::integral_constant<int, PF ? 1 : 0>;
-    if (PF && total > 0) load(0, S0{});
-    if (PF && total > 1) load(1, S1{});
-    for (int c = 0; c < total; c += 2) {
-        step(c, S0{});
-        if (c + 1 < total) step(c + 1, S1{});
-    }
-    float* out = un.slot < 0 ? g.W + int64_t(un.seg) * g.w_elems : g.partials + int64_t(un.slot) * g.w_elems;
-    out += g.tWB[b];
+    // output offset of this lane's accumulator r (the block is fixed); short
+    // units (no prefetch) keep them in registers across units
     const int n = n0 + wn * 32 + (lane & 31);
-#pragma unroll
-    for (int r = 0; r < 16; r++) {
+    auto w_offset = [&](int r) {
         const int m = m0 + wm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-        if (m < g.M && n < g.N) out[g.tWM[m] + g.tWN[n]] = acc[r];
+        return (m < g.M && n < g.N) ? g.tWB[b] + g.tWM[m] + g.tWN[n] : -1;
+    };
+    int32_t wofs[PF ? 1 : 16];
+    if constexpr (!PF) {
+#pragma unroll
+        for (int r = 0; r < 16; r++) wofs[r] = w_offset(r);
+    }
+    const int kcn = (g.K + kBK - 1) / kBK;
+    // without prefetch (short units) the grid may be smaller than the unit
+    // count: a workgroup takes units blockIdx.x, blockIdx.x + gridDim.x, ...
+    // (tables loaded once); with prefetch the grid covers every unit
+    const int64_t unit_step = PF ? n_units : int64_t(gridDim.x);
+    for (int64_t unit_id = blockIdx.x; unit_id < n_units; unit_id += unit_step) {
+        const Unit un = g.units[unit_id];
+#pragma unroll
+        for (int r = 0; r < 16; r++) acc[r] = 0.f;
+        // chunk c of the unit: pair p0 + c / kcn, k offset (c % kcn) * kBK; with
+        // PF two chunks are loaded ahead into two register sets used alternately
+        // (the LDS tile stays single, so many workgroups fit on a CU)
+        const int total = (un.p1 - un.p0) * kcn;
+        Staged<T, AK> sa[PF ? 2 : 1];
+        Staged<T, BK> sb[PF ? 2 : 1];
+        auto load = [&](int c, auto slot) {
+            constexpr int q = decltype(slot)::value;
+            const int p = un.p0 + c / kcn, k0 = (c % kcn) * kBK;
+            sa[q].load(Ag + int64_t(g.pa[p]) * g.a_elems + offAB, sAM, sAK, nra, k0, g.K, g.vec_a);
+            sb[q].load(Bg + int64_t(g.pb[p]) * g.b_elems + offBB, sBN, sBK, nrb, k0, g.K, g.vec_b);
+        };
+        const int row = lane & 31, half = lane >> 5;
+        auto step = [&](int c, auto slot) {
+            constexpr int q = decltype(slot)::value;
+            if (!PF) load(c, slot);
+            sa[q].store(As);
+            sb[q].store(Bs);
+            __syncthreads();
+            if (PF && c + 2 < total) load(c + 2, slot);
+            if constexpr (sizeof(T) == 4) {
+                // k-steps are taken in the order k = 16 half + s (s = 0 .. 15) in
+                // both operands, so a lane's k run is contiguous
+#pragma unroll
+                for (int s4 = 0; s4 < kBK / 2; s4 += 4) {
+                    const f32x4 a = frag4_f32<AK>(As, wm * 32 + row, 16 * half + s4);
+                    const f32x4 bb = frag4_f32<BK>(Bs, wn * 32 + row, 16 * half + s4);
+#pragma unroll
+                    for (int j = 0; j < 4; j++) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[j], bb[j], acc, 0, 0, 0);
+                }
+            } else {
+#pragma unroll
+                for (int ks = 0; ks < kBK; ks += 16) {
+                    bf16x8 a = frag_bf16<AK>(reinterpret_cast<const uint16_t*>(As), wm * 32 + row, ks + half * 8);
+                    bf16x8 bb = frag_bf16<BK>(reinterpret_cast<const uint16_t*>(Bs), wn * 32 + row, ks + half * 8);
+                    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bb, acc, 0, 0, 0);
+                }
+            }
+            __syncthreads();
+        };
+        using S0 = std::integral_constant<int, 0>;
+        using S1 = std::integral_constant<int, PF ? 1 : 0>;
+        if (PF && total > 0) load(0, S0{});
+        if (PF && total > 1) load(1, S1{});
+        for (int c = 0; c < total; c += 2) {
+            step(c, S0{});
+            if (c + 1 < total) step(c + 1, S1{});
+        }
+        float* out = un.slot < 0 ? g.W + int64_t(un.seg) * g.w_elems : g.partials + int64_t(un.slot) * g.w_elems;
+#pragma unroll
+        for (int r = 0; r < 16; r++) {
+            const int32_t o = PF ? w_offset(r) : wofs[r];
+            if (o >= 0) out[o] = acc[r];
+        }
     }
 }
 
@@ -546,6 +564,9 @@ inline unsigned blocks_for(int64_t n) { return unsigned((n + kThreads - 1) / kTh
 
 template <typename T, bool PF>
 hipError_t gemm_dispatch(const Plan& p, const GemmArgs& g, dim3 grid, hipStream_t s) {
+    // about 16 workgroups per CU; beyond that a workgroup loops over (short) units
+    constexpr unsigned kGemmGrid = 4096;
+    if (!PF) grid.x = std::min<unsigned>(grid.x, std::max<unsigned>(1, kGemmGrid / grid.y));
     const size_t tab = sizeof(int32_t) * size_t(kBM + kBN + 2 * int64_t(g.K));
     if (tab > 96 * 1024) return hipErrorInvalidConfiguration;
     if (p.a_kfast && p.b_kfast) k_gemm<T, true, true, PF><<<grid, kThreads, tab, s>>>(g);
