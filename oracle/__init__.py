@@ -92,6 +92,9 @@ def lib():
         L.orc_free.restype = None
         L.orc_f32_to_bf16.argtypes = [P, P, i64]
         L.orc_f32_to_bf16.restype = None
+        L.orc_repartition.argtypes = [ctypes.c_char_p, ctypes.c_char_p, ctypes.c_char_p, P, P, P, P, i64, P, P,
+                                      P, P]
+        L.orc_repartition.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -329,3 +332,47 @@ def stack_rows(keys: np.ndarray, tiles: np.ndarray, group: int):
     out = np.zeros((len(uk), group, rows.shape[1]), dtype=rows.dtype)
     out[inv, keys % group] = rows
     return uk.reshape(-1, 1).astype(np.int32), out.reshape(len(uk), -1)
+
+
+def repartition(labels: str, up_in: str, up_out: str, extents: dict, tiles_in: dict, tiles_out: dict,
+                keys: np.ndarray, tiles: np.ndarray):
+    """The same tensor under a second decomposition (Sec. 6: decompose on all
+    labels promoted in either decomposition, then STACK grouped by the
+    target's promoted labels), computed element by element by
+    orc_repartition.  keys int32 [n x r_in]; tiles [n x tile_elems_in] (any
+    real dtype, converted to float64 exactly).  Returns (keys_out int32
+    [n_out x r_out], tiles_out float64 [n_out x tile_elems_out])."""
+    L = lib()
+    ext = np.zeros(26, dtype=np.int64)
+    tin = np.ones(26, dtype=np.int32)
+    tout = np.ones(26, dtype=np.int32)
+    for k, v in extents.items():
+        ext[ord(k) - 97] = v
+    for k, v in (tiles_in or {}).items():
+        tin[ord(k) - 97] = v
+    for k, v in (tiles_out or {}).items():
+        tout[ord(k) - 97] = v
+    n = len(keys)
+    te_in = 1
+    for c in labels:
+        te_in *= int(tin[ord(c) - 97]) if c in up_in else int(ext[ord(c) - 97])
+    keys = np.ascontiguousarray(np.asarray(keys, dtype=np.int32).reshape(n, len(up_in)))
+    vals = np.ascontiguousarray(np.asarray(tiles, dtype=np.float64).reshape(n, te_in) if n else
+                                np.zeros((0, 1), np.float64))
+    n_out = ctypes.c_int64(0)
+    kp = ctypes.c_void_p(0)
+    tp = ctypes.c_void_p(0)
+    rc = L.orc_repartition(labels.encode(), up_in.encode(), up_out.encode(), _ptr(ext), _ptr(tin), _ptr(tout),
+                           _ptr(keys), n, _ptr(vals), ctypes.byref(n_out), ctypes.byref(kp), ctypes.byref(tp))
+    if rc != 0:
+        raise OracleError(rc, "repartition")
+    te_out = 1
+    for c in labels:
+        te_out *= tout[ord(c) - 97] if c in up_out else ext[ord(c) - 97]
+    no = n_out.value
+    r_out = len(up_out)
+    ko = np.ctypeslib.as_array((ctypes.c_int32 * max(no * r_out, 1)).from_address(kp.value))[:no * r_out].copy()
+    to = np.ctypeslib.as_array((ctypes.c_double * max(no * te_out, 1)).from_address(tp.value))[:no * te_out].copy()
+    L.orc_free(kp)
+    L.orc_free(tp)
+    return ko.reshape(no, r_out), to.reshape(no, te_out)

@@ -522,3 +522,167 @@ int orc_eval(const orc_plan *p, const int64_t *ucoo, const double *uval, int64_t
     free(idx);
     return ORC_OK;
 }
+
+/* ------------------------------------------------------ repartition */
+
+/*
+ * orc_repartition -- the same tensor under a second decomposition (Sec. 6,
+ * "changing representation" between two EinSums: decompose every tuple on
+ * all labels promoted in either decomposition, ALLINTS, then re-compose with
+ * the STACK aggregate grouped by the target's promoted labels).
+ *
+ * Written as its plain definition, element by element:
+ *   - the target holds one tuple for every target tile that contains at
+ *     least one position of a source tile (zero values included: a stored
+ *     tile joins like any other, so every position it covers is carried);
+ *   - every target element equals the source element at the same global
+ *     coordinate, and 0 where no source tile covers the coordinate.
+ * labels: the tensor's labels in string order (no repeats).  up_in / up_out:
+ * promoted labels of the two decompositions.  ext[26]: extents; tin / tout
+ * [26]: tile sizes of promoted labels (a demoted label keeps its extent).
+ * Keys are int32 [n x r] in label-string order of the promoted labels.
+ * Tile values are doubles; outputs are malloc'd (free with orc_free).
+ */
+typedef struct {
+    int nl;
+    int lab[26];
+    int64_t ext[26], tin[26], tout[26];   /* per position in `labels` */
+    int pin[26], pout[26];                /* promoted in source / target */
+    int rin, rout;
+    int64_t te_in, te_out;
+} rp_desc;
+
+static int rp_make(const char *labels, const char *up_in, const char *up_out, const int64_t *ext,
+                   const int32_t *tin, const int32_t *tout, rp_desc *d) {
+    memset(d, 0, sizeof(*d));
+    int seen[26] = {0};
+    for (const char *c = labels; *c; c++) {
+        if (*c < 'a' || *c > 'z' || seen[*c - 'a'] || d->nl == 26) return ORC_E_PARSE;
+        seen[*c - 'a'] = 1;
+        d->lab[d->nl++] = *c - 'a';
+    }
+    int inup[26] = {0}, outup[26] = {0};
+    for (const char *c = up_in; *c; c++) {
+        if (*c < 'a' || *c > 'z' || !seen[*c - 'a']) return ORC_E_SPLIT;
+        inup[*c - 'a'] = 1;
+    }
+    for (const char *c = up_out; *c; c++) {
+        if (*c < 'a' || *c > 'z' || !seen[*c - 'a']) return ORC_E_SPLIT;
+        outup[*c - 'a'] = 1;
+    }
+    d->te_in = d->te_out = 1;
+    for (int i = 0; i < d->nl; i++) {
+        int l = d->lab[i];
+        d->ext[i] = ext[l];
+        if (ext[l] < 1) return ORC_E_SHAPE;
+        d->pin[i] = inup[l];
+        d->pout[i] = outup[l];
+        d->tin[i] = inup[l] ? tin[l] : ext[l];
+        d->tout[i] = outup[l] ? tout[l] : ext[l];
+        if (d->tin[i] < 1 || ext[l] % d->tin[i] || d->tout[i] < 1 || ext[l] % d->tout[i]) return ORC_E_SHAPE;
+        d->rin += inup[l];
+        d->rout += outup[l];
+        d->te_in *= d->tin[i];
+        d->te_out *= d->tout[i];
+    }
+    return ORC_OK;
+}
+
+static int cmp_keyrow(const void *a, const void *b, void *c) {
+    int r = *(const int *)c;
+    const int32_t *x = (const int32_t *)a, *y = (const int32_t *)b;
+    for (int k = 0; k < r; k++) {
+        if (x[k] != y[k]) return x[k] < y[k] ? -1 : 1;
+    }
+    return 0;
+}
+
+/* global coordinate of element e of source tuple `key` on label position i */
+static void rp_coords(const rp_desc *d, const int32_t *key, int64_t e, int64_t *g) {
+    int64_t rem = e;
+    for (int i = d->nl - 1; i >= 0; i--) {
+        g[i] = rem % d->tin[i];
+        rem /= d->tin[i];
+    }
+    int ka = 0;
+    for (int i = 0; i < d->nl; i++)
+        if (d->pin[i]) g[i] += (int64_t)key[ka++] * d->tin[i];
+}
+
+/* target key and target offset of global coordinate g */
+static int64_t rp_target(const rp_desc *d, const int64_t *g, int32_t *tkey) {
+    int64_t off = 0;
+    int ka = 0;
+    for (int i = 0; i < d->nl; i++) {
+        if (d->pout[i]) tkey[ka++] = (int32_t)(g[i] / d->tout[i]);
+        off = off * d->tout[i] + g[i] % d->tout[i];
+    }
+    return off;
+}
+
+int orc_repartition(const char *labels, const char *up_in, const char *up_out, const int64_t *ext,
+                    const int32_t *tin, const int32_t *tout, const int32_t *keys_in, int64_t n_in,
+                    const double *tiles_in, int64_t *n_out, int32_t **keys_out, double **tiles_out) {
+    rp_desc d;
+    int st = rp_make(labels, up_in, up_out, ext, tin, tout, &d);
+    if (st != ORC_OK) return st;
+    *n_out = 0;
+    *keys_out = NULL;
+    *tiles_out = NULL;
+    const int rout = d.rout;
+    const int64_t total = n_in * d.te_in;
+    /* the target key of every source position, then sorted and made unique */
+    int32_t *all = (int32_t *)malloc(sizeof(int32_t) * (size_t)(total > 0 ? total : 1) * (size_t)(rout > 0 ? rout : 1));
+    if (!all) return ORC_E_NOMEM;
+    int64_t g[26];
+    for (int64_t s = 0; s < n_in; s++) {
+        for (int64_t e = 0; e < d.te_in; e++) {
+            rp_coords(&d, keys_in + s * d.rin, e, g);
+            rp_target(&d, g, all + (s * d.te_in + e) * rout);
+        }
+    }
+    int64_t nk = 0;
+    if (total > 0) {
+        if (rout > 0) {
+            qsort_r(all, (size_t)total, sizeof(int32_t) * (size_t)rout, cmp_keyrow, (void *)&rout);
+            for (int64_t i = 0; i < total; i++) {
+                if (nk == 0 || cmp_keyrow(all + (nk - 1) * rout, all + i * rout, (void *)&rout) != 0) {
+                    memmove(all + nk * rout, all + i * rout, sizeof(int32_t) * (size_t)rout);
+                    nk++;
+                }
+            }
+        } else {
+            nk = 1;
+        }
+    }
+    double *tiles = (double *)calloc((size_t)(nk > 0 ? nk : 1) * (size_t)d.te_out, sizeof(double));
+    if (!tiles) {
+        free(all);
+        return ORC_E_NOMEM;
+    }
+    int32_t tkey[26];
+    for (int64_t s = 0; s < n_in; s++) {
+        for (int64_t e = 0; e < d.te_in; e++) {
+            rp_coords(&d, keys_in + s * d.rin, e, g);
+            int64_t off = rp_target(&d, g, tkey);
+            int64_t a = 0, b = nk, found = rout == 0 ? 0 : -1;
+            while (found < 0 && a < b) {
+                int64_t m = (a + b) / 2;
+                int c = cmp_keyrow(all + m * rout, tkey, (void *)&rout);
+                if (c == 0) found = m;
+                else if (c < 0) a = m + 1;
+                else b = m;
+            }
+            if (found < 0) {  /* cannot happen: every position's key was listed */
+                free(all);
+                free(tiles);
+                return ORC_E_ARG;
+            }
+            tiles[found * d.te_out + off] = tiles_in[s * d.te_in + e];
+        }
+    }
+    *n_out = nk;
+    *keys_out = all;
+    *tiles_out = tiles;
+    return ORC_OK;
+}

@@ -444,3 +444,124 @@ def test_expand_roundtrip(orc):
     ref = sorted(zip(map(tuple, w["Y"]["coo"][0].tolist()), w["Y"]["coo"][1].tolist()))
     assert got == ref
     assert np.array_equal(orc.keys_from_coo(p1, 1, w["Y"]["coo"][0]), w["Y"]["keys"])
+
+
+# ------------------------------------------------------------ repartition
+
+def _dense(labels, up, ext, til, keys, tiles):
+    """Place every tuple's tile into a dense array (written independently of
+    the oracle: numpy slicing of each tuple's index box)."""
+    shape = [ext[c] for c in labels]
+    out = np.zeros(shape)
+    tshape = [til[c] if c in up else ext[c] for c in labels]
+    for key, tile in zip(np.asarray(keys).reshape(len(tiles), -1), tiles):
+        box, ka = [], 0
+        for c, t in zip(labels, tshape):
+            if c in up:
+                box.append(slice(int(key[ka]) * t, (int(key[ka]) + 1) * t))
+                ka += 1
+            else:
+                box.append(slice(0, t))
+        out[tuple(box)] = np.asarray(tile).reshape(tshape)
+    return out
+
+
+def _covered_keys(labels, up_in, up_out, ext, tin, tout, keys):
+    """Target keys whose tile meets at least one source tile (brute force over
+    the source tiles' index ranges)."""
+    import itertools
+
+    got = set()
+    for key in np.asarray(keys).reshape(len(keys), -1):
+        ranges, ka = {}, 0
+        for c in labels:
+            t = tin[c] if c in up_in else ext[c]
+            lo = int(key[ka]) * t if c in up_in else 0
+            ka += c in up_in
+            ranges[c] = (lo, lo + t)
+        axes = [range(ranges[c][0] // tout[c], (ranges[c][1] - 1) // tout[c] + 1) for c in labels if c in up_out]
+        got.update(itertools.product(*axes))
+    return sorted(got)
+
+
+def test_repartition_paper_example(orc):
+    """Sec. 6: T keyed by its row label (row vectors) re-partitioned to be
+    keyed by its column label (column vectors)."""
+    keys = np.array([[0], [1], [2]], np.int32)
+    tiles = np.array([[1.0, 2.0], [3.0, 4.0], [5.0, 6.0]])
+    k2, t2 = orc.repartition("ki", "k", "i", {"k": 3, "i": 2}, {"k": 1}, {"i": 1}, keys, tiles)
+    assert k2.tolist() == [[0], [1]]
+    assert t2.tolist() == [[1.0, 3.0, 5.0], [2.0, 4.0, 6.0]]
+
+
+def test_repartition_identity(orc):
+    rng = np.random.default_rng(3)
+    keys = np.array([[0, 1], [1, 0], [2, 2]], np.int32)
+    tiles = rng.standard_normal((3, 2 * 3 * 4))
+    k2, t2 = orc.repartition("abc", "ab", "ab", {"a": 6, "b": 9, "c": 4}, {"a": 2, "b": 3}, {"a": 2, "b": 3},
+                             keys, tiles)
+    assert np.array_equal(k2, keys) and np.array_equal(t2, tiles)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_repartition_random_dense_and_keys(orc, seed):
+    """Random decompositions of random sparse tensors: the dense tensor is
+    unchanged and the target key set is exactly the target tiles met by the
+    source tiles (zero tiles included)."""
+    rng = np.random.default_rng(300 + seed)
+    nl = int(rng.integers(1, 4))
+    labels = "".join(rng.choice(list("abcdefgh"), nl, replace=False))
+    divs = {c: int(rng.choice([2, 3, 4, 6])) for c in labels}
+    ext = {c: divs[c] * int(rng.integers(2, 5)) for c in labels}
+    up_in = "".join(c for c in labels if rng.random() < 0.7)
+    up_out = "".join(c for c in labels if rng.random() < 0.7)
+    # tile sizes: divisors of the extent, possibly not dividing each other
+    def pick(c):
+        ds = [d for d in range(1, ext[c] + 1) if ext[c] % d == 0]
+        return int(rng.choice(ds))
+    tin = {c: pick(c) for c in up_in}
+    tout = {c: pick(c) for c in up_out}
+    axes = [range(ext[c] // tin[c]) for c in up_in]
+    import itertools
+    all_keys = list(itertools.product(*axes)) if up_in else [()]
+    keep = [k for k in all_keys if rng.random() < 0.5] or all_keys[:1]
+    keys = np.array(keep, np.int32).reshape(len(keep), len(up_in))
+    te = int(np.prod([tin[c] if c in up_in else ext[c] for c in labels]))
+    tiles = rng.standard_normal((len(keep), te)) * (rng.random((len(keep), te)) < 0.6)
+    k2, t2 = orc.repartition(labels, up_in, up_out, ext, tin, tout, keys, tiles)
+    np.testing.assert_array_equal(_dense(labels, up_out, ext, tout, k2, t2),
+                                  _dense(labels, up_in, ext, tin, keys, tiles))
+    assert [tuple(r) for r in k2.tolist()] == _covered_keys(labels, up_in, up_out, ext, tin, tout, keys)
+
+
+def test_repartition_round_trip(orc):
+    rng = np.random.default_rng(8)
+    ext = {"i": 12, "j": 8}
+    keys = np.array([[0, 1], [2, 0], [3, 3]], np.int32)
+    tiles = rng.standard_normal((3, 3 * 2))
+    k2, t2 = orc.repartition("ij", "ij", "j", ext, {"i": 3, "j": 2}, {"j": 4}, keys, tiles)
+    k3, t3 = orc.repartition("ij", "j", "ij", ext, {"j": 4}, {"i": 3, "j": 2}, k2, t2)
+    # the source tuples come back unchanged; every extra tuple is all zeros
+    back = {tuple(k): t for k, t in zip(k3.tolist(), t3)}
+    for k, t in zip(keys.tolist(), tiles):
+        np.testing.assert_array_equal(back.pop(tuple(k)), t)
+    assert all(not np.any(t) for t in back.values())
+
+
+def test_repartition_stack_special_case(orc):
+    """Grouping one promoted label from tile 1 to tile g is the stack of rows."""
+    rng = np.random.default_rng(5)
+    keys = np.sort(rng.choice(64, 20, replace=False)).astype(np.int32).reshape(-1, 1)
+    rows = rng.standard_normal((20, 8))
+    k2, t2 = orc.repartition("ki", "k", "k", {"k": 64, "i": 8}, {"k": 1}, {"k": 16}, keys, rows)
+    k3, t3 = orc.stack_rows(keys, rows, 16)
+    assert np.array_equal(k2, k3) and np.array_equal(t2, t3)
+
+
+def test_repartition_errors(orc):
+    with pytest.raises(orc.OracleError):
+        orc.repartition("ij", "ij", "i", {"i": 4, "j": 4}, {"i": 3, "j": 1}, {"i": 2}, np.zeros((0, 2), np.int32),
+                        np.zeros((0, 3)))
+    with pytest.raises(orc.OracleError):
+        orc.repartition("ij", "ik", "i", {"i": 4, "j": 4}, {"i": 1}, {"i": 2}, np.zeros((0, 2), np.int32),
+                        np.zeros((0, 4)))
