@@ -213,6 +213,36 @@ tre_status tre_stack_rows(const int32_t *keys, int64_t n, const void *tiles, int
                           int32_t elem_bytes, int32_t *out_keys, void *out_tiles, int64_t out_cap, int64_t *n_out,
                           void *ws, size_t ws_bytes, void *stream);
 
+/* Repartition (Sec. 6, "changing representation" between two EinSums): the
+ * same tensor under a second decomposition.  The relation is decomposed on
+ * every label promoted in either decomposition (ALLINTS) and re-composed with
+ * the STACK aggregate grouped by the target's promoted labels; here both
+ * steps are one device pass.
+ *   labels            : the tensor's labels in string order, e.g. "ki" (at most 8).
+ *   upper_in/upper_out: promoted labels of the source / target decomposition.
+ *   extent[26], tile_in[26], tile_out[26]: per letter; a promoted label's tile
+ *                       size must divide its extent, a demoted label keeps its
+ *                       whole extent in the tile (its tile entry is ignored).
+ *   elem_bytes        : 2 (bf16 bits) or 4 (fp32); values are copied bit for bit.
+ *   keys_in, tiles_in : device source relation, conventions above (sorted keys).
+ *   keys_out, tiles_out: device [out_cap x r_out] int32 / [out_cap x tile_elems_out].
+ *   n_out             : host; the number of target tuples: one for every target
+ *                       tile that contains a position of a source tile (zero
+ *                       values included), keys sorted.  Target elements that no
+ *                       source tile covers are zero.
+ *   ws, ws_bytes      : device workspace, 256-byte aligned, at least
+ *                       tre_repartition_workspace_bytes(...) (0 on bad arguments).
+ * Synchronizes the stream twice.  TRE_E_CAPACITY (n_out set) if out_cap is
+ * short; TRE_E_UNSORTED / TRE_E_DUPKEY / TRE_E_KEYRANGE for bad source keys. */
+size_t tre_repartition_workspace_bytes(const char *labels, const char *upper_in, const char *upper_out,
+                                       const int64_t extent[26], const int32_t tile_in[26],
+                                       const int32_t tile_out[26], int64_t n_in);
+tre_status tre_repartition(const char *labels, const char *upper_in, const char *upper_out,
+                           const int64_t extent[26], const int32_t tile_in[26], const int32_t tile_out[26],
+                           int32_t elem_bytes, const int32_t *keys_in, int64_t n_in, const void *tiles_in,
+                           int32_t *keys_out, void *tiles_out, int64_t out_cap, int64_t *n_out, void *ws,
+                           size_t ws_bytes, void *stream);
+
 /* --- input preparation --------------------------------------------------- */
 
 /* Materialise tiles from scalar entries: tiles[slot[e] * tile_elems + offset[e]]

@@ -9,5 +9,5 @@ its ctypes binding.
 """
 from .tre import (  # noqa: F401
     EXPORTS, JoinResult, Output, Plan, TreError, Timing, alloc_workspace, cast_f32_bf16, contract, einsum, join, lib,
-    stack_rows, tiles_from_entries,
+    repartition, stack_rows, tiles_from_entries,
 )

@@ -1,0 +1,442 @@
+// Repartition of a tensor relation between two decompositions (Sec. 6: when
+// the decomposition an EinSum produces differs from the one its consumer
+// reads, the relation is decomposed on all labels promoted in either
+// decomposition -- ALLINTS -- and re-composed with the STACK aggregate
+// grouped by the consumer's promoted labels).
+//
+// On the device the two steps are fused: every source tile meets a small box
+// of target tiles; the (target key, source tuple) pairs are listed, sorted by
+// target key (stable LSD radix sort, so the target keys come out sorted and
+// a target's sources in source order), run-length encoded into the target
+// key set, and each pair copies the intersection of its source tile and its
+// target tile (one wavefront per pair, consecutive lanes on the innermost
+// label, which is contiguous in both tiles).  Target elements no source tile
+// covers are zero.
+#include "tre_internal.h"
+
+#include <algorithm>
+#include <cstring>
+
+namespace tre {
+
+namespace {
+
+constexpr int kThreads = 256;
+
+inline unsigned blocks_for(int64_t n) { return unsigned((n + kThreads - 1) / kThreads); }
+
+constexpr int kRpMaxLabels = kMaxDims;  // labels of one tensor (kept in registers)
+
+// Both decompositions of one tensor, per label position in the label string.
+struct RpDesc {
+    int32_t nl, rin, rout;
+    int32_t pin[kRpMaxLabels], pout[kRpMaxLabels];  // promoted in the source / target
+    int64_t ext[kRpMaxLabels], tin[kRpMaxLabels], tout[kRpMaxLabels];
+    int64_t sin_[kRpMaxLabels], sout[kRpMaxLabels];  // row-major strides of the source / target tile
+    int32_t bits[kRpMaxLabels];                      // bits of each target key attribute (target order)
+    int32_t key_bits;
+    int64_t te_in, te_out;
+    int64_t max_cover;              // target tiles one source tile can meet
+};
+
+struct RpHeader {
+    int32_t err;
+    int32_t pad;
+    int64_t pairs;
+    int64_t n_out;
+    int64_t pad1[5];
+};
+
+__device__ inline void source_range(const RpDesc& d, const int32_t* key, int i, int ka, int64_t& lo, int64_t& hi) {
+    lo = d.pin[i] ? int64_t(key[ka]) * d.tin[i] : 0;
+    hi = lo + d.tin[i];
+}
+
+__global__ void k_rp_count(const int32_t* __restrict__ keys, int64_t n, RpDesc d, int64_t* __restrict__ cnt) {
+    const int64_t s = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (s > n) return;
+    if (s == n) {
+        cnt[s] = 0;
+        return;
+    }
+    const int32_t* key = keys + s * d.rin;
+    int64_t c = 1;
+    int ka = 0;
+#pragma unroll
+    for (int i = 0; i < kRpMaxLabels; i++) {
+        if (i >= d.nl) break;
+        int64_t lo, hi;
+        source_range(d, key, i, ka, lo, hi);
+        ka += d.pin[i];
+        if (d.pout[i]) c *= (hi - 1) / d.tout[i] - lo / d.tout[i] + 1;
+    }
+    cnt[s] = c;
+}
+
+// List (target key, source) for every target tile source s meets, in target
+// key order within s.
+__global__ void k_rp_expand(const int32_t* __restrict__ keys, int64_t n, RpDesc d, const int64_t* __restrict__ off,
+                            uint64_t* __restrict__ tk, uint32_t* __restrict__ src) {
+    const int64_t s = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (s >= n) return;
+    const int32_t* key = keys + s * d.rin;
+    int64_t blo[kRpMaxLabels], bn[kRpMaxLabels];
+    int ka = 0;
+#pragma unroll
+    for (int i = 0; i < kRpMaxLabels; i++) {
+        blo[i] = 0;
+        bn[i] = 1;
+        if (i >= d.nl) continue;
+        int64_t lo, hi;
+        source_range(d, key, i, ka, lo, hi);
+        ka += d.pin[i];
+        blo[i] = lo / d.tout[i];
+        bn[i] = (hi - 1) / d.tout[i] - blo[i] + 1;
+    }
+    const int64_t c = off[s + 1] - off[s];
+    for (int64_t j = 0; j < c; j++) {
+        // digits of j over the target-promoted labels, last label fastest
+        int64_t rem = j, block[kRpMaxLabels];
+#pragma unroll
+        for (int i = kRpMaxLabels - 1; i >= 0; i--) {
+            block[i] = blo[i];
+            if (i >= d.nl || !d.pout[i]) continue;
+            block[i] += rem % bn[i];
+            rem /= bn[i];
+        }
+        uint64_t k = 0;
+        int ko = 0;
+#pragma unroll
+        for (int i = 0; i < kRpMaxLabels; i++) {
+            if (i >= d.nl || !d.pout[i]) continue;
+            k = (k << d.bits[ko]) | uint64_t(block[i]);
+            ko++;
+        }
+        tk[off[s] + j] = k;
+        src[off[s] + j] = uint32_t(s);
+    }
+}
+
+__global__ void k_rp_heads(const uint64_t* __restrict__ tk, int64_t m, int32_t* __restrict__ flags) {
+    const int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (p > m) return;
+    flags[p] = (p < m && (p == 0 || tk[p] != tk[p - 1])) ? 1 : 0;
+}
+
+__global__ void k_rp_compact(const uint64_t* __restrict__ tk, int64_t m, const int32_t* __restrict__ seg_of,
+                             uint64_t* __restrict__ seg_key, RpHeader* hdr) {
+    const int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (p > m) return;
+    if (p == m) {
+        hdr->n_out = seg_of[m];
+        return;
+    }
+    if (p == 0 || tk[p] != tk[p - 1]) seg_key[seg_of[p]] = tk[p];
+}
+
+__global__ void k_rp_write_keys(const uint64_t* __restrict__ seg_key, int64_t n_out, RpDesc d,
+                                int32_t* __restrict__ keys_out) {
+    const int64_t q = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (q >= n_out) return;
+    uint64_t k = seg_key[q];
+    for (int a = d.rout - 1; a >= 0; a--) {
+        keys_out[q * d.rout + a] = int32_t(k & ((uint64_t(1) << d.bits[a]) - 1));
+        k >>= d.bits[a];
+    }
+}
+
+// One wavefront per (target, source) pair: copy the intersection box.
+template <typename E>
+__global__ __launch_bounds__(kThreads) void k_rp_copy(const int32_t* __restrict__ keys, const E* __restrict__ tin,
+                                                      const uint64_t* __restrict__ tk,
+                                                      const uint32_t* __restrict__ src,
+                                                      const int32_t* __restrict__ seg_of, int64_t m, RpDesc d,
+                                                      E* __restrict__ tout) {
+    const int64_t p = int64_t(blockIdx.x) * (kThreads / 64) + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (p >= m) return;
+    // the pair's target tuple: segments are numbered by an exclusive scan of
+    // the head flags, so pair p belongs to segment seg_of[p + 1] - 1
+    const int64_t s = src[p], q = seg_of[p + 1] - 1;
+    const int32_t* key = keys + s * d.rin;
+    // target block of each target-promoted label, from the packed key
+    int64_t block[kRpMaxLabels];
+    uint64_t k = tk[p];
+    int ko = d.rout - 1;
+#pragma unroll
+    for (int i = kRpMaxLabels - 1; i >= 0; i--) {
+        block[i] = 0;
+        if (i >= d.nl || !d.pout[i]) continue;
+        block[i] = int64_t(k & ((uint64_t(1) << d.bits[ko]) - 1));
+        k >>= d.bits[ko];
+        ko--;
+    }
+    // intersection box: per label, start in source and target, and length
+    int64_t n[kRpMaxLabels], so = 0, to = 0, total = 1;
+    int ka = 0;
+#pragma unroll
+    for (int i = 0; i < kRpMaxLabels; i++) {
+        n[i] = 1;
+        if (i >= d.nl) continue;
+        int64_t slo, shi;
+        source_range(d, key, i, ka, slo, shi);
+        ka += d.pin[i];
+        const int64_t tlo = d.pout[i] ? block[i] * d.tout[i] : 0, thi = tlo + d.tout[i];
+        const int64_t a = max(slo, tlo);
+        n[i] = min(shi, thi) - a;
+        so += (a - slo) * d.sin_[i];
+        to += (a - tlo) * d.sout[i];
+        total *= n[i];
+    }
+    const E* sp = tin + s * d.te_in + so;
+    E* tp = tout + q * d.te_out + to;
+    for (int64_t x = lane; x < total; x += 64) {
+        int64_t rem = x, os = 0, ot = 0;
+#pragma unroll
+        for (int i = kRpMaxLabels - 1; i >= 0; i--) {
+            if (i >= d.nl) continue;
+            const int64_t c = rem % n[i];
+            rem /= n[i];
+            os += c * d.sin_[i];
+            ot += c * d.sout[i];
+        }
+        tp[ot] = sp[os];
+    }
+}
+
+tre_status dev_fail(hipError_t e, const char* where) {
+    set_error(std::string("tre_repartition: ") + where + ": " + hipGetErrorString(e));
+    return TRE_E_DEVICE;
+}
+
+int32_t bit_width(int64_t x) {
+    int32_t b = 0;
+    while (x > 0) {
+        b++;
+        x >>= 1;
+    }
+    return b;
+}
+
+tre_status make_desc(const char* labels, const char* up_in, const char* up_out, const int64_t* extent,
+                     const int32_t* tile_in, const int32_t* tile_out, RpDesc& d) {
+    std::memset(&d, 0, sizeof(d));
+    if (!labels || !up_in || !up_out || !extent || !tile_in || !tile_out) {
+        set_error("tre_repartition: null argument");
+        return TRE_E_ARG;
+    }
+    bool seen[26] = {}, in_up[26] = {}, out_up[26] = {};
+    int lab[26];
+    for (const char* c = labels; *c; c++) {
+        if (*c < 'a' || *c > 'z' || seen[*c - 'a']) {
+            set_error("tre_repartition: labels must be distinct lower-case letters");
+            return TRE_E_PARSE;
+        }
+        if (d.nl == kRpMaxLabels) {
+            set_error("tre_repartition: at most 8 labels");
+            return TRE_E_SHAPE;
+        }
+        seen[*c - 'a'] = true;
+        lab[d.nl++] = *c - 'a';
+    }
+    for (int pass = 0; pass < 2; pass++) {
+        for (const char* c = pass ? up_out : up_in; *c; c++) {
+            if (*c < 'a' || *c > 'z' || !seen[*c - 'a']) {
+                set_error("tre_repartition: a promoted label is not a label of the tensor");
+                return TRE_E_SPLIT;
+            }
+            (pass ? out_up : in_up)[*c - 'a'] = true;
+        }
+    }
+    d.te_in = d.te_out = 1;
+    d.max_cover = 1;
+    for (int i = 0; i < d.nl; i++) {
+        const int l = lab[i];
+        d.ext[i] = extent[l];
+        d.pin[i] = in_up[l];
+        d.pout[i] = out_up[l];
+        d.tin[i] = in_up[l] ? tile_in[l] : extent[l];
+        d.tout[i] = out_up[l] ? tile_out[l] : extent[l];
+        if (d.ext[i] < 1 || d.tin[i] < 1 || d.tout[i] < 1 || d.ext[i] % d.tin[i] || d.ext[i] % d.tout[i]) {
+            set_error("tre_repartition: every tile size must divide its label's extent");
+            return TRE_E_SHAPE;
+        }
+        d.rin += d.pin[i];
+        if (d.pout[i]) {
+            d.bits[d.rout] = bit_width(d.ext[i] / d.tout[i] - 1);
+            d.key_bits += d.bits[d.rout];
+            d.rout++;
+            // blocks of size tout met by an aligned run of length tin
+            d.max_cover *= std::min<int64_t>(d.ext[i] / d.tout[i], (d.tin[i] - 1) / d.tout[i] + 2);
+        }
+        d.te_in *= d.tin[i];
+        d.te_out *= d.tout[i];
+    }
+    if (d.key_bits > 64) {
+        set_error("tre_repartition: target key space exceeds 64 bits");
+        return TRE_E_SHAPE;
+    }
+    int64_t si = 1, so = 1;
+    for (int i = d.nl - 1; i >= 0; i--) {
+        d.sin_[i] = si;
+        d.sout[i] = so;
+        si *= d.tin[i];
+        so *= d.tout[i];
+    }
+    return TRE_OK;
+}
+
+struct RpLayout {
+    size_t hdr, cnt, tmp, tk, tk_alt, src, src_alt, hist, seg_of, seg_key, total;
+};
+
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+RpLayout rp_layout(const RpDesc& d, int64_t n_in) {
+    const int64_t m = std::max<int64_t>(n_in * d.max_cover, 1);
+    RpLayout L{};
+    size_t off = 0;
+    auto take = [&](size_t b) {
+        const size_t o = off;
+        off += align256(std::max<size_t>(b, 1));
+        return o;
+    };
+    L.hdr = take(sizeof(RpHeader));
+    L.cnt = take(sizeof(int64_t) * size_t(n_in + 1));
+    L.tmp = take(sizeof(int64_t) * scan_tmp_elems(std::max<int64_t>(n_in, m) + 1));
+    L.tk = take(sizeof(uint64_t) * size_t(m));
+    L.tk_alt = take(sizeof(uint64_t) * size_t(m));
+    L.src = take(sizeof(uint32_t) * size_t(m));
+    L.src_alt = take(sizeof(uint32_t) * size_t(m));
+    L.hist = take(sizeof(int32_t) * size_t(radix_hist_elems(m)));
+    L.seg_of = take(sizeof(int32_t) * size_t(m + 1));
+    L.seg_key = take(sizeof(uint64_t) * size_t(m));
+    L.total = off;
+    return L;
+}
+
+}  // namespace
+
+}  // namespace tre
+
+using namespace tre;
+
+extern "C" {
+
+size_t tre_repartition_workspace_bytes(const char* labels, const char* upper_in, const char* upper_out,
+                                       const int64_t extent[26], const int32_t tile_in[26],
+                                       const int32_t tile_out[26], int64_t n_in) {
+    RpDesc d;
+    if (n_in < 0 || make_desc(labels, upper_in, upper_out, extent, tile_in, tile_out, d) != TRE_OK) return 0;
+    return rp_layout(d, n_in).total;
+}
+
+tre_status tre_repartition(const char* labels, const char* upper_in, const char* upper_out,
+                           const int64_t extent[26], const int32_t tile_in[26], const int32_t tile_out[26],
+                           int32_t elem_bytes, const int32_t* keys_in, int64_t n_in, const void* tiles_in,
+                           int32_t* keys_out, void* tiles_out, int64_t out_cap, int64_t* n_out, void* ws,
+                           size_t ws_bytes, void* stream) {
+    RpDesc d;
+    tre_status st = make_desc(labels, upper_in, upper_out, extent, tile_in, tile_out, d);
+    if (st != TRE_OK) return st;
+    if (!n_out || n_in < 0 || out_cap < 0 || (elem_bytes != 2 && elem_bytes != 4)) {
+        set_error("tre_repartition: null n_out, negative size or elem_bytes not 2 / 4");
+        return TRE_E_ARG;
+    }
+    *n_out = 0;
+    if (n_in == 0) return TRE_OK;
+    if (d.rin == 0 && n_in > 1) {
+        set_error("tre_repartition: a relation without promoted labels holds at most one tuple");
+        return TRE_E_DUPKEY;
+    }
+    if ((d.rin > 0 && !keys_in) || !tiles_in || !ws || (reinterpret_cast<uintptr_t>(ws) & 255)) {
+        set_error("tre_repartition: null keys / tiles / workspace, or workspace not 256-byte aligned");
+        return TRE_E_ARG;
+    }
+    if (n_in * d.max_cover > int64_t(0xffffffffll) || n_in > int64_t(0x7fffffff)) {
+        set_error("tre_repartition: too many tuples");
+        return TRE_E_SHAPE;
+    }
+    const RpLayout L = rp_layout(d, n_in);
+    if (ws_bytes < L.total) {
+        set_error("tre_repartition: workspace too small");
+        return TRE_E_WORKSPACE;
+    }
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    char* w = reinterpret_cast<char*>(ws);
+    RpHeader* hdr = reinterpret_cast<RpHeader*>(w + L.hdr);
+    int64_t* cnt = reinterpret_cast<int64_t*>(w + L.cnt);
+    uint64_t* tk = reinterpret_cast<uint64_t*>(w + L.tk);
+    uint32_t* src = reinterpret_cast<uint32_t*>(w + L.src);
+    int32_t* seg_of = reinterpret_cast<int32_t*>(w + L.seg_of);
+    uint64_t* seg_key = reinterpret_cast<uint64_t*>(w + L.seg_key);
+    hipError_t e;
+    // keys: sorted, unique and in range (the relation conventions)
+    if ((e = launch_fill_zero(hdr, sizeof(RpHeader), s)) != hipSuccess) return dev_fail(e, "header");
+    if (d.rin > 0) {
+        int32_t radix[26];
+        for (int i = 0, ka = 0; i < d.nl; i++)
+            if (d.pin[i]) radix[ka++] = int32_t(d.ext[i] / d.tin[i]);
+        if ((e = launch_validate(keys_in, n_in, d.rin, radix, &hdr->err, s)) != hipSuccess)
+            return dev_fail(e, "validate");
+    }
+    k_rp_count<<<blocks_for(n_in + 1), kThreads, 0, s>>>(keys_in, n_in, d, cnt);
+    if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "count");
+    if ((e = scan_exclusive_i64(cnt, cnt, n_in + 1, reinterpret_cast<int64_t*>(w + L.tmp), s)) != hipSuccess)
+        return dev_fail(e, "scan");
+    RpHeader h{};
+    if ((e = hipMemcpyAsync(&h, hdr, sizeof(h), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+        (e = hipMemcpyAsync(&h.pairs, cnt + n_in, sizeof(int64_t), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+        (e = hipStreamSynchronize(s)) != hipSuccess)
+        return dev_fail(e, "count read-back");
+    if (h.err) {
+        set_error("tre_repartition: source keys out of range, unsorted or repeated");
+        return (h.err & 4) ? TRE_E_KEYRANGE : (h.err & 1) ? TRE_E_UNSORTED : TRE_E_DUPKEY;
+    }
+    const int64_t m = h.pairs;
+    k_rp_expand<<<blocks_for(n_in), kThreads, 0, s>>>(keys_in, n_in, d, cnt, tk, src);
+    if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "expand");
+    if ((e = radix_sort_u64(tk, src, reinterpret_cast<uint64_t*>(w + L.tk_alt), reinterpret_cast<uint32_t*>(w + L.src_alt),
+                            m, d.key_bits, reinterpret_cast<int32_t*>(w + L.hist), reinterpret_cast<int32_t*>(w + L.tmp),
+                            s)) != hipSuccess)
+        return dev_fail(e, "sort");
+    if (radix_result_in_alt(m, d.key_bits)) {
+        tk = reinterpret_cast<uint64_t*>(w + L.tk_alt);
+        src = reinterpret_cast<uint32_t*>(w + L.src_alt);
+    }
+    k_rp_heads<<<blocks_for(m + 1), kThreads, 0, s>>>(tk, m, seg_of);
+    if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "heads");
+    if ((e = scan_exclusive_i32(seg_of, seg_of, m + 1, reinterpret_cast<int32_t*>(w + L.tmp), s)) != hipSuccess)
+        return dev_fail(e, "segments");
+    k_rp_compact<<<blocks_for(m + 1), kThreads, 0, s>>>(tk, m, seg_of, seg_key, hdr);
+    if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "compact");
+    if ((e = hipMemcpyAsync(&h.n_out, &hdr->n_out, sizeof(int64_t), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+        (e = hipStreamSynchronize(s)) != hipSuccess)
+        return dev_fail(e, "target count read-back");
+    *n_out = h.n_out;
+    if (h.n_out > out_cap) {
+        set_error("tre_repartition: output capacity below the target tuple count");
+        return TRE_E_CAPACITY;
+    }
+    if ((d.rout > 0 && !keys_out) || !tiles_out) {
+        set_error("tre_repartition: null output buffers");
+        return TRE_E_ARG;
+    }
+    if ((e = launch_fill_zero(tiles_out, size_t(h.n_out) * size_t(d.te_out) * size_t(elem_bytes), s)) != hipSuccess)
+        return dev_fail(e, "zero fill");
+    if (d.rout > 0) {
+        k_rp_write_keys<<<blocks_for(h.n_out), kThreads, 0, s>>>(seg_key, h.n_out, d, keys_out);
+        if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "keys");
+    }
+    const unsigned grid = unsigned((m + kThreads / 64 - 1) / (kThreads / 64));
+    if (elem_bytes == 2)
+        k_rp_copy<uint16_t><<<grid, kThreads, 0, s>>>(keys_in, reinterpret_cast<const uint16_t*>(tiles_in), tk, src,
+                                                       seg_of, m, d, reinterpret_cast<uint16_t*>(tiles_out));
+    else
+        k_rp_copy<uint32_t><<<grid, kThreads, 0, s>>>(keys_in, reinterpret_cast<const uint32_t*>(tiles_in), tk, src,
+                                                       seg_of, m, d, reinterpret_cast<uint32_t*>(tiles_out));
+    if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "copy");
+    return TRE_OK;
+}
+
+}  // extern "C"

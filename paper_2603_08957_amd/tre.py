@@ -20,6 +20,7 @@ STATUS = {
     6: "TRE_E_UNSORTED", 7: "TRE_E_DUPKEY", 8: "TRE_E_KEYRANGE", 9: "TRE_E_CAPACITY", 10: "TRE_E_WORKSPACE",
     11: "TRE_E_DEVICE", 12: "TRE_E_STATE",
 }
+STATUS_CODE = {v: k for k, v in STATUS.items()}
 DTYPE = {"f32": 0, "bf16": 1}
 
 # every symbol include/tre.h declares
@@ -27,6 +28,7 @@ EXPORTS = [
     "tre_plan", "tre_plan_get_info", "tre_plan_destroy", "tre_workspace_bytes", "tre_workspace_max_pairs",
     "tre_join", "tre_contract", "tre_execute", "tre_timing_read", "tre_cast_f32_bf16", "tre_stack_workspace_bytes", "tre_stack_rows",
     "tre_tiles_from_entries", "tre_status_str", "tre_last_error", "tre_version",
+    "tre_repartition_workspace_bytes", "tre_repartition",
 ]
 
 
@@ -99,6 +101,10 @@ def lib():
         L.tre_stack_workspace_bytes.restype = sz
         L.tre_stack_rows.argtypes = [P, i64, P, i64, i32, i32, P, P, i64, P, P, sz, P]
         L.tre_tiles_from_entries.argtypes = [P, P, P, i64, i32, P, i64, i64, P]
+        cs = ctypes.c_char_p
+        L.tre_repartition_workspace_bytes.argtypes = [cs, cs, cs, P, P, P, i64]
+        L.tre_repartition_workspace_bytes.restype = sz
+        L.tre_repartition.argtypes = [cs, cs, cs, P, P, P, i32, P, i64, P, P, P, i64, P, P, sz, P]
         L.tre_status_str.restype = ctypes.c_char_p
         L.tre_last_error.restype = ctypes.c_char_p
         L.tre_version.restype = ctypes.c_char_p
@@ -268,6 +274,50 @@ def stack_rows(keys, tiles, group: int, stream=None):
     _check(rc, "tre_stack_rows")
     k = int(n_out.value)
     return out_keys[:k], out_tiles[:k]
+
+
+def repartition(labels: str, upper_in: str, upper_out: str, extents: dict, tiles_in: dict, tiles_out: dict,
+                keys, tiles, stream=None):
+    """The relation (keys, tiles) under the target decomposition (see
+    tre_repartition).  Returns (keys_out [n_out, r_out] int32, tiles_out
+    [n_out, tile_elems_out], same dtype as ``tiles``)."""
+    import numpy as _np
+    import torch
+
+    ext = _np.zeros(26, dtype=_np.int64)
+    tin = _np.ones(26, dtype=_np.int32)
+    tout = _np.ones(26, dtype=_np.int32)
+    for k, v in extents.items():
+        ext[ord(k) - 97] = v
+    for k, v in (tiles_in or {}).items():
+        tin[ord(k) - 97] = v
+    for k, v in (tiles_out or {}).items():
+        tout[ord(k) - 97] = v
+    args = (labels.encode(), upper_in.encode(), upper_out.encode(), ext.ctypes.data_as(ctypes.c_void_p),
+            tin.ctypes.data_as(ctypes.c_void_p), tout.ctypes.data_as(ctypes.c_void_p))
+    n = int(keys.shape[0]) if keys is not None else int(tiles.shape[0])
+    wsb = int(lib().tre_repartition_workspace_bytes(*args, n))
+    n_out = ctypes.c_int64(0)
+    if wsb == 0:  # bad arguments: let the call itself name the error
+        rc = lib().tre_repartition(*args, tiles.element_size(), _ptr(keys), n, _ptr(tiles), None, None, 0,
+                                   ctypes.byref(n_out), None, 0, _stream(stream))
+        _check(rc if rc else STATUS_CODE["TRE_E_ARG"], "tre_repartition")
+    ws = alloc_workspace(wsb, tiles.device)
+    te_out = 1
+    for c in labels:
+        te_out *= int(tout[ord(c) - 97]) if c in upper_out else int(ext[ord(c) - 97])
+    cap = 0
+    while True:
+        out_keys = torch.empty((max(cap, 1), len(upper_out)), dtype=torch.int32, device=tiles.device)
+        out_tiles = torch.empty((max(cap, 1), te_out), dtype=tiles.dtype, device=tiles.device)
+        rc = lib().tre_repartition(*args, tiles.element_size(), _ptr(keys), n, _ptr(tiles), _ptr(out_keys),
+                                   _ptr(out_tiles), cap, ctypes.byref(n_out), _ptr(ws), ws.numel(), _stream(stream))
+        if rc == STATUS_CODE["TRE_E_CAPACITY"] and n_out.value > cap:
+            cap = int(n_out.value)
+            continue
+        _check(rc, "tre_repartition")
+        k = int(n_out.value)
+        return out_keys[:k], out_tiles[:k]
 
 
 def tiles_from_entries(slot, offset, values, n_tiles: int, tile_elems: int, stream=None):

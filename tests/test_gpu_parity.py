@@ -307,3 +307,101 @@ def test_tiles_from_entries_gpu(orc):
     got = sorted(zip(map(tuple, c.tolist()), v.tolist()))
     ref = sorted(zip(map(tuple, Y["coo"][0].tolist()), Y["coo"][1].tolist()))
     assert got == ref
+
+
+# ------------------------------------------------------------ repartition
+
+def _rp_case(rng, nl_max=3, ext_mult=(2, 6)):
+    import itertools
+
+    nl = int(rng.integers(1, nl_max + 1))
+    labels = "".join(rng.choice(list("abcdefgh"), nl, replace=False))
+    base = {c: int(rng.choice([2, 3, 4, 8])) for c in labels}
+    ext = {c: base[c] * int(rng.integers(*ext_mult)) for c in labels}
+    up_in = "".join(c for c in labels if rng.random() < 0.75)
+    up_out = "".join(c for c in labels if rng.random() < 0.75)
+
+    def pick(c):
+        ds = [d for d in range(1, ext[c] + 1) if ext[c] % d == 0]
+        return int(rng.choice(ds))
+
+    tin = {c: pick(c) for c in up_in}
+    tout = {c: pick(c) for c in up_out}
+    axes = [range(ext[c] // tin[c]) for c in up_in]
+    all_keys = list(itertools.product(*axes)) if up_in else [()]
+    keep = [k for k in all_keys if rng.random() < 0.4] or all_keys[:1]
+    keys = np.array(keep, np.int32).reshape(len(keep), len(up_in))
+    te = int(np.prod([tin[c] if c in up_in else ext[c] for c in labels]))
+    return labels, up_in, up_out, ext, tin, tout, keys, te
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_repartition_gpu(orc, seed):
+    """Random decompositions: target keys and every target element bit-exact
+    against the oracle (fp32 and bf16 bit patterns)."""
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    rng = np.random.default_rng(900 + seed)
+    labels, up_in, up_out, ext, tin, tout, keys, te = _rp_case(rng)
+    dtype = "bf16" if seed % 2 else "f32"
+    vals = (rng.standard_normal((len(keys), te)) * (rng.random((len(keys), te)) < 0.7)).astype(np.float32)
+    if dtype == "bf16":
+        bits = orc.f32_to_bf16(vals)
+        dev_tiles = torch.from_numpy(bits.view(np.int16)).cuda()
+        ref_vals = orc.bf16_to_f64(bits)
+    else:
+        dev_tiles = torch.from_numpy(vals).cuda()
+        ref_vals = vals.astype(np.float64)
+    say("repartition", seed, labels, up_in, up_out, tin, tout, len(keys), dtype)
+    k2, t2 = tre.repartition(labels, up_in, up_out, ext, tin, tout, torch.from_numpy(keys).cuda(), dev_tiles)
+    rk, rt = orc.repartition(labels, up_in, up_out, ext, tin, tout, keys, ref_vals)
+    assert np.array_equal(k2.cpu().numpy().reshape(rk.shape), rk)
+    got = t2.cpu().numpy()
+    got = orc.bf16_to_f64(got.view(np.uint16)) if dtype == "bf16" else got.astype(np.float64)
+    assert np.array_equal(got.reshape(rt.shape), rt)
+
+
+def test_repartition_gpu_paper_example_and_stack(orc):
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    keys = torch.tensor([[0], [1], [2]], dtype=torch.int32).cuda()
+    tiles = torch.tensor([[1.0, 2.0], [3.0, 4.0], [5.0, 6.0]]).cuda()
+    k2, t2 = tre.repartition("ki", "k", "i", {"k": 3, "i": 2}, {"k": 1}, {"i": 1}, keys, tiles)
+    assert k2.cpu().tolist() == [[0], [1]]
+    assert t2.cpu().tolist() == [[1.0, 3.0, 5.0], [2.0, 4.0, 6.0]]
+    # stack of per-vertex rows into 256-row tiles (the chain's re-composition)
+    rng = np.random.default_rng(4)
+    n, emb = 4096, 256
+    present = np.sort(rng.choice(n, 3000, replace=False)).astype(np.int32).reshape(-1, 1)
+    rows = rng.standard_normal((len(present), emb)).astype(np.float32)
+    k2, t2 = tre.repartition("ki", "k", "k", {"k": n, "i": emb}, {"k": 1}, {"k": 256},
+                             torch.from_numpy(present).cuda(), torch.from_numpy(rows).cuda())
+    k3, t3 = tre.stack_rows(torch.from_numpy(present).cuda(), torch.from_numpy(rows).cuda(), 256)
+    assert torch.equal(k2, k3) and torch.equal(t2, t3)
+
+
+def test_repartition_gpu_errors_and_empty(orc):
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    t = torch.zeros((2, 4)).cuda()
+    with pytest.raises(tre.TreError) as ei:
+        tre.repartition("ij", "i", "j", {"i": 4, "j": 4}, {"i": 1}, {"j": 2},
+                        torch.tensor([[1], [0]], dtype=torch.int32).cuda(), t)
+    assert ei.value.status == "TRE_E_UNSORTED"
+    with pytest.raises(tre.TreError) as ei:
+        tre.repartition("ij", "i", "j", {"i": 4, "j": 4}, {"i": 1}, {"j": 2},
+                        torch.tensor([[0], [9]], dtype=torch.int32).cuda(), t)
+    assert ei.value.status == "TRE_E_KEYRANGE"
+    with pytest.raises(tre.TreError) as ei:
+        tre.repartition("ij", "i", "j", {"i": 4, "j": 4}, {"i": 3}, {"j": 2},
+                        torch.tensor([[0]], dtype=torch.int32).cuda(), t[:1])
+    assert ei.value.status == "TRE_E_SHAPE"
+    k2, t2 = tre.repartition("ij", "i", "j", {"i": 4, "j": 4}, {"i": 1}, {"j": 2},
+                             torch.zeros((0, 1), dtype=torch.int32).cuda(), torch.zeros((0, 4)).cuda())
+    assert k2.shape[0] == 0 and t2.shape[0] == 0
