@@ -150,6 +150,8 @@ class GnnChain:
         self.e2 = Stage(tre, torch, w["E2"], self.n_t2, 1, self.n_t2, "E2")
         self.t_cast = None
         self.n_t = n_t
+        self.measure_rp = False
+        self.rp_report = None
         torch.cuda.synchronize()
 
     def step(self, timing=None):
@@ -163,7 +165,22 @@ class GnnChain:
         else:
             tb = tt
         if self.stack > 1:
-            tk, tb = tre.stack_rows(tk, tb, self.stack)
+            # re-partition T from per-vertex rows (tile 1 along k) to the
+            # E2 tiles (tile_e2 along k): the Sec. 6 repartition
+            w = self.w
+            if self.measure_rp:
+                ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+                ev[0].record()
+            n_in, row = int(tk.shape[0]), int(tb.numel() // max(int(tk.shape[0]), 1))
+            tk, tb = tre.repartition("ki", "k", "k", {"k": w["n"], "i": w["emb"]}, {"k": 1}, {"k": self.stack},
+                                     tk, tb)
+            if self.measure_rp:
+                ev[1].record()
+                torch.cuda.synchronize()
+                eb = tb.element_size()
+                self.rp_report = {"ms": ev[0].elapsed_time(ev[1]), "n_in": n_in, "n_out": int(tk.shape[0]),
+                                  "alg_bytes": (n_in * row + tb.numel()) * eb}
+                self.rp_report["GBs"] = self.rp_report["alg_bytes"] / (self.rp_report["ms"] * 1e-3) / 1e9
         self.e2.n_u = int(tk.shape[0])
         return self.e2.run(tk, tb, self.zk, self.zt)
 
@@ -404,9 +421,14 @@ def main():
     # with synchronous library timing, outside the timed region
     for st in stages:
         st.record = tre.Timing()
+    if hasattr(W, "measure_rp"):
+        W.measure_rp = True
     W.step()
     torch.cuda.synchronize()
     phases = {st.name: st.phase_report() for st in stages}
+    if getattr(W, "rp_report", None):
+        phases["repartition"] = W.rp_report
+        W.measure_rp = False
     for st in stages:
         st.record = None
     flops = sum(st.flops() for st in stages)

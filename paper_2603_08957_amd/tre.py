@@ -303,10 +303,21 @@ def repartition(labels: str, upper_in: str, upper_out: str, extents: dict, tiles
                                    ctypes.byref(n_out), None, 0, _stream(stream))
         _check(rc if rc else STATUS_CODE["TRE_E_ARG"], "tre_repartition")
     ws = alloc_workspace(wsb, tiles.device)
-    te_out = 1
+    te_in = te_out = 1
+    grid = cover = 1
     for c in labels:
-        te_out *= int(tout[ord(c) - 97]) if c in upper_out else int(ext[ord(c) - 97])
-    cap = 0
+        e, ti, to = int(ext[ord(c) - 97]), int(tin[ord(c) - 97]), int(tout[ord(c) - 97])
+        ti = ti if c in upper_in else e
+        te_in *= ti
+        te_out *= to if c in upper_out else e
+        if c in upper_out and to > 0:
+            grid *= e // to
+            cover *= min(e // to, (ti - 1) // to + 2)
+    # first call with room for every target tile the sources can meet when
+    # that costs little memory; otherwise the call reports the count first
+    bound = min(grid, n * cover)
+    esz = tiles.element_size()
+    cap = bound if bound * te_out * esz <= max(2 * n * te_in * esz, 1 << 26) else 0
     while True:
         out_keys = torch.empty((max(cap, 1), len(upper_out)), dtype=torch.int32, device=tiles.device)
         out_tiles = torch.empty((max(cap, 1), te_out), dtype=tiles.dtype, device=tiles.device)

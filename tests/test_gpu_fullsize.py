@@ -160,8 +160,8 @@ def run_gnn(orc, c):
     # glue and E2 on the GPU
     tk, tt = o1.w_keys, o1.w_tiles
     stack = w["tile_e2"] // w["tile_e1"]
-    if stack > 1:
-        tk, tt = tre.stack_rows(tk, tt, stack)
+    if stack > 1:  # re-partition T (Sec. 6) from per-vertex rows to E2's tiles
+        tk, tt = tre.repartition("ki", "k", "k", {"k": w["n"], "i": w["emb"]}, {"k": 1}, {"k": stack}, tk, tt)
     tb = tre.cast_f32_bf16(tt).view(tt.shape) if bf else tt
     p2 = tre.Plan.from_spec(w["E2"])
     o2 = tre.einsum(p2, tk, tb, dev(w["Z"]["keys"]), dev(w["Z"]["tiles"], bf), want_pairs=True)
@@ -183,7 +183,8 @@ def run_gnn(orc, c):
     t32 = acc1.astype(np.float32)
     kk, tiles = need, t32
     if stack > 1:
-        kk, tiles = orc.stack_rows(need[:, 0], t32, stack)
+        kk, tiles = orc.repartition("ki", "k", "k", {"k": w["n"], "i": w["emb"]}, {"k": 1}, {"k": stack}, need, t32)
+        tiles = tiles.astype(np.float32)
     op2 = orc_plan(orc, w["E2"])
     if bf:
         Tin = {"keys": kk, "tiles": orc.f32_to_bf16(tiles), "dtype": "bf16"}

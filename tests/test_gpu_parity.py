@@ -363,6 +363,60 @@ def test_repartition_gpu(orc, seed):
     assert np.array_equal(got.reshape(rt.shape), rt)
 
 
+# Larger decompositions, each chosen for one path of the device copy: whole
+# rows stacked (target order already sorted, 16-byte chunks, one run per
+# pair), rows unstacked, row blocks to column blocks (sorted, many 16-byte
+# runs per pair), ragged boxes of unequal size (element chunks, binary
+# search over the pair prefix), a demoted inner label, and more pairs than
+# the copy grid holds workgroups (the batch loop).
+_RP_LARGE = [
+    ("ki", "k", "k", {"k": 8192, "i": 256}, {"k": 1}, {"k": 256}, "bf16", 1.0),
+    ("ki", "k", "k", {"k": 8192, "i": 256}, {"k": 256}, {"k": 1}, "bf16", 1.0),
+    ("ij", "i", "j", {"i": 512, "j": 512}, {"i": 64}, {"j": 64}, "f32", 1.0),
+    ("ij", "ij", "ij", {"i": 960, "j": 900}, {"i": 32, "j": 30}, {"i": 24, "j": 45}, "f32", 0.6),
+    ("ij", "ij", "ij", {"i": 1200, "j": 960}, {"i": 40, "j": 12}, {"i": 24, "j": 32}, "bf16", 0.5),
+    ("abc", "ab", "ab", {"a": 256, "b": 512, "c": 16}, {"a": 4, "b": 8}, {"a": 8, "b": 2}, "f32", 0.3),
+    ("k", "k", "k", {"k": 1 << 21}, {"k": 1}, {"k": 8}, "f32", 1.0),
+]
+
+
+@pytest.mark.parametrize("case", range(len(_RP_LARGE)))
+def test_repartition_gpu_large(orc, case):
+    """Bit-exact keys and tiles against the oracle on the cases above."""
+    import itertools
+
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    labels, up_in, up_out, ext, tin, tout, dtype, keep = _RP_LARGE[case]
+    rng = np.random.default_rng(1700 + case)
+    axes = [range(ext[c] // tin[c]) for c in up_in]
+    if keep < 1.0:
+        all_keys = np.array(list(itertools.product(*axes)), np.int32)
+        keys = all_keys[rng.random(len(all_keys)) < keep]
+    else:
+        grids = np.meshgrid(*[np.arange(len(a), dtype=np.int32) for a in axes], indexing="ij")
+        keys = np.stack([g.reshape(-1) for g in grids], axis=1)
+    keys = np.ascontiguousarray(keys.reshape(-1, len(up_in)))
+    te = int(np.prod([tin[c] if c in up_in else ext[c] for c in labels]))
+    vals = rng.standard_normal((len(keys), te)).astype(np.float32)
+    if dtype == "bf16":
+        bits = orc.f32_to_bf16(vals)
+        dev_tiles = torch.from_numpy(bits.view(np.int16)).cuda()
+        ref_vals = orc.bf16_to_f64(bits)
+    else:
+        dev_tiles = torch.from_numpy(vals).cuda()
+        ref_vals = vals.astype(np.float64)
+    say("repartition large", case, labels, up_in, up_out, tin, tout, len(keys), dtype)
+    k2, t2 = tre.repartition(labels, up_in, up_out, ext, tin, tout, torch.from_numpy(keys).cuda(), dev_tiles)
+    rk, rt = orc.repartition(labels, up_in, up_out, ext, tin, tout, keys, ref_vals)
+    assert np.array_equal(k2.cpu().numpy().reshape(rk.shape), rk)
+    got = t2.cpu().numpy()
+    got = orc.bf16_to_f64(got.view(np.uint16)) if dtype == "bf16" else got.astype(np.float64)
+    assert np.array_equal(got.reshape(rt.shape), rt)
+
+
 def test_repartition_gpu_paper_example_and_stack(orc):
     import torch
 
