@@ -376,3 +376,6 @@ def repartition(labels: str, up_in: str, up_out: str, extents: dict, tiles_in: d
     L.orc_free(kp)
     L.orc_free(tp)
     return ko.reshape(no, r_out), to.reshape(no, te_out)
+
+
+from .three_operand import Spec3Error, eval3, parse3  # noqa: E402  (numpy oracle of the 3-operand EinSum)

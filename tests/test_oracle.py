@@ -565,3 +565,130 @@ def test_repartition_errors(orc):
     with pytest.raises(orc.OracleError):
         orc.repartition("ij", "ik", "i", {"i": 4, "j": 4}, {"i": 1}, {"i": 2}, np.zeros((0, 2), np.int32),
                         np.zeros((0, 4)))
+
+
+# ------------------------------------------ the three-operand EinSum (eval3)
+
+_E3 = "ijk,jr,kr->ir"
+
+
+def _three_way_case(seed, n=32, r=6, block=4, density=0.08, fill=0.3, drop=0.25):
+    """A small sparse 3-way case whose B and C miss some blocks (so the
+    triple join drops tuples)."""
+    w = workloads.sparse_3way(n, r, block, density, fill, seed=seed)
+    rng = np.random.default_rng(seed + 1)
+    for name in ("B", "C"):
+        keep = rng.random(len(w[name]["keys"])) >= drop
+        keep[0] = True
+        w[name] = {"keys": w[name]["keys"][keep], "tiles": w[name]["tiles"][keep], "dtype": "f32"}
+    ext = {"i": n, "j": n, "k": n, "r": r}
+    til = {"i": block, "j": block, "k": block}
+    return w, ext, til
+
+
+def test_eval3_matches_binary_path(orc):
+    """The triple evaluation equals the two-EinSum path through the C oracle
+    (E1 = T join B on j, E2 = W join C on k): same keys, same values."""
+    for seed in (3, 4):
+        w, ext, til = _three_way_case(seed)
+        wk, acc, mag, tri = orc.eval3(_E3, "ijk", ext, til, w["T"], w["B"], w["C"])
+        p1 = orc.Plan("ijk,jr->ikr", "ijk", ext, til)
+        p2 = orc.Plan("ikr,kr->ir", "ik", {"i": ext["i"], "k": ext["k"], "r": ext["r"]},
+                      {"i": til["i"], "k": til["k"]})
+        r1 = orc.run(p1, w["T"], w["B"])
+        r2 = orc.run(p2, {"keys": r1.wkeys, "tiles": r1.acc, "dtype": "f64"}, w["C"])
+        assert np.array_equal(wk, r2.wkeys)
+        np.testing.assert_allclose(acc, r2.acc, rtol=1e-12, atol=1e-12)
+        assert (mag >= np.abs(acc) - 1e-12).all()
+        assert len(tri) < len(w["T"]["keys"])  # some T blocks lost their B or C partner
+
+
+def test_eval3_brute_force(orc):
+    """Pure-Python loops over every global coordinate of the dense tensors
+    (absent tuples are zero) give the same values; the output keys are the
+    I blocks of T tuples whose J block is in B and K block in C."""
+    w, ext, til = _three_way_case(7, n=16, r=3, block=4, density=0.2, fill=0.5)
+    wk, acc, mag, tri = orc.eval3(_E3, "ijk", ext, til, w["T"], w["B"], w["C"])
+    T = dense_of("ijk", "ijk", ext, til, w["T"]["keys"], vals_f64(w["T"]))
+    B = dense_of("jr", "j", ext, til, w["B"]["keys"], vals_f64(w["B"]))
+    C = dense_of("kr", "k", ext, til, w["C"]["keys"], vals_f64(w["C"]))
+    n, r = ext["i"], ext["r"]
+    A = [[0.0] * r for _ in range(n)]
+    for i in range(n):
+        for j in range(n):
+            for k in range(n):
+                t = T[i, j, k]
+                if t == 0.0:
+                    continue
+                for q in range(r):
+                    A[i][q] += t * B[j, q] * C[k, q]
+    bj = {int(k[0]) for k in w["B"]["keys"]}
+    ck = {int(k[0]) for k in w["C"]["keys"]}
+    want_keys = sorted({int(I) for I, J, K in w["T"]["keys"] if int(J) in bj and int(K) in ck})
+    assert wk.reshape(-1).tolist() == want_keys
+    got = dense_of("ir", "i", ext, til, wk, acc)
+    np.testing.assert_allclose(got, np.array(A), rtol=1e-12, atol=1e-12)
+    # blocks outside the key set hold nothing
+    mask = np.zeros(n, bool)
+    for I in want_keys:
+        mask[I * til["i"]:(I + 1) * til["i"]] = True
+    assert np.all(np.array(A)[~mask] == 0.0)
+
+
+def test_eval3_label_order_invariance(orc):
+    """Renaming the roles and transposing every operand (U as "ikj", the two
+    small operands swapped and one stored transposed, W as "ri") gives the
+    transposed result."""
+    w, ext, til = _three_way_case(5)
+    wk, acc, _, _ = orc.eval3(_E3, "ijk", ext, til, w["T"], w["B"], w["C"])
+    bt = til["i"]
+    T2 = w["T"]["tiles"].reshape(-1, bt, bt, bt).transpose(0, 1, 3, 2).reshape(len(w["T"]["keys"]), -1)
+    order = np.lexsort((w["T"]["keys"][:, 1], w["T"]["keys"][:, 2], w["T"]["keys"][:, 0]))
+    U2 = {"keys": np.ascontiguousarray(w["T"]["keys"][order][:, [0, 2, 1]]), "tiles": T2[order], "dtype": "f32"}
+    r = ext["r"]
+    B2 = {"keys": w["B"]["keys"], "tiles": w["B"]["tiles"].reshape(-1, bt, r).transpose(0, 2, 1).reshape(
+        len(w["B"]["keys"]), -1), "dtype": "f32"}
+    wk2, acc2, _, _ = orc.eval3("ikj,kr,rj->ri", "ijk", ext, til, U2, w["C"], B2)
+    assert np.array_equal(wk2, wk)
+    np.testing.assert_allclose(acc2.reshape(-1, r, bt).transpose(0, 2, 1).reshape(acc.shape), acc,
+                               rtol=1e-12, atol=1e-12)
+
+
+def test_eval3_magnitude_positive_inputs(orc):
+    """With non-negative inputs the magnitude sum equals the sum itself."""
+    w, ext, til = _three_way_case(9)
+    for name in ("T", "B", "C"):
+        w[name]["tiles"] = np.abs(w[name]["tiles"])
+    _, acc, mag, _ = orc.eval3(_E3, "ijk", ext, til, w["T"], w["B"], w["C"])
+    np.testing.assert_allclose(mag, acc, rtol=1e-13, atol=0)
+
+
+@pytest.mark.parametrize("einsum,upper,cat", [
+    ("ijk,jr->ir", "ijk", "PARSE"),
+    ("ijk,jr,kq->ir", "ijk", "SPLIT"),      # small operands share no label
+    ("ijk,jr,jr->ir", "ijk", "SPLIT"),      # both meet U on j
+    ("ijk,jr,kr->ikr", "ijk", "SPLIT"),     # W keeps a joined label
+    ("jik,jr,kr->ir", "ijk", "SPLIT"),      # joined labels not U's last two
+    ("ijk,jr,kr->ir", "ik", "SPLIT"),       # joined label demoted
+    ("ijk,jr,kr->ir", "ijkr", "SPLIT"),     # shared label promoted
+])
+def test_eval3_structure_errors(orc, einsum, upper, cat):
+    ext = {c: 8 for c in "ijkrq"}
+    til = {c: 4 for c in "ijkrq"}
+    with pytest.raises(orc.Spec3Error) as e:
+        orc.parse3(einsum, upper, ext, til)
+    assert e.value.category == cat
+
+
+def test_eval3_key_errors(orc):
+    w, ext, til = _three_way_case(3)
+    bad = dict(w["T"])
+    bad["keys"] = w["T"]["keys"][::-1].copy()
+    with pytest.raises(orc.Spec3Error) as e:
+        orc.eval3(_E3, "ijk", ext, til, bad, w["B"], w["C"])
+    assert e.value.category == "UNSORTED"
+    bad["keys"] = w["T"]["keys"].copy()
+    bad["keys"][0, 0] = ext["i"]
+    with pytest.raises(orc.Spec3Error) as e:
+        orc.eval3(_E3, "ijk", ext, til, bad, w["B"], w["C"])
+    assert e.value.category == "KEYRANGE"
