@@ -243,6 +243,52 @@ tre_status tre_repartition(const char *labels, const char *upper_in, const char 
                            int32_t *keys_out, void *tiles_out, int64_t out_cap, int64_t *n_out, void *ws,
                            size_t ws_bytes, void *stream);
 
+/* --- non-binary EinSum (Sec. 8) ------------------------------------------- */
+
+/* tre_execute3 -- one three-operand EinSum "U,V,X->W" whose two small
+ * operands each meet U on a promoted label of their own and share one
+ * demoted label r with the output, e.g. A[i,r] = sum_jk T[i,j,k] B[j,r] C[k,r]
+ * (the non-binary EinSum of Sec. 8).  Instead of two binary EinSums (U join
+ * V, then that result join X), U is joined with V and X in one pass (the join
+ * of Sec. 5 over three relations): every U tuple whose key on a has a V tuple
+ * and whose key on b has an X tuple forms a triple, each triple contributes
+ * the tile EinSum of its three tiles, and the contributions are summed per
+ * output key (GROUP BY W's promoted labels) in U order, atomic-free, as in
+ * tre_contract.  No intermediate relation is materialised.
+ * Structure (TRE_E_PARSE / TRE_E_SPLIT otherwise):
+ *   - V and X have two labels each and share exactly one, r, which is not in
+ *     U and is demoted; V's other label a and X's other label b are promoted
+ *     labels of U and are U's last two labels, in either order;
+ *   - W's labels are U's labels other than a and b, plus r, in any order.
+ * Shapes (TRE_E_SHAPE otherwise): tiles divide extents; the tile extent of
+ * U's last label is a multiple of 4; the tile extents of U's last two labels
+ * are at most 64 each.  in_dtype: TRE_F32 only (TRE_E_DTYPE otherwise).
+ *   extent, tile : host [26] per letter, as for tre_plan.
+ *   u_keys [n_u x r_U], v_keys [n_v x 1], x_keys [n_x x 1]: device int32,
+ *                  sorted strictly increasing (U keyed by its promoted labels
+ *                  in string order, V by a, X by b).
+ *   u_tiles, v_tiles, x_tiles: device fp32 tiles, 16-byte aligned, row-major
+ *                  over each operand's labels in string order.
+ *   w_keys  : device [w_cap x r_W] int32 (may be NULL when r_W = 0), sorted;
+ *   w_tiles : device [w_cap x tile_elems(W)] fp32.
+ *   n_w, n_triples: host; written also with TRE_E_CAPACITY.
+ *   ws, ws_bytes: device workspace, 256-byte aligned, at least
+ *                  tre_execute3_workspace_bytes(...) (0 on bad arguments).
+ *   timing  : optional (deferred mode as for tre_contract); join_ms covers
+ *             validation, the triple join and the output keys, units_ms the
+ *             work units, contract_ms the fused contraction kernel,
+ *             reduce_ms the sum of split keys and the key write-out.
+ * Synchronizes the stream twice (triple count, output key count); key errors
+ * as TRE_E_UNSORTED / TRE_E_DUPKEY / TRE_E_KEYRANGE. */
+size_t tre_execute3_workspace_bytes(const char *einsum, const char *upper, const int64_t *extent,
+                                    const int32_t *tile, int64_t n_u);
+tre_status tre_execute3(const char *einsum, const char *upper, const int64_t *extent, const int32_t *tile,
+                        tre_dtype in_dtype, const int32_t *u_keys, int64_t n_u, const void *u_tiles,
+                        const int32_t *v_keys, int64_t n_v, const void *v_tiles, const int32_t *x_keys,
+                        int64_t n_x, const void *x_tiles, int32_t *w_keys, float *w_tiles, int64_t w_cap,
+                        int64_t *n_w, int64_t *n_triples, void *ws, size_t ws_bytes, void *stream,
+                        tre_timing *timing);
+
 /* --- input preparation --------------------------------------------------- */
 
 /* Materialise tiles from scalar entries: tiles[slot[e] * tile_elems + offset[e]]

@@ -8,6 +8,6 @@ library ``libtre.so`` through the C ABI in ``include/tre.h``; this package is
 its ctypes binding.
 """
 from .tre import (  # noqa: F401
-    EXPORTS, JoinResult, Output, Plan, TreError, Timing, alloc_workspace, cast_f32_bf16, contract, einsum, join, lib,
-    repartition, stack_rows, tiles_from_entries,
+    EXPORTS, Einsum3, JoinResult, Output, Plan, TreError, Timing, alloc_workspace, cast_f32_bf16, contract, einsum,
+    execute3, join, lib, repartition, stack_rows, tiles_from_entries,
 )

@@ -18,45 +18,6 @@ tre_status dev_fail(hipError_t e, const char* where) {
     return TRE_E_DEVICE;
 }
 
-// hipEvent timer.  In deferred mode the events are handed to the caller's
-// tre_timing and read later by tre_timing_read.
-struct Timer {
-    bool on = false;
-    bool keep = false;
-    hipEvent_t ev[4] = {};
-    int n = 0;
-    explicit Timer(bool enable, bool deferred = false) : on(enable), keep(deferred) {
-        if (on)
-            for (auto& e : ev)
-                if (hipEventCreate(&e) != hipSuccess) on = false;
-    }
-    ~Timer() {
-        if (keep && on) return;
-        for (auto& e : ev)
-            if (e) (void)hipEventDestroy(e);
-    }
-    void mark(hipStream_t s) {
-        if (on && n < 4) (void)hipEventRecord(ev[n++], s);
-    }
-    float between(int a, int b) {
-        float ms = 0.f;
-        if (on && b < n) {
-            (void)hipEventSynchronize(ev[b]);
-            (void)hipEventElapsedTime(&ms, ev[a], ev[b]);
-        }
-        return ms;
-    }
-};
-
-float elapsed(void* a, void* b) {
-    float ms = 0.f;
-    if (a && b) {
-        (void)hipEventSynchronize(reinterpret_cast<hipEvent_t>(b));
-        (void)hipEventElapsedTime(&ms, reinterpret_cast<hipEvent_t>(a), reinterpret_cast<hipEvent_t>(b));
-    }
-    return ms;
-}
-
 tre_status key_error(int32_t flags) {
     if (flags & 4) return TRE_E_KEYRANGE;
     if (flags & 1) return TRE_E_UNSORTED;
@@ -188,7 +149,7 @@ tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const i
     const Layout L = make_layout(p, n_u, n_v, max_pairs);
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     char* w = reinterpret_cast<char*>(ws);
-    Timer tm(timing != nullptr);
+    PhaseTimer tm(timing != nullptr);
     tm.mark(s);
     hipError_t e = launch_fill_zero(w + L.hdr, sizeof(WsHeader), s);
     if (e != hipSuccess) return dev_fail(e, "header");
@@ -278,7 +239,7 @@ tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* 
     const Layout L = make_layout(p, jr->n_u, jr->n_v, int64_t(jr->internal[4]));
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const bool deferred = timing && timing->deferred;
-    Timer tm(timing != nullptr, deferred);
+    PhaseTimer tm(timing != nullptr);
     tm.mark(s);
     const int64_t slots = (p.kclass == KC_GEMM && p.fast) ? gemm_paced_slots(p) : 0;
     const int32_t pace = choose_pacing(p, jr->n_u, n_pairs, n_w, slots);
@@ -314,6 +275,7 @@ tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* 
         if (deferred && tm.on) {
             for (int i = 0; i < 4; i++) timing->events[i] = reinterpret_cast<void*>(tm.ev[i]);
             timing->pending = 1;
+            tm.keep = true;
         } else {
             timing->units_ms = tm.between(0, 1);
             timing->contract_ms = tm.between(1, 2);
@@ -333,10 +295,10 @@ tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* 
 tre_status tre_timing_read(tre_timing* t) {
     if (!t) return TRE_E_ARG;
     if (!t->pending) return TRE_OK;
-    t->units_ms = elapsed(t->events[0], t->events[1]);
-    t->contract_ms = elapsed(t->events[1], t->events[2]);
-    t->reduce_ms = elapsed(t->events[2], t->events[3]);
-    t->total_ms += elapsed(t->events[0], t->events[3]);
+    t->units_ms = event_elapsed(t->events[0], t->events[1]);
+    t->contract_ms = event_elapsed(t->events[1], t->events[2]);
+    t->reduce_ms = event_elapsed(t->events[2], t->events[3]);
+    t->total_ms += event_elapsed(t->events[0], t->events[3]);
     for (auto& e : t->events) {
         if (e) (void)hipEventDestroy(reinterpret_cast<hipEvent_t>(e));
         e = nullptr;

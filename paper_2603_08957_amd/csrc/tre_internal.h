@@ -180,6 +180,51 @@ size_t stack_ws_bytes(int64_t n);
 
 void set_error(const std::string& msg);
 
+// hipEvent timer.  In deferred mode the events are handed to the caller's
+// tre_timing (keep = true) and read and released later by tre_timing_read.
+struct PhaseTimer {
+    static constexpr int kMax = 5;
+    bool on = false;
+    bool keep = false;  // set once the events are handed to a deferred tre_timing
+    hipEvent_t ev[kMax] = {};
+    int n = 0;
+    explicit PhaseTimer(bool enable) : on(enable) {}
+    ~PhaseTimer() {
+        if (keep) return;
+        for (auto& e : ev)
+            if (e) (void)hipEventDestroy(e);
+    }
+    // events are created when first recorded, so a deferred timer hands over
+    // exactly the events it recorded
+    void mark(hipStream_t s) {
+        if (!on || n >= kMax) return;
+        if (hipEventCreate(&ev[n]) != hipSuccess) {
+            ev[n] = nullptr;
+            on = false;
+            return;
+        }
+        (void)hipEventRecord(ev[n++], s);
+    }
+    float between(int a, int b) {
+        float ms = 0.f;
+        if (on && b < n) {
+            (void)hipEventSynchronize(ev[b]);
+            (void)hipEventElapsedTime(&ms, ev[a], ev[b]);
+        }
+        return ms;
+    }
+};
+
+inline float event_elapsed(void* a, void* b) {
+    float ms = 0.f;
+    if (a && b) {
+        (void)hipEventSynchronize(reinterpret_cast<hipEvent_t>(b));
+        (void)hipEventElapsedTime(&ms, reinterpret_cast<hipEvent_t>(a), reinterpret_cast<hipEvent_t>(b));
+    }
+    return ms;
+}
+
+
 }  // namespace tre
 
 // Opaque plan handle of the C ABI.

@@ -28,7 +28,7 @@ EXPORTS = [
     "tre_plan", "tre_plan_get_info", "tre_plan_destroy", "tre_workspace_bytes", "tre_workspace_max_pairs",
     "tre_join", "tre_contract", "tre_execute", "tre_timing_read", "tre_cast_f32_bf16", "tre_stack_workspace_bytes", "tre_stack_rows",
     "tre_tiles_from_entries", "tre_status_str", "tre_last_error", "tre_version",
-    "tre_repartition_workspace_bytes", "tre_repartition",
+    "tre_repartition_workspace_bytes", "tre_repartition", "tre_execute3_workspace_bytes", "tre_execute3",
 ]
 
 
@@ -105,6 +105,10 @@ def lib():
         L.tre_repartition_workspace_bytes.argtypes = [cs, cs, cs, P, P, P, i64]
         L.tre_repartition_workspace_bytes.restype = sz
         L.tre_repartition.argtypes = [cs, cs, cs, P, P, P, i32, P, i64, P, P, P, i64, P, P, sz, P]
+        L.tre_execute3_workspace_bytes.argtypes = [cs, cs, P, P, i64]
+        L.tre_execute3_workspace_bytes.restype = sz
+        L.tre_execute3.argtypes = [cs, cs, P, P, ctypes.c_int, P, i64, P, P, i64, P, P, i64, P, P, P, i64, P, P, P, sz,
+                                   P, P]
         L.tre_status_str.restype = ctypes.c_char_p
         L.tre_last_error.restype = ctypes.c_char_p
         L.tre_version.restype = ctypes.c_char_p
@@ -340,3 +344,77 @@ def tiles_from_entries(slot, offset, values, n_tiles: int, tile_elems: int, stre
                                       values.element_size(), _ptr(tiles), n_tiles, tile_elems, _stream(stream))
     _check(rc, "tre_tiles_from_entries")
     return tiles
+
+
+class Einsum3:
+    """One three-operand EinSum "U,V,X->W" (see tre_execute3): U joined with V
+    and X in one pass, one fused contraction per matched triple.  Holds the
+    letter-indexed shape arrays and a workspace sized for ``n_u_max``."""
+
+    def __init__(self, einsum: str, upper: str, extents: dict, tiles: dict, n_u_max: int, device="cuda"):
+        import numpy as _np
+
+        self.einsum, self.upper = einsum, upper
+        self._ext = _np.zeros(26, dtype=_np.int64)
+        self._tile = _np.ones(26, dtype=_np.int32)
+        for k, v in extents.items():
+            self._ext[ord(k) - 97] = v
+        for k, v in (tiles or {}).items():
+            self._tile[ord(k) - 97] = v
+        w = einsum.split("->")[1]
+        self.w_arity = sum(1 for c in w if c in upper)
+        self.w_tile_elems = 1
+        self.w_key_space = 1
+        for c in w:
+            e, t = int(self._ext[ord(c) - 97]), int(self._tile[ord(c) - 97])
+            self.w_tile_elems *= t if c in upper else e
+            if c in upper:
+                self.w_key_space *= e // t
+        self.n_u_max = int(n_u_max)
+        wsb = int(lib().tre_execute3_workspace_bytes(*self._args(), self.n_u_max))
+        if wsb == 0:  # bad arguments: let the call itself name the error
+            n_w, n_t = ctypes.c_int64(0), ctypes.c_int64(0)
+            rc = lib().tre_execute3(*self._args(), 0, None, 0, None, None, 0, None, None, 0, None, None, None, 0,
+                                    ctypes.byref(n_w), ctypes.byref(n_t), None, 0, None, None)
+            _check(rc if rc else STATUS_CODE["TRE_E_ARG"], "tre_execute3")
+        self.ws = alloc_workspace(wsb, device)
+
+    def _args(self):
+        return (self.einsum.encode(), self.upper.encode(), self._ext.ctypes.data_as(ctypes.c_void_p),
+                self._tile.ctypes.data_as(ctypes.c_void_p))
+
+    def __call__(self, u_keys, u_tiles, v_keys, v_tiles, x_keys, x_tiles, stream=None, timing: Timing | None = None,
+                 out=None):
+        """Returns (w_keys int32 [n_w, r_W], w_tiles float32 [n_w, tile_elems(W)], n_triples).
+        ``out`` = (w_keys, w_tiles) preallocated buffers (their row count is the capacity)."""
+        import torch
+
+        n_u, n_v, n_x = int(u_tiles.shape[0]), int(v_tiles.shape[0]), int(x_tiles.shape[0])
+        if n_u > self.n_u_max:
+            raise ValueError(f"n_u {n_u} above the workspace sizing {self.n_u_max}")
+        dev = u_tiles.device
+        if out is None:
+            cap = min(n_u, self.w_key_space)
+            out = (torch.empty((max(cap, 1), self.w_arity), dtype=torch.int32, device=dev),
+                   torch.empty((max(cap, 1), self.w_tile_elems), dtype=torch.float32, device=dev))
+            cap_given = cap
+        else:
+            cap_given = int(out[1].shape[0])
+        n_w, n_t = ctypes.c_int64(0), ctypes.c_int64(0)
+        rc = lib().tre_execute3(*self._args(), 0, _ptr(u_keys), n_u, _ptr(u_tiles), _ptr(v_keys), n_v, _ptr(v_tiles),
+                                _ptr(x_keys), n_x, _ptr(x_tiles), _ptr(out[0]) if self.w_arity else None,
+                                _ptr(out[1]), cap_given, ctypes.byref(n_w), ctypes.byref(n_t), _ptr(self.ws),
+                                self.ws.numel(), _stream(stream), ctypes.byref(timing) if timing is not None else None)
+        _check(rc, "tre_execute3")
+        k = int(n_w.value)
+        return out[0][:k], out[1][:k], int(n_t.value)
+
+
+def execute3(einsum: str, upper: str, extents: dict, tiles: dict, u_keys, u_tiles, v_keys, v_tiles, x_keys, x_tiles,
+             stream=None, timing: bool = False):
+    """One-shot tre_execute3 with a fresh workspace; returns (w_keys, w_tiles,
+    n_triples[, timing dict])."""
+    op = Einsum3(einsum, upper, extents, tiles, int(u_tiles.shape[0]), u_tiles.device)
+    tm = Timing() if timing else None
+    wk, wt, nt = op(u_keys, u_tiles, v_keys, v_tiles, x_keys, x_tiles, stream, tm)
+    return (wk, wt, nt, tm.as_dict()) if timing else (wk, wt, nt)
