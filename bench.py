@@ -111,6 +111,63 @@ class Stage:
         return self.n_u * self.tile_bytes(0) + self.n_v * self.tile_bytes(1) + self.n_w * self.tile_bytes(2)
 
 
+class FusedStage:
+    """The three-operand EinSum through tre_execute3 (one triple join, one
+    fused contraction per matched triple, no intermediate relation), with
+    the same reporting interface as Stage."""
+
+    def __init__(self, tre, torch, einsum, upper, extents, tiles, n_u, n_v, n_x, name):
+        import types
+
+        self.tre, self.torch, self.name = tre, torch, name
+        self.op = tre.Einsum3(einsum, upper, extents, tiles, n_u)
+        self.spec = {"einsum": einsum, "upper": upper, "extents": extents, "tiles": tiles, "dtype": "f32"}
+        lhs, w = einsum.split("->")
+        ops = lhs.split(",")
+        te = [int(np.prod([tiles[c] if c in upper else extents[c] for c in op])) for op in ops + [w]]
+        self.te = te
+        u = ops[0]
+        r = (set(ops[1]) & set(ops[2])).pop()
+        # dense tile flops per triple: rows x r x the two contracted tile extents, x 2
+        fpt = 2 * (te[0] // (tiles[u[-2]] * tiles[u[-1]])) * extents[r] * tiles[u[-2]] * tiles[u[-1]]
+        self.plan = types.SimpleNamespace(kernel_class="fused three-operand MFMA", flops_per_pair=fpt,
+                                          key_arity=[len([c for c in op if c in upper]) for op in ops + [w]])
+        self.n_u, self.n_v, self.n_x = n_u, n_v, n_x
+        self.n_pairs = 0
+        self.n_w = 0
+        self.out = None
+        self.record = None
+
+    def run(self, uk, ut, vk, vt, xk, xt, timing=None):
+        if self.record is not None:
+            timing = self.record
+            timing.deferred = 0
+        if self.out is None:
+            cap = min(self.n_u, self.op.w_key_space)
+            self.out = (self.torch.empty((cap, max(self.op.w_arity, 1)), dtype=self.torch.int32, device="cuda"),
+                        self.torch.empty((cap, self.op.w_tile_elems), dtype=self.torch.float32, device="cuda"))
+        wk, wt, nt = self.op(uk, ut, vk, vt, xk, xt, timing=timing, out=self.out)
+        self.n_pairs, self.n_w = nt, int(wk.shape[0])
+        return wk, wt
+
+    def flops(self):
+        return self.n_pairs * self.plan.flops_per_pair
+
+    def alg_bytes(self):
+        """Read every input tuple once, write every output tile once."""
+        return 4 * (self.n_u * self.te[0] + self.n_v * self.te[1] + self.n_x * self.te[2] + self.n_w * self.te[3])
+
+    def phase_report(self):
+        t = self.record
+        jb = 4 * (self.n_u * self.plan.key_arity[0] + self.n_v + self.n_x) + 12 * self.n_pairs + 12 * self.n_w
+        gbs = lambda b, ms: (b / (ms * 1e-3) / 1e9) if ms > 0 else None  # noqa: E731
+        return {"join_ms": t.join_ms, "join_alg_bytes": jb, "join_GBs": gbs(jb, t.join_ms),
+                "contract_ms": t.contract_ms, "contract_alg_bytes": self.alg_bytes(),
+                "contract_GBs": gbs(self.alg_bytes(), t.contract_ms),
+                "contract_TFLOPs": self.flops() / (t.contract_ms * 1e-3) / 1e12 if t.contract_ms > 0 else None,
+                "units_ms": t.units_ms, "reduce_ms": t.reduce_ms, "n_triples": self.n_pairs}
+
+
 # ------------------------------------------------------------ workloads
 
 class GnnChain:
@@ -272,33 +329,45 @@ class BlockSparse:
 
 
 class ThreeWay:
-    def __init__(self, c, tre, torch):
+    def __init__(self, c, tre, torch, path="fused"):
         import workloads
 
         w = workloads.config(c)
-        self.w, self.tre, self.torch = w, tre, torch
+        self.w, self.tre, self.torch, self.path = w, tre, torch, path
         self.tk, self.tt = dev_rel(w["T"], torch)
         self.bk, self.bt = dev_rel(w["B"], torch)
         self.ck, self.ct = dev_rel(w["C"], torch)
         n = len(w["T"]["keys"])
-        self.e1 = Stage(tre, torch, w["E1"], n, len(w["B"]["keys"]), n, "E1")
-        self.e2 = Stage(tre, torch, w["E2"], n, len(w["C"]["keys"]), n, "E2")
+        if path == "fused":
+            ext = {"i": w["n"], "j": w["n"], "k": w["n"], "r": w["r"]}
+            til = {c: w["block"] for c in "ijk"}
+            self.f3 = FusedStage(tre, torch, "ijk,jr,kr->ir", "ijk", ext, til, n, len(w["B"]["keys"]),
+                                 len(w["C"]["keys"]), "E3")
+        else:
+            self.e1 = Stage(tre, torch, w["E1"], n, len(w["B"]["keys"]), n, "E1")
+            self.e2 = Stage(tre, torch, w["E2"], n, len(w["C"]["keys"]), n, "E2")
 
     def step(self, timing=None):
+        if self.path == "fused":
+            return self.f3.run(self.tk, self.tt, self.bk, self.bt, self.ck, self.ct, timing=timing)
         wk, wt = self.e1.run(self.tk, self.tt, self.bk, self.bt, timing=timing)
         self.e2.n_u = int(wk.shape[0])
         return self.e2.run(wk, wt, self.ck, self.ct)
 
     def stages(self):
-        return [self.e1, self.e2]
+        return [self.f3] if self.path == "fused" else [self.e1, self.e2]
 
     def describe(self):
         w = self.w
+        how = ("one three-operand EinSum ijk,jr,kr->ir (fused: triple join + Khatri-Rao MFMA contraction)"
+               if self.path == "fused" else "two binary EinSums ijk,jr->ikr then ikr,kr->ir")
         return {"workload": f"sparse 3-way A[i,r] = sum_jk T[i,j,k] B[j,r] C[k,r], fp32: T {w['n']}^3 as "
-                            f"{w['block']}^3 blocks (0.5% of blocks, 10% dense), r {w['r']}",
-                "t_blocks": len(w["T"]["keys"])}
+                            f"{w['block']}^3 blocks (0.5% of blocks, 10% dense), r {w['r']}; {how}",
+                "t_blocks": len(w["T"]["keys"]), "path": self.path}
 
     def oracle_sample(self, orc, n_keys=1):
+        if self.path == "fused":
+            return self._oracle_sample_fused(orc)
         w = self.w
         p = orc.Plan(w["E1"]["einsum"], w["E1"]["upper"], w["E1"]["extents"], w["E1"]["tiles"])
         keys = w["T"]["keys"]
@@ -312,6 +381,32 @@ class ThreeWay:
         flops = int(mu.sum()) * self.e1.plan.flops_per_pair
         return {"value": flops / secs / 1e9, "unit": "GFLOP/s", "cores": 1, "kind": "oracle",
                 "sample": f"E1 restricted to 64 output keys ({int(mu.sum())} tile pairs), {secs:.1f} s",
+                "seconds": secs}
+
+    def _oracle_sample_fused(self, orc, budget_s=10.0):
+        """The oracle's per-triple evaluation on the T tuples of the first
+        output keys (I blocks), one key at a time until about budget_s."""
+        from threadpoolctl import threadpool_info
+
+        w = self.w
+        ext = {"i": w["n"], "j": w["n"], "k": w["n"], "r": w["r"]}
+        til = {c: w["block"] for c in "ijk"}
+        tk = w["T"]["keys"]
+        secs, n_tri, n_keys = 0.0, 0, 0
+        for I in np.unique(tk[:, 0]):
+            sel = tk[:, 0] == I
+            T = {"keys": np.ascontiguousarray(tk[sel]), "tiles": w["T"]["tiles"][sel], "dtype": "f32"}
+            t0 = time.perf_counter()
+            _, _, _, tri = orc.eval3("ijk,jr,kr->ir", "ijk", ext, til, T, w["B"], w["C"])
+            secs += time.perf_counter() - t0
+            n_tri += len(tri)
+            n_keys += 1
+            if secs >= budget_s:
+                break
+        threads = max([int(d.get("num_threads", 1)) for d in threadpool_info()] or [1])
+        flops = n_tri * self.f3.plan.flops_per_pair
+        return {"value": flops / secs / 1e9, "unit": "GFLOP/s", "cores": threads, "kind": "oracle",
+                "sample": f"{n_keys} output keys ({n_tri} T blocks), numpy fp64 per-triple einsum, {secs:.1f} s",
                 "seconds": secs}
 
 
@@ -342,13 +437,13 @@ def traffic_record(config):
             "write_bytes": rec["write_bytes_per_launch"], "source": "profiles/" + name}
 
 
-def make_workload(c, tre, torch):
+def make_workload(c, tre, torch, three_way="fused"):
     if c in (1, 2, 5):
         return GnnChain(c, tre, torch)
     if c == 3:
         return BlockSparse(c, tre, torch)
     if c == 4:
-        return ThreeWay(c, tre, torch)
+        return ThreeWay(c, tre, torch, three_way)
     raise SystemExit(f"unknown workload {c}")
 
 
@@ -363,6 +458,8 @@ def main():
                     help="tre_options.u_ranges for every EinSum (0 = library default, < 0 = off)")
     ap.add_argument("--pace-windows", type=int, default=0,
                     help="tre_options.pace_windows for every EinSum (0 = library default, < 0 = off)")
+    ap.add_argument("--three-way", choices=["fused", "binary"], default="fused",
+                    help="workload 4: one fused three-operand EinSum (default) or two binary EinSums")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="first run one device copy of this many GiB (counter calibration under rocprofv3 --pmc)")
     args = ap.parse_args()
@@ -390,7 +487,7 @@ def main():
         del src, dst
     PLAN_OPTIONS["u_ranges"] = args.u_ranges
     PLAN_OPTIONS["pace_windows"] = args.pace_windows
-    W = make_workload(args.config, tre, torch)
+    W = make_workload(args.config, tre, torch, args.three_way)
     log("[bench] inputs resident; warming up")
     for _ in range(args.warmup):
         W.step()

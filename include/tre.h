@@ -275,9 +275,10 @@ tre_status tre_repartition(const char *labels, const char *upper_in, const char 
  *   ws, ws_bytes: device workspace, 256-byte aligned, at least
  *                  tre_execute3_workspace_bytes(...) (0 on bad arguments).
  *   timing  : optional (deferred mode as for tre_contract); join_ms covers
- *             validation, the triple join and the output keys, units_ms the
- *             work units, contract_ms the fused contraction kernel,
- *             reduce_ms the sum of split keys and the key write-out.
+ *             validation, the triple join and the output keys, units_ms is
+ *             empty (each workgroup finds its range of triples itself),
+ *             contract_ms the fused contraction kernel, reduce_ms the sum of
+ *             output blocks split between workgroups and the key write-out.
  * Synchronizes the stream twice (triple count, output key count); key errors
  * as TRE_E_UNSORTED / TRE_E_DUPKEY / TRE_E_KEYRANGE. */
 size_t tre_execute3_workspace_bytes(const char *einsum, const char *upper, const int64_t *extent,

@@ -10,8 +10,7 @@
 // tuples are compacted, in U order, into triples (u, v, x) with their packed
 // output key; a stable radix sort orders them by output key unless W's
 // promoted labels are a prefix of U's key (then U order already is); head
-// flags, a scan and compaction give the output keys and their segments, and
-// segments are cut into bounded work units as in the binary path.
+// flags, a scan and compaction give the output keys and their segments.
 //
 // Tile part: with p, q the last two labels of U (p outer), a U tile is a
 // matrix [M rows = U's other tile labels] x [tp * tq], and one triple
@@ -22,8 +21,14 @@
 // contracted elements (two stages, prefetched one chunk ahead in
 // registers), P and Q of the triple are staged in LDS (Q transposed), and
 // the B operand of each MFMA is formed in registers as P * Q, so KR is never
-// stored.  A unit's triples accumulate in registers; split segments are
-// summed by k3_reduce in unit order (no atomics on values).
+// stored.  When tq is 16, 32 or 64, k3_gemm_q is used instead: it contracts
+// over q' with MFMA (Q held in registers for the whole triple) and scales by
+// P[p', r] afterwards, one multiply-add per output element and p' (measured
+// 0.52 ms against 0.63 ms for k3_gemm on the 4096^3 sparse 3-way workload).
+// The triples are dealt to the resident workgroups in equal
+// contiguous ranges; a workgroup accumulates each segment's part of its range
+// in registers, and segments split between ranges are summed by k3_reduce in
+// range order (no atomics on values).
 #include "tre_internal.h"
 
 #include <algorithm>
@@ -41,7 +46,6 @@ constexpr int kCols = 64;              // output columns (r) per workgroup
 constexpr int kChunk = 128;            // contracted elements per staged chunk
 constexpr int kPitchT = kChunk + 4;    // floats per staged T row
 constexpr int kMaxPQ = 64;             // tile extent limit of p and q
-constexpr int kTargetUnits = 2048;     // about 8 workgroups per CU on 256 CUs
 constexpr int kMaxRows = kMaxDims - 2; // row labels of U
 
 inline unsigned blocks_for(int64_t n) { return unsigned((n + kThreads - 1) / kThreads); }
@@ -71,15 +75,7 @@ struct F3Header {
     int32_t err_u, err_p, err_q, pad0;
     int64_t n_tri;
     int64_t n_w;
-    int64_t n_units;
-    int64_t n_slots;
-    int32_t n_split;
-    int32_t pad1;
-    int64_t pad2[10];
-};
-
-struct F3Unit {
-    int32_t seg, t0, t1, slot;  // triples [t0, t1) of segment seg; slot >= 0: partial tile
+    int64_t pad2[12];
 };
 
 // ------------------------------------------------------------ relational part
@@ -168,42 +164,18 @@ __global__ void k3_segments(const uint64_t* __restrict__ wkey, int64_t n, const 
     }
 }
 
-// Per segment: (units << 32) | partial slots, for one int64 scan.
-__global__ void k3_unit_count(const int32_t* __restrict__ seg_start, int64_t n_w, int64_t per_unit,
-                              int64_t* __restrict__ cnt) {
-    const int64_t q = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (q > n_w) return;
-    if (q == n_w) {
-        cnt[q] = 0;
-        return;
-    }
-    const int64_t len = seg_start[q + 1] - seg_start[q];
-    const int64_t nu = (len + per_unit - 1) / per_unit;
-    cnt[q] = (nu << 32) | (nu > 1 ? nu : 0);
-}
-
-__global__ void k3_unit_fill(const int32_t* __restrict__ seg_start, int64_t n_w, int64_t per_unit,
-                             const int64_t* __restrict__ pref, F3Unit* __restrict__ units,
-                             int32_t* __restrict__ split_list, F3Header* hdr) {
-    const int64_t q = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (q > n_w) return;
-    if (q == n_w) {
-        hdr->n_units = pref[n_w] >> 32;
-        hdr->n_slots = pref[n_w] & 0xffffffffll;
-        return;
-    }
-    const int64_t s0 = seg_start[q], s1 = seg_start[q + 1];
-    const int64_t nu = (s1 - s0 + per_unit - 1) / per_unit;
-    const int64_t ub = pref[q] >> 32, sb = pref[q] & 0xffffffffll;
-    for (int64_t k = 0; k < nu; k++) {
-        const int64_t t0 = s0 + k * per_unit;
-        units[ub + k] = F3Unit{int32_t(q), int32_t(t0), int32_t(min(t0 + per_unit, s1)), nu > 1 ? int32_t(sb + k) : -1};
-    }
-    // split segments in any order: each is summed on its own
-    if (nu > 1) split_list[atomicAdd(&hdr->n_split, 1)] = int32_t(q);
-}
-
 // ------------------------------------------------------------ tile part
+//
+// Work split: the items are (output block, triple) pairs, blk * nt + t, in
+// that order (blk = mb * rblocks + rb), and workgroup b of the n_wg resident
+// workgroups takes items [b * total / n_wg, (b + 1) * total / n_wg), so every
+// workgroup gets the same number of triples to within one.  A workgroup
+// walks its range as pieces, each the part of one (segment, block) inside
+// the range, and accumulates a piece in registers.  A piece that is a whole
+// (segment, block) is written to W; otherwise it goes to a block-sized
+// partial slot -- slot 2b if the segment began in an earlier range, slot
+// 2b + 1 if it only continues into a later one -- and k3_reduce sums the
+// slots of every split (segment, block) in range order (no atomics).
 
 struct F3Args {
     const float* U;
@@ -212,10 +184,13 @@ struct F3Args {
     const int32_t* tu;
     const int32_t* tp;
     const int32_t* tq;
-    const F3Unit* units;
-    const F3Header* hdr;
+    const int32_t* seg_of;     // exclusive scan of the head flags: triple t is in segment seg_of[t + 1] - 1
+    const int32_t* seg_start;  // [n_w + 1]
+    int64_t nt;                // triples
+    int64_t n_wg;              // workgroups of the launch
+    int32_t brows, mblocks;    // output rows per block and row blocks
     float* W;
-    float* part;
+    float* part;               // [2 n_wg][brows][kCols]
     F3Desc d;
 };
 
@@ -230,8 +205,98 @@ __device__ inline int64_t w_row_offset(const F3Desc& d, int64_t m) {
     return off;
 }
 
-// Dynamic LDS: T stages [2][kRows][kPitchT], P slice [tp][kCols], Q slice
-// transposed [kCols][tq + 4] (floats).
+// Where a piece's block of output goes.
+struct Dest {
+    float* base;  // the W tile of the segment, or a partial slot
+    bool slot;    // slot: block-local [brows][kCols]
+    int64_t row0;
+    int col0;
+    __device__ void put(const F3Desc& d, int lr, int lc, float v) const {
+        const int64_t m = row0 + lr;
+        const int r = col0 + lc;
+        if (m >= d.M || r >= d.R) return;
+        if (slot) base[lr * kCols + lc] = v;
+        else base[w_row_offset(d, m) + int64_t(r) * d.w_sr] = v;
+    }
+};
+
+// The workgroup holding item x.
+__device__ inline int64_t wg_of(int64_t x, int64_t total, int64_t n_wg) { return ((x + 1) * n_wg - 1) / total; }
+
+// Walk this workgroup's pieces: begin(mb, rb) before a piece, triple(t,
+// t_next) for each of its triples (t_next = the piece's next triple or -1),
+// end(Dest) after it.
+template <typename Begin, typename Triple, typename End>
+__device__ inline void for_each_piece(const F3Args& g, Begin begin, Triple triple, End end) {
+    const F3Desc& d = g.d;
+    const int64_t total = g.nt * int64_t(g.mblocks) * d.rblocks;
+    const int64_t b = blockIdx.x;
+    const int64_t i1 = (b + 1) * total / g.n_wg;
+    for (int64_t i = b * total / g.n_wg; i < i1;) {
+        const int64_t blk = i / g.nt;
+        const int32_t t = int32_t(i - blk * g.nt);
+        const int32_t q = g.seg_of[t + 1] - 1;
+        const int32_t s0 = g.seg_start[q], s1 = g.seg_start[q + 1];
+        const int64_t pend = min(i1, blk * g.nt + s1);
+        const bool before = s0 < t, cont = blk * g.nt + s1 > i1;
+        const int mb = int(blk / d.rblocks), rb = int(blk % d.rblocks);
+        begin(mb, rb);
+        const int32_t t_end = t + int32_t(pend - i);
+        for (int32_t tt = t; tt < t_end; tt++) triple(tt, tt + 1 < t_end ? tt + 1 : -1);
+        Dest dst;
+        dst.row0 = int64_t(mb) * g.brows;
+        dst.col0 = rb * kCols;
+        dst.slot = before || cont;
+        dst.base = !dst.slot ? g.W + int64_t(q) * d.te_w
+                             : g.part + (2 * b + (before ? 0 : 1)) * int64_t(g.brows) * kCols;
+        end(dst);
+        i = pend;
+    }
+}
+
+// T chunk loads: 32 rows x kChunk elements, 4 float4 per thread.
+struct ChunkLoader {
+    float4 pre[4];
+    __device__ void load(const F3Desc& d, const float* Tt, int64_t row0, int64_t KK, int c) {
+        const int tid = threadIdx.x;
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            const int idx = tid + kThreads * i, row = idx >> 5, c4 = idx & 31;
+            const int64_t kk = int64_t(c) * kChunk + 4 * c4;
+            const int64_t m = row0 + row;
+            pre[i] = (m < d.M && kk < KK) ? *reinterpret_cast<const float4*>(Tt + m * KK + kk)
+                                          : float4{0.f, 0.f, 0.f, 0.f};
+        }
+    }
+    __device__ void store(float* st) const {
+        const int tid = threadIdx.x;
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            const int idx = tid + kThreads * i, row = idx >> 5, c4 = idx & 31;
+            *reinterpret_cast<float4*>(st + row * kPitchT + 4 * c4) = pre[i];
+        }
+    }
+};
+
+// Stage the block's columns of the triple's P tile ([tp][kCols]) and Q tile
+// (transposed, [kCols][qpitch]) in LDS.
+__device__ inline void stage_pq(const F3Desc& d, const float* Pt, const float* Qt, int col0, int tq, int qpitch,
+                                float* sP, float* sQ) {
+    const int tid = threadIdx.x;
+    for (int e = tid; e < d.tp * kCols; e += kThreads) {
+        const int pp = e / kCols, c = e % kCols, r = col0 + c;
+        sP[e] = r < d.R ? Pt[pp * d.p_sp + int64_t(r) * d.p_sr] : 0.f;
+    }
+    for (int e = tid; e < tq * kCols; e += kThreads) {
+        const int qq = e / kCols, c = e % kCols, r = col0 + c;
+        sQ[c * qpitch + qq] = r < d.R ? Qt[qq * d.q_sq + int64_t(r) * d.q_sr] : 0.f;
+    }
+}
+
+// Any tq (a multiple of 4).  Dynamic LDS: T stages [2][kRows][kPitchT], P
+// slice [tp][kCols], Q slice transposed [kCols][tq + 4] (floats).  Waves:
+// rows [16 mh, +16) and columns [32 rh, +32) of the block; the B operand of
+// every MFMA is P[p', r] * Q[q', r] formed in registers.
 __global__ __launch_bounds__(kThreads) void k3_gemm(F3Args g) {
     extern __shared__ float lds[];
     const F3Desc& d = g.d;
@@ -239,64 +304,33 @@ __global__ __launch_bounds__(kThreads) void k3_gemm(F3Args g) {
     float* sP = lds + 2 * kRows * kPitchT;
     const int qpitch = d.tq + 4;
     float* sQ = sP + d.tp * kCols;
-
-    const int64_t per_unit_blocks = int64_t(d.mblocks) * d.rblocks;
-    const int64_t u = int64_t(blockIdx.x) / per_unit_blocks;
-    if (u >= g.hdr->n_units) return;
-    const int rem = int(int64_t(blockIdx.x) - u * per_unit_blocks);
-    const int mb = rem / d.rblocks, rb = rem % d.rblocks;
-    const F3Unit un = g.units[u];
-
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int mh = w & 1, rh = w >> 1;  // wave: rows [16 mh, +16), columns [32 rh, +32)
+    const int mh = w & 1, rh = w >> 1;
     const int n = lane & 15, gq = lane >> 4;
     const int64_t KK = int64_t(d.tp) * d.tq;
     const int nchunks = int((KK + kChunk - 1) / kChunk);
-    const int64_t row0 = int64_t(mb) * kRows;
-    const int col0 = rb * kCols;
-
     floatx4 acc[2][2];
+    int64_t row0 = 0;
+    int col0 = 0;
+    ChunkLoader ld;
+    auto begin = [&](int mb, int rb) {
+        row0 = int64_t(mb) * kRows;
+        col0 = rb * kCols;
 #pragma unroll
-    for (int t = 0; t < 2; t++)
+        for (int t = 0; t < 2; t++)
 #pragma unroll
-        for (int e = 0; e < 2; e++) acc[t][e] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-    for (int32_t t = un.t0; t < un.t1; t++) {
-        const int64_t s = g.tu[t];
-        const float* Tt = g.U + s * d.te_u;
-        const float* Pt = g.P + int64_t(g.tp[t]) * d.te_p;
-        const float* Qt = g.Q + int64_t(g.tq[t]) * d.te_q;
+            for (int e = 0; e < 2; e++) acc[t][e] = floatx4{0.f, 0.f, 0.f, 0.f};
+    };
+    auto triple = [&](int32_t t, int32_t) {
+        const float* Tt = g.U + int64_t(g.tu[t]) * d.te_u;
         __syncthreads();  // the previous triple is done with sP, sQ and both T stages
-        for (int e = tid; e < d.tp * kCols; e += kThreads) {
-            const int pp = e / kCols, c = e % kCols, r = col0 + c;
-            sP[e] = r < d.R ? Pt[pp * d.p_sp + int64_t(r) * d.p_sr] : 0.f;
-        }
-        for (int e = tid; e < d.tq * kCols; e += kThreads) {
-            const int qq = e / kCols, c = e % kCols, r = col0 + c;
-            sQ[c * qpitch + qq] = r < d.R ? Qt[qq * d.q_sq + int64_t(r) * d.q_sr] : 0.f;
-        }
-        // chunk loads: 4 float4 per thread, row = idx / 32, float4 column idx % 32
-        float4 pre[4];
-        auto load_chunk = [&](int c) {
-#pragma unroll
-            for (int i = 0; i < 4; i++) {
-                const int idx = tid + kThreads * i, row = idx >> 5, c4 = idx & 31;
-                const int64_t kk = int64_t(c) * kChunk + 4 * c4;
-                const int64_t m = row0 + row;
-                pre[i] = (m < d.M && kk < KK) ? *reinterpret_cast<const float4*>(Tt + m * KK + kk)
-                                              : float4{0.f, 0.f, 0.f, 0.f};
-            }
-        };
-        load_chunk(0);
+        stage_pq(d, g.P + int64_t(g.tp[t]) * d.te_p, g.Q + int64_t(g.tq[t]) * d.te_q, col0, d.tq, qpitch, sP, sQ);
+        ld.load(d, Tt, row0, KK, 0);
         for (int c = 0; c < nchunks; c++) {
             float* st = sT + (c & 1) * kRows * kPitchT;
-#pragma unroll
-            for (int i = 0; i < 4; i++) {
-                const int idx = tid + kThreads * i, row = idx >> 5, c4 = idx & 31;
-                *reinterpret_cast<float4*>(st + row * kPitchT + 4 * c4) = pre[i];
-            }
+            ld.store(st);
             __syncthreads();
-            if (c + 1 < nchunks) load_chunk(c + 1);
+            if (c + 1 < nchunks) ld.load(d, Tt, row0, KK, c + 1);
             // this lane's contracted index at the chunk start, as (p', q')
             int64_t kk0 = int64_t(c) * kChunk + 4 * gq;
             int pp = int(kk0 / d.tq), qq = int(kk0 % d.tq);
@@ -324,37 +358,160 @@ __global__ __launch_bounds__(kThreads) void k3_gemm(F3Args g) {
                 }
             }
         }
-    }
-    // lane holds rows 4 gq + i, column n of each 16 x 16 tile
-    float* dst = un.slot >= 0 ? g.part + int64_t(un.slot) * d.te_w : g.W + int64_t(un.seg) * d.te_w;
+    };
+    auto end = [&](const Dest& dst) {
+        // lane holds rows 4 gq + i, column n of each 16 x 16 tile
 #pragma unroll
-    for (int tt = 0; tt < 2; tt++) {
-        const int r = col0 + 32 * rh + 16 * tt + n;
-        const floatx4 v = acc[tt][0] + acc[tt][1];
+        for (int tt = 0; tt < 2; tt++) {
+            const floatx4 v = acc[tt][0] + acc[tt][1];
 #pragma unroll
-        for (int i = 0; i < 4; i++) {
-            const int64_t m = row0 + 16 * mh + 4 * gq + i;
-            if (m < d.M && r < d.R) dst[w_row_offset(d, m) + int64_t(r) * d.w_sr] = v[i];
+            for (int i = 0; i < 4; i++) dst.put(d, 16 * mh + 4 * gq + i, 32 * rh + 16 * tt + n, v[i]);
         }
-    }
+    };
+    for_each_piece(g, begin, triple, end);
 }
 
-// Sum the partial tiles of every split segment, in unit order.
-__global__ __launch_bounds__(kThreads) void k3_reduce(const int32_t* __restrict__ split_list,
-                                                      const int64_t* __restrict__ pref,
-                                                      const int32_t* __restrict__ seg_start, int64_t per_unit,
-                                                      const float* __restrict__ part, int64_t te_w,
-                                                      int64_t chunks, const F3Header* hdr, float* __restrict__ W) {
-    const int64_t i = int64_t(blockIdx.x) / chunks;
-    if (i >= hdr->n_split) return;
-    const int64_t q = split_list[i];
-    const int64_t nu = (seg_start[q + 1] - seg_start[q] + per_unit - 1) / per_unit;
-    const int64_t sb = pref[q] & 0xffffffffll;
-    const int64_t e0 = (int64_t(blockIdx.x) % chunks) * kThreads * 4;
-    for (int64_t e = e0 + threadIdx.x; e < min(e0 + kThreads * 4, te_w); e += kThreads) {
-        float acc = 0.f;
-        for (int64_t k = 0; k < nu; k++) acc += part[(sb + k) * te_w + e];
-        W[q * te_w + e] = acc;
+// tq = TQ in {16, 32, 64}, ordered the other way round: for every p' the
+// MFMAs contract over q' only, Y[m, r] = sum_q' T[m, p', q'] Q[q', r], and
+// the result is scaled by P[p', r] and added to the accumulator (acc +=
+// P[p', r] * Y[m, r], one fused multiply-add per element and p').  The B
+// operand of every MFMA is then a plain Q element, held in registers for the
+// whole triple (lane group g of the 16x16x4 MFMA takes q' = g * TQ/4 + s for
+// step s, so a lane's A values are contiguous in the staged T row and come
+// in 16-byte LDS reads), and the scale-add of p' - 1 is issued after the
+// MFMAs of p' so that it does not wait for them.  The first T chunk of the
+// piece's next triple is loaded during the last chunk of the current one.
+template <int TQ>
+__global__ __launch_bounds__(kThreads, 3) void k3_gemm_q(F3Args g) {
+    constexpr int kS = TQ / 4;           // MFMA steps per p'
+    constexpr int kPpc = kChunk / TQ;    // p' rows per staged chunk
+    static_assert(kS % 4 == 0 && kChunk % TQ == 0, "TQ must be 16, 32 or 64");
+    extern __shared__ float lds[];
+    const F3Desc& d = g.d;
+    float* sT = lds;
+    float* sP = lds + 2 * kRows * kPitchT;
+    constexpr int qpitch = TQ + 4;
+    float* sQ = sP + d.tp * kCols;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int mh = w & 1, rh = w >> 1;
+    const int n = lane & 15, gq = lane >> 4;
+    const int64_t KK = int64_t(d.tp) * TQ;
+    const int nchunks = int((KK + kChunk - 1) / kChunk);
+    const int cl0 = 32 * rh + n, cl1 = cl0 + 16;  // this lane's two columns in the block
+    const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+    floatx4 acc[2], yprev[2];
+    float pvprev[2];
+    int64_t row0 = 0;
+    int col0 = 0;
+    bool have_next = false;  // the first chunk of the next triple is in ld
+    ChunkLoader ld;
+    auto begin = [&](int mb, int rb) {
+        row0 = int64_t(mb) * kRows;
+        col0 = rb * kCols;
+        have_next = false;
+#pragma unroll
+        for (int t = 0; t < 2; t++) {
+            acc[t] = yprev[t] = zero;
+            pvprev[t] = 0.f;
+        }
+    };
+    auto triple = [&](int32_t t, int32_t t_next) {
+        const float* Tt = g.U + int64_t(g.tu[t]) * d.te_u;
+        __syncthreads();  // the previous triple is done with sP, sQ and both T stages
+        stage_pq(d, g.P + int64_t(g.tp[t]) * d.te_p, g.Q + int64_t(g.tq[t]) * d.te_q, col0, TQ, qpitch, sP, sQ);
+        if (!have_next) ld.load(d, Tt, row0, KK, 0);
+        have_next = false;
+        float qreg[2][kS];
+        for (int c = 0; c < nchunks; c++) {
+            float* st = sT + (c & 1) * kRows * kPitchT;
+            ld.store(st);
+            __syncthreads();
+            if (c + 1 < nchunks) {
+                ld.load(d, Tt, row0, KK, c + 1);
+            } else if (t_next >= 0) {
+                ld.load(d, g.U + int64_t(g.tu[t_next]) * d.te_u, row0, KK, 0);
+                have_next = true;
+            }
+            if (c == 0) {
+                // this lane's Q elements for the whole triple: q' = gq * kS + j
+#pragma unroll
+                for (int j = 0; j < kS; j += 4) {
+                    const float4 v0 = *reinterpret_cast<const float4*>(sQ + cl0 * qpitch + gq * kS + j);
+                    const float4 v1 = *reinterpret_cast<const float4*>(sQ + cl1 * qpitch + gq * kS + j);
+                    qreg[0][j] = v0.x, qreg[0][j + 1] = v0.y, qreg[0][j + 2] = v0.z, qreg[0][j + 3] = v0.w;
+                    qreg[1][j] = v1.x, qreg[1][j + 1] = v1.y, qreg[1][j + 2] = v1.z, qreg[1][j + 3] = v1.w;
+                }
+            }
+            const float* arow = st + (16 * mh + n) * kPitchT + gq * kS;
+#pragma unroll
+            for (int pl = 0; pl < kPpc; pl++) {
+                const int pg = c * kPpc + pl;  // p' of this row of the chunk
+                float a[kS];
+#pragma unroll
+                for (int j = 0; j < kS; j += 4) {
+                    const float4 v = *reinterpret_cast<const float4*>(arow + pl * TQ + j);
+                    a[j] = v.x, a[j + 1] = v.y, a[j + 2] = v.z, a[j + 3] = v.w;
+                }
+                const int pc = min(pg, d.tp - 1);
+                const float p0 = sP[pc * kCols + cl0], p1 = sP[pc * kCols + cl1];
+                floatx4 y0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], qreg[0][0], zero, 0, 0, 0);
+                floatx4 y1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], qreg[1][0], zero, 0, 0, 0);
+#pragma unroll
+                for (int j = 1; j < kS; j++) {
+                    y0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], qreg[0][j], y0, 0, 0, 0);
+                    y1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], qreg[1][j], y1, 0, 0, 0);
+                }
+                // scale-add of the previous p' while these MFMAs run
+                acc[0] += pvprev[0] * yprev[0];
+                acc[1] += pvprev[1] * yprev[1];
+                yprev[0] = y0;
+                yprev[1] = y1;
+                pvprev[0] = pg < d.tp ? p0 : 0.f;
+                pvprev[1] = pg < d.tp ? p1 : 0.f;
+            }
+        }
+    };
+    auto end = [&](const Dest& dst) {
+        acc[0] += pvprev[0] * yprev[0];
+        acc[1] += pvprev[1] * yprev[1];
+#pragma unroll
+        for (int tt = 0; tt < 2; tt++)
+#pragma unroll
+            for (int i = 0; i < 4; i++) dst.put(d, 16 * mh + 4 * gq + i, 32 * rh + 16 * tt + n, acc[tt][i]);
+    };
+    for_each_piece(g, begin, triple, end);
+}
+
+// Sum the slots of every split (segment, block): workgroup b - 1 of this
+// launch looks at the boundary where range b starts; the first boundary
+// inside a (segment, block) sums slot 2 b0 + 1, slots 2 b of the ranges
+// inside it and slot 2 b1, in that order, into W.
+__global__ __launch_bounds__(kThreads) void k3_reduce(F3Args g) {
+    const F3Desc& d = g.d;
+    const int64_t total = g.nt * int64_t(g.mblocks) * d.rblocks;
+    const int64_t b = int64_t(blockIdx.x) + 1;
+    const int64_t x = b * total / g.n_wg;
+    if (x <= 0 || x >= total) return;
+    const int64_t blk = x / g.nt;
+    const int32_t t = int32_t(x - blk * g.nt);
+    const int32_t q = g.seg_of[t + 1] - 1;
+    const int32_t s0 = g.seg_start[q], s1 = g.seg_start[q + 1];
+    if (s0 == t) return;  // the range starts with a segment: nothing split here
+    const int64_t b0 = wg_of(blk * g.nt + s0, total, g.n_wg);
+    if (b != b0 + 1) return;
+    const int64_t b1 = wg_of(blk * g.nt + s1 - 1, total, g.n_wg);
+    const int mb = int(blk / d.rblocks), rb = int(blk % d.rblocks);
+    Dest dst;
+    dst.base = g.W + int64_t(q) * d.te_w;
+    dst.slot = false;
+    dst.row0 = int64_t(mb) * g.brows;
+    dst.col0 = rb * kCols;
+    const int64_t bs = int64_t(g.brows) * kCols;
+    for (int e = threadIdx.x; e < bs; e += kThreads) {
+        float v = g.part[(2 * b0 + 1) * bs + e];
+        for (int64_t bb = b0 + 1; bb < b1; bb++) v += g.part[(2 * bb) * bs + e];
+        v += g.part[(2 * b1) * bs + e];
+        dst.put(d, e / kCols, e % kCols, v);
     }
 }
 
@@ -505,21 +662,29 @@ tre_status parse3(const char* einsum, const char* upper, const int64_t* extent, 
     return TRE_OK;
 }
 
-int64_t target_units(const F3Desc& d) {
-    return std::max<int64_t>(1, kTargetUnits / (int64_t(d.mblocks) * d.rblocks));
+constexpr int kMaxOcc = 8;  // workgroups per CU counted for the partial slots
+
+// CUs of the current device (256 when it cannot be read).
+int64_t device_cus() {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                                 hipSuccess || cus < 1)
+        return 256;
+    return cus;
 }
 
 struct F3Layout {
     size_t hdr, flag, pos, ip, iq, tmp, tu, tp, tq, su, sp, sq, wkey, wkey_alt, perm, perm_alt, hist, heads, seg_of,
-        seg_start, seg_key, cnt, units, split, part, total;
+        seg_start, seg_key, part, total;
+    int64_t max_wg;  // workgroups the partial slots are sized for
 };
 
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 F3Layout f3_layout(const F3Desc& d, int64_t n_u) {
     const int64_t n = std::max<int64_t>(n_u, 1);
-    const int64_t T = target_units(d);
     F3Layout L{};
+    L.max_wg = device_cus() * kMaxOcc;
     size_t off = 0;
     auto take = [&](size_t b) {
         const size_t o = off;
@@ -547,10 +712,7 @@ F3Layout f3_layout(const F3Desc& d, int64_t n_u) {
     L.seg_of = take(sizeof(int32_t) * size_t(n + 1));
     L.seg_start = take(sizeof(int32_t) * size_t(n + 1));
     L.seg_key = take(sizeof(uint64_t) * size_t(n));
-    L.cnt = take(sizeof(int64_t) * size_t(n + 1));
-    L.units = take(sizeof(F3Unit) * size_t(T + n));
-    L.split = take(sizeof(int32_t) * size_t(T));
-    L.part = take(sizeof(float) * size_t(2 * T) * size_t(d.te_w));
+    L.part = take(sizeof(float) * size_t(2 * L.max_wg) * size_t(kRows * kCols));
     L.total = off;
     return L;
 }
@@ -685,53 +847,52 @@ tre_status tre_execute3(const char* einsum, const char* upper, const int64_t* ex
     tm.mark(s);
     if (nw > w_cap) return fail(TRE_E_CAPACITY, "w_cap below the output key count");
     if (nw > 0 && (!w_tiles || (d.rw > 0 && !w_keys))) return fail(TRE_E_ARG, "null output buffers");
-    // work units
-    const int64_t T = target_units(d);
-    const int64_t per_unit = std::max<int64_t>(1, (nt + T - 1) / T);
-    int64_t* cnt = static_cast<int64_t*>(at(L.cnt));
-    F3Unit* units = static_cast<F3Unit*>(at(L.units));
-    int32_t* split = static_cast<int32_t*>(at(L.split));
+    tm.mark(s);  // (no separate work-unit phase: ranges are computed in the kernel)
+    const void* fn = d.tq == 16   ? reinterpret_cast<const void*>(&k3_gemm_q<16>)
+                     : d.tq == 32 ? reinterpret_cast<const void*>(&k3_gemm_q<32>)
+                     : d.tq == 64 ? reinterpret_cast<const void*>(&k3_gemm_q<64>)
+                                  : reinterpret_cast<const void*>(&k3_gemm);
+    const size_t lds = gemm_lds_bytes(d);
+    F3Args g{};
     if (nw > 0) {
-        k3_unit_count<<<blocks_for(nw + 1), kThreads, 0, s>>>(seg_start, nw, per_unit, cnt);
-        if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "unit count");
-        if ((e = scan_exclusive_i64(cnt, cnt, nw + 1, static_cast<int64_t*>(at(L.tmp)), s)) != hipSuccess)
-            return dev_fail(e, "unit scan");
-        k3_unit_fill<<<blocks_for(nw + 1), kThreads, 0, s>>>(seg_start, nw, per_unit, cnt, units, split, hdr);
-        if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "units");
-    }
-    tm.mark(s);
-    if (nw > 0) {
-        // at most nt / per_unit + nw units; workgroups past the real count exit
-        const int64_t unit_bound = nt / per_unit + nw;
-        const int64_t blocks = unit_bound * d.mblocks * d.rblocks;
-        if (blocks > int64_t(0x7fffffff)) return fail(TRE_E_SHAPE, "too many output blocks");
-        F3Args g{};
+        if (lds > 65536 &&
+            (e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds))) != hipSuccess)
+            return dev_fail(e, "shared memory size");
+        // one workgroup per resident slot, each with an equal share of the
+        // (block, triple) items
+        int occ = 0;
+        if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, kThreads, lds)) != hipSuccess)
+            return dev_fail(e, "occupancy");
+        const int64_t items = nt * int64_t(d.mblocks) * d.rblocks;
+        const int64_t n_wg = std::max<int64_t>(1, std::min<int64_t>({device_cus() * std::max(occ, 1), L.max_wg, items}));
         g.U = static_cast<const float*>(u_tiles);
         g.P = static_cast<const float*>(d.v_on_p ? v_tiles : x_tiles);
         g.Q = static_cast<const float*>(d.v_on_p ? x_tiles : v_tiles);
         g.tu = tu;
         g.tp = tp;
         g.tq = tq;
-        g.units = units;
-        g.hdr = hdr;
+        g.seg_of = seg_of;
+        g.seg_start = seg_start;
+        g.nt = nt;
+        g.n_wg = n_wg;
+        g.brows = kRows;
+        g.mblocks = d.mblocks;
         g.W = w_tiles;
         g.part = static_cast<float*>(at(L.part));
         g.d = d;
-        const size_t lds = gemm_lds_bytes(d);
-        if (lds > 65536 &&
-            (e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k3_gemm),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, int(lds))) != hipSuccess)
-            return dev_fail(e, "shared memory size");
-        k3_gemm<<<dim3(unsigned(blocks)), kThreads, lds, s>>>(g);
+        const dim3 grid{unsigned(n_wg)};
+        if (d.tq == 16) k3_gemm_q<16><<<grid, kThreads, lds, s>>>(g);
+        else if (d.tq == 32) k3_gemm_q<32><<<grid, kThreads, lds, s>>>(g);
+        else if (d.tq == 64) k3_gemm_q<64><<<grid, kThreads, lds, s>>>(g);
+        else k3_gemm<<<grid, kThreads, lds, s>>>(g);
         if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "contract");
     }
     tm.mark(s);
     if (nw > 0) {
-        const int64_t chunks = (d.te_w + kThreads * 4 - 1) / (kThreads * 4);
-        k3_reduce<<<dim3(unsigned(T * chunks)), kThreads, 0, s>>>(split, cnt, seg_start, per_unit,
-                                                                   static_cast<const float*>(at(L.part)), d.te_w,
-                                                                   chunks, hdr, w_tiles);
-        if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "reduce");
+        if (g.n_wg > 1) {
+            k3_reduce<<<dim3(unsigned(g.n_wg - 1)), kThreads, 0, s>>>(g);
+            if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "reduce");
+        }
         if (d.rw > 0) {
             k3_write_keys<<<blocks_for(nw), kThreads, 0, s>>>(seg_key, nw, d, w_keys);
             if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "keys");

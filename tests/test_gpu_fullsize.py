@@ -266,3 +266,32 @@ def test_sparse_three_way_full(orc):
     worst, zeros_ok = value_error(o2.w_tiles[rows].cpu().numpy(), r2.acc[rr], r2.mag[rr])
     say(f"3-way end-to-end on {len(S)} rows: max mag-relative error {worst:.3e}")
     assert zeros_ok and worst <= TOL["f32"]
+
+
+def test_sparse_three_way_fused_full(orc):
+    """The same contraction through the fused three-operand path
+    (tre_execute3, the launch the benchmark times for this workload): triple
+    count = T blocks (B and C hold every block), output keys = distinct I
+    blocks of T, sampled output tiles against the oracle's per-triple
+    evaluation of the T tuples that feed them."""
+    import paper_2603_08957_amd as tre
+
+    w = workloads.config(4)
+    ext = {"i": w["n"], "j": w["n"], "k": w["n"], "r": w["r"]}
+    til = {c: w["block"] for c in "ijk"}
+    wk, wt, nt = tre.execute3("ijk,jr,kr->ir", "ijk", ext, til, dev(w["T"]["keys"]), dev(w["T"]["tiles"]),
+                              dev(w["B"]["keys"]), dev(w["B"]["tiles"]), dev(w["C"]["keys"]), dev(w["C"]["tiles"]))
+    tk = w["T"]["keys"]
+    assert nt == len(tk)
+    want = np.unique(tk[:, 0]).astype(np.int32).reshape(-1, 1)
+    gk = wk.cpu().numpy()
+    assert np.array_equal(gk, want)
+    rng = np.random.default_rng(105)
+    S = pick(rng, want, 4)[:, 0]
+    sel = np.isin(tk[:, 0], S)
+    T = {"keys": np.ascontiguousarray(tk[sel]), "tiles": w["T"]["tiles"][sel], "dtype": "f32"}
+    rk, acc, mag, _ = orc.eval3("ijk,jr,kr->ir", "ijk", ext, til, T, w["B"], w["C"])
+    rows = [int(np.nonzero(gk[:, 0] == k)[0][0]) for k in rk[:, 0]]
+    worst, zeros_ok = value_error(wt[rows].cpu().numpy(), acc, mag)
+    say(f"fused 3-way on {len(S)} output keys ({int(sel.sum())} triples): max mag-relative error {worst:.3e}")
+    assert zeros_ok and worst <= TOL["f32"]

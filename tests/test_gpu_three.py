@@ -59,7 +59,7 @@ def _case3(rng):
     upper = a + b + "".join(c for c in rows if rng.random() < 0.5)
     til, ext = {}, {}
     til[p] = int(rng.choice([1, 2, 3, 5, 8, 16, 32]))
-    til[q] = int(rng.choice([4, 8, 12, 16, 32]))
+    til[q] = int(rng.choice([4, 8, 12, 16, 32, 64]))
     for c in (p, q):
         ext[c] = til[c] * int(rng.integers(2, 6))
     for c in rows:
