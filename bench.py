@@ -255,9 +255,19 @@ class GnnChain:
                 "einsums": [w["E1"]["einsum"] + " upper " + w["E1"]["upper"],
                             w["E2"]["einsum"] + " upper " + w["E2"]["upper"]]}
 
-    def oracle_sample(self, orc, n_keys_e1=20, n_keys_e2=64):
-        """Time the oracle on a bounded sample: n_keys_e1 output keys of E1 and
-        n_keys_e2 of E2 (seeded choice), restricted to the tuples that feed them."""
+    def oracle_sample(self, orc, budget_s=10.0):
+        """Time the oracle on a bounded sample of about budget_s seconds: a
+        first pass on 20 output keys of E1 and 64 of E2 sizes a second one,
+        which is the one reported."""
+        r = self._oracle_sample(orc, 20, 64)
+        if r["seconds"] < 0.8 * budget_s:
+            f = budget_s / max(r["seconds"], 1e-3)
+            r = self._oracle_sample(orc, int(20 * f), int(64 * f))
+        return r
+
+    def _oracle_sample(self, orc, n_keys_e1, n_keys_e2):
+        """The oracle on n_keys_e1 output keys of E1 and n_keys_e2 of E2
+        (seeded choice), restricted to the tuples that feed them."""
         w = self.w
         rng = np.random.default_rng(0)
         p1 = orc.Plan(w["E1"]["einsum"], w["E1"]["upper"], w["E1"]["extents"], w["E1"]["tiles"])
@@ -412,17 +422,22 @@ class ThreeWay:
 
 # Counter-measured HBM traffic of the dominant kernel, kept in profiles/ with
 # the SHA-256 of the kernel source the counters were taken on.
-TRAFFIC_RECORDS = {2: "hbm_traffic_gemm128_gnn_chain_262144_bf16.md"}
+TRAFFIC_RECORDS = {1: "counters_gnn_chain_4096_fp32.md", 2: "counters_gnn_chain_262144_bf16.md",
+                   3: "counters_block_sparse_16384_fp32.md", 4: "counters_sparse_3way_4096_fp32.md",
+                   5: "counters_gnn_chain_1048576_bf16.md"}
 
 
-def traffic_record(config):
+def traffic_record(config, three_way="fused"):
     """HBM bytes per launch of the dominant kernel (FETCH_SIZE + WRITE_SIZE,
-    each scaled by a copy of known size), or None when no record exists for
-    this workload or the kernel source changed since it was taken."""
+    each scaled by a copy of known size) and its counter-measured MFMA work,
+    or None when no record exists for this workload and launch configuration
+    or the kernel source changed since it was taken."""
     import hashlib
 
     name = TRAFFIC_RECORDS.get(config)
     if name is None or PLAN_OPTIONS.get("u_ranges", 0) != 0 or PLAN_OPTIONS.get("pace_windows", 0) != 0:
+        return None
+    if config == 4 and three_way != "fused":
         return None
     path = os.path.join(ROOT, "profiles", name)
     try:
@@ -434,7 +449,9 @@ def traffic_record(config):
     if hashlib.sha256(src).hexdigest() != rec["kernel_source_sha256"]:
         return None
     return {"bytes": rec["traffic_bytes_per_launch"], "read_bytes": rec["read_bytes_per_launch"],
-            "write_bytes": rec["write_bytes_per_launch"], "source": "profiles/" + name}
+            "write_bytes": rec["write_bytes_per_launch"], "kernel": rec["kernel"],
+            "mfma_flops": rec.get("mfma_flops_per_launch"), "mfma_busy": rec.get("mfma_busy"),
+            "source": "profiles/" + name}
 
 
 def make_workload(c, tre, torch, three_way="fused"):
@@ -541,7 +558,7 @@ def main():
         roof = {"bound": "mfma", "achieved": dflops / (contract_ms * 1e-3) / 1e12, "peak": PEAK_TFLOPS[dtype],
                 "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    rec = traffic_record(args.config)
+    rec = traffic_record(args.config, args.three_way)
     roof["traffic"] = rec["bytes"] if rec else None
     if rec:
         roof["traffic_detail"] = rec
