@@ -1,6 +1,14 @@
 """Oracle for one three-operand EinSum whose two small operands meet the large
-one on different promoted labels and share one demoted label with the output
-(the non-binary EinSum of Sec. 8, e.g. A[i,r] = sum_jk T[i,j,k] B[j,r] C[k,r]).
+one on different promoted labels and share one demoted label r, in one of two
+forms:
+
+* r is kept in the output and the joined labels are summed (the non-binary
+  EinSum of Sec. 8, e.g. A[i,r] = sum_jk T[i,j,k] B[j,r] C[k,r]);
+* the output has exactly U's labels and r is summed ("masked" form, e.g. the
+  attention scores S[i,j] = sum_k A[i,j] T0[i,k] T1[j,k] of the graph
+  transformer in Sec. 9, which Table gt-schema computes as two binary
+  EinSums: T2[i,j,k] = T0[i,k] A[i,j] with no aggregation, then
+  T3[i,j] = sum_k T2[i,j,k] T1[j,k]).
 
 TEST INFRASTRUCTURE, NOT PART OF THE PRODUCT (see the package docstring).
 
@@ -40,9 +48,10 @@ class Spec3:
     upper: str
     a: str  # label V shares with U
     b: str  # label X shares with U
-    r: str  # label V and X share with W
+    r: str  # label V and X share (kept in W, or summed in the masked form)
     extents: dict
     tiles: dict
+    masked: bool = False  # W has exactly U's labels and r is summed
 
     def tile_ext(self, c: str) -> int:
         return int(self.tiles[c]) if c in self.upper else int(self.extents[c])
@@ -76,8 +85,9 @@ def parse3(einsum: str, upper: str, extents: dict, tiles: dict) -> Spec3:
     b = (set(x) - {r}).pop()
     if r in u or a not in u or b not in u or a == b:
         raise Spec3Error("SPLIT", "each small operand meets U on its own label")
-    if set(w) != (set(u) - {a, b}) | {r}:
-        raise Spec3Error("SPLIT", "W holds U's other labels and the shared label")
+    masked = w == u
+    if not masked and set(w) != (set(u) - {a, b}) | {r}:
+        raise Spec3Error("SPLIT", "W holds U's other labels and the shared label, or exactly U's labels")
     if set(u[-2:]) != {a, b}:
         raise Spec3Error("SPLIT", "the two joined labels are U's last two")
     for c in upper:
@@ -90,7 +100,7 @@ def parse3(einsum: str, upper: str, extents: dict, tiles: dict) -> Spec3:
         t = int(tiles[c]) if c in upper else e
         if e < 1 or t < 1 or e % t:
             raise Spec3Error("SHAPE", f"tile of {c!r} does not divide its extent")
-    return Spec3(u, v, x, w, upper, a, b, r, dict(extents), dict(tiles))
+    return Spec3(u, v, x, w, upper, a, b, r, dict(extents), dict(tiles), masked)
 
 
 def _check_keys(keys: np.ndarray, radix: list, what: str):

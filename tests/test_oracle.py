@@ -692,3 +692,153 @@ def test_eval3_key_errors(orc):
     with pytest.raises(orc.Spec3Error) as e:
         orc.eval3(_E3, "ijk", ext, til, bad, w["B"], w["C"])
     assert e.value.category == "KEYRANGE"
+
+
+# ------------------------- the masked three-operand form (attention scores)
+
+_EM = "ij,ik,jk->ij"
+
+
+def _masked_case(seed, n=24, r=7, ti=1, tj=1, keep=0.3, drop=0.25):
+    """A random masked case: U over (I, J) blocks, V keyed I and X keyed J
+    with some keys missing, so the triple join drops U tuples."""
+    rng = np.random.default_rng(seed)
+    ext = {"i": n, "j": n, "k": r}
+    til = {"i": ti, "j": tj}
+    U = workloads.random_relation(rng, "ij", "ij", ext, til, "f32", keep=keep)
+    V = workloads.random_relation(rng, "ik", "i", ext, til, "f32", keep=1 - drop)
+    X = workloads.random_relation(rng, "jk", "j", ext, til, "f32", keep=1 - drop)
+    return U, V, X, ext, til
+
+
+@pytest.mark.parametrize("ti,tj", [(1, 1), (2, 3), (4, 1)])
+def test_masked_matches_binary_path(orc, ti, tj):
+    """The masked triple evaluation equals the two binary EinSums of Table
+    gt-schema through the C oracle: T2 = V join U on i with no aggregation
+    ("ik,ij->ijk"), then T3 = T2 join X on j summing k ("ijk,jk->ij")."""
+    for seed in (11, 12):
+        U, V, X, ext, til = _masked_case(seed, ti=ti, tj=tj)
+        wk, acc, mag, tri = orc.eval3(_EM, "ij", ext, til, U, V, X)
+        r3 = orc.run(orc.Plan("ik,ij->ijk", "ij", ext, til), V, U)
+        r4 = orc.run(orc.Plan("ijk,jk->ij", "ij", ext, til), {"keys": r3.wkeys, "tiles": r3.acc, "dtype": "f64"}, X)
+        assert np.array_equal(wk, r4.wkeys)
+        np.testing.assert_allclose(acc, r4.acc, rtol=1e-12, atol=1e-12)
+        assert (mag >= np.abs(acc) - 1e-12).all()
+        assert 0 < len(tri) < len(U["keys"])  # some U tuples lost a partner
+        # every output key is a U key and the triples come in U order
+        assert np.array_equal(wk, U["keys"][tri[:, 0]])
+        assert np.all(np.diff(tri[:, 0]) > 0)
+
+
+def test_masked_brute_force(orc):
+    """Pure-Python loops over every global coordinate of the dense tensors
+    (absent tuples are zero): S[i, j] = sum_k U[i, j] V[i, k] X[j, k]; the
+    output keys are the U keys whose I block is in V and J block in X."""
+    U, V, X, ext, til = _masked_case(21, n=12, r=5, ti=2, tj=3, keep=0.5)
+    wk, acc, _, _ = orc.eval3(_EM, "ij", ext, til, U, V, X)
+    Ud = dense_of("ij", "ij", ext, til, U["keys"], vals_f64(U))
+    Vd = dense_of("ik", "i", ext, til, V["keys"], vals_f64(V))
+    Xd = dense_of("jk", "j", ext, til, X["keys"], vals_f64(X))
+    n, r = ext["i"], ext["k"]
+    S = [[0.0] * n for _ in range(n)]
+    for i in range(n):
+        for j in range(n):
+            for k in range(r):
+                S[i][j] += Ud[i, j] * Vd[i, k] * Xd[j, k]
+    vi = {int(k[0]) for k in V["keys"]}
+    xj = {int(k[0]) for k in X["keys"]}
+    want = [(int(I), int(J)) for I, J in U["keys"] if int(I) in vi and int(J) in xj]
+    assert [tuple(k) for k in wk.tolist()] == want
+    got = dense_of("ij", "ij", ext, til, wk, acc)
+    np.testing.assert_allclose(got, np.array(S), rtol=1e-12, atol=1e-12)
+
+
+def test_masked_sqlite_purely_relational(orc):
+    """All labels promoted with tiles of 1 is the purely relational form
+    (Sec. 2): SQLite's SUM(u.v * q.v * x.v) over the three-way join, grouped
+    by (i, j), gives the same keys and values."""
+    n, r = 20, 6
+    rng = np.random.default_rng(31)
+    ext = {"i": n, "j": n, "k": r}
+    til = {"i": 1, "j": 1}
+    U = workloads.random_relation(rng, "ij", "ij", ext, til, "f32", keep=0.25)
+    V = workloads.random_relation(rng, "ik", "i", ext, til, "f32", keep=0.8)
+    X = workloads.random_relation(rng, "jk", "j", ext, til, "f32", keep=0.8)
+    wk, acc, _, _ = orc.eval3(_EM, "ij", ext, til, U, V, X)
+    db = sqlite3.connect(":memory:")
+    db.execute("CREATE TABLE u (i INT, j INT, v DOUBLE)")
+    db.execute("CREATE TABLE q (i INT, k INT, v DOUBLE)")
+    db.execute("CREATE TABLE x (j INT, k INT, v DOUBLE)")
+    db.executemany("INSERT INTO u VALUES (?,?,?)",
+                   [(int(a), int(b), float(v)) for (a, b), v in zip(U["keys"], U["tiles"][:, 0])])
+    db.executemany("INSERT INTO q VALUES (?,?,?)",
+                   [(int(a[0]), k, float(t[k])) for a, t in zip(V["keys"], V["tiles"]) for k in range(r)])
+    db.executemany("INSERT INTO x VALUES (?,?,?)",
+                   [(int(a[0]), k, float(t[k])) for a, t in zip(X["keys"], X["tiles"]) for k in range(r)])
+    rows = db.execute("SELECT u.i, u.j, SUM(u.v * q.v * x.v) FROM u JOIN q ON q.i = u.i "
+                      "JOIN x ON x.j = u.j AND x.k = q.k GROUP BY u.i, u.j ORDER BY u.i, u.j").fetchall()
+    assert [tuple(k) for k in wk.tolist()] == [(a, b) for a, b, _ in rows]
+    np.testing.assert_allclose(acc[:, 0], [s for _, _, s in rows], rtol=1e-12, atol=1e-12)
+
+
+def test_masked_label_order_invariance(orc):
+    """V and X stored with the shared label first ("ki", "kj", transposed
+    tiles) give the same result."""
+    U, V, X, ext, til = _masked_case(41, ti=2, tj=2)
+    wk, acc, _, _ = orc.eval3(_EM, "ij", ext, til, U, V, X)
+    r = ext["k"]
+
+    def tr(rel, t):
+        return {"keys": rel["keys"], "dtype": "f32",
+                "tiles": rel["tiles"].reshape(-1, t, r).transpose(0, 2, 1).reshape(len(rel["keys"]), -1)}
+
+    wk2, acc2, _, _ = orc.eval3("ij,ki,kj->ij", "ij", ext, til, U, tr(V, til["i"]), tr(X, til["j"]))
+    assert np.array_equal(wk2, wk)
+    np.testing.assert_allclose(acc2, acc, rtol=1e-12, atol=1e-12)
+
+
+def test_masked_magnitude_positive_inputs(orc):
+    U, V, X, ext, til = _masked_case(51)
+    for rel in (U, V, X):
+        rel["tiles"] = np.abs(rel["tiles"])
+    _, acc, mag, _ = orc.eval3(_EM, "ij", ext, til, U, V, X)
+    np.testing.assert_allclose(mag, acc, rtol=1e-13, atol=0)
+
+
+@pytest.mark.parametrize("einsum,upper,cat", [
+    ("ij,ik,jk->ji", "ij", "SPLIT"),     # W neither U's labels nor U's others plus k
+    ("ij,ik,jk->ijk", "ij", "SPLIT"),    # W keeps the shared label and the joined ones
+    ("ij,ik,jk->ij", "ijk", "SPLIT"),    # shared label promoted
+    ("ij,ik,jk->ij", "i", "SPLIT"),      # joined label demoted
+])
+def test_masked_structure_errors(orc, einsum, upper, cat):
+    ext = {c: 8 for c in "ijk"}
+    til = {c: 4 for c in "ijk"}
+    with pytest.raises(orc.Spec3Error) as e:
+        orc.parse3(einsum, upper, ext, til)
+    assert e.value.category == cat
+
+
+def test_graph_attention_small_chain(orc):
+    """The attention workload (scaled down) through the oracle -- E1 and E2
+    with the C oracle, the masked EinSum with eval3, times 1/sqrt(d_k) --
+    equals dense attention scores written with numpy matrix products:
+    S = A * (F WQ)(F WK)^T / sqrt(d_k) on the edges, F the dense features."""
+    w = workloads.config(6, "small")
+    n, nf, dk = w["n"], w["n_feat"], w["d_k"]
+    e1, e2 = w["E1"], w["E2"]
+    r1 = orc.run(orc.Plan(e1["einsum"], e1["upper"], e1["extents"], e1["tiles"]), w["X"], w["WQ"])
+    r2 = orc.run(orc.Plan(e2["einsum"], e2["upper"], e2["extents"], e2["tiles"]), w["X"], w["WK"])
+    T0 = {"keys": r1.wkeys, "tiles": r1.acc, "dtype": "f64"}
+    T1 = {"keys": r2.wkeys, "tiles": r2.acc, "dtype": "f64"}
+    e = w["E34"]
+    wk, acc, mag, _ = orc.eval3(e["einsum"], e["upper"], e["extents"], e["tiles"], w["A"], T0, T1)
+    S = acc[:, 0] * w["scale"]
+    F = np.zeros((n, nf))
+    F[w["X"]["keys"][:, 0], w["X"]["keys"][:, 1]] = 1.0
+    Q = F @ w["WQ"]["tiles"].astype(np.float64)
+    K = F @ w["WK"]["tiles"].astype(np.float64)
+    ai, aj = w["A"]["keys"][:, 0], w["A"]["keys"][:, 1]
+    assert np.array_equal(wk, w["A"]["keys"])  # every node has a feature, so every edge is matched
+    np.testing.assert_allclose(S, (Q[ai] * K[aj]).sum(axis=1) / np.sqrt(dk), rtol=1e-10, atol=1e-10)
+    assert w["n_edges"] == len(ai) and len(np.unique(ai * n + aj)) == len(ai)

@@ -213,6 +213,55 @@ def sparse_3way(n: int, r: int, block: int, block_density: float, fill: float, s
     return {"E1": e1, "E2": e2, "T": t_rel, "B": b_rel, "C": c_rel, "n": n, "r": r, "block": block}
 
 
+# ------------------------------------------------------- graph attention
+
+def graph_attention(n: int, n_feat: int, feat_density: float, d_k: int, degree: dict, seed: int) -> dict:
+    """Attention scores of a graph transformer before normalisation (Sec. 9,
+    the plan of Table gt-schema), fp32:
+      E1  T0[i, k] = sum_m X[i, m] WQ[m, k]    "im,mk->ik",  promoted {i, m}
+      E2  T1[j, k] = sum_n X[j, n] WK[n, k]    "jn,nk->jk",  promoted {j, n}
+      E3  T2[i, j, k] = T0[i, k] A[i, j]       "ik,ij->ijk", promoted {i, j}, no aggregation
+      E4  T3[i, j] = sum_k T2[i, j, k] T1[j, k] "ijk,jk->ij", promoted {i, j}
+      E5  S[i, j] = T3[i, j] / sqrt(d_k)       (unary)
+    E3 and E4 together are the masked three-operand EinSum "ij,ik,jk->ij"
+    (U = A, V = T0, X = T1).
+    X: binary bag-of-words features, each (node, feature) present with
+    probability ``feat_density`` (a node with none gets one uniform feature),
+    stored as scalar tuples keyed (i, m); WQ, WK: n_feat x d_k N(0,1), stored
+    as d_k-vectors keyed by the feature; A: directed edges with the out-degree
+    law of ``degree`` and distinct uniform targets, value 1, stored as scalar
+    tuples keyed (i, j).  Draw order: features, the fix-up features, WQ, WK,
+    degrees, targets."""
+    rng = np.random.default_rng(seed)
+    F = rng.random((n, n_feat)) < feat_density
+    empty = np.nonzero(~F.any(axis=1))[0]
+    F[empty, rng.integers(0, n_feat, size=empty.size)] = True
+    fi, fm = np.nonzero(F)
+    WQ = rng.standard_normal((n_feat, d_k), dtype=np.float32)
+    WK = rng.standard_normal((n_feat, d_k), dtype=np.float32)
+    if degree["kind"] == "fixed":
+        deg = np.full(n, degree["d"], dtype=np.int64)
+    else:
+        deg = powerlaw_degrees(rng, n, degree["alpha"], degree["mean"])
+    src, dst = distinct_targets(rng, n, deg)
+    x_rel = {"keys": np.stack([fi, fm], axis=1).astype(np.int32), "tiles": np.ones((fi.size, 1), np.float32),
+             "dtype": "f32"}
+    fkeys = np.arange(n_feat, dtype=np.int32).reshape(n_feat, 1)
+    wq_rel = {"keys": fkeys, "tiles": WQ, "dtype": "f32"}
+    wk_rel = {"keys": fkeys.copy(), "tiles": WK, "dtype": "f32"}
+    a_rel = {"keys": np.stack([src, dst], axis=1).astype(np.int32), "tiles": np.ones((src.size, 1), np.float32),
+             "dtype": "f32"}
+    one = {"i": 1, "j": 1, "m": 1, "n": 1}
+    e1 = spec("im,mk->ik", "im", {"i": n, "m": n_feat, "k": d_k}, one, "f32")
+    e2 = spec("jn,nk->jk", "jn", {"j": n, "n": n_feat, "k": d_k}, one, "f32")
+    e3 = spec("ik,ij->ijk", "ij", {"i": n, "j": n, "k": d_k}, one, "f32")
+    e4 = spec("ijk,jk->ij", "ij", {"i": n, "j": n, "k": d_k}, one, "f32")
+    e34 = spec("ij,ik,jk->ij", "ij", {"i": n, "j": n, "k": d_k}, one, "f32")
+    return {"E1": e1, "E2": e2, "E3": e3, "E4": e4, "E34": e34, "X": x_rel, "WQ": wq_rel, "WK": wk_rel,
+            "A": a_rel, "scale": float(1.0 / np.sqrt(d_k)), "n": n, "n_feat": n_feat, "d_k": d_k,
+            "n_edges": int(src.size), "n_feat_entries": int(fi.size)}
+
+
 # ------------------------------------------------------- random small plans
 
 def random_relation(rng, labels: str, upper: str, extents: dict, tiles: dict, dtype: str, keep: float,
@@ -240,7 +289,7 @@ def random_relation(rng, labels: str, upper: str, extents: dict, tiles: dict, dt
 # --------------------------------------------------------- named configs
 
 def config(c: int, scale: str = "full", **kw) -> dict:
-    """The five workloads (1-based).  ``scale="small"`` gives a scaled-down twin
+    """The workloads (1-based; 6 is the graph-attention workload).  ``scale="small"`` gives a scaled-down twin
     with the same structure that the oracle finishes in seconds."""
     seed = SEED_BASE + c
     small = scale == "small"
@@ -261,4 +310,10 @@ def config(c: int, scale: str = "full", **kw) -> dict:
         n = 4096 if small else 1048576
         return gnn_chain(n, 256, 256, 1, 256, {"kind": "powerlaw", "alpha": 2.1, "mean": 32, "values": "normal"},
                          "bf16", seed, dense_y_tiles=True, **kw)
+    if c == 6:
+        # Amazon.Computers-shaped graph (13,752 nodes, ~0.4M edges, 767
+        # features), key dimension 1024 as in Table gt-schema
+        if small:
+            return graph_attention(512, 64, 0.1, 128, {"kind": "powerlaw", "alpha": 2.1, "mean": 8}, seed)
+        return graph_attention(13752, 767, 0.05, 1024, {"kind": "powerlaw", "alpha": 2.1, "mean": 29}, seed)
     raise ValueError(c)
