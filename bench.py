@@ -130,7 +130,8 @@ class FusedStage:
         r = (set(ops[1]) & set(ops[2])).pop()
         # dense tile flops per triple: rows x r x the two contracted tile extents, x 2
         fpt = 2 * (te[0] // (tiles[u[-2]] * tiles[u[-1]])) * extents[r] * tiles[u[-2]] * tiles[u[-1]]
-        self.plan = types.SimpleNamespace(kernel_class="fused three-operand MFMA", flops_per_pair=fpt,
+        kc = "masked three-operand dot" if w == u else "fused three-operand MFMA"
+        self.plan = types.SimpleNamespace(kernel_class=kc, flops_per_pair=fpt,
                                           key_arity=[len([c for c in op if c in upper]) for op in ops + [w]])
         self.n_u, self.n_v, self.n_x = n_u, n_v, n_x
         self.n_pairs = 0
@@ -420,6 +421,105 @@ class ThreeWay:
                 "seconds": secs}
 
 
+class Attention:
+    """Graph-attention scores (Sec. 9, the plan of Table gt-schema): E1 = X
+    join WQ on m (scale + segmented sum) -> T0, E2 = X join WK on n -> T1,
+    then the masked three-operand EinSum "ij,ik,jk->ij" over the edges A
+    (default: one triple join + one dot product per edge) or the binary pair
+    E3 = T0 join A on i with no aggregation and E4 = T2 join T1 on j, and the
+    unary 1/sqrt(d_k) on the scores."""
+
+    def __init__(self, c, tre, torch, path="fused"):
+        import workloads
+
+        w = workloads.config(c)
+        self.w, self.tre, self.torch, self.path = w, tre, torch, path
+        self.xk, self.xt = dev_rel(w["X"], torch)
+        self.qk, self.qt = dev_rel(w["WQ"], torch)
+        self.kk, self.kt = dev_rel(w["WK"], torch)
+        self.ak, self.at = dev_rel(w["A"], torch)
+        nx, nf, na, n = len(w["X"]["keys"]), w["n_feat"], w["n_edges"], w["n"]
+        self.e1 = Stage(tre, torch, w["E1"], nx, nf, nx, "E1")
+        self.e2 = Stage(tre, torch, w["E2"], nx, nf, nx, "E2")
+        if path == "fused":
+            e = w["E34"]
+            self.f = FusedStage(tre, torch, e["einsum"], e["upper"], e["extents"], e["tiles"], na, n, n, "E34")
+        else:
+            self.e3 = Stage(tre, torch, w["E3"], n, na, na, "E3")
+            self.e4 = Stage(tre, torch, w["E4"], na, n, na, "E4")
+
+    def step(self, timing=None):
+        t0k, t0t = self.e1.run(self.xk, self.xt, self.qk, self.qt)
+        t1k, t1t = self.e2.run(self.xk, self.xt, self.kk, self.kt)
+        if self.path == "fused":
+            self.f.n_v, self.f.n_x = int(t0k.shape[0]), int(t1k.shape[0])
+            wk, wt = self.f.run(self.ak, self.at, t0k, t0t, t1k, t1t, timing=timing)
+        else:
+            self.e3.n_u = int(t0k.shape[0])
+            k2, t2 = self.e3.run(t0k, t0t, self.ak, self.at)
+            self.e4.n_u, self.e4.n_v = int(k2.shape[0]), int(t1k.shape[0])
+            wk, wt = self.e4.run(k2, t2, t1k, t1t, timing=timing)
+        self.tre.scale_f32(wt, self.w["scale"], out=wt)
+        return wk, wt
+
+    def stages(self):
+        return [self.f, self.e1, self.e2] if self.path == "fused" else [self.e4, self.e3, self.e1, self.e2]
+
+    def describe(self):
+        w = self.w
+        how = ("masked three-operand EinSum ij,ik,jk->ij (triple join + one dot product per edge)"
+               if self.path == "fused" else "binary EinSums ik,ij->ijk (no aggregation) then ijk,jk->ij")
+        return {"workload": f"graph attention scores, fp32: {w['n']} nodes, {w['n_edges']} edges (power-law "
+                            f"out-degree), {w['n_feat']} binary features, d_k {w['d_k']}; E1/E2 im,mk->ik; {how}; "
+                            f"scale 1/sqrt(d_k)",
+                "nodes": w["n"], "edges": w["n_edges"], "features": w["n_feat"], "d_k": w["d_k"],
+                "feature_tuples": w["n_feat_entries"], "path": self.path}
+
+    def oracle_sample(self, orc, budget_s=10.0):
+        """The oracle on the edges of a seeded sample of source nodes: E1
+        restricted to those nodes, E2 to their targets (C oracle), the masked
+        EinSum on their edges (per-triple evaluation); a first pass on 8
+        nodes sizes a second one of about budget_s, which is reported."""
+        r = self._oracle_sample(orc, 8)
+        if r["seconds"] < 0.8 * budget_s:
+            r = self._oracle_sample(orc, max(8, int(8 * budget_s / max(r["seconds"], 1e-3))))
+        return r
+
+    def _oracle_sample(self, orc, n_src):
+        from threadpoolctl import threadpool_info
+
+        w = self.w
+        rng = np.random.default_rng(0)
+        ak = w["A"]["keys"]
+        src = np.sort(rng.choice(np.unique(ak[:, 0]), size=min(n_src, len(np.unique(ak[:, 0]))), replace=False))
+        esel = np.isin(ak[:, 0], src)
+        A = {"keys": np.ascontiguousarray(ak[esel]), "tiles": w["A"]["tiles"][esel], "dtype": "f32"}
+        dst = np.unique(A["keys"][:, 1])
+        secs, flops, T = 0.0, 0, {}
+        for name, wname, nodes in (("E1", "WQ", src), ("E2", "WK", dst)):
+            s = w[name]
+            p = orc.Plan(s["einsum"], s["upper"], s["extents"], s["tiles"])
+            mu, mv = orc.restrict(p, w["X"]["keys"], w[wname]["keys"], nodes.reshape(-1, 1).astype(np.int32))
+            U = {"keys": w["X"]["keys"][mu], "tiles": w["X"]["tiles"][mu], "dtype": "f32"}
+            V = {"keys": w[wname]["keys"][mv], "tiles": w[wname]["tiles"][mv], "dtype": "f32"}
+            t0 = time.perf_counter()
+            r = orc.run(p, U, V)
+            secs += time.perf_counter() - t0
+            flops += len(r.pairs) * 2 * w["d_k"]
+            T[name] = {"keys": r.wkeys, "tiles": r.acc, "dtype": "f64"}
+        e = w["E34"]
+        t0 = time.perf_counter()
+        _, _, _, tri = orc.eval3(e["einsum"], e["upper"], e["extents"], e["tiles"], A, T["E1"], T["E2"])
+        secs += time.perf_counter() - t0
+        flops += len(tri) * 2 * w["d_k"]
+        threads = max([int(d.get("num_threads", 1)) for d in threadpool_info()] or [1])
+        return {"value": flops / secs / 1e9, "unit": "GFLOP/s", "cores": threads, "kind": "oracle",
+                "sample": f"the {len(tri)} edges of {len(src)} of {w['n']} source nodes: E1 restricted to those "
+                          f"nodes and E2 to their {len(dst)} targets (single-threaded fp64 C oracle), the masked "
+                          f"EinSum per edge (numpy fp64 einsum); tile-flop-equivalent rate, {secs:.1f} s",
+                "seconds": secs}
+
+
 # Counter-measured HBM traffic of the dominant kernel, kept in profiles/ with
 # the SHA-256 of the kernel source the counters were taken on.
 TRAFFIC_RECORDS = {1: "counters_gnn_chain_4096_fp32.md", 2: "counters_gnn_chain_262144_bf16.md",
@@ -437,7 +537,7 @@ def traffic_record(config, three_way="fused"):
     name = TRAFFIC_RECORDS.get(config)
     if name is None or PLAN_OPTIONS.get("u_ranges", 0) != 0 or PLAN_OPTIONS.get("pace_windows", 0) != 0:
         return None
-    if config == 4 and three_way != "fused":
+    if config in (4, 6) and three_way != "fused":
         return None
     path = os.path.join(ROOT, "profiles", name)
     try:
@@ -461,6 +561,8 @@ def make_workload(c, tre, torch, three_way="fused"):
         return BlockSparse(c, tre, torch)
     if c == 4:
         return ThreeWay(c, tre, torch, three_way)
+    if c == 6:
+        return Attention(c, tre, torch, three_way)
     raise SystemExit(f"unknown workload {c}")
 
 
@@ -469,14 +571,15 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default 2: bf16 GNN chain, 262,144 vertices)")
+    ap.add_argument("--config", type=int, default=2,
+                    help="workload 1..6 (default 2: bf16 GNN chain, 262,144 vertices; 6: graph attention)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--u-ranges", type=int, default=0,
                     help="tre_options.u_ranges for every EinSum (0 = library default, < 0 = off)")
     ap.add_argument("--pace-windows", type=int, default=0,
                     help="tre_options.pace_windows for every EinSum (0 = library default, < 0 = off)")
     ap.add_argument("--three-way", choices=["fused", "binary"], default="fused",
-                    help="workload 4: one fused three-operand EinSum (default) or two binary EinSums")
+                    help="workloads 4 and 6: one fused three-operand EinSum (default) or two binary EinSums")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="first run one device copy of this many GiB (counter calibration under rocprofv3 --pmc)")
     args = ap.parse_args()

@@ -198,6 +198,12 @@ tre_status tre_execute(tre_plan_t plan, const int32_t *u_keys, int64_t n_u, cons
 /* Round fp32 to bf16 (nearest even; NaN stays NaN).  x, y device, n elements. */
 tre_status tre_cast_f32_bf16(const float *x, uint16_t *y, int64_t n, void *stream);
 
+/* y = scale * x, elementwise over n fp32 values (device, 16-byte aligned; x
+ * may equal y): a unary EinSum applied to every tuple's tile, e.g. the
+ * 1 / sqrt(d_k) of the attention scores (Sec. 9, Table gt-schema).
+ * TRE_E_ARG on a null or misaligned array or n < 0; asynchronous. */
+tre_status tre_scale_f32(const float *x, float *y, int64_t n, float scale, void *stream);
+
 /* Re-compose a relation keyed by ONE promoted label from tile size t_in to
  * t_out = group * t_in along that label (the STACK aggregate of Sec. 6 where
  * the new promoted set equals the old one):
@@ -247,22 +253,32 @@ tre_status tre_repartition(const char *labels, const char *upper_in, const char 
 
 /* tre_execute3 -- one three-operand EinSum "U,V,X->W" whose two small
  * operands each meet U on a promoted label of their own and share one
- * demoted label r with the output, e.g. A[i,r] = sum_jk T[i,j,k] B[j,r] C[k,r]
- * (the non-binary EinSum of Sec. 8).  Instead of two binary EinSums (U join
- * V, then that result join X), U is joined with V and X in one pass (the join
- * of Sec. 5 over three relations): every U tuple whose key on a has a V tuple
- * and whose key on b has an X tuple forms a triple, each triple contributes
- * the tile EinSum of its three tiles, and the contributions are summed per
- * output key (GROUP BY W's promoted labels) in U order, atomic-free, as in
- * tre_contract.  No intermediate relation is materialised.
+ * demoted label r, in one of two forms:
+ *   - r is kept in W and U's two joined labels are summed, e.g. A[i,r] =
+ *     sum_jk T[i,j,k] B[j,r] C[k,r] (the non-binary EinSum of Sec. 8);
+ *   - masked form: W has exactly U's labels and r is summed, e.g. the
+ *     attention scores S[i,j] = sum_k A[i,j] T0[i,k] T1[j,k] of the graph
+ *     transformer of Sec. 9, which Table gt-schema runs as two binary EinSums
+ *     (T2 = T0 A with no aggregation, then T3 = sum_k T2 T1).
+ * Instead of two binary EinSums (U join V, then that result join X), U is
+ * joined with V and X in one pass (the join of Sec. 5 over three relations):
+ * every U tuple whose key on a has a V tuple and whose key on b has an X
+ * tuple forms a triple, each triple contributes the tile EinSum of its three
+ * tiles, and the contributions are summed per output key (GROUP BY W's
+ * promoted labels) in U order, atomic-free, as in tre_contract.  No
+ * intermediate relation is materialised.  In the masked form every triple is
+ * its own output tuple: W's keys are the matched U keys, in U order.
  * Structure (TRE_E_PARSE / TRE_E_SPLIT otherwise):
  *   - V and X have two labels each and share exactly one, r, which is not in
  *     U and is demoted; V's other label a and X's other label b are promoted
  *     labels of U and are U's last two labels, in either order;
- *   - W's labels are U's labels other than a and b, plus r, in any order.
- * Shapes (TRE_E_SHAPE otherwise): tiles divide extents; the tile extent of
- * U's last label is a multiple of 4; the tile extents of U's last two labels
- * are at most 64 each.  in_dtype: TRE_F32 only (TRE_E_DTYPE otherwise).
+ *   - W's labels are U's labels other than a and b, plus r, in any order; or
+ *     W is U's label string itself (masked form).
+ * Shapes (TRE_E_SHAPE otherwise): tiles divide extents; first form: the tile
+ * extent of U's last label is a multiple of 4 and the tile extents of U's
+ * last two labels are at most 64 each; masked form: U's last two labels take
+ * tiles of 1 (one scalar per edge, as in Table gt-schema), U's other labels
+ * any tiles.  in_dtype: TRE_F32 only (TRE_E_DTYPE otherwise).
  *   extent, tile : host [26] per letter, as for tre_plan.
  *   u_keys [n_u x r_U], v_keys [n_v x 1], x_keys [n_x x 1]: device int32,
  *                  sorted strictly increasing (U keyed by its promoted labels
@@ -278,7 +294,8 @@ tre_status tre_repartition(const char *labels, const char *upper_in, const char 
  *             validation, the triple join and the output keys, units_ms is
  *             empty (each workgroup finds its range of triples itself),
  *             contract_ms the fused contraction kernel, reduce_ms the sum of
- *             output blocks split between workgroups and the key write-out.
+ *             output blocks split between workgroups (none in the masked
+ *             form) and the key write-out.
  * Synchronizes the stream twice (triple count, output key count); key errors
  * as TRE_E_UNSORTED / TRE_E_DUPKEY / TRE_E_KEYRANGE. */
 size_t tre_execute3_workspace_bytes(const char *einsum, const char *upper, const int64_t *extent,

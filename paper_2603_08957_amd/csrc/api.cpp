@@ -325,6 +325,16 @@ tre_status tre_cast_f32_bf16(const float* x, uint16_t* y, int64_t n, void* strea
     return e == hipSuccess ? TRE_OK : dev_fail(e, "cast");
 }
 
+tre_status tre_scale_f32(const float* x, float* y, int64_t n, float scale, void* stream) {
+    if (n < 0 || (n > 0 && (!x || !y))) return TRE_E_ARG;
+    if (n > 0 && ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(y)) & 15)) {
+        set_error("tre_scale_f32: arrays must be 16-byte aligned");
+        return TRE_E_ARG;
+    }
+    hipError_t e = launch_scale(x, y, n, scale, reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TRE_OK : dev_fail(e, "scale");
+}
+
 size_t tre_stack_workspace_bytes(int64_t n) { return n < 0 ? 0 : stack_ws_bytes(n); }
 
 tre_status tre_stack_rows(const int32_t* keys, int64_t n, const void* tiles, int64_t row_elems, int32_t group,

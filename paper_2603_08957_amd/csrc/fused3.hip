@@ -69,6 +69,7 @@ struct F3Desc {
     int32_t needs_sort;
     int32_t radix_u[kMaxDims];         // extent / tile of U's key attributes
     int32_t radix_p, radix_q;          // of the p and q key attributes
+    int32_t masked;                    // W has exactly U's labels and r is summed
 };
 
 struct F3Header {
@@ -515,6 +516,72 @@ __global__ __launch_bounds__(kThreads) void k3_reduce(F3Args g) {
     }
 }
 
+// Masked form: W has U's labels, so every triple is its own output tuple, in
+// U order, and with tiles of 1 on p and q its value is the U tile times one
+// dot product over r:  W[t][e] = U[tu[t]][e] * sum_r P[tp[t]][r] Q[tq[t]][r].
+// One wavefront per kMaskedBatch consecutive triples: the lanes stride over r
+// (16-byte loads when R is a multiple of 4 and the tiles are 16-byte aligned),
+// the batch's P and Q rows are all in flight at once, and a butterfly of lane
+// exchanges sums each dot product in a fixed order.  Consecutive triples of
+// one U row share their P row, which then comes from the cache.
+constexpr int kMaskedBatch = 4;
+
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+template <bool V4>
+__global__ __launch_bounds__(kThreads) void k3_masked(const float* __restrict__ U, const float* __restrict__ P,
+                                                      const float* __restrict__ Q, const int32_t* __restrict__ tu,
+                                                      const int32_t* __restrict__ tp, const int32_t* __restrict__ tq,
+                                                      int64_t nt, int64_t te_u, int64_t R, float* __restrict__ W) {
+    const int lane = threadIdx.x & 63;
+    const int64_t t0 = (int64_t(blockIdx.x) * (kThreads / 64) + (threadIdx.x >> 6)) * kMaskedBatch;
+    if (t0 >= nt) return;
+    const float* p[kMaskedBatch];
+    const float* q[kMaskedBatch];
+    float acc[kMaskedBatch];
+#pragma unroll
+    for (int b = 0; b < kMaskedBatch; b++) {
+        const int64_t t = min(t0 + b, nt - 1);  // past the end: repeat the last triple, never written
+        p[b] = P + int64_t(tp[t]) * R;
+        q[b] = Q + int64_t(tq[t]) * R;
+        acc[b] = 0.f;
+    }
+    if constexpr (V4) {
+        for (int64_t r = 4 * lane; r < R; r += 256) {
+            float4 x[kMaskedBatch], y[kMaskedBatch];
+#pragma unroll
+            for (int b = 0; b < kMaskedBatch; b++) {
+                x[b] = *reinterpret_cast<const float4*>(p[b] + r);
+                y[b] = *reinterpret_cast<const float4*>(q[b] + r);
+            }
+#pragma unroll
+            for (int b = 0; b < kMaskedBatch; b++) {
+                acc[b] = fmaf(x[b].x, y[b].x, acc[b]);
+                acc[b] = fmaf(x[b].y, y[b].y, acc[b]);
+                acc[b] = fmaf(x[b].z, y[b].z, acc[b]);
+                acc[b] = fmaf(x[b].w, y[b].w, acc[b]);
+            }
+        }
+    } else {
+        for (int64_t r = lane; r < R; r += 64)
+#pragma unroll
+            for (int b = 0; b < kMaskedBatch; b++) acc[b] = fmaf(p[b][r], q[b][r], acc[b]);
+    }
+#pragma unroll
+    for (int b = 0; b < kMaskedBatch; b++) {
+        const float dot = wave_sum(acc[b]);
+        const int64_t t = t0 + b;
+        if (t >= nt) break;
+        const float* u = U + int64_t(tu[t]) * te_u;
+        float* w = W + t * te_u;
+        for (int64_t e = lane; e < te_u; e += 64) w[e] = u[e] * dot;
+    }
+}
+
 __global__ void k3_write_keys(const uint64_t* __restrict__ seg_key, int64_t n_w, F3Desc d, int32_t* __restrict__ out) {
     const int64_t q = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (q >= n_w) return;
@@ -585,12 +652,16 @@ tre_status parse3(const char* einsum, const char* upper, const int64_t* extent, 
     if (u.find(r) != std::string::npos || a == b || nu < 2 || !((u[nu - 2] == a && u[nu - 1] == b) ||
                                                                  (u[nu - 2] == b && u[nu - 1] == a)))
         return fail(TRE_E_SPLIT, "V and X must meet U on U's last two labels, one each, and share a label not in U");
-    // W = U's other labels plus r
-    if (w.size() != nu - 1 || w.find(r) == std::string::npos)
-        return fail(TRE_E_SPLIT, "W holds U's labels other than the joined two, plus the shared label");
-    for (size_t i = 0; i + 2 < nu; i++)
-        if (w.find(u[i]) == std::string::npos)
-            return fail(TRE_E_SPLIT, "W holds U's labels other than the joined two, plus the shared label");
+    // W = U's other labels plus r, or exactly U's labels (masked form)
+    d.masked = (w == u) ? 1 : 0;
+    if (!d.masked) {
+        if (w.size() != nu - 1 || w.find(r) == std::string::npos)
+            return fail(TRE_E_SPLIT, "W holds U's labels other than the joined two plus the shared label, or U's labels");
+        for (size_t i = 0; i + 2 < nu; i++)
+            if (w.find(u[i]) == std::string::npos)
+                return fail(TRE_E_SPLIT,
+                            "W holds U's labels other than the joined two plus the shared label, or U's labels");
+    }
     for (int l = 0; l < 26; l++)
         if (up[l] && u.find(char('a' + l)) == std::string::npos && char('a' + l) != r)
             return fail(TRE_E_SPLIT, "a promoted label is not in the expression");
@@ -606,8 +677,11 @@ tre_status parse3(const char* einsum, const char* upper, const int64_t* extent, 
     d.tp = int32_t(tsz(p));
     d.tq = int32_t(tsz(q));
     d.R = int32_t(extent[r - 'a']);
-    if (d.tp > kMaxPQ || d.tq > kMaxPQ || d.tq % 4)
+    if (d.masked) {
+        if (d.tp != 1 || d.tq != 1) return fail(TRE_E_SHAPE, "masked form: the joined labels take tiles of 1");
+    } else if (d.tp > kMaxPQ || d.tq > kMaxPQ || d.tq % 4) {
         return fail(TRE_E_SHAPE, "tiles of U's last two labels must be at most 64, the last a multiple of 4");
+    }
     d.nm = int32_t(nu - 2);
     d.M = 1;
     for (int i = 0; i < d.nm; i++) {
@@ -626,7 +700,7 @@ tre_status parse3(const char* einsum, const char* upper, const int64_t* extent, 
     d.p_sr = pop[0] == r ? d.tp : 1;
     d.q_sq = qop[0] == r ? 1 : d.R;
     d.q_sr = qop[0] == r ? d.tq : 1;
-    // W strides
+    // W strides (the masked form's W tile is laid out as U's)
     int64_t st = 1;
     int64_t wst[26] = {};
     for (int i = int(w.size()) - 1; i >= 0; i--) {
@@ -634,7 +708,7 @@ tre_status parse3(const char* einsum, const char* upper, const int64_t* extent, 
         st *= (w[i] == r) ? d.R : tsz(w[i]);
     }
     d.te_w = st;
-    d.w_sr = wst[r - 'a'];
+    d.w_sr = d.masked ? 0 : wst[r - 'a'];
     for (int i = 0; i < d.nm; i++) d.mwst[i] = wst[u[i] - 'a'];
     // keys
     int upos[26];
@@ -848,57 +922,81 @@ tre_status tre_execute3(const char* einsum, const char* upper, const int64_t* ex
     if (nw > w_cap) return fail(TRE_E_CAPACITY, "w_cap below the output key count");
     if (nw > 0 && (!w_tiles || (d.rw > 0 && !w_keys))) return fail(TRE_E_ARG, "null output buffers");
     tm.mark(s);  // (no separate work-unit phase: ranges are computed in the kernel)
-    const void* fn = d.tq == 16   ? reinterpret_cast<const void*>(&k3_gemm_q<16>)
-                     : d.tq == 32 ? reinterpret_cast<const void*>(&k3_gemm_q<32>)
-                     : d.tq == 64 ? reinterpret_cast<const void*>(&k3_gemm_q<64>)
-                                  : reinterpret_cast<const void*>(&k3_gemm);
-    const size_t lds = gemm_lds_bytes(d);
-    F3Args g{};
-    if (nw > 0) {
-        if (lds > 65536 &&
-            (e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds))) != hipSuccess)
-            return dev_fail(e, "shared memory size");
-        // one workgroup per resident slot, each with an equal share of the
-        // (block, triple) items
-        int occ = 0;
-        if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, kThreads, lds)) != hipSuccess)
-            return dev_fail(e, "occupancy");
-        const int64_t items = nt * int64_t(d.mblocks) * d.rblocks;
-        const int64_t n_wg = std::max<int64_t>(1, std::min<int64_t>({device_cus() * std::max(occ, 1), L.max_wg, items}));
-        g.U = static_cast<const float*>(u_tiles);
-        g.P = static_cast<const float*>(d.v_on_p ? v_tiles : x_tiles);
-        g.Q = static_cast<const float*>(d.v_on_p ? x_tiles : v_tiles);
-        g.tu = tu;
-        g.tp = tp;
-        g.tq = tq;
-        g.seg_of = seg_of;
-        g.seg_start = seg_start;
-        g.nt = nt;
-        g.n_wg = n_wg;
-        g.brows = kRows;
-        g.mblocks = d.mblocks;
-        g.W = w_tiles;
-        g.part = static_cast<float*>(at(L.part));
-        g.d = d;
-        const dim3 grid{unsigned(n_wg)};
-        if (d.tq == 16) k3_gemm_q<16><<<grid, kThreads, lds, s>>>(g);
-        else if (d.tq == 32) k3_gemm_q<32><<<grid, kThreads, lds, s>>>(g);
-        else if (d.tq == 64) k3_gemm_q<64><<<grid, kThreads, lds, s>>>(g);
-        else k3_gemm<<<grid, kThreads, lds, s>>>(g);
-        if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "contract");
-    }
-    tm.mark(s);
-    if (nw > 0) {
-        if (g.n_wg > 1) {
-            k3_reduce<<<dim3(unsigned(g.n_wg - 1)), kThreads, 0, s>>>(g);
-            if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "reduce");
+    if (d.masked) {
+        // one output tuple per triple, already in U order
+        if (nw != nt) return fail(TRE_E_DEVICE, "internal: masked form with a key count other than the triple count");
+        if (nw > 0) {
+            const float* P = static_cast<const float*>(d.v_on_p ? v_tiles : x_tiles);
+            const float* Q = static_cast<const float*>(d.v_on_p ? x_tiles : v_tiles);
+            const bool v4 = d.R % 4 == 0 && ((reinterpret_cast<uintptr_t>(P) | reinterpret_cast<uintptr_t>(Q)) & 15) == 0;
+            const int64_t waves = (nt + kMaskedBatch - 1) / kMaskedBatch;
+            const dim3 grid{unsigned((waves + kThreads / 64 - 1) / (kThreads / 64))};
+            if (v4) k3_masked<true><<<grid, kThreads, 0, s>>>(static_cast<const float*>(u_tiles), P, Q, tu, tp, tq, nt,
+                                                             d.te_u, d.R, w_tiles);
+            else k3_masked<false><<<grid, kThreads, 0, s>>>(static_cast<const float*>(u_tiles), P, Q, tu, tp, tq, nt,
+                                                           d.te_u, d.R, w_tiles);
+            if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "masked contract");
         }
-        if (d.rw > 0) {
+        tm.mark(s);
+        if (nw > 0 && d.rw > 0) {
             k3_write_keys<<<blocks_for(nw), kThreads, 0, s>>>(seg_key, nw, d, w_keys);
             if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "keys");
         }
+        tm.mark(s);
+    } else {
+        const void* fn = d.tq == 16   ? reinterpret_cast<const void*>(&k3_gemm_q<16>)
+                         : d.tq == 32 ? reinterpret_cast<const void*>(&k3_gemm_q<32>)
+                         : d.tq == 64 ? reinterpret_cast<const void*>(&k3_gemm_q<64>)
+                                      : reinterpret_cast<const void*>(&k3_gemm);
+        const size_t lds = gemm_lds_bytes(d);
+        F3Args g{};
+        if (nw > 0) {
+            if (lds > 65536 &&
+                (e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds))) != hipSuccess)
+                return dev_fail(e, "shared memory size");
+            // one workgroup per resident slot, each with an equal share of the
+            // (block, triple) items
+            int occ = 0;
+            if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, kThreads, lds)) != hipSuccess)
+                return dev_fail(e, "occupancy");
+            const int64_t items = nt * int64_t(d.mblocks) * d.rblocks;
+            const int64_t n_wg =
+                std::max<int64_t>(1, std::min<int64_t>({device_cus() * std::max(occ, 1), L.max_wg, items}));
+            g.U = static_cast<const float*>(u_tiles);
+            g.P = static_cast<const float*>(d.v_on_p ? v_tiles : x_tiles);
+            g.Q = static_cast<const float*>(d.v_on_p ? x_tiles : v_tiles);
+            g.tu = tu;
+            g.tp = tp;
+            g.tq = tq;
+            g.seg_of = seg_of;
+            g.seg_start = seg_start;
+            g.nt = nt;
+            g.n_wg = n_wg;
+            g.brows = kRows;
+            g.mblocks = d.mblocks;
+            g.W = w_tiles;
+            g.part = static_cast<float*>(at(L.part));
+            g.d = d;
+            const dim3 grid{unsigned(n_wg)};
+            if (d.tq == 16) k3_gemm_q<16><<<grid, kThreads, lds, s>>>(g);
+            else if (d.tq == 32) k3_gemm_q<32><<<grid, kThreads, lds, s>>>(g);
+            else if (d.tq == 64) k3_gemm_q<64><<<grid, kThreads, lds, s>>>(g);
+            else k3_gemm<<<grid, kThreads, lds, s>>>(g);
+            if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "contract");
+        }
+        tm.mark(s);
+        if (nw > 0) {
+            if (g.n_wg > 1) {
+                k3_reduce<<<dim3(unsigned(g.n_wg - 1)), kThreads, 0, s>>>(g);
+                if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "reduce");
+            }
+            if (d.rw > 0) {
+                k3_write_keys<<<blocks_for(nw), kThreads, 0, s>>>(seg_key, nw, d, w_keys);
+                if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "keys");
+            }
+        }
+        tm.mark(s);
     }
-    tm.mark(s);
     if (timing) {
         std::memset(timing, 0, sizeof(*timing));
         timing->deferred = deferred ? 1 : 0;

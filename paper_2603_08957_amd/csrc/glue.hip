@@ -96,6 +96,30 @@ hipError_t launch_cast_bf16(const float* x, uint16_t* y, int64_t n, hipStream_t 
     return hipGetLastError();
 }
 
+// y = s * x elementwise (x may be y): a unary EinSum applied to every tuple's
+// tile, such as the attention scores' 1 / sqrt(d_k).
+__global__ void k_scale(const float* __restrict__ x, float* __restrict__ y, int64_t n, float sc) {
+    const int64_t stride = int64_t(gridDim.x) * kThreads * 4;
+    for (int64_t i = (int64_t(blockIdx.x) * kThreads + threadIdx.x) * 4; i < n; i += stride) {
+        if (i + 4 <= n) {
+            float4 v = *reinterpret_cast<const float4*>(x + i);
+            v.x *= sc;
+            v.y *= sc;
+            v.z *= sc;
+            v.w *= sc;
+            *reinterpret_cast<float4*>(y + i) = v;
+        } else {
+            for (int64_t j = i; j < n; j++) y[j] = x[j] * sc;
+        }
+    }
+}
+
+hipError_t launch_scale(const float* x, float* y, int64_t n, float sc, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    k_scale<<<grid_for(n, 4), kThreads, 0, s>>>(x, y, n, sc);
+    return hipGetLastError();
+}
+
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) {
     if (bytes == 0) return hipSuccess;
     const int64_t words = int64_t((bytes + 3) / 4);

@@ -169,6 +169,7 @@ hipError_t launch_write_outputs(const Plan& p, const Layout& L, char* ws, int32_
 
 // glue.hip
 hipError_t launch_cast_bf16(const float* x, uint16_t* y, int64_t n, hipStream_t s);
+hipError_t launch_scale(const float* x, float* y, int64_t n, float sc, hipStream_t s);
 hipError_t launch_tiles_from_entries(const int64_t* slot, const int64_t* off, const void* val, int64_t n,
                                      int elem_bytes, void* tiles, int64_t n_tiles, int64_t tile_elems,
                                      hipStream_t s);

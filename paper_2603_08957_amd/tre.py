@@ -26,7 +26,8 @@ DTYPE = {"f32": 0, "bf16": 1}
 # every symbol include/tre.h declares
 EXPORTS = [
     "tre_plan", "tre_plan_get_info", "tre_plan_destroy", "tre_workspace_bytes", "tre_workspace_max_pairs",
-    "tre_join", "tre_contract", "tre_execute", "tre_timing_read", "tre_cast_f32_bf16", "tre_stack_workspace_bytes", "tre_stack_rows",
+    "tre_join", "tre_contract", "tre_execute", "tre_timing_read", "tre_cast_f32_bf16", "tre_scale_f32",
+    "tre_stack_workspace_bytes", "tre_stack_rows",
     "tre_tiles_from_entries", "tre_status_str", "tre_last_error", "tre_version",
     "tre_repartition_workspace_bytes", "tre_repartition", "tre_execute3_workspace_bytes", "tre_execute3",
 ]
@@ -97,6 +98,7 @@ def lib():
         L.tre_execute.argtypes = [P, P, i64, P, P, i64, P, P, P, i64, P, P, i64, P, P, sz, P, P]
         L.tre_timing_read.argtypes = [P]
         L.tre_cast_f32_bf16.argtypes = [P, P, i64, P]
+        L.tre_scale_f32.argtypes = [P, P, i64, ctypes.c_float, P]
         L.tre_stack_workspace_bytes.argtypes = [i64]
         L.tre_stack_workspace_bytes.restype = sz
         L.tre_stack_rows.argtypes = [P, i64, P, i64, i32, i32, P, P, i64, P, P, sz, P]
@@ -258,6 +260,15 @@ def cast_f32_bf16(x, out=None, stream=None):
 
     y = out if out is not None else torch.empty(x.shape, dtype=torch.bfloat16, device=x.device)
     _check(lib().tre_cast_f32_bf16(_ptr(x), _ptr(y), x.numel(), _stream(stream)), "tre_cast_f32_bf16")
+    return y
+
+
+def scale_f32(x, scale: float, out=None, stream=None):
+    """out = scale * x (fp32, elementwise; out may be x)."""
+    import torch
+
+    y = out if out is not None else torch.empty_like(x)
+    _check(lib().tre_scale_f32(_ptr(x), _ptr(y), x.numel(), float(scale), _stream(stream)), "tre_scale_f32")
     return y
 
 

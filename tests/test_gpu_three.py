@@ -161,3 +161,134 @@ def test_execute3_edge_cases_gpu(orc):
     with pytest.raises(tre.TreError) as e:
         tre.execute3("ijk,jr,kr->ir", "ijk", ext, {"i": 4, "j": 4, "k": 2}, uk, ut, vk, vt, xk, xt)
     assert e.value.status == "TRE_E_SHAPE"
+
+
+# --------------------------------------------------------- masked form
+
+def _case_masked(rng):
+    """Random masked case "rows p q, (a r), (b r) -> rows p q": p, q promoted
+    with tiles of 1, row labels promoted or not, the small operands stored
+    either way round, R both below and above the 256 elements one wavefront
+    covers per step, multiples of 4 (16-byte loads) and not."""
+    letters = list("abcdefghlmnopst")
+    rng.shuffle(letters)
+    nm = int(rng.integers(0, 3))
+    rows = letters[:nm]
+    a, b, r = letters[nm:nm + 3]
+    p, q = (a, b) if rng.random() < 0.5 else (b, a)
+    u = "".join(rows) + p + q
+    v = a + r if rng.random() < 0.5 else r + a
+    x = b + r if rng.random() < 0.5 else r + b
+    upper = a + b + "".join(c for c in rows if rng.random() < 0.5)
+    til, ext = {p: 1, q: 1}, {}
+    for c in (p, q):
+        ext[c] = int(rng.integers(2, 40))
+    for c in rows:
+        if c in upper:
+            til[c] = int(rng.choice([1, 3, 8]))
+            ext[c] = til[c] * int(rng.integers(1, 4))
+        else:
+            ext[c] = int(rng.choice([1, 5, 33, 70]))
+    ext[r] = int(rng.choice([1, 3, 4, 17, 64, 256, 260, 1000, 1024]))
+    e = f"{u},{v},{x}->{u}"
+    U = _relation(rng, u, upper, ext, til, 0.4)
+    V = _relation(rng, v, upper, ext, til, 0.8)
+    X = _relation(rng, x, upper, ext, til, 0.8)
+    return e, upper, ext, til, U, V, X
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_masked_random_gpu(orc, seed):
+    rng = np.random.default_rng(5300 + seed)
+    e, upper, ext, til, U, V, X = _case_masked(rng)
+    say("masked random", seed, e, upper, ext, til, len(U["keys"]), len(V["keys"]), len(X["keys"]))
+    _run_and_check(orc, e, upper, ext, til, U, V, X)
+
+
+def _attention_inputs(w):
+    dev = {}
+    for name in ("X", "WQ", "WK", "A"):
+        dev[name] = to_dev(w[name])
+    return dev
+
+
+def test_masked_attention_small_gpu(orc):
+    """The graph-attention workload at its small size: E1 and E2 (scale +
+    segmented sum) and the fused masked EinSum on the GPU, each checked
+    against the oracle on the GPU's own inputs; the binary path (E3 with no
+    aggregation, then E4) gives the same keys and values; the unary
+    1/sqrt(d_k) matches an fp32 multiply bit for bit."""
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    w = workloads.config(6, "small")
+    d = _attention_inputs(w)
+    T = {}
+    for name, wname in (("E1", "WQ"), ("E2", "WK")):
+        s = w[name]
+        out = tre.einsum(tre.Plan.from_spec(s), d["X"][0], d["X"][1], d[wname][0], d[wname][1])
+        ref = orc.run(orc.Plan(s["einsum"], s["upper"], s["extents"], s["tiles"]), w["X"], w[wname])
+        assert np.array_equal(out.w_keys.cpu().numpy().reshape(ref.wkeys.shape), ref.wkeys)
+        worst, ok = value_error(out.w_tiles.cpu().numpy(), ref.acc, ref.mag)
+        assert ok and worst <= TOL["f32"], (name, worst)
+        T[name] = (out.w_keys.reshape(-1, 1).contiguous(), out.w_tiles)
+    host = {k: {"keys": v[0].cpu().numpy(), "tiles": v[1].cpu().numpy(), "dtype": "f32"} for k, v in T.items()}
+    e = w["E34"]
+    wk, wt, nt = tre.execute3(e["einsum"], e["upper"], e["extents"], e["tiles"], d["A"][0], d["A"][1],
+                              T["E1"][0], T["E1"][1], T["E2"][0], T["E2"][1])
+    rk, acc, mag, tri = orc.eval3(e["einsum"], e["upper"], e["extents"], e["tiles"], w["A"], host["E1"],
+                                  host["E2"])
+    assert nt == len(tri) == len(rk) == w["n_edges"]
+    assert np.array_equal(wk.cpu().numpy(), rk)
+    worst, ok = value_error(wt.cpu().numpy(), acc, mag)
+    assert ok and worst <= TOL["f32"], worst
+    S = tre.scale_f32(wt, w["scale"])
+    np.testing.assert_array_equal(S.cpu().numpy(), (wt.cpu().numpy() * np.float32(w["scale"])).astype(np.float32))
+    # binary path of Table gt-schema on the device
+    s3, s4 = w["E3"], w["E4"]
+    o3 = tre.einsum(tre.Plan.from_spec(s3), T["E1"][0], T["E1"][1], d["A"][0], d["A"][1])
+    o4 = tre.einsum(tre.Plan.from_spec(s4), o3.w_keys, o3.w_tiles, T["E2"][0], T["E2"][1])
+    assert torch.equal(o4.w_keys.reshape(wk.shape), wk)
+    worst, ok = value_error(o4.w_tiles.cpu().numpy(), acc, mag)
+    assert ok and worst <= TOL["f32"], worst
+
+
+def test_masked_edge_cases_gpu(orc):
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    rng = np.random.default_rng(8)
+    ext = {"i": 16, "j": 16, "k": 33}
+    til = {"i": 1, "j": 1}
+    U = _relation(rng, "ij", "ij", ext, til, 0.5)
+    V = _relation(rng, "ik", "ij", ext, til, 1.0)
+    X = _relation(rng, "jk", "ij", ext, til, 1.0)
+    uk, ut = to_dev(U)
+    vk, vt = to_dev(V)
+    xk, xt = to_dev(X)
+    e = "ij,ik,jk->ij"
+    wk, wt, nt = tre.execute3(e, "ij", ext, til, uk[:0], ut[:0], vk, vt, xk, xt)
+    assert nt == 0 and wk.shape[0] == 0
+    # no V tuple for any U row
+    wk, wt, nt = tre.execute3(e, "ij", ext, til, uk, ut, vk[:0], vt[:0], xk, xt)
+    assert nt == 0 and wk.shape[0] == 0
+    _, _, _, tm = tre.execute3(e, "ij", ext, til, uk, ut, vk, vt, xk, xt, timing=True)
+    assert tm["contract_ms"] > 0 and tm["join_ms"] > 0
+    with pytest.raises(tre.TreError) as err:
+        tre.execute3(e, "ij", ext, {"i": 2, "j": 1}, uk, ut, vk, vt, xk, xt)
+    assert err.value.status == "TRE_E_SHAPE"
+    with pytest.raises(tre.TreError) as err:
+        tre.execute3("ij,ik,jk->ji", "ij", ext, til, uk, ut, vk, vt, xk, xt)
+    assert err.value.status == "TRE_E_SPLIT"
+    with pytest.raises(tre.TreError) as err:
+        tre.execute3(e, "ij", ext, til, uk.flip(0).contiguous(), ut, vk, vt, xk, xt)
+    assert err.value.status == "TRE_E_UNSORTED"
+    # the scale glue: odd lengths, in place, a scale that rounds
+    x = torch.randn(1003, device="cuda")
+    y = tre.scale_f32(x, 0.1)
+    np.testing.assert_array_equal(y.cpu().numpy(), x.cpu().numpy() * np.float32(0.1))
+    z = x.clone()
+    tre.scale_f32(z, 3.0, out=z)
+    np.testing.assert_array_equal(z.cpu().numpy(), x.cpu().numpy() * np.float32(3.0))
