@@ -681,18 +681,21 @@ hipError_t launch_contract(const Plan& p, const Layout& L, char* ws, const void*
         return p.dtype == TRE_BF16 ? gemm_dispatch<uint16_t>(p, g, grid, n_pairs, unit_bound, s)
                                    : gemm_dispatch<float>(p, g, grid, n_pairs, unit_bound, s);
     }
+    // with vec_swap the kernel's first (vector) operand is V: the product is
+    // symmetric, so only the roles of the pointers and tables change
+    const bool sw = p.vec_swap;
     VecArgs a{};
-    a.U = u_tiles;
-    a.V = v_tiles;
-    a.pu = pu;
-    a.pv = pv;
-    a.u_elems = p.tile_elems[0];
-    a.v_elems = p.tile_elems[1];
+    a.U = sw ? v_tiles : u_tiles;
+    a.V = sw ? u_tiles : v_tiles;
+    a.pu = sw ? pv : pu;
+    a.pv = sw ? pu : pv;
+    a.u_elems = p.tile_elems[sw ? 1 : 0];
+    a.v_elems = p.tile_elems[sw ? 0 : 1];
     a.w_elems = p.tile_elems[2];
-    a.tEU = tb + p.table_off[T_EU];
-    a.tEV = tb + p.table_off[T_EV];
-    a.tKU = tb + p.table_off[T_KU];
-    a.tKV = tb + p.table_off[T_KV];
+    a.tEU = tb + p.table_off[sw ? T_EV : T_EU];
+    a.tEV = tb + p.table_off[sw ? T_EU : T_EV];
+    a.tKU = tb + p.table_off[sw ? T_KV : T_KU];
+    a.tKV = tb + p.table_off[sw ? T_KU : T_KV];
     a.K = int32_t(p.nK);
     a.units = units;
     a.hdr = hdr;

@@ -288,7 +288,9 @@ static tre_status classify(Plan& p) {
 
     // Vector class: EPT consecutive W elements per thread when U's offsets run
     // contiguously in aligned groups of EPT and V's either do too or stay
-    // constant over each group (V broadcast); otherwise one element.
+    // constant over each group (V broadcast), or the same with U and V
+    // exchanged (U broadcast: the kernel then reads V as its vector operand);
+    // otherwise one element.
     if (p.kclass == KC_VEC) {
         auto tEU = host_table(p.dims[T_EU]), tEV = host_table(p.dims[T_EV]);
         auto tKU = host_table(p.dims[T_KU]), tKV = host_table(p.dims[T_KV]);
@@ -316,6 +318,10 @@ static tre_status classify(Plan& p) {
         if (u_ok && p.tile_elems[2] % ept == 0 && (v_vec || v_const)) {
             p.vec_ept = ept;
             p.vec_vbcast = !v_vec;
+        } else if (v_vec && u_const && p.tile_elems[2] % ept == 0) {
+            p.vec_ept = ept;
+            p.vec_vbcast = true;
+            p.vec_swap = true;
         }
     }
     // GEMM staging: which dim of A / B has unit stride, and whether 8-wide

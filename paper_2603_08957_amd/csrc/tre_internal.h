@@ -76,6 +76,7 @@ struct Plan {
     // whether V's element is the same for a whole group of them
     int vec_ept = 1;
     bool vec_vbcast = false;
+    bool vec_swap = false;  // vector class: the kernel's vector operand is V and its broadcast one U
     bool fast = false;
     bool fast_a_rowfast = false, fast_b_rowfast = false;
     int64_t fast_lda = 0, fast_ldb = 0, fast_ldw = 0;
