@@ -524,7 +524,7 @@ class Attention:
 # the SHA-256 of the kernel source the counters were taken on.
 TRAFFIC_RECORDS = {1: "counters_gnn_chain_4096_fp32.md", 2: "counters_gnn_chain_262144_bf16.md",
                    3: "counters_block_sparse_16384_fp32.md", 4: "counters_sparse_3way_4096_fp32.md",
-                   5: "counters_gnn_chain_1048576_bf16.md"}
+                   5: "counters_gnn_chain_1048576_bf16.md", 6: "counters_graph_attention_13752_fp32.md"}
 
 
 def traffic_record(config, three_way="fused"):

@@ -26,12 +26,13 @@ def bench(monkeypatch):
 
 
 def test_traffic_record_matches_kernel_source(bench):
-    for c in (1, 2, 3, 4, 5):
+    for c in (1, 2, 3, 4, 5, 6):
         rec = bench.traffic_record(c)
         assert rec is not None, f"profile record of workload {c} should match the committed kernel source"
         assert rec["bytes"] == rec["read_bytes"] + rec["write_bytes"]
     # only for the launch configuration the counters were taken on
     assert bench.traffic_record(4, "binary") is None
+    assert bench.traffic_record(6, "binary") is None
     bench.PLAN_OPTIONS["u_ranges"] = 8
     assert bench.traffic_record(2) is None
 
