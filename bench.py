@@ -554,6 +554,162 @@ def traffic_record(config, three_way="fused"):
             "source": "profiles/" + name}
 
 
+# ------------------------------------------------ planner check (Sec. 8)
+
+def relation_from_dense(A, labels, promoted):
+    """Tensor relation of a dense array under the promoted set: one tuple per
+    combination of promoted indices whose slice holds a non-zero, keys in
+    lexicographic order, tiles row-major over the demoted labels."""
+    pa = [i for i, l in enumerate(labels) if l in promoted]
+    da = [i for i, l in enumerate(labels) if l not in promoted]
+    B = np.transpose(A, pa + da)
+    kshape = B.shape[:len(pa)]
+    flat = B.reshape(int(np.prod(kshape)) if kshape else 1, -1)
+    nz = np.nonzero(np.any(flat != 0, axis=1))[0]
+    keys = np.stack(np.unravel_index(nz, kshape), axis=1).astype(np.int32) if kshape \
+        else np.zeros((len(nz), 0), np.int32)
+    return {"keys": keys, "tiles": np.ascontiguousarray(flat[nz]), "dtype": "f32"}
+
+
+def dense_stats(pl, A, labels):
+    nz = A != 0
+    return pl.Stats(labels, {l: A.shape[i] for i, l in enumerate(labels)}, float(nz.sum()),
+                    {l: float(np.any(nz, axis=tuple(j for j in range(A.ndim) if j != i)).sum())
+                     for i, l in enumerate(labels)}, A.itemsize)
+
+
+def planner_check(tre, torch, top, steps):
+    """Rank every decomposition of the fp32 GNN chain (4096 vertices) with
+    the planner, calibrated to this GPU (c_xfer = 1 / 8 TB/s, c_flop = 1 /
+    157.3 TFLOP/s, c_fixed measured on a scalar cross product, c_call on a
+    one-pair EinSum), then run the
+    cheapest ``top`` plans and a spread of the rest through the library,
+    each decomposed as planned (inputs laid out on the host, the result of
+    E1 repartitioned on the device when E2 wants another decomposition), and
+    time them; every plan's result is checked against dense fp64."""
+    import workloads
+    from paper_2603_08957_amd import planner as pl
+
+    w = workloads.config(1)
+    n, emb, zo = w["n"], w["emb"], w["z_out"]
+    X = np.ascontiguousarray(w["X"]["tiles"].reshape(n // 64, emb, 64).transpose(1, 0, 2).reshape(emb, n))
+    Y = np.zeros((n, n), np.float32)
+    Y[w["Y"]["coo"][0][:, 0], w["Y"]["coo"][0][:, 1]] = w["Y"]["coo"][1]
+    Z = w["Z"]["tiles"].reshape(emb, zo)
+    ref = (X.astype(np.float64) @ Y).T @ Z.astype(np.float64)
+    mag = (np.abs(X.astype(np.float64)) @ np.abs(Y)).T @ np.abs(Z.astype(np.float64))
+    # c_fixed: a cross product of two 4096-tuple scalar relations into one group
+    m = 4096
+    cp = tre.Plan("i,j->", "ij", {"i": m, "j": m}, {"i": 1, "j": 1}, "f32", validate=False)
+    ck = torch.arange(m, dtype=torch.int32, device="cuda").reshape(m, 1)
+    ct = torch.ones((m, 1), dtype=torch.float32, device="cuda")
+    cst = Stage(tre, torch, {"einsum": "i,j->", "upper": "ij", "extents": {"i": m, "j": m},
+                             "tiles": {"i": 1, "j": 1}, "dtype": "f32"}, m, m, m * m, "cross")
+    for _ in range(2):
+        cst.run(ck, ct, ck, ct)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        cst.run(ck, ct, ck, ct)
+    e1.record()
+    torch.cuda.synchronize()
+    c_fixed = e0.elapsed_time(e1) * 1e-3 / steps / (m * m)
+    del cp
+    # c_call: one library call on one pair of one-element tuples
+    one = torch.zeros((1, 1), dtype=torch.int32, device="cuda")
+    lst = Stage(tre, torch, {"einsum": "i,i->i", "upper": "i", "extents": {"i": 1}, "tiles": {"i": 1},
+                             "dtype": "f32"}, 1, 1, 1, "latency")
+    for _ in range(2):
+        lst.run(one, ct[:1], one, ct[:1])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        lst.run(one, ct[:1], one, ct[:1])
+    torch.cuda.synchronize()
+    c_call = (time.perf_counter() - t0) / steps
+    cap = 64 << 20
+    prog = pl.Program({"X": dense_stats(pl, X, "ij"), "Y": dense_stats(pl, Y, "jk"), "Z": dense_stats(pl, Z, "im")},
+                      [pl.EinSum("E1", "ij,jk->ki", "X", "Y"), pl.EinSum("E2", "ki,im->km", "E1", "Z")])
+    costs = pl.Costs.mi355x("f32", c_fixed=c_fixed, max_call_bytes=cap, c_call=c_call)
+    ranked = pl.optimize(prog, costs, k=64)
+    picks = list(range(min(top, len(ranked))))
+    rest = list(range(len(picks), len(ranked)))
+    picks += [rest[int(i)] for i in np.linspace(0, len(rest) - 1, min(3, len(rest)))] if rest else []
+    ext1 = {"i": emb, "j": n, "k": n}
+    ext2 = {"k": n, "i": emb, "m": zo}
+    out = []
+    for r in picks:
+        cost, plan = ranked[r]
+        P1, P2 = set(plan["E1"]), set(plan["E2"])
+        s1 = {"einsum": "ij,jk->ki", "upper": "".join(sorted(P1)), "extents": ext1, "tiles": {l: 1 for l in P1},
+              "dtype": "f32"}
+        s2 = {"einsum": "ki,im->km", "upper": "".join(sorted(P2)), "extents": ext2, "tiles": {l: 1 for l in P2},
+              "dtype": "f32"}
+        xk, xt = dev_rel(relation_from_dense(X, "ij", P1), torch)
+        yk, yt = dev_rel(relation_from_dense(Y, "jk", P1), torch)
+        zk, zt = dev_rel(relation_from_dense(Z, "im", P2), torch)
+        w_in = "".join(l for l in "ki" if l in P1)
+        w_out = "".join(l for l in "ki" if l in P2)
+        probe = tre.einsum(tre.Plan.from_spec(s1, validate=False), xk, xt, yk, yt)
+        st1 = Stage(tre, torch, s1, int(xk.shape[0]), int(yk.shape[0]), max(probe.n_pairs, 1), "E1")
+        n2 = probe.n_w if w_in == w_out else None
+        if n2 is None:
+            rk, _ = tre.repartition("ki", w_in, w_out, {"k": n, "i": emb}, {l: 1 for l in w_in},
+                                    {l: 1 for l in w_out}, probe.w_keys, probe.w_tiles)
+            n2 = int(rk.shape[0])
+        probe2 = None
+        st2 = None
+
+        def step():
+            nonlocal probe2, st2
+            tk, tt = st1.run(xk, xt, yk, yt)
+            if w_in != w_out:
+                tk, tt = tre.repartition("ki", w_in, w_out, {"k": n, "i": emb}, {l: 1 for l in w_in},
+                                         {l: 1 for l in w_out}, tk if tk.shape[1] else None, tt)
+            if st2 is None:
+                probe2 = tre.einsum(tre.Plan.from_spec(s2, validate=False), tk, tt, zk, zt)
+                st2 = Stage(tre, torch, s2, int(tk.shape[0]), int(zk.shape[0]), max(probe2.n_pairs, 1), "E2")
+            st2.n_u = int(tk.shape[0])
+            return st2.run(tk, tt, zk, zt)
+
+        for _ in range(2):
+            wk, wt = step()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(steps):
+            wk, wt = step()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        # the result, assembled densely, against fp64
+        got = np.zeros((n, zo))
+        keys, tiles = wk.cpu().numpy(), wt.cpu().numpy()
+        pk = [l for l in "km" if l in P2]
+        for q in range(len(tiles)):
+            sl = []
+            for ax, l in enumerate("km"):
+                ln = (n, zo)[ax]
+                sl.append(slice(int(keys[q][pk.index(l)]), int(keys[q][pk.index(l)]) + 1) if l in pk else slice(0, ln))
+            got[tuple(sl)] = tiles[q].reshape(got[tuple(sl)].shape)
+        err = float((np.abs(got - ref) / np.maximum(mag, 1e-300))[mag > 0].max())
+        out.append({"rank": r + 1, "plan": plan, "estimated_ms": cost * 1e3, "measured_ms": ms,
+                    "e1_pairs": int(st1.n_pairs), "e2_pairs": int(st2.n_pairs), "repartition": w_in != w_out,
+                    "max_mag_rel_err": err})
+        log(f"[bench] plan rank {r + 1} {plan}: estimated {cost * 1e3:.3f} ms, measured {ms:.3f} ms, err {err:.1e}")
+        del st1, st2, xk, xt, yk, yt, zk, zt
+        torch.cuda.empty_cache()
+    order_est = [o["estimated_ms"] for o in out]
+    order_meas = [o["measured_ms"] for o in out]
+    from scipy.stats import spearmanr
+
+    return {"metric": "planner ranking: estimated vs measured step time of the fp32 GNN chain (4096 vertices), 1 "
+                      "MI355X", "c_fixed_s": c_fixed, "c_xfer_s_per_byte": costs.c_xfer, "c_flop_s": costs.c_flop,
+            "c_call_s": c_call, "max_call_bytes": cap, "feasible_plans": len(ranked), "plans": out,
+            "spearman_estimated_vs_measured": float(spearmanr(order_est, order_meas)[0]),
+            "measured_best_is_estimated_best": bool(int(np.argmin(order_meas)) == 0),
+            "steps": steps, "data": "synthetic"}
+
+
 def make_workload(c, tre, torch, three_way="fused"):
     if c in (1, 2, 5):
         return GnnChain(c, tre, torch)
@@ -582,6 +738,9 @@ def main():
                     help="workloads 4 and 6: one fused three-operand EinSum (default) or two binary EinSums")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="first run one device copy of this many GiB (counter calibration under rocprofv3 --pmc)")
+    ap.add_argument("--planner-top", type=int, default=0, metavar="K",
+                    help="instead of the benchmark: rank the decompositions of the fp32 GNN chain with the planner, "
+                         "run the K cheapest and a spread of the rest, and print estimated vs measured times")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (the path shards by output key "
@@ -607,6 +766,9 @@ def main():
         del src, dst
     PLAN_OPTIONS["u_ranges"] = args.u_ranges
     PLAN_OPTIONS["pace_windows"] = args.pace_windows
+    if args.planner_top:
+        print(json.dumps(planner_check(tre, torch, args.planner_top, args.steps)), flush=True)
+        return
     W = make_workload(args.config, tre, torch, args.three_way)
     log("[bench] inputs resident; warming up")
     for _ in range(args.warmup):

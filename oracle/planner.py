@@ -19,7 +19,9 @@ stated in the planner's documentation: C_add = one flop per W tile element,
 flops of the kernel = 2 x the product of all demoted extents of U and V,
 a key attribute takes 4 bytes, EinSum results hold 4-byte elements, and
 result statistics come from the classical estimators on the purely
-relational form (Algorithm GetStats).
+relational form (Algorithm GetStats).  The optional per-call latency
+``c_call`` (0 unless given) is charged once per EinSum and once per
+repartition that changes the decomposition.
 """
 from __future__ import annotations
 
@@ -126,7 +128,7 @@ def einsum_cost(tu, tv, tw, prom, p):
     t_agg = min(0.5 * t_join, groups)
     c_add = tile_elems(tw, prom) * p["c_flop"]
     c_agg = (t_join - t_agg) * (row_bytes(tw, prom) * p["c_xfer"] + c_add + p["c_fixed"])
-    return c_join + c_agg
+    return c_join + c_agg + p.get("c_call", 0.0)
 
 
 def repart(t, p_in, p_out, p):
@@ -136,7 +138,7 @@ def repart(t, p_in, p_out, p):
         return 0.0
     union = a | b
     moved = 2 * count(t, union) - count(t, a) - count(t, b)
-    return moved * (row_bytes(t, union) * p["c_xfer"] + p["c_fixed"])
+    return moved * (row_bytes(t, union) * p["c_xfer"] + p["c_fixed"]) + p.get("c_call", 0.0)
 
 
 def all_plans(prog):

@@ -37,6 +37,14 @@ extents of every demoted label of U and V (the dense tile contraction);
 C_add, which the paper leaves undefined, is read as one flop per element of
 a W tile.  A choice whose kernel call (one U, V and W tile) exceeds
 ``max_call_bytes`` is excluded (the memory constraint of Sec. 8).
+
+One term is added to the paper's model: ``c_call``, a fixed latency per
+EinSum and per repartition (kernel launches and the count read-backs of one
+library call).  The paper's constants are per tuple and per byte, which on
+a cluster dominate; on one GPU a small EinSum costs about one such latency
+whatever its tuples, so plans that repartition more are slower than the
+per-tuple terms say.  With ``c_call = 0`` (the default) the model is the
+paper's.
 """
 from __future__ import annotations
 
@@ -70,12 +78,15 @@ class Costs:
     c_flop: float
     c_fixed: float
     max_call_bytes: float = math.inf
+    c_call: float = 0.0
 
     @classmethod
-    def mi355x(cls, dtype: str = "f32", c_fixed: float = 2e-10, max_call_bytes: float = math.inf) -> "Costs":
+    def mi355x(cls, dtype: str = "f32", c_fixed: float = 2e-10, max_call_bytes: float = math.inf,
+               c_call: float = 0.0) -> "Costs":
         """c_xfer from the HBM bandwidth, c_flop from the dense peak of the
-        kernel's input type, c_fixed a measured per-tuple overhead."""
-        return cls(1.0 / PEAK_HBM_BYTES_S, 1.0 / PEAK_FLOPS[dtype], c_fixed, max_call_bytes)
+        kernel's input type, c_fixed a measured per-tuple overhead, c_call a
+        measured per-call latency."""
+        return cls(1.0 / PEAK_HBM_BYTES_S, 1.0 / PEAK_FLOPS[dtype], c_fixed, max_call_bytes, c_call)
 
 
 @dataclass
@@ -198,7 +209,7 @@ def local_cost(su: Stats, sv: Stats, sw: Stats, P: frozenset, c: Costs) -> float
     t_agg = min(t_join / 2.0, groups)
     add = tile_bytes(sw, pw) / sw.elem_bytes  # elements of a W tile
     c_agg = (t_join - t_agg) * (tuple_bytes(sw, pw) * c.c_xfer + add * c.c_flop + c.c_fixed)
-    return c_join + c_agg
+    return c_join + c_agg + c.c_call
 
 
 def repart_cost(st: Stats, p_in, p_out, c: Costs) -> float:
@@ -208,7 +219,7 @@ def repart_cost(st: Stats, p_in, p_out, c: Costs) -> float:
         return 0.0
     both = p_in | p_out
     n_int = 2.0 * tuples(st, both) - tuples(st, p_in) - tuples(st, p_out)
-    return n_int * (tuple_bytes(st, both) * c.c_xfer + c.c_fixed)
+    return n_int * (tuple_bytes(st, both) * c.c_xfer + c.c_fixed) + c.c_call
 
 
 def _renamed(st: Stats, letters: str) -> Stats:

@@ -49,3 +49,26 @@ def test_traffic_record_null_after_kernel_change(bench, tmp_path, monkeypatch):
     (tmp_path / rec["kernel_source"]).write_bytes(open(os.path.join(ROOT, rec["kernel_source"]), "rb").read())
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
     assert bench.traffic_record(2) is None
+
+
+def test_relation_from_dense_matches_the_generator(bench):
+    """The planner check lays out dense arrays as relations: for the
+    adjacency of the 4096-vertex graph in 64 x 64 tiles' promoted form (here
+    both labels promoted with tiles of 1) the keys are the edges and the
+    tiles their values; with nothing promoted one tuple holds the array."""
+    import numpy as np
+
+    import workloads
+
+    w = workloads.config(1, "small")
+    n = w["n"]
+    Y = np.zeros((n, n), np.float32)
+    Y[w["Y"]["coo"][0][:, 0], w["Y"]["coo"][0][:, 1]] = w["Y"]["coo"][1]
+    rel = bench.relation_from_dense(Y, "jk", {"j", "k"})
+    assert np.array_equal(rel["keys"], w["Y"]["coo"][0].astype(np.int32))
+    assert np.array_equal(rel["tiles"][:, 0], w["Y"]["coo"][1].astype(np.float32))
+    rows = bench.relation_from_dense(Y, "jk", {"k"})
+    assert np.array_equal(rows["keys"][:, 0], np.unique(w["Y"]["coo"][0][:, 1]))
+    assert np.array_equal(rows["tiles"], Y.T[rows["keys"][:, 0]])
+    one = bench.relation_from_dense(Y, "jk", set())
+    assert one["keys"].shape == (1, 0) and np.array_equal(one["tiles"][0], Y.reshape(-1))

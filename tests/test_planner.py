@@ -16,8 +16,8 @@ import workloads
 from oracle import planner as op
 
 
-def _costs(c_xfer=1e-12, c_flop=1e-14, c_fixed=1e-9, cap=math.inf):
-    return {"c_xfer": c_xfer, "c_flop": c_flop, "c_fixed": c_fixed, "max_call_bytes": cap}
+def _costs(c_xfer=1e-12, c_flop=1e-14, c_fixed=1e-9, cap=math.inf, c_call=0.0):
+    return {"c_xfer": c_xfer, "c_flop": c_flop, "c_fixed": c_fixed, "max_call_bytes": cap, "c_call": c_call}
 
 
 # ------------------------------------------------------------- oracle pins
@@ -107,6 +107,18 @@ def test_kernel_flops_and_memory_cap():
     assert op.einsum_cost(tu, tv, tw, set(), _costs(cap=tiles - 1)) == math.inf
 
 
+def test_per_call_latency():
+    """c_call is charged once per EinSum and once per changing repartition."""
+    tu = _dense_stats("ij", {"i": 4, "j": 3})
+    tv = _dense_stats("jk", {"j": 3, "k": 5})
+    tw = op.derive("ij", "jk", "ik", tu, tv)
+    base = op.einsum_cost(tu, tv, tw, {"i"}, _costs())
+    assert op.einsum_cost(tu, tv, tw, {"i"}, _costs(c_call=7.0)) == pytest.approx(base + 7.0, rel=1e-12)
+    assert op.repart(tw, {"i"}, {"i"}, _costs(c_call=7.0)) == 0.0
+    r = op.repart(tw, {"i"}, {"k"}, _costs())
+    assert op.repart(tw, {"i"}, {"k"}, _costs(c_call=7.0)) == pytest.approx(r + 7.0, rel=1e-12)
+
+
 def test_repart_properties():
     t = {"labels": "abc", "extents": {"a": 9, "b": 7, "c": 5}, "nnz": 120.0, "distinct": {"a": 9, "b": 7, "c": 5},
          "elem_bytes": 4}
@@ -171,7 +183,8 @@ def _to_product(prog, c):
     inputs = {k: pl.Stats(t["labels"], t["extents"], t["nnz"], t["distinct"], t["elem_bytes"])
               for k, t in prog["inputs"].items()}
     einsums = [pl.EinSum(n, e, a, b) for n, e, a, b in prog["einsums"]]
-    return pl.Program(inputs, einsums), pl.Costs(c["c_xfer"], c["c_flop"], c["c_fixed"], c["max_call_bytes"])
+    return pl.Program(inputs, einsums), pl.Costs(c["c_xfer"], c["c_flop"], c["c_fixed"], c["max_call_bytes"],
+                                                 c["c_call"])
 
 
 @pytest.mark.parametrize("seed", range(60))
@@ -183,7 +196,8 @@ def test_planner_matches_exhaustive_search(seed):
     rng = np.random.default_rng(900 + seed)
     prog = _rand_program(rng)
     cap = math.inf if seed % 3 else float(rng.integers(200, 20000))
-    c = _costs(10 ** rng.uniform(-13, -10), 10 ** rng.uniform(-15, -12), 10 ** rng.uniform(-11, -8), cap)
+    c = _costs(10 ** rng.uniform(-13, -10), 10 ** rng.uniform(-15, -12), 10 ** rng.uniform(-11, -8), cap,
+               0.0 if seed % 2 else 10 ** rng.uniform(-6, -3))
     want = op.best_plans(prog, c, k=4)
     P, C = _to_product(prog, c)
     got = pl.optimize(P, C, k=4)
