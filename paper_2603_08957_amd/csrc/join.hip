@@ -14,7 +14,9 @@
 //            order.  Each pair gets its packed W key; a stable radix sort by
 //            W key (skipped when W's keys are a prefix of U's) carrying the
 //            packed (u, v) gives the canonical (w_key, u, v) order; run-length
-//            encoding gives the output keys and segment offsets.
+//            encoding gives the output keys and segment offsets (by a scan
+//            over the key space instead of the pairs when the W key space
+//            is smaller than the pair count).
 #include "tre_internal.h"
 
 namespace tre {
@@ -115,6 +117,51 @@ __global__ void k_count(const int32_t* __restrict__ ukeys, int64_t n_u, int ru, 
     cnt[u] = c - a;
 }
 
+// Same as k_count when the join labels are the first attributes of V's key
+// (V is then sorted by them): the search compares those attributes of V's
+// rows directly, so V's join keys need not be packed first.
+__device__ inline int cmp_prefix(const int32_t* vrow, const int32_t* key, int n) {
+    for (int i = 0; i < n; i++) {
+        if (vrow[i] != key[i]) return vrow[i] < key[i] ? -1 : 1;
+    }
+    return 0;
+}
+
+__global__ void k_count_prefix(const int32_t* __restrict__ ukeys, int64_t n_u, int ru, KeyDesc du,
+                               const int32_t* __restrict__ vkeys, int64_t n_v, int rv, int64_t* __restrict__ cnt,
+                               int64_t* __restrict__ lo) {
+    const int64_t u = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (u > n_u) return;
+    if (u == n_u) {
+        cnt[u] = 0;
+        return;
+    }
+    int32_t key[26];
+    for (int i = 0; i < du.n; i++) key[i] = ukeys[u * ru + du.pos[i]];
+    int64_t a = 0, b = n_v;
+    while (a < b) {
+        const int64_t m = (a + b) >> 1;
+        if (cmp_prefix(vkeys + m * rv, key, du.n) < 0) a = m + 1; else b = m;
+    }
+    int64_t c = a;
+    if (a < n_v && cmp_prefix(vkeys + a * rv, key, du.n) == 0) {
+        int64_t last = a, step = 1, probe = a + 1;
+        while (probe < n_v && cmp_prefix(vkeys + probe * rv, key, du.n) == 0) {
+            last = probe;
+            step <<= 1;
+            probe = a + step;
+        }
+        int64_t x = last + 1, y = min(probe, n_v);
+        while (x < y) {
+            const int64_t m = (x + y) >> 1;
+            if (cmp_prefix(vkeys + m * rv, key, du.n) == 0) x = m + 1; else y = m;
+        }
+        c = x;
+    }
+    lo[u] = a;
+    cnt[u] = c - a;
+}
+
 __global__ void k_store_count(const int64_t* __restrict__ off, int64_t n_u, WsHeader* hdr) {
     hdr->n_pairs = off[n_u];
 }
@@ -174,6 +221,40 @@ __global__ __launch_bounds__(kThreads) void k_expand(const int64_t* __restrict__
             pu[b0 + q] = int32_t(suv[q] >> 32);
             pv[b0 + q] = int32_t(suv[q] & 0xffffffffu);
         }
+    }
+}
+
+// Segments over a small key space (2^bits <= pairs): first[k] = 1 + the
+// index of key k's first pair (0: absent), then the present keys are
+// compacted in key order by a scan over the key space instead of over the
+// pairs.
+__global__ void k_first_of_key(const uint64_t* __restrict__ wk, int64_t n, int32_t* __restrict__ first) {
+    const int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (p >= n) return;
+    const uint64_t k = wk[p];
+    if (p == 0 || k != wk[p - 1]) first[k] = int32_t(p + 1);
+}
+
+__global__ void k_key_flags(const int32_t* __restrict__ first, int64_t nk, int32_t* __restrict__ flags) {
+    const int64_t q = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (q > nk) return;
+    flags[q] = (q < nk && first[q] != 0) ? 1 : 0;
+}
+
+__global__ void k_key_compact(const int32_t* __restrict__ first, int64_t nk, const int32_t* __restrict__ seg_of,
+                              int64_t n_pairs, int32_t* __restrict__ seg_start, uint64_t* __restrict__ seg_key,
+                              WsHeader* hdr) {
+    const int64_t q = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (q > nk) return;
+    if (q == nk) {
+        seg_start[seg_of[nk]] = int32_t(n_pairs);
+        hdr->n_w = seg_of[nk];
+        return;
+    }
+    const int32_t f = first[q];
+    if (f != 0) {
+        seg_start[seg_of[q]] = f - 1;
+        seg_key[seg_of[q]] = uint64_t(q);
     }
 }
 
@@ -246,18 +327,22 @@ hipError_t launch_join(const Plan& p, const Layout& L, char* ws, const int32_t* 
     int32_t* hist = reinterpret_cast<int32_t*>(ws + L.hist);
     const int64_t n_u = L.n_u, n_v = L.n_v;
     hipError_t e = hipSuccess;
-    if (p.n_join > 0 && n_v > 0) {
-        k_pack_join<<<blocks_for(n_v), kThreads, 0, s>>>(v_keys, n_v, p.nk[1], desc_v(p), vjk, vperm);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-        if (p.v_needs_sort) {
+    if (p.n_join > 0 && n_v > 0 && !p.v_needs_sort) {
+        // the join labels lead V's key: search V's rows as they are
+        k_count_prefix<<<blocks_for(n_u + 1), kThreads, 0, s>>>(u_keys, n_u, p.nk[0], desc_u(p), v_keys, n_v,
+                                                                 p.nk[1], cnt, lo);
+    } else {
+        if (p.n_join > 0 && n_v > 0) {
+            k_pack_join<<<blocks_for(n_v), kThreads, 0, s>>>(v_keys, n_v, p.nk[1], desc_v(p), vjk, vperm);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
             e = radix_sort_u64(vjk, vperm, reinterpret_cast<uint64_t*>(ws + L.vjk_alt),
                                reinterpret_cast<uint32_t*>(ws + L.vperm_alt), n_v, p.join_total_bits, hist,
                                reinterpret_cast<int32_t*>(tmp), s);
             if (e != hipSuccess) return e;
         }
+        k_count<<<blocks_for(n_u + 1), kThreads, 0, s>>>(u_keys, n_u, p.nk[0], desc_u(p), vjk_sorted, n_v,
+                                                          p.n_join > 0, cnt, lo);
     }
-    k_count<<<blocks_for(n_u + 1), kThreads, 0, s>>>(u_keys, n_u, p.nk[0], desc_u(p), vjk_sorted, n_v, p.n_join > 0,
-                                                      cnt, lo);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = scan_exclusive_i64(cnt, cnt, n_u + 1, tmp, s)) != hipSuccess) return e;
     k_store_count<<<1, 1, 0, s>>>(cnt, n_u, hdr);
@@ -304,6 +389,21 @@ hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t*
                                  pv, s);
         if (e != hipSuccess) return e;
         if (radix_result_in_alt(n_pairs, p.w_total_bits)) wk = reinterpret_cast<uint64_t*>(ws + L.wk_alt);
+    }
+    const int64_t key_space = int64_t(1) << p.w_total_bits;
+    if (p.w_total_bits > 0 && p.w_total_bits <= 30 && key_space <= n_pairs) {
+        // small key space: find the segments by key instead of by pair
+        int32_t* first = flags;  // key_space + 1 <= n_pairs + 1 entries
+        int32_t* kflags = reinterpret_cast<int32_t*>(ws + L.part_off);  // free until the work units are made
+        if ((e = launch_fill_zero(first, sizeof(int32_t) * size_t(key_space), s)) != hipSuccess) return e;
+        k_first_of_key<<<blocks_for(n_pairs), kThreads, 0, s>>>(wk, n_pairs, first);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        k_key_flags<<<blocks_for(key_space + 1), kThreads, 0, s>>>(first, key_space, kflags);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = scan_exclusive_i32(kflags, kflags, key_space + 1, tmp, s)) != hipSuccess) return e;
+        k_key_compact<<<blocks_for(key_space + 1), kThreads, 0, s>>>(first, key_space, kflags, n_pairs, seg_start,
+                                                                      seg_key, hdr);
+        return hipGetLastError();
     }
     k_heads<<<blocks_for(n_pairs + 1), kThreads, 0, s>>>(wk, n_pairs, flags);
     if ((e = hipGetLastError()) != hipSuccess) return e;
