@@ -179,14 +179,17 @@ __device__ inline uint64_t pack_w(const int32_t* urow, const int32_t* vrow, cons
 // arrays (no group sort) or packed (u << 32 | v) payloads for the sort.  A
 // workgroup's 2048 pairs are staged in LDS and written out by consecutive
 // threads, so every store instruction covers consecutive pairs.
+// KT: uint32 W keys when they fit in 32 bits (less traffic in the sort),
+// else uint64.
+template <typename KT>
 __global__ __launch_bounds__(kThreads) void k_expand(const int64_t* __restrict__ off, const int64_t* __restrict__ lo,
                                                      int64_t n_u, int64_t n_pairs, const uint32_t* __restrict__ vperm,
                                                      const int32_t* __restrict__ ukeys, int ru,
                                                      const int32_t* __restrict__ vkeys, int rv, WDesc wd,
                                                      int32_t* __restrict__ pu, int32_t* __restrict__ pv,
-                                                     uint64_t* __restrict__ wk, uint64_t* __restrict__ uv) {
+                                                     KT* __restrict__ wk, uint64_t* __restrict__ uv) {
     constexpr int kBlockPairs = kThreads * kPairsPerThread;
-    __shared__ uint64_t swk[kBlockPairs];
+    __shared__ KT swk[kBlockPairs];
     __shared__ uint64_t suv[kBlockPairs];
     const int64_t b0 = int64_t(blockIdx.x) * kBlockPairs;
     const int64_t p0 = b0 + int64_t(threadIdx.x) * kPairsPerThread;
@@ -207,7 +210,7 @@ __global__ __launch_bounds__(kThreads) void k_expand(const int64_t* __restrict__
             }
             const int64_t vs = lo[u] + (p - off[u]);
             const int64_t v = vperm ? int64_t(vperm[vs]) : vs;
-            swk[p - b0] = pack_w(ukeys + u * ru, vkeys + v * rv, wd);
+            swk[p - b0] = KT(pack_w(ukeys + u * ru, vkeys + v * rv, wd));
             suv[p - b0] = (uint64_t(uint32_t(u)) << 32) | uint64_t(uint32_t(v));
         }
     }
@@ -228,10 +231,11 @@ __global__ __launch_bounds__(kThreads) void k_expand(const int64_t* __restrict__
 // index of key k's first pair (0: absent), then the present keys are
 // compacted in key order by a scan over the key space instead of over the
 // pairs.
-__global__ void k_first_of_key(const uint64_t* __restrict__ wk, int64_t n, int32_t* __restrict__ first) {
+template <typename KT>
+__global__ void k_first_of_key(const KT* __restrict__ wk, int64_t n, int32_t* __restrict__ first) {
     const int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (p >= n) return;
-    const uint64_t k = wk[p];
+    const KT k = wk[p];
     if (p == 0 || k != wk[p - 1]) first[k] = int32_t(p + 1);
 }
 
@@ -258,13 +262,15 @@ __global__ void k_key_compact(const int32_t* __restrict__ first, int64_t nk, con
     }
 }
 
-__global__ void k_heads(const uint64_t* __restrict__ wk, int64_t n, int32_t* __restrict__ flags) {
+template <typename KT>
+__global__ void k_heads(const KT* __restrict__ wk, int64_t n, int32_t* __restrict__ flags) {
     const int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (p > n) return;
     flags[p] = (p < n && (p == 0 || wk[p] != wk[p - 1])) ? 1 : 0;
 }
 
-__global__ void k_compact(const uint64_t* __restrict__ wk, int64_t n, const int32_t* __restrict__ seg_of,
+template <typename KT>
+__global__ void k_compact(const KT* __restrict__ wk, int64_t n, const int32_t* __restrict__ seg_of,
                           int32_t* __restrict__ seg_start, uint64_t* __restrict__ seg_key, WsHeader* hdr) {
     const int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (p > n) return;
@@ -276,7 +282,7 @@ __global__ void k_compact(const uint64_t* __restrict__ wk, int64_t n, const int3
     if (p == 0 || wk[p] != wk[p - 1]) {
         const int32_t s = seg_of[p];
         seg_start[s] = int32_t(p);
-        seg_key[s] = wk[p];
+        seg_key[s] = uint64_t(wk[p]);
     }
 }
 
@@ -349,9 +355,11 @@ hipError_t launch_join(const Plan& p, const Layout& L, char* ws, const int32_t* 
     return hipGetLastError();
 }
 
-hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
-                        int64_t n_pairs, hipStream_t s, int stage) {
-    (void)stage;
+namespace {
+
+template <typename KT>
+hipError_t group_impl(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
+                      int64_t n_pairs, hipStream_t s) {
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
     int64_t* off = reinterpret_cast<int64_t*>(ws + L.ucnt);
     int64_t* lo = reinterpret_cast<int64_t*>(ws + L.ulo);
@@ -360,7 +368,7 @@ hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t*
         vperm = reinterpret_cast<uint32_t*>(ws + (radix_result_in_alt(L.n_v, p.join_total_bits) ? L.vperm_alt : L.vperm));
     int32_t* pu = reinterpret_cast<int32_t*>(ws + L.pu);
     int32_t* pv = reinterpret_cast<int32_t*>(ws + L.pv);
-    uint64_t* wk = reinterpret_cast<uint64_t*>(ws + L.wk);
+    KT* wk = reinterpret_cast<KT*>(ws + L.wk);
     int32_t* tmp = reinterpret_cast<int32_t*>(ws + L.scan_tmp);
     int32_t* hist = reinterpret_cast<int32_t*>(ws + L.hist);
     int32_t* flags = reinterpret_cast<int32_t*>(ws + L.flags);
@@ -378,17 +386,20 @@ hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t*
     uint64_t* uv = sort ? reinterpret_cast<uint64_t*>(ws + L.pidx) : nullptr;
     if (n_pairs > 0) {
         const int64_t threads = (n_pairs + kPairsPerThread - 1) / kPairsPerThread;
-        k_expand<<<blocks_for(threads), kThreads, 0, s>>>(off, lo, L.n_u, n_pairs, vperm, u_keys, p.nk[0], v_keys,
-                                                          p.nk[1], wd, pu, pv, wk, uv);
+        k_expand<KT><<<blocks_for(threads), kThreads, 0, s>>>(off, lo, L.n_u, n_pairs, vperm, u_keys, p.nk[0], v_keys,
+                                                              p.nk[1], wd, pu, pv, wk, uv);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (sort) {
         // the last pass writes the sorted (u, v) straight into pu / pv
-        e = radix_sort_u64_pairs(wk, uv, reinterpret_cast<uint64_t*>(ws + L.wk_alt),
-                                 reinterpret_cast<uint64_t*>(ws + L.pidx_alt), n_pairs, p.w_total_bits, hist, tmp, pu,
-                                 pv, s);
+        KT* wk_alt = reinterpret_cast<KT*>(ws + L.wk_alt);
+        uint64_t* uv_alt = reinterpret_cast<uint64_t*>(ws + L.pidx_alt);
+        if constexpr (sizeof(KT) == 4)
+            e = radix_sort_u32_pairs(wk, uv, wk_alt, uv_alt, n_pairs, p.w_total_bits, hist, tmp, pu, pv, s);
+        else
+            e = radix_sort_u64_pairs(wk, uv, wk_alt, uv_alt, n_pairs, p.w_total_bits, hist, tmp, pu, pv, s);
         if (e != hipSuccess) return e;
-        if (radix_result_in_alt(n_pairs, p.w_total_bits)) wk = reinterpret_cast<uint64_t*>(ws + L.wk_alt);
+        if (radix_result_in_alt(n_pairs, p.w_total_bits)) wk = wk_alt;
     }
     const int64_t key_space = int64_t(1) << p.w_total_bits;
     if (p.w_total_bits > 0 && p.w_total_bits <= 30 && key_space <= n_pairs) {
@@ -396,7 +407,7 @@ hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t*
         int32_t* first = flags;  // key_space + 1 <= n_pairs + 1 entries
         int32_t* kflags = reinterpret_cast<int32_t*>(ws + L.part_off);  // free until the work units are made
         if ((e = launch_fill_zero(first, sizeof(int32_t) * size_t(key_space), s)) != hipSuccess) return e;
-        k_first_of_key<<<blocks_for(n_pairs), kThreads, 0, s>>>(wk, n_pairs, first);
+        k_first_of_key<KT><<<blocks_for(n_pairs), kThreads, 0, s>>>(wk, n_pairs, first);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         k_key_flags<<<blocks_for(key_space + 1), kThreads, 0, s>>>(first, key_space, kflags);
         if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -405,11 +416,20 @@ hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t*
                                                                       seg_key, hdr);
         return hipGetLastError();
     }
-    k_heads<<<blocks_for(n_pairs + 1), kThreads, 0, s>>>(wk, n_pairs, flags);
+    k_heads<KT><<<blocks_for(n_pairs + 1), kThreads, 0, s>>>(wk, n_pairs, flags);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = scan_exclusive_i32(flags, flags, n_pairs + 1, tmp, s)) != hipSuccess) return e;
-    k_compact<<<blocks_for(n_pairs + 1), kThreads, 0, s>>>(wk, n_pairs, flags, seg_start, seg_key, hdr);
+    k_compact<KT><<<blocks_for(n_pairs + 1), kThreads, 0, s>>>(wk, n_pairs, flags, seg_start, seg_key, hdr);
     return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
+                        int64_t n_pairs, hipStream_t s, int stage) {
+    (void)stage;
+    return p.w_total_bits <= 32 ? group_impl<uint32_t>(p, L, ws, u_keys, v_keys, n_pairs, s)
+                                : group_impl<uint64_t>(p, L, ws, u_keys, v_keys, n_pairs, s);
 }
 
 }  // namespace tre

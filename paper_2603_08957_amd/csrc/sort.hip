@@ -1,5 +1,5 @@
-// Stable LSD radix sort of (uint64 key, payload) pairs over the low `bits`
-// bits of the key, in passes of at most 8-bit digits (a 20-bit key takes
+// Stable LSD radix sort of (uint64 or uint32 key, payload) pairs over the low
+// `bits` bits of the key, in passes of at most 8-bit digits (a 20-bit key takes
 // three passes of 7 bits).  Payload: uint32 (a permutation) or uint64 (a
 // packed pair, optionally split into two int32 arrays by the last pass).
 // Passes ping-pong between the two buffers; the result stays where the last
@@ -36,7 +36,8 @@ constexpr int kRadix = 1 << kMaxBits;
 constexpr int kDpt = kRadix / kThreads;  // digits per thread in the prefix step
 static_assert(kDpt >= 1 && kDpt * kThreads == kRadix, "radix must be a multiple of the workgroup size");
 
-__global__ __launch_bounds__(kThreads) void k_digit_hist(const uint64_t* __restrict__ keys, int64_t n, int shift,
+template <typename KT>
+__global__ __launch_bounds__(kThreads) void k_digit_hist(const KT* __restrict__ keys, int64_t n, int shift,
                                                          int dbits, int32_t* __restrict__ hist, int64_t n_tiles) {
     __shared__ int32_t cnt[kRadix];
     const int radix = 1 << dbits;
@@ -54,14 +55,15 @@ __global__ __launch_bounds__(kThreads) void k_digit_hist(const uint64_t* __restr
 }
 
 // SPLIT (uint64 payloads only): write the payload's high and low halves to
-// two int32 arrays instead of vout.
-template <typename VT, bool SPLIT>
-__global__ __launch_bounds__(kThreads) void k_digit_scatter(const uint64_t* __restrict__ kin, const VT* __restrict__ vin,
-                                                            uint64_t* __restrict__ kout, VT* __restrict__ vout,
+// two int32 arrays instead of vout.  KT: uint64 keys, or uint32 keys when
+// the sorted bits fit (less traffic per pass).
+template <typename KT, typename VT, bool SPLIT>
+__global__ __launch_bounds__(kThreads) void k_digit_scatter(const KT* __restrict__ kin, const VT* __restrict__ vin,
+                                                            KT* __restrict__ kout, VT* __restrict__ vout,
                                                             int32_t* __restrict__ hi_out, int32_t* __restrict__ lo_out,
                                                             int64_t n, int shift, int dbits,
                                                             const int32_t* __restrict__ offs, int64_t n_tiles) {
-    __shared__ uint64_t skey[kTile];
+    __shared__ KT skey[kTile];
     __shared__ VT sval[kTile];
     __shared__ int32_t wcnt[kWaves][kRadix];  // per-(wave, digit) counts, then wave prefixes
     __shared__ int32_t dstart[kRadix];        // tile-local start of each digit
@@ -78,21 +80,21 @@ __global__ __launch_bounds__(kThreads) void k_digit_scatter(const uint64_t* __re
     const uint64_t dmask = uint64_t(radix - 1);
     const int64_t tile0 = int64_t(blockIdx.x) * kTile;
     const int64_t item0 = tile0 + int64_t(w) * kPerWave + lane;
-    uint64_t key[kIpt];
+    KT key[kIpt];
     VT val[kIpt];
     int32_t rank[kIpt];
 #pragma unroll
     for (int r = 0; r < kIpt; r++) {
         const int64_t i = item0 + int64_t(r) * 64;
         const bool valid = i < n;
-        key[r] = valid ? kin[i] : 0ull;
+        key[r] = valid ? kin[i] : KT(0);
         val[r] = valid ? vin[i] : VT(0);
     }
     // ranks among equal digits inside this wave's quarter, in index order
 #pragma unroll
     for (int r = 0; r < kIpt; r++) {
         const bool valid = item0 + int64_t(r) * 64 < n;
-        const int d = int((key[r] >> shift) & dmask);
+        const int d = int((uint64_t(key[r]) >> shift) & dmask);
         uint64_t mask = __ballot(valid);
         for (int b = 0; b < dbits; b++) {
             const bool bit = (d >> b) & 1;
@@ -145,7 +147,7 @@ __global__ __launch_bounds__(kThreads) void k_digit_scatter(const uint64_t* __re
 #pragma unroll
     for (int r = 0; r < kIpt; r++) {
         if (item0 + int64_t(r) * 64 < n) {
-            const int d = int((key[r] >> shift) & dmask);
+            const int d = int((uint64_t(key[r]) >> shift) & dmask);
             const int pos = dstart[d] + wcnt[w][d] + rank[r];
             skey[pos] = key[r];
             sval[pos] = val[r];
@@ -156,8 +158,8 @@ __global__ __launch_bounds__(kThreads) void k_digit_scatter(const uint64_t* __re
     // consecutive output positions
     const int cnt = int(min<int64_t>(kTile, n - tile0));
     for (int q = tid; q < cnt; q += kThreads) {
-        const uint64_t k = skey[q];
-        const int d = int((k >> shift) & dmask);
+        const KT k = skey[q];
+        const int d = int((uint64_t(k) >> shift) & dmask);
         const int64_t dest = int64_t(gbase[d]) + (q - dstart[d]);
         kout[dest] = k;
         if constexpr (SPLIT) {
@@ -171,26 +173,26 @@ __global__ __launch_bounds__(kThreads) void k_digit_scatter(const uint64_t* __re
 
 int sort_passes(int bits) { return bits <= 0 ? 0 : (bits + kMaxBits - 1) / kMaxBits; }
 
-template <typename VT>
-hipError_t sort_impl(uint64_t* keys, VT* vals, uint64_t* keys_alt, VT* vals_alt, int64_t n, int bits, int32_t* hist,
+template <typename KT, typename VT>
+hipError_t sort_impl(KT* keys, VT* vals, KT* keys_alt, VT* vals_alt, int64_t n, int bits, int32_t* hist,
                      int32_t* scan_tmp, int32_t* split_hi, int32_t* split_lo, hipStream_t s) {
     if (n <= 1 || bits <= 0) return hipSuccess;
     const int64_t nt = (n + kTile - 1) / kTile;
     const int passes = sort_passes(bits);
     const int dbits = (bits + passes - 1) / passes;
-    uint64_t *ki = keys, *ko = keys_alt;
+    KT *ki = keys, *ko = keys_alt;
     VT *vi = vals, *vo = vals_alt;
     for (int p = 0; p < passes; p++) {
         const int shift = dbits * p;
-        k_digit_hist<<<dim3(unsigned(nt)), kThreads, 0, s>>>(ki, n, shift, dbits, hist, nt);
+        k_digit_hist<KT><<<dim3(unsigned(nt)), kThreads, 0, s>>>(ki, n, shift, dbits, hist, nt);
         hipError_t e = scan_exclusive_i32(hist, hist, (int64_t(1) << dbits) * nt, scan_tmp, s);
         if (e != hipSuccess) return e;
         if (split_hi && p == passes - 1)
-            k_digit_scatter<VT, true><<<dim3(unsigned(nt)), kThreads, 0, s>>>(ki, vi, ko, vo, split_hi, split_lo, n,
-                                                                             shift, dbits, hist, nt);
+            k_digit_scatter<KT, VT, true><<<dim3(unsigned(nt)), kThreads, 0, s>>>(ki, vi, ko, vo, split_hi,
+                                                                                 split_lo, n, shift, dbits, hist, nt);
         else
-            k_digit_scatter<VT, false><<<dim3(unsigned(nt)), kThreads, 0, s>>>(ki, vi, ko, vo, nullptr, nullptr, n,
-                                                                              shift, dbits, hist, nt);
+            k_digit_scatter<KT, VT, false><<<dim3(unsigned(nt)), kThreads, 0, s>>>(ki, vi, ko, vo, nullptr, nullptr,
+                                                                                  n, shift, dbits, hist, nt);
         std::swap(ki, ko);
         std::swap(vi, vo);
     }
@@ -205,13 +207,22 @@ bool radix_result_in_alt(int64_t n, int bits) { return n > 1 && (sort_passes(bit
 
 hipError_t radix_sort_u64(uint64_t* keys, uint32_t* vals, uint64_t* keys_alt, uint32_t* vals_alt, int64_t n,
                           int bits, int32_t* hist, int32_t* scan_tmp, hipStream_t s) {
-    return sort_impl<uint32_t>(keys, vals, keys_alt, vals_alt, n, bits, hist, scan_tmp, nullptr, nullptr, s);
+    return sort_impl<uint64_t, uint32_t>(keys, vals, keys_alt, vals_alt, n, bits, hist, scan_tmp, nullptr, nullptr, s);
 }
 
 hipError_t radix_sort_u64_pairs(uint64_t* keys, uint64_t* vals, uint64_t* keys_alt, uint64_t* vals_alt, int64_t n,
                                 int bits, int32_t* hist, int32_t* scan_tmp, int32_t* split_hi, int32_t* split_lo,
                                 hipStream_t s) {
-    return sort_impl<uint64_t>(keys, vals, keys_alt, vals_alt, n, bits, hist, scan_tmp, split_hi, split_lo, s);
+    return sort_impl<uint64_t, uint64_t>(keys, vals, keys_alt, vals_alt, n, bits, hist, scan_tmp, split_hi, split_lo,
+                                         s);
+}
+
+hipError_t radix_sort_u32_pairs(uint32_t* keys, uint64_t* vals, uint32_t* keys_alt, uint64_t* vals_alt, int64_t n,
+                                int bits, int32_t* hist, int32_t* scan_tmp, int32_t* split_hi, int32_t* split_lo,
+                                hipStream_t s) {
+    if (bits > 32) return hipErrorInvalidValue;
+    return sort_impl<uint32_t, uint64_t>(keys, vals, keys_alt, vals_alt, n, bits, hist, scan_tmp, split_hi, split_lo,
+                                         s);
 }
 
 }  // namespace tre

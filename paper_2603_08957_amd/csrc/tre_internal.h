@@ -136,6 +136,9 @@ hipError_t radix_sort_u64(uint64_t* keys, uint32_t* vals, uint64_t* keys_alt, ui
 hipError_t radix_sort_u64_pairs(uint64_t* keys, uint64_t* vals, uint64_t* keys_alt, uint64_t* vals_alt, int64_t n,
                                 int bits, int32_t* hist, int32_t* scan_tmp, int32_t* split_hi, int32_t* split_lo,
                                 hipStream_t s);
+hipError_t radix_sort_u32_pairs(uint32_t* keys, uint64_t* vals, uint32_t* keys_alt, uint64_t* vals_alt, int64_t n,
+                                int bits, int32_t* hist, int32_t* scan_tmp, int32_t* split_hi, int32_t* split_lo,
+                                hipStream_t s);
 
 // join.hip
 hipError_t launch_validate(const int32_t* keys, int64_t n, int r, const int32_t* radix, int32_t* err_flag,
