@@ -73,10 +73,10 @@ typedef struct tre_plan_s *tre_plan_t;
 typedef struct {
     int32_t validate_keys;      /* nonzero: check key order, uniqueness and range on the device (default 1) */
     int32_t max_pairs_per_unit; /* work-unit length cap; 0 = chosen from the pair count */
-    int32_t u_ranges;           /* bf16 128x128 path: cut every output key's pairs into this many ranges of
+    int32_t u_ranges;           /* 128x128 path: cut every output key's pairs into this many ranges of
                                    U tuple index and run range by range so concurrent workgroups share U
                                    tiles in L2 (partials summed after); 0 = automatic, < 0 = never */
-    int32_t pace_windows;       /* bf16 128x128 path with one 128x128 block per W tile: one persistent
+    int32_t pace_windows;       /* 128x128 path with one 128x128 block per W tile: one persistent
                                    workgroup per resident slot walks whole keys while the workgroups of each
                                    XCD keep within a few windows of U tuple index of each other (the U
                                    index range is cut into this many windows), so U tiles stay in L2 with
@@ -90,7 +90,9 @@ typedef struct {
     int32_t key_arity[3];     /* r_U, r_V, r_W */
     int64_t tile_elems[3];    /* elements per tile of U, V, W */
     int32_t n_join;           /* promoted labels shared by U and V */
-    int32_t kernel_class;     /* 0 = MFMA tile GEMM, 1 = vector (scale / GEMV / dot), 2 = bf16 MFMA GEMM, 128x128 blocks */
+    int32_t kernel_class;     /* 0 = MFMA tile GEMM, 1 = vector (scale / GEMV / dot), 2 = MFMA GEMM with
+                                 128x128 blocks and direct-to-LDS copies (bf16 with K a multiple of 64,
+                                 fp32 with K a multiple of 32) */
     int64_t batch, m, n, k;   /* per-pair contraction: W[b,m,n] += sum_k U[b,m,k] V[b,k,n] */
     int64_t flops_per_pair;   /* 2 * batch * m * n * k */
     char key_labels[3][27];   /* promoted labels of U, V, W in key order (NUL-terminated) */

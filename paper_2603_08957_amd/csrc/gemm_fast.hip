@@ -1,10 +1,12 @@
-// bf16 tile contraction for plain 2-D tiles: each workgroup owns a 128x128
-// block of one output tile and accumulates sum over the pairs of its work
-// unit of A_p (128 x K) * B_p (K x 128) on v_mfma_f32_32x32x16_bf16.
+// Tile contraction for plain 2-D tiles, bf16 or fp32: each workgroup owns a
+// 128x128 block of one output tile and accumulates sum over the pairs of its
+// work unit of A_p (128 x K) * B_p (K x 128) on v_mfma_f32_32x32x16_bf16
+// (bf16) or v_mfma_f32_32x32x2_f32 (fp32).
 //
 // 256 threads = 4 waves in a 2x2 grid, each wave a 64x64 sub-block (2x2 MFMA
 // tiles, 64 fp32 accumulators per lane).  K advances over the concatenation
-// of all pairs of the unit.
+// of all pairs of the unit.  The ring geometry below is in bytes and is the
+// same for both element types; a stage holds half as many k for fp32.
 //
 // Global memory is copied straight into LDS by global_load_lds_dwordx4 (16
 // bytes per lane, lane l to LDS base + 16 l), so no registers hold staged
@@ -18,12 +20,19 @@
 //     256-byte k-rows, 8 KB, four stages; granule g of k-row k sits in slot
 //     g ^ (4 (k & 3)).  Read with ds_read_b64_tr_b16, which hands each lane
 //     4 consecutive k of one row.
+//   fp32: KFAST stages are K = 32 ([row][32 k], 128-byte rows, same
+//     swizzle), RFAST stages K = 16 ([k][128 rows], 512-byte k-rows, granule
+//     g of k-row k in slot g ^ (8 ((k >> 3) & 1))).  The MFMA takes one k per
+//     lane and half-wave per step; the k of a tick are taken in the order
+//     k = 8 half + s (s = 0 .. 7) in both operands, so a KFAST lane reads its
+//     8 k with two ds_read_b128 and an RFAST lane with eight ds_read_b32 at
+//     one base address.
 // The swizzles are applied by choosing, per lane, which global granule goes
 // to the lane's fixed LDS slot; all reads are free of bank conflicts and
 // every global access covers whole contiguous row segments.  With one ring
 // of each kind a workgroup takes 80 KB of LDS (two per CU).
 //
-// The main loop advances in ticks of K = 32: an RFAST ring is refilled every
+// The main loop advances in ticks (K = 32 bf16, 16 fp32): an RFAST ring is refilled every
 // tick three ticks ahead, a KFAST ring every second tick four ticks ahead,
 // so only the stage being computed on is ever read while the others fill.
 // The copies are issued from inline assembly (the compiler's own wait
@@ -46,8 +55,8 @@ constexpr int kThreads = 256;
 constexpr int kB = 128;  // output block (rows and columns)
 
 struct FastArgs {
-    const uint16_t* A;
-    const uint16_t* B;
+    const void* A;
+    const void* B;
     const int32_t* pa;
     const int32_t* pb;
     int64_t a_elems, b_elems, w_elems;
@@ -69,15 +78,19 @@ typedef __attribute__((address_space(4))) int32_t const_i32;
 // s_waitcnt immediate: vmcnt(n) with expcnt and lgkmcnt left alone
 constexpr int vmcnt_only(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
-// ring geometry of one operand
-template <bool RF>
+// ring geometry of one operand of element type T
+template <typename T, bool RF>
 struct Ring {
-    static constexpr int kK = RF ? 32 : 64;            // K per stage
-    static constexpr int kStageBytes = 128 * kK * 2;   // 8 or 16 KB
+    static constexpr int kK = (RF ? 64 : 128) / int(sizeof(T));  // K per stage
+    static constexpr int kStageBytes = RF ? 8192 : 16384;
     static constexpr int kStages = RF ? 4 : 3;
     static constexpr int kBytes = kStages * kStageBytes;
     static constexpr int kPerWave = kStageBytes / 1024 / 4;  // copy instructions per wave per refill
 };
+
+// K of one tick of the main loop
+template <typename T>
+constexpr int kTickK = 64 / int(sizeof(T));
 
 __device__ inline uint64_t uniform64(uint64_t x) {
     const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(x));
@@ -98,14 +111,20 @@ __device__ inline void dma16(uint32_t lds_addr, const void* base, uint32_t voff)
 // Byte offset, from the stage's chunk origin, of the 16 bytes this lane
 // copies for copy instruction q of an operand with leading dimension ld
 // (elements); the copy lands at stage offset q * 1024 + 16 * lane.
-template <bool RF>
+template <typename T, bool RF>
 __device__ inline uint32_t dma_src(int lane, int q, int64_t ld) {
+    constexpr int E = int(sizeof(T));
     if (!RF) {  // 8 rows x 128 B; row & 7 == lane >> 3, (row >> 3) & 7 == q & 7
         const int row = 8 * q + (lane >> 3);
-        return uint32_t(row * ld * 2 + (((lane & 7) ^ (lane >> 3) ^ (q & 7)) << 4));
+        return uint32_t(row * ld * E + (((lane & 7) ^ (lane >> 3) ^ (q & 7)) << 4));
     }
-    const int krow = 4 * q + (lane >> 4);  // 4 k-rows x 256 B; krow & 3 == lane >> 4
-    return uint32_t(krow * ld * 2 + (((lane & 15) ^ ((lane >> 4) << 2)) << 4));
+    if constexpr (E == 2) {
+        const int krow = 4 * q + (lane >> 4);  // 4 k-rows x 256 B; krow & 3 == lane >> 4
+        return uint32_t(krow * ld * E + (((lane & 15) ^ ((lane >> 4) << 2)) << 4));
+    } else {
+        const int krow = 2 * q + (lane >> 5);  // 2 k-rows x 512 B
+        return uint32_t(krow * ld * E + (((lane & 31) ^ (((krow >> 3) & 1) << 3)) << 4));
+    }
 }
 
 // Element offset inside a tile of the chunk origin (rows r0.., k0..).
@@ -144,37 +163,80 @@ __device__ inline bf16x8 frag_read(const char* stage, uint32_t off) {
     return __builtin_bit_cast(bf16x8, both);
 }
 
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) f32x4 lds_f32x4;
+typedef __attribute__((address_space(3))) float lds_f32;
+
+// fp32: stage offsets of the lane's reads for the 32-row tile at rb.
+//   KFAST: off[2 p + j] = granule j of the lane's 8 k in tick half p.
+//   RFAST: off[0] = the first of the lane's 8 k-rows (the others follow at
+//          512-byte steps).
+template <bool RF>
+__device__ inline void frag_offsets_f32(int lane, int rb, uint32_t (&off)[4]) {
+    const int h = lane >> 5;
+    if (!RF) {
+        const int r = rb + (lane & 31);
+        const int x = (r ^ (r >> 3)) & 7;
+#pragma unroll
+        for (int p = 0; p < 2; p++)
+#pragma unroll
+            for (int j = 0; j < 2; j++) off[2 * p + j] = uint32_t(r * 128 + (((4 * p + 2 * h + j) ^ x) << 4));
+    } else {
+        const int c = rb + (lane & 31);
+        off[0] = uint32_t(8 * h * 512 + ((((c >> 2) ^ (h << 3))) << 4) + 4 * (c & 3));
+        off[1] = off[2] = off[3] = 0;
+    }
+}
+
+// The lane's 8 fp32 operand values of tick half p (k = 8 half + s).
+template <bool RF>
+__device__ inline void frag8_f32(const char* stage, const uint32_t (&off)[4], int p, float (&v)[8]) {
+    if (!RF) {
+        const f32x4 a = *(const lds_f32x4*)((lds_char*)stage + off[2 * p]);
+        const f32x4 b = *(const lds_f32x4*)((lds_char*)stage + off[2 * p + 1]);
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            v[i] = a[i];
+            v[4 + i] = b[i];
+        }
+    } else {
+        (void)p;
+#pragma unroll
+        for (int i = 0; i < 8; i++) v[i] = *(const lds_f32*)((lds_char*)stage + off[0] + i * 512);
+    }
+}
+
 // Copy cursor of one operand: walks the unit's pairs stage by stage; past
 // the end it copies the last stage again (never read).
-template <bool RF, bool NT>
+template <typename T, bool RF, bool NT>
 struct Cursor {
-    const uint16_t* base;  // operand tiles, offset to the block's chunk origin
+    using R = Ring<T, RF>;
+    const T* base;         // operand tiles, offset to the block's chunk origin
     const const_i32* idx;  // tile index of each pair of the unit
     int64_t elems, step;   // tile elements; element step from one stage to the next
     int np, per_pair;      // pairs; stages per pair
     int ip = 0, ik = 0, stage = 0;
     int32_t next = 0;
-    const uint16_t* cur = nullptr;
-    uint32_t src[Ring<RF>::kPerWave];
+    const T* cur = nullptr;
+    uint32_t src[R::kPerWave];
 
-    __device__ void init(const uint16_t* b, const const_i32* ix, int64_t e, int64_t ld, int K, int npairs, int lane,
-                         int w) {
+    __device__ void init(const T* b, const const_i32* ix, int64_t e, int64_t ld, int K, int npairs, int lane, int w) {
         base = b;
         idx = ix;
         elems = e;
-        step = RF ? int64_t(Ring<RF>::kK) * ld : Ring<RF>::kK;
+        step = RF ? int64_t(R::kK) * ld : R::kK;
         np = npairs;
-        per_pair = K / Ring<RF>::kK;
+        per_pair = K / R::kK;
         cur = base + int64_t(idx[0]) * elems;
         next = idx[min(1, np - 1)];
 #pragma unroll
-        for (int j = 0; j < Ring<RF>::kPerWave; j++) src[j] = dma_src<RF>(lane, Ring<RF>::kPerWave * w + j, ld);
+        for (int j = 0; j < R::kPerWave; j++) src[j] = dma_src<T, RF>(lane, R::kPerWave * w + j, ld);
     }
     __device__ void issue(uint32_t ring_lds, int w) {
-        const uint32_t l0 = ring_lds + stage * Ring<RF>::kStageBytes + Ring<RF>::kPerWave * w * 1024;
+        const uint32_t l0 = ring_lds + stage * R::kStageBytes + R::kPerWave * w * 1024;
 #pragma unroll
-        for (int j = 0; j < Ring<RF>::kPerWave; j++) dma16<NT>(l0 + j * 1024, cur, src[j]);
-        stage = stage == Ring<RF>::kStages - 1 ? 0 : stage + 1;
+        for (int j = 0; j < R::kPerWave; j++) dma16<NT>(l0 + j * 1024, cur, src[j]);
+        stage = stage == R::kStages - 1 ? 0 : stage + 1;
         if (++ik < per_pair) {
             cur += step;
             return;
@@ -190,10 +252,10 @@ struct Cursor {
     }
 };
 
-template <bool AROW, bool BROW>
+template <typename T, bool AROW, bool BROW>
 struct DmaShape {
-    using RA = Ring<AROW>;
-    using RB = Ring<BROW>;
+    using RA = Ring<T, AROW>;
+    using RB = Ring<T, BROW>;
     static constexpr int kLds = RA::kBytes + RB::kBytes;
     static constexpr int kOcc = 163840 / kLds;
     // Copies still allowed in flight when a tick's data must have landed (see
@@ -248,11 +310,12 @@ struct Pace {
 
 // One work unit: sum over its pairs of A_p B_p into the 128x128 block
 // (m0, n0) of its output tile, written to W (whole key) or a partial slot.
-template <bool AROW, bool BROW, bool ANT, bool BNT, class Pacer>
+template <typename T, bool AROW, bool BROW, bool ANT, bool BNT, class Pacer>
 __device__ inline void run_unit(const FastArgs& g, const Unit& un, int m0, int n0, char* lds, Pacer& pc) {
-    using SH = DmaShape<AROW, BROW>;
-    using RA = Ring<AROW>;
-    using RB = Ring<BROW>;
+    using SH = DmaShape<T, AROW, BROW>;
+    using RA = Ring<T, AROW>;
+    using RB = Ring<T, BROW>;
+    constexpr bool F32 = sizeof(T) == 4;
     const uint32_t lds_a = uint32_t(reinterpret_cast<uintptr_t>((lds_char*)(lds)));
     const uint32_t lds_b = lds_a + RA::kBytes;
 
@@ -267,7 +330,7 @@ __device__ inline void run_unit(const FastArgs& g, const Unit& un, int m0, int n
             for (int r = 0; r < 16; r++) acc[i][j][r] = 0.f;
 
     const int np = un.p1 - un.p0;
-    const int tpp = g.K / 32;  // ticks per pair
+    const int tpp = g.K / kTickK<T>;  // ticks per pair
     const int ticks = np * tpp;
     float* out = un.slot < 0 ? g.W + int64_t(un.seg) * g.w_elems : g.partials + int64_t(un.slot) * g.w_elems;
     if (ticks == 0) {
@@ -278,18 +341,23 @@ __device__ inline void run_unit(const FastArgs& g, const Unit& un, int m0, int n
     }
     // the pair list is read-only here; reading it through the constant
     // address space keeps the (uniform) index loads on the scalar unit
-    Cursor<AROW, ANT> ca;
-    Cursor<BROW, BNT> cb;
-    ca.init(g.A + dma_origin<AROW>(g.lda, m0, 0), (const const_i32*)(g.pa + un.p0), g.a_elems, g.lda, g.K, np,
-            lane, w);
-    cb.init(g.B + dma_origin<BROW>(g.ldb, n0, 0), (const const_i32*)(g.pb + un.p0), g.b_elems, g.ldb, g.K, np,
-            lane, w);
+    Cursor<T, AROW, ANT> ca;
+    Cursor<T, BROW, BNT> cb;
+    ca.init(reinterpret_cast<const T*>(g.A) + dma_origin<AROW>(g.lda, m0, 0), (const const_i32*)(g.pa + un.p0),
+            g.a_elems, g.lda, g.K, np, lane, w);
+    cb.init(reinterpret_cast<const T*>(g.B) + dma_origin<BROW>(g.ldb, n0, 0), (const const_i32*)(g.pb + un.p0),
+            g.b_elems, g.ldb, g.K, np, lane, w);
 
     uint32_t oa[2][4], ob[2][4];
 #pragma unroll
     for (int t = 0; t < 2; t++) {
-        frag_offsets<AROW>(lane, wm * 64 + t * 32, oa[t]);
-        frag_offsets<BROW>(lane, wn * 64 + t * 32, ob[t]);
+        if constexpr (F32) {
+            frag_offsets_f32<AROW>(lane, wm * 64 + t * 32, oa[t]);
+            frag_offsets_f32<BROW>(lane, wn * 64 + t * 32, ob[t]);
+        } else {
+            frag_offsets<AROW>(lane, wm * 64 + t * 32, oa[t]);
+            frag_offsets<BROW>(lane, wn * 64 + t * 32, ob[t]);
+        }
     }
 
     // refills of tick tau: KFAST rings on even ticks (stage tau / 2 + 2),
@@ -317,20 +385,36 @@ __device__ inline void run_unit(const FastArgs& g, const Unit& un, int m0, int n
         refill(p, true);
         const char* As = lds + sa * RA::kStageBytes;
         const char* Bs = lds + RA::kBytes + sb * RB::kStageBytes;
-        bf16x8 a[2][2], b[2][2];
-#pragma unroll
-        for (int s = 0; s < 2; s++)
+        if constexpr (F32) {
+            float a[2][8], b[2][8];
 #pragma unroll
             for (int t = 0; t < 2; t++) {
-                a[s][t] = frag_read<AROW>(As, oa[t][AROW ? s : 2 * p + s]);
-                b[s][t] = frag_read<BROW>(Bs, ob[t][BROW ? s : 2 * p + s]);
+                frag8_f32<AROW>(As, oa[t], p, a[t]);
+                frag8_f32<BROW>(Bs, ob[t], p, b[t]);
             }
 #pragma unroll
-        for (int s = 0; s < 2; s++) {
-            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s][0], b[s][0], acc[0][0], 0, 0, 0);
-            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s][0], b[s][1], acc[0][1], 0, 0, 0);
-            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s][1], b[s][0], acc[1][0], 0, 0, 0);
-            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s][1], b[s][1], acc[1][1], 0, 0, 0);
+            for (int s = 0; s < 8; s++) {
+                acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0][s], b[0][s], acc[0][0], 0, 0, 0);
+                acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0][s], b[1][s], acc[0][1], 0, 0, 0);
+                acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[1][s], b[0][s], acc[1][0], 0, 0, 0);
+                acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[1][s], b[1][s], acc[1][1], 0, 0, 0);
+            }
+        } else {
+            bf16x8 a[2][2], b[2][2];
+#pragma unroll
+            for (int s = 0; s < 2; s++)
+#pragma unroll
+                for (int t = 0; t < 2; t++) {
+                    a[s][t] = frag_read<AROW>(As, oa[t][AROW ? s : 2 * p + s]);
+                    b[s][t] = frag_read<BROW>(Bs, ob[t][BROW ? s : 2 * p + s]);
+                }
+#pragma unroll
+            for (int s = 0; s < 2; s++) {
+                acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s][0], b[s][0], acc[0][0], 0, 0, 0);
+                acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s][0], b[s][1], acc[0][1], 0, 0, 0);
+                acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s][1], b[s][0], acc[1][0], 0, 0, 0);
+                acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s][1], b[s][1], acc[1][1], 0, 0, 0);
+            }
         }
         // advance the read stages: RFAST every tick, KFAST after odd ticks
         if (AROW || p == 1) sa = sa == RA::kStages - 1 ? 0 : sa + 1;
@@ -360,8 +444,8 @@ __device__ inline void run_unit(const FastArgs& g, const Unit& un, int m0, int n
         }
 }
 
-template <bool AROW, bool BROW, bool ANT, bool BNT>
-__global__ __launch_bounds__(kThreads, (DmaShape<AROW, BROW>::kOcc)) void k_gemm_dma(FastArgs g) {
+template <typename T, bool AROW, bool BROW, bool ANT, bool BNT>
+__global__ __launch_bounds__(kThreads, (DmaShape<T, AROW, BROW>::kOcc)) void k_gemm_dma(FastArgs g) {
     // Workgroup -> (unit, row block, column block).  Workgroups are dealt to
     // the 8 XCDs round-robin; the column blocks of one (unit, row block) take
     // consecutive slots of one XCD, so they share the A tile in its L2.
@@ -370,9 +454,9 @@ __global__ __launch_bounds__(kThreads, (DmaShape<AROW, BROW>::kOcc)) void k_gemm
     const int nblk = int(slot % g.nblocks), mblk = int(grp % g.mblocks);
     const int64_t unit_id = grp / g.mblocks;
     if (unit_id >= g.hdr->n_units) return;
-    __shared__ __attribute__((aligned(1024))) char lds[DmaShape<AROW, BROW>::kLds];
+    __shared__ __attribute__((aligned(1024))) char lds[DmaShape<T, AROW, BROW>::kLds];
     NoPace pc;
-    run_unit<AROW, BROW, ANT, BNT>(g, g.units[unit_id], mblk * kB, nblk * kB, lds, pc);
+    run_unit<T, AROW, BROW, ANT, BNT>(g, g.units[unit_id], mblk * kB, nblk * kB, lds, pc);
 }
 
 // Persistent, paced variant for one 128x128 block per key (M = N = 128):
@@ -382,11 +466,11 @@ __global__ __launch_bounds__(kThreads, (DmaShape<AROW, BROW>::kOcc)) void k_gemm
 // reused operand, so its tiles stay in that XCD's L2 without cutting keys
 // into ranges (no partial tiles).  pace: rounds x 8 x windows counters,
 // zeroed by the host before the launch.
-template <bool AROW, bool BROW, bool ANT, bool BNT>
-__global__ __launch_bounds__(kThreads, (DmaShape<AROW, BROW>::kOcc)) void k_gemm_paced(FastArgs g, int32_t* pace,
+template <typename T, bool AROW, bool BROW, bool ANT, bool BNT>
+__global__ __launch_bounds__(kThreads, (DmaShape<T, AROW, BROW>::kOcc)) void k_gemm_paced(FastArgs g, int32_t* pace,
                                                                                       int32_t n_wg, int32_t windows,
                                                                                       int32_t ahead, int32_t slack_div) {
-    __shared__ __attribute__((aligned(1024))) char lds[DmaShape<AROW, BROW>::kLds];
+    __shared__ __attribute__((aligned(1024))) char lds[DmaShape<T, AROW, BROW>::kLds];
     const int64_t n_units = g.hdr->n_units;
     const int xcd = int(blockIdx.x % 8);
     for (int64_t round = 0;; round++) {
@@ -405,7 +489,7 @@ __global__ __launch_bounds__(kThreads, (DmaShape<AROW, BROW>::kOcc)) void k_gemm
         pc.thr = int(max<int64_t>(active - active / slack_div, 1));
         pc.cur = -1;
         __syncthreads();  // the previous unit's LDS reads are done
-        run_unit<AROW, BROW, ANT, BNT>(g, un, 0, 0, lds, pc);
+        run_unit<T, AROW, BROW, ANT, BNT>(g, un, 0, 0, lds, pc);
     }
 }
 
@@ -418,8 +502,8 @@ FastArgs fast_args(const Plan& p, const Layout& L, char* ws, const void* u_tiles
     FastArgs g{};
     const int32_t* pu = reinterpret_cast<const int32_t*>(ws + L.pu);
     const int32_t* pv = reinterpret_cast<const int32_t*>(ws + L.pv);
-    g.A = reinterpret_cast<const uint16_t*>(p.swap ? v_tiles : u_tiles);
-    g.B = reinterpret_cast<const uint16_t*>(p.swap ? u_tiles : v_tiles);
+    g.A = p.swap ? v_tiles : u_tiles;
+    g.B = p.swap ? u_tiles : v_tiles;
     g.pa = p.swap ? pv : pu;
     g.pb = p.swap ? pu : pv;
     g.a_elems = p.tile_elems[p.swap ? 1 : 0];
@@ -458,9 +542,12 @@ hipError_t launch_gemm_fast(const Plan& p, const Layout& L, char* ws, const void
     const int64_t blocks = (groups + 7) / 8 * 8 * g.nblocks;
     if (blocks > int64_t(0x7fffffff)) return hipErrorInvalidConfiguration;
     dim3 grid{unsigned(blocks), 1u, 1u};
-#define TRE_FAST_CASE(X)                                                                                   \
-    case X:                                                                                                \
-        k_gemm_dma<bool(X & 8), bool(X & 4), bool(X & 2), bool(X & 1)><<<grid, kThreads, 0, s>>>(g); \
+#define TRE_FAST_CASE(X)                                                                                      \
+    case X:                                                                                                   \
+        if (p.dtype == TRE_BF16)                                                                              \
+            k_gemm_dma<uint16_t, bool(X & 8), bool(X & 4), bool(X & 2), bool(X & 1)><<<grid, kThreads, 0, s>>>(g); \
+        else                                                                                                  \
+            k_gemm_dma<float, bool(X & 8), bool(X & 4), bool(X & 2), bool(X & 1)><<<grid, kThreads, 0, s>>>(g);    \
         break;
     switch (fast_variant(p, L, n_pairs)) {
         TRE_FAST_CASE(0) TRE_FAST_CASE(1) TRE_FAST_CASE(2) TRE_FAST_CASE(3)
@@ -492,8 +579,12 @@ hipError_t launch_gemm_paced(const Plan& p, const Layout& L, char* ws, const voi
     dim3 grid{unsigned(n_wg), 1u, 1u};
 #define TRE_PACED_CASE(X)                                                                                      \
     case X:                                                                                                    \
-        k_gemm_paced<bool(X & 8), bool(X & 4), bool(X & 2), bool(X & 1)><<<grid, kThreads, 0, s>>>(           \
-            g, pace, int32_t(n_wg), windows, kAhead, kSlackDiv);                                               \
+        if (p.dtype == TRE_BF16)                                                                               \
+            k_gemm_paced<uint16_t, bool(X & 8), bool(X & 4), bool(X & 2), bool(X & 1)><<<grid, kThreads, 0, s>>>( \
+                g, pace, int32_t(n_wg), windows, kAhead, kSlackDiv);                                           \
+        else                                                                                                   \
+            k_gemm_paced<float, bool(X & 8), bool(X & 4), bool(X & 2), bool(X & 1)><<<grid, kThreads, 0, s>>>(    \
+                g, pace, int32_t(n_wg), windows, kAhead, kSlackDiv);                                           \
         break;
     switch (fast_variant(p, L, n_pairs)) {
         TRE_PACED_CASE(0) TRE_PACED_CASE(1) TRE_PACED_CASE(2) TRE_PACED_CASE(3)

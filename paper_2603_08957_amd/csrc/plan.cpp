@@ -337,9 +337,10 @@ static tre_status classify(Plan& p) {
                   (p.a_kfast ? (runs_of_8(tAK) && all_mult_8(tAM)) : (runs_of_8(tAM) && all_mult_8(tAK)));
         p.vec_b = te_b && all_mult_8(tBB) &&
                   (p.b_kfast ? (runs_of_8(tBK) && all_mult_8(tBN)) : (runs_of_8(tBN) && all_mult_8(tBK)));
-        // Fast path: bf16, no batch, 128-multiple M/N, 64-multiple K, every
-        // operand a plain 2-D row-major matrix (one unit stride, one leading
-        // dimension) and W stored with N fastest.
+        // Fast path: bf16 (K a multiple of 64) or fp32 (K a multiple of 32),
+        // no batch, 128-multiple M/N, every operand a plain 2-D row-major
+        // matrix (one unit stride, one leading dimension) and W stored with N
+        // fastest.
         auto affine = [](const std::vector<int32_t>& t, int64_t& s) {
             s = t.size() > 1 ? t[1] - t[0] : 0;
             for (size_t i = 0; i < t.size(); i++)
@@ -349,7 +350,8 @@ static tre_status classify(Plan& p) {
         auto tWM = host_table(p.dims[T_WM]), tWN = host_table(p.dims[T_WN]);
         const int64_t M = p.swap ? p.nN : p.nM, N = p.swap ? p.nM : p.nN;
         int64_t sAM, sAK, sBN, sBK, sWM, sWN;
-        bool ok = p.dtype == TRE_BF16 && p.nB == 1 && M % 128 == 0 && N % 128 == 0 && p.nK % 64 == 0 &&
+        const int64_t kq = p.dtype == TRE_BF16 ? 64 : 32;
+        bool ok = p.nB == 1 && M % 128 == 0 && N % 128 == 0 && p.nK % kq == 0 &&
                   affine(tAM, sAM) && affine(tAK, sAK) && affine(tBN, sBN) && affine(tBK, sBK) &&
                   affine(tWM, sWM) && affine(tWN, sWN) && sWN == 1 && sWM >= N;
         if (ok) {

@@ -106,7 +106,8 @@ def test_wider_plans_gpu(orc, idx, dtype):
 
 FAST_PLANS = [
     # (einsum, upper, extents, tiles): each hits one operand-layout variant of
-    # the bf16 128x128 kernel (A row- or k-contiguous, B row- or k-contiguous)
+    # the 128x128 kernel (A row- or k-contiguous, B row- or k-contiguous), in
+    # bf16 and in fp32
     ("ij,jk->ki", "jk", {"i": 128, "j": 1024, "k": 1024}, {"j": 128, "k": 128}),
     ("ki,im->km", "k", {"k": 2048, "i": 128, "m": 256}, {"k": 128}),
     ("ik,jk->ij", "ij", {"i": 512, "j": 384, "k": 192}, {"i": 128, "j": 128}),
@@ -116,41 +117,44 @@ FAST_PLANS = [
 
 @pytest.mark.parametrize("idx", range(len(FAST_PLANS)))
 @pytest.mark.parametrize("pmax,ur", [(0, -1), (3, -1), (0, 3), (0, 64)])
-def test_fast_path_gpu(orc, idx, pmax, ur):
-    """bf16 128x128 path, including U-range units (ur > 0: every key's pairs cut
-    into ur ranges of U index, empty ranges included, partials summed after)."""
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_fast_path_gpu(orc, idx, pmax, ur, dtype):
+    """128x128 MFMA path (bf16 and fp32), including U-range units (ur > 0:
+    every key's pairs cut into ur ranges of U index, empty ranges included,
+    partials summed after)."""
     import paper_2603_08957_amd as tre
 
     e, upper, ext, til = FAST_PLANS[idx]
-    assert tre.Plan(e, upper, ext, til, "bf16").kernel_class == "gemm128"
+    assert tre.Plan(e, upper, ext, til, dtype).kernel_class == "gemm128"
     rng = np.random.default_rng(77 + idx)
     u_lab, v_lab, _ = split_einsum(e)
-    U = workloads.random_relation(rng, u_lab, upper, ext, til, "bf16", keep=0.6, zero_frac=0.05)
-    V = workloads.random_relation(rng, v_lab, upper, ext, til, "bf16", keep=0.6, zero_frac=0.05)
-    spec = workloads.spec(e, upper, ext, til, "bf16")
-    say("fast path", idx, pmax, ur, e, len(U["keys"]), len(V["keys"]))
+    U = workloads.random_relation(rng, u_lab, upper, ext, til, dtype, keep=0.6, zero_frac=0.05)
+    V = workloads.random_relation(rng, v_lab, upper, ext, til, dtype, keep=0.6, zero_frac=0.05)
+    spec = workloads.spec(e, upper, ext, til, dtype)
+    say("fast path", idx, dtype, pmax, ur, e, len(U["keys"]), len(V["keys"]))
     _, out = gpu_run(spec, U, V, max_pairs_per_unit=pmax, u_ranges=ur)
-    check(out, orc.run(orc_plan(orc, spec), U, V), "bf16")
+    check(out, orc.run(orc_plan(orc, spec), U, V), dtype)
 
 
 @pytest.mark.parametrize("idx", [0, 2])
 @pytest.mark.parametrize("windows", [1, 3, 64])
-def test_paced_path_gpu(orc, idx, windows):
-    """Persistent paced bf16 kernel (one 128x128 block per W tile): whole keys
-    per workgroup, rounds of units, pacing over windows of U index; the result
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_paced_path_gpu(orc, idx, windows, dtype):
+    """Persistent paced kernel (one 128x128 block per W tile): whole keys per
+    workgroup, rounds of units, pacing over windows of U index; the result
     must not depend on the window count."""
     import paper_2603_08957_amd as tre
 
     e, upper, ext, til = FAST_PLANS[idx]
     rng = np.random.default_rng(177 + idx)
     u_lab, v_lab, _ = split_einsum(e)
-    U = workloads.random_relation(rng, u_lab, upper, ext, til, "bf16", keep=0.6, zero_frac=0.05)
-    V = workloads.random_relation(rng, v_lab, upper, ext, til, "bf16", keep=0.6, zero_frac=0.05)
-    spec = workloads.spec(e, upper, ext, til, "bf16")
-    assert tre.Plan(e, upper, ext, til, "bf16").kernel_class == "gemm128"
-    say("paced path", idx, windows, e, len(U["keys"]), len(V["keys"]))
+    U = workloads.random_relation(rng, u_lab, upper, ext, til, dtype, keep=0.6, zero_frac=0.05)
+    V = workloads.random_relation(rng, v_lab, upper, ext, til, dtype, keep=0.6, zero_frac=0.05)
+    spec = workloads.spec(e, upper, ext, til, dtype)
+    assert tre.Plan(e, upper, ext, til, dtype).kernel_class == "gemm128"
+    say("paced path", idx, dtype, windows, e, len(U["keys"]), len(V["keys"]))
     _, out = gpu_run(spec, U, V, pace_windows=windows)
-    check(out, orc.run(orc_plan(orc, spec), U, V), "bf16")
+    check(out, orc.run(orc_plan(orc, spec), U, V), dtype)
 
 
 def test_paced_rounds_gpu(orc):
