@@ -34,7 +34,7 @@ int64_t blocks_per_unit(const Plan& p) {
     return (p.tile_elems[2] + 255) / 256;
 }
 
-// Number of U-index ranges for the bf16 128x128 path (0 or 1 = off).  Worth
+// Number of U-index ranges for the 128x128 path (0 or 1 = off).  Worth
 // it when the U tiles are reused by many keys (pairs per U tuple high) but do
 // not fit in one XCD's 4 MB L2: cutting every key's pairs into ranges of U and
 // dispatching range by range lets the workgroups resident on an XCD share

@@ -70,7 +70,7 @@ struct Plan {
     bool b_kfast = false;
     bool vec_a = false;    // GEMM: 8-wide vector loads legal along A's fast dim
     bool vec_b = false;
-    // bf16 fast path: A(m,k) = A[k*lda + m] if a_rowfast else A[m*lda + k];
+    // 128x128 fast path (bf16, fp32): A(m,k) = A[k*lda + m] if a_rowfast else A[m*lda + k];
     // B(n,k) = B[k*ldb + n] if b_rowfast else B[n*ldb + k]; W(m,n) = W[m*ldw + n]
     // vector class: W elements per thread (1, 4 for fp32, 8 for bf16) and
     // whether V's element is the same for a whole group of them
