@@ -578,29 +578,63 @@ def dense_stats(pl, A, labels):
                      for i, l in enumerate(labels)}, A.itemsize)
 
 
-def planner_check(tre, torch, top, steps):
-    """Rank every decomposition of the fp32 GNN chain (4096 vertices) with
-    the planner, calibrated to this GPU (c_xfer = 1 / 8 TB/s, c_flop = 1 /
-    157.3 TFLOP/s, c_fixed measured on a scalar cross product, c_call on a
-    one-pair EinSum), then run the
-    cheapest ``top`` plans and a spread of the rest through the library,
-    each decomposed as planned (inputs laid out on the host, the result of
-    E1 repartitioned on the device when E2 wants another decomposition), and
-    time them; every plan's result is checked against dense fp64."""
+def relation_from_coo(coords, vals, labels, promoted, extents, max_bytes, dtype):
+    """Tensor relation of a sparse tensor given by its entries: one tuple per
+    distinct combination of promoted coordinates, tiles dense over the
+    demoted labels; None when the tiles would exceed max_bytes."""
+    pa = [i for i, l in enumerate(labels) if l in promoted]
+    da = [i for i, l in enumerate(labels) if l not in promoted]
+    te = int(np.prod([extents[labels[i]] for i in da])) if da else 1
+    if pa:
+        keys, slot = np.unique(coords[:, pa], axis=0, return_inverse=True)
+    else:
+        keys, slot = np.zeros((1 if len(coords) else 0, 0), np.int64), np.zeros(len(coords), np.int64)
+    if len(keys) * te * (2 if dtype == "bf16" else 4) > max_bytes:
+        return None
+    off = np.zeros(len(coords), np.int64)
+    for i in da:
+        off = off * extents[labels[i]] + coords[:, i]
+    tiles = np.zeros((len(keys), te), vals.dtype)
+    tiles[slot.reshape(-1), off] = vals
+    return {"keys": np.ascontiguousarray(keys.astype(np.int32)), "tiles": tiles, "dtype": dtype}
+
+
+def coo_stats(pl, coords, labels, extents, elem_bytes):
+    return pl.Stats(labels, dict(extents), float(len(coords)),
+                    {l: float(len(np.unique(coords[:, i]))) for i, l in enumerate(labels)}, elem_bytes)
+
+
+def planner_check(tre, torch, config, top, steps):
+    """Rank every decomposition of a GNN chain (X.Y)^T.Z (workload 1: fp32,
+    4096 vertices; workload 2: bf16, 262,144 vertices) with the planner,
+    calibrated to this GPU (c_xfer = 1 / 8 TB/s, c_flop = 1 / peak of the
+    input type, c_fixed measured on a scalar cross product, c_call on a
+    one-pair EinSum), then run the cheapest ``top`` plans and a spread of the
+    rest through the library, each decomposed as planned (inputs laid out on
+    the host, skipped when that would take more than 8 GB; the result of E1
+    cast to bf16 for a bf16 chain and repartitioned on the device when E2
+    wants another decomposition), and time them; every plan's result is
+    checked against fp64."""
+    import scipy.sparse as sp
+
     import workloads
     from paper_2603_08957_amd import planner as pl
 
-    w = workloads.config(1)
-    n, emb, zo = w["n"], w["emb"], w["z_out"]
-    X = np.ascontiguousarray(w["X"]["tiles"].reshape(n // 64, emb, 64).transpose(1, 0, 2).reshape(emb, n))
-    Y = np.zeros((n, n), np.float32)
-    Y[w["Y"]["coo"][0][:, 0], w["Y"]["coo"][0][:, 1]] = w["Y"]["coo"][1]
-    Z = w["Z"]["tiles"].reshape(emb, zo)
-    ref = (X.astype(np.float64) @ Y).T @ Z.astype(np.float64)
-    mag = (np.abs(X.astype(np.float64)) @ np.abs(Y)).T @ np.abs(Z.astype(np.float64))
+    w = workloads.config(config)
+    n, emb, zo, dt = w["n"], w["emb"], w["z_out"], w["dtype"]
+    t1 = w["tile_e1"]
+    eb = 2 if dt == "bf16" else 4
+    X = np.ascontiguousarray(w["X"]["tiles"].reshape(n // t1, emb, t1).transpose(1, 0, 2).reshape(emb, n))
+    Z = np.ascontiguousarray(w["Z"]["tiles"].reshape(emb, zo))
+    yc = w["Y"]["coo"][0]
+    yv = w["Y"]["values"] if "values" in w["Y"] else w["Y"]["coo"][1].astype(np.float32)
+    f64 = (lambda a: workloads.bf16_bits_to_f32(a).astype(np.float64)) if dt == "bf16" else \
+        (lambda a: a.astype(np.float64))
+    Yd = sp.csr_matrix((f64(yv), (yc[:, 0], yc[:, 1])), shape=(n, n))
+    ref = (Yd.T @ f64(X).T) @ f64(Z)
+    mag = (abs(Yd).T @ np.abs(f64(X)).T) @ np.abs(f64(Z))
     # c_fixed: a cross product of two 4096-tuple scalar relations into one group
     m = 4096
-    cp = tre.Plan("i,j->", "ij", {"i": m, "j": m}, {"i": 1, "j": 1}, "f32", validate=False)
     ck = torch.arange(m, dtype=torch.int32, device="cuda").reshape(m, 1)
     ct = torch.ones((m, 1), dtype=torch.float32, device="cuda")
     cst = Stage(tre, torch, {"einsum": "i,j->", "upper": "ij", "extents": {"i": m, "j": m},
@@ -614,7 +648,6 @@ def planner_check(tre, torch, top, steps):
     e1.record()
     torch.cuda.synchronize()
     c_fixed = e0.elapsed_time(e1) * 1e-3 / steps / (m * m)
-    del cp
     # c_call: one library call on one pair of one-element tuples
     one = torch.zeros((1, 1), dtype=torch.int32, device="cuda")
     lst = Stage(tre, torch, {"einsum": "i,i->i", "upper": "i", "extents": {"i": 1}, "tiles": {"i": 1},
@@ -627,42 +660,55 @@ def planner_check(tre, torch, top, steps):
         lst.run(one, ct[:1], one, ct[:1])
     torch.cuda.synchronize()
     c_call = (time.perf_counter() - t0) / steps
-    cap = 64 << 20
-    prog = pl.Program({"X": dense_stats(pl, X, "ij"), "Y": dense_stats(pl, Y, "jk"), "Z": dense_stats(pl, Z, "im")},
+    cap = (64 << 20) if config == 1 else (256 << 20)
+    ext1 = {"i": emb, "j": n, "k": n}
+    ext2 = {"k": n, "i": emb, "m": zo}
+    prog = pl.Program({"X": dense_stats(pl, X, "ij"), "Y": coo_stats(pl, yc, "jk", {"j": n, "k": n}, eb),
+                       "Z": dense_stats(pl, Z, "im")},
                       [pl.EinSum("E1", "ij,jk->ki", "X", "Y"), pl.EinSum("E2", "ki,im->km", "E1", "Z")])
-    costs = pl.Costs.mi355x("f32", c_fixed=c_fixed, max_call_bytes=cap, c_call=c_call)
+    costs = pl.Costs.mi355x(dt, c_fixed=c_fixed, max_call_bytes=cap, c_call=c_call)
     ranked = pl.optimize(prog, costs, k=64)
     picks = list(range(min(top, len(ranked))))
     rest = list(range(len(picks), len(ranked)))
     picks += [rest[int(i)] for i in np.linspace(0, len(rest) - 1, min(3, len(rest)))] if rest else []
-    ext1 = {"i": emb, "j": n, "k": n}
-    ext2 = {"k": n, "i": emb, "m": zo}
-    out = []
+    out, skipped = [], []
+    budget = 8 << 30
     for r in picks:
         cost, plan = ranked[r]
         P1, P2 = set(plan["E1"]), set(plan["E2"])
+        yrel = relation_from_coo(yc, yv, "jk", P1, {"j": n, "k": n}, budget, dt)
+        if yrel is None:
+            skipped.append({"rank": r + 1, "plan": plan, "estimated_ms": cost * 1e3,
+                            "reason": "Y in this decomposition would take more than 8 GB"})
+            log(f"[bench] plan rank {r + 1} {plan}: estimated {cost * 1e3:.3f} ms, not run (inputs too large)")
+            continue
         s1 = {"einsum": "ij,jk->ki", "upper": "".join(sorted(P1)), "extents": ext1, "tiles": {l: 1 for l in P1},
-              "dtype": "f32"}
+              "dtype": dt}
         s2 = {"einsum": "ki,im->km", "upper": "".join(sorted(P2)), "extents": ext2, "tiles": {l: 1 for l in P2},
-              "dtype": "f32"}
-        xk, xt = dev_rel(relation_from_dense(X, "ij", P1), torch)
-        yk, yt = dev_rel(relation_from_dense(Y, "jk", P1), torch)
-        zk, zt = dev_rel(relation_from_dense(Z, "im", P2), torch)
+              "dtype": dt}
+        xr = relation_from_dense(X, "ij", P1)
+        xr["dtype"] = dt
+        zr = relation_from_dense(Z, "im", P2)
+        zr["dtype"] = dt
+        xk, xt = dev_rel(xr, torch)
+        yk, yt = dev_rel(yrel, torch)
+        zk, zt = dev_rel(zr, torch)
+        del yrel
         w_in = "".join(l for l in "ki" if l in P1)
         w_out = "".join(l for l in "ki" if l in P2)
         probe = tre.einsum(tre.Plan.from_spec(s1, validate=False), xk, xt, yk, yt)
         st1 = Stage(tre, torch, s1, int(xk.shape[0]), int(yk.shape[0]), max(probe.n_pairs, 1), "E1")
-        n2 = probe.n_w if w_in == w_out else None
-        if n2 is None:
-            rk, _ = tre.repartition("ki", w_in, w_out, {"k": n, "i": emb}, {l: 1 for l in w_in},
-                                    {l: 1 for l in w_out}, probe.w_keys, probe.w_tiles)
-            n2 = int(rk.shape[0])
-        probe2 = None
+        del probe
         st2 = None
+        tbuf = None
 
         def step():
-            nonlocal probe2, st2
+            nonlocal st2, tbuf
             tk, tt = st1.run(xk, xt, yk, yt)
+            if dt == "bf16":
+                if tbuf is None or tbuf.numel() < tt.numel():
+                    tbuf = torch.empty(tt.numel(), dtype=torch.bfloat16, device="cuda")
+                tt = tre.cast_f32_bf16(tt, out=tbuf[:tt.numel()]).view(tt.shape)
             if w_in != w_out:
                 tk, tt = tre.repartition("ki", w_in, w_out, {"k": n, "i": emb}, {l: 1 for l in w_in},
                                          {l: 1 for l in w_out}, tk if tk.shape[1] else None, tt)
@@ -696,17 +742,19 @@ def planner_check(tre, torch, top, steps):
                     "e1_pairs": int(st1.n_pairs), "e2_pairs": int(st2.n_pairs), "repartition": w_in != w_out,
                     "max_mag_rel_err": err})
         log(f"[bench] plan rank {r + 1} {plan}: estimated {cost * 1e3:.3f} ms, measured {ms:.3f} ms, err {err:.1e}")
-        del st1, st2, xk, xt, yk, yt, zk, zt
+        del st1, st2, xk, xt, yk, yt, zk, zt, tbuf
         torch.cuda.empty_cache()
     order_est = [o["estimated_ms"] for o in out]
     order_meas = [o["measured_ms"] for o in out]
     from scipy.stats import spearmanr
 
-    return {"metric": "planner ranking: estimated vs measured step time of the fp32 GNN chain (4096 vertices), 1 "
-                      "MI355X", "c_fixed_s": c_fixed, "c_xfer_s_per_byte": costs.c_xfer, "c_flop_s": costs.c_flop,
+    name = f"{dt} GNN chain ({n} vertices)"
+    return {"metric": f"planner ranking: estimated vs measured step time of the {name}, 1 MI355X",
+            "config": config, "c_fixed_s": c_fixed, "c_xfer_s_per_byte": costs.c_xfer, "c_flop_s": costs.c_flop,
             "c_call_s": c_call, "max_call_bytes": cap, "feasible_plans": len(ranked), "plans": out,
-            "spearman_estimated_vs_measured": float(spearmanr(order_est, order_meas)[0]),
-            "measured_best_is_estimated_best": bool(int(np.argmin(order_meas)) == 0),
+            "not_run": skipped,
+            "spearman_estimated_vs_measured": float(spearmanr(order_est, order_meas)[0]) if len(out) > 2 else None,
+            "measured_best_is_estimated_best": bool(out and int(np.argmin(order_meas)) == 0 and out[0]["rank"] == 1),
             "steps": steps, "data": "synthetic"}
 
 
@@ -739,8 +787,9 @@ def main():
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="first run one device copy of this many GiB (counter calibration under rocprofv3 --pmc)")
     ap.add_argument("--planner-top", type=int, default=0, metavar="K",
-                    help="instead of the benchmark: rank the decompositions of the fp32 GNN chain with the planner, "
-                         "run the K cheapest and a spread of the rest, and print estimated vs measured times")
+                    help="instead of the benchmark: rank the decompositions of the GNN chain of --config 1 or 2 with "
+                         "the planner, run the K cheapest and a spread of the rest, and print estimated vs measured "
+                         "times")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (the path shards by output key "
@@ -767,7 +816,9 @@ def main():
     PLAN_OPTIONS["u_ranges"] = args.u_ranges
     PLAN_OPTIONS["pace_windows"] = args.pace_windows
     if args.planner_top:
-        print(json.dumps(planner_check(tre, torch, args.planner_top, args.steps)), flush=True)
+        if args.config not in (1, 2):
+            raise SystemExit("--planner-top covers the GNN chains of workloads 1 and 2")
+        print(json.dumps(planner_check(tre, torch, args.config, args.planner_top, args.steps)), flush=True)
         return
     W = make_workload(args.config, tre, torch, args.three_way)
     log("[bench] inputs resident; warming up")

@@ -72,3 +72,25 @@ def test_relation_from_dense_matches_the_generator(bench):
     assert np.array_equal(rows["tiles"], Y.T[rows["keys"][:, 0]])
     one = bench.relation_from_dense(Y, "jk", set())
     assert one["keys"].shape == (1, 0) and np.array_equal(one["tiles"][0], Y.reshape(-1))
+
+
+def test_relation_from_coo(bench):
+    """Entries of a sparse tensor laid out under a promoted set: keys are the
+    distinct promoted coordinates, tiles dense over the demoted labels; too
+    large a layout is refused."""
+    import numpy as np
+
+    coords = np.array([[0, 2], [0, 5], [3, 1], [3, 2]], np.int64)
+    vals = np.array([1.0, 2.0, 3.0, 4.0], np.float32)
+    ext = {"j": 4, "k": 6}
+    r = bench.relation_from_coo(coords, vals, "jk", {"j", "k"}, ext, 1 << 20, "f32")
+    assert np.array_equal(r["keys"], coords.astype(np.int32)) and np.array_equal(r["tiles"][:, 0], vals)
+    r = bench.relation_from_coo(coords, vals, "jk", {"j"}, ext, 1 << 20, "f32")
+    assert r["keys"].reshape(-1).tolist() == [0, 3]
+    assert r["tiles"].tolist() == [[0, 0, 1, 0, 0, 2], [0, 3, 4, 0, 0, 0]]
+    r = bench.relation_from_coo(coords, vals, "jk", {"k"}, ext, 1 << 20, "f32")
+    assert r["keys"].reshape(-1).tolist() == [1, 2, 5]
+    assert r["tiles"].tolist() == [[0, 0, 0, 3], [1, 0, 0, 4], [2, 0, 0, 0]]
+    r = bench.relation_from_coo(coords, vals, "jk", set(), ext, 1 << 20, "f32")
+    assert r["keys"].shape == (1, 0) and r["tiles"].reshape(4, 6)[3, 2] == 4.0
+    assert bench.relation_from_coo(coords, vals, "jk", set(), ext, 64, "f32") is None
