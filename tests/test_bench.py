@@ -72,6 +72,16 @@ def test_relation_from_dense_matches_the_generator(bench):
     assert np.array_equal(rows["tiles"], Y.T[rows["keys"][:, 0]])
     one = bench.relation_from_dense(Y, "jk", set())
     assert one["keys"].shape == (1, 0) and np.array_equal(one["tiles"][0], Y.reshape(-1))
+    # with tiles: the generator's own 64 x 64 relation
+    tiled = bench.relation_from_dense(Y, "jk", {"j": 64, "k": 64})
+    assert np.array_equal(tiled["keys"], w["Y"]["keys"]) and np.array_equal(tiled["tiles"], w["Y"]["tiles"])
+    coo = bench.relation_from_coo(w["Y"]["coo"][0], w["Y"]["values"], "jk", {"j": 64, "k": 64}, {"j": n, "k": n},
+                                  1 << 30, "f32")
+    assert np.array_equal(coo["keys"], w["Y"]["keys"]) and np.array_equal(coo["tiles"], w["Y"]["tiles"])
+    emb = w["emb"]
+    X = np.ascontiguousarray(w["X"]["tiles"].reshape(n // 64, emb, 64).transpose(1, 0, 2).reshape(emb, n))
+    xr = bench.relation_from_dense(X, "ij", {"j": 64})
+    assert np.array_equal(xr["keys"], w["X"]["keys"]) and np.array_equal(xr["tiles"], w["X"]["tiles"])
 
 
 def test_relation_from_coo(bench):

@@ -135,27 +135,41 @@ def test_repart_properties():
 
 # ---------------------------------------------------- planner vs the oracle
 
-def _rand_tensor(rng, labels, ext):
+def _rand_tensor(rng, labels, ext, tiles=None):
+    """Random statistics; ``tiles`` maps a label to candidate tile sizes
+    (V_t drawn between V / t and min(V, extent / t))."""
     cells = 1
     for l in labels:
         cells *= ext[l]
     nnz = float(rng.integers(1, cells + 1))
     distinct = {l: float(rng.integers(max(1, int(ext[l] * 0.3)), ext[l] + 1)) for l in labels}
+    tiled = {}
+    for l in labels:
+        for t in (tiles or {}).get(l, []):
+            lo, hi = math.ceil(distinct[l] / t), min(distinct[l], ext[l] // t)
+            tiled.setdefault(l, {})[t] = float(rng.integers(lo, max(lo, hi) + 1))
     return {"labels": labels, "extents": {l: ext[l] for l in labels}, "nnz": nnz, "distinct": distinct,
-            "elem_bytes": int(rng.choice([2, 4]))}
+            "elem_bytes": int(rng.choice([2, 4])), "tiled": tiled}
 
 
-def _rand_program(rng):
+def _rand_program(rng, with_tiles=False):
     """A chain of 1-3 binary EinSums over 2-3 labels per operand; the next
-    EinSum consumes the previous result on the left or the right."""
+    EinSum consumes the previous result on the left or the right.  With
+    ``with_tiles`` the extents are multiples of 4 and some labels carry
+    candidate tile sizes 2 and 4."""
     letters = list("abcdefgh")
-    ext = {l: int(rng.integers(2, 40)) for l in letters}
+    if with_tiles:
+        ext = {l: 4 * int(rng.integers(1, 10)) for l in letters}
+        cand = {l: [2, 4] for l in letters if rng.random() < 0.5}
+    else:
+        ext = {l: int(rng.integers(2, 40)) for l in letters}
+        cand = {}
     rng.shuffle(letters)
-    n_e = int(rng.integers(1, 4))
+    n_e = int(rng.integers(1, 4 if not with_tiles else 3))
     inputs, einsums = {}, []
     u = "".join(letters[:2])
     cur = "x0"
-    inputs["x0"] = _rand_tensor(rng, u, ext)
+    inputs["x0"] = _rand_tensor(rng, u, ext, cand)
     cur_labels = u
     pool = letters[2:]
     for i in range(n_e):
@@ -168,7 +182,7 @@ def _rand_program(rng):
         w = "".join(dict.fromkeys(keep))
         w = "".join(rng.permutation(list(w)))
         name_v = f"y{i}"
-        inputs[name_v] = _rand_tensor(rng, v, ext)
+        inputs[name_v] = _rand_tensor(rng, v, ext, cand)
         if rng.random() < 0.5:
             einsums.append((f"e{i}", f"{cur_labels},{v}->{w}", cur, name_v))
         else:
@@ -180,7 +194,7 @@ def _rand_program(rng):
 def _to_product(prog, c):
     from paper_2603_08957_amd import planner as pl
 
-    inputs = {k: pl.Stats(t["labels"], t["extents"], t["nnz"], t["distinct"], t["elem_bytes"])
+    inputs = {k: pl.Stats(t["labels"], t["extents"], t["nnz"], t["distinct"], t["elem_bytes"], t.get("tiled", {}))
               for k, t in prog["inputs"].items()}
     einsums = [pl.EinSum(n, e, a, b) for n, e, a, b in prog["einsums"]]
     return pl.Program(inputs, einsums), pl.Costs(c["c_xfer"], c["c_flop"], c["c_fixed"], c["max_call_bytes"],
@@ -204,8 +218,62 @@ def test_planner_matches_exhaustive_search(seed):
     assert len(got) == len(want)
     for (gc, gplan), (wc, _) in zip(got, want):
         assert gc == pytest.approx(wc, rel=1e-9)
-        assert op.total_cost(prog, {k: frozenset(v) for k, v in gplan.items()}, c) == pytest.approx(gc, rel=1e-9)
+        assert op.total_cost(prog, gplan, c) == pytest.approx(gc, rel=1e-9)
         assert pl.plan_cost(P, C, gplan) == pytest.approx(gc, rel=1e-9)
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_planner_with_tiles_matches_exhaustive_search(seed):
+    """Labels with candidate tile sizes: each EinSum picks, per label,
+    demoted or promoted at tile 1, 2 or 4; the dynamic programme still
+    finds the oracle's four cheapest plans."""
+    from paper_2603_08957_amd import planner as pl
+
+    rng = np.random.default_rng(7100 + seed)
+    prog = _rand_program(rng, with_tiles=True)
+    cap = math.inf if seed % 3 else float(rng.integers(200, 20000))
+    c = _costs(10 ** rng.uniform(-13, -10), 10 ** rng.uniform(-15, -12), 10 ** rng.uniform(-11, -8), cap,
+               0.0 if seed % 2 else 10 ** rng.uniform(-6, -3))
+    want = op.best_plans(prog, c, k=4)
+    P, C = _to_product(prog, c)
+    got = pl.optimize(P, C, k=4)
+    assert len(got) == len(want)
+    for (gc, gplan), (wc, _) in zip(got, want):
+        assert gc == pytest.approx(wc, rel=1e-9)
+        assert op.total_cost(prog, gplan, c) == pytest.approx(gc, rel=1e-9)
+
+
+def test_tiled_count_matches_generated_tiles():
+    """The 4096-vertex graph's adjacency at tile 64 on both labels: the
+    tiled statistics (64 non-empty 64-slices per label) give Eq. eqn-count's
+    4094.6 tuples, the generator stores 4094 tiles."""
+    from paper_2603_08957_amd import planner as pl
+
+    w = workloads.config(1)
+    st = pl.stats_from_coo("jk", {"j": 4096, "k": 4096}, w["Y"]["coo"][0], 4, {"j": [64], "k": [64]})
+    assert st.v("j", 64) == 64 and st.v("k", 64) == 64
+    t = {"labels": "jk", "extents": st.extents, "nnz": st.nnz, "distinct": st.distinct, "tiled": st.tiled,
+         "elem_bytes": 4}
+    assert op.count(t, {"j": 64, "k": 64}) == pytest.approx(op.eqn_count(32768, [64, 64]), rel=1e-12)
+    assert abs(len(w["Y"]["keys"]) - op.count(t, {"j": 64, "k": 64})) < 1.0
+    # tile-1 counts are the distinct-coordinate counts
+    assert op.count(t, {"j": 1}) == pytest.approx(op.eqn_count(32768, [st.v("j")]), rel=1e-12)
+
+
+def test_tiled_kernel_and_tuple_sizes():
+    """A label promoted at tile t contributes t to the kernel's extents and
+    to the tile bytes, and one key attribute."""
+    tu = {"labels": "ij", "extents": {"i": 8, "j": 12}, "nnz": 1e12, "distinct": {"i": 8, "j": 12},
+          "tiled": {"j": {4: 3}}, "elem_bytes": 4}
+    tv = {"labels": "jk", "extents": {"j": 12, "k": 5}, "nnz": 1e12, "distinct": {"j": 12, "k": 5},
+          "tiled": {"j": {4: 3}}, "elem_bytes": 4}
+    tw = op.derive("ij", "jk", "ik", tu, tv)
+    assert op.row_bytes(tu, {"j": 4}) == 4 + 4 * 8 * 4
+    # 3 x 3 / 3 = 3 join tuples of a 2 * 8 * 4 * 5-flop kernel; one group
+    # (W has no promoted label), T_agg = min(3 / 2, 1) = 1, so 2 adds of an
+    # 8 x 5 tile
+    c = op.einsum_cost(tu, tv, tw, {"j": 4}, _costs(0.0, 1.0, 0.0))
+    assert c == pytest.approx(3 * 2 * 8 * 4 * 5 + (3 - 1) * 8 * 5, rel=1e-12)
 
 
 def test_planner_rejects_reused_results():
@@ -233,6 +301,26 @@ def test_planner_picks_scalar_adjacency_for_the_large_gcn():
                       [pl.EinSum("E1", "ij,jk->ki", "X", "Y"), pl.EinSum("E2", "ki,im->km", "E1", "Z")])
     best = pl.optimize(prog, pl.Costs.mi355x("bf16", max_call_bytes=256 << 20), k=3)
     cost, plan = best[0]
-    assert set(plan["E1"]) == {"j", "k"}
+    assert plan["E1"] == {"j": 1, "k": 1}
     assert "k" in plan["E2"]
     assert all(c >= cost for c, _ in best)
+
+
+def test_planner_prefers_scalar_adjacency_to_128_tiles():
+    """The 262,144-vertex chain with 128x128 tiles allowed for the vertex
+    labels (Y's 128-slices all non-empty): the cheapest plan still stores the
+    adjacency as scalar tuples, and the 128-tiled split the workload fixes
+    costs more than ten times as much under the model."""
+    from paper_2603_08957_amd import planner as pl
+
+    n, emb, nb = 1 << 18, 128, (1 << 18) // 128
+    X = pl.Stats("ij", {"i": emb, "j": n}, float(emb * n), {"i": emb, "j": n}, 2, {"j": {128: nb}})
+    Y = pl.Stats("jk", {"j": n, "k": n}, 4194304.0, {"j": n, "k": n}, 2, {"j": {128: nb}, "k": {128: nb}})
+    Z = pl.Stats("im", {"i": emb, "m": emb}, float(emb * emb), {"i": emb, "m": emb}, 2)
+    prog = pl.Program({"X": X, "Y": Y, "Z": Z},
+                      [pl.EinSum("E1", "ij,jk->ki", "X", "Y"), pl.EinSum("E2", "ki,im->km", "E1", "Z")])
+    costs = pl.Costs.mi355x("bf16", max_call_bytes=256 << 20, c_call=1.2e-4)
+    cost, plan = pl.optimize(prog, costs, k=1)[0]
+    assert plan["E1"] == {"j": 1, "k": 1}
+    literal = pl.plan_cost(prog, costs, {"E1": {"j": 128, "k": 128}, "E2": {"k": 128}})
+    assert literal > 10 * cost
