@@ -234,6 +234,14 @@ tre_status tre_stack_rows(const int32_t *keys, int64_t n, const void *tiles, int
  *   elem_bytes        : 2 (bf16 bits) or 4 (fp32); values are copied bit for bit.
  *   keys_in, tiles_in : device source relation, conventions above (sorted keys).
  *   keys_out, tiles_out: device [out_cap x r_out] int32 / [out_cap x tile_elems_out].
+ *                       tiles_out may be tiles_in (in place) when the target
+ *                       tiles are the source tiles regrouped: every source tile
+ *                       lies in one target tile as one contiguous run, every
+ *                       target tile is covered, and source key order is target
+ *                       order (e.g. stacking per-vertex rows into row blocks
+ *                       with no vertex missing).  Then no tile byte moves and
+ *                       only keys_out is written; otherwise in place is
+ *                       TRE_E_ARG, with the tiles untouched.
  *   n_out             : host; the number of target tuples: one for every target
  *                       tile that contains a position of a source tile (zero
  *                       values included), keys sorted.  Target elements that no

@@ -96,12 +96,22 @@ double unit_workgroups(const Plan& p) {
     return double(t) / 256.0;
 }
 
+// Unit length cap.  GEMM-class units are dispatched longest first, so once
+// the keys' output blocks fill every resident slot (two workgroups per CU)
+// one unit per key is the better schedule: measured on the block-sparse
+// product (1,024 blocks of 6.4 pairs on average), cutting keys into units of
+// 4-8 pairs cost 10% more in contraction and partial-tile sums.
 int64_t choose_unit(const Plan& p, const Layout& L, int64_t n_pairs, int64_t n_w) {
     const double uw = unit_workgroups(p);
+    int dev = 0, cus = 0;
+    const int64_t fill = (hipGetDevice(&dev) == hipSuccess &&
+                          hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0)
+                             ? 2 * int64_t(cus)
+                             : int64_t(kTargetWorkgroups);
     int64_t pu;
     if (p.opt.max_pairs_per_unit > 0) {
         pu = p.opt.max_pairs_per_unit;
-    } else if (double(n_w) * uw >= kTargetWorkgroups) {
+    } else if (double(n_w) * uw >= kTargetWorkgroups || (p.kclass == KC_GEMM && double(n_w) * uw >= fill)) {
         pu = std::max<int64_t>(n_pairs, 1);  // enough output blocks: one unit per key
     } else {
         pu = std::max<int64_t>(4, int64_t(std::ceil(double(n_pairs) * uw / kTargetWorkgroups)));
@@ -248,7 +258,7 @@ tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* 
     hipError_t e;
     if ((e = launch_tables(p, reinterpret_cast<int32_t*>(w + L.tables), s)) != hipSuccess) return dev_fail(e, "tables");
     if (R > 1) e = launch_range_units(p, L, w, n_w, jr->n_u, R, s);
-    else e = launch_units(p, L, w, n_pairs, n_w, p_unit, s);
+    else e = launch_units(p, L, w, n_pairs, n_w, p_unit, !pace, s);
     if (e != hipSuccess) return dev_fail(e, "units");
     tm.mark(s);
     const int64_t unit_bound = R > 1 ? int64_t(R) * n_w : n_w + n_pairs / p_unit + 1;

@@ -76,7 +76,7 @@ __global__ void k_seg_units(const int32_t* __restrict__ seg_start, int64_t n_w, 
     nsplit[s] = u > 1 ? 1 : 0;
 }
 
-__global__ void k_fill_units(const int32_t* __restrict__ seg_start, int64_t n_w, int64_t p_unit,
+__global__ void k_fill_units(const int32_t* __restrict__ seg_start, int64_t n_w,
                              const int32_t* __restrict__ uoff, const int32_t* __restrict__ poff,
                              const int32_t* __restrict__ soff, Unit* __restrict__ units, int32_t* __restrict__ split,
                              WsHeader* hdr) {
@@ -90,15 +90,56 @@ __global__ void k_fill_units(const int32_t* __restrict__ seg_start, int64_t n_w,
     }
     const int32_t a = seg_start[s], b = seg_start[s + 1];
     const int32_t nu = uoff[s + 1] - uoff[s];
+    // a split key is cut into nu units of equal length (within one pair)
+    const int64_t len = int64_t(b) - a;
     for (int32_t j = 0; j < nu; j++) {
         Unit u;
         u.seg = int32_t(s);
-        u.p0 = a + int32_t(j * p_unit);
-        u.p1 = int32_t(min<int64_t>(int64_t(a) + (j + 1) * p_unit, b));
+        u.p0 = a + int32_t(len * j / nu);
+        u.p1 = a + int32_t(len * (j + 1) / nu);
         u.slot = nu > 1 ? poff[s] + j : -1;
         units[uoff[s] + j] = u;
     }
     if (nu > 1) split[soff[s]] = int32_t(s);
+}
+
+// Longest units first: one workgroup reorders a unit table of at most
+// kOrderMax entries by decreasing length (counting sort on the length, capped
+// at kOrderBins - 1), so that the hardware's in-order dispatch of the
+// contraction grid is a longest-processing-time-first schedule and the
+// longest keys do not start in the last wave.  Each unit's sum does not depend
+// on when it runs, so the order within a length class is left to the LDS
+// atomics.
+constexpr int kOrderMax = 4096, kOrderBins = 1024;
+
+__global__ __launch_bounds__(kOrderBins) void k_order_units(Unit* __restrict__ units, const WsHeader* __restrict__ hdr) {
+    __shared__ Unit buf[kOrderMax];
+    __shared__ int32_t cnt[kOrderBins];
+    const int32_t n = hdr->n_units;
+    if (n < 2 || n > kOrderMax) return;
+    const int t = threadIdx.x;
+    auto bin = [](const Unit& u) { return kOrderBins - 1 - min(u.p1 - u.p0, kOrderBins - 1); };
+    cnt[t] = 0;
+    __syncthreads();
+    for (int i = t; i < n; i += kOrderBins) {
+        const Unit u = units[i];
+        buf[i] = u;
+        atomicAdd(&cnt[bin(u)], 1);
+    }
+    __syncthreads();
+    const int32_t own = cnt[t];
+    for (int off = 1; off < kOrderBins; off <<= 1) {
+        const int32_t add = t >= off ? cnt[t - off] : 0;
+        __syncthreads();
+        cnt[t] += add;
+        __syncthreads();
+    }
+    cnt[t] -= own;  // exclusive start of bin t
+    __syncthreads();
+    for (int i = t; i < n; i += kOrderBins) {
+        const Unit u = buf[i];
+        units[atomicAdd(&cnt[bin(u)], 1)] = u;
+    }
 }
 
 // U-range units (see launch_range_units): unit r * n_w + s covers the pairs of
@@ -601,9 +642,7 @@ hipError_t launch_tables(const Plan& p, int32_t* tables, hipStream_t s) {
 }
 
 hipError_t launch_units(const Plan& p, const Layout& L, char* ws, int64_t n_pairs, int64_t n_w, int64_t p_unit,
-                        hipStream_t s) {
-    (void)p;
-    (void)n_pairs;
+                        bool longest_first, hipStream_t s) {
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
     int32_t* seg_start = reinterpret_cast<int32_t*>(ws + L.seg_start);
     int32_t* nunits = reinterpret_cast<int32_t*>(ws + L.seg_units);
@@ -616,10 +655,16 @@ hipError_t launch_units(const Plan& p, const Layout& L, char* ws, int64_t n_pair
     if ((e = scan_exclusive_i32(nunits, nunits, n_w + 1, tmp, s)) != hipSuccess) return e;
     if ((e = scan_exclusive_i32(nparts, nparts, n_w + 1, tmp, s)) != hipSuccess) return e;
     if ((e = scan_exclusive_i32(nsplit, nsplit, n_w + 1, tmp, s)) != hipSuccess) return e;
-    k_fill_units<<<blocks_for(n_w + 1), kThreads, 0, s>>>(seg_start, n_w, p_unit, nunits, nparts, nsplit,
+    k_fill_units<<<blocks_for(n_w + 1), kThreads, 0, s>>>(seg_start, n_w, nunits, nparts, nsplit,
                                                           reinterpret_cast<Unit*>(ws + L.unit_desc),
                                                           reinterpret_cast<int32_t*>(ws + L.split_list), hdr);
-    return hipGetLastError();
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // one workgroup per output block and unit: dispatch the longest first
+    if (longest_first && p.kclass == KC_GEMM && n_w + n_pairs / p_unit + 1 <= kOrderMax) {
+        k_order_units<<<1, kOrderBins, 0, s>>>(reinterpret_cast<Unit*>(ws + L.unit_desc), hdr);
+        e = hipGetLastError();
+    }
+    return e;
 }
 
 hipError_t launch_range_units(const Plan& p, const Layout& L, char* ws, int64_t n_w, int64_t n_u, int32_t R,

@@ -38,6 +38,7 @@ struct RpDesc {
     int32_t key_bits;
     int64_t te_in, te_out;
     int64_t max_cover;              // target tiles one source tile can meet
+    int32_t regroup;                // a source tile is one contiguous run of its target tile
 };
 
 struct RpHeader {
@@ -434,6 +435,20 @@ tre_status make_desc(const char* labels, const char* up_in, const char* up_out, 
         set_error("tre_repartition: target key space exceeds 64 bits");
         return TRE_E_SHAPE;
     }
+    // A source tile is one contiguous run of the target tile (row-major) when,
+    // at the first label whose source tile is shorter than the target's, every
+    // label before it has a source tile of 1 and every label after it the
+    // target's tile.  Sources of one target then sit in source key order.
+    d.regroup = 1;
+    int first = 0;
+    while (first < d.nl && d.tin[first] >= d.tout[first]) first++;
+    for (int i = 0; i < d.nl; i++)
+        if (i < first ? d.tin[i] != 1 : (i > first && d.tin[i] != d.tout[i])) d.regroup = 0;
+    if (first == d.nl) {  // no source tile shorter than its target: the same tiles
+        d.regroup = 1;
+        for (int i = 0; i < d.nl; i++)
+            if (d.tin[i] != d.tout[i]) d.regroup = 0;
+    }
     int64_t si = 1, so = 1;
     for (int i = d.nl - 1, sh = 0, ko = d.rout - 1; i >= 0; i--) {
         if (d.pout[i]) {
@@ -583,6 +598,14 @@ tre_status tre_repartition(const char* labels, const char* upper_in, const char*
         (e = hipStreamSynchronize(s)) != hipSuccess)
         return dev_fail(e, "target count read-back");
     *n_out = h.n_out;
+    // in place: only a regrouping of whole source tiles, in source order,
+    // with nothing missing, leaves the bytes where they are
+    const bool in_place = tiles_out == tiles_in;
+    if (in_place && !(d.regroup && !h.unsorted && m == n_in && n_in * d.te_in == h.n_out * d.te_out)) {
+        set_error("tre_repartition: tiles_out == tiles_in needs every target tile to be its source tiles, "
+                  "complete and in source order");
+        return TRE_E_ARG;
+    }
     if (h.n_out > out_cap) {
         set_error("tre_repartition: output capacity below the target tuple count");
         return TRE_E_CAPACITY;
@@ -590,6 +613,13 @@ tre_status tre_repartition(const char* labels, const char* upper_in, const char*
     if ((d.rout > 0 && !keys_out) || !tiles_out) {
         set_error("tre_repartition: null output buffers");
         return TRE_E_ARG;
+    }
+    if (in_place) {
+        if (d.rout > 0) {
+            k_rp_write_keys<<<blocks_for(h.n_out), kThreads, 0, s>>>(seg_key, h.n_out, d, keys_out);
+            if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "keys");
+        }
+        return TRE_OK;
     }
     // source tiles are disjoint, so they cover n_in x tile_elems_in target
     // positions; zero the targets only when that leaves some uncovered

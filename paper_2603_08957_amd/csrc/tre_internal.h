@@ -150,8 +150,10 @@ hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t*
 
 // contract.hip
 hipError_t launch_tables(const Plan& p, int32_t* tables, hipStream_t s);
+// longest_first: reorder the units by decreasing length (GEMM class, at most
+// a few thousand units) for a dispatch in that order
 hipError_t launch_units(const Plan& p, const Layout& L, char* ws, int64_t n_pairs, int64_t n_w, int64_t p_unit,
-                        hipStream_t s);
+                        bool longest_first, hipStream_t s);
 // U-range units: unit r * n_w + s holds the pairs of key s whose U index lies
 // in [r * n_u / R, (r + 1) * n_u / R); its partial tile is slot s * R + r.
 hipError_t launch_range_units(const Plan& p, const Layout& L, char* ws, int64_t n_w, int64_t n_u, int32_t R,

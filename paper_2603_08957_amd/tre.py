@@ -292,10 +292,12 @@ def stack_rows(keys, tiles, group: int, stream=None):
 
 
 def repartition(labels: str, upper_in: str, upper_out: str, extents: dict, tiles_in: dict, tiles_out: dict,
-                keys, tiles, stream=None):
+                keys, tiles, stream=None, in_place: bool = False):
     """The relation (keys, tiles) under the target decomposition (see
     tre_repartition).  Returns (keys_out [n_out, r_out] int32, tiles_out
-    [n_out, tile_elems_out], same dtype as ``tiles``)."""
+    [n_out, tile_elems_out], same dtype as ``tiles``).  ``in_place``: the
+    target tiles are a view of ``tiles`` (a regrouping of whole tiles in
+    order, nothing missing; TreError otherwise)."""
     import numpy as _np
     import torch
 
@@ -328,6 +330,14 @@ def repartition(labels: str, upper_in: str, upper_out: str, extents: dict, tiles
         if c in upper_out and to > 0:
             grid *= e // to
             cover *= min(e // to, (ti - 1) // to + 2)
+    if in_place:
+        cap = (n * te_in) // max(te_out, 1)
+        out_keys = torch.empty((max(cap, 1), len(upper_out)), dtype=torch.int32, device=tiles.device)
+        rc = lib().tre_repartition(*args, tiles.element_size(), _ptr(keys), n, _ptr(tiles), _ptr(out_keys),
+                                   _ptr(tiles), cap, ctypes.byref(n_out), _ptr(ws), ws.numel(), _stream(stream))
+        _check(rc, "tre_repartition")
+        k = int(n_out.value)
+        return out_keys[:k], tiles.reshape(-1)[:k * te_out].view(k, te_out)
     # first call with room for every target tile the sources can meet when
     # that costs little memory; otherwise the call reports the count first
     bound = min(grid, n * cover)

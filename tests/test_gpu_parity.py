@@ -492,3 +492,64 @@ def test_repartition_gpu_errors_and_empty(orc):
     k2, t2 = tre.repartition("ij", "i", "j", {"i": 4, "j": 4}, {"i": 1}, {"j": 2},
                              torch.zeros((0, 1), dtype=torch.int32).cuda(), torch.zeros((0, 4)).cuda())
     assert k2.shape[0] == 0 and t2.shape[0] == 0
+
+
+def test_repartition_gpu_in_place(orc):
+    """In place (tiles_out is tiles_in): stacking complete per-vertex rows
+    into row blocks leaves every byte where it is and only writes the keys;
+    a missing row, a column stack or a split is refused with the tiles
+    untouched.  Random full-coverage cases: whenever in place is accepted,
+    keys and tiles equal the oracle's copy."""
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    rng = np.random.default_rng(77)
+    n, emb = 4096, 64
+    keys = torch.arange(n, dtype=torch.int32).reshape(-1, 1).cuda()
+    for dtype in (torch.float32, torch.bfloat16):
+        rows = torch.from_numpy(rng.standard_normal((n, emb)).astype(np.float32)).cuda().to(dtype)
+        before = rows.clone()
+        k2, t2 = tre.repartition("ki", "k", "k", {"k": n, "i": emb}, {"k": 1}, {"k": 256}, keys, rows,
+                                 in_place=True)
+        assert t2.data_ptr() == rows.data_ptr() and tuple(t2.shape) == (n // 256, 256 * emb)
+        k3, t3 = tre.repartition("ki", "k", "k", {"k": n, "i": emb}, {"k": 1}, {"k": 256}, keys, before)
+        assert torch.equal(k2, k3) and torch.equal(t2, t3)
+    rows = torch.from_numpy(rng.standard_normal((n, emb)).astype(np.float32)).cuda()
+    refused = [
+        ("ki", "k", "k", {"k": n, "i": emb}, {"k": 1}, {"k": 256}, keys[1:], rows[1:]),  # row 0 missing
+        ("ki", "ki", "ki", {"k": n, "i": emb}, {"k": 1, "i": 8}, {"k": 4, "i": 8},  # source order is not target order
+         torch.stack(torch.meshgrid(torch.arange(n), torch.arange(emb // 8), indexing="ij"), -1).reshape(-1, 2)
+         .to(torch.int32).contiguous().cuda(), rows.reshape(-1, 8)),
+        ("ki", "k", "k", {"k": n, "i": emb}, {"k": 4}, {"k": 1}, keys[:n // 4], rows.reshape(n // 4, -1)),  # split
+    ]
+    for labels, ui, uo, ext, ti, to, kk, tt in refused:
+        before = tt.clone()
+        with pytest.raises(tre.TreError) as ei:
+            tre.repartition(labels, ui, uo, ext, ti, to, kk, tt, in_place=True)
+        assert ei.value.status == "TRE_E_ARG"
+        assert torch.equal(tt, before)
+    accepted = 0
+    for seed in range(40):
+        r = np.random.default_rng(5000 + seed)
+        labels, up_in, up_out, ext, tin, tout, _, te = _rp_case(r)
+        import itertools
+
+        axes = [range(ext[c] // tin[c]) for c in up_in]
+        combos = list(itertools.product(*axes)) if up_in else [()]
+        keys_all = np.array(combos, np.int32).reshape(len(combos), len(up_in))
+        vals = r.standard_normal((len(keys_all), te)).astype(np.float32)
+        dev = torch.from_numpy(vals).cuda()
+        say("repartition in place", seed, labels, up_in, up_out, tin, tout, len(keys_all))
+        try:
+            k2, t2 = tre.repartition(labels, up_in, up_out, ext, tin, tout, torch.from_numpy(keys_all).cuda(), dev,
+                                     in_place=True)
+        except tre.TreError as e:
+            assert e.status == "TRE_E_ARG"
+            assert np.array_equal(dev.cpu().numpy(), vals)
+            continue
+        accepted += 1
+        rk, rt = orc.repartition(labels, up_in, up_out, ext, tin, tout, keys_all, vals.astype(np.float64))
+        assert np.array_equal(k2.cpu().numpy().reshape(rk.shape), rk)
+        assert np.array_equal(t2.cpu().numpy().astype(np.float64).reshape(rt.shape), rt)
+    assert accepted > 0
