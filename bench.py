@@ -532,6 +532,22 @@ TRAFFIC_RECORDS = {1: "counters_gnn_chain_4096_fp32.md", 2: "counters_gnn_chain_
                    5: "counters_gnn_chain_1048576_bf16.md", 6: "counters_graph_attention_13752_fp32.md"}
 
 
+def library_sha256(root):
+    """SHA-256 over the library's sources (csrc/, sorted by name; each name
+    and its bytes), or None when they cannot be read."""
+    import hashlib
+
+    d = os.path.join(root, "paper_2603_08957_amd", "csrc")
+    h = hashlib.sha256()
+    try:
+        for name in sorted(os.listdir(d)):
+            h.update(name.encode() + b"\0")
+            h.update(open(os.path.join(d, name), "rb").read())
+    except OSError:
+        return None
+    return h.hexdigest()
+
+
 def traffic_record(config, three_way="fused"):
     """HBM bytes per launch of the dominant kernel (FETCH_SIZE + WRITE_SIZE,
     each scaled by a copy of known size) and its counter-measured MFMA work,
@@ -552,6 +568,10 @@ def traffic_record(config, three_way="fused"):
     except (OSError, IndexError, KeyError, ValueError):
         return None
     if hashlib.sha256(src).hexdigest() != rec["kernel_source_sha256"]:
+        return None
+    # the launch (units, pair order, grid) is decided by the rest of the
+    # library: any change there also voids the counters
+    if rec.get("library_sha256") != library_sha256(ROOT):
         return None
     return {"bytes": rec["traffic_bytes_per_launch"], "read_bytes": rec["read_bytes_per_launch"],
             "write_bytes": rec["write_bytes_per_launch"], "kernel": rec["kernel"],

@@ -51,6 +51,21 @@ def test_traffic_record_null_after_kernel_change(bench, tmp_path, monkeypatch):
     assert bench.traffic_record(2) is None
 
 
+def test_traffic_record_null_after_library_change(bench, tmp_path, monkeypatch):
+    """A change anywhere in the library (unit building, join order, launch
+    choice) voids the counters even when the kernel's own file is unchanged."""
+    import shutil
+
+    name = bench.TRAFFIC_RECORDS[3]
+    shutil.copytree(os.path.join(ROOT, "profiles"), tmp_path / "profiles")
+    shutil.copytree(os.path.join(ROOT, "paper_2603_08957_amd", "csrc"), tmp_path / "paper_2603_08957_amd" / "csrc")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.traffic_record(3) is not None, name
+    with open(tmp_path / "paper_2603_08957_amd" / "csrc" / "api.cpp", "a") as f:
+        f.write("\n")
+    assert bench.traffic_record(3) is None
+
+
 def test_relation_from_dense_matches_the_generator(bench):
     """The planner check lays out dense arrays as relations: for the
     adjacency of the 4096-vertex graph in 64 x 64 tiles' promoted form (here
