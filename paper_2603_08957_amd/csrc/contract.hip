@@ -641,6 +641,26 @@ hipError_t launch_tables(const Plan& p, int32_t* tables, hipStream_t s) {
     return hipGetLastError();
 }
 
+// One unit per key (no key longer than the cap): the unit table is the
+// segment table, with no partial tiles and no split keys.
+__global__ void k_key_units(const int32_t* __restrict__ seg_start, int64_t n_w, Unit* __restrict__ units,
+                            WsHeader* hdr) {
+    const int64_t s = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (s > n_w) return;
+    if (s == n_w) {
+        hdr->n_units = int32_t(n_w);
+        hdr->n_parts = 0;
+        hdr->n_split = 0;
+        return;
+    }
+    Unit u;
+    u.seg = int32_t(s);
+    u.p0 = seg_start[s];
+    u.p1 = seg_start[s + 1];
+    u.slot = -1;
+    units[s] = u;
+}
+
 hipError_t launch_units(const Plan& p, const Layout& L, char* ws, int64_t n_pairs, int64_t n_w, int64_t p_unit,
                         bool longest_first, hipStream_t s) {
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
@@ -650,6 +670,16 @@ hipError_t launch_units(const Plan& p, const Layout& L, char* ws, int64_t n_pair
     int32_t* nsplit = reinterpret_cast<int32_t*>(ws + L.flags);
     int32_t* tmp = reinterpret_cast<int32_t*>(ws + L.scan_tmp);
     hipError_t e;
+    if (p_unit >= n_pairs) {  // no key can be longer than the cap
+        k_key_units<<<blocks_for(n_w + 1), kThreads, 0, s>>>(seg_start, n_w, reinterpret_cast<Unit*>(ws + L.unit_desc),
+                                                             hdr);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if (longest_first && p.kclass == KC_GEMM && n_w <= kOrderMax) {
+            k_order_units<<<1, kOrderBins, 0, s>>>(reinterpret_cast<Unit*>(ws + L.unit_desc), hdr);
+            e = hipGetLastError();
+        }
+        return e;
+    }
     k_seg_units<<<blocks_for(n_w + 1), kThreads, 0, s>>>(seg_start, n_w, p_unit, nunits, nparts, nsplit);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = scan_exclusive_i32(nunits, nunits, n_w + 1, tmp, s)) != hipSuccess) return e;

@@ -24,7 +24,7 @@ namespace tre {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kPairsPerThread = 8;
+constexpr int kPairsPerThread = 8;  // pairs per thread of the expansion
 
 struct KeyDesc {
     int32_t n;
@@ -181,6 +181,40 @@ __device__ inline uint64_t pack_w(const int32_t* urow, const int32_t* vrow, cons
 // threads, so every store instruction covers consecutive pairs.
 // KT: uint32 W keys when they fit in 32 bits (less traffic in the sort),
 // else uint64.
+// Expansion of the join into pairs: a workgroup writes the consecutive pairs
+// [b0, b0 + kBlockPairs), thread t the pairs b0 + t + i * kThreads, so every
+// load of V keys and every store is coalesced.  The U tuples whose pair runs
+// meet the block are found by two binary searches over the run offsets; when
+// there are at most kSpan of them their offsets are staged in LDS and each
+// pair finds its U tuple there (the search starts from the thread's previous
+// answer, pairs being visited in increasing order).
+constexpr int kSpan = 4096;
+
+// Largest u in [a, b] with off[u] <= x (off non-decreasing, off[a] <= x),
+// found by the 64 lanes of one wavefront together: each round the lanes probe
+// 64 evenly spaced positions of the interval and one ballot keeps the part
+// between the last probe that passes and the next, so an interval of n
+// positions takes about log64(n) dependent loads instead of log2(n).
+__device__ inline int64_t wave_find_u(const int64_t* __restrict__ off, int64_t x, int64_t a, int64_t b) {
+    const int lane = threadIdx.x & 63;
+    while (a < b) {
+        const int64_t len = b - a;
+        const int64_t pos = a + ((int64_t(lane) + 1) * len + 63) / 64;  // in (a, b], non-decreasing in lane
+        const uint64_t ok = __ballot(off[pos] <= x);
+        const int L = __popcll(ok);  // the passing probes are the lowest L lanes
+        const int64_t first = a + (len + 63) / 64;
+        if (L == 0) {
+            b = first - 1;
+        } else {
+            const int64_t lastok = a + ((int64_t(L) * len + 63) / 64);
+            const int64_t next = L < 64 ? a + ((int64_t(L) + 1) * len + 63) / 64 : b + 1;
+            a = lastok;
+            b = next - 1;
+        }
+    }
+    return a;
+}
+
 template <typename KT>
 __global__ __launch_bounds__(kThreads) void k_expand(const int64_t* __restrict__ off, const int64_t* __restrict__ lo,
                                                      int64_t n_u, int64_t n_pairs, const uint32_t* __restrict__ vperm,
@@ -189,40 +223,76 @@ __global__ __launch_bounds__(kThreads) void k_expand(const int64_t* __restrict__
                                                      int32_t* __restrict__ pu, int32_t* __restrict__ pv,
                                                      KT* __restrict__ wk, uint64_t* __restrict__ uv) {
     constexpr int kBlockPairs = kThreads * kPairsPerThread;
-    __shared__ KT swk[kBlockPairs];
-    __shared__ uint64_t suv[kBlockPairs];
+    __shared__ int32_t s_off[kSpan + 1];  // pair counts stay below 2^31
+    __shared__ int64_t s_ends[2];
     const int64_t b0 = int64_t(blockIdx.x) * kBlockPairs;
-    const int64_t p0 = b0 + int64_t(threadIdx.x) * kPairsPerThread;
-    if (p0 < n_pairs) {
-        // largest u with off[u] <= p0
-        int64_t a = 0, b = n_u - 1;
+    if (b0 >= n_pairs) return;
+    const int64_t b1 = min<int64_t>(b0 + kBlockPairs, n_pairs);
+    // largest u with off[u] <= x
+    auto find_u = [&](int64_t x, int64_t a, int64_t b) {
         while (a < b) {
-            int64_t m = (a + b + 1) >> 1;
-            if (off[m] <= p0) a = m; else b = m - 1;
+            const int64_t m = (a + b + 1) >> 1;
+            if (off[m] <= x) a = m;
+            else b = m - 1;
         }
-        int64_t u = a;
-        int64_t next = off[u + 1];
-        const int64_t p1 = min<int64_t>(p0 + kPairsPerThread, n_pairs);
-        for (int64_t p = p0; p < p1; p++) {
-            while (p >= next) {
-                u++;
-                next = off[u + 1];
-            }
-            const int64_t vs = lo[u] + (p - off[u]);
-            const int64_t v = vperm ? int64_t(vperm[vs]) : vs;
-            swk[p - b0] = KT(pack_w(ukeys + u * ru, vkeys + v * rv, wd));
-            suv[p - b0] = (uint64_t(uint32_t(u)) << 32) | uint64_t(uint32_t(v));
-        }
+        return a;
+    };
+    if (threadIdx.x < 128) {
+        const int64_t e = wave_find_u(off, threadIdx.x < 64 ? b0 : b1 - 1, 0, n_u - 1);
+        if ((threadIdx.x & 63) == 0) s_ends[threadIdx.x >> 6] = e;
     }
     __syncthreads();
-    const int cnt = int(min<int64_t>(kBlockPairs, n_pairs - b0));
-    for (int q = threadIdx.x; q < cnt; q += kThreads) {
-        wk[b0 + q] = swk[q];
+    const int64_t ua = s_ends[0], ub = s_ends[1];
+    const int64_t span = ub - ua + 1;
+    const bool staged = span <= kSpan;
+    if (staged) {
+        for (int64_t i = threadIdx.x; i <= span; i += kThreads) s_off[i] = int32_t(off[ua + i]);
+        __syncthreads();
+    }
+    // the thread's pairs in three rounds, each issuing all of its loads
+    // before using them: U tuple and run offset (LDS), then the run starts,
+    // then the V keys
+    int32_t u[kPairsPerThread], vv[kPairsPerThread];
+    int32_t idx = 0;  // position of the current U tuple in [ua, ub]
+#pragma unroll
+    for (int i = 0; i < kPairsPerThread; i++) {
+        const int64_t p = b0 + int64_t(i) * kThreads + threadIdx.x;
+        u[i] = -1;
+        if (p < b1) {
+            if (staged) {
+                int32_t a = idx, b = int32_t(span) - 1;
+                while (a < b) {
+                    const int32_t m = (a + b + 1) >> 1;
+                    if (s_off[m] <= p) a = m;
+                    else b = m - 1;
+                }
+                idx = a;
+                vv[i] = int32_t(p - s_off[a]);
+            } else {
+                idx = int32_t(find_u(p, ua + idx, ub) - ua);
+                vv[i] = int32_t(p - off[ua + idx]);
+            }
+            u[i] = int32_t(ua + idx);
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < kPairsPerThread; i++)
+        if (u[i] >= 0) vv[i] += int32_t(lo[u[i]]);
+    if (vperm) {
+#pragma unroll
+        for (int i = 0; i < kPairsPerThread; i++)
+            if (u[i] >= 0) vv[i] = int32_t(vperm[vv[i]]);
+    }
+#pragma unroll
+    for (int i = 0; i < kPairsPerThread; i++) {
+        if (u[i] < 0) continue;
+        const int64_t p = b0 + int64_t(i) * kThreads + threadIdx.x;
+        wk[p] = KT(pack_w(ukeys + int64_t(u[i]) * ru, vkeys + int64_t(vv[i]) * rv, wd));
         if (uv) {
-            uv[b0 + q] = suv[q];
+            uv[p] = (uint64_t(uint32_t(u[i])) << 32) | uint64_t(uint32_t(vv[i]));
         } else {
-            pu[b0 + q] = int32_t(suv[q] >> 32);
-            pv[b0 + q] = int32_t(suv[q] & 0xffffffffu);
+            pu[p] = int32_t(u[i]);
+            pv[p] = int32_t(vv[i]);
         }
     }
 }

@@ -45,11 +45,16 @@ __global__ __launch_bounds__(kThreads) void k_digit_hist(const KT* __restrict__ 
     __syncthreads();
     const int64_t base = int64_t(blockIdx.x) * kTile;
     const uint64_t mask = uint64_t(radix - 1);
-#pragma unroll 4
+    // all of the thread's loads in flight before the first count
+    KT k[kIpt];
+#pragma unroll
     for (int r = 0; r < kIpt; r++) {
         const int64_t i = base + int64_t(r) * kThreads + threadIdx.x;
-        if (i < n) atomicAdd(&cnt[(keys[i] >> shift) & mask], 1);
+        k[r] = i < n ? keys[i] : KT(0);
     }
+#pragma unroll
+    for (int r = 0; r < kIpt; r++)
+        if (base + int64_t(r) * kThreads + threadIdx.x < n) atomicAdd(&cnt[(k[r] >> shift) & mask], 1);
     __syncthreads();
     for (int d = threadIdx.x; d < radix; d += kThreads) hist[int64_t(d) * n_tiles + blockIdx.x] = cnt[d];
 }
