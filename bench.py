@@ -84,19 +84,36 @@ class Stage:
                 "n_split_segments": t.n_split_segments}
 
     def run(self, uk, ut, vk, vt, timing=None):
-        tre = self.tre
+        jr = self.join(uk, vk, timing=timing)
+        return self.contract(jr, ut, vt, timing=timing)
+
+    def join(self, uk, vk, timing=None, stream=None):
+        """tre_join (synchronises ``stream``) and output buffers sized for it."""
         if self.record is not None:
             timing = self.record
             timing.deferred = 0
-        jr = tre.join(self.plan, uk, self.n_u, vk, self.n_v, self.ws, timing=timing)
+        jr = self.tre.join(self.plan, uk, self.n_u, vk, self.n_v, self.ws, stream=stream, timing=timing)
         if self.w_tiles is None or self.w_tiles.shape[0] < jr.n_w:
-            self.w_keys = self.torch.empty((jr.n_w, max(self.plan.key_arity[2], 1)), dtype=self.torch.int32,
-                                           device="cuda")
+            shape = (jr.n_w, max(self.plan.key_arity[2], 1))
+            self.w_keys = self.torch.empty(shape, dtype=self.torch.int32, device="cuda")
+            self.w_keys_early = self.torch.empty(shape, dtype=self.torch.int32, device="cuda")
             self.w_tiles = self.torch.empty((jr.n_w, self.plan.tile_elems[2]), dtype=self.torch.float32,
                                             device="cuda")
-        tre.contract(self.plan, jr, ut, vt, self.w_keys if self.plan.key_arity[2] else None,
-                     self.w_tiles[:jr.n_w], None, timing=timing)
         self.n_pairs, self.n_w = int(jr.n_pairs), int(jr.n_w)
+        return jr
+
+    def keys_early(self, jr, stream=None):
+        """The output keys straight after the join (tre_join_keys), in a buffer
+        of their own, for a consumer that starts before the contraction ends."""
+        self.tre.join_keys(self.plan, jr, self.w_keys_early if self.plan.key_arity[2] else None, stream=stream)
+        return self.w_keys_early[:jr.n_w]
+
+    def contract(self, jr, ut, vt, timing=None, stream=None):
+        if self.record is not None:
+            timing = self.record
+            timing.deferred = 0
+        self.tre.contract(self.plan, jr, ut, vt, self.w_keys if self.plan.key_arity[2] else None,
+                          self.w_tiles[:jr.n_w], None, stream=stream, timing=timing)
         return self.w_keys[:jr.n_w], self.w_tiles[:jr.n_w]
 
     def tile_bytes(self, op):
@@ -207,14 +224,60 @@ class GnnChain:
         self.n_t2 = w["n"] // w["tile_e2"]
         self.e2 = Stage(tre, torch, w["E2"], self.n_t2, 1, self.n_t2, "E2")
         self.t_cast = None
+        self.side = torch.cuda.Stream()  # default priority, like every stream here
         self.n_t = n_t
         self.measure_rp = False
         self.rp_report = None
         torch.cuda.synchronize()
 
     def step(self, timing=None):
+        """E1's output keys are known once its join is done, so E2's join (and
+        the key-only stack of the per-vertex rows) runs on a second stream
+        while E1's contraction runs; the cast and E2's contraction follow on
+        the first.  The synchronous phase pass, a stack that has to move
+        tiles, and an E1 on the 128x128 path take the serial order: that path
+        may run as a persistent grid that expects all of its workgroups
+        resident at once, and kernels of a second stream would take their
+        slots (measured: 13.8 instead of 12.8 ms for E1 of the 262,144-vertex
+        chain, with nothing gained for E2)."""
         tre, torch = self.tre, self.torch
+        if self.measure_rp or self.e1.record is not None or self.e2.record is not None or \
+                self.e1.plan.kernel_class == "gemm128":
+            return self._step_serial(timing)
+        w = self.w
+        main = torch.cuda.current_stream()
+        jr1 = self.e1.join(self.xk, self.yk, timing=timing, stream=main)
+        n_t = int(jr1.n_w)
+        if self.stack > 1 and n_t * w["tile_e1"] != w["n"]:
+            tk, tt = self.e1.contract(jr1, self.xt, self.yt, timing=timing, stream=main)
+            return self._step_after_e1(tk, tt)
+        tk_early = self.e1.keys_early(jr1, stream=main)
+        ready = torch.cuda.Event()
+        ready.record(main)
+        tk, tt = self.e1.contract(jr1, self.xt, self.yt, timing=timing, stream=main)
+        if self.bf and (self.t_cast is None or self.t_cast.numel() < tt.numel()):
+            self.t_cast = torch.empty(tt.numel(), dtype=torch.bfloat16, device="cuda")
+        tbuf = self.t_cast[:tt.numel()].view(tt.shape) if self.bf else tt
+        side = self.side
+        side.wait_event(ready)
+        with torch.cuda.stream(side):
+            if self.stack > 1:
+                tk2, tb2 = tre.repartition("ki", "k", "k", {"k": w["n"], "i": w["emb"]}, {"k": 1},
+                                           {"k": self.stack}, tk_early, tbuf, stream=side, in_place=True)
+            else:
+                tk2, tb2 = tk_early, tbuf
+            self.e2.n_u = int(tk2.shape[0])
+            jr2 = self.e2.join(tk2, self.zk, stream=side)
+        if self.bf:
+            tre.cast_f32_bf16(tt, out=self.t_cast[:tt.numel()], stream=main)
+        return self.e2.contract(jr2, tb2, self.zt, stream=main)
+
+    def _step_serial(self, timing=None):
         tk, tt = self.e1.run(self.xk, self.xt, self.yk, self.yt, timing=timing)
+        return self._step_after_e1(tk, tt)
+
+    def _step_after_e1(self, tk, tt):
+        tre, torch = self.tre, self.torch
         if self.bf:
             # cast first: the stack then moves half the bytes
             if self.t_cast is None or self.t_cast.numel() < tt.numel():

@@ -170,6 +170,15 @@ int64_t tre_workspace_max_pairs(tre_plan_t plan, int64_t n_u, int64_t n_v, size_
 tre_status tre_join(tre_plan_t plan, const int32_t *u_keys, int64_t n_u, const int32_t *v_keys, int64_t n_v,
                     void *ws, size_t ws_bytes, void *stream, tre_join_result *out, tre_timing *timing);
 
+/* tre_join_keys -- the output keys of a join (the GROUP BY keys of Sec. 5),
+ * before any contraction: lets a consumer EinSum start its own join on
+ * another stream while tre_contract runs.  Writes the same keys tre_contract
+ * writes.
+ *   join   : host, from tre_join with this plan; its workspace untouched since.
+ *   w_keys : device [w_cap x r_W] int32 (r_W = 0: nothing is written), sorted.
+ * Asynchronous on the stream; TRE_E_CAPACITY if w_cap < n_w. */
+tre_status tre_join_keys(tre_plan_t plan, const tre_join_result *join, int32_t *w_keys, int64_t w_cap, void *stream);
+
 /* tre_contract -- steps (2) and (3) of Sec. 5: contract every matched tile
  * pair and sum the results per output key.  Pairs of one output key are
  * processed together (split into bounded work units when long); a unit

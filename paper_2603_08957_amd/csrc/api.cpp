@@ -302,6 +302,32 @@ tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* 
     return TRE_OK;
 }
 
+tre_status tre_join_keys(tre_plan_t plan, const tre_join_result* jr, int32_t* w_keys, int64_t w_cap, void* stream) {
+    if (!plan || !jr) {
+        set_error("tre_join_keys: null plan or join result");
+        return TRE_E_ARG;
+    }
+    if (jr->internal[0] != kMagic || jr->internal[1] != reinterpret_cast<uint64_t>(plan)) {
+        set_error("tre_join_keys: join result was not produced by tre_join with this plan");
+        return TRE_E_STATE;
+    }
+    const Plan& p = plan->p;
+    if (w_cap < jr->n_w) {
+        set_error("tre_join_keys: output capacity below n_w");
+        return TRE_E_CAPACITY;
+    }
+    if (p.nk[2] == 0 || jr->n_w == 0) return TRE_OK;
+    if (!w_keys) {
+        set_error("tre_join_keys: null key buffer");
+        return TRE_E_ARG;
+    }
+    char* w = reinterpret_cast<char*>(jr->internal[2]);
+    const Layout L = make_layout(p, jr->n_u, jr->n_v, int64_t(jr->internal[4]));
+    const hipError_t e = launch_write_outputs(p, L, w, w_keys, nullptr, jr->n_pairs, jr->n_w,
+                                              reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TRE_OK : dev_fail(e, "keys");
+}
+
 tre_status tre_timing_read(tre_timing* t) {
     if (!t) return TRE_E_ARG;
     if (!t->pending) return TRE_OK;

@@ -26,7 +26,7 @@ DTYPE = {"f32": 0, "bf16": 1}
 # every symbol include/tre.h declares
 EXPORTS = [
     "tre_plan", "tre_plan_get_info", "tre_plan_destroy", "tre_workspace_bytes", "tre_workspace_max_pairs",
-    "tre_join", "tre_contract", "tre_execute", "tre_timing_read", "tre_cast_f32_bf16", "tre_scale_f32",
+    "tre_join", "tre_join_keys", "tre_contract", "tre_execute", "tre_timing_read", "tre_cast_f32_bf16", "tre_scale_f32",
     "tre_stack_workspace_bytes", "tre_stack_rows",
     "tre_tiles_from_entries", "tre_status_str", "tre_last_error", "tre_version",
     "tre_repartition_workspace_bytes", "tre_repartition", "tre_execute3_workspace_bytes", "tre_execute3",
@@ -94,6 +94,7 @@ def lib():
         L.tre_workspace_max_pairs.argtypes = [P, i64, i64, sz]
         L.tre_workspace_max_pairs.restype = i64
         L.tre_join.argtypes = [P, P, i64, P, i64, P, sz, P, P, P]
+        L.tre_join_keys.argtypes = [P, P, P, i64, P]
         L.tre_contract.argtypes = [P, P, P, P, P, i64, P, P, i64, P, P]
         L.tre_execute.argtypes = [P, P, i64, P, P, i64, P, P, P, i64, P, P, i64, P, P, sz, P, P]
         L.tre_timing_read.argtypes = [P]
@@ -214,6 +215,13 @@ def contract(plan: Plan, jr: JoinResult, u_tiles, v_tiles, w_keys, w_tiles, pair
                             _ptr(w_tiles), _ptr(pairs_out), pair_cap, _stream(stream),
                             ctypes.byref(timing) if timing is not None else None)
     _check(rc, "tre_contract")
+
+
+def join_keys(plan: Plan, jr: JoinResult, w_keys, stream=None):
+    """Write the join's output keys (tre_join_keys) into w_keys [>= n_w, r_W]."""
+    w_cap = w_keys.shape[0] if w_keys is not None else 0
+    _check(lib().tre_join_keys(plan.handle, ctypes.byref(jr), _ptr(w_keys), w_cap, _stream(stream)),
+           "tre_join_keys")
 
 
 @dataclass

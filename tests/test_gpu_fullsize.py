@@ -345,3 +345,26 @@ def test_graph_attention_full(orc):
     worst, ok = value_error(o4.w_tiles.cpu().numpy()[sel], acc, mag)
     say("attention binary", o3.n_w, worst)
     assert ok and worst <= TOL["f32"], worst
+
+
+@pytest.mark.parametrize("config", [1, 5])
+def test_bench_chain_overlap_matches_serial(config):
+    """The benchmark's chain step runs E2's join (and, for the 1,048,576-vertex
+    chain, the key-only stack) on a second stream while E1's contraction runs;
+    its result must equal the serial order's bit for bit, on every repeat."""
+    import torch
+
+    import bench
+    import paper_2603_08957_amd as tre
+
+    print(f"[chain overlap] config {config}", flush=True)
+    W = bench.GnnChain(config, tre, torch)
+    k_ref, t_ref = (x.clone() for x in W._step_serial())
+    for _ in range(3):
+        k, t = W.step()
+        torch.cuda.synchronize()
+        assert torch.equal(k, k_ref)
+        assert torch.equal(t, t_ref)
+    del W
+    gc.collect()
+    torch.cuda.empty_cache()

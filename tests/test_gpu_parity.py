@@ -553,3 +553,33 @@ def test_repartition_gpu_in_place(orc):
         assert np.array_equal(k2.cpu().numpy().reshape(rk.shape), rk)
         assert np.array_equal(t2.cpu().numpy().astype(np.float64).reshape(rt.shape), rt)
     assert accepted > 0
+
+
+def test_join_keys_gpu(orc):
+    """tre_join_keys writes, before any contraction, the keys tre_contract
+    writes; a short buffer is TRE_E_CAPACITY."""
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    rng = np.random.default_rng(31)
+    plan = tre.Plan("ij,jk->ik", "ijk", {"i": 64, "j": 64, "k": 64}, {"i": 8, "j": 8, "k": 8})
+    def rel(n_keys):
+        import itertools
+        allk = np.array(list(itertools.product(range(8), range(8))), np.int32)
+        keep = np.sort(rng.choice(len(allk), n_keys, replace=False))
+        return torch.from_numpy(allk[keep]).cuda(), torch.from_numpy(rng.standard_normal((n_keys, 64)).astype(np.float32)).cuda()
+    uk, ut = rel(40)
+    vk, vt = rel(30)
+    ws = tre.alloc_workspace(plan.workspace_bytes(40, 30, 40 * 30))
+    jr = tre.join(plan, uk, 40, vk, 30, ws)
+    early = torch.full((jr.n_w, 2), -1, dtype=torch.int32, device="cuda")
+    tre.join_keys(plan, jr, early)
+    wk = torch.empty((jr.n_w, 2), dtype=torch.int32, device="cuda")
+    wt = torch.empty((jr.n_w, 64), dtype=torch.float32, device="cuda")
+    tre.contract(plan, jr, ut, vt, wk, wt)
+    torch.cuda.synchronize()
+    assert jr.n_w > 1 and torch.equal(early, wk)
+    with pytest.raises(tre.TreError) as ei:
+        tre.join_keys(plan, jr, early[:jr.n_w - 1])
+    assert ei.value.status == "TRE_E_CAPACITY"
