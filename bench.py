@@ -502,6 +502,7 @@ class Attention:
 
         w = workloads.config(c)
         self.w, self.tre, self.torch, self.path = w, tre, torch, path
+        self.side = torch.cuda.Stream()  # default priority
         self.xk, self.xt = dev_rel(w["X"], torch)
         self.qk, self.qt = dev_rel(w["WQ"], torch)
         self.kk, self.kt = dev_rel(w["WK"], torch)
@@ -516,9 +517,23 @@ class Attention:
             self.e3 = Stage(tre, torch, w["E3"], n, na, na, "E3")
             self.e4 = Stage(tre, torch, w["E4"], na, n, na, "E4")
 
-    def step(self, timing=None):
-        t0k, t0t = self.e1.run(self.xk, self.xt, self.qk, self.qt)
-        t1k, t1t = self.e2.run(self.xk, self.xt, self.kk, self.kt)
+    def step(self, timing=None, overlap=True):
+        """E1 and E2 (the two projections) are independent: both joins first,
+        then the two contractions on two streams at once (E2's on a second
+        stream of default priority); the synchronous phase pass runs them in
+        order."""
+        torch = self.torch
+        if not overlap or self.e1.record is not None or self.e2.record is not None:
+            t0k, t0t = self.e1.run(self.xk, self.xt, self.qk, self.qt)
+            t1k, t1t = self.e2.run(self.xk, self.xt, self.kk, self.kt)
+        else:
+            main = torch.cuda.current_stream()
+            jr1 = self.e1.join(self.xk, self.qk, stream=main)
+            jr2 = self.e2.join(self.xk, self.kk, stream=main)
+            t0k, t0t = self.e1.contract(jr1, self.xt, self.qt, stream=main)
+            self.side.wait_stream(main)  # also orders E2's output after the last step's readers
+            t1k, t1t = self.e2.contract(jr2, self.xt, self.kt, stream=self.side)
+            main.wait_stream(self.side)
         if self.path == "fused":
             self.f.n_v, self.f.n_x = int(t0k.shape[0]), int(t1k.shape[0])
             wk, wt = self.f.run(self.ak, self.at, t0k, t0t, t1k, t1t, timing=timing)

@@ -368,3 +368,25 @@ def test_bench_chain_overlap_matches_serial(config):
     del W
     gc.collect()
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("path", ["fused", "binary"])
+def test_bench_attention_overlap_matches_serial(path):
+    """The attention step contracts its two projections on two streams at
+    once; the scores must equal the serial order's bit for bit."""
+    import torch
+
+    import bench
+    import paper_2603_08957_amd as tre
+
+    print(f"[attention overlap] {path}", flush=True)
+    W = bench.Attention(6, tre, torch, path=path)
+    k_ref, t_ref = (x.clone() for x in W.step(overlap=False))
+    for _ in range(3):
+        k, t = W.step()
+        torch.cuda.synchronize()
+        assert torch.equal(k, k_ref)
+        assert torch.equal(t, t_ref)
+    del W
+    gc.collect()
+    torch.cuda.empty_cache()
