@@ -171,6 +171,43 @@ tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const i
             return dev_fail(e, "validate V");
     }
     WsHeader h{};
+    if (n_u > 0 && n_v == 1 && keyed_by_u(p)) {
+        // one pair and one group per U tuple: nothing to count, and with key
+        // validation off nothing to wait for
+        if (n_u > max_pairs) {
+            out->n_pairs = n_u;
+            set_error("tre_join: workspace too small for the matched pairs (see n_pairs)");
+            return TRE_E_WORKSPACE;
+        }
+        if ((e = launch_keyed_by_u(p, L, w, u_keys, s)) != hipSuccess) return dev_fail(e, "join");
+        if (p.opt.validate_keys) {
+            if ((e = hipMemcpyAsync(&h, hdr, sizeof(h), hipMemcpyDeviceToHost, s)) != hipSuccess)
+                return dev_fail(e, "key check read-back");
+            if ((e = hipStreamSynchronize(s)) != hipSuccess) return dev_fail(e, "join sync");
+            tre_status ks = key_error(h.err_u);
+            if (ks == TRE_OK) ks = key_error(h.err_v);
+            if (ks != TRE_OK) {
+                set_error(std::string("tre_join: invalid keys in ") + (key_error(h.err_u) != TRE_OK ? "U" : "V"));
+                return ks;
+            }
+        }
+        tm.mark(s);
+        out->n_pairs = n_u;
+        out->n_w = n_u;
+        out->internal[0] = kMagic;
+        out->internal[1] = reinterpret_cast<uint64_t>(plan);
+        out->internal[2] = reinterpret_cast<uint64_t>(ws);
+        out->internal[3] = uint64_t(ws_bytes);
+        out->internal[4] = uint64_t(max_pairs);
+        if (timing) {
+            const int32_t deferred = timing->deferred;
+            std::memset(timing, 0, sizeof(*timing));
+            timing->deferred = deferred;
+            timing->join_ms = tm.between(0, 1);
+            timing->total_ms = timing->join_ms;
+        }
+        return TRE_OK;
+    }
     if (n_u > 0 && n_v > 0) {
         if ((e = launch_join(p, L, w, u_keys, v_keys, s, 0)) != hipSuccess) return dev_fail(e, "join");
     }

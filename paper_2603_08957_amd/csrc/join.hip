@@ -297,6 +297,26 @@ __global__ __launch_bounds__(kThreads) void k_expand(const int64_t* __restrict__
     }
 }
 
+// Join with a keyless single-tuple V whose output is keyed by U's own key
+// (e.g. T keyed k times a whole weight matrix): every U tuple is one pair and
+// its own group, in U order, so the pair list and the segments are written
+// directly and the counts are known on the host.
+__global__ void k_keyed_by_u(const int32_t* __restrict__ ukeys, int64_t n_u, int ru, WDesc wd,
+                             int32_t* __restrict__ pu, int32_t* __restrict__ pv, int32_t* __restrict__ seg_start,
+                             uint64_t* __restrict__ seg_key, WsHeader* __restrict__ hdr) {
+    const int64_t u = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (u > n_u) return;
+    seg_start[u] = int32_t(u);
+    if (u == n_u) {
+        hdr->n_pairs = n_u;
+        hdr->n_w = n_u;
+        return;
+    }
+    pu[u] = int32_t(u);
+    pv[u] = 0;
+    seg_key[u] = pack_w(ukeys + u * ru, ukeys + u * ru, wd);
+}
+
 // Segments over a small key space (2^bits <= pairs): first[k] = 1 + the
 // index of key k's first pair (0: absent), then the present keys are
 // compacted in key order by a scan over the key space instead of over the
@@ -494,6 +514,28 @@ hipError_t group_impl(const Plan& p, const Layout& L, char* ws, const int32_t* u
 }
 
 }  // namespace
+
+bool keyed_by_u(const Plan& p) {
+    if (p.nk[1] != 0 || p.nk[2] != p.nk[0]) return false;
+    for (int c = 0; c < p.nk[2]; c++)
+        if (p.w_src[c] != 0 || p.w_pos[c] != c) return false;
+    return true;
+}
+
+hipError_t launch_keyed_by_u(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, hipStream_t s) {
+    WDesc wd{};
+    wd.n = p.nk[2];
+    for (int c = 0; c < p.nk[2]; c++) {
+        wd.src[c] = 0;
+        wd.pos[c] = c;
+        wd.bits[c] = p.w_bits[c];
+    }
+    k_keyed_by_u<<<blocks_for(L.n_u + 1), kThreads, 0, s>>>(
+        u_keys, L.n_u, p.nk[0], wd, reinterpret_cast<int32_t*>(ws + L.pu), reinterpret_cast<int32_t*>(ws + L.pv),
+        reinterpret_cast<int32_t*>(ws + L.seg_start), reinterpret_cast<uint64_t*>(ws + L.seg_key),
+        reinterpret_cast<WsHeader*>(ws + L.hdr));
+    return hipGetLastError();
+}
 
 hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
                         int64_t n_pairs, hipStream_t s, int stage) {

@@ -145,6 +145,10 @@ hipError_t launch_validate(const int32_t* keys, int64_t n, int r, const int32_t*
                            hipStream_t s);
 hipError_t launch_join(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
                        hipStream_t s, int stage);
+// V without promoted labels (one tuple) and W keyed by U's key as it is:
+// every U tuple is one pair and one group, written without counting
+bool keyed_by_u(const Plan& p);
+hipError_t launch_keyed_by_u(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, hipStream_t s);
 hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
                         int64_t n_pairs, hipStream_t s, int stage);
 

@@ -583,3 +583,41 @@ def test_join_keys_gpu(orc):
     with pytest.raises(tre.TreError) as ei:
         tre.join_keys(plan, jr, early[:jr.n_w - 1])
     assert ei.value.status == "TRE_E_CAPACITY"
+
+
+@pytest.mark.parametrize("validate", [True, False])
+def test_join_keyed_by_u_gpu(orc, validate):
+    """A keyless one-tuple V with W keyed by U's key (the chains' E2,
+    T keyed k times the whole Z): pairs are (u, 0) in U order and W's keys
+    are U's; values against the oracle.  With validation, a repeated U key is
+    still reported."""
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    rng = np.random.default_rng(8)
+    ext = {"k": 4096, "i": 64, "m": 32}
+    til = {"k": 64}
+    keys = np.sort(rng.choice(64, 40, replace=False)).astype(np.int32).reshape(-1, 1)
+    ut = rng.standard_normal((40, 64 * 64)).astype(np.float32)
+    vt = rng.standard_normal((1, 64 * 32)).astype(np.float32)
+    plan = tre.Plan("ki,im->km", "k", ext, til, validate=validate)
+    out = tre.einsum(plan, torch.from_numpy(keys).cuda(), torch.from_numpy(ut).cuda(),
+                     torch.zeros((1, 0), dtype=torch.int32).cuda(), torch.from_numpy(vt).cuda(), want_pairs=True)
+    assert out.n_pairs == 40 and out.n_w == 40
+    assert np.array_equal(out.w_keys.cpu().numpy(), keys)
+    pairs = out.pairs.cpu().numpy()
+    assert np.array_equal(pairs[:, 0], np.arange(40)) and not pairs[:, 1].any()
+    op = orc.Plan("ki,im->km", "k", ext, til)
+    uc, uv, _ = orc.expand(op, 0, keys, ut, "f32")
+    vc, vv, _ = orc.expand(op, 1, np.zeros((1, 0), np.int32), vt, "f32")
+    acc, mag, _ = orc.evaluate(op, uc, uv, vc, vv, keys)
+    err, zeros_ok = value_error(out.w_tiles.cpu().numpy().reshape(acc.shape), acc, mag)
+    assert err <= TOL["f32"] and zeros_ok, err
+    if validate:
+        bad = keys.copy()
+        bad[5] = bad[4]
+        with pytest.raises(tre.TreError) as ei:
+            tre.einsum(plan, torch.from_numpy(bad).cuda(), torch.from_numpy(ut).cuda(),
+                       torch.zeros((1, 0), dtype=torch.int32).cuda(), torch.from_numpy(vt).cuda())
+        assert ei.value.status == "TRE_E_DUPKEY"
