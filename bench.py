@@ -931,7 +931,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (the path shards by output key "
-              f"across GPUs by design, but this build runs on a single MI355X)", file=sys.stderr)
+              f"across GPUs by design; this library runs the one-GPU share on a single MI355X)", file=sys.stderr)
         sys.exit(2)
 
     import torch
