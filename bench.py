@@ -392,7 +392,8 @@ class BlockSparse:
         return {"workload": f"block-sparse A.B, fp32: A {w['n']}x{w['n']} with 5% of {w['block']}x{w['block']} "
                             f"blocks, B {w['n']}x{w['n_cols']}", "a_blocks": len(w["A"]["keys"])}
 
-    def oracle_sample(self, orc, n_keys=2):
+    def oracle_sample(self, orc, n_keys=20):
+        """The oracle on the first n_keys output row blocks (about 10 s)."""
         w = self.w
         p = orc.Plan(w["E"]["einsum"], w["E"]["upper"], w["E"]["extents"], w["E"]["tiles"])
         S = np.unique(w["A"]["keys"][:, 0])[:n_keys].reshape(-1, 1).astype(np.int32)
