@@ -52,9 +52,9 @@ def dev_rel(rel, torch):
 class Stage:
     """One binary EinSum with preallocated workspace and outputs."""
 
-    def __init__(self, tre, torch, spec, n_u, n_v, n_pairs, name):
+    def __init__(self, tre, torch, spec, n_u, n_v, n_pairs, name, w_bf16=False):
         self.tre, self.torch, self.name = tre, torch, name
-        self.plan = tre.Plan.from_spec(spec, validate=False, **PLAN_OPTIONS)
+        self.plan = tre.Plan.from_spec(spec, validate=False, w_bf16=w_bf16, **PLAN_OPTIONS)
         self.spec = spec
         self.ws = tre.alloc_workspace(self.plan.workspace_bytes(n_u, n_v, n_pairs))
         self.n_u, self.n_v = n_u, n_v
@@ -97,7 +97,8 @@ class Stage:
             shape = (jr.n_w, max(self.plan.key_arity[2], 1))
             self.w_keys = self.torch.empty(shape, dtype=self.torch.int32, device="cuda")
             self.w_keys_early = self.torch.empty(shape, dtype=self.torch.int32, device="cuda")
-            self.w_tiles = self.torch.empty((jr.n_w, self.plan.tile_elems[2]), dtype=self.torch.float32,
+            self.w_tiles = self.torch.empty((jr.n_w, self.plan.tile_elems[2]),
+                                            dtype=self.torch.bfloat16 if self.plan.w_bf16 else self.torch.float32,
                                             device="cuda")
         self.n_pairs, self.n_w = int(jr.n_pairs), int(jr.n_w)
         return jr
@@ -118,7 +119,7 @@ class Stage:
 
     def tile_bytes(self, op):
         eb = 2 if self.spec["dtype"] == "bf16" else 4
-        return self.plan.tile_elems[op] * (4 if op == 2 else eb)
+        return self.plan.tile_elems[op] * ((2 if self.plan.w_bf16 else 4) if op == 2 else eb)
 
     def flops(self):
         return self.n_pairs * self.plan.flops_per_pair
@@ -216,10 +217,12 @@ class GnnChain:
         self.zk, self.zt = dev_rel(w["Z"], torch)
         nY = len(Y["keys"])
         nX = len(w["X"]["keys"])
-        self.e1 = Stage(tre, torch, w["E1"], nX, nY, nY, "E1")
+        self.bf = w["dtype"] == "bf16"
+        # a bf16 chain's E1 writes T as bf16 straight from its fp32 sums (the
+        # bits the cast would give), so no cast pass runs between the EinSums
+        self.e1 = Stage(tre, torch, w["E1"], nX, nY, nY, "E1", w_bf16=self.bf)
         n_t = w["n"] // w["tile_e1"]
         self.e2 = None
-        self.bf = w["dtype"] == "bf16"
         self.stack = w["tile_e2"] // w["tile_e1"]
         self.n_t2 = w["n"] // w["tile_e2"]
         self.e2 = Stage(tre, torch, w["E2"], self.n_t2, 1, self.n_t2, "E2")
@@ -255,9 +258,10 @@ class GnnChain:
         ready = torch.cuda.Event()
         ready.record(main)
         tk, tt = self.e1.contract(jr1, self.xt, self.yt, timing=timing, stream=main)
-        if self.bf and (self.t_cast is None or self.t_cast.numel() < tt.numel()):
+        cast = self.bf and tt.dtype != torch.bfloat16
+        if cast and (self.t_cast is None or self.t_cast.numel() < tt.numel()):
             self.t_cast = torch.empty(tt.numel(), dtype=torch.bfloat16, device="cuda")
-        tbuf = self.t_cast[:tt.numel()].view(tt.shape) if self.bf else tt
+        tbuf = self.t_cast[:tt.numel()].view(tt.shape) if cast else tt
         side = self.side
         side.wait_event(ready)
         with torch.cuda.stream(side):
@@ -268,7 +272,7 @@ class GnnChain:
                 tk2, tb2 = tk_early, tbuf
             self.e2.n_u = int(tk2.shape[0])
             jr2 = self.e2.join(tk2, self.zk, stream=side)
-        if self.bf:
+        if cast:
             tre.cast_f32_bf16(tt, out=self.t_cast[:tt.numel()], stream=main)
         return self.e2.contract(jr2, tb2, self.zt, stream=main)
 
@@ -278,7 +282,7 @@ class GnnChain:
 
     def _step_after_e1(self, tk, tt):
         tre, torch = self.tre, self.torch
-        if self.bf:
+        if self.bf and tt.dtype != torch.bfloat16:
             # cast first: the stack then moves half the bytes
             if self.t_cast is None or self.t_cast.numel() < tt.numel():
                 self.t_cast = torch.empty(tt.numel(), dtype=torch.bfloat16, device="cuda")

@@ -82,7 +82,12 @@ typedef struct {
                                    index range is cut into this many windows), so U tiles stay in L2 with
                                    no partial tiles; 0 = automatic (preferred over u_ranges when both
                                    apply), < 0 = never.  Results do not depend on it. */
-    int32_t reserved[4];
+    int32_t w_bf16;             /* nonzero: tre_contract writes W as bf16 (round to nearest even from the
+                                   fp32 sum; the bits tre_cast_f32_bf16 gives) instead of fp32, for a
+                                   consumer that reads bf16: the producer writes half the bytes and no
+                                   cast pass runs.  Vector class and 128x128 path only (TRE_E_DTYPE in
+                                   tre_plan otherwise). */
+    int32_t reserved[3];
 } tre_options;
 
 /* Static facts about a plan (host). */

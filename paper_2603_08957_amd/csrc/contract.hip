@@ -441,8 +441,9 @@ struct VecArgs {
     int32_t upb;  // units per block
     const Unit* units;
     const WsHeader* hdr;
-    float* W;
+    float* W;  // bf16 bits when w_bf16 (partials stay fp32)
     float* partials;
+    int32_t w_bf16;
 };
 
 constexpr int kVecMaxK = 2048;
@@ -525,6 +526,24 @@ __global__ __launch_bounds__(kThreads) void k_vec(VecArgs a) {
 #pragma unroll 4
         for (int k = 0; k < a.K; k++) pair_step(ub, vb, k);
     }
+    if (a.w_bf16 && un.slot < 0) {
+        uint16_t* o = reinterpret_cast<uint16_t*>(a.W) + int64_t(un.seg) * a.w_elems + e0;
+        if constexpr (EPT % 4 == 0) {
+#pragma unroll
+            for (int i = 0; i < EPT; i += 4) {
+                ushort4 v;
+                v.x = f32_to_bf16_rne(acc[i]);
+                v.y = f32_to_bf16_rne(acc[i + 1]);
+                v.z = f32_to_bf16_rne(acc[i + 2]);
+                v.w = f32_to_bf16_rne(acc[i + 3]);
+                *reinterpret_cast<ushort4*>(o + i) = v;
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < EPT; i++) o[i] = f32_to_bf16_rne(acc[i]);
+        }
+        return;
+    }
     float* out = un.slot < 0 ? a.W + int64_t(un.seg) * a.w_elems : a.partials + int64_t(un.slot) * a.w_elems;
     if constexpr (EPT == 1) {
         out[e0] = acc[0];
@@ -552,12 +571,12 @@ hipError_t vec_dispatch(const Plan& p, const VecArgs& a, dim3 grid, hipStream_t 
 
 __global__ __launch_bounds__(kThreads) void k_reduce(const int32_t* __restrict__ split, const WsHeader* hdr,
                                                      const int32_t* __restrict__ poff, const float* __restrict__ parts,
-                                                     float* __restrict__ W, int64_t w_elems) {
+                                                     float* __restrict__ W, int64_t w_elems, int32_t w_bf16) {
     const int64_t x = blockIdx.x;
     if (x >= hdr->n_split) return;
     const int32_t s = split[x];
     const int32_t first = poff[s], cnt = poff[s + 1] - poff[s];
-    if (w_elems % 4 == 0) {
+    if (w_elems % 4 == 0 && !w_bf16) {
         // 16-byte lanes; partials are read once, so they bypass L2 retention
         const int64_t q = w_elems / 4;
         for (int64_t e = int64_t(blockIdx.y) * kThreads + threadIdx.x; e < q; e += int64_t(gridDim.y) * kThreads) {
@@ -571,7 +590,8 @@ __global__ __launch_bounds__(kThreads) void k_reduce(const int32_t* __restrict__
     for (int64_t e = int64_t(blockIdx.y) * kThreads + threadIdx.x; e < w_elems; e += int64_t(gridDim.y) * kThreads) {
         float acc = 0.f;
         for (int j = 0; j < cnt; j++) acc += parts[int64_t(first + j) * w_elems + e];
-        W[int64_t(s) * w_elems + e] = acc;
+        if (w_bf16) reinterpret_cast<uint16_t*>(W)[int64_t(s) * w_elems + e] = f32_to_bf16_rne(acc);
+        else W[int64_t(s) * w_elems + e] = acc;
     }
 }
 
@@ -776,6 +796,7 @@ hipError_t launch_contract(const Plan& p, const Layout& L, char* ws, const void*
     a.hdr = hdr;
     a.W = w_tiles;
     a.partials = parts;
+    a.w_bf16 = p.opt.w_bf16;
     const int ept = p.vec_ept;
     const int64_t threads = (p.tile_elems[2] + ept - 1) / ept;
     dim3 grid;
@@ -807,7 +828,7 @@ hipError_t launch_reduce(const Plan& p, const Layout& L, char* ws, float* w_tile
     k_reduce<<<dim3(unsigned(split_bound), gy), kThreads, 0, s>>>(
         reinterpret_cast<const int32_t*>(ws + L.split_list), reinterpret_cast<const WsHeader*>(ws + L.hdr),
         reinterpret_cast<const int32_t*>(ws + L.part_off), reinterpret_cast<const float*>(ws + L.partials), w_tiles,
-        we);
+        we, p.opt.w_bf16);
     return hipGetLastError();
 }
 

@@ -66,8 +66,9 @@ struct FastArgs {
     int64_t n_r;
     const Unit* units;
     const WsHeader* hdr;
-    float* W;
+    float* W;  // bf16 bits when w_bf16 (partials stay fp32)
     float* partials;
+    int32_t w_bf16;
 };
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
@@ -333,9 +334,14 @@ __device__ inline void run_unit(const FastArgs& g, const Unit& un, int m0, int n
     const int tpp = g.K / kTickK<T>;  // ticks per pair
     const int ticks = np * tpp;
     float* out = un.slot < 0 ? g.W + int64_t(un.seg) * g.w_elems : g.partials + int64_t(un.slot) * g.w_elems;
+    uint16_t* out16 = (g.w_bf16 && un.slot < 0) ? reinterpret_cast<uint16_t*>(g.W) + int64_t(un.seg) * g.w_elems
+                                                 : nullptr;
     if (ticks == 0) {
-        for (int e = threadIdx.x; e < kB * kB; e += kThreads)
-            out[int64_t(m0 + e / kB) * g.ldw + n0 + e % kB] = 0.f;
+        for (int e = threadIdx.x; e < kB * kB; e += kThreads) {
+            const int64_t o = int64_t(m0 + e / kB) * g.ldw + n0 + e % kB;
+            if (out16) out16[o] = 0;
+            else out[o] = 0.f;
+        }
         pc.at_end();
         return;
     }
@@ -439,7 +445,8 @@ __device__ inline void run_unit(const FastArgs& g, const Unit& un, int m0, int n
 #pragma unroll
             for (int r = 0; r < 16; r++) {
                 const int m = m0 + wm * 64 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-                out[int64_t(m) * g.ldw + n] = acc[i][j][r];
+                if (out16) out16[int64_t(m) * g.ldw + n] = f32_to_bf16_rne(acc[i][j][r]);
+                else out[int64_t(m) * g.ldw + n] = acc[i][j][r];
             }
         }
 }
@@ -522,6 +529,7 @@ FastArgs fast_args(const Plan& p, const Layout& L, char* ws, const void* u_tiles
     g.hdr = reinterpret_cast<const WsHeader*>(ws + L.hdr);
     g.W = w_tiles;
     g.partials = reinterpret_cast<float*>(ws + L.partials);
+    g.w_bf16 = p.opt.w_bf16;
     return g;
 }
 

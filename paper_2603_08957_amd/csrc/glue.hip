@@ -18,13 +18,6 @@ inline unsigned grid_for(int64_t n, int64_t per_thread = 1) {
     return unsigned(std::max<int64_t>(1, std::min<int64_t>(b, int64_t(1) << 20)));
 }
 
-__device__ inline uint16_t f32_to_bf16_rne(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return uint16_t((u >> 16) | 0x40u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return uint16_t(u >> 16);
-}
-
 __global__ void k_cast(const float* __restrict__ x, uint16_t* __restrict__ y, int64_t n) {
     const int64_t stride = int64_t(gridDim.x) * kThreads * 4;
     for (int64_t i = (int64_t(blockIdx.x) * kThreads + threadIdx.x) * 4; i < n; i += stride) {

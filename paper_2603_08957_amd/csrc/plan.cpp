@@ -466,6 +466,10 @@ tre_status tre_plan(const char* einsum, const char* upper, const int64_t* extent
     }
     tre_status st = parse(p, einsum, upper, extent, tile);
     if (st == TRE_OK) st = classify(p);
+    if (st == TRE_OK && p.opt.w_bf16 && p.kclass == KC_GEMM && !p.fast) {
+        set_error("w_bf16: bf16 output is written by the vector class and the 128x128 path only");
+        st = TRE_E_DTYPE;
+    }
     if (st != TRE_OK) {
         delete h;
         return st;

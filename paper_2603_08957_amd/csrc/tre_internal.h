@@ -11,6 +11,15 @@
 
 namespace tre {
 
+// fp32 -> bf16 bits, round to nearest even, NaN kept quiet (the cast glue and
+// the bf16 output of tre_contract)
+__device__ inline uint16_t f32_to_bf16_rne(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return uint16_t((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return uint16_t(u >> 16);
+}
+
 constexpr int kMaxDims = 8;
 constexpr int kMaxURanges = 64;
 constexpr int64_t kPaceCounters = int64_t(1) << 20;  // int32 pacing counters in the workspace

@@ -42,8 +42,8 @@ class TreError(RuntimeError):
 
 class Options(ctypes.Structure):
     _fields_ = [("validate_keys", ctypes.c_int32), ("max_pairs_per_unit", ctypes.c_int32),
-                ("u_ranges", ctypes.c_int32), ("pace_windows", ctypes.c_int32),
-                ("reserved", ctypes.c_int32 * 4)]
+                ("u_ranges", ctypes.c_int32), ("pace_windows", ctypes.c_int32), ("w_bf16", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 3)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -142,7 +142,8 @@ class Plan:
     """A parsed, classified binary EinSum (host object, see tre_plan)."""
 
     def __init__(self, einsum: str, upper: str, extents: dict, tiles: dict, dtype: str = "f32",
-                 validate: bool = True, max_pairs_per_unit: int = 0, u_ranges: int = 0, pace_windows: int = 0):
+                 validate: bool = True, max_pairs_per_unit: int = 0, u_ranges: int = 0, pace_windows: int = 0,
+                 w_bf16: bool = False):
         L = lib()
         ext = np.zeros(26, dtype=np.int64)
         til = np.ones(26, dtype=np.int32)
@@ -150,7 +151,8 @@ class Plan:
             ext[ord(k) - 97] = v
         for k, v in (tiles or {}).items():
             til[ord(k) - 97] = v
-        opt = Options(int(validate), int(max_pairs_per_unit), int(u_ranges), int(pace_windows))
+        opt = Options(int(validate), int(max_pairs_per_unit), int(u_ranges), int(pace_windows), int(w_bf16))
+        self.w_bf16 = bool(w_bf16)
         h = ctypes.c_void_p(0)
         rc = L.tre_plan(einsum.encode(), upper.encode(), ext.ctypes.data_as(ctypes.c_void_p),
                         til.ctypes.data_as(ctypes.c_void_p), DTYPE[dtype], ctypes.byref(opt), ctypes.byref(h))
@@ -257,7 +259,8 @@ def einsum(plan: Plan, u_keys, u_tiles, v_keys, v_tiles, want_pairs: bool = Fals
     n_w, n_p = int(jr.n_w), int(jr.n_pairs)
     rw = plan.key_arity[2]
     w_keys = torch.empty((n_w, rw), dtype=torch.int32, device=dev)
-    w_tiles = torch.empty((n_w, plan.tile_elems[2]), dtype=torch.float32, device=dev)
+    w_tiles = torch.empty((n_w, plan.tile_elems[2]), dtype=torch.bfloat16 if plan.w_bf16 else torch.float32,
+                          device=dev)
     pairs = torch.empty((n_p, 2), dtype=torch.int32, device=dev) if want_pairs else None
     contract(plan, jr, u_tiles, v_tiles, w_keys if rw > 0 else None, w_tiles, pairs, stream, tm)
     return Output(w_keys, w_tiles, pairs, n_p, n_w, tm.as_dict() if tm is not None else None, ws)

@@ -621,3 +621,51 @@ def test_join_keyed_by_u_gpu(orc, validate):
             tre.einsum(plan, torch.from_numpy(bad).cuda(), torch.from_numpy(ut).cuda(),
                        torch.zeros((1, 0), dtype=torch.int32).cuda(), torch.from_numpy(vt).cuda())
         assert ei.value.status == "TRE_E_DUPKEY"
+
+
+def _rand_rel(rng, grid, tile_elems, keep, dtype):
+    import itertools
+
+    import torch
+
+    allk = np.array(list(itertools.product(*[range(g) for g in grid])), np.int32).reshape(-1, len(grid))
+    keys = allk[rng.random(len(allk)) < keep]
+    vals = torch.from_numpy(rng.standard_normal((len(keys), tile_elems)).astype(np.float32))
+    return torch.from_numpy(np.ascontiguousarray(keys)).cuda(), vals.to(dtype).cuda()
+
+
+@pytest.mark.parametrize("case", ["vec", "vec_split", "fast", "fast_split", "fast_ranges"])
+def test_w_bf16_gpu(case):
+    """W written as bf16 by the vector class, the 128x128 path, and the
+    partial-tile sum of split keys is bit for bit the bf16 cast of the fp32
+    result of the same plan; the generic GEMM class refuses the option."""
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    rng = np.random.default_rng(["vec", "vec_split", "fast", "fast_split", "fast_ranges"].index(case) + 60)
+    if case.startswith("vec"):
+        spec = ("ij,jk->ki", "jk", {"i": 64, "j": 300, "k": 300}, {"j": 1, "k": 1})
+        uk, ut = _rand_rel(rng, [300], 64, 1.0, torch.bfloat16)
+        vk, vt = _rand_rel(rng, [300, 300], 1, 0.05, torch.bfloat16)
+    else:
+        spec = ("ik,kj->ij", "ijk", {"i": 512, "j": 512, "k": 2048}, {"i": 128, "j": 128, "k": 128})
+        uk, ut = _rand_rel(rng, [4, 16], 128 * 128, 0.5, torch.bfloat16)
+        vk, vt = _rand_rel(rng, [16, 4], 128 * 128, 0.5, torch.bfloat16)
+    opts = {"max_pairs_per_unit": 3} if case.endswith("split") else {"u_ranges": 2} if case.endswith("ranges") else {}
+    say("w_bf16", case, opts)
+    p32 = tre.Plan(*spec, dtype="bf16", **opts)
+    p16 = tre.Plan(*spec, dtype="bf16", w_bf16=True, **opts)
+    assert p16.kernel_class == ("vec" if case.startswith("vec") else "gemm128")
+    o32 = tre.einsum(p32, uk, ut, vk, vt)
+    o16 = tre.einsum(p16, uk, ut, vk, vt)
+    torch.cuda.synchronize()
+    assert o16.w_tiles.dtype == torch.bfloat16 and o16.n_w == o32.n_w and o32.n_w > 1
+    assert torch.equal(o16.w_keys, o32.w_keys)
+    ref = tre.cast_f32_bf16(o32.w_tiles)
+    assert torch.equal(o16.w_tiles.view(torch.int16), ref.view(torch.int16))
+    generic = ("ij,jk->ki", "jk", {"i": 64, "j": 4096, "k": 4096}, {"j": 64, "k": 64})
+    assert tre.Plan(*generic).kernel_class == "gemm"
+    with pytest.raises(tre.TreError) as ei:
+        tre.Plan(*generic, w_bf16=True)
+    assert ei.value.status == "TRE_E_DTYPE"
