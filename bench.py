@@ -799,7 +799,7 @@ def planner_check(tre, torch, config, top, steps):
     prog = pl.Program({"X": dense_stats(pl, X, "ij", tl), "Y": coo_stats(pl, yc, "jk", {"j": n, "k": n}, eb, tl),
                        "Z": dense_stats(pl, Z, "im")},
                       [pl.EinSum("E1", "ij,jk->ki", "X", "Y"), pl.EinSum("E2", "ki,im->km", "E1", "Z")])
-    costs = pl.Costs.mi355x(dt, c_fixed=c_fixed, max_call_bytes=cap, c_call=c_call)
+    costs = pl.Costs.mi355x(dt, c_fixed=c_fixed, max_call_bytes=cap, c_call=c_call, c_block=pl.Costs.block_rate(dt))
     ranked = pl.optimize(prog, costs, k=64)
     picks = list(range(min(top, len(ranked))))
     rest = list(range(len(picks), len(ranked)))
@@ -894,7 +894,7 @@ def planner_check(tre, torch, config, top, steps):
     name = f"{dt} GNN chain ({n} vertices)"
     return {"metric": f"planner ranking: estimated vs measured step time of the {name}, 1 MI355X",
             "config": config, "c_fixed_s": c_fixed, "c_xfer_s_per_byte": costs.c_xfer, "c_flop_s": costs.c_flop,
-            "c_call_s": c_call, "max_call_bytes": cap, "feasible_plans": len(ranked), "plans": out,
+            "c_call_s": c_call, "c_block_s": costs.c_block, "max_call_bytes": cap, "feasible_plans": len(ranked), "plans": out,
             "not_run": skipped,
             "spearman_estimated_vs_measured": float(spearmanr(order_est, order_meas)[0]) if len(out) > 2 else None,
             "measured_best_is_estimated_best": bool(out and int(np.argmin(order_meas)) == 0 and out[0]["rank"] == 1),

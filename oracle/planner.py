@@ -150,7 +150,11 @@ def einsum_cost(tu, tv, tw, prom, p):
     t_agg = min(0.5 * t_join, groups)
     c_add = tile_elems(tw, prom) * p["c_flop"]
     c_agg = (t_join - t_agg) * (row_bytes(tw, prom) * p["c_xfer"] + c_add + p["c_fixed"])
-    return c_join + c_agg + p.get("c_call", 0.0)
+    # added term: one pair's kernel flops over the 64 x 64 blocks of a W tile,
+    # at the rate c_block of one workgroup (0 unless given)
+    blocks = max(1.0, tile_elems(tw, prom) / 4096.0)
+    span = p.get("c_block", 0.0) * 2 * dem / blocks if t_join > 0 else 0.0
+    return c_join + c_agg + p.get("c_call", 0.0) + span
 
 
 def repart(t, p_in, p_out, p):

@@ -92,14 +92,22 @@ class Costs:
     c_fixed: float
     max_call_bytes: float = math.inf
     c_call: float = 0.0
+    c_block: float = 0.0  # seconds per flop of one workgroup (a 64 x 64 block of a W tile)
 
     @classmethod
     def mi355x(cls, dtype: str = "f32", c_fixed: float = 2e-10, max_call_bytes: float = math.inf,
-               c_call: float = 0.0) -> "Costs":
+               c_call: float = 0.0, c_block: float = 0.0) -> "Costs":
         """c_xfer from the HBM bandwidth, c_flop from the dense peak of the
         kernel's input type, c_fixed a measured per-tuple overhead, c_call a
-        measured per-call latency."""
-        return cls(1.0 / PEAK_HBM_BYTES_S, 1.0 / PEAK_FLOPS[dtype], c_fixed, max_call_bytes, c_call)
+        measured per-call latency, c_block the time per flop of one of the
+        two workgroups sharing a CU (2 x 256 / the dense peak on MI355X, see
+        block_rate)."""
+        return cls(1.0 / PEAK_HBM_BYTES_S, 1.0 / PEAK_FLOPS[dtype], c_fixed, max_call_bytes, c_call, c_block)
+
+    @staticmethod
+    def block_rate(dtype: str = "f32", cus: int = 256) -> float:
+        """c_block for MI355X: one of two resident workgroups of one CU."""
+        return 2.0 * cus / PEAK_FLOPS[dtype]
 
 
 @dataclass
@@ -225,7 +233,10 @@ def local_cost(su: Stats, sv: Stats, sw: Stats, P: dict, c: Costs) -> float:
     t_agg = min(t_join / 2.0, groups)
     add = tile_bytes(sw, pw) / sw.elem_bytes  # elements of a W tile
     c_agg = (t_join - t_agg) * (tuple_bytes(sw, pw) * c.c_xfer + add * c.c_flop + c.c_fixed)
-    return c_join + c_agg + c.c_call
+    # the span: one pair's kernel is the smallest piece of work, shared by the
+    # workgroups of its W tile's 64 x 64 blocks (an added term, 0 = the paper)
+    span = c.c_block * flops / max(1.0, add / 4096.0) if t_join > 0 else 0.0
+    return c_join + c_agg + c.c_call + span
 
 
 def repart_cost(st: Stats, p_in: dict, p_out: dict, c: Costs) -> float:

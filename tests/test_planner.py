@@ -16,8 +16,9 @@ import workloads
 from oracle import planner as op
 
 
-def _costs(c_xfer=1e-12, c_flop=1e-14, c_fixed=1e-9, cap=math.inf, c_call=0.0):
-    return {"c_xfer": c_xfer, "c_flop": c_flop, "c_fixed": c_fixed, "max_call_bytes": cap, "c_call": c_call}
+def _costs(c_xfer=1e-12, c_flop=1e-14, c_fixed=1e-9, cap=math.inf, c_call=0.0, c_block=0.0):
+    return {"c_xfer": c_xfer, "c_flop": c_flop, "c_fixed": c_fixed, "max_call_bytes": cap, "c_call": c_call,
+            "c_block": c_block}
 
 
 # ------------------------------------------------------------- oracle pins
@@ -119,6 +120,30 @@ def test_per_call_latency():
     assert op.repart(tw, {"i"}, {"k"}, _costs(c_call=7.0)) == pytest.approx(r + 7.0, rel=1e-12)
 
 
+def test_span_term_hand_count():
+    """The added span term: one pair's kernel flops over the 64 x 64 blocks
+    of its W tile, times c_block; none without pairs.  Here U [i 128][j 32]
+    and V [j 32][k 256] dense, nothing promoted: one pair, 2*128*32*256 flops,
+    a W tile of 128 x 256 = 8 blocks; with j promoted at a tile of 8 there are
+    4 pairs of 2*128*8*256 flops and the same 8 blocks."""
+    from paper_2603_08957_amd import planner as pl
+
+    tu = dict(_dense_stats("ij", {"i": 128, "j": 32}), tiled={"j": {8: 4}})
+    tv = dict(_dense_stats("jk", {"j": 32, "k": 256}), tiled={"j": {8: 4}})
+    tw = op.derive("ij", "jk", "ik", tu, tv)
+    su = pl.Stats("ij", tu["extents"], tu["nnz"], tu["distinct"], tu["elem_bytes"], tu["tiled"])
+    sv = pl.Stats("jk", tv["extents"], tv["nnz"], tv["distinct"], tv["elem_bytes"], tv["tiled"])
+    sw = pl.result_stats(su, sv, pl.EinSum("E", "ij,jk->ik", "U", "V"), 4)
+    for prom, flops in (({}, 2 * 128 * 32 * 256), ({"j": 8}, 2 * 128 * 8 * 256)):
+        base = op.einsum_cost(tu, tv, tw, prom, _costs())
+        got = op.einsum_cost(tu, tv, tw, prom, _costs(c_block=1e-9))
+        assert got - base == pytest.approx(1e-9 * flops / 8, rel=1e-12)
+        c0 = pl.local_cost(su, sv, sw, prom, pl.Costs(1e-12, 1e-14, 1e-9))
+        c1 = pl.local_cost(su, sv, sw, prom, pl.Costs(1e-12, 1e-14, 1e-9, c_block=1e-9))
+        assert c1 - c0 == pytest.approx(1e-9 * flops / 8, rel=1e-12)
+    assert pl.Costs.block_rate("f32") == pytest.approx(512 / 157.3e12)
+
+
 def test_repart_properties():
     t = {"labels": "abc", "extents": {"a": 9, "b": 7, "c": 5}, "nnz": 120.0, "distinct": {"a": 9, "b": 7, "c": 5},
          "elem_bytes": 4}
@@ -198,7 +223,7 @@ def _to_product(prog, c):
               for k, t in prog["inputs"].items()}
     einsums = [pl.EinSum(n, e, a, b) for n, e, a, b in prog["einsums"]]
     return pl.Program(inputs, einsums), pl.Costs(c["c_xfer"], c["c_flop"], c["c_fixed"], c["max_call_bytes"],
-                                                 c["c_call"])
+                                                 c["c_call"], c.get("c_block", 0.0))
 
 
 @pytest.mark.parametrize("seed", range(60))
@@ -211,7 +236,7 @@ def test_planner_matches_exhaustive_search(seed):
     prog = _rand_program(rng)
     cap = math.inf if seed % 3 else float(rng.integers(200, 20000))
     c = _costs(10 ** rng.uniform(-13, -10), 10 ** rng.uniform(-15, -12), 10 ** rng.uniform(-11, -8), cap,
-               0.0 if seed % 2 else 10 ** rng.uniform(-6, -3))
+               0.0 if seed % 2 else 10 ** rng.uniform(-6, -3), 0.0 if seed % 4 < 2 else 10 ** rng.uniform(-13, -10))
     want = op.best_plans(prog, c, k=4)
     P, C = _to_product(prog, c)
     got = pl.optimize(P, C, k=4)
@@ -233,7 +258,7 @@ def test_planner_with_tiles_matches_exhaustive_search(seed):
     prog = _rand_program(rng, with_tiles=True)
     cap = math.inf if seed % 3 else float(rng.integers(200, 20000))
     c = _costs(10 ** rng.uniform(-13, -10), 10 ** rng.uniform(-15, -12), 10 ** rng.uniform(-11, -8), cap,
-               0.0 if seed % 2 else 10 ** rng.uniform(-6, -3))
+               0.0 if seed % 2 else 10 ** rng.uniform(-6, -3), 0.0 if seed % 4 < 2 else 10 ** rng.uniform(-13, -10))
     want = op.best_plans(prog, c, k=4)
     P, C = _to_product(prog, c)
     got = pl.optimize(P, C, k=4)
