@@ -24,9 +24,9 @@ x the product of the tile extents of all labels of U and V, a key attribute
 takes 4 bytes, EinSum results hold 4-byte elements, result statistics from
 the classical estimators on the purely relational form (Algorithm
 GetStats), and a repartition's intermediate at the smaller tile of a label
-promoted on both sides.  The optional per-call latency ``c_call`` (0 unless
-given) is charged once per EinSum and once per repartition that changes the
-decomposition.
+promoted on both sides.  Only the paper's terms are here: the product
+planner's own additions (a per-call latency and a span term) are not part of
+Sec. 7 and are checked in the product's tests by hand counts.
 """
 from __future__ import annotations
 
@@ -150,11 +150,7 @@ def einsum_cost(tu, tv, tw, prom, p):
     t_agg = min(0.5 * t_join, groups)
     c_add = tile_elems(tw, prom) * p["c_flop"]
     c_agg = (t_join - t_agg) * (row_bytes(tw, prom) * p["c_xfer"] + c_add + p["c_fixed"])
-    # added term: one pair's kernel flops over the 64 x 64 blocks of a W tile,
-    # at the rate c_block of one workgroup (0 unless given)
-    blocks = max(1.0, tile_elems(tw, prom) / 4096.0)
-    span = p.get("c_block", 0.0) * 2 * dem / blocks if t_join > 0 else 0.0
-    return c_join + c_agg + p.get("c_call", 0.0) + span
+    return c_join + c_agg
 
 
 def repart(t, p_in, p_out, p):
@@ -173,7 +169,7 @@ def repart(t, p_in, p_out, p):
         elif l in b:
             union[l] = b[l]
     moved = 2 * count(t, union) - count(t, a) - count(t, b)
-    return moved * (row_bytes(t, union) * p["c_xfer"] + p["c_fixed"]) + p.get("c_call", 0.0)
+    return moved * (row_bytes(t, union) * p["c_xfer"] + p["c_fixed"])
 
 
 def _sizes(t, l):

@@ -6,7 +6,12 @@ Eq. eqn-count against the stored tiles of a generated graph and against a
 simulated sparse tensor, the join estimate against real join sizes of
 uniform random relations, and the join / aggregation / repartition terms
 against hand-counted cases.  The planner's dynamic programme must then find
-exactly the oracle's cheapest plans."""
+exactly the oracle's cheapest plans.
+
+The oracle holds only the paper's model.  The product planner adds two terms
+of its own (a per-call latency c_call and a span term c_block, both 0 by
+default); every comparison with the oracle runs them at 0, and the two terms
+are pinned separately by hand counts against the product alone."""
 import math
 
 import numpy as np
@@ -16,9 +21,8 @@ import workloads
 from oracle import planner as op
 
 
-def _costs(c_xfer=1e-12, c_flop=1e-14, c_fixed=1e-9, cap=math.inf, c_call=0.0, c_block=0.0):
-    return {"c_xfer": c_xfer, "c_flop": c_flop, "c_fixed": c_fixed, "max_call_bytes": cap, "c_call": c_call,
-            "c_block": c_block}
+def _costs(c_xfer=1e-12, c_flop=1e-14, c_fixed=1e-9, cap=math.inf):
+    return {"c_xfer": c_xfer, "c_flop": c_flop, "c_fixed": c_fixed, "max_call_bytes": cap}
 
 
 # ------------------------------------------------------------- oracle pins
@@ -108,40 +112,70 @@ def test_kernel_flops_and_memory_cap():
     assert op.einsum_cost(tu, tv, tw, set(), _costs(cap=tiles - 1)) == math.inf
 
 
-def test_per_call_latency():
-    """c_call is charged once per EinSum and once per changing repartition."""
+def _product_stats(t):
+    from paper_2603_08957_amd import planner as pl
+
+    return pl.Stats(t["labels"], t["extents"], t["nnz"], t["distinct"], t["elem_bytes"], t.get("tiled", {}))
+
+
+def test_per_call_latency_product_hand_count():
+    """Product-only term: c_call is charged once per EinSum and once per
+    repartition that changes the decomposition, nothing else changes.  Hand
+    count on U [i 4][j 3] x V [j 3][k 5] dense, i promoted: the paper's terms
+    with c_xfer = c_flop = 0 and c_fixed = 1 are the tuples touched, 4 join
+    tuples and (4 - min(2, 4)) = 2 aggregated, 6 in all."""
+    from paper_2603_08957_amd import planner as pl
+
     tu = _dense_stats("ij", {"i": 4, "j": 3})
     tv = _dense_stats("jk", {"j": 3, "k": 5})
-    tw = op.derive("ij", "jk", "ik", tu, tv)
-    base = op.einsum_cost(tu, tv, tw, {"i"}, _costs())
-    assert op.einsum_cost(tu, tv, tw, {"i"}, _costs(c_call=7.0)) == pytest.approx(base + 7.0, rel=1e-12)
-    assert op.repart(tw, {"i"}, {"i"}, _costs(c_call=7.0)) == 0.0
-    r = op.repart(tw, {"i"}, {"k"}, _costs())
-    assert op.repart(tw, {"i"}, {"k"}, _costs(c_call=7.0)) == pytest.approx(r + 7.0, rel=1e-12)
+    su, sv = _product_stats(tu), _product_stats(tv)
+    sw = pl.result_stats(su, sv, pl.EinSum("E", "ij,jk->ik", "U", "V"), 4)
+    base = pl.local_cost(su, sv, sw, {"i": 1}, pl.Costs(0.0, 0.0, 1.0))
+    assert base == pytest.approx(4 + 2, rel=1e-12)
+    assert pl.local_cost(su, sv, sw, {"i": 1}, pl.Costs(0.0, 0.0, 1.0, c_call=7.0)) == pytest.approx(base + 7.0,
+                                                                                                      rel=1e-12)
+    assert pl.repart_cost(sw, {"i": 1}, {"i": 1}, pl.Costs(0.0, 0.0, 1.0, c_call=7.0)) == 0.0
+    r = pl.repart_cost(sw, {"i": 1}, {"k": 1}, pl.Costs(0.0, 0.0, 1.0))
+    assert r > 0
+    assert pl.repart_cost(sw, {"i": 1}, {"k": 1}, pl.Costs(0.0, 0.0, 1.0, c_call=7.0)) == pytest.approx(r + 7.0,
+                                                                                                         rel=1e-12)
 
 
-def test_span_term_hand_count():
-    """The added span term: one pair's kernel flops over the 64 x 64 blocks
-    of its W tile, times c_block; none without pairs.  Here U [i 128][j 32]
-    and V [j 32][k 256] dense, nothing promoted: one pair, 2*128*32*256 flops,
-    a W tile of 128 x 256 = 8 blocks; with j promoted at a tile of 8 there are
+def test_span_term_product_hand_count():
+    """Product-only term: one pair's kernel flops over the 64 x 64 blocks of
+    its W tile, times c_block; none without pairs.  Here U [i 128][j 32] and
+    V [j 32][k 256] dense, nothing promoted: one pair, 2*128*32*256 flops, a
+    W tile of 128 x 256 = 8 blocks; with j promoted at a tile of 8 there are
     4 pairs of 2*128*8*256 flops and the same 8 blocks."""
     from paper_2603_08957_amd import planner as pl
 
     tu = dict(_dense_stats("ij", {"i": 128, "j": 32}), tiled={"j": {8: 4}})
     tv = dict(_dense_stats("jk", {"j": 32, "k": 256}), tiled={"j": {8: 4}})
-    tw = op.derive("ij", "jk", "ik", tu, tv)
-    su = pl.Stats("ij", tu["extents"], tu["nnz"], tu["distinct"], tu["elem_bytes"], tu["tiled"])
-    sv = pl.Stats("jk", tv["extents"], tv["nnz"], tv["distinct"], tv["elem_bytes"], tv["tiled"])
+    su, sv = _product_stats(tu), _product_stats(tv)
     sw = pl.result_stats(su, sv, pl.EinSum("E", "ij,jk->ik", "U", "V"), 4)
     for prom, flops in (({}, 2 * 128 * 32 * 256), ({"j": 8}, 2 * 128 * 8 * 256)):
-        base = op.einsum_cost(tu, tv, tw, prom, _costs())
-        got = op.einsum_cost(tu, tv, tw, prom, _costs(c_block=1e-9))
-        assert got - base == pytest.approx(1e-9 * flops / 8, rel=1e-12)
         c0 = pl.local_cost(su, sv, sw, prom, pl.Costs(1e-12, 1e-14, 1e-9))
         c1 = pl.local_cost(su, sv, sw, prom, pl.Costs(1e-12, 1e-14, 1e-9, c_block=1e-9))
         assert c1 - c0 == pytest.approx(1e-9 * flops / 8, rel=1e-12)
     assert pl.Costs.block_rate("f32") == pytest.approx(512 / 157.3e12)
+
+
+def test_product_terms_zero_is_the_papers_model():
+    """With c_call = c_block = 0 the product prices every EinSum and
+    repartition as the oracle does (hand-built cases of each kind)."""
+    from paper_2603_08957_amd import planner as pl
+
+    c = _costs(3e-12, 2e-14, 5e-9)
+    C = pl.Costs(c["c_xfer"], c["c_flop"], c["c_fixed"])
+    tu = dict(_dense_stats("ij", {"i": 128, "j": 32}), tiled={"j": {8: 4}})
+    tv = dict(_dense_stats("jk", {"j": 32, "k": 256}), tiled={"j": {8: 4}})
+    tw = op.derive("ij", "jk", "ik", tu, tv)
+    su, sv = _product_stats(tu), _product_stats(tv)
+    sw = pl.result_stats(su, sv, pl.EinSum("E", "ij,jk->ik", "U", "V"), 4)
+    for prom in ({}, {"i": 1}, {"j": 8}, {"i": 1, "k": 1}, {"i": 1, "j": 1, "k": 1}):
+        assert pl.local_cost(su, sv, sw, prom, C) == pytest.approx(op.einsum_cost(tu, tv, tw, prom, c), rel=1e-12)
+    for a, b in (({"i": 1}, {"k": 1}), ({}, {"i": 1, "k": 1}), ({"i": 1}, {"i": 1})):
+        assert pl.repart_cost(sw, a, b, C) == pytest.approx(op.repart(tw, a, b, c), rel=1e-12)
 
 
 def test_repart_properties():
@@ -216,14 +250,16 @@ def _rand_program(rng, with_tiles=False):
     return {"inputs": inputs, "einsums": einsums}
 
 
-def _to_product(prog, c):
+def _to_product(prog, c, c_call=0.0, c_block=0.0):
+    """The program and costs for the product planner; c_call and c_block
+    are the product's own terms (0 = the paper's model, the oracle's)."""
     from paper_2603_08957_amd import planner as pl
 
     inputs = {k: pl.Stats(t["labels"], t["extents"], t["nnz"], t["distinct"], t["elem_bytes"], t.get("tiled", {}))
               for k, t in prog["inputs"].items()}
     einsums = [pl.EinSum(n, e, a, b) for n, e, a, b in prog["einsums"]]
     return pl.Program(inputs, einsums), pl.Costs(c["c_xfer"], c["c_flop"], c["c_fixed"], c["max_call_bytes"],
-                                                 c["c_call"], c.get("c_block", 0.0))
+                                                 c_call, c_block)
 
 
 @pytest.mark.parametrize("seed", range(60))
@@ -235,8 +271,7 @@ def test_planner_matches_exhaustive_search(seed):
     rng = np.random.default_rng(900 + seed)
     prog = _rand_program(rng)
     cap = math.inf if seed % 3 else float(rng.integers(200, 20000))
-    c = _costs(10 ** rng.uniform(-13, -10), 10 ** rng.uniform(-15, -12), 10 ** rng.uniform(-11, -8), cap,
-               0.0 if seed % 2 else 10 ** rng.uniform(-6, -3), 0.0 if seed % 4 < 2 else 10 ** rng.uniform(-13, -10))
+    c = _costs(10 ** rng.uniform(-13, -10), 10 ** rng.uniform(-15, -12), 10 ** rng.uniform(-11, -8), cap)
     want = op.best_plans(prog, c, k=4)
     P, C = _to_product(prog, c)
     got = pl.optimize(P, C, k=4)
@@ -257,8 +292,7 @@ def test_planner_with_tiles_matches_exhaustive_search(seed):
     rng = np.random.default_rng(7100 + seed)
     prog = _rand_program(rng, with_tiles=True)
     cap = math.inf if seed % 3 else float(rng.integers(200, 20000))
-    c = _costs(10 ** rng.uniform(-13, -10), 10 ** rng.uniform(-15, -12), 10 ** rng.uniform(-11, -8), cap,
-               0.0 if seed % 2 else 10 ** rng.uniform(-6, -3), 0.0 if seed % 4 < 2 else 10 ** rng.uniform(-13, -10))
+    c = _costs(10 ** rng.uniform(-13, -10), 10 ** rng.uniform(-15, -12), 10 ** rng.uniform(-11, -8), cap)
     want = op.best_plans(prog, c, k=4)
     P, C = _to_product(prog, c)
     got = pl.optimize(P, C, k=4)
@@ -266,6 +300,25 @@ def test_planner_with_tiles_matches_exhaustive_search(seed):
     for (gc, gplan), (wc, _) in zip(got, want):
         assert gc == pytest.approx(wc, rel=1e-9)
         assert op.total_cost(prog, gplan, c) == pytest.approx(gc, rel=1e-9)
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_planner_with_product_terms_is_exact(seed):
+    """With the product's own terms switched on (c_call, c_block) the dynamic
+    programme's four cheapest plans are still the four cheapest under the
+    product's pricing of whole plans, found by listing every plan (the
+    oracle's enumeration supplies the list; the prices are the product's,
+    whose extra terms are pinned by the hand counts above)."""
+    from paper_2603_08957_amd import planner as pl
+
+    rng = np.random.default_rng(4200 + seed)
+    prog = _rand_program(rng, with_tiles=bool(seed % 2))
+    c = _costs(10 ** rng.uniform(-13, -10), 10 ** rng.uniform(-15, -12), 10 ** rng.uniform(-11, -8))
+    P, C = _to_product(prog, c, 10 ** rng.uniform(-6, -3), 10 ** rng.uniform(-13, -10))
+    priced = sorted(pl.plan_cost(P, C, plan) for plan in op.all_plans(prog))
+    priced = [x for x in priced if not math.isinf(x)][:4]
+    got = pl.optimize(P, C, k=4)
+    assert [g for g, _ in got] == pytest.approx(priced, rel=1e-9)
 
 
 def test_tiled_count_matches_generated_tiles():
