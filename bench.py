@@ -63,6 +63,7 @@ class Stage:
         self.n_pairs = 0
         self.n_w = 0
         self.record = None  # a Timing to fill synchronously on the next run
+        self.pairs_out = None  # optional int32 [>= n_pairs, 2] buffer that receives the pair list (tests)
 
     def phase_report(self):
         """Join / contract / reduce times of the last recorded run and their
@@ -114,7 +115,7 @@ class Stage:
             timing = self.record
             timing.deferred = 0
         self.tre.contract(self.plan, jr, ut, vt, self.w_keys if self.plan.key_arity[2] else None,
-                          self.w_tiles[:jr.n_w], None, stream=stream, timing=timing)
+                          self.w_tiles[:jr.n_w], self.pairs_out, stream=stream, timing=timing)
         return self.w_keys[:jr.n_w], self.w_tiles[:jr.n_w]
 
     def tile_bytes(self, op):

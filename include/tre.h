@@ -33,8 +33,10 @@
  *   - Tiles: [n x tile_elems] contiguous, each tile row-major over ALL the
  *     operand's labels in string order, with extent t_l for a promoted label
  *     and the full extent for a demoted one.  Inputs are fp32 or bf16 (raw
- *     bits, uint16); W tiles are always fp32.  Tile arrays start on a
- *     16-byte boundary (TRE_E_ARG otherwise).
+ *     bits, uint16).  Accumulation is fp32; W tiles are fp32, or bf16 bits
+ *     rounded to nearest even from the fp32 sums when the plan was made with
+ *     the w_bf16 option (tre_plan_info.w_dtype says which).  Tile arrays
+ *     start on a 16-byte boundary (TRE_E_ARG otherwise).
  *   - Output order: W keys sorted lexicographically; the pair list in order of
  *     (W key, u index, v index), u/v being positions in the caller's arrays.
  *   - Errors are returned as tre_status; the library never aborts and never
@@ -104,6 +106,7 @@ typedef struct {
     char roles[27];           /* per letter a..z: 'b','m','n','k','p' (pre-sum) or '.' unused */
     int32_t group_needs_sort; /* 1 if pairs are radix-sorted by W key */
     int32_t v_needs_sort;     /* 1 if V is radix-sorted by its join key */
+    int32_t w_dtype;          /* element type tre_contract writes to w_tiles: TRE_F32, or TRE_BF16 with w_bf16 */
 } tre_plan_info;
 
 /* Result of tre_join, consumed by tre_contract (host struct; the pair list,
@@ -133,6 +136,10 @@ typedef struct {
     int64_t n_split_segments;
     int64_t n_partials;       /* partial tiles written by units of split segments */
     void *events[4];          /* library-owned while pending */
+    int32_t contract_path;    /* out: the contraction launch tre_contract chose: 0 generic MFMA GEMM (64x64
+                                 blocks), 1 vector class, 2 128x128 MFMA path, 3 the same as a paced
+                                 persistent grid, 4 the same with U-range units (partials summed after) */
+    int32_t reserved;
 } tre_timing;
 
 /* tre_plan -- parse and classify one binary EinSum (host only, no device work).
@@ -143,7 +150,8 @@ typedef struct {
  *   extent : host [26], indexed by letter - 'a'; >= 1 for used labels.
  *   tile   : host [26]; for a promoted label 1 <= t <= extent and extent % t == 0;
  *            ignored for demoted labels (their tile extent is the full extent).
- *   in_dtype : TRE_F32 or TRE_BF16 for both inputs; accumulation and W are fp32.
+ *   in_dtype : TRE_F32 or TRE_BF16 for both inputs; accumulation is fp32 and W
+ *            is fp32 unless opt->w_bf16 asks for bf16 output.
  *   opt    : host, may be NULL for defaults.
  *   out    : receives a host-owned, immutable plan; thread-safe to share. */
 tre_status tre_plan(const char *einsum, const char *upper, const int64_t *extent, const int32_t *tile,
@@ -194,21 +202,24 @@ tre_status tre_join_keys(tre_plan_t plan, const tre_join_result *join, int32_t *
  * fixed-order segmented reduction, so results are run-to-run deterministic.
  *   u_tiles, v_tiles : device tiles of the same arrays given to tre_join.
  *   w_keys  : device [w_cap x r_W] int32 (may be NULL when r_W = 0).
- *   w_tiles : device [w_cap x tile_elems(W)] fp32.
+ *   w_tiles : device [w_cap x tile_elems(W)] of the plan's W element type
+ *             (tre_plan_info.w_dtype): fp32, or bf16 bits (uint16) when the
+ *             plan was made with w_bf16.
  *   pairs_out : device [pair_cap x 2] int32 (u, v) or NULL.
  * TRE_E_CAPACITY if w_cap < n_w or (pairs_out and pair_cap < n_pairs).
  * Asynchronous on the stream unless timing is non-NULL and not deferred. */
 tre_status tre_contract(tre_plan_t plan, const tre_join_result *jr, const void *u_tiles, const void *v_tiles,
-                        int32_t *w_keys, int64_t w_cap, float *w_tiles, int32_t *pairs_out, int64_t pair_cap,
+                        int32_t *w_keys, int64_t w_cap, void *w_tiles, int32_t *pairs_out, int64_t pair_cap,
                         void *stream, tre_timing *timing);
 
 /* Wait for the events of a deferred tre_contract timing and fill its fields. */
 tre_status tre_timing_read(tre_timing *timing);
 
-/* tre_execute -- tre_join followed by tre_contract.  n_w / n_pairs (host) are
- * always written when the join succeeded, also with TRE_E_CAPACITY. */
+/* tre_execute -- tre_join followed by tre_contract (w_tiles of the plan's W
+ * element type, as for tre_contract).  n_w / n_pairs (host) are always
+ * written when the join succeeded, also with TRE_E_CAPACITY. */
 tre_status tre_execute(tre_plan_t plan, const int32_t *u_keys, int64_t n_u, const void *u_tiles,
-                       const int32_t *v_keys, int64_t n_v, const void *v_tiles, int32_t *w_keys, float *w_tiles,
+                       const int32_t *v_keys, int64_t n_v, const void *v_tiles, int32_t *w_keys, void *w_tiles,
                        int64_t w_cap, int64_t *n_w, int32_t *pairs_out, int64_t pair_cap, int64_t *n_pairs,
                        void *ws, size_t ws_bytes, void *stream, tre_timing *timing);
 

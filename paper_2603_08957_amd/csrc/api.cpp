@@ -256,8 +256,12 @@ tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const i
 }
 
 tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* u_tiles, const void* v_tiles,
-                        int32_t* w_keys, int64_t w_cap, float* w_tiles, int32_t* pairs_out, int64_t pair_cap,
+                        int32_t* w_keys, int64_t w_cap, void* w_out, int32_t* pairs_out, int64_t pair_cap,
                         void* stream, tre_timing* timing) {
+    // W's element type is the plan's (fp32, or bf16 bits with w_bf16); the
+    // kernels take the array as float* and store 16-bit elements through it
+    // when the plan says bf16
+    float* w_tiles = static_cast<float*>(w_out);
     if (!plan || !jr) {
         set_error("tre_contract: null plan or join result");
         return TRE_E_ARG;
@@ -319,6 +323,7 @@ tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* 
         return dev_fail(e, "outputs");
     tm.mark(s);
     if (timing) {
+        timing->contract_path = pace ? 3 : R > 1 ? 4 : (p.kclass == KC_VEC ? 1 : p.fast ? 2 : 0);
         if (deferred && tm.on) {
             for (int i = 0; i < 4; i++) timing->events[i] = reinterpret_cast<void*>(tm.ev[i]);
             timing->pending = 1;
@@ -381,7 +386,7 @@ tre_status tre_timing_read(tre_timing* t) {
 }
 
 tre_status tre_execute(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const void* u_tiles,
-                       const int32_t* v_keys, int64_t n_v, const void* v_tiles, int32_t* w_keys, float* w_tiles,
+                       const int32_t* v_keys, int64_t n_v, const void* v_tiles, int32_t* w_keys, void* w_tiles,
                        int64_t w_cap, int64_t* n_w, int32_t* pairs_out, int64_t pair_cap, int64_t* n_pairs,
                        void* ws, size_t ws_bytes, void* stream, tre_timing* timing) {
     tre_join_result jr;

@@ -372,6 +372,20 @@ static tre_status classify(Plan& p) {
 
 static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
+// Whether the 128x128 path may cut keys into U ranges (each (key, range)
+// leaving a partial tile): asked for explicitly, or where the paced
+// persistent grid cannot run instead -- several 128x128 blocks per W tile,
+// pacing switched off, or a unit length cap.  Where pacing can run, the
+// automatic choice takes it, and a U-range fallback (output keys beyond
+// what the pacing counters cover) sizes its ranges to the partial tiles the
+// workspace holds.
+bool u_ranges_possible(const Plan& p) {
+    if (!(p.kclass == KC_GEMM && p.fast) || p.opt.u_ranges < 0) return false;
+    const int64_t M = p.swap ? p.nN : p.nM, N = p.swap ? p.nM : p.nN;
+    return p.opt.u_ranges > 0 || (M / 128) * (N / 128) != 1 || p.opt.pace_windows < 0 ||
+           p.opt.max_pairs_per_unit > 0;
+}
+
 Layout make_layout(const Plan& p, int64_t n_u, int64_t n_v, int64_t max_pairs) {
     Layout L;
     L.n_u = n_u;
@@ -383,7 +397,7 @@ Layout make_layout(const Plan& p, int64_t n_u, int64_t n_v, int64_t max_pairs) {
     int64_t cap = std::max<int64_t>(16, (int64_t(1) << 30) / wtile_bytes);
     cap = std::min<int64_t>(cap, 4096);
     cap = std::min<int64_t>(cap, P + 1);
-    if (p.kclass == KC_GEMM && p.fast) {
+    if (u_ranges_possible(p)) {
         // U-range mode: up to kMaxURanges partial tiles per output key, at
         // most 4 GiB of them
         int64_t wspace = 1;
@@ -497,6 +511,7 @@ tre_status tre_plan_get_info(tre_plan_t plan, tre_plan_info* info) {
     for (int l = 0; l < 26; l++) info->roles[l] = p.used[l] ? p.role[l] : '.';
     info->group_needs_sort = p.group_needs_sort;
     info->v_needs_sort = p.v_needs_sort;
+    info->w_dtype = p.opt.w_bf16 ? TRE_BF16 : TRE_F32;
     return TRE_OK;
 }
 

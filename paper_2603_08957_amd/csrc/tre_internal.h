@@ -126,6 +126,7 @@ struct Unit {
 };
 
 Layout make_layout(const Plan& p, int64_t n_u, int64_t n_v, int64_t max_pairs);
+bool u_ranges_possible(const Plan& p);
 
 // ----- launchers (defined in the .hip files) -----
 // scan.hip

@@ -51,7 +51,7 @@ class PlanInfo(ctypes.Structure):
                 ("kernel_class", ctypes.c_int32), ("batch", ctypes.c_int64), ("m", ctypes.c_int64),
                 ("n", ctypes.c_int64), ("k", ctypes.c_int64), ("flops_per_pair", ctypes.c_int64),
                 ("key_labels", (ctypes.c_char * 27) * 3), ("roles", ctypes.c_char * 27),
-                ("group_needs_sort", ctypes.c_int32), ("v_needs_sort", ctypes.c_int32)]
+                ("group_needs_sort", ctypes.c_int32), ("v_needs_sort", ctypes.c_int32), ("w_dtype", ctypes.c_int32)]
 
 
 class JoinResult(ctypes.Structure):
@@ -63,7 +63,10 @@ class Timing(ctypes.Structure):
     _fields_ = [("join_ms", ctypes.c_float), ("units_ms", ctypes.c_float), ("contract_ms", ctypes.c_float),
                 ("reduce_ms", ctypes.c_float), ("total_ms", ctypes.c_float), ("deferred", ctypes.c_int32),
                 ("pending", ctypes.c_int32), ("n_units", ctypes.c_int64), ("n_split_segments", ctypes.c_int64),
-                ("n_partials", ctypes.c_int64), ("events", ctypes.c_void_p * 4)]
+                ("n_partials", ctypes.c_int64), ("events", ctypes.c_void_p * 4), ("contract_path", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+    PATHS = {0: "gemm", 1: "vec", 2: "gemm128", 3: "gemm128_paced", 4: "gemm128_u_ranges"}
 
     def read(self):
         """Wait for deferred events and fill the millisecond fields."""
@@ -71,7 +74,9 @@ class Timing(ctypes.Structure):
         return self
 
     def as_dict(self):
-        return {k: getattr(self, k) for k, _ in self._fields_ if k not in ("events", "deferred", "pending")}
+        d = {k: getattr(self, k) for k, _ in self._fields_ if k not in ("events", "deferred", "pending", "reserved")}
+        d["contract_path"] = self.PATHS.get(self.contract_path, self.contract_path)
+        return d
 
 
 _lib = None
@@ -171,6 +176,7 @@ class Plan:
         self.roles = bytes(info.roles).split(b"\0")[0].decode()
         self.group_needs_sort = bool(info.group_needs_sort)
         self.v_needs_sort = bool(info.v_needs_sort)
+        self.w_dtype = {0: "f32", 1: "bf16"}[info.w_dtype]
 
     @classmethod
     def from_spec(cls, spec: dict, **kw):

