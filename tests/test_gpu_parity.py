@@ -151,8 +151,9 @@ def test_paced_path_gpu(orc, idx, windows, dtype, w_bf16):
     e, upper, ext, til = FAST_PLANS[idx]
     rng = np.random.default_rng(177 + idx)
     u_lab, v_lab, _ = split_einsum(e)
-    U = workloads.random_relation(rng, u_lab, upper, ext, til, dtype, keep=0.6, zero_frac=0.05)
-    V = workloads.random_relation(rng, v_lab, upper, ext, til, dtype, keep=0.6, zero_frac=0.05)
+    # every U tile present: the paced grid needs at least two U tuples
+    U = workloads.random_relation(rng, u_lab, upper, ext, til, dtype, keep=1.0, zero_frac=0.05)
+    V = workloads.random_relation(rng, v_lab, upper, ext, til, dtype, keep=0.6 if idx == 0 else 1.0, zero_frac=0.05)
     spec = workloads.spec(e, upper, ext, til, dtype)
     assert tre.Plan(e, upper, ext, til, dtype).kernel_class == "gemm128"
     say("paced path", idx, dtype, windows, w_bf16, e, len(U["keys"]), len(V["keys"]))
