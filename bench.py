@@ -1,6 +1,6 @@
 """Benchmark: one decomposed EinSum chain per step on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config N]
 
 A step is one pass of the whole hot path over one batch of synthetic input
 that is already resident in HBM: for the default workload (the bf16 GNN
@@ -14,7 +14,15 @@ contraction.  Prints one JSON line:
   roofline    the dominant kernel (E1's tile contraction): algorithmic bytes
               or flops per launch / its average launch time, measured with
               HIP events on the launch stream inside the timed region
-  cpu_baseline the CPU oracle timed on a bounded sample of the same inputs
+  cpu_baseline the CPU oracle timed on a bounded sample of the same inputs,
+              with the host's CPU count and model
+  configs     the same report for every workload (1-6), the headline first:
+              step time (mean, median, min over the timed steps), the
+              dominant kernel's roofline, and per EinSum its join,
+              contraction and reduction times with their algorithmic HBM
+              rates as fractions of 8 TB/s, its whole-EinSum roofline
+              fraction, and the read-once and per-pair byte bounds
+With --config N only that workload runs (no configs list).
 """
 from __future__ import annotations
 
@@ -82,7 +90,8 @@ class Stage:
                 "contract_TFLOPs": self.flops() / (t.contract_ms * 1e-3) / 1e12 if t.contract_ms > 0 else None,
                 "units_ms": t.units_ms, "reduce_ms": t.reduce_ms, "reduce_alg_bytes": rb,
                 "reduce_GBs": gbs(rb, t.reduce_ms) if rb else None, "n_units": t.n_units,
-                "n_split_segments": t.n_split_segments}
+                "n_split_segments": t.n_split_segments,
+                "contract_path": self.tre.Timing.PATHS.get(t.contract_path, t.contract_path)}
 
     def run(self, uk, ut, vk, vt, timing=None):
         jr = self.join(uk, vk, timing=timing)
@@ -128,6 +137,10 @@ class Stage:
     def alg_bytes(self):
         """Read every input tuple once, write every output tile once."""
         return self.n_u * self.tile_bytes(0) + self.n_v * self.tile_bytes(1) + self.n_w * self.tile_bytes(2)
+
+    def pair_bytes(self):
+        """Every pair reads both of its tiles, every output tile written once."""
+        return self.n_pairs * (self.tile_bytes(0) + self.tile_bytes(1)) + self.n_w * self.tile_bytes(2)
 
 
 class FusedStage:
@@ -177,6 +190,10 @@ class FusedStage:
         """Read every input tuple once, write every output tile once."""
         return 4 * (self.n_u * self.te[0] + self.n_v * self.te[1] + self.n_x * self.te[2] + self.n_w * self.te[3])
 
+    def pair_bytes(self):
+        """Every triple reads its three tiles, every output tile written once."""
+        return 4 * (self.n_pairs * (self.te[0] + self.te[1] + self.te[2]) + self.n_w * self.te[3])
+
     def phase_report(self):
         t = self.record
         jb = 4 * (self.n_u * self.plan.key_arity[0] + self.n_v + self.n_x) + 12 * self.n_pairs + 12 * self.n_w
@@ -191,7 +208,9 @@ class FusedStage:
 # ------------------------------------------------------------ workloads
 
 class GnnChain:
-    """(X.Y)^T.Z: E1 'ij,jk->ki' over (X keyed J, Y keyed (J,K)), cast, E2 'ki,im->km'."""
+    """(X.Y)^T.Z: E1 'ij,jk->ki' over (X keyed J, Y keyed (J,K)), or 'ij,kj->ki'
+    with Y keyed (K,J) (the 1,048,576-vertex chain's destination-major
+    adjacency), cast, E2 'ki,im->km'."""
 
     def __init__(self, c, tre, torch):
         import workloads
@@ -326,6 +345,7 @@ class GnnChain:
                             f"E2 tiles {w['tile_e2']}",
                 "vertices": w["n"], "edges": w["n_edges"], "embedding": w["emb"], "tile_e1": w["tile_e1"],
                 "tile_e2": w["tile_e2"], "y_tuples": len(w["Y"]["keys"]),
+                "y_keyed": "(K, J), destination-major" if w["y_layout"] == "kj" else "(J, K), source-major",
                 "einsums": [w["E1"]["einsum"] + " upper " + w["E1"]["upper"],
                             w["E2"]["einsum"] + " upper " + w["E2"]["upper"]]}
 
@@ -346,7 +366,8 @@ class GnnChain:
         rng = np.random.default_rng(0)
         p1 = orc.Plan(w["E1"]["einsum"], w["E1"]["upper"], w["E1"]["extents"], w["E1"]["tiles"])
         Y = w["Y"]
-        all_k = np.unique(Y["keys"][:, 1])
+        kc = w["y_k_col"]
+        all_k = np.unique(Y["keys"][:, kc])
         S = np.sort(rng.choice(all_k, size=min(n_keys_e1, len(all_k)), replace=False)).reshape(-1, 1).astype(np.int32)
         mu, mv = orc.restrict(p1, w["X"]["keys"], Y["keys"], S)
         ykeep = mv[Y["slot"]]
@@ -354,7 +375,7 @@ class GnnChain:
         uc, uv, _ = orc.expand(p1, 0, w["X"]["keys"][mu], w["X"]["tiles"][mu], w["dtype"])
         acc, mag, _ = orc.evaluate(p1, uc, uv, Y["coo"][0][ykeep], Y["coo"][1][ykeep], S)
         t1 = time.perf_counter()
-        pairs1 = int(np.isin(Y["keys"][:, 1], S[:, 0]).sum())
+        pairs1 = int(np.isin(Y["keys"][:, kc], S[:, 0]).sum())
         flops1 = pairs1 * self.e1.plan.flops_per_pair
         # E2 sample: synthetic T rows for the sampled keys (same shapes)
         p2 = orc.Plan(w["E2"]["einsum"], w["E2"]["upper"], w["E2"]["extents"], w["E2"]["tiles"])
@@ -397,8 +418,15 @@ class BlockSparse:
         return {"workload": f"block-sparse A.B, fp32: A {w['n']}x{w['n']} with 5% of {w['block']}x{w['block']} "
                             f"blocks, B {w['n']}x{w['n_cols']}", "a_blocks": len(w["A"]["keys"])}
 
-    def oracle_sample(self, orc, n_keys=20):
-        """The oracle on the first n_keys output row blocks (about 10 s)."""
+    def oracle_sample(self, orc, budget_s=10.0):
+        """The oracle on the first output row blocks: 2 of them, then as many
+        as about budget_s seconds allow."""
+        r = self._oracle_sample(orc, 2)
+        if r["seconds"] < 0.8 * budget_s:
+            r = self._oracle_sample(orc, max(2, int(2 * budget_s / max(r["seconds"], 1e-3))))
+        return r
+
+    def _oracle_sample(self, orc, n_keys):
         w = self.w
         p = orc.Plan(w["E"]["einsum"], w["E"]["upper"], w["E"]["extents"], w["E"]["tiles"])
         S = np.unique(w["A"]["keys"][:, 0])[:n_keys].reshape(-1, 1).astype(np.int32)
@@ -450,13 +478,19 @@ class ThreeWay:
                             f"{w['block']}^3 blocks (0.5% of blocks, 10% dense), r {w['r']}; {how}",
                 "t_blocks": len(w["T"]["keys"]), "path": self.path}
 
-    def oracle_sample(self, orc, n_keys=1):
+    def oracle_sample(self, orc, budget_s=10.0):
         if self.path == "fused":
-            return self._oracle_sample_fused(orc)
+            return self._oracle_sample_fused(orc, budget_s)
+        r = self._oracle_sample_binary(orc, 8)
+        if r["seconds"] < 0.8 * budget_s:
+            r = self._oracle_sample_binary(orc, max(8, int(8 * budget_s / max(r["seconds"], 1e-3))))
+        return r
+
+    def _oracle_sample_binary(self, orc, n_keys):
         w = self.w
         p = orc.Plan(w["E1"]["einsum"], w["E1"]["upper"], w["E1"]["extents"], w["E1"]["tiles"])
         keys = w["T"]["keys"]
-        ik = np.unique(keys[:, [0, 2]], axis=0)[:64].astype(np.int32)
+        ik = np.unique(keys[:, [0, 2]], axis=0)[:n_keys].astype(np.int32)
         mu, mv = orc.restrict(p, keys, w["B"]["keys"], ik)
         t0 = time.perf_counter()
         uc, uv, _ = orc.expand(p, 0, keys[mu], w["T"]["tiles"][mu], "f32")
@@ -465,7 +499,7 @@ class ThreeWay:
         secs = time.perf_counter() - t0
         flops = int(mu.sum()) * self.e1.plan.flops_per_pair
         return {"value": flops / secs / 1e9, "unit": "GFLOP/s", "cores": 1, "kind": "oracle",
-                "sample": f"E1 restricted to 64 output keys ({int(mu.sum())} tile pairs), {secs:.1f} s",
+                "sample": f"E1 restricted to {len(ik)} output keys ({int(mu.sum())} tile pairs), {secs:.1f} s",
                 "seconds": secs}
 
     def _oracle_sample_fused(self, orc, budget_s=10.0):
@@ -914,14 +948,159 @@ def make_workload(c, tre, torch, three_way="fused"):
     raise SystemExit(f"unknown workload {c}")
 
 
+def host_facts():
+    """The CPU the oracle baseline runs on: logical CPUs, CPUs this process
+    may use, and the model name."""
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = os.cpu_count()
+    return {"nproc": os.cpu_count(), "usable_cpus": usable, "model": model}
+
+
+def stage_report(st, dtype):
+    """Per EinSum: join / contraction / reduction times of the synchronous
+    phase pass and their algorithmic rates as fractions of 8 TB/s, and the
+    EinSum's roofline: the larger of its MFMA time and its HBM time (every
+    input tuple read once, every output tile written once), over the time
+    of all its phases.  Also the per-pair bound: every pair reads both of
+    its tiles (the traffic a gather-bound kernel pays when tiles are not
+    reused on chip)."""
+    ph = st.phase_report()
+    frac = lambda gbs: (gbs / PEAK_HBM_GBS) if gbs else None  # noqa: E731
+    t_all = sum(ph.get(k) or 0.0 for k in ("join_ms", "units_ms", "contract_ms", "reduce_ms"))
+    peak_f = PEAK_TFLOPS[dtype] * 1e12
+    t_roof = max(st.flops() / peak_f, st.alg_bytes() / (PEAK_HBM_GBS * 1e9))
+    pb = st.pair_bytes()
+    c_ms = ph.get("contract_ms") or 0.0
+    out = {"name": st.name, "einsum": st.spec["einsum"], "upper": st.spec["upper"],
+           "kernel_class": st.plan.kernel_class, "n_pairs": st.n_pairs, "n_w": st.n_w,
+           "tile_gflop": st.flops() / 1e9, "alg_bytes": st.alg_bytes(), "pair_bytes": pb,
+           "ms": t_all, "roofline_frac": (t_roof / (t_all * 1e-3)) if t_all > 0 else None,
+           "join_ms": ph.get("join_ms"), "join_alg_bytes": ph.get("join_alg_bytes"), "join_GBs": ph.get("join_GBs"),
+           "join_frac": frac(ph.get("join_GBs")),
+           "contract_ms": c_ms, "contract_GBs": ph.get("contract_GBs"), "contract_frac": frac(ph.get("contract_GBs")),
+           "contract_TFLOPs": ph.get("contract_TFLOPs"),
+           "contract_mfma_frac": (ph["contract_TFLOPs"] / PEAK_TFLOPS[dtype]) if ph.get("contract_TFLOPs") else None,
+           "contract_roofline_frac": (t_roof / (c_ms * 1e-3)) if c_ms > 0 else None,
+           "contract_pair_bytes_frac": (pb / (c_ms * 1e-3) / 1e9 / PEAK_HBM_GBS) if c_ms > 0 else None,
+           "reduce_ms": ph.get("reduce_ms"), "reduce_alg_bytes": ph.get("reduce_alg_bytes"),
+           "reduce_GBs": ph.get("reduce_GBs"), "reduce_frac": frac(ph.get("reduce_GBs"))}
+    for k in ("n_units", "n_split_segments", "n_triples", "contract_path"):
+        if k in ph:
+            out[k] = ph[k]
+    return out
+
+
+def measure(W, args, torch, tre, config, cpu_budget_s):
+    """Warm-up, K timed steps (HIP events around every step on the launch
+    stream; deferred library events around the dominant kernel), one
+    synchronous phase pass outside the timed region, and the oracle on a
+    bounded sample.  Returns the config's report."""
+    for _ in range(args.warmup):
+        W.step()
+    torch.cuda.synchronize()
+    stages = W.stages()
+    dom = stages[0]
+    timings = []
+    log(f"[bench] config {config}: timing {args.steps} steps")
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    t0 = time.perf_counter()
+    evs[0].record()
+    for i in range(args.steps):
+        tm = tre.Timing()
+        tm.deferred = 1
+        W.step(timing=tm)
+        evs[i + 1].record()
+        timings.append(tm)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
+    ms_step = evs[0].elapsed_time(evs[-1]) / args.steps
+    for tm in timings:
+        tm.read()
+    contract_ms = float(np.mean([t.contract_ms for t in timings]))
+    units_ms = float(np.mean([t.units_ms for t in timings]))
+    reduce_ms = float(np.mean([t.reduce_ms for t in timings]))
+    for st in stages:
+        st.record = tre.Timing()
+    if hasattr(W, "measure_rp"):
+        W.measure_rp = True
+    W.step()
+    torch.cuda.synchronize()
+    dtype = "bf16" if dom.spec["dtype"] == "bf16" else "f32"
+    einsums = [stage_report(st, dtype) for st in stages]
+    rp = getattr(W, "rp_report", None)
+    if rp:
+        W.measure_rp = False
+    for st in stages:
+        st.record = None
+    flops = sum(st.flops() for st in stages)
+    alg = dom.alg_bytes()
+    dflops = dom.flops()
+    t_hbm = alg / (PEAK_HBM_GBS * 1e9)
+    t_mfma = dflops / (PEAK_TFLOPS[dtype] * 1e12)
+    if t_hbm >= t_mfma:
+        roof = {"bound": "hbm", "achieved": alg / (contract_ms * 1e-3) / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    else:
+        roof = {"bound": "mfma", "achieved": dflops / (contract_ms * 1e-3) / 1e12, "peak": PEAK_TFLOPS[dtype],
+                "unit": "TFLOP/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    rec = traffic_record(config, args.three_way)
+    roof["traffic"] = rec["bytes"] if rec else None
+    if rec:
+        roof["traffic_detail"] = rec
+    roof["kernel"] = f"{dom.name} tile contraction ({dom.plan.kernel_class})"
+    roof["kernel_ms"] = contract_ms
+    roof["alg_bytes_per_launch"] = alg
+    roof["pair_bytes_per_launch"] = dom.pair_bytes()
+    roof["pair_bytes_frac"] = dom.pair_bytes() / (contract_ms * 1e-3) / 1e9 / PEAK_HBM_GBS
+    roof["flops_per_launch"] = dflops
+    roof["mfma_tflops"] = dflops / (contract_ms * 1e-3) / 1e12
+    roof["mfma_frac"] = roof["mfma_tflops"] / PEAK_TFLOPS[dtype]
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+
+        oracle.build()
+        log(f"[bench] config {config}: timing the CPU oracle on a bounded sample (~{cpu_budget_s:.0f} s)")
+        cpu = W.oracle_sample(oracle, cpu_budget_s)
+        cpu.pop("seconds", None)
+        cpu["host"] = host_facts()
+    rep = {"config": config, "workload": W.describe(), "dtype": dtype, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": ms_step, "ms_per_step_median": float(np.median(per_step)),
+           "ms_per_step_min": float(np.min(per_step)), "ms_per_step_max": float(np.max(per_step)),
+           "value": flops / (ms_step * 1e-3) / 1e9, "unit": "GFLOP/s", "roofline": roof, "einsums": einsums,
+           "timed_region": {"dominant_contract_ms": contract_ms, "dominant_units_ms": units_ms,
+                            "dominant_reduce_and_write_ms": reduce_ms, "wall_s": wall},
+           "cpu_baseline": cpu}
+    if rp:
+        rep["repartition"] = rp
+    return rep
+
+
+ALL_CONFIGS = (2, 1, 3, 4, 5, 6)  # the headline workload first
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", type=int, default=2,
-                    help="workload 1..6 (default 2: bf16 GNN chain, 262,144 vertices; 6: graph attention)")
+    ap.add_argument("--config", type=int, default=0,
+                    help="one workload 1..6 only (default: the headline workload 2, the bf16 GNN chain on 262,144 "
+                         "vertices, then every other workload in a 'configs' list of the same line)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=0.0, metavar="S",
+                    help="seconds of oracle time per workload (default 6 for the headline, 3 for the others)")
     ap.add_argument("--u-ranges", type=int, default=0,
                     help="tre_options.u_ranges for every EinSum (0 = library default, < 0 = off)")
     ap.add_argument("--pace-windows", type=int, default=0,
@@ -939,6 +1118,8 @@ def main():
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (the path shards by output key "
               f"across GPUs by design; this library runs the one-GPU share on a single MI355X)", file=sys.stderr)
         sys.exit(2)
+
+    import gc
 
     import torch
 
@@ -964,94 +1145,29 @@ def main():
             raise SystemExit("--planner-top covers the GNN chains of workloads 1 and 2")
         print(json.dumps(planner_check(tre, torch, args.config, args.planner_top, args.steps)), flush=True)
         return
-    W = make_workload(args.config, tre, torch, args.three_way)
-    log("[bench] inputs resident; warming up")
-    for _ in range(args.warmup):
-        W.step()
-    torch.cuda.synchronize()
-    stages = W.stages()
-    dom = stages[0]
-    timings = []
-    log(f"[bench] timing {args.steps} steps")
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    t0 = time.perf_counter()
-    ev0.record()
-    for _ in range(args.steps):
-        tm = tre.Timing()
-        tm.deferred = 1
-        W.step(timing=tm)
-        timings.append(tm)
-    ev1.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_step = ev0.elapsed_time(ev1) / args.steps
-    for tm in timings:
-        tm.read()
-    contract_ms = float(np.mean([t.contract_ms for t in timings]))
-    units_ms = float(np.mean([t.units_ms for t in timings]))
-    reduce_ms = float(np.mean([t.reduce_ms for t in timings]))
-    # per-EinSum phase times (join / contract / reduce) from one extra pass
-    # with synchronous library timing, outside the timed region
-    for st in stages:
-        st.record = tre.Timing()
-    if hasattr(W, "measure_rp"):
-        W.measure_rp = True
-    W.step()
-    torch.cuda.synchronize()
-    phases = {st.name: st.phase_report() for st in stages}
-    if getattr(W, "rp_report", None):
-        phases["repartition"] = W.rp_report
-        W.measure_rp = False
-    for st in stages:
-        st.record = None
-    flops = sum(st.flops() for st in stages)
-    value = flops / (ms_step * 1e-3) / 1e9
-    dtype = "bf16" if dom.spec["dtype"] == "bf16" else "f32"
-    alg = dom.alg_bytes()
-    dflops = dom.flops()
-    t_hbm = alg / (PEAK_HBM_GBS * 1e9)
-    t_mfma = dflops / (PEAK_TFLOPS[dtype] * 1e12)
-    if t_hbm >= t_mfma:
-        roof = {"bound": "hbm", "achieved": alg / (contract_ms * 1e-3) / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
-    else:
-        roof = {"bound": "mfma", "achieved": dflops / (contract_ms * 1e-3) / 1e12, "peak": PEAK_TFLOPS[dtype],
-                "unit": "TFLOP/s"}
-    roof["frac"] = roof["achieved"] / roof["peak"]
-    rec = traffic_record(args.config, args.three_way)
-    roof["traffic"] = rec["bytes"] if rec else None
-    if rec:
-        roof["traffic_detail"] = rec
-    roof["kernel"] = f"{dom.name} tile contraction ({dom.plan.kernel_class})"
-    roof["kernel_ms"] = contract_ms
-    roof["alg_bytes_per_launch"] = alg
-    roof["flops_per_launch"] = dflops
-    roof["mfma_tflops"] = dflops / (contract_ms * 1e-3) / 1e12
-    roof["mfma_frac"] = roof["mfma_tflops"] / PEAK_TFLOPS[dtype]
-    cpu = None
-    if not args.no_cpu_baseline:
-        import oracle
-
-        oracle.build()
-        log("[bench] timing the CPU oracle on a bounded sample")
-        cpu = W.oracle_sample(oracle)
-    per_stage = []
-    for st in stages:
-        per_stage.append({"einsum": st.spec["einsum"], "upper": st.spec["upper"], "n_pairs": st.n_pairs,
-                          "n_w": st.n_w, "tile_gflop": st.flops() / 1e9, "alg_bytes": st.alg_bytes()})
+    todo = [args.config] if args.config else list(ALL_CONFIGS)
+    reports = []
+    for c in todo:
+        W = make_workload(c, tre, torch, args.three_way)
+        log(f"[bench] config {c}: inputs resident; warming up")
+        budget = args.cpu_budget or (6.0 if c == todo[0] else 3.0)
+        reports.append(measure(W, args, torch, tre, c, budget))
+        del W
+        gc.collect()
+        torch.cuda.empty_cache()
+    head = reports[0]
     out = {
-        "metric": METRIC, "value": value, "unit": "GFLOP/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": dtype, "data": "synthetic",
-        "config": W.describe(),
-        "roofline": roof, "cpu_baseline": cpu,
-        "timed_region": {"dominant_contract_ms": contract_ms, "dominant_units_ms": units_ms,
-                         "dominant_reduce_and_write_ms": reduce_ms, "wall_s": wall},
-        "phases": phases,
-        "einsums": per_stage,
+        "metric": METRIC, "value": head["value"], "unit": "GFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": head["ms_per_step"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": head["dtype"], "data": "synthetic",
+        "config": head["workload"],
+        "roofline": head["roofline"], "cpu_baseline": head["cpu_baseline"],
+        "ms_per_step_median": head["ms_per_step_median"], "ms_per_step_min": head["ms_per_step_min"],
+        "timed_region": head["timed_region"],
+        "einsums": head["einsums"],
     }
-    if cpu is not None:
-        cpu.pop("seconds", None)
+    if len(reports) > 1:
+        out["configs"] = [{k: v for k, v in r.items()} for r in reports]
     print(json.dumps(out), flush=True)
 
 

@@ -107,6 +107,9 @@ typedef struct {
     int32_t group_needs_sort; /* 1 if pairs are radix-sorted by W key */
     int32_t v_needs_sort;     /* 1 if V is radix-sorted by its join key */
     int32_t w_dtype;          /* element type tre_contract writes to w_tiles: TRE_F32, or TRE_BF16 with w_bf16 */
+    int32_t join_outer;       /* 0: the join walks U and searches V; 1: it walks V and searches U, which
+                                 emits the pairs already grouped by W key (W's key is V's key prefix,
+                                 followed by the join labels, which U's key starts with) */
 } tre_plan_info;
 
 /* Result of tre_join, consumed by tre_contract (host struct; the pair list,
@@ -150,12 +153,14 @@ typedef struct {
  *   extent : host [26], indexed by letter - 'a'; >= 1 for used labels.
  *   tile   : host [26]; for a promoted label 1 <= t <= extent and extent % t == 0;
  *            ignored for demoted labels (their tile extent is the full extent).
- *   in_dtype : TRE_F32 or TRE_BF16 for both inputs; accumulation is fp32 and W
- *            is fp32 unless opt->w_bf16 asks for bf16 output.
+ *   in_dtype : a tre_dtype value, TRE_F32 or TRE_BF16, for both inputs (passed
+ *            as int32 so that any other value is a defined TRE_E_DTYPE);
+ *            accumulation is fp32 and W is fp32 unless opt->w_bf16 asks for
+ *            bf16 output.
  *   opt    : host, may be NULL for defaults.
  *   out    : receives a host-owned, immutable plan; thread-safe to share. */
 tre_status tre_plan(const char *einsum, const char *upper, const int64_t *extent, const int32_t *tile,
-                    tre_dtype in_dtype, const tre_options *opt, tre_plan_t *out);
+                    int32_t in_dtype, const tre_options *opt, tre_plan_t *out);
 
 tre_status tre_plan_get_info(tre_plan_t plan, tre_plan_info *info);
 
@@ -177,10 +182,13 @@ int64_t tre_workspace_max_pairs(tre_plan_t plan, int64_t n_u, int64_t n_v, size_
  *   ws, ws_bytes   : device workspace (256-byte aligned); must stay untouched
  *                    until the matching tre_contract has completed.
  *   out            : host; receives n_pairs and n_w.
- * Synchronizes the stream (twice) to read the pair and key counts; when V
- * has no promoted labels (one tuple) and W's key is U's key as it is, every
- * U tuple is one pair and one output tuple, the counts are known without the
- * device, and the call synchronizes only to report key validation.
+ * Synchronizes the stream once, reading back the key checks, the pair count
+ * and the output key count together (the GROUP BY stage takes the pair
+ * count from device memory, its grids sized for the pairs the workspace can
+ * hold); when V has no promoted labels (one tuple) and W's key is U's key as
+ * it is, every U tuple is one pair and one output tuple, the counts are
+ * known without the device, and the call synchronizes only to report key
+ * validation.
  * TRE_E_WORKSPACE (out->n_pairs set) if the pairs do not fit; key errors are
  * reported as TRE_E_UNSORTED / TRE_E_DUPKEY / TRE_E_KEYRANGE. */
 tre_status tre_join(tre_plan_t plan, const int32_t *u_keys, int64_t n_u, const int32_t *v_keys, int64_t n_v,
@@ -316,7 +324,8 @@ tre_status tre_repartition(const char *labels, const char *upper_in, const char 
  * extent of U's last label is a multiple of 4 and the tile extents of U's
  * last two labels are at most 64 each; masked form: U's last two labels take
  * tiles of 1 (one scalar per edge, as in Table gt-schema), U's other labels
- * any tiles.  in_dtype: TRE_F32 only (TRE_E_DTYPE otherwise).
+ * any tiles.  in_dtype: TRE_F32 only (TRE_E_DTYPE otherwise; an int32 holding a
+ * tre_dtype value, as for tre_plan).
  *   extent, tile : host [26] per letter, as for tre_plan.
  *   u_keys [n_u x r_U], v_keys [n_v x 1], x_keys [n_x x 1]: device int32,
  *                  sorted strictly increasing (U keyed by its promoted labels
@@ -339,7 +348,7 @@ tre_status tre_repartition(const char *labels, const char *upper_in, const char 
 size_t tre_execute3_workspace_bytes(const char *einsum, const char *upper, const int64_t *extent,
                                     const int32_t *tile, int64_t n_u);
 tre_status tre_execute3(const char *einsum, const char *upper, const int64_t *extent, const int32_t *tile,
-                        tre_dtype in_dtype, const int32_t *u_keys, int64_t n_u, const void *u_tiles,
+                        int32_t in_dtype, const int32_t *u_keys, int64_t n_u, const void *u_tiles,
                         const int32_t *v_keys, int64_t n_v, const void *v_tiles, const int32_t *x_keys,
                         int64_t n_x, const void *x_tiles, int32_t *w_keys, float *w_tiles, int64_t w_cap,
                         int64_t *n_w, int64_t *n_triples, void *ws, size_t ws_bytes, void *stream,

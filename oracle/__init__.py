@@ -29,7 +29,11 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "tre_oracle.c")
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# TRE_HOST_SANITIZED=1: the AddressSanitizer / UBSan build (clang, the same
+# sanitizer runtime as the library's sanitized host build)
+_SANITIZED = os.environ.get("TRE_HOST_SANITIZED") == "1"
+_LIB_PATH = os.path.join(_HERE, "liboracle_san.so" if _SANITIZED else "liboracle.so")
+_CLANG = "/opt/rocm/llvm/bin/clang"
 
 ERRORS = {
     0: "OK",
@@ -54,10 +58,17 @@ class OracleError(RuntimeError):
 
 
 def build(force: bool = False) -> str:
-    """Compile the oracle with gcc (plain C, -O2, no OpenMP)."""
+    """Compile the oracle with gcc (plain C, -O2, no OpenMP); with
+    TRE_HOST_SANITIZED=1, with clang and AddressSanitizer + UBSan instead."""
     if force or not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
         tmp = _LIB_PATH + ".tmp"
-        subprocess.check_call(["gcc", "-O2", "-std=c11", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"])
+        if _SANITIZED:
+            cmd = [_CLANG, "-O1", "-g", "-std=c11", "-shared", "-fPIC", "-fno-omit-frame-pointer",
+                   "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-shared-libsan", "-o", tmp,
+                   _SRC, "-lm"]
+        else:
+            cmd = ["gcc", "-O2", "-std=c11", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"]
+        subprocess.check_call(cmd)
         os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
 

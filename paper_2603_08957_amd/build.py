@@ -51,6 +51,50 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+SAN_LIB = os.path.join(HERE, "libtre_host_san.so")
+SAN_OBJ = os.path.join(HERE, "_build_san")
+# AddressSanitizer + UBSan on the host code only (-Xarch_host keeps them off
+# the gfx950 device pass, which is built as usual), linked against the
+# compiler's shared sanitizer runtime
+SAN_FLAGS = [
+    "-O1", "-g", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-fno-omit-frame-pointer",
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Xarch_host", "-fsanitize=address,undefined", "-Xarch_host", "-fno-sanitize-recover=undefined",
+    "-Xarch_host", "-shared-libsan", "-I", os.path.join(ROOT, "include"),
+]
+
+
+def build_host_sanitized(verbose: bool = False) -> str:
+    """Build ``libtre_host_san.so``: the library with its host code (plan
+    parsing, classification, workspace layout, argument checks, launch
+    set-up) under AddressSanitizer and UBSan, for the CPU tests
+    (``tests/sanitize.sh``); never loaded unless TRE_HOST_SANITIZED=1."""
+    os.makedirs(SAN_OBJ, exist_ok=True)
+
+    def one(src):
+        obj = os.path.join(SAN_OBJ, os.path.basename(src) + ".o")
+        cmd = [HIPCC, "-x", "hip", *SAN_FLAGS, "-c", src, "-o", obj]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stderr}")
+        return obj
+
+    with cf.ThreadPoolExecutor(max_workers=min(8, os.cpu_count() or 1)) as ex:
+        objs = list(ex.map(one, sources()))
+    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-Xarch_host", "-fsanitize=address,undefined",
+           "-Xarch_host", "-shared-libsan", "-o", SAN_LIB + ".tmp", *objs]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stderr}")
+    os.replace(SAN_LIB + ".tmp", SAN_LIB)
+    if verbose:
+        print(f"built {SAN_LIB}")
+    return SAN_LIB
+
+
 if __name__ == "__main__":
-    build(verbose=True)
+    if "--host-sanitized" in sys.argv:
+        build_host_sanitized(verbose=True)
+    else:
+        build(verbose=True)
     sys.exit(0)

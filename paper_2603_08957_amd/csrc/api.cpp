@@ -1,5 +1,5 @@
 // C-ABI entry points: argument checks, workspace layout, phase ordering,
-// the two count read-backs of the join, capacity checks and timing.
+// the join's one count read-back, capacity checks and timing.
 #include <algorithm>
 #include <cmath>
 #include <cstring>
@@ -121,6 +121,17 @@ int64_t choose_unit(const Plan& p, const Layout& L, int64_t n_pairs, int64_t n_w
     return std::max<int64_t>(pu, std::max<int64_t>(need, 1));
 }
 
+// Most pairs a join of n_u and n_v tuples (unique keys) can make: the cross
+// product, or one pair per tuple of the other side when one side's key is
+// made of join labels only.  The GROUP BY grids are sized for min(this,
+// workspace capacity).
+int64_t pair_bound(const Plan& p, int64_t n_u, int64_t n_v) {
+    int64_t b = (n_v > 0 && n_u > INT64_MAX / n_v) ? INT64_MAX : n_u * n_v;
+    if (p.nk[0] == p.n_join) b = std::min(b, n_v);  // a V tuple meets at most one U tuple
+    if (p.nk[1] == p.n_join) b = std::min(b, n_u);
+    return b;
+}
+
 }  // namespace
 
 extern "C" {
@@ -208,7 +219,16 @@ tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const i
         }
         return TRE_OK;
     }
-    if (n_u > 0 && n_v > 0) {
+    // the join counts the pairs into the header; the GROUP BY stage reads
+    // that count on the device (its grids are sized for the workspace's
+    // capacity), so one read-back at the end returns the key checks, the
+    // pair count and the key count together
+    if (n_u > 0 && n_v > 0 && max_pairs > 0) {
+        if ((e = launch_join(p, L, w, u_keys, v_keys, s, 0)) != hipSuccess) return dev_fail(e, "join");
+        const int64_t cap = std::min(max_pairs, pair_bound(p, n_u, n_v));
+        if ((e = launch_group(p, L, w, u_keys, v_keys, cap, s)) != hipSuccess) return dev_fail(e, "group");
+    } else if (n_u > 0 && n_v > 0) {
+        // no room for any pair: count only, to report the size needed
         if ((e = launch_join(p, L, w, u_keys, v_keys, s, 0)) != hipSuccess) return dev_fail(e, "join");
     }
     if ((e = hipMemcpyAsync(&h, hdr, sizeof(h), hipMemcpyDeviceToHost, s)) != hipSuccess)
@@ -230,14 +250,7 @@ tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const i
         set_error("tre_join: more than 2^31 - 1 pairs");
         return TRE_E_SHAPE;
     }
-    int64_t n_w = 0;
-    if (n_pairs > 0) {
-        if ((e = launch_group(p, L, w, u_keys, v_keys, n_pairs, s, 0)) != hipSuccess) return dev_fail(e, "group");
-        if ((e = hipMemcpyAsync(&h, hdr, sizeof(h), hipMemcpyDeviceToHost, s)) != hipSuccess)
-            return dev_fail(e, "key read-back");
-        if ((e = hipStreamSynchronize(s)) != hipSuccess) return dev_fail(e, "group sync");
-        n_w = h.n_w;
-    }
+    const int64_t n_w = n_pairs > 0 ? h.n_w : 0;
     tm.mark(s);
     out->n_w = n_w;
     out->internal[0] = kMagic;

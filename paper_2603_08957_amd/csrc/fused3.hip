@@ -811,7 +811,7 @@ size_t tre_execute3_workspace_bytes(const char* einsum, const char* upper, const
 }
 
 tre_status tre_execute3(const char* einsum, const char* upper, const int64_t* extent, const int32_t* tile,
-                        tre_dtype in_dtype, const int32_t* u_keys, int64_t n_u, const void* u_tiles,
+                        int32_t in_dtype, const int32_t* u_keys, int64_t n_u, const void* u_tiles,
                         const int32_t* v_keys, int64_t n_v, const void* v_tiles, const int32_t* x_keys,
                         int64_t n_x, const void* x_tiles, int32_t* w_keys, float* w_tiles, int64_t w_cap,
                         int64_t* n_w, int64_t* n_triples, void* ws, size_t ws_bytes, void* stream,

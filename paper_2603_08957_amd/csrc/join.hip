@@ -6,7 +6,10 @@
 //            V's key order does not start with the join labels; for every U
 //            tuple binary-search the run of equal join keys in V, then an
 //            exclusive scan of the run lengths gives each U tuple its first
-//            pair index and the total pair count.
+//            pair index and the total pair count.  When W's key is V's key
+//            prefix followed by the join labels (and U's key starts with
+//            them), the roles turn: every V tuple searches its run of U
+//            tuples and the pairs come out already grouped by W key.
 //   stage 1  load-balanced expansion: a thread owns 8 consecutive pair
 //            indices, finds the U tuple of the first by binary search over
 //            the scanned counts and walks forward, so hub tuples with long
@@ -166,6 +169,66 @@ __global__ void k_store_count(const int64_t* __restrict__ off, int64_t n_u, WsHe
     hdr->n_pairs = off[n_u];
 }
 
+// The join driven by V when U's key is exactly the join labels: a V tuple
+// meets at most one U tuple.  k_vmatch1 finds it (flag[v] = 1, uidx[v] = u)
+// by a search over U's rows that starts, for a one-attribute key, at the
+// position the key would have if U's keys were spread evenly over their
+// range (exact when every key is present) and gallops from there; an
+// exclusive scan of the flags gives every matched V tuple its pair index.
+__device__ inline int64_t find_row(const int32_t* __restrict__ ukeys, int64_t n_u, int ru, const int32_t* key,
+                                   int n, int32_t radix0) {
+    int64_t a = 0, b = n_u;  // the lower bound of key lies in [a, b]
+    if (ru == 1 && n == 1 && radix0 > 0 && n_u > 0) {
+        const int32_t k = key[0];
+        // clamped: keys outside [0, radix0) only come from unvalidated input
+        const int64_t g = max<int64_t>(0, min<int64_t>(n_u - 1, int64_t(k) * n_u / radix0));
+        if (ukeys[g] < k) {  // gallop right: the bound is in (prev, pos]
+            int64_t prev = g, step = 1, pos = g + 1;
+            while (pos < n_u && ukeys[pos] < k) {
+                prev = pos;
+                step <<= 1;
+                pos = g + step;
+            }
+            a = prev + 1;
+            b = min(pos, n_u);
+        } else {  // gallop left: the bound is in (pos, hi]
+            int64_t hi = g, step = 1, pos = g - 1;
+            while (pos >= 0 && ukeys[pos] >= k) {
+                hi = pos;
+                step <<= 1;
+                pos = g - step;
+            }
+            a = pos < 0 ? 0 : pos + 1;
+            b = hi;
+        }
+    }
+    while (a < b) {
+        const int64_t m = (a + b) >> 1;
+        if (cmp_prefix(ukeys + m * ru, key, n) < 0) a = m + 1; else b = m;
+    }
+    return (a < n_u && cmp_prefix(ukeys + a * ru, key, n) == 0) ? a : -1;
+}
+
+__global__ void k_vmatch1(const int32_t* __restrict__ vkeys, int64_t n_v, int rv, KeyDesc dv,
+                          const int32_t* __restrict__ ukeys, int64_t n_u, int ru, int32_t radix0,
+                          int32_t* __restrict__ flag, int32_t* __restrict__ uidx) {
+    const int64_t v = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (v > n_v) return;
+    if (v == n_v) {
+        flag[v] = 0;
+        return;
+    }
+    int32_t key[26];
+    for (int i = 0; i < dv.n; i++) key[i] = vkeys[v * rv + dv.pos[i]];
+    const int64_t u = find_row(ukeys, n_u, ru, key, dv.n, radix0);
+    flag[v] = u >= 0 ? 1 : 0;
+    uidx[v] = int32_t(u);
+}
+
+__global__ void k_store_count32(const int32_t* __restrict__ pos, int64_t n, WsHeader* hdr) {
+    hdr->n_pairs = pos[n];
+}
+
 __device__ inline uint64_t pack_w(const int32_t* urow, const int32_t* vrow, const WDesc& d) {
     uint64_t k = 0;
     for (int i = 0; i < d.n; i++) {
@@ -215,9 +278,16 @@ __device__ inline int64_t wave_find_u(const int64_t* __restrict__ off, int64_t x
     return a;
 }
 
-template <typename KT>
+// The pair count comes from device memory (the scan's total in the
+// header), clamped to the capacity `cap` the grid is sized for.
+__device__ inline int64_t pair_count(const WsHeader* hdr, int64_t cap) { return min(hdr->n_pairs, cap); }
+
+// VO: the outer relation (whose runs `off` / `lo` describe) is V and the
+// runs index U (the join driven by V); otherwise the outer relation is U.
+template <typename KT, bool VO>
 __global__ __launch_bounds__(kThreads) void k_expand(const int64_t* __restrict__ off, const int64_t* __restrict__ lo,
-                                                     int64_t n_u, int64_t n_pairs, const uint32_t* __restrict__ vperm,
+                                                     int64_t n_u, const WsHeader* __restrict__ hdr, int64_t cap,
+                                                     const uint32_t* __restrict__ vperm,
                                                      const int32_t* __restrict__ ukeys, int ru,
                                                      const int32_t* __restrict__ vkeys, int rv, WDesc wd,
                                                      int32_t* __restrict__ pu, int32_t* __restrict__ pv,
@@ -225,6 +295,7 @@ __global__ __launch_bounds__(kThreads) void k_expand(const int64_t* __restrict__
     constexpr int kBlockPairs = kThreads * kPairsPerThread;
     __shared__ int32_t s_off[kSpan + 1];  // pair counts stay below 2^31
     __shared__ int64_t s_ends[2];
+    const int64_t n_pairs = pair_count(hdr, cap);
     const int64_t b0 = int64_t(blockIdx.x) * kBlockPairs;
     if (b0 >= n_pairs) return;
     const int64_t b1 = min<int64_t>(b0 + kBlockPairs, n_pairs);
@@ -287,14 +358,33 @@ __global__ __launch_bounds__(kThreads) void k_expand(const int64_t* __restrict__
     for (int i = 0; i < kPairsPerThread; i++) {
         if (u[i] < 0) continue;
         const int64_t p = b0 + int64_t(i) * kThreads + threadIdx.x;
-        wk[p] = KT(pack_w(ukeys + int64_t(u[i]) * ru, vkeys + int64_t(vv[i]) * rv, wd));
+        const int32_t iu = VO ? vv[i] : u[i], iv = VO ? u[i] : vv[i];  // (outer, run) -> (u, v)
+        wk[p] = KT(pack_w(ukeys + int64_t(iu) * ru, vkeys + int64_t(iv) * rv, wd));
         if (uv) {
-            uv[p] = (uint64_t(uint32_t(u[i])) << 32) | uint64_t(uint32_t(vv[i]));
+            uv[p] = (uint64_t(uint32_t(iu)) << 32) | uint64_t(uint32_t(iv));
         } else {
-            pu[p] = int32_t(u[i]);
-            pv[p] = int32_t(vv[i]);
+            pu[p] = iu;
+            pv[p] = iv;
         }
     }
+}
+
+// Pairs of the join driven by V with at most one U tuple per V tuple:
+// matched V tuple v writes pair pos[v] = (uidx[v], v) and its W key.  Pair
+// indices follow V order, so consecutive threads write consecutive pairs.
+template <typename KT>
+__global__ void k_vwrite(const int32_t* __restrict__ pos, const int32_t* __restrict__ uidx, int64_t n_v,
+                         const WsHeader* __restrict__ hdr, int64_t cap, const int32_t* __restrict__ ukeys, int ru,
+                         const int32_t* __restrict__ vkeys, int rv, WDesc wd, int32_t* __restrict__ pu,
+                         int32_t* __restrict__ pv, KT* __restrict__ wk) {
+    const int64_t v = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (v >= n_v) return;
+    const int64_t p = pos[v];
+    if (pos[v + 1] == p || p >= pair_count(hdr, cap)) return;
+    const int32_t u = uidx[v];
+    pu[p] = u;
+    pv[p] = int32_t(v);
+    wk[p] = KT(pack_w(ukeys + int64_t(u) * ru, vkeys + v * rv, wd));
 }
 
 // Join with a keyless single-tuple V whose output is keyed by U's own key
@@ -321,12 +411,16 @@ __global__ void k_keyed_by_u(const int32_t* __restrict__ ukeys, int64_t n_u, int
 // index of key k's first pair (0: absent), then the present keys are
 // compacted in key order by a scan over the key space instead of over the
 // pairs.
+// (keys outside the key space come only from keys that fail validation,
+// which the host reports; they are skipped so nothing is written out of
+// bounds)
 template <typename KT>
-__global__ void k_first_of_key(const KT* __restrict__ wk, int64_t n, int32_t* __restrict__ first) {
+__global__ void k_first_of_key(const KT* __restrict__ wk, const WsHeader* __restrict__ hdr, int64_t cap,
+                               int64_t nk, int32_t* __restrict__ first) {
     const int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (p >= n) return;
+    if (p >= pair_count(hdr, cap)) return;
     const KT k = wk[p];
-    if (p == 0 || k != wk[p - 1]) first[k] = int32_t(p + 1);
+    if ((p == 0 || k != wk[p - 1]) && uint64_t(k) < uint64_t(nk)) first[k] = int32_t(p + 1);
 }
 
 __global__ void k_key_flags(const int32_t* __restrict__ first, int64_t nk, int32_t* __restrict__ flags) {
@@ -336,12 +430,12 @@ __global__ void k_key_flags(const int32_t* __restrict__ first, int64_t nk, int32
 }
 
 __global__ void k_key_compact(const int32_t* __restrict__ first, int64_t nk, const int32_t* __restrict__ seg_of,
-                              int64_t n_pairs, int32_t* __restrict__ seg_start, uint64_t* __restrict__ seg_key,
+                              int64_t cap, int32_t* __restrict__ seg_start, uint64_t* __restrict__ seg_key,
                               WsHeader* hdr) {
     const int64_t q = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (q > nk) return;
     if (q == nk) {
-        seg_start[seg_of[nk]] = int32_t(n_pairs);
+        seg_start[seg_of[nk]] = int32_t(pair_count(hdr, cap));
         hdr->n_w = seg_of[nk];
         return;
     }
@@ -352,17 +446,22 @@ __global__ void k_key_compact(const int32_t* __restrict__ first, int64_t nk, con
     }
 }
 
+// flags over [0, cap] (zero from the pair count on, so the scan over the
+// capacity counts the segments of the pairs only)
 template <typename KT>
-__global__ void k_heads(const KT* __restrict__ wk, int64_t n, int32_t* __restrict__ flags) {
+__global__ void k_heads(const KT* __restrict__ wk, const WsHeader* __restrict__ hdr, int64_t cap,
+                        int32_t* __restrict__ flags) {
     const int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (p > n) return;
+    if (p > cap) return;
+    const int64_t n = pair_count(hdr, cap);
     flags[p] = (p < n && (p == 0 || wk[p] != wk[p - 1])) ? 1 : 0;
 }
 
 template <typename KT>
-__global__ void k_compact(const KT* __restrict__ wk, int64_t n, const int32_t* __restrict__ seg_of,
+__global__ void k_compact(const KT* __restrict__ wk, int64_t cap, const int32_t* __restrict__ seg_of,
                           int32_t* __restrict__ seg_start, uint64_t* __restrict__ seg_key, WsHeader* hdr) {
     const int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    const int64_t n = pair_count(hdr, cap);
     if (p > n) return;
     if (p == n) {
         seg_start[seg_of[n]] = int32_t(n);
@@ -423,6 +522,26 @@ hipError_t launch_join(const Plan& p, const Layout& L, char* ws, const int32_t* 
     int32_t* hist = reinterpret_cast<int32_t*>(ws + L.hist);
     const int64_t n_u = L.n_u, n_v = L.n_v;
     hipError_t e = hipSuccess;
+    if (p.v_outer && p.nk[0] == p.n_join) {
+        // walk V: each V tuple meets at most one U tuple (U's key is the join labels)
+        int32_t* pos = reinterpret_cast<int32_t*>(ws + L.ucnt);
+        int32_t* uidx = reinterpret_cast<int32_t*>(ws + L.ulo);
+        k_vmatch1<<<blocks_for(n_v + 1), kThreads, 0, s>>>(v_keys, n_v, p.nk[1], desc_v(p), u_keys, n_u, p.nk[0],
+                                                            p.nk[0] == 1 ? p.radix[0][0] : 0, pos, uidx);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = scan_exclusive_i32(pos, pos, n_v + 1, reinterpret_cast<int32_t*>(tmp), s)) != hipSuccess) return e;
+        k_store_count32<<<1, 1, 0, s>>>(pos, n_v, hdr);
+        return hipGetLastError();
+    }
+    if (p.v_outer) {
+        // walk V: each V tuple's run of U tuples, searched on U's key prefix
+        k_count_prefix<<<blocks_for(n_v + 1), kThreads, 0, s>>>(v_keys, n_v, p.nk[1], desc_v(p), u_keys, n_u,
+                                                                 p.nk[0], cnt, lo);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = scan_exclusive_i64(cnt, cnt, n_v + 1, tmp, s)) != hipSuccess) return e;
+        k_store_count<<<1, 1, 0, s>>>(cnt, n_v, hdr);
+        return hipGetLastError();
+    }
     if (p.n_join > 0 && n_v > 0 && !p.v_needs_sort) {
         // the join labels lead V's key: search V's rows as they are
         k_count_prefix<<<blocks_for(n_u + 1), kThreads, 0, s>>>(u_keys, n_u, p.nk[0], desc_u(p), v_keys, n_v,
@@ -449,7 +568,9 @@ namespace {
 
 template <typename KT>
 hipError_t group_impl(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
-                      int64_t n_pairs, hipStream_t s) {
+                      int64_t cap, hipStream_t s) {
+    // every grid below is sized for the capacity; the kernels read the
+    // pair count itself from the header
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
     int64_t* off = reinterpret_cast<int64_t*>(ws + L.ucnt);
     int64_t* lo = reinterpret_cast<int64_t*>(ws + L.ulo);
@@ -472,44 +593,54 @@ hipError_t group_impl(const Plan& p, const Layout& L, char* ws, const int32_t* u
         wd.bits[c] = p.w_bits[c];
     }
     hipError_t e;
-    const bool sort = p.group_needs_sort && n_pairs > 1 && p.w_total_bits > 0;
+    const bool sort = p.group_needs_sort && cap > 1 && p.w_total_bits > 0;
     uint64_t* uv = sort ? reinterpret_cast<uint64_t*>(ws + L.pidx) : nullptr;
-    if (n_pairs > 0) {
-        const int64_t threads = (n_pairs + kPairsPerThread - 1) / kPairsPerThread;
-        k_expand<KT><<<blocks_for(threads), kThreads, 0, s>>>(off, lo, L.n_u, n_pairs, vperm, u_keys, p.nk[0], v_keys,
-                                                              p.nk[1], wd, pu, pv, wk, uv);
+    if (cap > 0 && p.v_outer && p.nk[0] == p.n_join) {
+        k_vwrite<KT><<<blocks_for(L.n_v), kThreads, 0, s>>>(
+            reinterpret_cast<const int32_t*>(ws + L.ucnt), reinterpret_cast<const int32_t*>(ws + L.ulo), L.n_v, hdr,
+            cap, u_keys, p.nk[0], v_keys, p.nk[1], wd, pu, pv, wk);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    } else if (cap > 0) {
+        const int64_t threads = (cap + kPairsPerThread - 1) / kPairsPerThread;
+        if (p.v_outer)
+            k_expand<KT, true><<<blocks_for(threads), kThreads, 0, s>>>(off, lo, L.n_v, hdr, cap, nullptr, u_keys,
+                                                                        p.nk[0], v_keys, p.nk[1], wd, pu, pv, wk, uv);
+        else
+            k_expand<KT, false><<<blocks_for(threads), kThreads, 0, s>>>(off, lo, L.n_u, hdr, cap, vperm, u_keys,
+                                                                         p.nk[0], v_keys, p.nk[1], wd, pu, pv, wk, uv);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (sort) {
         // the last pass writes the sorted (u, v) straight into pu / pv
         KT* wk_alt = reinterpret_cast<KT*>(ws + L.wk_alt);
         uint64_t* uv_alt = reinterpret_cast<uint64_t*>(ws + L.pidx_alt);
+        const int64_t* dn = &hdr->n_pairs;
         if constexpr (sizeof(KT) == 4)
-            e = radix_sort_u32_pairs(wk, uv, wk_alt, uv_alt, n_pairs, p.w_total_bits, hist, tmp, pu, pv, s);
+            e = radix_sort_u32_pairs(wk, uv, wk_alt, uv_alt, cap, dn, p.w_total_bits, hist, tmp, pu, pv, s);
         else
-            e = radix_sort_u64_pairs(wk, uv, wk_alt, uv_alt, n_pairs, p.w_total_bits, hist, tmp, pu, pv, s);
+            e = radix_sort_u64_pairs(wk, uv, wk_alt, uv_alt, cap, dn, p.w_total_bits, hist, tmp, pu, pv, s);
         if (e != hipSuccess) return e;
-        if (radix_result_in_alt(n_pairs, p.w_total_bits)) wk = wk_alt;
+        if (radix_result_in_alt(cap, p.w_total_bits)) wk = wk_alt;
     }
     const int64_t key_space = int64_t(1) << p.w_total_bits;
-    if (p.w_total_bits > 0 && p.w_total_bits <= 30 && key_space <= n_pairs) {
+    if (p.w_total_bits > 0 && p.w_total_bits <= 30 && key_space <= cap) {
         // small key space: find the segments by key instead of by pair
         int32_t* first = flags;  // key_space + 1 <= n_pairs + 1 entries
         int32_t* kflags = reinterpret_cast<int32_t*>(ws + L.part_off);  // free until the work units are made
         if ((e = launch_fill_zero(first, sizeof(int32_t) * size_t(key_space), s)) != hipSuccess) return e;
-        k_first_of_key<KT><<<blocks_for(n_pairs), kThreads, 0, s>>>(wk, n_pairs, first);
+        k_first_of_key<KT><<<blocks_for(cap), kThreads, 0, s>>>(wk, hdr, cap, key_space, first);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         k_key_flags<<<blocks_for(key_space + 1), kThreads, 0, s>>>(first, key_space, kflags);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if ((e = scan_exclusive_i32(kflags, kflags, key_space + 1, tmp, s)) != hipSuccess) return e;
-        k_key_compact<<<blocks_for(key_space + 1), kThreads, 0, s>>>(first, key_space, kflags, n_pairs, seg_start,
+        k_key_compact<<<blocks_for(key_space + 1), kThreads, 0, s>>>(first, key_space, kflags, cap, seg_start,
                                                                       seg_key, hdr);
         return hipGetLastError();
     }
-    k_heads<KT><<<blocks_for(n_pairs + 1), kThreads, 0, s>>>(wk, n_pairs, flags);
+    k_heads<KT><<<blocks_for(cap + 1), kThreads, 0, s>>>(wk, hdr, cap, flags);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = scan_exclusive_i32(flags, flags, n_pairs + 1, tmp, s)) != hipSuccess) return e;
-    k_compact<KT><<<blocks_for(n_pairs + 1), kThreads, 0, s>>>(wk, n_pairs, flags, seg_start, seg_key, hdr);
+    if ((e = scan_exclusive_i32(flags, flags, cap + 1, tmp, s)) != hipSuccess) return e;
+    k_compact<KT><<<blocks_for(cap + 1), kThreads, 0, s>>>(wk, cap, flags, seg_start, seg_key, hdr);
     return hipGetLastError();
 }
 
@@ -538,10 +669,10 @@ hipError_t launch_keyed_by_u(const Plan& p, const Layout& L, char* ws, const int
 }
 
 hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
-                        int64_t n_pairs, hipStream_t s, int stage) {
-    (void)stage;
-    return p.w_total_bits <= 32 ? group_impl<uint32_t>(p, L, ws, u_keys, v_keys, n_pairs, s)
-                                : group_impl<uint64_t>(p, L, ws, u_keys, v_keys, n_pairs, s);
+                        int64_t cap, hipStream_t s) {
+    if (cap < 0 || cap > L.max_pairs) return hipErrorInvalidValue;
+    return p.w_total_bits <= 32 ? group_impl<uint32_t>(p, L, ws, u_keys, v_keys, cap, s)
+                                : group_impl<uint64_t>(p, L, ws, u_keys, v_keys, cap, s);
 }
 
 }  // namespace tre

@@ -187,6 +187,23 @@ static tre_status classify(Plan& p) {
     // pairs come out of the join in (u, v) order: already grouped when W's
     // promoted labels are a prefix of U's key
     p.group_needs_sort = !(p.nk[2] == 0 || prefix_of_u);
+    // Otherwise the join can be driven by V instead when V's key is W's key
+    // followed by the join labels and U's key starts with the same join
+    // labels in the same order.  V's tuples of one W key then carry distinct
+    // join keys in increasing order, each meets one run of U tuples (U is
+    // sorted by its join attributes first), and those runs increase with the
+    // join key, so walking V and expanding each tuple's U run gives the pairs
+    // in the canonical (W key, u, v) order directly.
+    if (p.group_needs_sort && p.nk[1] == p.nk[2] + p.n_join) {
+        bool ok = true;
+        for (int c = 0; c < p.nk[2] && ok; c++) ok = p.w_src[c] == 1 && p.w_pos[c] == c;
+        for (int i = 0; i < p.n_join && ok; i++) ok = p.join_pos_v[i] == p.nk[2] + i && p.join_pos_u[i] == i;
+        if (ok) {
+            p.v_outer = true;
+            p.group_needs_sort = false;
+            p.v_needs_sort = false;
+        }
+    }
 
     // ---- tile roles ----
     std::vector<int> bl, ml, nl, kl, pul, pvl;
@@ -420,9 +437,10 @@ Layout make_layout(const Plan& p, int64_t n_u, int64_t n_v, int64_t max_pairs) {
     L.vjk_alt = take(p.v_needs_sort ? sizeof(uint64_t) * size_t(n_v) : 0);
     L.vperm = take(p.v_needs_sort ? sizeof(uint32_t) * size_t(n_v) : 0);
     L.vperm_alt = take(p.v_needs_sort ? sizeof(uint32_t) * size_t(n_v) : 0);
-    L.ucnt = take(sizeof(int64_t) * size_t(n_u + 1));
-    L.ulo = take(sizeof(int64_t) * size_t(std::max<int64_t>(n_u, 1)));
-    int64_t scan_n = std::max<int64_t>({n_u + 1, P + 1, radix_hist_elems(std::max<int64_t>(sort_n, 1))});
+    const int64_t n_outer = p.v_outer ? n_v : n_u;  // the relation whose tuples find their runs
+    L.ucnt = take(sizeof(int64_t) * size_t(n_outer + 1));
+    L.ulo = take(sizeof(int64_t) * size_t(std::max<int64_t>(n_outer, 1)));
+    int64_t scan_n = std::max<int64_t>({n_outer + 1, P + 1, radix_hist_elems(std::max<int64_t>(sort_n, 1))});
     L.scan_tmp = take(sizeof(int64_t) * scan_tmp_elems(scan_n));
     L.pu = take(sizeof(int32_t) * size_t(P));
     L.pv = take(sizeof(int32_t) * size_t(P));
@@ -454,7 +472,7 @@ using namespace tre;
 extern "C" {
 
 tre_status tre_plan(const char* einsum, const char* upper, const int64_t* extent, const int32_t* tile,
-                    tre_dtype in_dtype, const tre_options* opt, tre_plan_t* out) {
+                    int32_t in_dtype, const tre_options* opt, tre_plan_t* out) {
     if (!einsum || !extent || !out) {
         set_error("null argument");
         return TRE_E_ARG;
@@ -468,7 +486,7 @@ tre_status tre_plan(const char* einsum, const char* upper, const int64_t* extent
     if (!h) return TRE_E_ARG;
     Plan& p = h->p;
     p.einsum = einsum;
-    p.dtype = in_dtype;
+    p.dtype = in_dtype == TRE_BF16 ? TRE_BF16 : TRE_F32;
     p.opt.validate_keys = 1;
     if (opt) {
         p.opt = *opt;
@@ -512,6 +530,7 @@ tre_status tre_plan_get_info(tre_plan_t plan, tre_plan_info* info) {
     info->group_needs_sort = p.group_needs_sort;
     info->v_needs_sort = p.v_needs_sort;
     info->w_dtype = p.opt.w_bf16 ? TRE_BF16 : TRE_F32;
+    info->join_outer = p.v_outer ? 1 : 0;
     return TRE_OK;
 }
 

@@ -36,10 +36,16 @@ constexpr int kRadix = 1 << kMaxBits;
 constexpr int kDpt = kRadix / kThreads;  // digits per thread in the prefix step
 static_assert(kDpt >= 1 && kDpt * kThreads == kRadix, "radix must be a multiple of the workgroup size");
 
+// Item count: the host's n, or min(*dn, n) when the count lives in device
+// memory (the grid is then sized for n, the capacity).
+__device__ inline int64_t item_count(int64_t n, const int64_t* dn) { return dn ? min(*dn, n) : n; }
+
 template <typename KT>
-__global__ __launch_bounds__(kThreads) void k_digit_hist(const KT* __restrict__ keys, int64_t n, int shift,
-                                                         int dbits, int32_t* __restrict__ hist, int64_t n_tiles) {
+__global__ __launch_bounds__(kThreads) void k_digit_hist(const KT* __restrict__ keys, int64_t cap,
+                                                         const int64_t* __restrict__ dn, int shift, int dbits,
+                                                         int32_t* __restrict__ hist, int64_t n_tiles) {
     __shared__ int32_t cnt[kRadix];
+    const int64_t n = item_count(cap, dn);
     const int radix = 1 << dbits;
     for (int d = threadIdx.x; d < radix; d += kThreads) cnt[d] = 0;
     __syncthreads();
@@ -66,8 +72,11 @@ template <typename KT, typename VT, bool SPLIT>
 __global__ __launch_bounds__(kThreads) void k_digit_scatter(const KT* __restrict__ kin, const VT* __restrict__ vin,
                                                             KT* __restrict__ kout, VT* __restrict__ vout,
                                                             int32_t* __restrict__ hi_out, int32_t* __restrict__ lo_out,
-                                                            int64_t n, int shift, int dbits,
-                                                            const int32_t* __restrict__ offs, int64_t n_tiles) {
+                                                            int64_t cap, const int64_t* __restrict__ dn, int shift,
+                                                            int dbits, const int32_t* __restrict__ offs,
+                                                            int64_t n_tiles) {
+    const int64_t n = item_count(cap, dn);
+    if (int64_t(blockIdx.x) * kTile >= n) return;  // tiles past the count (their counts are 0)
     __shared__ KT skey[kTile];
     __shared__ VT sval[kTile];
     __shared__ int32_t wcnt[kWaves][kRadix];  // per-(wave, digit) counts, then wave prefixes
@@ -179,8 +188,8 @@ __global__ __launch_bounds__(kThreads) void k_digit_scatter(const KT* __restrict
 int sort_passes(int bits) { return bits <= 0 ? 0 : (bits + kMaxBits - 1) / kMaxBits; }
 
 template <typename KT, typename VT>
-hipError_t sort_impl(KT* keys, VT* vals, KT* keys_alt, VT* vals_alt, int64_t n, int bits, int32_t* hist,
-                     int32_t* scan_tmp, int32_t* split_hi, int32_t* split_lo, hipStream_t s) {
+hipError_t sort_impl(KT* keys, VT* vals, KT* keys_alt, VT* vals_alt, int64_t n, const int64_t* dn, int bits,
+                     int32_t* hist, int32_t* scan_tmp, int32_t* split_hi, int32_t* split_lo, hipStream_t s) {
     if (n <= 1 || bits <= 0) return hipSuccess;
     const int64_t nt = (n + kTile - 1) / kTile;
     const int passes = sort_passes(bits);
@@ -189,15 +198,15 @@ hipError_t sort_impl(KT* keys, VT* vals, KT* keys_alt, VT* vals_alt, int64_t n, 
     VT *vi = vals, *vo = vals_alt;
     for (int p = 0; p < passes; p++) {
         const int shift = dbits * p;
-        k_digit_hist<KT><<<dim3(unsigned(nt)), kThreads, 0, s>>>(ki, n, shift, dbits, hist, nt);
+        k_digit_hist<KT><<<dim3(unsigned(nt)), kThreads, 0, s>>>(ki, n, dn, shift, dbits, hist, nt);
         hipError_t e = scan_exclusive_i32(hist, hist, (int64_t(1) << dbits) * nt, scan_tmp, s);
         if (e != hipSuccess) return e;
         if (split_hi && p == passes - 1)
-            k_digit_scatter<KT, VT, true><<<dim3(unsigned(nt)), kThreads, 0, s>>>(ki, vi, ko, vo, split_hi,
-                                                                                 split_lo, n, shift, dbits, hist, nt);
+            k_digit_scatter<KT, VT, true><<<dim3(unsigned(nt)), kThreads, 0, s>>>(
+                ki, vi, ko, vo, split_hi, split_lo, n, dn, shift, dbits, hist, nt);
         else
-            k_digit_scatter<KT, VT, false><<<dim3(unsigned(nt)), kThreads, 0, s>>>(ki, vi, ko, vo, nullptr, nullptr,
-                                                                                  n, shift, dbits, hist, nt);
+            k_digit_scatter<KT, VT, false><<<dim3(unsigned(nt)), kThreads, 0, s>>>(
+                ki, vi, ko, vo, nullptr, nullptr, n, dn, shift, dbits, hist, nt);
         std::swap(ki, ko);
         std::swap(vi, vo);
     }
@@ -212,22 +221,23 @@ bool radix_result_in_alt(int64_t n, int bits) { return n > 1 && (sort_passes(bit
 
 hipError_t radix_sort_u64(uint64_t* keys, uint32_t* vals, uint64_t* keys_alt, uint32_t* vals_alt, int64_t n,
                           int bits, int32_t* hist, int32_t* scan_tmp, hipStream_t s) {
-    return sort_impl<uint64_t, uint32_t>(keys, vals, keys_alt, vals_alt, n, bits, hist, scan_tmp, nullptr, nullptr, s);
+    return sort_impl<uint64_t, uint32_t>(keys, vals, keys_alt, vals_alt, n, nullptr, bits, hist, scan_tmp, nullptr,
+                                         nullptr, s);
 }
 
 hipError_t radix_sort_u64_pairs(uint64_t* keys, uint64_t* vals, uint64_t* keys_alt, uint64_t* vals_alt, int64_t n,
-                                int bits, int32_t* hist, int32_t* scan_tmp, int32_t* split_hi, int32_t* split_lo,
-                                hipStream_t s) {
-    return sort_impl<uint64_t, uint64_t>(keys, vals, keys_alt, vals_alt, n, bits, hist, scan_tmp, split_hi, split_lo,
-                                         s);
+                                const int64_t* dn, int bits, int32_t* hist, int32_t* scan_tmp, int32_t* split_hi,
+                                int32_t* split_lo, hipStream_t s) {
+    return sort_impl<uint64_t, uint64_t>(keys, vals, keys_alt, vals_alt, n, dn, bits, hist, scan_tmp, split_hi,
+                                         split_lo, s);
 }
 
 hipError_t radix_sort_u32_pairs(uint32_t* keys, uint64_t* vals, uint32_t* keys_alt, uint64_t* vals_alt, int64_t n,
-                                int bits, int32_t* hist, int32_t* scan_tmp, int32_t* split_hi, int32_t* split_lo,
-                                hipStream_t s) {
+                                const int64_t* dn, int bits, int32_t* hist, int32_t* scan_tmp, int32_t* split_hi,
+                                int32_t* split_lo, hipStream_t s) {
     if (bits > 32) return hipErrorInvalidValue;
-    return sort_impl<uint32_t, uint64_t>(keys, vals, keys_alt, vals_alt, n, bits, hist, scan_tmp, split_hi, split_lo,
-                                         s);
+    return sort_impl<uint32_t, uint64_t>(keys, vals, keys_alt, vals_alt, n, dn, bits, hist, scan_tmp, split_hi,
+                                         split_lo, s);
 }
 
 }  // namespace tre

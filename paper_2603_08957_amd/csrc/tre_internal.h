@@ -70,6 +70,11 @@ struct Plan {
     int w_src[26] = {}, w_pos[26] = {}, w_bits[26] = {};
     int w_total_bits = 0;
     bool group_needs_sort = false;
+    // join driven by V: W's key is V's key prefix and V's remaining key
+    // attributes are the join labels, which U's key starts with; each V tuple
+    // then meets one run of U tuples and the pairs come out in (W key, u, v)
+    // order with no sort (see classify)
+    bool v_outer = false;
     // tile roles
     char role[26] = {};
     int64_t nB = 1, nM = 1, nN = 1, nK = 1;
@@ -138,17 +143,20 @@ hipError_t scan_exclusive_i32(const int32_t* in, int32_t* out, int64_t n, int32_
 // `bits` bits.  The passes alternate between the primary and the alt
 // buffers; the sorted result is in the alt buffers iff
 // radix_result_in_alt(n, bits).  The pair variant can split the uint64
-// payload (hi, lo) into two int32 arrays instead (split_hi non-null).
+// payload (hi, lo) into two int32 arrays instead (split_hi non-null).  The
+// pair variants also take the item count from device memory: with dn
+// non-null they sort min(*dn, n) items, n being the capacity the grids and
+// the histogram matrix are sized for (passes and buffers as for n).
 int64_t radix_hist_elems(int64_t n);
 bool radix_result_in_alt(int64_t n, int bits);
 hipError_t radix_sort_u64(uint64_t* keys, uint32_t* vals, uint64_t* keys_alt, uint32_t* vals_alt, int64_t n,
                           int bits, int32_t* hist, int32_t* scan_tmp, hipStream_t s);
 hipError_t radix_sort_u64_pairs(uint64_t* keys, uint64_t* vals, uint64_t* keys_alt, uint64_t* vals_alt, int64_t n,
-                                int bits, int32_t* hist, int32_t* scan_tmp, int32_t* split_hi, int32_t* split_lo,
-                                hipStream_t s);
+                                const int64_t* dn, int bits, int32_t* hist, int32_t* scan_tmp, int32_t* split_hi,
+                                int32_t* split_lo, hipStream_t s);
 hipError_t radix_sort_u32_pairs(uint32_t* keys, uint64_t* vals, uint32_t* keys_alt, uint64_t* vals_alt, int64_t n,
-                                int bits, int32_t* hist, int32_t* scan_tmp, int32_t* split_hi, int32_t* split_lo,
-                                hipStream_t s);
+                                const int64_t* dn, int bits, int32_t* hist, int32_t* scan_tmp, int32_t* split_hi,
+                                int32_t* split_lo, hipStream_t s);
 
 // join.hip
 hipError_t launch_validate(const int32_t* keys, int64_t n, int r, const int32_t* radix, int32_t* err_flag,
@@ -159,8 +167,12 @@ hipError_t launch_join(const Plan& p, const Layout& L, char* ws, const int32_t* 
 // every U tuple is one pair and one group, written without counting
 bool keyed_by_u(const Plan& p);
 hipError_t launch_keyed_by_u(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, hipStream_t s);
+// GROUP BY stage: the pair count is read on the device from the workspace
+// header (written by launch_join), clamped to the capacity `cap` (at most
+// L.max_pairs) that every grid is sized for, so the host launches it
+// without waiting
 hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
-                        int64_t n_pairs, hipStream_t s, int stage);
+                        int64_t cap, hipStream_t s);
 
 // contract.hip
 hipError_t launch_tables(const Plan& p, int32_t* tables, hipStream_t s);

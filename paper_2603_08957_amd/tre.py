@@ -13,7 +13,10 @@ from dataclasses import dataclass
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libtre.so")
+# TRE_HOST_SANITIZED=1 loads the host-only AddressSanitizer / UBSan build
+# (no device code) for the CPU tests; see build.build_host_sanitized
+SANITIZED = os.environ.get("TRE_HOST_SANITIZED") == "1"
+LIB_PATH = os.path.join(_HERE, "libtre_host_san.so" if SANITIZED else "libtre.so")
 
 STATUS = {
     0: "TRE_OK", 1: "TRE_E_ARG", 2: "TRE_E_PARSE", 3: "TRE_E_SPLIT", 4: "TRE_E_SHAPE", 5: "TRE_E_DTYPE",
@@ -51,7 +54,8 @@ class PlanInfo(ctypes.Structure):
                 ("kernel_class", ctypes.c_int32), ("batch", ctypes.c_int64), ("m", ctypes.c_int64),
                 ("n", ctypes.c_int64), ("k", ctypes.c_int64), ("flops_per_pair", ctypes.c_int64),
                 ("key_labels", (ctypes.c_char * 27) * 3), ("roles", ctypes.c_char * 27),
-                ("group_needs_sort", ctypes.c_int32), ("v_needs_sort", ctypes.c_int32), ("w_dtype", ctypes.c_int32)]
+                ("group_needs_sort", ctypes.c_int32), ("v_needs_sort", ctypes.c_int32), ("w_dtype", ctypes.c_int32),
+                ("join_outer", ctypes.c_int32)]
 
 
 class JoinResult(ctypes.Structure):
@@ -177,6 +181,7 @@ class Plan:
         self.group_needs_sort = bool(info.group_needs_sort)
         self.v_needs_sort = bool(info.v_needs_sort)
         self.w_dtype = {0: "f32", 1: "bf16"}[info.w_dtype]
+        self.join_outer = "v" if info.join_outer else "u"
 
     @classmethod
     def from_spec(cls, spec: dict, **kw):

@@ -74,9 +74,33 @@ def test_roles_of_the_paper_examples(tre):
     # per-vertex vectors and scalar edges: a scale kernel
     p = tre.Plan("ij,jk->ki", "jk", {"i": 256, "j": 1 << 20, "k": 1 << 20}, {"j": 1, "k": 1}, "bf16")
     assert p.kernel_class == "vec" and p.bmnk == (1, 256, 1, 1)
-    # V keyed (K, J): join label not a prefix -> V is sorted on the device
+    # V keyed (K, J) with W keyed K: the join walks V and the pairs come out
+    # grouped by K, nothing is sorted
     p = tre.Plan("ij,kj->ik", "jk", {"i": 8, "j": 8, "k": 8}, {"j": 2, "k": 2}, "f32")
-    assert p.v_needs_sort
+    assert p.join_outer == "v" and not p.v_needs_sort and not p.group_needs_sort
+    # V keyed (K, J) with K summed: V is sorted by its join key on the device
+    p = tre.Plan("ij,kj->i", "jk", {"i": 8, "j": 8, "k": 8}, {"j": 2, "k": 2}, "f32")
+    assert p.join_outer == "u" and p.v_needs_sort
+    # V keyed (J, K): the join walks U and the pairs are sorted by K
+    p = tre.Plan("ij,jk->ki", "jk", {"i": 8, "j": 8, "k": 8}, {"j": 2, "k": 2}, "f32")
+    assert p.join_outer == "u" and p.group_needs_sort and not p.v_needs_sort
+
+
+@pytest.mark.parametrize("e,upper,outer", [
+    ("ij,kj->ki", "jk", "v"),      # adjacency keyed by destination, then source
+    ("ja,kj->k", "jka", "v"),      # U keyed (J, A): each V tuple meets a run of U tuples
+    ("jlx,kjl->kx", "jlk", "v"),   # two join labels, in the same order in U and V
+    ("jx,kmj->kmx", "jkm", "v"),   # W keyed by two of V's labels
+    ("jlx,klj->kx", "jlk", "u"),   # join labels in another order in V than in U
+    ("ix,kj->ki", "ijk", "u"),     # W takes a label from U
+    ("jx,jk->kx", "jk", "u"),      # V keyed (J, K): W's label is not V's prefix
+])
+def test_join_direction(tre, e, upper, outer):
+    ext = {c: 8 for c in set(e) if c.isalpha()}
+    p = tre.Plan(e, upper, ext, {c: 2 for c in upper}, "f32")
+    assert p.join_outer == outer, (e, p.join_outer)
+    if outer == "v":
+        assert not p.group_needs_sort and not p.v_needs_sort
 
 
 @pytest.mark.parametrize("e,upper,ext,til,cat", [

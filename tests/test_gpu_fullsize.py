@@ -150,7 +150,7 @@ def run_gnn(orc, c):
     torch.cuda.empty_cache()
     # closed forms: one pair per Y tuple (X holds every J); keys = distinct K
     assert o1.n_pairs == len(Y["keys"])
-    assert np.array_equal(o1.w_keys.cpu().numpy()[:, 0], np.unique(Y["keys"][:, 1]))
+    assert np.array_equal(o1.w_keys.cpu().numpy()[:, 0], np.unique(Y["keys"][:, w["y_k_col"]]))
     pairs = o1.pairs.cpu().numpy()
     rng = np.random.default_rng(100 + c)
     S1 = pick(rng, o1.w_keys.cpu().numpy(), 6)
@@ -181,7 +181,7 @@ def chain_end_to_end(orc, w, e2_keys, e2_tiles, rng, n_keys):
     S2 = pick(rng, e2_keys, n_keys)
     t2, t1 = w["tile_e2"], w["tile_e1"]
     need = np.unique(np.concatenate([np.arange(k * t2 // t1, (k + 1) * t2 // t1) for k in S2[:, 0]]))
-    have = set(np.unique(Y["keys"][:, 1]).tolist())
+    have = set(np.unique(Y["keys"][:, w["y_k_col"]]).tolist())
     need = np.array([k for k in need if k in have], dtype=np.int32).reshape(-1, 1)
     op1 = orc_plan(orc, w["E1"])
     mu, mv = orc.restrict(op1, w["X"]["keys"], Y["keys"], need)

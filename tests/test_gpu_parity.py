@@ -687,3 +687,58 @@ def test_w_bf16_gpu(case):
     with pytest.raises(tre.TreError) as ei:
         tre.Plan(*generic, w_bf16=True)
     assert ei.value.status == "TRE_E_DTYPE"
+
+
+V_OUTER_PLANS = [
+    # (einsum, upper, extents, tiles, dtype, keep of V): joins the plan drives
+    # from V (W's key is V's key prefix, then the join labels, which U's key
+    # starts with); pairs come out grouped with no sort
+    ("ij,kj->ki", "jk", {"i": 64, "j": 300, "k": 300}, {"j": 1, "k": 1}, "bf16", 0.05),
+    ("ij,kj->ki", "jk", {"i": 64, "j": 512, "k": 512}, {"j": 64, "k": 64}, "f32", 0.5),
+    ("ij,kj->ki", "jk", {"i": 128, "j": 1024, "k": 512}, {"j": 128, "k": 128}, "bf16", 0.6),
+    ("ja,kj->k", "jka", {"j": 40, "a": 12, "k": 40}, {"j": 4, "a": 3, "k": 4}, "f32", 0.5),
+    ("jlx,kjl->kx", "jlk", {"j": 16, "l": 12, "x": 8, "k": 20}, {"j": 2, "l": 3, "k": 4}, "f32", 0.4),
+    ("jx,kmj->kmx", "jkm", {"j": 24, "x": 16, "k": 12, "m": 8}, {"j": 3, "k": 2, "m": 2}, "bf16", 0.5),
+]
+
+
+@pytest.mark.parametrize("idx", range(len(V_OUTER_PLANS)))
+@pytest.mark.parametrize("validate", [True, False])
+def test_v_outer_join_gpu(orc, idx, validate):
+    """Joins driven by V: pair list, keys and values against the oracle, with
+    U missing some join keys (unmatched V tuples) and key validation on or
+    off."""
+    import paper_2603_08957_amd as tre
+
+    e, upper, ext, til, dtype, keep_v = V_OUTER_PLANS[idx]
+    rng = np.random.default_rng(500 + idx)
+    u_lab, v_lab, _ = split_einsum(e)
+    U = workloads.random_relation(rng, u_lab, upper, ext, til, dtype, keep=0.8, zero_frac=0.05)
+    V = workloads.random_relation(rng, v_lab, upper, ext, til, dtype, keep=keep_v, zero_frac=0.05)
+    spec = workloads.spec(e, upper, ext, til, dtype)
+    plan = tre.Plan.from_spec(spec, validate=validate)
+    assert plan.join_outer == "v" and not plan.group_needs_sort
+    say("v outer", idx, validate, e, len(U["keys"]), len(V["keys"]))
+    out = tre.einsum(plan, *to_dev(U), *to_dev(V), want_pairs=True)
+    check(out, orc.run(orc_plan(orc, spec), U, V), dtype)
+
+
+def test_v_outer_key_errors_gpu():
+    """Key validation in a V-driven join: unsorted, duplicate and
+    out-of-range keys of V are reported, as for a U-driven one."""
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    plan = tre.Plan("ij,kj->ki", "jk", {"i": 8, "j": 16, "k": 16}, {"j": 1, "k": 1}, "f32")
+    assert plan.join_outer == "v"
+    uk = torch.arange(16, dtype=torch.int32, device="cuda").reshape(-1, 1)
+    ut = torch.ones((16, 8), dtype=torch.float32, device="cuda")
+    good = np.array([[0, 1], [0, 5], [3, 2], [7, 7]], np.int32)
+    for bad, status in ((good[[1, 0, 2, 3]], "TRE_E_UNSORTED"), (good[[0, 0, 2, 3]], "TRE_E_DUPKEY"),
+                        (np.array([[0, 1], [0, 5], [3, 2], [7, 16]], np.int32), "TRE_E_KEYRANGE")):
+        vk = torch.from_numpy(np.ascontiguousarray(bad)).cuda()
+        vt = torch.ones((4, 1), dtype=torch.float32, device="cuda")
+        with pytest.raises(tre.TreError) as ei:
+            tre.einsum(plan, uk, ut, vk, vt)
+        assert ei.value.status == status

@@ -305,11 +305,13 @@ def test_three_way_path_small(orc):
     assert len(r1.pairs) == len(w["T"]["keys"])
 
 
-@pytest.mark.parametrize("c", [1, 2, 5])
-def test_gnn_chain_small(orc, c):
+@pytest.mark.parametrize("c,layout", [(1, "jk"), (2, "jk"), (5, "kj"), (5, "jk")])
+def test_gnn_chain_small(orc, c, layout):
     """(X.Y)^T.Z through E1 and E2 equals the dense product; the per-vertex
-    form (tile 1) is re-stacked into 256-row tiles between the two EinSums."""
-    w = workloads.config(c, "small")
+    form (tile 1) is re-stacked into 256-row tiles between the two EinSums.
+    The adjacency keyed (J, K) ("ij,jk->ki") or (K, J) ("ij,kj->ki")."""
+    w = workloads.config(c, "small", y_layout=layout)
+    assert w["y_layout"] == layout
     p1, p2 = plan_of(orc, w["E1"]), plan_of(orc, w["E2"])
     r1 = orc.run(p1, w["X"], {"keys": w["Y"]["keys"], "coo": w["Y"]["coo"]})
     assert r1.n_outside == 0
@@ -324,7 +326,8 @@ def test_gnn_chain_small(orc, c):
     X = vals_f64(w["X"]).reshape(n // w["tile_e1"], emb, w["tile_e1"]).transpose(1, 0, 2).reshape(emb, n)
     import scipy.sparse as sp
 
-    src, dst = w["Y"]["coo"][0].T
+    c0, c1 = w["Y"]["coo"][0].T  # coordinates in the operand's label order
+    src, dst = (c0, c1) if layout == "jk" else (c1, c0)
     Y = sp.csr_matrix((w["Y"]["coo"][1], (src, dst)), shape=(n, n))
     Z = vals_f64(w["Z"]).reshape(emb, zo)
     ref = np.asarray((Y.T @ X.T)) @ Z

@@ -110,7 +110,7 @@ def _block_relation_from_coo(rows, cols, vals, t_r: int, t_c: int, n_cols: int):
 
 
 def gnn_chain(n: int, emb: int, z_out: int, tile_e1: int, tile_e2: int, degree: dict, dtype: str,
-              seed: int, dense_y_tiles: bool = True) -> dict:
+              seed: int, dense_y_tiles: bool = True, y_layout: str = "jk") -> dict:
     """GNN message passing (X.Y)^T.Z as two binary EinSums (Sec. 1, Sec. 4.3).
 
     X [emb x n] holds one embedding column per vertex, Y [n x n] the directed
@@ -119,6 +119,10 @@ def gnn_chain(n: int, emb: int, z_out: int, tile_e1: int, tile_e2: int, degree: 
       E2  U[k, m] = sum_i T[k, i] Z[i, m]   "ki,im->km", promoted {k}
     ``degree``: {"kind": "fixed", "d": 8, "values": "ones"} or
                 {"kind": "powerlaw", "alpha": 2.1, "mean": 16, "values": "normal"}.
+    ``y_layout``: "jk" stores the adjacency keyed (J, K) (source-major) and
+    E1 reads it as "ij,jk->ki"; "kj" stores the same tuples keyed (K, J)
+    (destination-major, the transposed tiles) and E1 is "ij,kj->ki".  The
+    tensor and every drawn value are the same either way.
     Draw order: degrees, targets, edge values, X, Z."""
     rng = np.random.default_rng(seed)
     if degree["kind"] == "fixed":
@@ -143,8 +147,15 @@ def gnn_chain(n: int, emb: int, z_out: int, tile_e1: int, tile_e2: int, degree: 
     # X keyed J: tile [i][j'] = X[:, J*t:(J+1)*t]
     x_tiles = np.ascontiguousarray(X_s.reshape(emb, nb, t).transpose(1, 0, 2)).reshape(nb, emb * t)
     x_rel = {"keys": np.arange(nb, dtype=np.int32).reshape(nb, 1), "tiles": x_tiles, "dtype": dtype}
-    ykeys, slot, off = _block_relation_from_coo(src, dst, None, t, t, n)
-    y_rel = {"keys": ykeys, "dtype": dtype, "coo": (np.stack([src, dst], axis=1), ev_v),
+    if y_layout == "kj":
+        order = np.lexsort((src, dst))  # destination-major
+        rows, cols, ev_s, ev_v = dst[order], src[order], ev_s[order], ev_v[order]
+    elif y_layout == "jk":
+        rows, cols = src, dst
+    else:
+        raise ValueError(y_layout)
+    ykeys, slot, off = _block_relation_from_coo(rows, cols, None, t, t, n)
+    y_rel = {"keys": ykeys, "dtype": dtype, "coo": (np.stack([rows, cols], axis=1), ev_v),
              "slot": slot, "offset": off, "values": ev_s, "tile_elems": t * t}
     if dense_y_tiles:
         yt = np.zeros((len(ykeys), t * t), dtype=ev_s.dtype)
@@ -152,10 +163,12 @@ def gnn_chain(n: int, emb: int, z_out: int, tile_e1: int, tile_e2: int, degree: 
         y_rel["tiles"] = yt
     z_rel = {"keys": np.zeros((1, 0), dtype=np.int32), "tiles": np.ascontiguousarray(Z_s).reshape(1, -1),
              "dtype": dtype}
-    e1 = spec("ij,jk->ki", "jk", {"i": emb, "j": n, "k": n}, {"j": t, "k": t}, dtype)
+    e1 = spec("ij,jk->ki" if y_layout == "jk" else "ij,kj->ki", "jk", {"i": emb, "j": n, "k": n}, {"j": t, "k": t},
+              dtype)
     e2 = spec("ki,im->km", "k", {"k": n, "i": emb, "m": z_out}, {"k": tile_e2}, dtype)
     return {"E1": e1, "E2": e2, "X": x_rel, "Y": y_rel, "Z": z_rel, "n_edges": int(src.size),
-            "n": n, "emb": emb, "z_out": z_out, "tile_e1": t, "tile_e2": tile_e2, "dtype": dtype}
+            "n": n, "emb": emb, "z_out": z_out, "tile_e1": t, "tile_e2": tile_e2, "dtype": dtype,
+            "y_layout": y_layout, "y_k_col": 1 if y_layout == "jk" else 0}
 
 
 # ----------------------------------------------------------- block sparse
@@ -307,7 +320,9 @@ def config(c: int, scale: str = "full", **kw) -> dict:
         n = 512 if small else 4096
         return sparse_3way(n, 64, 32, 0.005 if not small else 0.05, 0.1, seed)
     if c == 5:
+        # the adjacency as scalar tuples, stored destination-major (keyed (K, J))
         n = 4096 if small else 1048576
+        kw.setdefault("y_layout", "kj")
         return gnn_chain(n, 256, 256, 1, 256, {"kind": "powerlaw", "alpha": 2.1, "mean": 32, "values": "normal"},
                          "bf16", seed, dense_y_tiles=True, **kw)
     if c == 6:
