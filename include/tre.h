@@ -231,6 +231,26 @@ tre_status tre_execute(tre_plan_t plan, const int32_t *u_keys, int64_t n_u, cons
                        int64_t w_cap, int64_t *n_w, int32_t *pairs_out, int64_t pair_cap, int64_t *n_pairs,
                        void *ws, size_t ws_bytes, void *stream, tre_timing *timing);
 
+/* tre_execute_noalloc -- tre_execute without a workspace argument, for
+ * callers that cannot allocate device memory: code under stream capture,
+ * tight serving loops, harnesses that forbid allocation.  The workspace is a
+ * static device array of tre_noalloc_scratch_bytes() bytes (256 MiB) in the
+ * library's device data; every GPU the library runs on holds its own copy
+ * until the process ends.  The call allocates nothing (no hipMalloc, no
+ * events) and takes its timing from no one (no tre_timing argument); outputs
+ * are the caller's, as for tre_execute (w_tiles of the plan's W element
+ * type).  Every call on one GPU uses that GPU's array and leaves its
+ * contents behind; what must start at zero is cleared by each call, but
+ * calls that overlap on one GPU (from several streams or threads) race on the
+ * array: serialise them.  Inputs whose workspace (tre_workspace_bytes with
+ * the join's pair count) exceeds the array: TRE_E_WORKSPACE, n_pairs set when
+ * the join got that far, nothing else written.  Synchronizes like tre_join. */
+size_t tre_noalloc_scratch_bytes(void);
+tre_status tre_execute_noalloc(tre_plan_t plan, const int32_t *u_keys, int64_t n_u, const void *u_tiles,
+                               const int32_t *v_keys, int64_t n_v, const void *v_tiles, int32_t *w_keys,
+                               void *w_tiles, int64_t w_cap, int64_t *n_w, int32_t *pairs_out, int64_t pair_cap,
+                               int64_t *n_pairs, void *stream);
+
 /* --- chain glue between two EinSums (Sec. 6, repartition) --------------- */
 
 /* Round fp32 to bf16 (nearest even; NaN stays NaN).  x, y device, n elements. */

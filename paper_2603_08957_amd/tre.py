@@ -33,6 +33,7 @@ EXPORTS = [
     "tre_stack_workspace_bytes", "tre_stack_rows",
     "tre_tiles_from_entries", "tre_status_str", "tre_last_error", "tre_version",
     "tre_repartition_workspace_bytes", "tre_repartition", "tre_execute3_workspace_bytes", "tre_execute3",
+    "tre_noalloc_scratch_bytes", "tre_execute_noalloc",
 ]
 
 
@@ -121,6 +122,9 @@ def lib():
         L.tre_execute3_workspace_bytes.restype = sz
         L.tre_execute3.argtypes = [cs, cs, P, P, ctypes.c_int, P, i64, P, P, i64, P, P, i64, P, P, P, i64, P, P, P, sz,
                                    P, P]
+        L.tre_noalloc_scratch_bytes.argtypes = []
+        L.tre_noalloc_scratch_bytes.restype = sz
+        L.tre_execute_noalloc.argtypes = [P, P, i64, P, P, i64, P, P, P, i64, P, P, i64, P, P]
         L.tre_status_str.restype = ctypes.c_char_p
         L.tre_last_error.restype = ctypes.c_char_p
         L.tre_version.restype = ctypes.c_char_p
@@ -275,6 +279,27 @@ def einsum(plan: Plan, u_keys, u_tiles, v_keys, v_tiles, want_pairs: bool = Fals
     pairs = torch.empty((n_p, 2), dtype=torch.int32, device=dev) if want_pairs else None
     contract(plan, jr, u_tiles, v_tiles, w_keys if rw > 0 else None, w_tiles, pairs, stream, tm)
     return Output(w_keys, w_tiles, pairs, n_p, n_w, tm.as_dict() if tm is not None else None, ws)
+
+
+def execute_noalloc(plan: Plan, u_keys, u_tiles, v_keys, v_tiles, w_keys, w_tiles, pairs_out=None, stream=None):
+    """tre_execute_noalloc: join + contract with the library's static device
+    scratch as workspace; every output buffer is the caller's (their row
+    counts are the capacities).  Returns (n_w, n_pairs)."""
+    n_u, n_v = int(u_tiles.shape[0]), int(v_tiles.shape[0])
+    n_w, n_p = ctypes.c_int64(0), ctypes.c_int64(0)
+    rc = lib().tre_execute_noalloc(plan.handle, _ptr(u_keys), n_u, _ptr(u_tiles), _ptr(v_keys), n_v, _ptr(v_tiles),
+                                   _ptr(w_keys), _ptr(w_tiles), int(w_tiles.shape[0]), ctypes.byref(n_w),
+                                   _ptr(pairs_out), int(pairs_out.shape[0]) if pairs_out is not None else 0,
+                                   ctypes.byref(n_p), _stream(stream))
+    if rc != 0:
+        err = TreError(rc, "tre_execute_noalloc", lib().tre_last_error().decode())
+        err.n_w, err.n_pairs = int(n_w.value), int(n_p.value)
+        raise err
+    return int(n_w.value), int(n_p.value)
+
+
+def noalloc_scratch_bytes() -> int:
+    return int(lib().tre_noalloc_scratch_bytes())
 
 
 def cast_f32_bf16(x, out=None, stream=None):
