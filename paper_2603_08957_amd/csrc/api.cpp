@@ -223,6 +223,12 @@ tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const i
     // that count on the device (its grids are sized for the workspace's
     // capacity), so one read-back at the end returns the key checks, the
     // pair count and the key count together
+    if (n_u > 0 && n_v > 0 && v_dense(p, n_u) && n_v > max_pairs) {
+        // one pair per V tuple, known without the device
+        out->n_pairs = n_v;
+        set_error("tre_join: workspace too small for the matched pairs (see n_pairs)");
+        return TRE_E_WORKSPACE;
+    }
     if (n_u > 0 && n_v > 0 && max_pairs > 0) {
         if ((e = launch_join(p, L, w, u_keys, v_keys, s, 0)) != hipSuccess) return dev_fail(e, "join");
         const int64_t cap = std::min(max_pairs, pair_bound(p, n_u, n_v));

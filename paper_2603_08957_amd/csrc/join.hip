@@ -229,6 +229,7 @@ __global__ void k_store_count32(const int32_t* __restrict__ pos, int64_t n, WsHe
     hdr->n_pairs = pos[n];
 }
 
+
 __device__ inline uint64_t pack_w(const int32_t* urow, const int32_t* vrow, const WDesc& d) {
     uint64_t k = 0;
     for (int i = 0; i < d.n; i++) {
@@ -367,6 +368,33 @@ __global__ __launch_bounds__(kThreads) void k_expand(const int64_t* __restrict__
             pv[p] = iv;
         }
     }
+}
+
+// The join driven by V when U holds every key of its key space (n_u = the
+// product of its radices) and that key is the join labels: sorted strictly
+// increasing keys are then exactly 0 .. n_u - 1, so V tuple v meets the U
+// tuple whose index is its join key read as a mixed-radix number, and pair
+// v is (that index, v) -- no search, no flags, no scan.  Attributes outside
+// their range (keys that fail validation, reported by the host) are clamped
+// so nothing is read out of bounds.
+struct Radices {
+    int32_t n;
+    int32_t r[26];
+};
+
+template <typename KT>
+__global__ void k_vdense(const int32_t* __restrict__ vkeys, int64_t n_v, int rv, KeyDesc dv, Radices ur,
+                         const int32_t* __restrict__ ukeys, int ru, WDesc wd, int32_t* __restrict__ pu,
+                         int32_t* __restrict__ pv, KT* __restrict__ wk, WsHeader* __restrict__ hdr) {
+    const int64_t v = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (v >= n_v) return;
+    if (v == 0) hdr->n_pairs = n_v;
+    const int32_t* vrow = vkeys + v * rv;
+    int64_t u = 0;
+    for (int i = 0; i < dv.n; i++) u = u * ur.r[i] + min(max(vrow[dv.pos[i]], 0), ur.r[i] - 1);
+    pu[v] = int32_t(u);
+    pv[v] = int32_t(v);
+    wk[v] = KT(pack_w(ukeys + u * ru, vrow, wd));
 }
 
 // Pairs of the join driven by V with at most one U tuple per V tuple:
@@ -522,6 +550,7 @@ hipError_t launch_join(const Plan& p, const Layout& L, char* ws, const int32_t* 
     int32_t* hist = reinterpret_cast<int32_t*>(ws + L.hist);
     const int64_t n_u = L.n_u, n_v = L.n_v;
     hipError_t e = hipSuccess;
+    if (v_dense(p, n_u)) return hipSuccess;  // the pairs are written by the GROUP BY stage, one per V tuple
     if (p.v_outer && p.nk[0] == p.n_join) {
         // walk V: each V tuple meets at most one U tuple (U's key is the join labels)
         int32_t* pos = reinterpret_cast<int32_t*>(ws + L.ucnt);
@@ -595,7 +624,14 @@ hipError_t group_impl(const Plan& p, const Layout& L, char* ws, const int32_t* u
     hipError_t e;
     const bool sort = p.group_needs_sort && cap > 1 && p.w_total_bits > 0;
     uint64_t* uv = sort ? reinterpret_cast<uint64_t*>(ws + L.pidx) : nullptr;
-    if (cap > 0 && p.v_outer && p.nk[0] == p.n_join) {
+    if (cap > 0 && v_dense(p, L.n_u)) {
+        Radices ur{};
+        ur.n = p.nk[0];
+        for (int i = 0; i < p.nk[0]; i++) ur.r[i] = p.radix[0][i];
+        k_vdense<KT><<<blocks_for(L.n_v), kThreads, 0, s>>>(v_keys, L.n_v, p.nk[1], desc_v(p), ur, u_keys, p.nk[0], wd,
+                                                             pu, pv, wk, hdr);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    } else if (cap > 0 && p.v_outer && p.nk[0] == p.n_join) {
         k_vwrite<KT><<<blocks_for(L.n_v), kThreads, 0, s>>>(
             reinterpret_cast<const int32_t*>(ws + L.ucnt), reinterpret_cast<const int32_t*>(ws + L.ulo), L.n_v, hdr,
             cap, u_keys, p.nk[0], v_keys, p.nk[1], wd, pu, pv, wk);
@@ -645,6 +681,16 @@ hipError_t group_impl(const Plan& p, const Layout& L, char* ws, const int32_t* u
 }
 
 }  // namespace
+
+bool v_dense(const Plan& p, int64_t n_u) {
+    if (!(p.v_outer && p.nk[0] == p.n_join && p.nk[0] > 0)) return false;
+    int64_t space = 1;
+    for (int i = 0; i < p.nk[0]; i++) {
+        space *= p.radix[0][i];
+        if (space > n_u) return false;
+    }
+    return space == n_u;
+}
 
 bool keyed_by_u(const Plan& p) {
     if (p.nk[1] != 0 || p.nk[2] != p.nk[0]) return false;

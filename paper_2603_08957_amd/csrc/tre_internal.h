@@ -163,6 +163,10 @@ hipError_t launch_validate(const int32_t* keys, int64_t n, int r, const int32_t*
                            hipStream_t s);
 hipError_t launch_join(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
                        hipStream_t s, int stage);
+// A V-driven join where U's key is the join labels and U holds every key of
+// that key space: U's index is the join key itself, one pair per V tuple,
+// written by the GROUP BY stage (the pair count is n_v, known on the host)
+bool v_dense(const Plan& p, int64_t n_u);
 // V without promoted labels (one tuple) and W keyed by U's key as it is:
 // every U tuple is one pair and one group, written without counting
 bool keyed_by_u(const Plan& p);

@@ -703,17 +703,18 @@ V_OUTER_PLANS = [
 
 
 @pytest.mark.parametrize("idx", range(len(V_OUTER_PLANS)))
-@pytest.mark.parametrize("validate", [True, False])
-def test_v_outer_join_gpu(orc, idx, validate):
+@pytest.mark.parametrize("validate,keep_u", [(True, 0.8), (False, 0.8), (True, 1.0), (False, 1.0)])
+def test_v_outer_join_gpu(orc, idx, validate, keep_u):
     """Joins driven by V: pair list, keys and values against the oracle, with
-    U missing some join keys (unmatched V tuples) and key validation on or
-    off."""
+    U missing some join keys (unmatched V tuples) or holding all of them (U
+    indexed by the key itself where U's key is the join labels), and key
+    validation on or off."""
     import paper_2603_08957_amd as tre
 
     e, upper, ext, til, dtype, keep_v = V_OUTER_PLANS[idx]
     rng = np.random.default_rng(500 + idx)
     u_lab, v_lab, _ = split_einsum(e)
-    U = workloads.random_relation(rng, u_lab, upper, ext, til, dtype, keep=0.8, zero_frac=0.05)
+    U = workloads.random_relation(rng, u_lab, upper, ext, til, dtype, keep=keep_u, zero_frac=0.05)
     V = workloads.random_relation(rng, v_lab, upper, ext, til, dtype, keep=keep_v, zero_frac=0.05)
     spec = workloads.spec(e, upper, ext, til, dtype)
     plan = tre.Plan.from_spec(spec, validate=validate)
@@ -742,3 +743,25 @@ def test_v_outer_key_errors_gpu():
         with pytest.raises(tre.TreError) as ei:
             tre.einsum(plan, uk, ut, vk, vt)
         assert ei.value.status == status
+
+
+def test_v_dense_workspace_gpu(orc):
+    """A V-driven join over a U that holds every key: with room for no pair
+    the join reports TRE_E_WORKSPACE and the pair count (one per V tuple)
+    before any device work; with room it matches the oracle."""
+    import paper_2603_08957_amd as tre
+
+    spec = workloads.spec("ij,kj->ki", "jk", {"i": 16, "j": 64, "k": 64}, {"j": 1, "k": 1}, "f32")
+    rng = np.random.default_rng(77)
+    U = workloads.random_relation(rng, "ij", "jk", spec["extents"], spec["tiles"], "f32", keep=1.0)
+    V = workloads.random_relation(rng, "kj", "jk", spec["extents"], spec["tiles"], "f32", keep=0.2)
+    plan = tre.Plan.from_spec(spec)
+    assert plan.join_outer == "v" and len(U["keys"]) == 64
+    uk, ut = to_dev(U)
+    vk, vt = to_dev(V)
+    ws = tre.alloc_workspace(plan.workspace_bytes(64, len(V["keys"]), 0))
+    with pytest.raises(tre.TreError) as ei:
+        tre.join(plan, uk, 64, vk, len(V["keys"]), ws)
+    assert ei.value.status == "TRE_E_WORKSPACE" and ei.value.join_result.n_pairs == len(V["keys"])
+    out = tre.einsum(plan, uk, ut, vk, vt, want_pairs=True, pair_hint=1)
+    check(out, orc.run(orc_plan(orc, spec), U, V), "f32")
