@@ -212,12 +212,12 @@ class GnnChain:
     with Y keyed (K,J) (the 1,048,576-vertex chain's destination-major
     adjacency), cast, E2 'ki,im->km'."""
 
-    def __init__(self, c, tre, torch):
+    def __init__(self, c, tre, torch, y_layout=None):
         import workloads
 
         self.c = c
         t0 = time.time()
-        w = workloads.config(c)
+        w = workloads.config(c, **({"y_layout": y_layout} if y_layout else {}))
         log(f"[bench] generated workload {c} in {time.time() - t0:.1f}s: {w['n_edges']} edges, "
             f"{len(w['Y']['keys'])} Y tuples")
         self.w = w
@@ -787,7 +787,7 @@ def planner_check(tre, torch, config, top, steps):
     import workloads
     from paper_2603_08957_amd import planner as pl
 
-    w = workloads.config(config)
+    w = workloads.config(config, y_layout="jk")  # the source-major COO every plan is laid out from
     n, emb, zo, dt = w["n"], w["emb"], w["z_out"], w["dtype"]
     t1 = w["tile_e1"]
     eb = 2 if dt == "bf16" else 4
@@ -936,9 +936,9 @@ def planner_check(tre, torch, config, top, steps):
             "steps": steps, "data": "synthetic"}
 
 
-def make_workload(c, tre, torch, three_way="fused"):
+def make_workload(c, tre, torch, three_way="fused", y_layout=None):
     if c in (1, 2, 5):
-        return GnnChain(c, tre, torch)
+        return GnnChain(c, tre, torch, y_layout)
     if c == 3:
         return BlockSparse(c, tre, torch)
     if c == 4:
@@ -1054,7 +1054,9 @@ def measure(W, args, torch, tre, config, cpu_budget_s):
         roof = {"bound": "mfma", "achieved": dflops / (contract_ms * 1e-3) / 1e12, "peak": PEAK_TFLOPS[dtype],
                 "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    rec = traffic_record(config, args.three_way)
+    own_layout = "jk" if config == 2 else "kj"
+    other_layout = config in (1, 2, 5) and args.y_layout not in (None, own_layout)
+    rec = None if other_layout else traffic_record(config, args.three_way)
     roof["traffic"] = rec["bytes"] if rec else None
     if rec:
         roof["traffic_detail"] = rec
@@ -1105,6 +1107,9 @@ def main():
                     help="tre_options.u_ranges for every EinSum (0 = library default, < 0 = off)")
     ap.add_argument("--pace-windows", type=int, default=0,
                     help="tre_options.pace_windows for every EinSum (0 = library default, < 0 = off)")
+    ap.add_argument("--y-layout", choices=["jk", "kj"], default=None,
+                    help="GNN chains: the adjacency keyed (J, K) or (K, J) (default: the workload's own, (J, K) for "
+                         "the 262,144-vertex chain, (K, J) for the others)")
     ap.add_argument("--three-way", choices=["fused", "binary"], default="fused",
                     help="workloads 4 and 6: one fused three-operand EinSum (default) or two binary EinSums")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
@@ -1148,7 +1153,7 @@ def main():
     todo = [args.config] if args.config else list(ALL_CONFIGS)
     reports = []
     for c in todo:
-        W = make_workload(c, tre, torch, args.three_way)
+        W = make_workload(c, tre, torch, args.three_way, args.y_layout)
         log(f"[bench] config {c}: inputs resident; warming up")
         budget = args.cpu_budget or (6.0 if c == todo[0] else 3.0)
         reports.append(measure(W, args, torch, tre, c, budget))

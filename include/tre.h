@@ -89,7 +89,10 @@ typedef struct {
                                    consumer that reads bf16: the producer writes half the bytes and no
                                    cast pass runs.  Vector class and 128x128 path only (TRE_E_DTYPE in
                                    tre_plan otherwise). */
-    int32_t reserved[3];
+    int32_t small_join;         /* 0 = automatic: a join whose pairs come out grouped by W key, whose driving
+                                   relation has at most 4096 tuples and at most 4096 pairs runs in one
+                                   workgroup (one launch); < 0 = never */
+    int32_t reserved[2];
 } tre_options;
 
 /* Static facts about a plan (host). */
@@ -142,7 +145,10 @@ typedef struct {
     int32_t contract_path;    /* out: the contraction launch tre_contract chose: 0 generic MFMA GEMM (64x64
                                  blocks), 1 vector class, 2 128x128 MFMA path, 3 the same as a paced
                                  persistent grid, 4 the same with U-range units (partials summed after) */
-    int32_t reserved;
+    int32_t join_path;        /* out (tre_join): 0 driven by U (runs searched in V), 1 driven by V (runs
+                                 searched in U), 2 driven by V with at most one U tuple each, 3 driven by V
+                                 over a U holding every key (no search), 4 keyless one-tuple V with W keyed by
+                                 U, 5 the whole join in one workgroup (small inputs) */
 } tre_timing;
 
 /* tre_plan -- parse and classify one binary EinSum (host only, no device work).

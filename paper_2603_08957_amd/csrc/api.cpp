@@ -216,6 +216,7 @@ tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const i
             timing->deferred = deferred;
             timing->join_ms = tm.between(0, 1);
             timing->total_ms = timing->join_ms;
+            timing->join_path = 4;
         }
         return TRE_OK;
     }
@@ -229,9 +230,12 @@ tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const i
         set_error("tre_join: workspace too small for the matched pairs (see n_pairs)");
         return TRE_E_WORKSPACE;
     }
-    if (n_u > 0 && n_v > 0 && max_pairs > 0) {
+    const int64_t cap = std::min(max_pairs, pair_bound(p, n_u, n_v));
+    const bool small = n_u > 0 && n_v > 0 && small_join_ok(p, n_u, n_v, cap);
+    if (small) {
+        if ((e = launch_join_small(p, L, w, u_keys, v_keys, cap, s)) != hipSuccess) return dev_fail(e, "join");
+    } else if (n_u > 0 && n_v > 0 && max_pairs > 0) {
         if ((e = launch_join(p, L, w, u_keys, v_keys, s, 0)) != hipSuccess) return dev_fail(e, "join");
-        const int64_t cap = std::min(max_pairs, pair_bound(p, n_u, n_v));
         if ((e = launch_group(p, L, w, u_keys, v_keys, cap, s)) != hipSuccess) return dev_fail(e, "group");
     } else if (n_u > 0 && n_v > 0) {
         // no room for any pair: count only, to report the size needed
@@ -270,6 +274,11 @@ tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const i
         timing->deferred = deferred;
         timing->join_ms = tm.between(0, 1);
         timing->total_ms = timing->join_ms;
+        timing->join_path = small ? 5
+                            : v_dense(p, n_u)                          ? 3
+                            : (p.v_outer && p.nk[0] == p.n_join)       ? 2
+                            : p.v_outer                                ? 1
+                                                                       : 0;
     }
     return TRE_OK;
 }

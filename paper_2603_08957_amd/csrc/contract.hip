@@ -142,6 +142,90 @@ __global__ __launch_bounds__(kOrderBins) void k_order_units(Unit* __restrict__ u
     }
 }
 
+// The unit table of at most kOrderMax keys in one workgroup: per key the
+// unit count (keys longer than the cap cut into equal units), scans of the
+// unit, partial-slot and split counts, the fill, and for the GEMM class the
+// longest-first order (counting sort on the unit length, as k_order_units)
+// -- one launch instead of up to six.
+constexpr int kUnitsThreads = kOrderBins;
+constexpr int kUnitsPer = kOrderMax / kUnitsThreads;
+
+// part_off[s]: the first partial slot of key s (n_w + 1 entries; k_reduce
+// sums slots part_off[s] .. part_off[s + 1] - 1 of each split key).
+__global__ __launch_bounds__(kUnitsThreads) void k_units_small(const int32_t* __restrict__ seg_start, int64_t n_w,
+                                                                int64_t p_unit, int order, Unit* __restrict__ units,
+                                                                int32_t* __restrict__ split,
+                                                                int32_t* __restrict__ part_off,
+                                                                WsHeader* __restrict__ hdr) {
+    __shared__ Unit buf[kOrderMax];
+    __shared__ int32_t cnt[kOrderBins];
+    __shared__ int32_t wsum[kUnitsThreads / 64];
+    const int t = threadIdx.x;
+    int32_t nu[kUnitsPer], su = 0, sp = 0, ss = 0;
+#pragma unroll
+    for (int j = 0; j < kUnitsPer; j++) {
+        const int64_t s = int64_t(t) * kUnitsPer + j;
+        nu[j] = 0;
+        if (s < n_w) {
+            const int64_t len = seg_start[s + 1] - seg_start[s];
+            nu[j] = int32_t((len + p_unit - 1) / p_unit);
+        }
+        su += nu[j];
+        sp += nu[j] > 1 ? nu[j] : 0;
+        ss += nu[j] > 1 ? 1 : 0;
+    }
+    int32_t n_units, n_parts, n_split;
+    int32_t uo = block_scan_excl<kUnitsThreads>(su, wsum, &n_units);
+    int32_t po = block_scan_excl<kUnitsThreads>(sp, wsum, &n_parts);
+    int32_t so = block_scan_excl<kUnitsThreads>(ss, wsum, &n_split);
+    const bool in_lds = order && n_units >= 2 && n_units <= kOrderMax;
+#pragma unroll
+    for (int j = 0; j < kUnitsPer; j++) {
+        const int64_t s = int64_t(t) * kUnitsPer + j;
+        if (s >= n_w) continue;
+        part_off[s] = po;
+        const int32_t a = seg_start[s], b = seg_start[s + 1];
+        const int64_t len = int64_t(b) - a;
+        for (int32_t q = 0; q < nu[j]; q++) {
+            Unit u;
+            u.seg = int32_t(s);
+            u.p0 = a + int32_t(len * q / nu[j]);
+            u.p1 = a + int32_t(len * (q + 1) / nu[j]);
+            u.slot = nu[j] > 1 ? po + q : -1;
+            if (in_lds) buf[uo + q] = u;
+            else units[uo + q] = u;
+        }
+        if (nu[j] > 1) {
+            split[so++] = int32_t(s);
+            po += nu[j];
+        }
+        uo += nu[j];
+    }
+    if (t == 0) {
+        part_off[n_w] = n_parts;
+        hdr->n_units = n_units;
+        hdr->n_parts = n_parts;
+        hdr->n_split = n_split;
+    }
+    if (!in_lds) return;
+    // longest first (unit lengths capped at kOrderBins - 1; order within a
+    // length class is free: a unit's sum does not depend on when it runs)
+    auto bin = [](const Unit& u) { return kOrderBins - 1 - min(u.p1 - u.p0, kOrderBins - 1); };
+    cnt[t] = 0;
+    __syncthreads();
+    for (int i = t; i < n_units; i += kUnitsThreads) atomicAdd(&cnt[bin(buf[i])], 1);
+    __syncthreads();
+    int32_t total;
+    const int32_t start = block_scan_excl<kUnitsThreads>(cnt[t], wsum, &total);
+    __syncthreads();
+    cnt[t] = start;
+    __syncthreads();
+    for (int i = t; i < n_units; i += kUnitsThreads) {
+        const Unit u = buf[i];
+        units[atomicAdd(&cnt[bin(u)], 1)] = u;
+    }
+}
+
 // U-range units (see launch_range_units): unit r * n_w + s covers the pairs of
 // key s with U index in [r * n_u / R, (r + 1) * n_u / R); within a key the
 // pairs are sorted by U index, so that is one contiguous run, found by binary
@@ -690,6 +774,13 @@ hipError_t launch_units(const Plan& p, const Layout& L, char* ws, int64_t n_pair
     int32_t* nsplit = reinterpret_cast<int32_t*>(ws + L.flags);
     int32_t* tmp = reinterpret_cast<int32_t*>(ws + L.scan_tmp);
     hipError_t e;
+    if (n_w <= kOrderMax) {
+        k_units_small<<<1, kUnitsThreads, 0, s>>>(seg_start, n_w, std::max<int64_t>(p_unit, 1),
+                                                   longest_first && p.kclass == KC_GEMM ? 1 : 0,
+                                                   reinterpret_cast<Unit*>(ws + L.unit_desc),
+                                                   reinterpret_cast<int32_t*>(ws + L.split_list), nparts, hdr);
+        return hipGetLastError();
+    }
     if (p_unit >= n_pairs) {  // no key can be longer than the cap
         k_key_units<<<blocks_for(n_w + 1), kThreads, 0, s>>>(seg_start, n_w, reinterpret_cast<Unit*>(ws + L.unit_desc),
                                                              hdr);

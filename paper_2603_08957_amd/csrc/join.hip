@@ -382,10 +382,13 @@ struct Radices {
     int32_t r[26];
 };
 
+// With `first` (the key-space segment search, zeroed), the pass also marks
+// every W key's first pair, as k_first_of_key would: first[k] = 1 + v.
 template <typename KT>
 __global__ void k_vdense(const int32_t* __restrict__ vkeys, int64_t n_v, int rv, KeyDesc dv, Radices ur,
                          const int32_t* __restrict__ ukeys, int ru, WDesc wd, int32_t* __restrict__ pu,
-                         int32_t* __restrict__ pv, KT* __restrict__ wk, WsHeader* __restrict__ hdr) {
+                         int32_t* __restrict__ pv, KT* __restrict__ wk, WsHeader* __restrict__ hdr,
+                         int32_t* __restrict__ first, int64_t nk) {
     const int64_t v = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (v >= n_v) return;
     if (v == 0) hdr->n_pairs = n_v;
@@ -394,7 +397,12 @@ __global__ void k_vdense(const int32_t* __restrict__ vkeys, int64_t n_v, int rv,
     for (int i = 0; i < dv.n; i++) u = u * ur.r[i] + min(max(vrow[dv.pos[i]], 0), ur.r[i] - 1);
     pu[v] = int32_t(u);
     pv[v] = int32_t(v);
-    wk[v] = KT(pack_w(ukeys + u * ru, vrow, wd));
+    // W's key is V's key prefix (a V-driven join): the key of pair v is that
+    // of V tuple v
+    const KT k = KT(pack_w(ukeys + u * ru, vrow, wd));
+    wk[v] = k;
+    if (first && (v == 0 || KT(pack_w(ukeys, vrow - rv, wd)) != k) && uint64_t(k) < uint64_t(nk))
+        first[k] = int32_t(v + 1);
 }
 
 // Pairs of the join driven by V with at most one U tuple per V tuple:
@@ -413,6 +421,147 @@ __global__ void k_vwrite(const int32_t* __restrict__ pos, const int32_t* __restr
     pu[p] = u;
     pv[p] = int32_t(v);
     wk[p] = KT(pack_w(ukeys + int64_t(u) * ru, vkeys + v * rv, wd));
+}
+
+// One workgroup for the whole join of a small input (at most kSmallMax outer
+// tuples and kSmallMax pairs): the same steps as the multi-kernel path --
+// every outer tuple finds its run of inner tuples by binary search on the
+// inner relation's key prefix, an exclusive scan gives the pair offsets, the
+// expansion lists the pairs in (outer, inner) order with their W keys, a
+// sort by (W key, expansion index) puts them in the canonical (W key, u, v)
+// order when the join order does not already group them, and head flags
+// with a second scan give the segments -- all in LDS, in one launch.
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallMax = 4096;
+constexpr int kSmallPer = kSmallMax / kSmallThreads;
+constexpr int kSmallIdxBits = 12;  // pair index bits of the sort key
+static_assert((1 << kSmallIdxBits) == kSmallMax, "sort key layout");
+
+__device__ inline int32_t small_scan(int32_t v, int32_t* wsum, int32_t* total) {
+    return block_scan_excl<kSmallThreads>(v, wsum, total);
+}
+
+// VO: the outer relation is V (a V-driven join) and the inner one U.
+template <bool VO>
+__global__ __launch_bounds__(kSmallThreads) void k_join_small(
+    const int32_t* __restrict__ okeys, int64_t n_o, int ro, KeyDesc dout, const int32_t* __restrict__ ikeys,
+    int64_t n_i, int ri, const int32_t* __restrict__ ukeys, int ru, const int32_t* __restrict__ vkeys, int rv,
+    WDesc wd, int sort, int64_t cap, int32_t* __restrict__ pu, int32_t* __restrict__ pv,
+    int32_t* __restrict__ seg_start, uint64_t* __restrict__ seg_key, WsHeader* __restrict__ hdr) {
+    __shared__ int32_t s_off[kSmallMax + 1];
+    __shared__ int32_t s_lo[kSmallMax];
+    __shared__ uint64_t s_key[kSmallMax];  // W key << kSmallIdxBits | expansion index
+    __shared__ int32_t s_pu[kSmallMax], s_pv[kSmallMax];
+    __shared__ int32_t s_wsum[kSmallThreads / 64];
+    const int t = threadIdx.x;
+    // runs: outer tuple o meets inner tuples [s_lo[o], s_lo[o] + c)
+    int32_t c[kSmallPer];
+    int32_t csum = 0;
+#pragma unroll
+    for (int j = 0; j < kSmallPer; j++) {
+        const int64_t o = int64_t(t) * kSmallPer + j;
+        c[j] = 0;
+        if (o < n_o) {
+            int32_t key[26];
+            for (int i = 0; i < dout.n; i++) key[i] = okeys[o * ro + dout.pos[i]];
+            int64_t a = 0, b = n_i;
+            while (a < b) {
+                const int64_t m = (a + b) >> 1;
+                if (cmp_prefix(ikeys + m * ri, key, dout.n) < 0) a = m + 1; else b = m;
+            }
+            int64_t e = a, f = n_i;  // first inner row past the run
+            while (e < f) {
+                const int64_t m = (e + f) >> 1;
+                if (cmp_prefix(ikeys + m * ri, key, dout.n) <= 0) e = m + 1; else f = m;
+            }
+            s_lo[o] = int32_t(a);
+            c[j] = int32_t(min<int64_t>(e - a, kSmallMax));  // more cannot be listed (and the sums stay small)
+        }
+        csum += c[j];
+    }
+    int32_t total;
+    int32_t run = small_scan(csum, s_wsum, &total);
+#pragma unroll
+    for (int j = 0; j < kSmallPer; j++) {
+        const int64_t o = int64_t(t) * kSmallPer + j;
+        if (o < n_o) s_off[o] = run;
+        run += c[j];
+    }
+    if (t == 0) {
+        s_off[n_o] = total;
+        hdr->n_pairs = total;
+    }
+    __syncthreads();
+    const int32_t n = int32_t(min<int64_t>(total, min<int64_t>(cap, kSmallMax)));
+    // expansion: pair q belongs to the last outer tuple whose offset is <= q
+#pragma unroll
+    for (int j = 0; j < kSmallPer; j++) {
+        const int32_t q = t * kSmallPer + j;
+        if (q >= n) continue;
+        int32_t a = 0, b = int32_t(n_o) - 1;
+        while (a < b) {
+            const int32_t m = (a + b + 1) >> 1;
+            if (s_off[m] <= q) a = m; else b = m - 1;
+        }
+        const int32_t in = s_lo[a] + (q - s_off[a]);
+        const int32_t u = VO ? in : a, v = VO ? a : in;
+        s_pu[q] = u;
+        s_pv[q] = v;
+        s_key[q] = (pack_w(ukeys + int64_t(u) * ru, vkeys + int64_t(v) * rv, wd) << kSmallIdxBits) | uint64_t(q);
+    }
+    __syncthreads();
+    if (sort) {
+        // bitonic sort of the (W key, index) words, padded to a power of two
+        int32_t m = 1;
+        while (m < n) m <<= 1;
+        for (int32_t q = n + t; q < m; q += kSmallThreads) s_key[q] = ~0ull;
+        __syncthreads();
+        for (int32_t k = 2; k <= m; k <<= 1) {
+            for (int32_t jj = k >> 1; jj > 0; jj >>= 1) {
+                for (int32_t i = t; i < m; i += kSmallThreads) {
+                    const int32_t ixj = i ^ jj;
+                    if (ixj > i) {
+                        const uint64_t x = s_key[i], y = s_key[ixj];
+                        if ((x > y) == ((i & k) == 0)) {
+                            s_key[i] = y;
+                            s_key[ixj] = x;
+                        }
+                    }
+                }
+                __syncthreads();
+            }
+        }
+    }
+    // pairs in order, segment heads, segments
+    int32_t h[kSmallPer];
+    int32_t hs = 0;
+#pragma unroll
+    for (int j = 0; j < kSmallPer; j++) {
+        const int32_t q = t * kSmallPer + j;
+        h[j] = 0;
+        if (q < n) {
+            const int32_t e = int32_t(s_key[q] & uint64_t(kSmallMax - 1));
+            pu[q] = s_pu[e];
+            pv[q] = s_pv[e];
+            h[j] = (q == 0 || (s_key[q] >> kSmallIdxBits) != (s_key[q - 1] >> kSmallIdxBits)) ? 1 : 0;
+        }
+        hs += h[j];
+    }
+    int32_t n_seg;
+    int32_t sr = small_scan(hs, s_wsum, &n_seg);
+#pragma unroll
+    for (int j = 0; j < kSmallPer; j++) {
+        const int32_t q = t * kSmallPer + j;
+        if (q < n && h[j]) {
+            seg_start[sr] = q;
+            seg_key[sr] = s_key[q] >> kSmallIdxBits;
+            sr++;
+        }
+    }
+    if (t == 0) {
+        seg_start[n_seg] = n;
+        hdr->n_w = n_seg;
+    }
 }
 
 // Join with a keyless single-tuple V whose output is keyed by U's own key
@@ -624,13 +773,19 @@ hipError_t group_impl(const Plan& p, const Layout& L, char* ws, const int32_t* u
     hipError_t e;
     const bool sort = p.group_needs_sort && cap > 1 && p.w_total_bits > 0;
     uint64_t* uv = sort ? reinterpret_cast<uint64_t*>(ws + L.pidx) : nullptr;
+    const int64_t key_space = int64_t(1) << p.w_total_bits;
+    const bool by_key = p.w_total_bits > 0 && p.w_total_bits <= 30 && key_space <= cap;
+    int32_t* first = flags;  // key-space segment search: key_space + 1 <= cap + 1 entries
+    bool first_done = false;
     if (cap > 0 && v_dense(p, L.n_u)) {
         Radices ur{};
         ur.n = p.nk[0];
         for (int i = 0; i < p.nk[0]; i++) ur.r[i] = p.radix[0][i];
+        if (by_key && (e = launch_fill_zero(first, sizeof(int32_t) * size_t(key_space), s)) != hipSuccess) return e;
         k_vdense<KT><<<blocks_for(L.n_v), kThreads, 0, s>>>(v_keys, L.n_v, p.nk[1], desc_v(p), ur, u_keys, p.nk[0], wd,
-                                                             pu, pv, wk, hdr);
+                                                             pu, pv, wk, hdr, by_key ? first : nullptr, key_space);
         if ((e = hipGetLastError()) != hipSuccess) return e;
+        first_done = by_key;
     } else if (cap > 0 && p.v_outer && p.nk[0] == p.n_join) {
         k_vwrite<KT><<<blocks_for(L.n_v), kThreads, 0, s>>>(
             reinterpret_cast<const int32_t*>(ws + L.ucnt), reinterpret_cast<const int32_t*>(ws + L.ulo), L.n_v, hdr,
@@ -658,14 +813,14 @@ hipError_t group_impl(const Plan& p, const Layout& L, char* ws, const int32_t* u
         if (e != hipSuccess) return e;
         if (radix_result_in_alt(cap, p.w_total_bits)) wk = wk_alt;
     }
-    const int64_t key_space = int64_t(1) << p.w_total_bits;
-    if (p.w_total_bits > 0 && p.w_total_bits <= 30 && key_space <= cap) {
+    if (by_key) {
         // small key space: find the segments by key instead of by pair
-        int32_t* first = flags;  // key_space + 1 <= n_pairs + 1 entries
         int32_t* kflags = reinterpret_cast<int32_t*>(ws + L.part_off);  // free until the work units are made
-        if ((e = launch_fill_zero(first, sizeof(int32_t) * size_t(key_space), s)) != hipSuccess) return e;
-        k_first_of_key<KT><<<blocks_for(cap), kThreads, 0, s>>>(wk, hdr, cap, key_space, first);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if (!first_done) {
+            if ((e = launch_fill_zero(first, sizeof(int32_t) * size_t(key_space), s)) != hipSuccess) return e;
+            k_first_of_key<KT><<<blocks_for(cap), kThreads, 0, s>>>(wk, hdr, cap, key_space, first);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
         k_key_flags<<<blocks_for(key_space + 1), kThreads, 0, s>>>(first, key_space, kflags);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if ((e = scan_exclusive_i32(kflags, kflags, key_space + 1, tmp, s)) != hipSuccess) return e;
@@ -681,6 +836,44 @@ hipError_t group_impl(const Plan& p, const Layout& L, char* ws, const int32_t* u
 }
 
 }  // namespace
+
+bool small_join_ok(const Plan& p, int64_t n_u, int64_t n_v, int64_t cap) {
+    // joins whose pairs need the GROUP BY sort stay on the multi-kernel path:
+    // sorting 4096 pairs on one CU (a bitonic sort, 78 barrier stages) took
+    // longer than the device-wide radix sort it replaces (96 us against about
+    // 90 us for the whole multi-kernel join of the 4096-vertex chain's E1)
+    if (p.opt.small_join < 0 || p.v_needs_sort || p.group_needs_sort || keyed_by_u(p) || v_dense(p, n_u) ||
+        p.w_total_bits > 32)
+        return false;
+    const int64_t n_o = p.v_outer ? n_v : n_u;
+    return n_o >= 1 && n_o <= kSmallMax && cap >= 1 && cap <= kSmallMax;
+}
+
+hipError_t launch_join_small(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
+                             int64_t cap, hipStream_t s) {
+    WDesc wd{};
+    wd.n = p.nk[2];
+    for (int c = 0; c < p.nk[2]; c++) {
+        wd.src[c] = p.w_src[c];
+        wd.pos[c] = p.w_pos[c];
+        wd.bits[c] = p.w_bits[c];
+    }
+    int32_t* pu = reinterpret_cast<int32_t*>(ws + L.pu);
+    int32_t* pv = reinterpret_cast<int32_t*>(ws + L.pv);
+    int32_t* seg_start = reinterpret_cast<int32_t*>(ws + L.seg_start);
+    uint64_t* seg_key = reinterpret_cast<uint64_t*>(ws + L.seg_key);
+    WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
+    const int sort = p.group_needs_sort ? 1 : 0;
+    if (p.v_outer)
+        k_join_small<true><<<1, kSmallThreads, 0, s>>>(v_keys, L.n_v, p.nk[1], desc_v(p), u_keys, L.n_u, p.nk[0],
+                                                        u_keys, p.nk[0], v_keys, p.nk[1], wd, sort, cap, pu, pv,
+                                                        seg_start, seg_key, hdr);
+    else
+        k_join_small<false><<<1, kSmallThreads, 0, s>>>(u_keys, L.n_u, p.nk[0], desc_u(p), v_keys, L.n_v, p.nk[1],
+                                                         u_keys, p.nk[0], v_keys, p.nk[1], wd, sort, cap, pu, pv,
+                                                         seg_start, seg_key, hdr);
+    return hipGetLastError();
+}
 
 bool v_dense(const Plan& p, int64_t n_u) {
     if (!(p.v_outer && p.nk[0] == p.n_join && p.nk[0] > 0)) return false;

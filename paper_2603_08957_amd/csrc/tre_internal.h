@@ -20,6 +20,32 @@ __device__ inline uint16_t f32_to_bf16_rne(float f) {
     return uint16_t(u >> 16);
 }
 
+// Exclusive scan of one int32 per thread over a workgroup of W threads
+// (a multiple of 64); wsum holds W / 64 ints of LDS.  Every thread of the
+// workgroup must call it.
+template <int W>
+__device__ inline int32_t block_scan_excl(int32_t v, int32_t* wsum, int32_t* total) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    int32_t x = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int32_t y = __shfl_up(x, d, 64);
+        if (lane >= d) x += y;
+    }
+    if (lane == 63) wsum[w] = x;
+    __syncthreads();
+    int32_t before = 0, all = 0;
+#pragma unroll
+    for (int i = 0; i < W / 64; i++) {
+        const int32_t s = wsum[i];
+        if (i < w) before += s;
+        all += s;
+    }
+    __syncthreads();
+    *total = all;
+    return before + x - v;
+}
+
 constexpr int kMaxDims = 8;
 constexpr int kMaxURanges = 64;
 constexpr int64_t kPaceCounters = int64_t(1) << 20;  // int32 pacing counters in the workspace
@@ -167,6 +193,13 @@ hipError_t launch_join(const Plan& p, const Layout& L, char* ws, const int32_t* 
 // that key space: U's index is the join key itself, one pair per V tuple,
 // written by the GROUP BY stage (the pair count is n_v, known on the host)
 bool v_dense(const Plan& p, int64_t n_u);
+// The whole join (runs, offsets, expansion, segments) in one workgroup when
+// the pairs come out grouped by W key, the driving relation has at most 4096
+// tuples and the capacity (min(workspace pairs, pair bound)) is at most 4096
+// pairs
+bool small_join_ok(const Plan& p, int64_t n_u, int64_t n_v, int64_t cap);
+hipError_t launch_join_small(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
+                             int64_t cap, hipStream_t s);
 // V without promoted labels (one tuple) and W keyed by U's key as it is:
 // every U tuple is one pair and one group, written without counting
 bool keyed_by_u(const Plan& p);

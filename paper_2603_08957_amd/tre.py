@@ -47,7 +47,7 @@ class TreError(RuntimeError):
 class Options(ctypes.Structure):
     _fields_ = [("validate_keys", ctypes.c_int32), ("max_pairs_per_unit", ctypes.c_int32),
                 ("u_ranges", ctypes.c_int32), ("pace_windows", ctypes.c_int32), ("w_bf16", ctypes.c_int32),
-                ("reserved", ctypes.c_int32 * 3)]
+                ("small_join", ctypes.c_int32), ("reserved", ctypes.c_int32 * 2)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -69,9 +69,11 @@ class Timing(ctypes.Structure):
                 ("reduce_ms", ctypes.c_float), ("total_ms", ctypes.c_float), ("deferred", ctypes.c_int32),
                 ("pending", ctypes.c_int32), ("n_units", ctypes.c_int64), ("n_split_segments", ctypes.c_int64),
                 ("n_partials", ctypes.c_int64), ("events", ctypes.c_void_p * 4), ("contract_path", ctypes.c_int32),
-                ("reserved", ctypes.c_int32)]
+                ("join_path", ctypes.c_int32)]
 
     PATHS = {0: "gemm", 1: "vec", 2: "gemm128", 3: "gemm128_paced", 4: "gemm128_u_ranges"}
+    JOIN_PATHS = {0: "u_driven", 1: "v_driven", 2: "v_driven_one_match", 3: "v_driven_dense", 4: "keyed_by_u",
+                  5: "one_workgroup"}
 
     def read(self):
         """Wait for deferred events and fill the millisecond fields."""
@@ -79,8 +81,9 @@ class Timing(ctypes.Structure):
         return self
 
     def as_dict(self):
-        d = {k: getattr(self, k) for k, _ in self._fields_ if k not in ("events", "deferred", "pending", "reserved")}
+        d = {k: getattr(self, k) for k, _ in self._fields_ if k not in ("events", "deferred", "pending")}
         d["contract_path"] = self.PATHS.get(self.contract_path, self.contract_path)
+        d["join_path"] = self.JOIN_PATHS.get(self.join_path, self.join_path)
         return d
 
 
@@ -156,7 +159,7 @@ class Plan:
 
     def __init__(self, einsum: str, upper: str, extents: dict, tiles: dict, dtype: str = "f32",
                  validate: bool = True, max_pairs_per_unit: int = 0, u_ranges: int = 0, pace_windows: int = 0,
-                 w_bf16: bool = False):
+                 w_bf16: bool = False, small_join: int = 0):
         L = lib()
         ext = np.zeros(26, dtype=np.int64)
         til = np.ones(26, dtype=np.int32)
@@ -164,7 +167,8 @@ class Plan:
             ext[ord(k) - 97] = v
         for k, v in (tiles or {}).items():
             til[ord(k) - 97] = v
-        opt = Options(int(validate), int(max_pairs_per_unit), int(u_ranges), int(pace_windows), int(w_bf16))
+        opt = Options(int(validate), int(max_pairs_per_unit), int(u_ranges), int(pace_windows), int(w_bf16),
+                      int(small_join))
         self.w_bf16 = bool(w_bf16)
         h = ctypes.c_void_p(0)
         rc = L.tre_plan(einsum.encode(), upper.encode(), ext.ctypes.data_as(ctypes.c_void_p),

@@ -92,7 +92,7 @@ def test_relation_from_dense_matches_the_generator(bench):
 
     import workloads
 
-    w = workloads.config(1, "small")
+    w = workloads.config(1, "small", y_layout="jk")
     n = w["n"]
     Y = np.zeros((n, n), np.float32)
     Y[w["Y"]["coo"][0][:, 0], w["Y"]["coo"][0][:, 1]] = w["Y"]["coo"][1]

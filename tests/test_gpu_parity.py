@@ -54,7 +54,11 @@ def test_worked_example_gpu(orc, name):
 
 
 @pytest.mark.parametrize("seed", range(60))
-def test_random_plans_gpu(orc, seed):
+@pytest.mark.parametrize("small_join", [0, -1])
+def test_random_plans_gpu(orc, seed, small_join):
+    """Random small EinSums against the oracle, with the one-workgroup join
+    allowed (most of these inputs take it) and switched off (the multi-kernel
+    join on the same inputs)."""
     rng = np.random.default_rng(1000 + seed)
     e, upper, ext, til = random_plan(rng)
     u_lab, v_lab, _ = split_einsum(e)
@@ -64,10 +68,10 @@ def test_random_plans_gpu(orc, seed):
     spec = workloads.spec(e, upper, ext, til, dtype)
     say("random plan", seed, e, upper, til, len(U["keys"]), len(V["keys"]))
     if len(U["keys"]) == 0 or len(V["keys"]) == 0:
-        _, out = gpu_run(spec, U, V)
+        _, out = gpu_run(spec, U, V, small_join=small_join)
         assert out.n_pairs == 0 and out.n_w == 0
         return
-    _, out = gpu_run(spec, U, V)
+    _, out = gpu_run(spec, U, V, small_join=small_join)
     ref = orc.run(orc_plan(orc, spec), U, V)
     check(out, ref, dtype)
 
@@ -765,3 +769,67 @@ def test_v_dense_workspace_gpu(orc):
     assert ei.value.status == "TRE_E_WORKSPACE" and ei.value.join_result.n_pairs == len(V["keys"])
     out = tre.einsum(plan, uk, ut, vk, vt, want_pairs=True, pair_hint=1)
     check(out, orc.run(orc_plan(orc, spec), U, V), "f32")
+
+
+SMALL_JOINS = [
+    # (einsum, upper, extents, tiles, keep U, keep V): small joins of every
+    # join direction and GROUP BY order; those whose pairs come out grouped
+    # take the one-workgroup path, the others (sorted by W key) must not
+    ("ij,jk->ki", "jk", {"i": 8, "j": 64, "k": 64}, {"j": 1, "k": 1}, 0.9, 0.3),       # driven by U, sorted by K
+    ("ik,kn->in", "ik", {"i": 64, "k": 64, "n": 8}, {"i": 4, "k": 4}, 0.3, 1.0),       # driven by U, in order
+    ("ij,kj->ki", "jk", {"i": 8, "j": 64, "k": 64}, {"j": 1, "k": 1}, 0.7, 0.3),       # driven by V, one match
+    ("ja,kj->k", "jka", {"j": 40, "a": 12, "k": 40}, {"j": 4, "a": 3, "k": 4}, 0.5, 0.5),  # driven by V, runs
+    ("i,j->ij", "ij", {"i": 60, "j": 50}, {"i": 1, "j": 1}, 0.8, 0.8),                 # cross product
+    ("ij,jk->ik", "ijk", {"i": 12, "j": 12, "k": 12}, {"i": 1, "j": 1, "k": 1}, 0.5, 0.5),  # sorted by (I, K)
+    ("ij,jk->ki", "jk", {"i": 8, "j": 64, "k": 64}, {"j": 1, "k": 1}, 0.9, 0.0),       # no V tuples
+]
+
+
+@pytest.mark.parametrize("idx", range(len(SMALL_JOINS)))
+def test_small_join_gpu(orc, idx):
+    """The one-workgroup join: pairs, keys and values against the oracle,
+    the path reported by tre_timing, and the multi-kernel join's pair list,
+    keys and bits on the same inputs."""
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    e, upper, ext, til, ku, kv = SMALL_JOINS[idx]
+    rng = np.random.default_rng(600 + idx)
+    u_lab, v_lab, _ = split_einsum(e)
+    U = workloads.random_relation(rng, u_lab, upper, ext, til, "f32", keep=ku, zero_frac=0.1)
+    V = workloads.random_relation(rng, v_lab, upper, ext, til, "f32", keep=kv, zero_frac=0.1)
+    spec = workloads.spec(e, upper, ext, til, "f32")
+    say("small join", idx, e, len(U["keys"]), len(V["keys"]))
+    uk, ut = to_dev(U)
+    vk, vt = to_dev(V)
+    small = tre.einsum(tre.Plan.from_spec(spec), uk, ut, vk, vt, want_pairs=True, timing=True)
+    multi = tre.einsum(tre.Plan.from_spec(spec, small_join=-1), uk, ut, vk, vt, want_pairs=True, timing=True)
+    torch.cuda.synchronize()
+    plan = tre.Plan.from_spec(spec)
+    if len(V["keys"]) and len(U["keys"]) and not plan.group_needs_sort:
+        assert small.timing["join_path"] == "one_workgroup", small.timing
+    assert multi.timing["join_path"] != "one_workgroup"
+    assert small.n_pairs == multi.n_pairs and small.n_w == multi.n_w
+    if small.n_pairs:
+        assert torch.equal(small.pairs, multi.pairs) and torch.equal(small.w_keys, multi.w_keys)
+        assert torch.equal(small.w_tiles.view(torch.int32), multi.w_tiles.view(torch.int32))
+        check(small, orc.run(orc_plan(orc, spec), U, V), "f32")
+    else:
+        assert small.n_w == 0
+
+
+def test_small_join_workspace_gpu():
+    """The one-workgroup join with room for fewer pairs than the join makes:
+    TRE_E_WORKSPACE with the full pair count."""
+    import paper_2603_08957_amd as tre
+    import torch
+
+    plan = tre.Plan("i,j->ij", "ij", {"i": 40, "j": 30}, {"i": 1, "j": 1}, "f32")
+    k40 = torch.arange(40, dtype=torch.int32, device="cuda").reshape(-1, 1)
+    k30 = torch.arange(30, dtype=torch.int32, device="cuda").reshape(-1, 1)
+    ws = tre.alloc_workspace(plan.workspace_bytes(40, 30, 100))
+    tm = tre.Timing()
+    with pytest.raises(tre.TreError) as ei:
+        tre.join(plan, k40, 40, k30, 30, ws, timing=tm)
+    assert ei.value.status == "TRE_E_WORKSPACE" and ei.value.join_result.n_pairs == 1200

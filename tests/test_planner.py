@@ -327,7 +327,7 @@ def test_tiled_count_matches_generated_tiles():
     4094.6 tuples, the generator stores 4094 tiles."""
     from paper_2603_08957_amd import planner as pl
 
-    w = workloads.config(1)
+    w = workloads.config(1, y_layout="jk")
     st = pl.stats_from_coo("jk", {"j": 4096, "k": 4096}, w["Y"]["coo"][0], 4, {"j": [64], "k": [64]})
     assert st.v("j", 64) == 64 and st.v("k", 64) == 64
     t = {"labels": "jk", "extents": st.extents, "nnz": st.nnz, "distinct": st.distinct, "tiled": st.tiled,

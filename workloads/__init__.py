@@ -307,9 +307,13 @@ def config(c: int, scale: str = "full", **kw) -> dict:
     seed = SEED_BASE + c
     small = scale == "small"
     if c == 1:
+        # the adjacency stored destination-major (keyed (K, J)), as for workload 5
         n = 1024 if small else 4096
+        kw.setdefault("y_layout", "kj")
         return gnn_chain(n, 64, 32, 64, 64, {"kind": "fixed", "d": 8, "values": "ones"}, "f32", seed, **kw)
     if c == 2:
+        # source-major (keyed (J, K)): its 128x128 MFMA path streams the tiles
+        # with their rows contiguous
         n = 4096 if small else 262144
         return gnn_chain(n, 128, 128, 128, 128, {"kind": "powerlaw", "alpha": 2.1, "mean": 16, "values": "normal"},
                          "bf16", seed, dense_y_tiles=small, **kw)
