@@ -148,7 +148,8 @@ typedef struct {
     int32_t join_path;        /* out (tre_join): 0 driven by U (runs searched in V), 1 driven by V (runs
                                  searched in U), 2 driven by V with at most one U tuple each, 3 driven by V
                                  over a U holding every key (no search), 4 keyless one-tuple V with W keyed by
-                                 U, 5 the whole join in one workgroup (small inputs) */
+                                 U, 5 the whole join in one workgroup (small inputs), 6 driven by U over a V
+                                 holding every key (no search) */
 } tre_timing;
 
 /* tre_plan -- parse and classify one binary EinSum (host only, no device work).

@@ -224,9 +224,10 @@ tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const i
     // that count on the device (its grids are sized for the workspace's
     // capacity), so one read-back at the end returns the key checks, the
     // pair count and the key count together
-    if (n_u > 0 && n_v > 0 && v_dense(p, n_u) && n_v > max_pairs) {
-        // one pair per V tuple, known without the device
-        out->n_pairs = n_v;
+    if (n_u > 0 && n_v > 0 && (v_dense(p, n_u) || u_dense(p, n_v)) &&
+        (v_dense(p, n_u) ? n_v : n_u) > max_pairs) {
+        // one pair per tuple of the driving relation, known without the device
+        out->n_pairs = v_dense(p, n_u) ? n_v : n_u;
         set_error("tre_join: workspace too small for the matched pairs (see n_pairs)");
         return TRE_E_WORKSPACE;
     }
@@ -276,6 +277,7 @@ tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const i
         timing->total_ms = timing->join_ms;
         timing->join_path = small ? 5
                             : v_dense(p, n_u)                          ? 3
+                            : u_dense(p, n_v)                          ? 6
                             : (p.v_outer && p.nk[0] == p.n_join)       ? 2
                             : p.v_outer                                ? 1
                                                                        : 0;

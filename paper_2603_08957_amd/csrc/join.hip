@@ -370,39 +370,59 @@ __global__ __launch_bounds__(kThreads) void k_expand(const int64_t* __restrict__
     }
 }
 
-// The join driven by V when U holds every key of its key space (n_u = the
-// product of its radices) and that key is the join labels: sorted strictly
-// increasing keys are then exactly 0 .. n_u - 1, so V tuple v meets the U
-// tuple whose index is its join key read as a mixed-radix number, and pair
-// v is (that index, v) -- no search, no flags, no scan.  Attributes outside
-// their range (keys that fail validation, reported by the host) are clamped
-// so nothing is read out of bounds.
+// A join where the searched relation holds every key of its key space and
+// that key is exactly the join labels: sorted strictly increasing keys are
+// then 0 .. n - 1 read as mixed-radix numbers, so every tuple of the driving
+// ("outer") relation meets the one tuple whose index is its join key -- no
+// search, no counts, no scan; pair o is the outer tuple o.  VO: the outer
+// relation is V (a V-driven join, the pairs come out grouped by W key);
+// otherwise U drives and V is the complete one.  Attributes outside their
+// range (keys that fail validation, reported by the host) are clamped so
+// nothing is read out of bounds.
 struct Radices {
     int32_t n;
     int32_t r[26];
 };
 
-// With `first` (the key-space segment search, zeroed), the pass also marks
-// every W key's first pair, as k_first_of_key would: first[k] = 1 + v.
-template <typename KT>
-__global__ void k_vdense(const int32_t* __restrict__ vkeys, int64_t n_v, int rv, KeyDesc dv, Radices ur,
-                         const int32_t* __restrict__ ukeys, int ru, WDesc wd, int32_t* __restrict__ pu,
-                         int32_t* __restrict__ pv, KT* __restrict__ wk, WsHeader* __restrict__ hdr,
-                         int32_t* __restrict__ first, int64_t nk) {
-    const int64_t v = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (v >= n_v) return;
-    if (v == 0) hdr->n_pairs = n_v;
-    const int32_t* vrow = vkeys + v * rv;
-    int64_t u = 0;
-    for (int i = 0; i < dv.n; i++) u = u * ur.r[i] + min(max(vrow[dv.pos[i]], 0), ur.r[i] - 1);
-    pu[v] = int32_t(u);
-    pv[v] = int32_t(v);
-    // W's key is V's key prefix (a V-driven join): the key of pair v is that
-    // of V tuple v
-    const KT k = KT(pack_w(ukeys + u * ru, vrow, wd));
-    wk[v] = k;
-    if (first && (v == 0 || KT(pack_w(ukeys, vrow - rv, wd)) != k) && uint64_t(k) < uint64_t(nk))
-        first[k] = int32_t(v + 1);
+// With `uv` (the GROUP BY sort follows) the pass writes packed (u, v)
+// payloads instead of the pair arrays.  With `first` (the key-space segment
+// search, zeroed; only when no sort follows), it also marks every W key's
+// first pair, as k_first_of_key would: first[k] = 1 + o.
+template <typename KT, bool VO>
+__global__ void k_dense(const int32_t* __restrict__ okeys, int64_t n_o, int ro, KeyDesc dout, Radices ir,
+                        const int32_t* __restrict__ ukeys, int ru, const int32_t* __restrict__ vkeys, int rv, WDesc wd,
+                        int32_t* __restrict__ pu, int32_t* __restrict__ pv, KT* __restrict__ wk,
+                        uint64_t* __restrict__ uv, WsHeader* __restrict__ hdr, int32_t* __restrict__ first,
+                        int64_t nk) {
+    const int64_t o = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (o >= n_o) return;
+    if (o == 0) hdr->n_pairs = n_o;
+    auto pair_of = [&](int64_t x, int64_t& u, int64_t& v) {
+        const int32_t* row = okeys + x * ro;
+        int64_t in = 0;
+        for (int i = 0; i < dout.n; i++) in = in * ir.r[i] + min(max(row[dout.pos[i]], 0), ir.r[i] - 1);
+        u = VO ? in : x;
+        v = VO ? x : in;
+    };
+    int64_t u, v;
+    pair_of(o, u, v);
+    const KT k = KT(pack_w(ukeys + u * ru, vkeys + v * rv, wd));
+    wk[o] = k;
+    if (uv) {
+        uv[o] = (uint64_t(uint32_t(u)) << 32) | uint64_t(uint32_t(v));
+        return;
+    }
+    pu[o] = int32_t(u);
+    pv[o] = int32_t(v);
+    if (first && uint64_t(k) < uint64_t(nk)) {
+        bool head = o == 0;
+        if (!head) {
+            int64_t u1, v1;
+            pair_of(o - 1, u1, v1);
+            head = KT(pack_w(ukeys + u1 * ru, vkeys + v1 * rv, wd)) != k;
+        }
+        if (head) first[k] = int32_t(o + 1);
+    }
 }
 
 // Pairs of the join driven by V with at most one U tuple per V tuple:
@@ -699,7 +719,8 @@ hipError_t launch_join(const Plan& p, const Layout& L, char* ws, const int32_t* 
     int32_t* hist = reinterpret_cast<int32_t*>(ws + L.hist);
     const int64_t n_u = L.n_u, n_v = L.n_v;
     hipError_t e = hipSuccess;
-    if (v_dense(p, n_u)) return hipSuccess;  // the pairs are written by the GROUP BY stage, one per V tuple
+    // one pair per tuple of the driving relation, written by the GROUP BY stage
+    if (v_dense(p, n_u) || u_dense(p, n_v)) return hipSuccess;
     if (p.v_outer && p.nk[0] == p.n_join) {
         // walk V: each V tuple meets at most one U tuple (U's key is the join labels)
         int32_t* pos = reinterpret_cast<int32_t*>(ws + L.ucnt);
@@ -777,15 +798,24 @@ hipError_t group_impl(const Plan& p, const Layout& L, char* ws, const int32_t* u
     const bool by_key = p.w_total_bits > 0 && p.w_total_bits <= 30 && key_space <= cap;
     int32_t* first = flags;  // key-space segment search: key_space + 1 <= cap + 1 entries
     bool first_done = false;
-    if (cap > 0 && v_dense(p, L.n_u)) {
-        Radices ur{};
-        ur.n = p.nk[0];
-        for (int i = 0; i < p.nk[0]; i++) ur.r[i] = p.radix[0][i];
-        if (by_key && (e = launch_fill_zero(first, sizeof(int32_t) * size_t(key_space), s)) != hipSuccess) return e;
-        k_vdense<KT><<<blocks_for(L.n_v), kThreads, 0, s>>>(v_keys, L.n_v, p.nk[1], desc_v(p), ur, u_keys, p.nk[0], wd,
-                                                             pu, pv, wk, hdr, by_key ? first : nullptr, key_space);
+    if (cap > 0 && (v_dense(p, L.n_u) || u_dense(p, L.n_v))) {
+        const bool vo = v_dense(p, L.n_u);
+        const int in_op = vo ? 0 : 1;  // the complete relation, indexed by the join key
+        Radices ir{};
+        ir.n = p.nk[in_op];
+        for (int i = 0; i < p.nk[in_op]; i++) ir.r[i] = p.radix[in_op][i];
+        const bool mark = by_key && !sort;
+        if (mark && (e = launch_fill_zero(first, sizeof(int32_t) * size_t(key_space), s)) != hipSuccess) return e;
+        if (vo)
+            k_dense<KT, true><<<blocks_for(L.n_v), kThreads, 0, s>>>(v_keys, L.n_v, p.nk[1], desc_v(p), ir, u_keys,
+                                                                     p.nk[0], v_keys, p.nk[1], wd, pu, pv, wk, uv, hdr,
+                                                                     mark ? first : nullptr, key_space);
+        else
+            k_dense<KT, false><<<blocks_for(L.n_u), kThreads, 0, s>>>(u_keys, L.n_u, p.nk[0], desc_u(p), ir, u_keys,
+                                                                      p.nk[0], v_keys, p.nk[1], wd, pu, pv, wk, uv, hdr,
+                                                                      mark ? first : nullptr, key_space);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        first_done = by_key;
+        first_done = mark;
     } else if (cap > 0 && p.v_outer && p.nk[0] == p.n_join) {
         k_vwrite<KT><<<blocks_for(L.n_v), kThreads, 0, s>>>(
             reinterpret_cast<const int32_t*>(ws + L.ucnt), reinterpret_cast<const int32_t*>(ws + L.ulo), L.n_v, hdr,
@@ -873,6 +903,16 @@ hipError_t launch_join_small(const Plan& p, const Layout& L, char* ws, const int
                                                          u_keys, p.nk[0], v_keys, p.nk[1], wd, sort, cap, pu, pv,
                                                          seg_start, seg_key, hdr);
     return hipGetLastError();
+}
+
+bool u_dense(const Plan& p, int64_t n_v) {
+    if (p.v_outer || p.v_needs_sort || !(p.nk[1] == p.n_join && p.nk[1] > 0)) return false;
+    int64_t space = 1;
+    for (int i = 0; i < p.nk[1]; i++) {
+        space *= p.radix[1][i];
+        if (space > n_v) return false;
+    }
+    return space == n_v;
 }
 
 bool v_dense(const Plan& p, int64_t n_u) {

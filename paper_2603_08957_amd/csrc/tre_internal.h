@@ -193,6 +193,9 @@ hipError_t launch_join(const Plan& p, const Layout& L, char* ws, const int32_t* 
 // that key space: U's index is the join key itself, one pair per V tuple,
 // written by the GROUP BY stage (the pair count is n_v, known on the host)
 bool v_dense(const Plan& p, int64_t n_u);
+// The same with U driving: V's key is the join labels and V holds every key of
+// that key space (one pair per U tuple, the pair count n_u known on the host)
+bool u_dense(const Plan& p, int64_t n_v);
 // The whole join (runs, offsets, expansion, segments) in one workgroup when
 // the pairs come out grouped by W key, the driving relation has at most 4096
 // tuples and the capacity (min(workspace pairs, pair bound)) is at most 4096

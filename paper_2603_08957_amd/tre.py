@@ -73,7 +73,7 @@ class Timing(ctypes.Structure):
 
     PATHS = {0: "gemm", 1: "vec", 2: "gemm128", 3: "gemm128_paced", 4: "gemm128_u_ranges"}
     JOIN_PATHS = {0: "u_driven", 1: "v_driven", 2: "v_driven_one_match", 3: "v_driven_dense", 4: "keyed_by_u",
-                  5: "one_workgroup"}
+                  5: "one_workgroup", 6: "u_driven_dense"}
 
     def read(self):
         """Wait for deferred events and fill the millisecond fields."""

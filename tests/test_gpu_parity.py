@@ -833,3 +833,35 @@ def test_small_join_workspace_gpu():
     with pytest.raises(tre.TreError) as ei:
         tre.join(plan, k40, 40, k30, 30, ws, timing=tm)
     assert ei.value.status == "TRE_E_WORKSPACE" and ei.value.join_result.n_pairs == 1200
+
+
+U_DENSE_PLANS = [
+    # (einsum, upper, extents, tiles, dtype): joins driven by U over a V that
+    # holds every key of its key space (V's key is the join labels), with and
+    # without the GROUP BY sort
+    ("im,mk->ik", "im", {"i": 300, "m": 40, "k": 16}, {"i": 1, "m": 1}, "f32"),   # attention projection form
+    ("ik,kn->in", "ik", {"i": 64, "k": 64, "n": 8}, {"i": 4, "k": 4}, "f32"),     # block-sparse form
+    ("mi,mk->ik", "im", {"i": 50, "m": 30, "k": 16}, {"i": 1, "m": 1}, "bf16"),   # W key not U's prefix: sorted
+    ("iab,ab->i", "iab", {"i": 40, "a": 6, "b": 5}, {"i": 1, "a": 2, "b": 1}, "f32"),  # two join labels
+]
+
+
+@pytest.mark.parametrize("idx", range(len(U_DENSE_PLANS)))
+@pytest.mark.parametrize("validate", [True, False])
+def test_u_dense_join_gpu(orc, idx, validate):
+    """U-driven joins over a complete V (V's index is the join key itself),
+    with the one-workgroup join switched off so the dense pass runs: pairs,
+    keys and values against the oracle."""
+    import paper_2603_08957_amd as tre
+
+    e, upper, ext, til, dtype = U_DENSE_PLANS[idx]
+    rng = np.random.default_rng(700 + idx)
+    u_lab, v_lab, _ = split_einsum(e)
+    U = workloads.random_relation(rng, u_lab, upper, ext, til, dtype, keep=0.4, zero_frac=0.05)
+    V = workloads.random_relation(rng, v_lab, upper, ext, til, dtype, keep=1.0, zero_frac=0.05)
+    spec = workloads.spec(e, upper, ext, til, dtype)
+    plan = tre.Plan.from_spec(spec, validate=validate, small_join=-1)
+    say("u dense", idx, validate, e, len(U["keys"]), len(V["keys"]))
+    out = tre.einsum(plan, *to_dev(U), *to_dev(V), want_pairs=True, timing=True)
+    assert out.timing["join_path"] == "u_driven_dense", out.timing
+    check(out, orc.run(orc_plan(orc, spec), U, V), dtype)
