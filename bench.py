@@ -94,6 +94,19 @@ class Stage:
                 "contract_path": self.tre.Timing.PATHS.get(t.contract_path, t.contract_path)}
 
     def run(self, uk, ut, vk, vt, timing=None):
+        """Join + contraction: one tre_execute call once the outputs are
+        sized (no return to Python between the two), else join, size the
+        outputs, contract."""
+        if self.w_tiles is not None and self.record is None:
+            try:
+                n_w, n_p = self.tre.execute(self.plan, uk, ut, vk, vt,
+                                            self.w_keys if self.plan.key_arity[2] else None, self.w_tiles, self.ws,
+                                            self.pairs_out, timing=timing)
+                self.n_pairs, self.n_w = n_p, n_w
+                return self.w_keys[:n_w], self.w_tiles[:n_w]
+            except self.tre.TreError as e:
+                if e.status not in ("TRE_E_CAPACITY", "TRE_E_WORKSPACE"):
+                    raise
         jr = self.join(uk, vk, timing=timing)
         return self.contract(jr, ut, vt, timing=timing)
 

@@ -591,13 +591,31 @@ __global__ __launch_bounds__(kThreads) void k_vec(VecArgs a) {
     };
     int p = un.p0;
     if constexpr (PU > 1) {
+        // groups of PU pairs; the pair indices of the next group are loaded
+        // while the current group's tiles are read, so the dependent index ->
+        // tile loads overlap across groups
+        int32_t iu[PU], iv[PU];
+        if (p + PU <= un.p1) {
+#pragma unroll
+            for (int j = 0; j < PU; j++) {
+                iu[j] = a.pu[p + j];
+                iv[j] = a.pv[p + j];
+            }
+        }
         for (; p + PU <= un.p1; p += PU) {
             const T* ub[PU];
             const T* vb[PU];
 #pragma unroll
             for (int j = 0; j < PU; j++) {
-                ub[j] = U + int64_t(a.pu[p + j]) * a.u_elems + eu;
-                vb[j] = V + int64_t(a.pv[p + j]) * a.v_elems + ev;
+                ub[j] = U + int64_t(iu[j]) * a.u_elems + eu;
+                vb[j] = V + int64_t(iv[j]) * a.v_elems + ev;
+            }
+            if (p + 2 * PU <= un.p1) {
+#pragma unroll
+                for (int j = 0; j < PU; j++) {
+                    iu[j] = a.pu[p + PU + j];
+                    iv[j] = a.pv[p + PU + j];
+                }
             }
             for (int k = 0; k < a.K; k++)
 #pragma unroll
@@ -642,7 +660,7 @@ template <typename T, int EPT>
 hipError_t vec_dispatch(const Plan& p, const VecArgs& a, dim3 grid, hipStream_t s) {
     const bool pu4 = p.nK <= 2;
     if (p.vec_vbcast) {
-        if (pu4) k_vec<T, EPT, true, 4><<<grid, kThreads, 0, s>>>(a);
+        if (pu4) k_vec<T, EPT, true, 8><<<grid, kThreads, 0, s>>>(a);
         else k_vec<T, EPT, true, 1><<<grid, kThreads, 0, s>>>(a);
     } else {
         if (pu4) k_vec<T, EPT, false, 4><<<grid, kThreads, 0, s>>>(a);

@@ -245,6 +245,25 @@ def join_keys(plan: Plan, jr: JoinResult, w_keys, stream=None):
            "tre_join_keys")
 
 
+def execute(plan: Plan, u_keys, u_tiles, v_keys, v_tiles, w_keys, w_tiles, ws, pairs_out=None, stream=None,
+            timing: Timing | None = None):
+    """tre_execute into caller-owned outputs and workspace (their row counts
+    are the capacities): the join and the contraction in one call.  Returns
+    (n_w, n_pairs); a TreError carries them when a capacity is short."""
+    n_u, n_v = int(u_tiles.shape[0]), int(v_tiles.shape[0])
+    n_w, n_p = ctypes.c_int64(0), ctypes.c_int64(0)
+    rc = lib().tre_execute(plan.handle, _ptr(u_keys), n_u, _ptr(u_tiles), _ptr(v_keys), n_v, _ptr(v_tiles),
+                           _ptr(w_keys), _ptr(w_tiles), int(w_tiles.shape[0]) if w_tiles is not None else 0,
+                           ctypes.byref(n_w), _ptr(pairs_out), int(pairs_out.shape[0]) if pairs_out is not None else 0,
+                           ctypes.byref(n_p), _ptr(ws), ws.numel(), _stream(stream),
+                           ctypes.byref(timing) if timing is not None else None)
+    if rc != 0:
+        err = TreError(rc, "tre_execute", lib().tre_last_error().decode())
+        err.n_w, err.n_pairs = int(n_w.value), int(n_p.value)
+        raise err
+    return int(n_w.value), int(n_p.value)
+
+
 @dataclass
 class Output:
     w_keys: object      # torch int32 [n_w, r_W]
