@@ -145,7 +145,7 @@ typedef struct {
     int32_t contract_path;    /* out: the contraction launch tre_contract chose: 0 generic MFMA GEMM (64x64
                                  blocks), 1 vector class, 2 128x128 MFMA path, 3 the same as a paced
                                  persistent grid, 4 the same with U-range units (partials summed after) */
-    int32_t join_path;        /* out (tre_join): 0 driven by U (runs searched in V), 1 driven by V (runs
+    int32_t join_path;        /* out (tre_join, tre_execute3): 0 driven by U (runs searched in V), 1 driven by V (runs
                                  searched in U), 2 driven by V with at most one U tuple each, 3 driven by V
                                  over a U holding every key (no search), 4 keyless one-tuple V with W keyed by
                                  U, 5 the whole join in one workgroup (small inputs), 6 driven by U over a V
@@ -369,9 +369,16 @@ tre_status tre_repartition(const char *labels, const char *upper_in, const char 
  *             empty (each workgroup finds its range of triples itself),
  *             contract_ms the fused contraction kernel, reduce_ms the sum of
  *             output blocks split between workgroups (none in the masked
- *             form) and the key write-out.
- * Synchronizes the stream twice (triple count, output key count); key errors
- * as TRE_E_UNSORTED / TRE_E_DUPKEY / TRE_E_KEYRANGE. */
+ *             form) and the key write-out; join_path 6 (partners indexed by
+ *             key value) or 0 (searched).
+ * When V and X each hold every key of their label's range (n_v and n_x equal
+ * the number of tiles along a and b), every U tuple is a triple whose
+ * partners are its own key values: no search and no triple count to read
+ * back.  Synchronizes the stream twice (triple count, output key count) when
+ * searching, once (output key count) otherwise, and once at the end in the
+ * masked form without search, whose outputs are then written before the key
+ * checks are read (their contents are unspecified when a key error is
+ * returned).  Key errors as TRE_E_UNSORTED / TRE_E_DUPKEY / TRE_E_KEYRANGE. */
 size_t tre_execute3_workspace_bytes(const char *einsum, const char *upper, const int64_t *extent,
                                     const int32_t *tile, int64_t n_u);
 tre_status tre_execute3(const char *einsum, const char *upper, const int64_t *extent, const int32_t *tile,

@@ -131,6 +131,32 @@ __global__ void k3_compact(const int32_t* __restrict__ u_keys, int64_t n_u, F3De
     if (perm) perm[t] = uint32_t(t);
 }
 
+// When the p and q operands hold every key of their key spaces, every U
+// tuple is a triple and its partners are its own key values (sorted strictly
+// increasing keys of n = radix tuples are exactly 0 .. n - 1): triple s is
+// U tuple s, no search, no scan.  Key values outside their range come only
+// from keys that fail validation (reported by the host) and are clamped so
+// nothing is read out of bounds.  `wkey` may be null (the masked form, whose
+// output keys are U's keys).
+__global__ void k3_dense(const int32_t* __restrict__ u_keys, int64_t n_u, F3Desc d, int32_t* __restrict__ tu,
+                         int32_t* __restrict__ tp, int32_t* __restrict__ tq, uint64_t* __restrict__ wkey,
+                         uint32_t* __restrict__ perm) {
+    const int64_t s = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (s >= n_u) return;
+    const int32_t* key = u_keys + s * d.ru;
+    tu[s] = int32_t(s);
+    tp[s] = min(max(key[d.pos_p], 0), d.radix_p - 1);
+    tq[s] = min(max(key[d.pos_q], 0), d.radix_q - 1);
+    if (wkey) wkey[s] = pack_w(key, d);
+    if (perm) perm[s] = uint32_t(s);
+}
+
+// Output keys of the masked form: U's keys, row for row.
+__global__ void k3_copy_keys(const int32_t* __restrict__ u_keys, int64_t n, int32_t* __restrict__ out) {
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i < n) out[i] = u_keys[i];
+}
+
 // Triples in sorted order, from the permutation of the sort.
 __global__ void k3_gather(const uint32_t* __restrict__ perm, int64_t n, const int32_t* __restrict__ tu,
                           const int32_t* __restrict__ tp, const int32_t* __restrict__ tq, int32_t* __restrict__ su,
@@ -599,6 +625,28 @@ tre_status dev_fail(hipError_t e, const char* where) {
     return TRE_E_DEVICE;
 }
 
+// Phase times from the five marks (join | units | contraction | reduction).
+void finish_timing(tre_timing* timing, PhaseTimer& tm, bool deferred, bool dense) {
+    if (!timing) return;
+    std::memset(timing, 0, sizeof(*timing));
+    timing->deferred = deferred ? 1 : 0;
+    timing->join_path = dense ? 6 : 0;  // U drives the join; dense: partners indexed by key value
+    timing->join_ms = tm.between(0, 1);
+    timing->total_ms = timing->join_ms;
+    if (deferred && tm.on) {
+        // the events after the join go to the caller; the first is ours
+        for (int i = 0; i < 4; i++) timing->events[i] = reinterpret_cast<void*>(tm.ev[i + 1]);
+        timing->pending = 1;
+        tm.keep = true;
+        (void)hipEventDestroy(tm.ev[0]);
+    } else {
+        timing->units_ms = tm.between(1, 2);
+        timing->contract_ms = tm.between(2, 3);
+        timing->reduce_ms = tm.between(3, 4);
+        timing->total_ms += tm.between(1, 4);
+    }
+}
+
 tre_status fail(tre_status st, const char* msg) {
     set_error(std::string("tre_execute3: ") + msg);
     return st;
@@ -859,31 +907,87 @@ tre_status tre_execute3(const char* einsum, const char* upper, const int64_t* ex
     int32_t* pos = static_cast<int32_t*>(at(L.pos));
     int32_t* ip = static_cast<int32_t*>(at(L.ip));
     int32_t* iq = static_cast<int32_t*>(at(L.iq));
-    k3_match<<<blocks_for(n_u + 1), kThreads, 0, s>>>(u_keys, n_u, d, p_keys, n_p, q_keys, n_q, flag, ip, iq);
-    if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "match");
-    if ((e = scan_exclusive_i32(flag, pos, n_u + 1, static_cast<int32_t*>(at(L.tmp)), s)) != hipSuccess)
-        return dev_fail(e, "scan");
-    F3Header h{};
-    int32_t n_tri32 = 0;
-    if ((e = hipMemcpyAsync(&h, hdr, sizeof(h), hipMemcpyDeviceToHost, s)) != hipSuccess ||
-        (e = hipMemcpyAsync(&n_tri32, pos + n_u, sizeof(int32_t), hipMemcpyDeviceToHost, s)) != hipSuccess ||
-        (e = hipStreamSynchronize(s)) != hipSuccess)
-        return dev_fail(e, "triple count read-back");
-    const int32_t kerr = h.err_u | h.err_p | h.err_q;
-    if (kerr) {
-        set_error("tre_execute3: keys out of range, unsorted or repeated");
-        return (kerr & 4) ? TRE_E_KEYRANGE : (kerr & 1) ? TRE_E_UNSORTED : TRE_E_DUPKEY;
-    }
-    const int64_t nt = n_tri32;
-    *n_triples = nt;
     int32_t* tu = static_cast<int32_t*>(at(L.tu));
     int32_t* tp = static_cast<int32_t*>(at(L.tp));
     int32_t* tq = static_cast<int32_t*>(at(L.tq));
     uint64_t* wkey = static_cast<uint64_t*>(at(L.wkey));
     uint32_t* perm = d.needs_sort ? static_cast<uint32_t*>(at(L.perm)) : nullptr;
+    F3Header h{};
+    auto key_errors = [&]() -> tre_status {
+        const int32_t kerr = h.err_u | h.err_p | h.err_q;
+        if (!kerr) return TRE_OK;
+        set_error("tre_execute3: keys out of range, unsorted or repeated");
+        return (kerr & 4) ? TRE_E_KEYRANGE : (kerr & 1) ? TRE_E_UNSORTED : TRE_E_DUPKEY;
+    };
+    // p and q operands holding every key: each U tuple is a triple (no
+    // search, no count to read back; key checks are read with the key count,
+    // or at the end in the masked form)
+    const bool dense = n_p == d.radix_p && n_q == d.radix_q;
+    int64_t nt = n_u;
+    if (dense) {
+        k3_dense<<<blocks_for(n_u), kThreads, 0, s>>>(u_keys, n_u, d, tu, tp, tq, d.masked ? nullptr : wkey,
+                                                       d.masked ? nullptr : perm);
+        if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "dense triples");
+    } else {
+        k3_match<<<blocks_for(n_u + 1), kThreads, 0, s>>>(u_keys, n_u, d, p_keys, n_p, q_keys, n_q, flag, ip, iq);
+        if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "match");
+        if ((e = scan_exclusive_i32(flag, pos, n_u + 1, static_cast<int32_t*>(at(L.tmp)), s)) != hipSuccess)
+            return dev_fail(e, "scan");
+        int32_t n_tri32 = 0;
+        if ((e = hipMemcpyAsync(&h, hdr, sizeof(h), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+            (e = hipMemcpyAsync(&n_tri32, pos + n_u, sizeof(int32_t), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+            (e = hipStreamSynchronize(s)) != hipSuccess)
+            return dev_fail(e, "triple count read-back");
+        const tre_status ks = key_errors();
+        if (ks != TRE_OK) return ks;
+        nt = n_tri32;
+    }
+    *n_triples = nt;
+    if (dense && d.masked) {
+        // one output tuple per U tuple, keyed as U: nothing to group; the
+        // contraction is enqueued before the one read-back (key checks)
+        *n_w = n_u;
+        if (n_u > w_cap || !w_tiles || (d.rw > 0 && !w_keys)) {
+            // key errors take precedence, as on the searching path
+            if ((e = hipMemcpyAsync(&h, hdr, sizeof(h), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+                (e = hipStreamSynchronize(s)) != hipSuccess)
+                return dev_fail(e, "key check read-back");
+            const tre_status ks = key_errors();
+            if (ks != TRE_OK) return ks;
+            if (n_u > w_cap) return fail(TRE_E_CAPACITY, "w_cap below the output key count");
+            return fail(TRE_E_ARG, "null output buffers");
+        }
+        tm.mark(s);
+        tm.mark(s);
+        const float* P = static_cast<const float*>(d.v_on_p ? v_tiles : x_tiles);
+        const float* Q = static_cast<const float*>(d.v_on_p ? x_tiles : v_tiles);
+        const bool v4 = d.R % 4 == 0 && ((reinterpret_cast<uintptr_t>(P) | reinterpret_cast<uintptr_t>(Q)) & 15) == 0;
+        const int64_t waves = (nt + kMaskedBatch - 1) / kMaskedBatch;
+        const dim3 grid{unsigned((waves + kThreads / 64 - 1) / (kThreads / 64))};
+        if (v4) k3_masked<true><<<grid, kThreads, 0, s>>>(static_cast<const float*>(u_tiles), P, Q, tu, tp, tq, nt,
+                                                         d.te_u, d.R, w_tiles);
+        else k3_masked<false><<<grid, kThreads, 0, s>>>(static_cast<const float*>(u_tiles), P, Q, tu, tp, tq, nt,
+                                                       d.te_u, d.R, w_tiles);
+        if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "masked contract");
+        tm.mark(s);
+        if (d.rw > 0) {
+            k3_copy_keys<<<blocks_for(n_u * d.ru), kThreads, 0, s>>>(u_keys, n_u * d.ru, w_keys);
+            if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "keys");
+        }
+        tm.mark(s);
+        if ((e = hipMemcpyAsync(&h, hdr, sizeof(h), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+            (e = hipStreamSynchronize(s)) != hipSuccess)
+            return dev_fail(e, "key check read-back");
+        const tre_status ks = key_errors();
+        if (ks != TRE_OK) return ks;
+        finish_timing(timing, tm, deferred, dense);
+        return TRE_OK;
+    }
     if (nt > 0) {
-        k3_compact<<<blocks_for(n_u), kThreads, 0, s>>>(u_keys, n_u, d, pos, ip, iq, tu, tp, tq, wkey, perm);
-        if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "compact");
+        if (!dense) {
+            k3_compact<<<blocks_for(n_u), kThreads, 0, s>>>(u_keys, n_u, d, pos, ip, iq, tu, tp, tq, wkey, perm);
+            if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "compact");
+        }
         if (d.needs_sort) {
             if ((e = radix_sort_u64(wkey, perm, static_cast<uint64_t*>(at(L.wkey_alt)),
                                     static_cast<uint32_t*>(at(L.perm_alt)), nt, d.wkey_bits,
@@ -916,6 +1020,10 @@ tre_status tre_execute3(const char* einsum, const char* upper, const int64_t* ex
     if ((e = hipMemcpyAsync(&h, hdr, sizeof(h), hipMemcpyDeviceToHost, s)) != hipSuccess ||
         (e = hipStreamSynchronize(s)) != hipSuccess)
         return dev_fail(e, "key count read-back");
+    if (dense) {
+        const tre_status ks = key_errors();
+        if (ks != TRE_OK) return ks;
+    }
     const int64_t nw = h.n_w;
     *n_w = nw;
     tm.mark(s);
@@ -997,24 +1105,7 @@ tre_status tre_execute3(const char* einsum, const char* upper, const int64_t* ex
         }
         tm.mark(s);
     }
-    if (timing) {
-        std::memset(timing, 0, sizeof(*timing));
-        timing->deferred = deferred ? 1 : 0;
-        timing->join_ms = tm.between(0, 1);
-        timing->total_ms = timing->join_ms;
-        if (deferred && tm.on) {
-            // the events after the join go to the caller; the first is ours
-            for (int i = 0; i < 4; i++) timing->events[i] = reinterpret_cast<void*>(tm.ev[i + 1]);
-            timing->pending = 1;
-            tm.keep = true;
-            (void)hipEventDestroy(tm.ev[0]);
-        } else {
-            timing->units_ms = tm.between(1, 2);
-            timing->contract_ms = tm.between(2, 3);
-            timing->reduce_ms = tm.between(3, 4);
-            timing->total_ms += tm.between(1, 4);
-        }
-    }
+    finish_timing(timing, tm, deferred, dense);
     return TRE_OK;
 }
 

@@ -286,3 +286,96 @@ def test_masked_edge_cases_gpu(orc):
     z = x.clone()
     tre.scale_f32(z, 3.0, out=z)
     np.testing.assert_array_equal(z.cpu().numpy(), x.cpu().numpy() * np.float32(3.0))
+
+
+# ------------------------------------------- small operands holding every key
+
+def _complete(rng, case, keep_u):
+    """The case with V and X refilled to hold every key of their label (the
+    dense path: each U tuple is a triple, partners indexed by key value)
+    and U thinned to `keep_u`."""
+    e, upper, ext, til, U, V, X = case
+    u, v, x = e.split("->")[0].split(",")
+    U = _relation(rng, u, upper, ext, til, keep_u)
+    V = _relation(rng, v, upper, ext, til, 1.0)
+    X = _relation(rng, x, upper, ext, til, 1.0)
+    return e, upper, ext, til, U, V, X
+
+
+def _run_dense(orc, case):
+    import paper_2603_08957_amd as tre
+
+    e, upper, ext, til, U, V, X = case
+    _run_and_check(orc, e, upper, ext, til, U, V, X)
+    uk, ut = to_dev(U)
+    vk, vt = to_dev(V)
+    xk, xt = to_dev(X)
+    _, _, nt, tm = tre.execute3(e, upper, ext, til, uk, ut, vk, vt, xk, xt, timing=True)
+    assert tm["join_path"] == "u_driven_dense" and nt == len(U["keys"])
+    # one V tuple fewer: the searching path, same triples minus those of the dropped key
+    _, _, _, tm = tre.execute3(e, upper, ext, til, uk, ut, vk[1:].contiguous(), vt[1:].contiguous(), xk, xt,
+                               timing=True)
+    assert tm["join_path"] == "u_driven"
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_execute3_dense_gpu(orc, seed):
+    rng = np.random.default_rng(6100 + seed)
+    case = _complete(rng, _case3(rng), [1.0, 0.5, 0.05][seed % 3])
+    say("execute3 dense", seed, case[0], case[1], case[2], case[3], len(case[4]["keys"]))
+    _run_dense(orc, case)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_masked_dense_gpu(orc, seed):
+    rng = np.random.default_rng(6200 + seed)
+    case = _complete(rng, _case_masked(rng), [1.0, 0.4, 0.05][seed % 3])
+    say("masked dense", seed, case[0], case[1], case[2], case[3], len(case[4]["keys"]))
+    _run_dense(orc, case)
+
+
+@pytest.mark.parametrize("masked", [False, True])
+def test_dense_key_errors_gpu(masked):
+    """Key errors on the dense path: out-of-range U values (clamped on the
+    device, reported by the key checks), unsorted U, a repeated key in a
+    complete-sized V, and too small an output capacity after a good key set
+    (capacity) versus after a bad one (the key error wins)."""
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    rng = np.random.default_rng(91)
+    if masked:
+        e, upper, ext, til = "ij,ik,jk->ij", "ij", {"i": 12, "j": 9, "k": 33}, {"i": 1, "j": 1}
+    else:
+        e, upper, ext, til = "ijk,jr,kr->ir", "ijk", {"i": 8, "j": 12, "k": 16, "r": 5}, {"i": 4, "j": 4, "k": 4}
+    u, v, x = e.split("->")[0].split(",")
+    U = _relation(rng, u, upper, ext, til, 0.7)
+    V = _relation(rng, v, upper, ext, til, 1.0)
+    X = _relation(rng, x, upper, ext, til, 1.0)
+    uk, ut = to_dev(U)
+    vk, vt = to_dev(V)
+    xk, xt = to_dev(X)
+    op = tre.Einsum3(e, upper, ext, til, len(U["keys"]))
+    op(uk, ut, vk, vt, xk, xt)
+    bad = uk.clone()
+    bad[-1, -1] = ext[u[-1]] // til[u[-1]]  # one past the last tile along U's last label
+    with pytest.raises(tre.TreError) as err:
+        op(bad, ut, vk, vt, xk, xt)
+    assert err.value.status == "TRE_E_KEYRANGE"
+    with pytest.raises(tre.TreError) as err:
+        op(uk.flip(0).contiguous(), ut, vk, vt, xk, xt)
+    assert err.value.status == "TRE_E_UNSORTED"
+    vdup = vk.clone()
+    vdup[1] = vdup[0]
+    with pytest.raises(tre.TreError) as err:
+        op(uk, ut, vdup, vt, xk, xt)
+    assert err.value.status == "TRE_E_DUPKEY"
+    small = (torch.empty((1, op.w_arity), dtype=torch.int32, device="cuda"),
+             torch.empty((1, op.w_tile_elems), dtype=torch.float32, device="cuda"))
+    with pytest.raises(tre.TreError) as err:
+        op(uk, ut, vk, vt, xk, xt, out=small)
+    assert err.value.status == "TRE_E_CAPACITY"
+    with pytest.raises(tre.TreError) as err:
+        op(bad, ut, vk, vt, xk, xt, out=small)
+    assert err.value.status == "TRE_E_KEYRANGE"
