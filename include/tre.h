@@ -125,13 +125,16 @@ typedef struct {
 } tre_join_result;
 
 /* Optional per-phase device timings (milliseconds, hipEvent based).
- * With `deferred` = 0 the call waits for its own events before returning.
- * With `deferred` != 0 tre_contract only records events on the stream (no
- * wait); tre_timing_read later waits for them, fills the millisecond fields
- * and releases the events.  A struct with `pending` set must be read (or the
- * events leak). */
+ * With `deferred` = 0 every phase is bracketed by events recorded on the
+ * stream and the call waits for them before returning.
+ * With `deferred` != 0 only the contraction kernel is timed, by start and end
+ * events that its own launch records (hipExtLaunchKernel: no marker packets,
+ * no wait, next to no cost for a small call); tre_timing_read later waits for
+ * them, fills contract_ms (the other phase fields stay 0) and releases the
+ * events.  A struct with `pending` set must be read (or the events leak). */
 typedef struct {
-    float join_ms;            /* key validation, join, group-by (tre_join; always immediate) */
+    float join_ms;            /* key validation, join, group-by up to the count read-back (tre_join; not with
+                                 deferred) */
     float units_ms;           /* offset tables and work units */
     float contract_ms;        /* the tile-contraction kernel alone */
     float reduce_ms;          /* segmented sum of split segments + key / pair write-out */
@@ -227,7 +230,8 @@ tre_status tre_contract(tre_plan_t plan, const tre_join_result *jr, const void *
                         int32_t *w_keys, int64_t w_cap, void *w_tiles, int32_t *pairs_out, int64_t pair_cap,
                         void *stream, tre_timing *timing);
 
-/* Wait for the events of a deferred tre_contract timing and fill its fields. */
+/* Wait for the events of a deferred tre_contract / tre_execute3 timing and
+ * fill contract_ms (and total_ms). */
 tre_status tre_timing_read(tre_timing *timing);
 
 /* tre_execute -- tre_join followed by tre_contract (w_tiles of the plan's W
@@ -364,7 +368,8 @@ tre_status tre_repartition(const char *labels, const char *upper_in, const char 
  *   n_w, n_triples: host; written also with TRE_E_CAPACITY.
  *   ws, ws_bytes: device workspace, 256-byte aligned, at least
  *                  tre_execute3_workspace_bytes(...) (0 on bad arguments).
- *   timing  : optional (deferred mode as for tre_contract); join_ms covers
+ *   timing  : optional (deferred mode as for tre_contract: the fused
+ *             contraction kernel only); join_ms covers
  *             validation, the triple join and the output keys, units_ms is
  *             empty (each workgroup finds its range of triples itself),
  *             contract_ms the fused contraction kernel, reduce_ms the sum of

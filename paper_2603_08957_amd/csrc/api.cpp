@@ -134,10 +134,21 @@ int64_t pair_bound(const Plan& p, int64_t n_u, int64_t n_v) {
 
 }  // namespace
 
-extern "C" {
+namespace {
 
-tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const int32_t* v_keys, int64_t n_v,
-                    void* ws, size_t ws_bytes, void* stream, tre_join_result* out, tre_timing* timing) {
+// What the join leaves for its read-back.
+struct JoinState {
+    int64_t max_pairs = 0;
+    int64_t cap = 0;      // pairs the GROUP BY grids are sized for
+    bool counts_known = false;  // pair and key counts known on the host (no read-back needed for them)
+    bool small = false;
+    int32_t path = 0;     // tre_timing.join_path
+};
+
+// tre_join up to its read-back: argument checks, workspace layout and every
+// join launch.  `out` gets the sizes and the internal fields.
+tre_status join_enqueue(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const int32_t* v_keys, int64_t n_v,
+                        void* ws, size_t ws_bytes, hipStream_t s, tre_join_result* out, JoinState* st) {
     if (!plan || !out || n_u < 0 || n_v < 0 || !ws) {
         set_error("tre_join: null plan/out/workspace or negative size");
         return TRE_E_ARG;
@@ -167,11 +178,14 @@ tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const i
         set_error("tre_join: workspace smaller than tre_workspace_bytes(plan, n_u, n_v, 0)");
         return TRE_E_WORKSPACE;
     }
+    st->max_pairs = max_pairs;
+    out->internal[0] = kMagic;
+    out->internal[1] = reinterpret_cast<uint64_t>(plan);
+    out->internal[2] = reinterpret_cast<uint64_t>(ws);
+    out->internal[3] = uint64_t(ws_bytes);
+    out->internal[4] = uint64_t(max_pairs);
     const Layout L = make_layout(p, n_u, n_v, max_pairs);
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     char* w = reinterpret_cast<char*>(ws);
-    PhaseTimer tm(timing != nullptr);
-    tm.mark(s);
     hipError_t e = launch_fill_zero(w + L.hdr, sizeof(WsHeader), s);
     if (e != hipSuccess) return dev_fail(e, "header");
     WsHeader* hdr = reinterpret_cast<WsHeader*>(w + L.hdr);
@@ -181,59 +195,36 @@ tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const i
         if ((e = launch_validate(v_keys, n_v, p.nk[1], p.radix[1], &hdr->err_v, s)) != hipSuccess)
             return dev_fail(e, "validate V");
     }
-    WsHeader h{};
     if (n_u > 0 && n_v == 1 && keyed_by_u(p)) {
-        // one pair and one group per U tuple: nothing to count, and with key
-        // validation off nothing to wait for
+        // one pair and one group per U tuple: nothing to count
         if (n_u > max_pairs) {
             out->n_pairs = n_u;
             set_error("tre_join: workspace too small for the matched pairs (see n_pairs)");
             return TRE_E_WORKSPACE;
         }
         if ((e = launch_keyed_by_u(p, L, w, u_keys, s)) != hipSuccess) return dev_fail(e, "join");
-        if (p.opt.validate_keys) {
-            if ((e = hipMemcpyAsync(&h, hdr, sizeof(h), hipMemcpyDeviceToHost, s)) != hipSuccess)
-                return dev_fail(e, "key check read-back");
-            if ((e = hipStreamSynchronize(s)) != hipSuccess) return dev_fail(e, "join sync");
-            tre_status ks = key_error(h.err_u);
-            if (ks == TRE_OK) ks = key_error(h.err_v);
-            if (ks != TRE_OK) {
-                set_error(std::string("tre_join: invalid keys in ") + (key_error(h.err_u) != TRE_OK ? "U" : "V"));
-                return ks;
-            }
-        }
-        tm.mark(s);
+        st->cap = n_u;
+        st->counts_known = true;
+        st->path = 4;
         out->n_pairs = n_u;
         out->n_w = n_u;
-        out->internal[0] = kMagic;
-        out->internal[1] = reinterpret_cast<uint64_t>(plan);
-        out->internal[2] = reinterpret_cast<uint64_t>(ws);
-        out->internal[3] = uint64_t(ws_bytes);
-        out->internal[4] = uint64_t(max_pairs);
-        if (timing) {
-            const int32_t deferred = timing->deferred;
-            std::memset(timing, 0, sizeof(*timing));
-            timing->deferred = deferred;
-            timing->join_ms = tm.between(0, 1);
-            timing->total_ms = timing->join_ms;
-            timing->join_path = 4;
-        }
         return TRE_OK;
     }
     // the join counts the pairs into the header; the GROUP BY stage reads
     // that count on the device (its grids are sized for the workspace's
     // capacity), so one read-back at the end returns the key checks, the
     // pair count and the key count together
-    if (n_u > 0 && n_v > 0 && (v_dense(p, n_u) || u_dense(p, n_v)) &&
-        (v_dense(p, n_u) ? n_v : n_u) > max_pairs) {
+    const bool vd = n_u > 0 && n_v > 0 && v_dense(p, n_u), ud = n_u > 0 && n_v > 0 && u_dense(p, n_v);
+    if ((vd || ud) && (vd ? n_v : n_u) > max_pairs) {
         // one pair per tuple of the driving relation, known without the device
-        out->n_pairs = v_dense(p, n_u) ? n_v : n_u;
+        out->n_pairs = vd ? n_v : n_u;
         set_error("tre_join: workspace too small for the matched pairs (see n_pairs)");
         return TRE_E_WORKSPACE;
     }
     const int64_t cap = std::min(max_pairs, pair_bound(p, n_u, n_v));
-    const bool small = n_u > 0 && n_v > 0 && small_join_ok(p, n_u, n_v, cap);
-    if (small) {
+    st->cap = (n_u > 0 && n_v > 0) ? std::max<int64_t>(cap, 0) : 0;
+    st->small = n_u > 0 && n_v > 0 && small_join_ok(p, n_u, n_v, cap);
+    if (st->small) {
         if ((e = launch_join_small(p, L, w, u_keys, v_keys, cap, s)) != hipSuccess) return dev_fail(e, "join");
     } else if (n_u > 0 && n_v > 0 && max_pairs > 0) {
         if ((e = launch_join(p, L, w, u_keys, v_keys, s, 0)) != hipSuccess) return dev_fail(e, "join");
@@ -242,7 +233,24 @@ tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const i
         // no room for any pair: count only, to report the size needed
         if ((e = launch_join(p, L, w, u_keys, v_keys, s, 0)) != hipSuccess) return dev_fail(e, "join");
     }
-    if ((e = hipMemcpyAsync(&h, hdr, sizeof(h), hipMemcpyDeviceToHost, s)) != hipSuccess)
+    st->path = st->small                               ? 5
+               : vd                                     ? 3
+               : ud                                     ? 6
+               : (p.v_outer && p.nk[0] == p.n_join)     ? 2
+               : p.v_outer                              ? 1
+                                                        : 0;
+    return TRE_OK;
+}
+
+// The join's read-back: key checks and, unless known on the host, the pair
+// and key counts.  With key checks off and counts known, nothing to wait for.
+tre_status join_finish(const Plan& p, const JoinState& st, tre_join_result* out, hipStream_t s) {
+    if (st.counts_known && !p.opt.validate_keys) return TRE_OK;
+    const Layout L = make_layout(p, out->n_u, out->n_v, st.max_pairs);
+    const char* w = reinterpret_cast<const char*>(out->internal[2]);
+    WsHeader h{};
+    hipError_t e;
+    if ((e = hipMemcpyAsync(&h, w + L.hdr, sizeof(h), hipMemcpyDeviceToHost, s)) != hipSuccess)
         return dev_fail(e, "count read-back");
     if ((e = hipStreamSynchronize(s)) != hipSuccess) return dev_fail(e, "join sync");
     tre_status ks = key_error(h.err_u);
@@ -251,9 +259,10 @@ tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const i
         set_error(std::string("tre_join: invalid keys in ") + (key_error(h.err_u) != TRE_OK ? "U" : "V"));
         return ks;
     }
-    const int64_t n_pairs = (n_u > 0 && n_v > 0) ? h.n_pairs : 0;
+    if (st.counts_known) return TRE_OK;
+    const int64_t n_pairs = (out->n_u > 0 && out->n_v > 0) ? h.n_pairs : 0;
     out->n_pairs = n_pairs;
-    if (n_pairs > max_pairs) {
+    if (n_pairs > st.max_pairs) {
         set_error("tre_join: workspace too small for the matched pairs (see n_pairs)");
         return TRE_E_WORKSPACE;
     }
@@ -261,51 +270,27 @@ tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const i
         set_error("tre_join: more than 2^31 - 1 pairs");
         return TRE_E_SHAPE;
     }
-    const int64_t n_w = n_pairs > 0 ? h.n_w : 0;
-    tm.mark(s);
-    out->n_w = n_w;
-    out->internal[0] = kMagic;
-    out->internal[1] = reinterpret_cast<uint64_t>(plan);
-    out->internal[2] = reinterpret_cast<uint64_t>(ws);
-    out->internal[3] = uint64_t(ws_bytes);
-    out->internal[4] = uint64_t(max_pairs);
-    if (timing) {
-        const int32_t deferred = timing->deferred;
-        std::memset(timing, 0, sizeof(*timing));
-        timing->deferred = deferred;
-        timing->join_ms = tm.between(0, 1);
-        timing->total_ms = timing->join_ms;
-        timing->join_path = small ? 5
-                            : v_dense(p, n_u)                          ? 3
-                            : u_dense(p, n_v)                          ? 6
-                            : (p.v_outer && p.nk[0] == p.n_join)       ? 2
-                            : p.v_outer                                ? 1
-                                                                       : 0;
-    }
+    out->n_w = n_pairs > 0 ? h.n_w : 0;
     return TRE_OK;
 }
 
-tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* u_tiles, const void* v_tiles,
-                        int32_t* w_keys, int64_t w_cap, void* w_out, int32_t* pairs_out, int64_t pair_cap,
-                        void* stream, tre_timing* timing) {
+void join_timing(tre_timing* timing, int32_t path) {
+    if (!timing) return;
+    const int32_t deferred = timing->deferred;
+    std::memset(timing, 0, sizeof(*timing));
+    timing->deferred = deferred;
+    timing->join_path = path;
+}
+
+// tre_contract's launches, for the join's counts n_pairs and n_w.
+tre_status contract_enqueue(tre_plan_t plan, const tre_join_result* jr, int64_t n_pairs, int64_t n_w,
+                            const void* u_tiles, const void* v_tiles, int32_t* w_keys, void* w_out,
+                            int32_t* pairs_out, hipStream_t s, tre_timing* timing) {
     // W's element type is the plan's (fp32, or bf16 bits with w_bf16); the
     // kernels take the array as float* and store 16-bit elements through it
     // when the plan says bf16
     float* w_tiles = static_cast<float*>(w_out);
-    if (!plan || !jr) {
-        set_error("tre_contract: null plan or join result");
-        return TRE_E_ARG;
-    }
-    if (jr->internal[0] != kMagic || jr->internal[1] != reinterpret_cast<uint64_t>(plan)) {
-        set_error("tre_contract: join result was not produced by tre_join with this plan");
-        return TRE_E_STATE;
-    }
     const Plan& p = plan->p;
-    const int64_t n_pairs = jr->n_pairs, n_w = jr->n_w;
-    if (w_cap < n_w || (pairs_out && pair_cap < n_pairs)) {
-        set_error("tre_contract: output capacity below n_w / n_pairs");
-        return TRE_E_CAPACITY;
-    }
     if (n_pairs == 0) return TRE_OK;
     if (!u_tiles || !v_tiles || !w_tiles || (p.nk[2] > 0 && !w_keys)) {
         set_error("tre_contract: null tile or key buffer");
@@ -318,18 +303,29 @@ tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* 
     }
     char* w = reinterpret_cast<char*>(jr->internal[2]);
     const Layout L = make_layout(p, jr->n_u, jr->n_v, int64_t(jr->internal[4]));
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    // deferred timing: only the contraction kernel, by its own start / end
+    // events (no marker packets); otherwise marks around every phase
     const bool deferred = timing && timing->deferred;
-    PhaseTimer tm(timing != nullptr);
+    PhaseTimer tm(timing != nullptr && !deferred);
+    KernelEvents ke;
+    if (deferred) {
+        ke.start = event_acquire();
+        ke.stop = event_acquire();
+    }
     tm.mark(s);
     const int64_t slots = (p.kclass == KC_GEMM && p.fast) ? gemm_paced_slots(p) : 0;
     const int32_t pace = choose_pacing(p, jr->n_u, n_pairs, n_w, slots);
     const int32_t R = pace ? 0 : choose_u_ranges(p, L, jr->n_u, n_pairs, n_w);
     const int64_t p_unit = (R > 1 || pace) ? n_pairs : choose_unit(p, L, n_pairs, n_w);
     hipError_t e;
-    if ((e = launch_tables(p, reinterpret_cast<int32_t*>(w + L.tables), s)) != hipSuccess) return dev_fail(e, "tables");
-    if (R > 1) e = launch_range_units(p, L, w, n_w, jr->n_u, R, s);
-    else e = launch_units(p, L, w, n_pairs, n_w, p_unit, !pace, s);
+    // (launch_units writes the tile offset tables itself)
+    if (R > 1) {
+        if ((e = launch_tables(p, reinterpret_cast<int32_t*>(w + L.tables), s)) != hipSuccess)
+            return dev_fail(e, "tables");
+        e = launch_range_units(p, L, w, n_w, jr->n_u, R, s);
+    } else {
+        e = launch_units(p, L, w, n_pairs, n_w, p_unit, !pace, s);
+    }
     if (e != hipSuccess) return dev_fail(e, "units");
     tm.mark(s);
     const int64_t unit_bound = R > 1 ? int64_t(R) * n_w : n_w + n_pairs / p_unit + 1;
@@ -339,10 +335,13 @@ tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* 
         const int64_t rounds = (n_w + n_wg - 1) / n_wg;
         if ((e = launch_fill_zero(w + L.pace, sizeof(int32_t) * size_t(rounds * 8 * pace), s)) != hipSuccess)
             return dev_fail(e, "pace");
+        if (ke.start && ke.stop) t_kernel_events = &ke;
         e = launch_gemm_paced(p, L, w, u_tiles, v_tiles, w_tiles, n_pairs, n_wg, pace, s);
     } else {
+        if (ke.start && ke.stop) t_kernel_events = &ke;
         e = launch_contract(p, L, w, u_tiles, v_tiles, w_tiles, n_pairs, n_w, unit_bound, s);
     }
+    t_kernel_events = nullptr;
     if (e != hipSuccess) return dev_fail(e, "contract");
     tm.mark(s);
     if (R > 1 || p_unit < n_pairs) {
@@ -354,10 +353,13 @@ tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* 
     tm.mark(s);
     if (timing) {
         timing->contract_path = pace ? 3 : R > 1 ? 4 : (p.kclass == KC_VEC ? 1 : p.fast ? 2 : 0);
-        if (deferred && tm.on) {
-            for (int i = 0; i < 4; i++) timing->events[i] = reinterpret_cast<void*>(tm.ev[i]);
-            timing->pending = 1;
-            tm.keep = true;
+        if (deferred) {
+            if (ke.launched) {
+                timing->events[0] = reinterpret_cast<void*>(ke.start);
+                timing->events[1] = reinterpret_cast<void*>(ke.stop);
+                timing->pending = 1;
+                ke.keep = true;
+            }
         } else {
             timing->units_ms = tm.between(0, 1);
             timing->contract_ms = tm.between(1, 2);
@@ -372,6 +374,49 @@ tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* 
         }
     }
     return TRE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+tre_status tre_join(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const int32_t* v_keys, int64_t n_v,
+                    void* ws, size_t ws_bytes, void* stream, tre_join_result* out, tre_timing* timing) {
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    PhaseTimer tm(timing != nullptr && !timing->deferred);  // (deferred timing covers the contraction only)
+    tm.mark(s);
+    JoinState st;
+    tre_status r = join_enqueue(plan, u_keys, n_u, v_keys, n_v, ws, ws_bytes, s, out, &st);
+    if (r != TRE_OK) return r;
+    // the end mark goes before the read-back, so reading the join time after
+    // the wait needs no further wait
+    tm.mark(s);
+    if ((r = join_finish(plan->p, st, out, s)) != TRE_OK) return r;
+    join_timing(timing, st.path);
+    if (timing) {
+        timing->join_ms = tm.between(0, 1);
+        timing->total_ms = timing->join_ms;
+    }
+    return TRE_OK;
+}
+
+tre_status tre_contract(tre_plan_t plan, const tre_join_result* jr, const void* u_tiles, const void* v_tiles,
+                        int32_t* w_keys, int64_t w_cap, void* w_out, int32_t* pairs_out, int64_t pair_cap,
+                        void* stream, tre_timing* timing) {
+    if (!plan || !jr) {
+        set_error("tre_contract: null plan or join result");
+        return TRE_E_ARG;
+    }
+    if (jr->internal[0] != kMagic || jr->internal[1] != reinterpret_cast<uint64_t>(plan)) {
+        set_error("tre_contract: join result was not produced by tre_join with this plan");
+        return TRE_E_STATE;
+    }
+    if (w_cap < jr->n_w || (pairs_out && pair_cap < jr->n_pairs)) {
+        set_error("tre_contract: output capacity below n_w / n_pairs");
+        return TRE_E_CAPACITY;
+    }
+    return contract_enqueue(plan, jr, jr->n_pairs, jr->n_w, u_tiles, v_tiles, w_keys, w_out, pairs_out,
+                            reinterpret_cast<hipStream_t>(stream), timing);
 }
 
 tre_status tre_join_keys(tre_plan_t plan, const tre_join_result* jr, int32_t* w_keys, int64_t w_cap, void* stream) {
@@ -403,12 +448,11 @@ tre_status tre_join_keys(tre_plan_t plan, const tre_join_result* jr, int32_t* w_
 tre_status tre_timing_read(tre_timing* t) {
     if (!t) return TRE_E_ARG;
     if (!t->pending) return TRE_OK;
-    t->units_ms = event_elapsed(t->events[0], t->events[1]);
-    t->contract_ms = event_elapsed(t->events[1], t->events[2]);
-    t->reduce_ms = event_elapsed(t->events[2], t->events[3]);
-    t->total_ms += event_elapsed(t->events[0], t->events[3]);
+    // the contraction kernel's start and end
+    t->contract_ms = event_elapsed(t->events[0], t->events[1]);
+    t->total_ms += t->contract_ms;
     for (auto& e : t->events) {
-        if (e) (void)hipEventDestroy(reinterpret_cast<hipEvent_t>(e));
+        event_release(reinterpret_cast<hipEvent_t>(e));
         e = nullptr;
     }
     t->pending = 0;
@@ -419,7 +463,7 @@ tre_status tre_execute(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, cons
                        const int32_t* v_keys, int64_t n_v, const void* v_tiles, int32_t* w_keys, void* w_tiles,
                        int64_t w_cap, int64_t* n_w, int32_t* pairs_out, int64_t pair_cap, int64_t* n_pairs,
                        void* ws, size_t ws_bytes, void* stream, tre_timing* timing) {
-    tre_join_result jr;
+    tre_join_result jr{};
     tre_status st = tre_join(plan, u_keys, n_u, v_keys, n_v, ws, ws_bytes, stream, &jr, timing);
     if (n_pairs) *n_pairs = jr.n_pairs;
     if (n_w) *n_w = jr.n_w;

@@ -146,9 +146,15 @@ __global__ __launch_bounds__(kOrderBins) void k_order_units(Unit* __restrict__ u
 // unit count (keys longer than the cap cut into equal units), scans of the
 // unit, partial-slot and split counts, the fill, and for the GEMM class the
 // longest-first order (counting sort on the unit length, as k_order_units)
-// -- one launch instead of up to six.
+// -- one launch instead of up to six.  Each thread counts four consecutive
+// keys; the fill then gives each thread whole units (a unit finds its key by
+// binary search of the per-key unit offsets in LDS), so a cut key's units
+// are written by many threads at once.  With `ts` non-null the workgroup also
+// writes the tile offset tables first (small tables only, `tables`
+// non-null), saving their launch.
 constexpr int kUnitsThreads = kOrderBins;
 constexpr int kUnitsPer = kOrderMax / kUnitsThreads;
+constexpr int64_t kUnitsTableMax = 16384;
 
 // part_off[s]: the first partial slot of key s (n_w + 1 entries; k_reduce
 // sums slots part_off[s] .. part_off[s + 1] - 1 of each split key).
@@ -156,19 +162,40 @@ __global__ __launch_bounds__(kUnitsThreads) void k_units_small(const int32_t* __
                                                                 int64_t p_unit, int order, Unit* __restrict__ units,
                                                                 int32_t* __restrict__ split,
                                                                 int32_t* __restrict__ part_off,
-                                                                WsHeader* __restrict__ hdr) {
+                                                                WsHeader* __restrict__ hdr, TableSet ts,
+                                                                int32_t* __restrict__ tables) {
     __shared__ Unit buf[kOrderMax];
     __shared__ int32_t cnt[kOrderBins];
     __shared__ int32_t wsum[kUnitsThreads / 64];
+    __shared__ int32_t key_uo[kOrderMax + 1], key_po[kOrderMax], key_a[kOrderMax + 1];
     const int t = threadIdx.x;
-    int32_t nu[kUnitsPer], su = 0, sp = 0, ss = 0;
+    if (tables) {
+        for (int k = 0; k < T_COUNT; k++) {
+            const Dims& d = ts.d[k];
+            int32_t c = 1;
+            for (int i = 0; i < d.n; i++) c *= d.size[i];
+            for (int32_t x = t; x < c; x += kUnitsThreads) {
+                int32_t rem = x, o = 0;
+                for (int i = d.n - 1; i >= 0; i--) {
+                    o += (rem % d.size[i]) * d.stride[i];
+                    rem /= d.size[i];
+                }
+                tables[ts.off[k] + x] = o;
+            }
+        }
+    }
+    int32_t nu[kUnitsPer], a0[kUnitsPer], su = 0, sp = 0, ss = 0;
 #pragma unroll
     for (int j = 0; j < kUnitsPer; j++) {
         const int64_t s = int64_t(t) * kUnitsPer + j;
         nu[j] = 0;
+        a0[j] = 0;
         if (s < n_w) {
-            const int64_t len = seg_start[s + 1] - seg_start[s];
-            nu[j] = int32_t((len + p_unit - 1) / p_unit);
+            a0[j] = seg_start[s];
+            const int32_t len = seg_start[s + 1] - a0[j];
+            nu[j] = len <= 0     ? 0
+                    : p_unit >= len ? 1
+                                    : int32_t((uint32_t(len) + uint32_t(p_unit) - 1) / uint32_t(p_unit));
         }
         su += nu[j];
         sp += nu[j] > 1 ? nu[j] : 0;
@@ -178,23 +205,14 @@ __global__ __launch_bounds__(kUnitsThreads) void k_units_small(const int32_t* __
     int32_t uo = block_scan_excl<kUnitsThreads>(su, wsum, &n_units);
     int32_t po = block_scan_excl<kUnitsThreads>(sp, wsum, &n_parts);
     int32_t so = block_scan_excl<kUnitsThreads>(ss, wsum, &n_split);
-    const bool in_lds = order && n_units >= 2 && n_units <= kOrderMax;
 #pragma unroll
     for (int j = 0; j < kUnitsPer; j++) {
         const int64_t s = int64_t(t) * kUnitsPer + j;
         if (s >= n_w) continue;
         part_off[s] = po;
-        const int32_t a = seg_start[s], b = seg_start[s + 1];
-        const int64_t len = int64_t(b) - a;
-        for (int32_t q = 0; q < nu[j]; q++) {
-            Unit u;
-            u.seg = int32_t(s);
-            u.p0 = a + int32_t(len * q / nu[j]);
-            u.p1 = a + int32_t(len * (q + 1) / nu[j]);
-            u.slot = nu[j] > 1 ? po + q : -1;
-            if (in_lds) buf[uo + q] = u;
-            else units[uo + q] = u;
-        }
+        key_uo[s] = uo;
+        key_po[s] = po;
+        key_a[s] = a0[j];
         if (nu[j] > 1) {
             split[so++] = int32_t(s);
             po += nu[j];
@@ -202,10 +220,42 @@ __global__ __launch_bounds__(kUnitsThreads) void k_units_small(const int32_t* __
         uo += nu[j];
     }
     if (t == 0) {
+        key_uo[n_w] = n_units;
+        key_a[n_w] = seg_start[n_w];
         part_off[n_w] = n_parts;
         hdr->n_units = n_units;
         hdr->n_parts = n_parts;
         hdr->n_split = n_split;
+    }
+    __syncthreads();
+    const bool in_lds = order && n_units >= 2 && n_units <= kOrderMax;
+    for (int32_t i = t; i < n_units; i += kUnitsThreads) {
+        // the key of unit i: the last s with key_uo[s] <= i (keys without
+        // pairs own no unit and are skipped by taking the last such s)
+        int32_t lo = 0, hi = int32_t(n_w) - 1;
+        while (lo < hi) {
+            const int32_t m = (lo + hi + 1) >> 1;
+            if (key_uo[m] <= i) lo = m; else hi = m - 1;
+        }
+        const int32_t k = key_uo[lo + 1] - key_uo[lo];
+        const int32_t q = i - key_uo[lo];
+        const int32_t a = key_a[lo];
+        const uint32_t len = uint32_t(key_a[lo + 1] - a);
+        Unit u;
+        u.seg = lo;
+        if (k == 1) {
+            u.p0 = a;
+            u.p1 = a + int32_t(len);
+            u.slot = -1;
+        } else {
+            // a cut key: k units of equal length (within one pair)
+            const uint64_t x0 = uint64_t(len) * uint32_t(q), x1 = x0 + len;
+            u.p0 = a + int32_t(x1 >> 32 ? x0 / uint32_t(k) : uint32_t(x0) / uint32_t(k));
+            u.p1 = a + int32_t(x1 >> 32 ? x1 / uint32_t(k) : uint32_t(x1) / uint32_t(k));
+            u.slot = key_po[lo] + q;
+        }
+        if (in_lds) buf[i] = u;
+        else units[i] = u;
     }
     if (!in_lds) return;
     // longest first (unit lengths capped at kOrderBins - 1; order within a
@@ -591,31 +641,13 @@ __global__ __launch_bounds__(kThreads) void k_vec(VecArgs a) {
     };
     int p = un.p0;
     if constexpr (PU > 1) {
-        // groups of PU pairs; the pair indices of the next group are loaded
-        // while the current group's tiles are read, so the dependent index ->
-        // tile loads overlap across groups
-        int32_t iu[PU], iv[PU];
-        if (p + PU <= un.p1) {
-#pragma unroll
-            for (int j = 0; j < PU; j++) {
-                iu[j] = a.pu[p + j];
-                iv[j] = a.pv[p + j];
-            }
-        }
         for (; p + PU <= un.p1; p += PU) {
             const T* ub[PU];
             const T* vb[PU];
 #pragma unroll
             for (int j = 0; j < PU; j++) {
-                ub[j] = U + int64_t(iu[j]) * a.u_elems + eu;
-                vb[j] = V + int64_t(iv[j]) * a.v_elems + ev;
-            }
-            if (p + 2 * PU <= un.p1) {
-#pragma unroll
-                for (int j = 0; j < PU; j++) {
-                    iu[j] = a.pu[p + PU + j];
-                    iv[j] = a.pv[p + PU + j];
-                }
+                ub[j] = U + int64_t(a.pu[p + j]) * a.u_elems + eu;
+                vb[j] = V + int64_t(a.pv[p + j]) * a.v_elems + ev;
             }
             for (int k = 0; k < a.K; k++)
 #pragma unroll
@@ -659,14 +691,11 @@ __global__ __launch_bounds__(kThreads) void k_vec(VecArgs a) {
 template <typename T, int EPT>
 hipError_t vec_dispatch(const Plan& p, const VecArgs& a, dim3 grid, hipStream_t s) {
     const bool pu4 = p.nK <= 2;
-    if (p.vec_vbcast) {
-        if (pu4) k_vec<T, EPT, true, 8><<<grid, kThreads, 0, s>>>(a);
-        else k_vec<T, EPT, true, 1><<<grid, kThreads, 0, s>>>(a);
-    } else {
-        if (pu4) k_vec<T, EPT, false, 4><<<grid, kThreads, 0, s>>>(a);
-        else k_vec<T, EPT, false, 1><<<grid, kThreads, 0, s>>>(a);
-    }
-    return hipGetLastError();
+    const dim3 block{unsigned(kThreads)};
+    if (p.vec_vbcast) return pu4 ? launch_k(k_vec<T, EPT, true, 4>, grid, block, 0, s, a)
+                                 : launch_k(k_vec<T, EPT, true, 1>, grid, block, 0, s, a);
+    return pu4 ? launch_k(k_vec<T, EPT, false, 4>, grid, block, 0, s, a)
+               : launch_k(k_vec<T, EPT, false, 1>, grid, block, 0, s, a);
 }
 
 // ---------------------------------------------------------------- reduce
@@ -732,11 +761,11 @@ hipError_t gemm_dispatch(const Plan& p, const GemmArgs& g, dim3 grid, hipStream_
     if (!PF) grid.x = std::min<unsigned>(grid.x, std::max<unsigned>(1, kGemmGrid / grid.y));
     const size_t tab = sizeof(int32_t) * size_t(kBM + kBN + 2 * int64_t(g.K));
     if (tab > 96 * 1024) return hipErrorInvalidConfiguration;
-    if (p.a_kfast && p.b_kfast) k_gemm<T, true, true, PF><<<grid, kThreads, tab, s>>>(g);
-    else if (p.a_kfast) k_gemm<T, true, false, PF><<<grid, kThreads, tab, s>>>(g);
-    else if (p.b_kfast) k_gemm<T, false, true, PF><<<grid, kThreads, tab, s>>>(g);
-    else k_gemm<T, false, false, PF><<<grid, kThreads, tab, s>>>(g);
-    return hipGetLastError();
+    const dim3 block{unsigned(kThreads)};
+    if (p.a_kfast && p.b_kfast) return launch_k(k_gemm<T, true, true, PF>, grid, block, tab, s, g);
+    if (p.a_kfast) return launch_k(k_gemm<T, true, false, PF>, grid, block, tab, s, g);
+    if (p.b_kfast) return launch_k(k_gemm<T, false, true, PF>, grid, block, tab, s, g);
+    return launch_k(k_gemm<T, false, false, PF>, grid, block, tab, s, g);
 }
 
 // Prefetch pays when units run many K chunks (pairs per unit x chunks per pair).
@@ -750,14 +779,26 @@ hipError_t gemm_dispatch(const Plan& p, const GemmArgs& g, dim3 grid, int64_t n_
 
 }  // namespace
 
-hipError_t launch_tables(const Plan& p, int32_t* tables, hipStream_t s) {
+namespace {
+
+TableSet table_set(const Plan& p, int64_t* largest, int64_t* total) {
     TableSet ts{};
-    int64_t mx = 1;
+    *largest = 1;
+    *total = 0;
     for (int t = 0; t < T_COUNT; t++) {
         ts.d[t] = p.dims[t];
         ts.off[t] = p.table_off[t];
-        mx = std::max<int64_t>(mx, p.dims[t].count());
+        *largest = std::max<int64_t>(*largest, p.dims[t].count());
+        *total += p.dims[t].count();
     }
+    return ts;
+}
+
+}  // namespace
+
+hipError_t launch_tables(const Plan& p, int32_t* tables, hipStream_t s) {
+    int64_t mx, total;
+    const TableSet ts = table_set(p, &mx, &total);
     const unsigned gx = unsigned(std::min<int64_t>((mx + kThreads - 1) / kThreads, 1024));
     k_tables<<<dim3(gx, T_COUNT), kThreads, 0, s>>>(ts, tables);
     return hipGetLastError();
@@ -792,13 +833,21 @@ hipError_t launch_units(const Plan& p, const Layout& L, char* ws, int64_t n_pair
     int32_t* nsplit = reinterpret_cast<int32_t*>(ws + L.flags);
     int32_t* tmp = reinterpret_cast<int32_t*>(ws + L.scan_tmp);
     hipError_t e;
+    int32_t* tables = reinterpret_cast<int32_t*>(ws + L.tables);
     if (n_w <= kOrderMax) {
+        // the tables too, when small (one launch for both)
+        int64_t mx, total;
+        const TableSet ts = table_set(p, &mx, &total);
+        const bool with_tables = total <= kUnitsTableMax;
+        if (!with_tables && (e = launch_tables(p, tables, s)) != hipSuccess) return e;
         k_units_small<<<1, kUnitsThreads, 0, s>>>(seg_start, n_w, std::max<int64_t>(p_unit, 1),
                                                    longest_first && p.kclass == KC_GEMM ? 1 : 0,
                                                    reinterpret_cast<Unit*>(ws + L.unit_desc),
-                                                   reinterpret_cast<int32_t*>(ws + L.split_list), nparts, hdr);
+                                                   reinterpret_cast<int32_t*>(ws + L.split_list), nparts, hdr, ts,
+                                                   with_tables ? tables : nullptr);
         return hipGetLastError();
     }
+    if ((e = launch_tables(p, tables, s)) != hipSuccess) return e;
     if (p_unit >= n_pairs) {  // no key can be longer than the cap
         k_key_units<<<blocks_for(n_w + 1), kThreads, 0, s>>>(seg_start, n_w, reinterpret_cast<Unit*>(ws + L.unit_desc),
                                                              hdr);

@@ -626,25 +626,26 @@ tre_status dev_fail(hipError_t e, const char* where) {
 }
 
 // Phase times from the five marks (join | units | contraction | reduction).
-void finish_timing(tre_timing* timing, PhaseTimer& tm, bool deferred, bool dense) {
+void finish_timing(tre_timing* timing, PhaseTimer& tm, bool deferred, bool dense, KernelEvents& ke) {
     if (!timing) return;
     std::memset(timing, 0, sizeof(*timing));
     timing->deferred = deferred ? 1 : 0;
     timing->join_path = dense ? 6 : 0;  // U drives the join; dense: partners indexed by key value
-    timing->join_ms = tm.between(0, 1);
-    timing->total_ms = timing->join_ms;
-    if (deferred && tm.on) {
-        // the events after the join go to the caller; the first is ours
-        for (int i = 0; i < 4; i++) timing->events[i] = reinterpret_cast<void*>(tm.ev[i + 1]);
-        timing->pending = 1;
-        tm.keep = true;
-        (void)hipEventDestroy(tm.ev[0]);
-    } else {
-        timing->units_ms = tm.between(1, 2);
-        timing->contract_ms = tm.between(2, 3);
-        timing->reduce_ms = tm.between(3, 4);
-        timing->total_ms += tm.between(1, 4);
+    if (deferred) {
+        // the contraction kernel's own start and end, read later
+        if (ke.launched) {
+            timing->events[0] = reinterpret_cast<void*>(ke.start);
+            timing->events[1] = reinterpret_cast<void*>(ke.stop);
+            timing->pending = 1;
+            ke.keep = true;
+        }
+        return;
     }
+    timing->join_ms = tm.between(0, 1);
+    timing->units_ms = tm.between(1, 2);
+    timing->contract_ms = tm.between(2, 3);
+    timing->reduce_ms = tm.between(3, 4);
+    timing->total_ms = timing->join_ms + tm.between(1, 4);
 }
 
 tre_status fail(tre_status st, const char* msg) {
@@ -890,8 +891,16 @@ tre_status tre_execute3(const char* einsum, const char* upper, const int64_t* ex
     const int32_t* p_keys = d.v_on_p ? v_keys : x_keys;
     const int32_t* q_keys = d.v_on_p ? x_keys : v_keys;
     const int64_t n_p = d.v_on_p ? n_v : n_x, n_q = d.v_on_p ? n_x : n_v;
+    // deferred timing: only the contraction kernel, by its own start / end
+    // events; otherwise marks around every phase
     const bool deferred = timing && timing->deferred;
-    PhaseTimer tm(timing != nullptr);
+    PhaseTimer tm(timing != nullptr && !deferred);
+    KernelEvents ke;
+    if (deferred) {
+        ke.start = event_acquire();
+        ke.stop = event_acquire();
+    }
+    KernelEvents* kep = (ke.start && ke.stop) ? &ke : nullptr;
     hipError_t e;
     tm.mark(s);
     if ((e = launch_fill_zero(hdr, sizeof(F3Header), s)) != hipSuccess) return dev_fail(e, "header");
@@ -964,11 +973,11 @@ tre_status tre_execute3(const char* einsum, const char* upper, const int64_t* ex
         const bool v4 = d.R % 4 == 0 && ((reinterpret_cast<uintptr_t>(P) | reinterpret_cast<uintptr_t>(Q)) & 15) == 0;
         const int64_t waves = (nt + kMaskedBatch - 1) / kMaskedBatch;
         const dim3 grid{unsigned((waves + kThreads / 64 - 1) / (kThreads / 64))};
-        if (v4) k3_masked<true><<<grid, kThreads, 0, s>>>(static_cast<const float*>(u_tiles), P, Q, tu, tp, tq, nt,
-                                                         d.te_u, d.R, w_tiles);
-        else k3_masked<false><<<grid, kThreads, 0, s>>>(static_cast<const float*>(u_tiles), P, Q, tu, tp, tq, nt,
-                                                       d.te_u, d.R, w_tiles);
-        if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "masked contract");
+        t_kernel_events = kep;
+        e = launch_k(v4 ? k3_masked<true> : k3_masked<false>, grid, dim3(kThreads), 0, s,
+                     static_cast<const float*>(u_tiles), P, Q, tu, tp, tq, nt, d.te_u, d.R, w_tiles);
+        t_kernel_events = nullptr;
+        if (e != hipSuccess) return dev_fail(e, "masked contract");
         tm.mark(s);
         if (d.rw > 0) {
             k3_copy_keys<<<blocks_for(n_u * d.ru), kThreads, 0, s>>>(u_keys, n_u * d.ru, w_keys);
@@ -980,7 +989,7 @@ tre_status tre_execute3(const char* einsum, const char* upper, const int64_t* ex
             return dev_fail(e, "key check read-back");
         const tre_status ks = key_errors();
         if (ks != TRE_OK) return ks;
-        finish_timing(timing, tm, deferred, dense);
+        finish_timing(timing, tm, deferred, dense, ke);
         return TRE_OK;
     }
     if (nt > 0) {
@@ -1017,6 +1026,9 @@ tre_status tre_execute3(const char* einsum, const char* upper, const int64_t* ex
         return dev_fail(e, "segment scan");
     k3_segments<<<blocks_for(nt + 1), kThreads, 0, s>>>(wkey, nt, seg_of, seg_start, seg_key, hdr);
     if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "segments");
+    // the join's end mark goes before the read-back, so reading the join
+    // time after the wait needs no further wait
+    tm.mark(s);
     if ((e = hipMemcpyAsync(&h, hdr, sizeof(h), hipMemcpyDeviceToHost, s)) != hipSuccess ||
         (e = hipStreamSynchronize(s)) != hipSuccess)
         return dev_fail(e, "key count read-back");
@@ -1026,7 +1038,6 @@ tre_status tre_execute3(const char* einsum, const char* upper, const int64_t* ex
     }
     const int64_t nw = h.n_w;
     *n_w = nw;
-    tm.mark(s);
     if (nw > w_cap) return fail(TRE_E_CAPACITY, "w_cap below the output key count");
     if (nw > 0 && (!w_tiles || (d.rw > 0 && !w_keys))) return fail(TRE_E_ARG, "null output buffers");
     tm.mark(s);  // (no separate work-unit phase: ranges are computed in the kernel)
@@ -1039,11 +1050,11 @@ tre_status tre_execute3(const char* einsum, const char* upper, const int64_t* ex
             const bool v4 = d.R % 4 == 0 && ((reinterpret_cast<uintptr_t>(P) | reinterpret_cast<uintptr_t>(Q)) & 15) == 0;
             const int64_t waves = (nt + kMaskedBatch - 1) / kMaskedBatch;
             const dim3 grid{unsigned((waves + kThreads / 64 - 1) / (kThreads / 64))};
-            if (v4) k3_masked<true><<<grid, kThreads, 0, s>>>(static_cast<const float*>(u_tiles), P, Q, tu, tp, tq, nt,
-                                                             d.te_u, d.R, w_tiles);
-            else k3_masked<false><<<grid, kThreads, 0, s>>>(static_cast<const float*>(u_tiles), P, Q, tu, tp, tq, nt,
-                                                           d.te_u, d.R, w_tiles);
-            if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "masked contract");
+            t_kernel_events = kep;
+            e = launch_k(v4 ? k3_masked<true> : k3_masked<false>, grid, dim3(kThreads), 0, s,
+                         static_cast<const float*>(u_tiles), P, Q, tu, tp, tq, nt, d.te_u, d.R, w_tiles);
+            t_kernel_events = nullptr;
+            if (e != hipSuccess) return dev_fail(e, "masked contract");
         }
         tm.mark(s);
         if (nw > 0 && d.rw > 0) {
@@ -1086,11 +1097,14 @@ tre_status tre_execute3(const char* einsum, const char* upper, const int64_t* ex
             g.part = static_cast<float*>(at(L.part));
             g.d = d;
             const dim3 grid{unsigned(n_wg)};
-            if (d.tq == 16) k3_gemm_q<16><<<grid, kThreads, lds, s>>>(g);
-            else if (d.tq == 32) k3_gemm_q<32><<<grid, kThreads, lds, s>>>(g);
-            else if (d.tq == 64) k3_gemm_q<64><<<grid, kThreads, lds, s>>>(g);
-            else k3_gemm<<<grid, kThreads, lds, s>>>(g);
-            if ((e = hipGetLastError()) != hipSuccess) return dev_fail(e, "contract");
+            t_kernel_events = kep;
+            e = launch_k(d.tq == 16   ? k3_gemm_q<16>
+                         : d.tq == 32 ? k3_gemm_q<32>
+                         : d.tq == 64 ? k3_gemm_q<64>
+                                      : k3_gemm,
+                         grid, dim3(kThreads), lds, s, g);
+            t_kernel_events = nullptr;
+            if (e != hipSuccess) return dev_fail(e, "contract");
         }
         tm.mark(s);
         if (nw > 0) {
@@ -1105,7 +1119,7 @@ tre_status tre_execute3(const char* einsum, const char* upper, const int64_t* ex
         }
         tm.mark(s);
     }
-    finish_timing(timing, tm, deferred, dense);
+    finish_timing(timing, tm, deferred, dense, ke);
     return TRE_OK;
 }
 

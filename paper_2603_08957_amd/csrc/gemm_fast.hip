@@ -550,12 +550,15 @@ hipError_t launch_gemm_fast(const Plan& p, const Layout& L, char* ws, const void
     const int64_t blocks = (groups + 7) / 8 * 8 * g.nblocks;
     if (blocks > int64_t(0x7fffffff)) return hipErrorInvalidConfiguration;
     dim3 grid{unsigned(blocks), 1u, 1u};
+    hipError_t e = hipErrorInvalidValue;
 #define TRE_FAST_CASE(X)                                                                                      \
     case X:                                                                                                   \
         if (p.dtype == TRE_BF16)                                                                              \
-            k_gemm_dma<uint16_t, bool(X & 8), bool(X & 4), bool(X & 2), bool(X & 1)><<<grid, kThreads, 0, s>>>(g); \
+            e = launch_k(k_gemm_dma<uint16_t, bool(X & 8), bool(X & 4), bool(X & 2), bool(X & 1)>, grid,        \
+                         dim3(kThreads), 0, s, g);                                                            \
         else                                                                                                  \
-            k_gemm_dma<float, bool(X & 8), bool(X & 4), bool(X & 2), bool(X & 1)><<<grid, kThreads, 0, s>>>(g);    \
+            e = launch_k(k_gemm_dma<float, bool(X & 8), bool(X & 4), bool(X & 2), bool(X & 1)>, grid,           \
+                         dim3(kThreads), 0, s, g);                                                            \
         break;
     switch (fast_variant(p, L, n_pairs)) {
         TRE_FAST_CASE(0) TRE_FAST_CASE(1) TRE_FAST_CASE(2) TRE_FAST_CASE(3)
@@ -564,7 +567,7 @@ hipError_t launch_gemm_fast(const Plan& p, const Layout& L, char* ws, const void
         TRE_FAST_CASE(12) TRE_FAST_CASE(13) TRE_FAST_CASE(14) TRE_FAST_CASE(15)
     }
 #undef TRE_FAST_CASE
-    return hipGetLastError();
+    return e;
 }
 
 int64_t gemm_paced_slots(const Plan& p) {
@@ -585,14 +588,15 @@ hipError_t launch_gemm_paced(const Plan& p, const Layout& L, char* ws, const voi
     // before the one it enters
     constexpr int32_t kAhead = 0, kSlackDiv = 4;
     dim3 grid{unsigned(n_wg), 1u, 1u};
+    hipError_t e = hipErrorInvalidValue;
 #define TRE_PACED_CASE(X)                                                                                      \
     case X:                                                                                                    \
         if (p.dtype == TRE_BF16)                                                                               \
-            k_gemm_paced<uint16_t, bool(X & 8), bool(X & 4), bool(X & 2), bool(X & 1)><<<grid, kThreads, 0, s>>>( \
-                g, pace, int32_t(n_wg), windows, kAhead, kSlackDiv);                                           \
+            e = launch_k(k_gemm_paced<uint16_t, bool(X & 8), bool(X & 4), bool(X & 2), bool(X & 1)>, grid,      \
+                         dim3(kThreads), 0, s, g, pace, int32_t(n_wg), windows, kAhead, kSlackDiv);             \
         else                                                                                                   \
-            k_gemm_paced<float, bool(X & 8), bool(X & 4), bool(X & 2), bool(X & 1)><<<grid, kThreads, 0, s>>>(    \
-                g, pace, int32_t(n_wg), windows, kAhead, kSlackDiv);                                           \
+            e = launch_k(k_gemm_paced<float, bool(X & 8), bool(X & 4), bool(X & 2), bool(X & 1)>, grid,         \
+                         dim3(kThreads), 0, s, g, pace, int32_t(n_wg), windows, kAhead, kSlackDiv);             \
         break;
     switch (fast_variant(p, L, n_pairs)) {
         TRE_PACED_CASE(0) TRE_PACED_CASE(1) TRE_PACED_CASE(2) TRE_PACED_CASE(3)
@@ -601,7 +605,7 @@ hipError_t launch_gemm_paced(const Plan& p, const Layout& L, char* ws, const voi
         TRE_PACED_CASE(12) TRE_PACED_CASE(13) TRE_PACED_CASE(14) TRE_PACED_CASE(15)
     }
 #undef TRE_PACED_CASE
-    return hipGetLastError();
+    return e;
 }
 
 }  // namespace tre

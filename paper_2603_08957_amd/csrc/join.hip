@@ -472,30 +472,55 @@ __global__ __launch_bounds__(kSmallThreads) void k_join_small(
     __shared__ int32_t s_lo[kSmallMax];
     __shared__ uint64_t s_key[kSmallMax];  // W key << kSmallIdxBits | expansion index
     __shared__ int32_t s_pu[kSmallMax], s_pv[kSmallMax];
+    __shared__ uint64_t s_ikey[kSmallMax];  // the inner relation's packed join keys (non-decreasing)
     __shared__ int32_t s_wsum[kSmallThreads / 64];
     const int t = threadIdx.x;
-    // runs: outer tuple o meets inner tuples [s_lo[o], s_lo[o] + c)
+    // join keys packed into one word (the caller checks that they fit): the
+    // inner relation's are a prefix of its sorted key, staged in LDS
+    auto pack_join = [&](const int32_t* row, bool outer) {
+        uint64_t k = 0;
+        for (int i = 0; i < dout.n; i++) k = (k << dout.bits[i]) | uint64_t(uint32_t(row[outer ? dout.pos[i] : i]));
+        return k;
+    };
+    for (int64_t i = t; i < n_i; i += kSmallThreads) s_ikey[i] = pack_join(ikeys + i * ri, false);
+    __syncthreads();
+    // runs: outer tuple o meets inner tuples [s_lo[o], s_lo[o] + c); the
+    // kSmallPer searches of a thread advance in lockstep (branch-free lower
+    // and upper bounds, the same step count for every thread)
     int32_t c[kSmallPer];
+    uint64_t kk[kSmallPer];
+    int32_t lb[kSmallPer], ub[kSmallPer];
+#pragma unroll
+    for (int j = 0; j < kSmallPer; j++) {
+        const int64_t o = int64_t(t) * kSmallPer + j;
+        kk[j] = o < n_o ? pack_join(okeys + o * ro, true) : 0;
+        lb[j] = 0;
+        ub[j] = 0;
+    }
+    if (n_i > 0) {
+        for (int32_t len = int32_t(n_i); len > 1;) {
+            const int32_t half = len >> 1;
+#pragma unroll
+            for (int j = 0; j < kSmallPer; j++) {
+                if (s_ikey[lb[j] + half] < kk[j]) lb[j] += half;
+                if (s_ikey[ub[j] + half] <= kk[j]) ub[j] += half;
+            }
+            len -= half;
+        }
+#pragma unroll
+        for (int j = 0; j < kSmallPer; j++) {
+            lb[j] += s_ikey[lb[j]] < kk[j] ? 1 : 0;
+            ub[j] += s_ikey[ub[j]] <= kk[j] ? 1 : 0;
+        }
+    }
     int32_t csum = 0;
 #pragma unroll
     for (int j = 0; j < kSmallPer; j++) {
         const int64_t o = int64_t(t) * kSmallPer + j;
         c[j] = 0;
         if (o < n_o) {
-            int32_t key[26];
-            for (int i = 0; i < dout.n; i++) key[i] = okeys[o * ro + dout.pos[i]];
-            int64_t a = 0, b = n_i;
-            while (a < b) {
-                const int64_t m = (a + b) >> 1;
-                if (cmp_prefix(ikeys + m * ri, key, dout.n) < 0) a = m + 1; else b = m;
-            }
-            int64_t e = a, f = n_i;  // first inner row past the run
-            while (e < f) {
-                const int64_t m = (e + f) >> 1;
-                if (cmp_prefix(ikeys + m * ri, key, dout.n) <= 0) e = m + 1; else f = m;
-            }
-            s_lo[o] = int32_t(a);
-            c[j] = int32_t(min<int64_t>(e - a, kSmallMax));  // more cannot be listed (and the sums stay small)
+            s_lo[o] = lb[j];
+            c[j] = min(ub[j] - lb[j], kSmallMax);  // more cannot be listed (and the sums stay small)
         }
         csum += c[j];
     }
@@ -640,6 +665,62 @@ __global__ void k_key_compact(const int32_t* __restrict__ first, int64_t nk, con
     if (f != 0) {
         seg_start[seg_of[q]] = f - 1;
         seg_key[seg_of[q]] = uint64_t(q);
+    }
+}
+
+// The three steps above in one workgroup for a key space of at most
+// kKeySmallMax keys: each wavefront owns a contiguous range of keys and reads
+// it 64 keys at a time (all its loads issued at once), counts the present
+// keys with ballots, a scan over the wavefront totals gives each wavefront
+// its first segment, and the segments are written in key order (a lane's
+// position within a batch from the ballot mask below it).
+constexpr int kKeySmallThreads = 1024;
+constexpr int kKeySmallWaves = kKeySmallThreads / 64;
+constexpr int kKeySmallBatches = 32;  // batches of 64 keys per wavefront
+constexpr int64_t kKeySmallMax = int64_t(kKeySmallWaves) * 64 * kKeySmallBatches;
+
+__global__ __launch_bounds__(kKeySmallThreads) void k_key_segments_small(const int32_t* __restrict__ first,
+                                                                           int64_t nk, int64_t cap,
+                                                                           int32_t* __restrict__ seg_start,
+                                                                           uint64_t* __restrict__ seg_key,
+                                                                           WsHeader* hdr) {
+    __shared__ int32_t wtot[kKeySmallWaves];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int32_t per = int32_t((nk + kKeySmallWaves * 64 - 1) / (kKeySmallWaves * 64)) * 64;  // keys per wavefront
+    const int32_t q0 = w * per;
+    const int32_t q1 = min(q0 + per, int32_t(nk));
+    int32_t f[kKeySmallBatches];
+#pragma unroll
+    for (int b = 0; b < kKeySmallBatches; b++) {
+        const int32_t q = q0 + b * 64 + lane;
+        f[b] = q < q1 ? first[q] : 0;
+    }
+    int32_t c = 0;
+#pragma unroll
+    for (int b = 0; b < kKeySmallBatches; b++) c += __popcll(__ballot(f[b] != 0));
+    if (lane == 0) wtot[w] = c;
+    __syncthreads();
+    int32_t base = 0, n_seg = 0;
+#pragma unroll
+    for (int i = 0; i < kKeySmallWaves; i++) {
+        const int32_t x = wtot[i];
+        if (i < w) base += x;
+        n_seg += x;
+    }
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+#pragma unroll
+    for (int b = 0; b < kKeySmallBatches; b++) {
+        const uint64_t m = __ballot(f[b] != 0);
+        if (f[b] != 0) {
+            const int32_t o = base + __popcll(m & below);
+            seg_start[o] = f[b] - 1;
+            seg_key[o] = uint64_t(q0 + b * 64 + lane);
+        }
+        base += __popcll(m);
+    }
+    if (threadIdx.x == 0) {
+        seg_start[n_seg] = int32_t(pair_count(hdr, cap));
+        hdr->n_w = n_seg;
     }
 }
 
@@ -851,6 +932,10 @@ hipError_t group_impl(const Plan& p, const Layout& L, char* ws, const int32_t* u
             k_first_of_key<KT><<<blocks_for(cap), kThreads, 0, s>>>(wk, hdr, cap, key_space, first);
             if ((e = hipGetLastError()) != hipSuccess) return e;
         }
+        if (key_space <= kKeySmallMax) {
+            k_key_segments_small<<<1, kKeySmallThreads, 0, s>>>(first, key_space, cap, seg_start, seg_key, hdr);
+            return hipGetLastError();
+        }
         k_key_flags<<<blocks_for(key_space + 1), kThreads, 0, s>>>(first, key_space, kflags);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if ((e = scan_exclusive_i32(kflags, kflags, key_space + 1, tmp, s)) != hipSuccess) return e;
@@ -875,8 +960,11 @@ bool small_join_ok(const Plan& p, int64_t n_u, int64_t n_v, int64_t cap) {
     if (p.opt.small_join < 0 || p.v_needs_sort || p.group_needs_sort || keyed_by_u(p) || v_dense(p, n_u) ||
         p.w_total_bits > 32)
         return false;
-    const int64_t n_o = p.v_outer ? n_v : n_u;
-    return n_o >= 1 && n_o <= kSmallMax && cap >= 1 && cap <= kSmallMax;
+    // the inner relation's join keys, packed into one word each, are staged in LDS
+    int join_bits = 0;
+    for (int i = 0; i < p.n_join; i++) join_bits += p.join_bits[i];
+    const int64_t n_o = p.v_outer ? n_v : n_u, n_i = p.v_outer ? n_u : n_v;
+    return join_bits <= 64 && n_i <= kSmallMax && n_o >= 1 && n_o <= kSmallMax && cap >= 1 && cap <= kSmallMax;
 }
 
 hipError_t launch_join_small(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,

@@ -5,7 +5,8 @@
 // consecutive items, wavefront-level inclusive scans of the per-thread sums
 // run on 64-wide DPP-friendly shuffles, and wave totals meet in LDS.  Inputs
 // longer than one tile take a reduce -> scan-of-sums -> rescan pass, applied
-// recursively to the block sums.  In-place operation (in == out) is allowed.
+// recursively to the block sums (up to 32768 items: one workgroup, one
+// launch).  In-place operation (in == out) is allowed.
 #include "tre_internal.h"
 
 namespace tre {
@@ -79,12 +80,58 @@ __global__ __launch_bounds__(kThreads) void k_tile_scan(const T* in, T* out, int
     }
 }
 
+// Inputs of a few tiles: one workgroup of 1024 threads walks them in
+// chunks of 16384 items (16 consecutive items per thread), carrying the
+// running total, so the scan is one launch instead of three.
+constexpr int kOneThreads = 1024;
+constexpr int64_t kOneChunk = int64_t(kOneThreads) * kIpt;
+constexpr int64_t kOneMax = 2 * kOneChunk;
+
+template <typename T>
+__global__ __launch_bounds__(kOneThreads) void k_scan_one(const T* in, T* out, int64_t n) {
+    __shared__ T wsum[kOneThreads / 64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    T carry = 0;
+    for (int64_t c0 = 0; c0 < n; c0 += kOneChunk) {
+        const int64_t base = c0 + int64_t(threadIdx.x) * kIpt;
+        T v[kIpt];
+        T sum = 0;
+#pragma unroll
+        for (int i = 0; i < kIpt; i++) {
+            v[i] = (base + i < n) ? in[base + i] : T(0);
+            sum += v[i];
+        }
+        const T inc = wave_inclusive(sum);
+        if (lane == 63) wsum[w] = inc;
+        __syncthreads();
+        T before = 0, all = 0;
+#pragma unroll
+        for (int i = 0; i < kOneThreads / 64; i++) {
+            const T x = wsum[i];
+            if (i < w) before += x;
+            all += x;
+        }
+        __syncthreads();
+        T run = carry + before + inc - sum;
+#pragma unroll
+        for (int i = 0; i < kIpt; i++) {
+            if (base + i < n) out[base + i] = run;
+            run += v[i];
+        }
+        carry += all;
+    }
+}
+
 template <typename T>
 hipError_t scan_rec(const T* in, T* out, int64_t n, T* tmp, hipStream_t s) {
     if (n <= 0) return hipSuccess;
     const int64_t nt = (n + kTile - 1) / kTile;
     if (nt == 1) {
         k_tile_scan<T><<<1, kThreads, 0, s>>>(in, out, n, nullptr);
+        return hipGetLastError();
+    }
+    if (n <= kOneMax) {
+        k_scan_one<T><<<1, kOneThreads, 0, s>>>(in, out, n);
         return hipGetLastError();
     }
     T* sums = tmp;

@@ -1,6 +1,7 @@
 // Internal declarations shared by the host planner and the gfx950 kernels.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstddef>
@@ -253,6 +254,48 @@ size_t stack_ws_bytes(int64_t n);
 
 void set_error(const std::string& msg);
 
+// Timing events from a per-device pool (created on first use, reused after
+// release).
+hipEvent_t event_acquire();
+void event_release(hipEvent_t e);
+
+// Start and end events of one kernel, recorded by the kernel's own dispatch
+// (hipExtLaunchKernel): no marker packets on the stream, so timing a kernel
+// this way adds next to nothing to the launch sequence.  While
+// t_kernel_events is set, the contraction kernel launches attach it.
+struct KernelEvents {
+    hipEvent_t start = nullptr, stop = nullptr;
+    bool launched = false;
+    bool keep = false;  // handed to a tre_timing (released by tre_timing_read)
+    KernelEvents() = default;
+    KernelEvents(const KernelEvents&) = delete;
+    KernelEvents& operator=(const KernelEvents&) = delete;
+    ~KernelEvents();  // back to the pool unless kept
+};
+extern thread_local KernelEvents* t_kernel_events;
+
+template <typename T>
+struct same_type {
+    using type = T;
+};
+
+// Launch `kernel` (<<<>>> semantics); with t_kernel_events set, through
+// hipExtLaunchKernel with its start / stop events.
+template <typename... KArgs>
+inline hipError_t launch_k(void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t shmem, hipStream_t s,
+                           typename same_type<KArgs>::type... args) {
+    KernelEvents* ke = t_kernel_events;
+    if (!ke) {
+        kernel<<<grid, block, shmem, s>>>(args...);
+        return hipGetLastError();
+    }
+    void* argv[] = {static_cast<void*>(&args)...};
+    const hipError_t e = hipExtLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, argv, shmem, s,
+                                            ke->start, ke->stop, 0);
+    if (e == hipSuccess) ke->launched = true;
+    return e;
+}
+
 // hipEvent timer.  In deferred mode the events are handed to the caller's
 // tre_timing (keep = true) and read and released later by tre_timing_read.
 struct PhaseTimer {
@@ -264,15 +307,14 @@ struct PhaseTimer {
     explicit PhaseTimer(bool enable) : on(enable) {}
     ~PhaseTimer() {
         if (keep) return;
-        for (auto& e : ev)
-            if (e) (void)hipEventDestroy(e);
+        for (auto& e : ev) event_release(e);
     }
-    // events are created when first recorded, so a deferred timer hands over
+    // events are taken when first recorded, so a deferred timer hands over
     // exactly the events it recorded
     void mark(hipStream_t s) {
         if (!on || n >= kMax) return;
-        if (hipEventCreate(&ev[n]) != hipSuccess) {
-            ev[n] = nullptr;
+        ev[n] = event_acquire();
+        if (!ev[n]) {
             on = false;
             return;
         }

@@ -161,3 +161,28 @@ def test_null_arguments_rejected_without_device(tre):
     assert tre.tre.STATUS[L.tre_contract(p.handle, ctypes.byref(jr), None, None, None, 0, None, None, 0, None,
                                          None)] == "TRE_E_STATE"
     assert tre.tre.STATUS[L.tre_cast_f32_bf16(None, None, -1, None)] == "TRE_E_ARG"
+
+
+def test_binding_structs_match_the_header(tre, tmp_path):
+    """Every struct the binding mirrors has the header's size and field
+    offsets (a C program built with gcc against include/tre.h prints them)."""
+    import subprocess
+
+    structs = {"tre_options": tre.tre.Options, "tre_plan_info": tre.tre.PlanInfo,
+               "tre_join_result": tre.tre.JoinResult, "tre_timing": tre.Timing}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "tre.h"', "int main(void) {"]
+    for cname, cls in structs.items():
+        lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
+        for f, _ in cls._fields_:
+            lines.append(f'printf("{cname} {f} %zu\\n", offsetof({cname}, {f}));')
+    lines += ["return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c11", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    got = {tuple(l.split()[:2]): int(l.split()[2]) for l in out if l.strip()}
+    for cname, cls in structs.items():
+        assert got[(cname, "size")] == ctypes.sizeof(cls), cname
+        for f, _ in cls._fields_:
+            assert got[(cname, f)] == getattr(cls, f).offset, (cname, f)

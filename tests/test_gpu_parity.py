@@ -865,3 +865,140 @@ def test_u_dense_join_gpu(orc, idx, validate):
     out = tre.einsum(plan, *to_dev(U), *to_dev(V), want_pairs=True, timing=True)
     assert out.timing["join_path"] == "u_driven_dense", out.timing
     check(out, orc.run(orc_plan(orc, spec), U, V), dtype)
+
+
+# ------------------------------------------------------------ tre_execute
+
+def _execute(spec, U, V, w_cap=None, max_pairs=None, **plan_kw):
+    """tre_execute into caller buffers; returns (output namespace, timing dict)."""
+    import types
+
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    plan = tre.Plan.from_spec(spec, **plan_kw)
+    uk, ut = to_dev(U)
+    vk, vt = to_dev(V)
+    n_u, n_v = len(U["keys"]), len(V["keys"])
+    cross = max(n_u * n_v, 1)
+    w_space = 1
+    for c in plan.key_labels[2]:
+        w_space *= spec["extents"][c] // spec["tiles"][c]
+    cap = min(cross, w_space) if w_cap is None else w_cap
+    mp = cross if max_pairs is None else max_pairs
+    ws = tre.alloc_workspace(plan.workspace_bytes(n_u, n_v, mp))
+    wk = torch.empty((max(cap, 1), max(plan.key_arity[2], 1)), dtype=torch.int32, device="cuda")
+    wt = torch.empty((max(cap, 1), plan.tile_elems[2]), dtype=torch.float32, device="cuda")
+    pairs = torch.empty((cross, 2), dtype=torch.int32, device="cuda")
+    tm = tre.Timing()
+    n_w, n_p = tre.execute(plan, uk, ut, vk, vt, wk if plan.key_arity[2] else None, wt, ws, pairs_out=pairs,
+                           timing=tm)
+    keys = wk[:n_w] if plan.key_arity[2] else wk[:n_w, :0]
+    out = types.SimpleNamespace(w_keys=keys, w_tiles=wt[:n_w], n_w=n_w, n_pairs=n_p, pairs=pairs[:n_p])
+    return out, tm.as_dict()
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_execute_random_plans_gpu(orc, seed):
+    """tre_execute (join and contraction in one call, into caller buffers)
+    on random plans against the oracle: pair lists and key sets bit for bit,
+    values within the tolerance."""
+    rng = np.random.default_rng(7100 + seed)
+    e, upper, ext, til = random_plan(rng)
+    u_lab, v_lab, _ = split_einsum(e)
+    U = workloads.random_relation(rng, u_lab, upper, ext, til, "f32", keep=0.6, zero_frac=0.3)
+    V = workloads.random_relation(rng, v_lab, upper, ext, til, "f32", keep=0.6, zero_frac=0.3)
+    spec = workloads.spec(e, upper, ext, til, "f32")
+    say("execute", seed, e, upper, til, len(U["keys"]), len(V["keys"]))
+    if len(U["keys"]) == 0 or len(V["keys"]) == 0:
+        return
+    out, tm = _execute(spec, U, V, validate=bool(seed % 2))
+    say("  ", tm["join_path"], tm["contract_path"], out.n_pairs, out.n_w)
+    ref = orc.run(orc_plan(orc, spec), U, V)
+    check(out, ref, "f32")
+
+
+def test_execute_errors_gpu():
+    """tre_execute's errors: key errors (validation on), pairs beyond the
+    workspace and an output capacity below the key count, each with the
+    counts reported."""
+    import paper_2603_08957_amd as tre
+
+    rng = np.random.default_rng(5)
+    e, upper, ext, til = "ij,jk->ik", "ijk", {"i": 64, "j": 64, "k": 64}, {"i": 8, "j": 8, "k": 8}
+    U = workloads.random_relation(rng, "ij", upper, ext, til, "f32", keep=0.3, zero_frac=0.0)
+    V = workloads.random_relation(rng, "jk", upper, ext, til, "f32", keep=0.3, zero_frac=0.0)
+    spec = workloads.spec(e, upper, ext, til, "f32")
+    out, _ = _execute(spec, U, V)
+    n_pairs, n_w = out.n_pairs, out.n_w
+    assert 0 < n_w < 64
+    bad = dict(U)
+    bad["keys"] = np.ascontiguousarray(U["keys"][::-1])
+    bad["tiles"] = np.ascontiguousarray(U["tiles"][::-1])
+    with pytest.raises(tre.TreError) as err:
+        _execute(spec, bad, V)
+    assert err.value.status == "TRE_E_UNSORTED"
+    with pytest.raises(tre.TreError) as err:
+        _execute(spec, U, V, max_pairs=n_pairs // 2)
+    assert err.value.status == "TRE_E_WORKSPACE" and err.value.n_pairs == n_pairs
+    with pytest.raises(tre.TreError) as err:
+        _execute(spec, U, V, w_cap=n_w - 1)
+    assert err.value.status == "TRE_E_CAPACITY" and err.value.n_w == n_w and err.value.n_pairs == n_pairs
+
+
+def test_deferred_timing_gpu():
+    """Deferred timing records the contraction kernel's own start and end
+    (no wait in the call): read later, contract_ms is positive and close to
+    the synchronous phase timing's; with no pairs nothing is pending; the
+    three-operand call does the same."""
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    rng = np.random.default_rng(11)
+    e, upper, ext, til = "ij,jk->ik", "ijk", {"i": 512, "j": 512, "k": 512}, {"i": 64, "j": 64, "k": 64}
+    U = workloads.random_relation(rng, "ij", upper, ext, til, "f32", keep=0.8, zero_frac=0.0)
+    V = workloads.random_relation(rng, "jk", upper, ext, til, "f32", keep=0.8, zero_frac=0.0)
+    plan = tre.Plan.from_spec(workloads.spec(e, upper, ext, til, "f32"), validate=False)
+    uk, ut = to_dev(U)
+    vk, vt = to_dev(V)
+    ws = tre.alloc_workspace(plan.workspace_bytes(len(uk), len(vk), len(uk) * len(vk)))
+    wk = torch.empty((64, 2), dtype=torch.int32, device="cuda")
+    wt = torch.empty((64, 64 * 64), dtype=torch.float32, device="cuda")
+    sync = tre.Timing()
+    tre.execute(plan, uk, ut, vk, vt, wk, wt, ws, timing=sync)
+    ref = wt.clone()
+    ms = []
+    for _ in range(3):
+        tm = tre.Timing()
+        tm.deferred = 1
+        tre.execute(plan, uk, ut, vk, vt, wk, wt, ws, timing=tm)
+        assert tm.pending == 1 and tm.join_ms == 0.0
+        tm.read()
+        assert tm.pending == 0 and tm.contract_ms > 0 and tm.units_ms == 0.0
+        ms.append(tm.contract_ms)
+    torch.cuda.synchronize()
+    assert torch.equal(wt, ref)
+    say("deferred", ms, "synchronous", sync.contract_ms)
+    assert min(ms) <= 1.5 * sync.contract_ms + 0.05
+    # no pairs: no kernel, nothing pending
+    tm = tre.Timing()
+    tm.deferred = 1
+    n_w, n_p = tre.execute(plan, uk[:0], ut[:0], vk, vt, wk, wt, ws, timing=tm)
+    assert n_p == 0 and tm.pending == 0
+    # three operands (masked form)
+    ext3, til3 = {"i": 16, "j": 16, "k": 33}, {"i": 1, "j": 1}
+    A = workloads.random_relation(rng, "ij", "ij", ext3, til3, "f32", keep=0.5, zero_frac=0.0)
+    B = workloads.random_relation(rng, "ik", "ij", ext3, til3, "f32", keep=1.0, zero_frac=0.0)
+    C = workloads.random_relation(rng, "jk", "ij", ext3, til3, "f32", keep=1.0, zero_frac=0.0)
+    ak, at = to_dev(A)
+    bk, bt = to_dev(B)
+    ck, ct = to_dev(C)
+    op = tre.Einsum3("ij,ik,jk->ij", "ij", ext3, til3, len(A["keys"]))
+    tm = tre.Timing()
+    tm.deferred = 1
+    op(ak, at, bk, bt, ck, ct, timing=tm)
+    assert tm.pending == 1
+    tm.read()
+    assert tm.contract_ms > 0 and tm.pending == 0
