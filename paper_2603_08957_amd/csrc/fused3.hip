@@ -320,6 +320,37 @@ __device__ inline void stage_pq(const F3Desc& d, const float* Pt, const float* Q
     }
 }
 
+// The P and Q slices for k3_gemm_q, both row-major [rows][kCols] (Q not
+// transposed).  When the block's columns all lie inside R, straight from
+// memory into LDS (global_load_lds_dword: lane l of a wavefront lands at the
+// instruction's LDS address + 4 l), every load issued before the wait at the
+// next barrier and no registers held; otherwise through registers as above.
+__device__ inline void stage_pq_rows(const F3Desc& d, const float* Pt, const float* Qt, int col0, int tq, float* sP,
+                                     float* sQ) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    if (col0 + kCols <= d.R) {
+        const int64_t r = col0 + lane;
+        for (int row = w; row < d.tp; row += kThreads / 64)
+            __builtin_amdgcn_global_load_lds(
+                (const __attribute__((address_space(1))) void*)(Pt + row * d.p_sp + r * d.p_sr),
+                (__attribute__((address_space(3))) void*)(sP + row * kCols), 4, 0, 0);
+        for (int row = w; row < tq; row += kThreads / 64)
+            __builtin_amdgcn_global_load_lds(
+                (const __attribute__((address_space(1))) void*)(Qt + row * d.q_sq + r * d.q_sr),
+                (__attribute__((address_space(3))) void*)(sQ + row * kCols), 4, 0, 0);
+        return;
+    }
+    const int tid = threadIdx.x;
+    for (int e = tid; e < d.tp * kCols; e += kThreads) {
+        const int r = col0 + e % kCols;
+        sP[e] = r < d.R ? Pt[(e / kCols) * d.p_sp + int64_t(r) * d.p_sr] : 0.f;
+    }
+    for (int e = tid; e < tq * kCols; e += kThreads) {
+        const int r = col0 + e % kCols;
+        sQ[e] = r < d.R ? Qt[(e / kCols) * d.q_sq + int64_t(r) * d.q_sr] : 0.f;
+    }
+}
+
 // Any tq (a multiple of 4).  Dynamic LDS: T stages [2][kRows][kPitchT], P
 // slice [tp][kCols], Q slice transposed [kCols][tq + 4] (floats).  Waves:
 // rows [16 mh, +16) and columns [32 rh, +32) of the block; the B operand of
@@ -445,7 +476,7 @@ __global__ __launch_bounds__(kThreads, 3) void k3_gemm_q(F3Args g) {
     auto triple = [&](int32_t t, int32_t t_next) {
         const float* Tt = g.U + int64_t(g.tu[t]) * d.te_u;
         __syncthreads();  // the previous triple is done with sP, sQ and both T stages
-        stage_pq(d, g.P + int64_t(g.tp[t]) * d.te_p, g.Q + int64_t(g.tq[t]) * d.te_q, col0, TQ, qpitch, sP, sQ);
+        stage_pq_rows(d, g.P + int64_t(g.tp[t]) * d.te_p, g.Q + int64_t(g.tq[t]) * d.te_q, col0, TQ, sP, sQ);
         if (!have_next) ld.load(d, Tt, row0, KK, 0);
         have_next = false;
         float qreg[2][kS];
@@ -462,11 +493,9 @@ __global__ __launch_bounds__(kThreads, 3) void k3_gemm_q(F3Args g) {
             if (c == 0) {
                 // this lane's Q elements for the whole triple: q' = gq * kS + j
 #pragma unroll
-                for (int j = 0; j < kS; j += 4) {
-                    const float4 v0 = *reinterpret_cast<const float4*>(sQ + cl0 * qpitch + gq * kS + j);
-                    const float4 v1 = *reinterpret_cast<const float4*>(sQ + cl1 * qpitch + gq * kS + j);
-                    qreg[0][j] = v0.x, qreg[0][j + 1] = v0.y, qreg[0][j + 2] = v0.z, qreg[0][j + 3] = v0.w;
-                    qreg[1][j] = v1.x, qreg[1][j + 1] = v1.y, qreg[1][j + 2] = v1.z, qreg[1][j + 3] = v1.w;
+                for (int j = 0; j < kS; j++) {
+                    qreg[0][j] = sQ[(gq * kS + j) * kCols + cl0];
+                    qreg[1][j] = sQ[(gq * kS + j) * kCols + cl1];
                 }
             }
             const float* arow = st + (16 * mh + n) * kPitchT + gq * kS;
