@@ -700,6 +700,8 @@ hipError_t vec_dispatch(const Plan& p, const VecArgs& a, dim3 grid, hipStream_t 
 
 // ---------------------------------------------------------------- reduce
 
+constexpr int kReduceBatch = 8;
+
 __global__ __launch_bounds__(kThreads) void k_reduce(const int32_t* __restrict__ split, const WsHeader* hdr,
                                                      const int32_t* __restrict__ poff, const float* __restrict__ parts,
                                                      float* __restrict__ W, int64_t w_elems, int32_t w_bf16) {
@@ -711,16 +713,34 @@ __global__ __launch_bounds__(kThreads) void k_reduce(const int32_t* __restrict__
         // 16-byte lanes; partials are read once, so they bypass L2 retention
         const int64_t q = w_elems / 4;
         for (int64_t e = int64_t(blockIdx.y) * kThreads + threadIdx.x; e < q; e += int64_t(gridDim.y) * kThreads) {
+            const f32x4* src = reinterpret_cast<const f32x4*>(parts) + int64_t(first) * q + e;
             f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-            for (int j = 0; j < cnt; j++)
-                acc += __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(parts) + int64_t(first + j) * q + e);
+            int j = 0;
+            // eight partials in flight, added in slot order
+            for (; j + kReduceBatch <= cnt; j += kReduceBatch) {
+                f32x4 v[kReduceBatch];
+#pragma unroll
+                for (int i = 0; i < kReduceBatch; i++) v[i] = __builtin_nontemporal_load(src + int64_t(j + i) * q);
+#pragma unroll
+                for (int i = 0; i < kReduceBatch; i++) acc += v[i];
+            }
+            for (; j < cnt; j++) acc += __builtin_nontemporal_load(src + int64_t(j) * q);
             reinterpret_cast<f32x4*>(W)[int64_t(s) * q + e] = acc;
         }
         return;
     }
     for (int64_t e = int64_t(blockIdx.y) * kThreads + threadIdx.x; e < w_elems; e += int64_t(gridDim.y) * kThreads) {
+        const float* src = parts + int64_t(first) * w_elems + e;
         float acc = 0.f;
-        for (int j = 0; j < cnt; j++) acc += parts[int64_t(first + j) * w_elems + e];
+        int j = 0;
+        for (; j + kReduceBatch <= cnt; j += kReduceBatch) {
+            float v[kReduceBatch];
+#pragma unroll
+            for (int i = 0; i < kReduceBatch; i++) v[i] = src[int64_t(j + i) * w_elems];
+#pragma unroll
+            for (int i = 0; i < kReduceBatch; i++) acc += v[i];
+        }
+        for (; j < cnt; j++) acc += src[int64_t(j) * w_elems];
         if (w_bf16) reinterpret_cast<uint16_t*>(W)[int64_t(s) * w_elems + e] = f32_to_bf16_rne(acc);
         else W[int64_t(s) * w_elems + e] = acc;
     }

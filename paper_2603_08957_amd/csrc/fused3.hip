@@ -563,11 +563,32 @@ __global__ __launch_bounds__(kThreads) void k3_reduce(F3Args g) {
     dst.row0 = int64_t(mb) * g.brows;
     dst.col0 = rb * kCols;
     const int64_t bs = int64_t(g.brows) * kCols;
-    for (int e = threadIdx.x; e < bs; e += kThreads) {
-        float v = g.part[(2 * b0 + 1) * bs + e];
-        for (int64_t bb = b0 + 1; bb < b1; bb++) v += g.part[(2 * bb) * bs + e];
-        v += g.part[(2 * b1) * bs + e];
-        dst.put(d, e / kCols, e % kCols, v);
+    // kRedPer elements per thread at a time, so each slot's loads are all in
+    // flight together (the sum still runs slot by slot, in range order)
+    constexpr int kRedPer = 8;
+    for (int e0 = threadIdx.x; e0 < bs; e0 += kRedPer * kThreads) {
+        float v[kRedPer];
+#pragma unroll
+        for (int i = 0; i < kRedPer; i++) {
+            const int64_t e = e0 + i * kThreads;
+            v[i] = e < bs ? g.part[(2 * b0 + 1) * bs + e] : 0.f;
+        }
+        for (int64_t bb = b0 + 1; bb <= b1; bb++) {
+            const float* src = g.part + (bb < b1 ? 2 * bb : 2 * b1) * bs;
+            float x[kRedPer];
+#pragma unroll
+            for (int i = 0; i < kRedPer; i++) {
+                const int64_t e = e0 + i * kThreads;
+                x[i] = e < bs ? src[e] : 0.f;
+            }
+#pragma unroll
+            for (int i = 0; i < kRedPer; i++) v[i] += x[i];
+        }
+#pragma unroll
+        for (int i = 0; i < kRedPer; i++) {
+            const int64_t e = e0 + i * kThreads;
+            if (e < bs) dst.put(d, int(e / kCols), int(e % kCols), v[i]);
+        }
     }
 }
 
