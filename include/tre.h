@@ -198,7 +198,9 @@ int64_t tre_workspace_max_pairs(tre_plan_t plan, int64_t n_u, int64_t n_v, size_
  * hold); when V has no promoted labels (one tuple) and W's key is U's key as
  * it is, every U tuple is one pair and one output tuple, the counts are
  * known without the device, and the call synchronizes only to report key
- * validation.
+ * validation: without it, the join's kernels may still be running on the
+ * stream when the call returns, so work on another stream that reads the
+ * workspace (tre_contract, tre_join_keys) must wait for this stream.
  * TRE_E_WORKSPACE (out->n_pairs set) if the pairs do not fit; key errors are
  * reported as TRE_E_UNSORTED / TRE_E_DUPKEY / TRE_E_KEYRANGE. */
 tre_status tre_join(tre_plan_t plan, const int32_t *u_keys, int64_t n_u, const int32_t *v_keys, int64_t n_v,
