@@ -1002,3 +1002,72 @@ def test_deferred_timing_gpu():
     assert tm.pending == 1
     tm.read()
     assert tm.contract_ms > 0 and tm.pending == 0
+
+
+# ------------------------------------------------ size boundaries of the paths
+
+def _rel(rng, keys, tile_elems):
+    keys = np.ascontiguousarray(np.asarray(keys, dtype=np.int32).reshape(len(keys), -1))
+    return {"keys": keys, "tiles": rng.standard_normal((len(keys), tile_elems)).astype(np.float32), "dtype": "f32"}
+
+
+@pytest.mark.parametrize("n_u,n_v", [(64, 64), (64, 65), (181, 181), (182, 181), (300, 300)])
+def test_cross_product_sizes_gpu(orc, n_u, n_v):
+    """A cross product (no join label) whose pairs and output keys number
+    4,096 / 4,160 / 32,761 / 32,942 / 90,000: the pair-head scan in one tile,
+    in one workgroup and in three passes; the unit table in one workgroup
+    (4,096 keys) and over several launches; compared with the oracle, and
+    through tre_execute as well."""
+    rng = np.random.default_rng(n_u * 1000 + n_v)
+    ext, til = {"i": 1 << 14, "k": 1 << 14, "a": 3}, {"i": 1, "k": 1}
+    e, upper = "ia,ka->ik", "ik"
+    U = _rel(rng, np.sort(rng.choice(1 << 14, n_u, replace=False)), 3)
+    V = _rel(rng, np.sort(rng.choice(1 << 14, n_v, replace=False)), 3)
+    spec = workloads.spec(e, upper, ext, til, "f32")
+    say("cross product", n_u, n_v)
+    _, out = gpu_run(spec, U, V, validate=True)
+    ref = orc.run(orc_plan(orc, spec), U, V)
+    check(out, ref, "f32")
+    out2, _ = _execute(spec, U, V, validate=False, max_pairs=n_u * n_v)
+    check(out2, ref, "f32")
+
+
+@pytest.mark.parametrize("radix_k", [32768, 32769])
+def test_key_space_segments_sizes_gpu(orc, radix_k):
+    """The segments over a dense W key space: 32,768 keys (one workgroup) and
+    65,536 (a radix of 32,769 takes 16 key bits: flags, scan, compaction),
+    with about a third of the keys absent; the join driven by V over a U that
+    holds every key."""
+    rng = np.random.default_rng(radix_k)
+    n_j = 512
+    ext, til = {"i": 4, "j": n_j, "k": radix_k}, {"j": 1, "k": 1}
+    e, upper = "ij,kj->ki", "jk"
+    X = _rel(rng, np.arange(n_j), 4)
+    ks = np.sort(rng.choice(radix_k, (2 * radix_k) // 3, replace=False))
+    pairs = [(k, j) for k in ks for j in np.sort(rng.choice(n_j, 3, replace=False))]
+    Y = _rel(rng, pairs, 1)
+    spec = workloads.spec(e, upper, ext, til, "f32")
+    say("key space", radix_k, len(pairs))
+    plan, out = gpu_run(spec, X, Y, validate=True)
+    ref = orc.run(orc_plan(orc, spec), X, Y)
+    check(out, ref, "f32")
+
+
+@pytest.mark.parametrize("n", [4096, 4097])
+def test_small_join_limit_gpu(orc, n):
+    """A one-to-one join of n keys (W keyed by the join label): 4,096 pairs
+    take the one-workgroup join at its limit, 4,097 the multi-kernel join;
+    both against the oracle, and the path taken as reported."""
+    rng = np.random.default_rng(n)
+    ext, til = {"j": 1 << 20, "a": 5, "b": 4}, {"j": 1}
+    e, upper = "ja,jb->jab", "j"
+    keys = np.sort(rng.choice(1 << 20, n, replace=False))
+    U = _rel(rng, keys, 5)
+    V = _rel(rng, keys, 4)
+    spec = workloads.spec(e, upper, ext, til, "f32")
+    out, tm = _execute(spec, U, V, validate=True)
+    say("small join limit", n, tm["join_path"])
+    assert (tm["join_path"] == "one_workgroup") == (n <= 4096)
+    ref = orc.run(orc_plan(orc, spec), U, V)
+    check(out, ref, "f32")
+    assert out.n_pairs == n
