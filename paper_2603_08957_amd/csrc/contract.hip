@@ -170,8 +170,17 @@ __global__ __launch_bounds__(kUnitsThreads) void k_units_small(const int32_t* __
     __shared__ int32_t key_uo[kOrderMax + 1], key_po[kOrderMax], key_a[kOrderMax + 1];
     const int t = threadIdx.x;
     if (tables) {
+        // the table shapes through LDS: read from the kernel arguments with
+        // dynamic indices they would be one dependent scalar load each
+        constexpr int kWords = int(sizeof(TableSet) / sizeof(int32_t));
+        static_assert(sizeof(TableSet) % sizeof(int64_t) == 0, "TableSet words");
+        __shared__ int64_t s_ts_raw[sizeof(TableSet) / sizeof(int64_t)];
+        for (int i = t; i < kWords; i += kUnitsThreads)
+            reinterpret_cast<int32_t*>(s_ts_raw)[i] = reinterpret_cast<const int32_t*>(&ts)[i];
+        __syncthreads();
+        const TableSet& s_ts = *reinterpret_cast<const TableSet*>(s_ts_raw);
         for (int k = 0; k < T_COUNT; k++) {
-            const Dims& d = ts.d[k];
+            const Dims& d = s_ts.d[k];
             int32_t c = 1;
             for (int i = 0; i < d.n; i++) c *= d.size[i];
             for (int32_t x = t; x < c; x += kUnitsThreads) {
@@ -180,7 +189,7 @@ __global__ __launch_bounds__(kUnitsThreads) void k_units_small(const int32_t* __
                     o += (rem % d.size[i]) * d.stride[i];
                     rem /= d.size[i];
                 }
-                tables[ts.off[k] + x] = o;
+                tables[s_ts.off[k] + x] = o;
             }
         }
     }
