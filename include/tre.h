@@ -244,6 +244,48 @@ tre_status tre_execute(tre_plan_t plan, const int32_t *u_keys, int64_t n_u, cons
                        int64_t w_cap, int64_t *n_w, int32_t *pairs_out, int64_t pair_cap, int64_t *n_pairs,
                        void *ws, size_t ws_bytes, void *stream, tre_timing *timing);
 
+/* tre_output_bounds -- upper bounds on the pair and output key counts of a
+ * join of n_u and n_v tuples with a workspace of ws_bytes (host only, no
+ * device work): the pair bound is the cross product, or n_u (n_v) when one
+ * side's key is made of the join labels only, capped by the workspace's
+ * pair capacity; the key bound is that, capped by W's key space; both are
+ * n_u for a keyless one-tuple V with W keyed by U.  async_ok = 1 when
+ * tre_execute_async can enqueue the whole EinSum without a read-back for
+ * these sizes.  TRE_E_WORKSPACE if ws_bytes is below tre_workspace_bytes(
+ * plan, n_u, n_v, 0). */
+tre_status tre_output_bounds(tre_plan_t plan, int64_t n_u, int64_t n_v, size_t ws_bytes, int64_t *pairs_bound,
+                             int64_t *keys_bound, int32_t *async_ok);
+
+/* tre_execute_async -- tre_execute with no wait on the host: the join (Sec.
+ * 5), the GROUP BY keys and the contraction are all enqueued on the stream
+ * with their grids sized for the bounds of tre_output_bounds, every kernel
+ * reading the counts the join wrote in device memory, and the counts come
+ * back in device memory, so calls (and chains of them) run back to back.
+ *   counts  : device int64 [4], written last on the stream: [0] pairs, [1]
+ *             output keys, [2] a tre_status (TRE_OK, TRE_E_UNSORTED /
+ *             TRE_E_DUPKEY / TRE_E_KEYRANGE when key validation finds an
+ *             error, TRE_E_WORKSPACE when the pairs exceed the workspace's
+ *             capacity: then [0] is the number needed), [3] 0.  W and the
+ *             pair list hold [1] and [0] entries when [2] is TRE_OK and are
+ *             unspecified otherwise.
+ *   w_cap, pair_cap : at least the key and pair bounds (TRE_E_CAPACITY on
+ *             the host otherwise).
+ *   n_u_dev : optional device int64 holding U's tuple count when only a
+ *             bound n_u is known on the host (the keys and tiles of U are
+ *             read up to that count): for a keyless one-tuple V with W keyed
+ *             by U, e.g. the second EinSum of a chain whose U is the first
+ *             one's output (TRE_E_ARG for other plans, or when the sizes are
+ *             not async_ok).
+ *   Everything else as for tre_execute.  When the sizes are not async_ok
+ *   (and n_u_dev is NULL) the call runs tre_execute, waiting for its counts,
+ *   and writes them to `counts`.  The summation order follows the bounds,
+ *   so results can differ in the last bits from tre_execute's when a bound
+ *   exceeds the count it stands for. */
+tre_status tre_execute_async(tre_plan_t plan, const int32_t *u_keys, int64_t n_u, const int64_t *n_u_dev,
+                             const void *u_tiles, const int32_t *v_keys, int64_t n_v, const void *v_tiles,
+                             int32_t *w_keys, void *w_tiles, int64_t w_cap, int32_t *pairs_out, int64_t pair_cap,
+                             int64_t *counts, void *ws, size_t ws_bytes, void *stream, tre_timing *timing);
+
 /* tre_execute_noalloc -- tre_execute without a workspace argument, for
  * callers that cannot allocate device memory: code under stream capture,
  * tight serving loops, harnesses that forbid allocation.  The workspace is a

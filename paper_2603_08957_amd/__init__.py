@@ -9,6 +9,6 @@ its ctypes binding.
 """
 from .tre import (  # noqa: F401
     EXPORTS, Einsum3, JoinResult, Output, Plan, TreError, Timing, alloc_workspace, cast_f32_bf16, contract, einsum,
-    execute, execute3, execute_noalloc, join, join_keys, lib, noalloc_scratch_bytes, repartition, scale_f32, stack_rows,
-    tiles_from_entries,
+    execute, execute3, execute_async, execute_noalloc, join, join_keys, lib, noalloc_scratch_bytes, output_bounds,
+    repartition, scale_f32, stack_rows, tiles_from_entries,
 )

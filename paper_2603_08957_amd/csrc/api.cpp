@@ -12,6 +12,7 @@ namespace {
 
 constexpr uint64_t kMagic = 0x7472655f6a6f696eull;  // "tre_join"
 constexpr int kTargetWorkgroups = 2048;              // 8 per CU on 256 CUs
+constexpr int64_t kAsyncMaxKeys = 4096;              // output keys of the one-workgroup unit table
 
 tre_status dev_fail(hipError_t e, const char* where) {
     set_error(std::string(where) + ": " + hipGetErrorString(e));
@@ -148,7 +149,8 @@ struct JoinState {
 // tre_join up to its read-back: argument checks, workspace layout and every
 // join launch.  `out` gets the sizes and the internal fields.
 tre_status join_enqueue(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const int32_t* v_keys, int64_t n_v,
-                        void* ws, size_t ws_bytes, hipStream_t s, tre_join_result* out, JoinState* st) {
+                        void* ws, size_t ws_bytes, hipStream_t s, tre_join_result* out, JoinState* st,
+                        const int64_t* n_u_dev = nullptr) {
     if (!plan || !out || n_u < 0 || n_v < 0 || !ws) {
         set_error("tre_join: null plan/out/workspace or negative size");
         return TRE_E_ARG;
@@ -190,7 +192,7 @@ tre_status join_enqueue(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, con
     if (e != hipSuccess) return dev_fail(e, "header");
     WsHeader* hdr = reinterpret_cast<WsHeader*>(w + L.hdr);
     if (p.opt.validate_keys) {
-        if ((e = launch_validate(u_keys, n_u, p.nk[0], p.radix[0], &hdr->err_u, s)) != hipSuccess)
+        if ((e = launch_validate(u_keys, n_u, p.nk[0], p.radix[0], &hdr->err_u, s, n_u_dev)) != hipSuccess)
             return dev_fail(e, "validate U");
         if ((e = launch_validate(v_keys, n_v, p.nk[1], p.radix[1], &hdr->err_v, s)) != hipSuccess)
             return dev_fail(e, "validate V");
@@ -202,7 +204,7 @@ tre_status join_enqueue(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, con
             set_error("tre_join: workspace too small for the matched pairs (see n_pairs)");
             return TRE_E_WORKSPACE;
         }
-        if ((e = launch_keyed_by_u(p, L, w, u_keys, s)) != hipSuccess) return dev_fail(e, "join");
+        if ((e = launch_keyed_by_u(p, L, w, u_keys, s, n_u_dev)) != hipSuccess) return dev_fail(e, "join");
         st->cap = n_u;
         st->counts_known = true;
         st->path = 4;
@@ -282,10 +284,13 @@ void join_timing(tre_timing* timing, int32_t path) {
     timing->join_path = path;
 }
 
-// tre_contract's launches, for the join's counts n_pairs and n_w.
+// tre_contract's launches, for the join's counts n_pairs and n_w.  With
+// `dev` those are upper bounds and every kernel reads the join's counts from
+// the workspace header (the caller has checked that the bounds need no
+// pacing, no U ranges, and a one-workgroup unit table or one unit per key).
 tre_status contract_enqueue(tre_plan_t plan, const tre_join_result* jr, int64_t n_pairs, int64_t n_w,
                             const void* u_tiles, const void* v_tiles, int32_t* w_keys, void* w_out,
-                            int32_t* pairs_out, hipStream_t s, tre_timing* timing) {
+                            int32_t* pairs_out, hipStream_t s, tre_timing* timing, bool dev = false) {
     // W's element type is the plan's (fp32, or bf16 bits with w_bf16); the
     // kernels take the array as float* and store 16-bit elements through it
     // when the plan says bf16
@@ -314,8 +319,8 @@ tre_status contract_enqueue(tre_plan_t plan, const tre_join_result* jr, int64_t 
     }
     tm.mark(s);
     const int64_t slots = (p.kclass == KC_GEMM && p.fast) ? gemm_paced_slots(p) : 0;
-    const int32_t pace = choose_pacing(p, jr->n_u, n_pairs, n_w, slots);
-    const int32_t R = pace ? 0 : choose_u_ranges(p, L, jr->n_u, n_pairs, n_w);
+    const int32_t pace = dev ? 0 : choose_pacing(p, jr->n_u, n_pairs, n_w, slots);
+    const int32_t R = (pace || dev) ? 0 : choose_u_ranges(p, L, jr->n_u, n_pairs, n_w);
     const int64_t p_unit = (R > 1 || pace) ? n_pairs : choose_unit(p, L, n_pairs, n_w);
     hipError_t e;
     // (launch_units writes the tile offset tables itself)
@@ -324,7 +329,7 @@ tre_status contract_enqueue(tre_plan_t plan, const tre_join_result* jr, int64_t 
             return dev_fail(e, "tables");
         e = launch_range_units(p, L, w, n_w, jr->n_u, R, s);
     } else {
-        e = launch_units(p, L, w, n_pairs, n_w, p_unit, !pace, s);
+        e = launch_units(p, L, w, n_pairs, n_w, p_unit, !pace, s, dev);
     }
     if (e != hipSuccess) return dev_fail(e, "units");
     tm.mark(s);
@@ -348,7 +353,7 @@ tre_status contract_enqueue(tre_plan_t plan, const tre_join_result* jr, int64_t 
         const int64_t split_bound = R > 1 ? n_w : std::min<int64_t>(n_w, n_pairs / (p_unit + 1) + 1);
         if ((e = launch_reduce(p, L, w, w_tiles, split_bound, s)) != hipSuccess) return dev_fail(e, "reduce");
     }
-    if ((e = launch_write_outputs(p, L, w, w_keys, pairs_out, n_pairs, n_w, s)) != hipSuccess)
+    if ((e = launch_write_outputs(p, L, w, w_keys, pairs_out, n_pairs, n_w, s, dev)) != hipSuccess)
         return dev_fail(e, "outputs");
     tm.mark(s);
     if (timing) {
@@ -374,6 +379,38 @@ tre_status contract_enqueue(tre_plan_t plan, const tre_join_result* jr, int64_t 
         }
     }
     return TRE_OK;
+}
+
+// Upper bounds on a join's pair and output key counts, from the sizes alone
+// (exact when the host knows them), and whether the contraction can be
+// enqueued on them with the counts read on the device: no pacing and no U
+// ranges at the bounds, and a one-workgroup unit table or one unit per key.
+struct AsyncBounds {
+    int64_t pairs = 0, keys = 0;
+    bool ok = false;
+};
+
+AsyncBounds async_bounds(const Plan& p, int64_t n_u, int64_t n_v, int64_t max_pairs) {
+    AsyncBounds b;
+    if (n_u > 0 && n_v == 1 && keyed_by_u(p)) {
+        b.pairs = b.keys = n_u;
+    } else {
+        int64_t w_space = 1;
+        for (int c = 0; c < p.nk[2] && w_space <= (int64_t(1) << 40); c++) w_space *= p.radix[2][c];
+        b.pairs = (n_u > 0 && n_v > 0) ? std::max<int64_t>(0, std::min(max_pairs, pair_bound(p, n_u, n_v))) : 0;
+        b.keys = std::min(b.pairs, w_space);
+    }
+    if (b.pairs <= 0) {
+        b.ok = true;
+        return b;
+    }
+    const Layout L = make_layout(p, n_u, n_v, max_pairs);
+    const int64_t slots = (p.kclass == KC_GEMM && p.fast) ? gemm_paced_slots(p) : 0;
+    if (choose_pacing(p, n_u, b.pairs, b.keys, slots) != 0 || choose_u_ranges(p, L, n_u, b.pairs, b.keys) != 0)
+        return b;
+    const int64_t p_unit = choose_unit(p, L, b.pairs, b.keys);
+    b.ok = b.keys <= kAsyncMaxKeys || p_unit >= b.pairs;
+    return b;
 }
 
 }  // namespace
@@ -469,6 +506,84 @@ tre_status tre_execute(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, cons
     if (n_w) *n_w = jr.n_w;
     if (st != TRE_OK) return st;
     return tre_contract(plan, &jr, u_tiles, v_tiles, w_keys, w_cap, w_tiles, pairs_out, pair_cap, stream, timing);
+}
+
+tre_status tre_output_bounds(tre_plan_t plan, int64_t n_u, int64_t n_v, size_t ws_bytes, int64_t* pairs_bound,
+                             int64_t* keys_bound, int32_t* async_ok) {
+    if (!plan || n_u < 0 || n_v < 0 || !pairs_bound || !keys_bound || !async_ok) {
+        set_error("tre_output_bounds: null argument or negative size");
+        return TRE_E_ARG;
+    }
+    const int64_t max_pairs = tre_workspace_max_pairs(plan, n_u, n_v, ws_bytes);
+    if (max_pairs < 0) {
+        set_error("tre_output_bounds: workspace smaller than tre_workspace_bytes(plan, n_u, n_v, 0)");
+        return TRE_E_WORKSPACE;
+    }
+    const AsyncBounds b = async_bounds(plan->p, n_u, n_v, max_pairs);
+    *pairs_bound = b.pairs;
+    *keys_bound = b.keys;
+    *async_ok = b.ok ? 1 : 0;
+    return TRE_OK;
+}
+
+tre_status tre_execute_async(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, const int64_t* n_u_dev,
+                             const void* u_tiles, const int32_t* v_keys, int64_t n_v, const void* v_tiles,
+                             int32_t* w_keys, void* w_tiles, int64_t w_cap, int32_t* pairs_out, int64_t pair_cap,
+                             int64_t* counts, void* ws, size_t ws_bytes, void* stream, tre_timing* timing) {
+    if (!plan || !counts || n_u < 0 || n_v < 0) {
+        set_error("tre_execute_async: null plan / counts or negative size");
+        return TRE_E_ARG;
+    }
+    const Plan& p = plan->p;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (n_u_dev && !(n_v == 1 && keyed_by_u(p))) {
+        set_error("tre_execute_async: a device-side U count needs a keyless one-tuple V with W keyed by U");
+        return TRE_E_ARG;
+    }
+    const int64_t max_pairs = tre_workspace_max_pairs(plan, n_u, n_v, ws_bytes);
+    if (max_pairs < 0) {
+        set_error("tre_execute_async: workspace smaller than tre_workspace_bytes(plan, n_u, n_v, 0)");
+        return TRE_E_WORKSPACE;
+    }
+    const AsyncBounds b = async_bounds(p, n_u, n_v, max_pairs);
+    if (!b.ok) {
+        if (n_u_dev) {
+            set_error("tre_execute_async: a device-side U count needs an output within the device-count launches");
+            return TRE_E_ARG;
+        }
+        // the counts are needed on the host: the synchronous call, then the
+        // counts and the status to the device
+        int64_t nw = 0, np = 0;
+        const tre_status st = tre_execute(plan, u_keys, n_u, u_tiles, v_keys, n_v, v_tiles, w_keys, w_tiles, w_cap,
+                                          &nw, pairs_out, pair_cap, &np, ws, ws_bytes, stream, timing);
+        if (st == TRE_E_ARG || st == TRE_E_DEVICE || st == TRE_E_STATE) return st;
+        const hipError_t e = launch_counts_set(np, nw, int64_t(st), counts, s);
+        return e == hipSuccess ? st : dev_fail(e, "counts");
+    }
+    if (w_cap < b.keys || (pairs_out && pair_cap < b.pairs)) {
+        set_error("tre_execute_async: output capacity below the bounds of tre_output_bounds");
+        return TRE_E_CAPACITY;
+    }
+    tre_join_result jr{};
+    JoinState js;
+    PhaseTimer tm(timing != nullptr && !timing->deferred);
+    tm.mark(s);
+    tre_status st = join_enqueue(plan, u_keys, n_u, v_keys, n_v, ws, ws_bytes, s, &jr, &js, n_u_dev);
+    if (st != TRE_OK) return st;
+    tm.mark(s);
+    join_timing(timing, js.path);
+    if ((st = contract_enqueue(plan, &jr, b.pairs, b.keys, u_tiles, v_tiles, w_keys, w_tiles, pairs_out, s, timing,
+                               true)) != TRE_OK)
+        return st;
+    const Layout L = make_layout(p, n_u, n_v, max_pairs);
+    const hipError_t e = launch_counts_out(L, static_cast<char*>(ws), max_pairs, counts, s);
+    if (e != hipSuccess) return dev_fail(e, "counts");
+    if (timing && !timing->deferred) {
+        const float jm = tm.between(0, 1);
+        timing->join_ms = jm;
+        timing->total_ms += jm;
+    }
+    return TRE_OK;
 }
 
 tre_status tre_cast_f32_bf16(const float* x, uint16_t* y, int64_t n, void* stream) {

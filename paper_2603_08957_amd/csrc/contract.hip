@@ -151,7 +151,9 @@ __global__ __launch_bounds__(kOrderBins) void k_order_units(Unit* __restrict__ u
 // binary search of the per-key unit offsets in LDS), so a cut key's units
 // are written by many threads at once.  With `ts` non-null the workgroup also
 // writes the tile offset tables first (small tables only, `tables`
-// non-null), saving their launch.
+// non-null), saving their launch.  With `dev_nw` the key count is the one the
+// join wrote into the header (`n_w` is then an upper bound), so the launch
+// needs no count from the host.
 constexpr int kUnitsThreads = kOrderBins;
 constexpr int kUnitsPer = kOrderMax / kUnitsThreads;
 constexpr int64_t kUnitsTableMax = 16384;
@@ -163,12 +165,13 @@ __global__ __launch_bounds__(kUnitsThreads) void k_units_small(const int32_t* __
                                                                 int32_t* __restrict__ split,
                                                                 int32_t* __restrict__ part_off,
                                                                 WsHeader* __restrict__ hdr, TableSet ts,
-                                                                int32_t* __restrict__ tables) {
+                                                                int32_t* __restrict__ tables, int dev_nw) {
     __shared__ Unit buf[kOrderMax];
     __shared__ int32_t cnt[kOrderBins];
     __shared__ int32_t wsum[kUnitsThreads / 64];
     __shared__ int32_t key_uo[kOrderMax + 1], key_po[kOrderMax], key_a[kOrderMax + 1];
     const int t = threadIdx.x;
+    if (dev_nw) n_w = min(n_w, hdr->n_w);  // n_w is then a bound; the key count is the join's
     if (tables) {
         // the table shapes through LDS: read from the kernel arguments with
         // dynamic indices they would be one dependent scalar load each
@@ -762,8 +765,11 @@ struct Unpack {
     int32_t bits[26];
 };
 
-__global__ void k_write_keys(const uint64_t* __restrict__ seg_key, int64_t n_w, Unpack up, int32_t* __restrict__ out) {
+// (dn: the counts from the join's header, the host's being bounds)
+__global__ void k_write_keys(const uint64_t* __restrict__ seg_key, int64_t n_w, Unpack up, int32_t* __restrict__ out,
+                             const WsHeader* __restrict__ dn) {
     const int64_t s = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (dn) n_w = min(n_w, dn->n_w);
     if (s >= n_w) return;
     uint64_t k = seg_key[s];
     for (int c = up.n - 1; c >= 0; c--) {
@@ -774,8 +780,9 @@ __global__ void k_write_keys(const uint64_t* __restrict__ seg_key, int64_t n_w, 
 }
 
 __global__ void k_write_pairs(const int32_t* __restrict__ pu, const int32_t* __restrict__ pv, int64_t n,
-                              int32_t* __restrict__ out) {
+                              int32_t* __restrict__ out, const WsHeader* __restrict__ dn) {
     const int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (dn) n = min(n, dn->n_pairs);
     if (p >= n) return;
     out[2 * p] = pu[p];
     out[2 * p + 1] = pv[p];
@@ -835,9 +842,11 @@ hipError_t launch_tables(const Plan& p, int32_t* tables, hipStream_t s) {
 
 // One unit per key (no key longer than the cap): the unit table is the
 // segment table, with no partial tiles and no split keys.
+// (dev_nw: the key count from the header, n_w a bound)
 __global__ void k_key_units(const int32_t* __restrict__ seg_start, int64_t n_w, Unit* __restrict__ units,
-                            WsHeader* hdr) {
+                            WsHeader* hdr, int dev_nw) {
     const int64_t s = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (dev_nw) n_w = min(n_w, hdr->n_w);
     if (s > n_w) return;
     if (s == n_w) {
         hdr->n_units = int32_t(n_w);
@@ -854,7 +863,7 @@ __global__ void k_key_units(const int32_t* __restrict__ seg_start, int64_t n_w, 
 }
 
 hipError_t launch_units(const Plan& p, const Layout& L, char* ws, int64_t n_pairs, int64_t n_w, int64_t p_unit,
-                        bool longest_first, hipStream_t s) {
+                        bool longest_first, hipStream_t s, bool dev_counts) {
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
     int32_t* seg_start = reinterpret_cast<int32_t*>(ws + L.seg_start);
     int32_t* nunits = reinterpret_cast<int32_t*>(ws + L.seg_units);
@@ -873,13 +882,13 @@ hipError_t launch_units(const Plan& p, const Layout& L, char* ws, int64_t n_pair
                                                    longest_first && p.kclass == KC_GEMM ? 1 : 0,
                                                    reinterpret_cast<Unit*>(ws + L.unit_desc),
                                                    reinterpret_cast<int32_t*>(ws + L.split_list), nparts, hdr, ts,
-                                                   with_tables ? tables : nullptr);
+                                                   with_tables ? tables : nullptr, dev_counts ? 1 : 0);
         return hipGetLastError();
     }
     if ((e = launch_tables(p, tables, s)) != hipSuccess) return e;
     if (p_unit >= n_pairs) {  // no key can be longer than the cap
         k_key_units<<<blocks_for(n_w + 1), kThreads, 0, s>>>(seg_start, n_w, reinterpret_cast<Unit*>(ws + L.unit_desc),
-                                                             hdr);
+                                                             hdr, dev_counts ? 1 : 0);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (longest_first && p.kclass == KC_GEMM && n_w <= kOrderMax) {
             k_order_units<<<1, kOrderBins, 0, s>>>(reinterpret_cast<Unit*>(ws + L.unit_desc), hdr);
@@ -887,6 +896,7 @@ hipError_t launch_units(const Plan& p, const Layout& L, char* ws, int64_t n_pair
         }
         return e;
     }
+    if (dev_counts) return hipErrorInvalidValue;  // device key counts: one-workgroup table or one unit per key
     k_seg_units<<<blocks_for(n_w + 1), kThreads, 0, s>>>(seg_start, n_w, p_unit, nunits, nparts, nsplit);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = scan_exclusive_i32(nunits, nunits, n_w + 1, tmp, s)) != hipSuccess) return e;
@@ -1020,23 +1030,61 @@ hipError_t launch_reduce(const Plan& p, const Layout& L, char* ws, float* w_tile
 }
 
 hipError_t launch_write_outputs(const Plan& p, const Layout& L, char* ws, int32_t* w_keys, int32_t* pairs_out,
-                                int64_t n_pairs, int64_t n_w, hipStream_t s) {
+                                int64_t n_pairs, int64_t n_w, hipStream_t s, bool dev_counts) {
+    const WsHeader* dn = dev_counts ? reinterpret_cast<const WsHeader*>(ws + L.hdr) : nullptr;
     if (w_keys && p.nk[2] > 0 && n_w > 0) {
         Unpack up{};
         up.n = p.nk[2];
         for (int c = 0; c < p.nk[2]; c++) up.bits[c] = p.w_bits[c];
         k_write_keys<<<blocks_for(n_w), kThreads, 0, s>>>(reinterpret_cast<const uint64_t*>(ws + L.seg_key), n_w, up,
-                                                           w_keys);
+                                                           w_keys, dn);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     if (pairs_out && n_pairs > 0) {
         k_write_pairs<<<blocks_for(n_pairs), kThreads, 0, s>>>(reinterpret_cast<const int32_t*>(ws + L.pu),
                                                                 reinterpret_cast<const int32_t*>(ws + L.pv), n_pairs,
-                                                                pairs_out);
+                                                                pairs_out, dn);
         return hipGetLastError();
     }
     return hipSuccess;
+}
+
+// The counts of an asynchronous call, from the join's header: counts[0] the
+// pairs, [1] the output keys, [2] a tre_status (key errors as on the host,
+// pairs beyond the workspace's capacity), [3] zero.
+__global__ void k_counts_out(const WsHeader* __restrict__ hdr, int64_t max_pairs, int64_t* __restrict__ counts) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    auto key_status = [](int32_t f) {
+        return (f & 4) ? int64_t(TRE_E_KEYRANGE) : (f & 1) ? int64_t(TRE_E_UNSORTED) : (f & 2) ? int64_t(TRE_E_DUPKEY) : 0;
+    };
+    int64_t st = key_status(hdr->err_u);
+    if (st == 0) st = key_status(hdr->err_v);
+    const int64_t n_pairs = hdr->n_pairs;
+    if (st == 0 && n_pairs > max_pairs) st = TRE_E_WORKSPACE;
+    counts[0] = n_pairs;
+    counts[1] = n_pairs > 0 ? hdr->n_w : 0;
+    counts[2] = st;
+    counts[3] = 0;
+}
+
+// The counts of a call that knew them on the host.
+__global__ void k_counts_set(int64_t n_pairs, int64_t n_w, int64_t status, int64_t* __restrict__ counts) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    counts[0] = n_pairs;
+    counts[1] = n_w;
+    counts[2] = status;
+    counts[3] = 0;
+}
+
+hipError_t launch_counts_out(const Layout& L, char* ws, int64_t max_pairs, int64_t* counts, hipStream_t s) {
+    k_counts_out<<<1, 64, 0, s>>>(reinterpret_cast<const WsHeader*>(ws + L.hdr), max_pairs, counts);
+    return hipGetLastError();
+}
+
+hipError_t launch_counts_set(int64_t n_pairs, int64_t n_w, int64_t status, int64_t* counts, hipStream_t s) {
+    k_counts_set<<<1, 64, 0, s>>>(n_pairs, n_w, status, counts);
+    return hipGetLastError();
 }
 
 }  // namespace tre

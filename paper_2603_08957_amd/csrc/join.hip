@@ -54,8 +54,11 @@ __device__ inline uint64_t pack_row(const int32_t* row, const KeyDesc& d) {
     return k;
 }
 
-__global__ void k_validate(const int32_t* __restrict__ keys, int64_t n, int r, Radix rad, int32_t* err) {
+// (dn: the tuple count on the device, at most n; null: n)
+__global__ void k_validate(const int32_t* __restrict__ keys, int64_t n, int r, Radix rad, int32_t* err,
+                           const int64_t* __restrict__ dn) {
     const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (dn) n = min(n, *dn);
     if (i >= n) return;
     int flags = 0;
     const int32_t* row = keys + i * r;
@@ -613,10 +616,13 @@ __global__ __launch_bounds__(kSmallThreads) void k_join_small(
 // (e.g. T keyed k times a whole weight matrix): every U tuple is one pair and
 // its own group, in U order, so the pair list and the segments are written
 // directly and the counts are known on the host.
+// (n_dev: U's tuple count on the device, at most n_u; null: n_u)
 __global__ void k_keyed_by_u(const int32_t* __restrict__ ukeys, int64_t n_u, int ru, WDesc wd,
                              int32_t* __restrict__ pu, int32_t* __restrict__ pv, int32_t* __restrict__ seg_start,
-                             uint64_t* __restrict__ seg_key, WsHeader* __restrict__ hdr) {
+                             uint64_t* __restrict__ seg_key, WsHeader* __restrict__ hdr,
+                             const int64_t* __restrict__ n_dev) {
     const int64_t u = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (n_dev) n_u = max<int64_t>(0, min(n_u, *n_dev));
     if (u > n_u) return;
     seg_start[u] = int32_t(u);
     if (u == n_u) {
@@ -776,11 +782,11 @@ KeyDesc desc_v(const Plan& p) {
 }  // namespace
 
 hipError_t launch_validate(const int32_t* keys, int64_t n, int r, const int32_t* radix, int32_t* err_flag,
-                           hipStream_t s) {
+                           hipStream_t s, const int64_t* dn) {
     if (n <= 0 || r == 0) return hipSuccess;  // r == 0: at most one tuple, checked on the host
     Radix rad{};
     for (int a = 0; a < r; a++) rad.r[a] = radix[a];
-    k_validate<<<blocks_for(n), kThreads, 0, s>>>(keys, n, r, rad, err_flag);
+    k_validate<<<blocks_for(n), kThreads, 0, s>>>(keys, n, r, rad, err_flag, dn);
     return hipGetLastError();
 }
 
@@ -1020,7 +1026,8 @@ bool keyed_by_u(const Plan& p) {
     return true;
 }
 
-hipError_t launch_keyed_by_u(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, hipStream_t s) {
+hipError_t launch_keyed_by_u(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, hipStream_t s,
+                             const int64_t* n_dev) {
     WDesc wd{};
     wd.n = p.nk[2];
     for (int c = 0; c < p.nk[2]; c++) {
@@ -1031,7 +1038,7 @@ hipError_t launch_keyed_by_u(const Plan& p, const Layout& L, char* ws, const int
     k_keyed_by_u<<<blocks_for(L.n_u + 1), kThreads, 0, s>>>(
         u_keys, L.n_u, p.nk[0], wd, reinterpret_cast<int32_t*>(ws + L.pu), reinterpret_cast<int32_t*>(ws + L.pv),
         reinterpret_cast<int32_t*>(ws + L.seg_start), reinterpret_cast<uint64_t*>(ws + L.seg_key),
-        reinterpret_cast<WsHeader*>(ws + L.hdr));
+        reinterpret_cast<WsHeader*>(ws + L.hdr), n_dev);
     return hipGetLastError();
 }
 

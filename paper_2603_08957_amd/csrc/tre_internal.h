@@ -187,7 +187,7 @@ hipError_t radix_sort_u32_pairs(uint32_t* keys, uint64_t* vals, uint32_t* keys_a
 
 // join.hip
 hipError_t launch_validate(const int32_t* keys, int64_t n, int r, const int32_t* radix, int32_t* err_flag,
-                           hipStream_t s);
+                           hipStream_t s, const int64_t* dn = nullptr);
 hipError_t launch_join(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
                        hipStream_t s, int stage);
 // A V-driven join where U's key is the join labels and U holds every key of
@@ -207,7 +207,8 @@ hipError_t launch_join_small(const Plan& p, const Layout& L, char* ws, const int
 // V without promoted labels (one tuple) and W keyed by U's key as it is:
 // every U tuple is one pair and one group, written without counting
 bool keyed_by_u(const Plan& p);
-hipError_t launch_keyed_by_u(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, hipStream_t s);
+hipError_t launch_keyed_by_u(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, hipStream_t s,
+                             const int64_t* n_dev = nullptr);
 // GROUP BY stage: the pair count is read on the device from the workspace
 // header (written by launch_join), clamped to the capacity `cap` (at most
 // L.max_pairs) that every grid is sized for, so the host launches it
@@ -219,8 +220,11 @@ hipError_t launch_group(const Plan& p, const Layout& L, char* ws, const int32_t*
 hipError_t launch_tables(const Plan& p, int32_t* tables, hipStream_t s);
 // longest_first: reorder the units by decreasing length (GEMM class, at most
 // a few thousand units) for a dispatch in that order
+// dev_counts: n_pairs and n_w are upper bounds and the kernels read the
+// join's counts from the workspace header (no read-back before the launch;
+// one-workgroup unit tables or one unit per key only)
 hipError_t launch_units(const Plan& p, const Layout& L, char* ws, int64_t n_pairs, int64_t n_w, int64_t p_unit,
-                        bool longest_first, hipStream_t s);
+                        bool longest_first, hipStream_t s, bool dev_counts = false);
 // U-range units: unit r * n_w + s holds the pairs of key s whose U index lies
 // in [r * n_u / R, (r + 1) * n_u / R); its partial tile is slot s * R + r.
 hipError_t launch_range_units(const Plan& p, const Layout& L, char* ws, int64_t n_w, int64_t n_u, int32_t R,
@@ -238,7 +242,9 @@ hipError_t launch_gemm_paced(const Plan& p, const Layout& L, char* ws, const voi
 hipError_t launch_reduce(const Plan& p, const Layout& L, char* ws, float* w_tiles, int64_t split_bound,
                          hipStream_t s);
 hipError_t launch_write_outputs(const Plan& p, const Layout& L, char* ws, int32_t* w_keys, int32_t* pairs_out,
-                                int64_t n_pairs, int64_t n_w, hipStream_t s);
+                                int64_t n_pairs, int64_t n_w, hipStream_t s, bool dev_counts = false);
+hipError_t launch_counts_out(const Layout& L, char* ws, int64_t max_pairs, int64_t* counts, hipStream_t s);
+hipError_t launch_counts_set(int64_t n_pairs, int64_t n_w, int64_t status, int64_t* counts, hipStream_t s);
 
 // glue.hip
 hipError_t launch_cast_bf16(const float* x, uint16_t* y, int64_t n, hipStream_t s);

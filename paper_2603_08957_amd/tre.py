@@ -33,7 +33,7 @@ EXPORTS = [
     "tre_stack_workspace_bytes", "tre_stack_rows",
     "tre_tiles_from_entries", "tre_status_str", "tre_last_error", "tre_version",
     "tre_repartition_workspace_bytes", "tre_repartition", "tre_execute3_workspace_bytes", "tre_execute3",
-    "tre_noalloc_scratch_bytes", "tre_execute_noalloc",
+    "tre_noalloc_scratch_bytes", "tre_execute_noalloc", "tre_output_bounds", "tre_execute_async",
 ]
 
 
@@ -110,6 +110,8 @@ def lib():
         L.tre_join_keys.argtypes = [P, P, P, i64, P]
         L.tre_contract.argtypes = [P, P, P, P, P, i64, P, P, i64, P, P]
         L.tre_execute.argtypes = [P, P, i64, P, P, i64, P, P, P, i64, P, P, i64, P, P, sz, P, P]
+        L.tre_output_bounds.argtypes = [P, i64, i64, sz, P, P, P]
+        L.tre_execute_async.argtypes = [P, P, i64, P, P, P, i64, P, P, P, i64, P, i64, P, P, sz, P, P]
         L.tre_timing_read.argtypes = [P]
         L.tre_cast_f32_bf16.argtypes = [P, P, i64, P]
         L.tre_scale_f32.argtypes = [P, P, i64, ctypes.c_float, P]
@@ -262,6 +264,31 @@ def execute(plan: Plan, u_keys, u_tiles, v_keys, v_tiles, w_keys, w_tiles, ws, p
         err.n_w, err.n_pairs = int(n_w.value), int(n_p.value)
         raise err
     return int(n_w.value), int(n_p.value)
+
+
+def output_bounds(plan: Plan, n_u: int, n_v: int, ws_bytes: int):
+    """tre_output_bounds: (pair bound, key bound, whether tre_execute_async
+    runs without a read-back for these sizes)."""
+    pb, kb, ok = ctypes.c_int64(0), ctypes.c_int64(0), ctypes.c_int32(0)
+    _check(lib().tre_output_bounds(plan.handle, int(n_u), int(n_v), int(ws_bytes), ctypes.byref(pb), ctypes.byref(kb),
+                                   ctypes.byref(ok)), "tre_output_bounds")
+    return int(pb.value), int(kb.value), bool(ok.value)
+
+
+def execute_async(plan: Plan, u_keys, u_tiles, v_keys, v_tiles, w_keys, w_tiles, ws, counts, pairs_out=None,
+                  n_u=None, n_u_dev=None, stream=None, timing: Timing | None = None):
+    """tre_execute_async: join and contraction enqueued with no wait; the
+    counts ([pairs, keys, status, 0]) land in ``counts`` (device int64 [4]).
+    ``n_u`` defaults to u_tiles' rows; ``n_u_dev`` (a device int64 tensor)
+    holds U's actual count when n_u is only a bound."""
+    n_u = int(u_tiles.shape[0]) if n_u is None else int(n_u)
+    n_v = int(v_tiles.shape[0])
+    rc = lib().tre_execute_async(plan.handle, _ptr(u_keys), n_u, _ptr(n_u_dev), _ptr(u_tiles), _ptr(v_keys), n_v,
+                                 _ptr(v_tiles), _ptr(w_keys), _ptr(w_tiles),
+                                 int(w_tiles.shape[0]) if w_tiles is not None else 0, _ptr(pairs_out),
+                                 int(pairs_out.shape[0]) if pairs_out is not None else 0, _ptr(counts), _ptr(ws),
+                                 ws.numel(), _stream(stream), ctypes.byref(timing) if timing is not None else None)
+    _check(rc, "tre_execute_async")
 
 
 @dataclass

@@ -1071,3 +1071,151 @@ def test_small_join_limit_gpu(orc, n):
     ref = orc.run(orc_plan(orc, spec), U, V)
     check(out, ref, "f32")
     assert out.n_pairs == n
+
+
+# ------------------------------------------------- tre_execute_async
+
+def _execute_async(spec, U, V, w_cap=None, pair_cap=None, max_pairs=None, **plan_kw):
+    """tre_execute_async into buffers sized by tre_output_bounds; returns
+    (output namespace built from the device counts, counts, async_ok)."""
+    import types
+
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    plan = tre.Plan.from_spec(spec, **plan_kw)
+    uk, ut = to_dev(U)
+    vk, vt = to_dev(V)
+    n_u, n_v = len(U["keys"]), len(V["keys"])
+    mp = max(n_u * n_v, 1) if max_pairs is None else max_pairs
+    ws = tre.alloc_workspace(plan.workspace_bytes(n_u, n_v, mp))
+    pb, kb, ok = tre.output_bounds(plan, n_u, n_v, ws.numel())
+    kc = kb if w_cap is None else w_cap
+    pc = pb if pair_cap is None else pair_cap
+    wk = torch.empty((max(kc, 1), max(plan.key_arity[2], 1)), dtype=torch.int32, device="cuda")
+    wt = torch.empty((max(kc, 1), plan.tile_elems[2]), dtype=torch.float32, device="cuda")
+    pairs = torch.empty((max(pc, 1), 2), dtype=torch.int32, device="cuda")
+    counts = torch.full((4,), -1, dtype=torch.int64, device="cuda")
+    tre.execute_async(plan, uk, ut, vk, vt, wk if plan.key_arity[2] else None, wt, ws, counts, pairs_out=pairs)
+    c = counts.cpu().tolist()
+    n_p, n_w = int(c[0]), int(c[1])
+    keys = wk[:n_w] if plan.key_arity[2] else wk[:n_w, :0]
+    out = types.SimpleNamespace(w_keys=keys, w_tiles=wt[:n_w], n_w=n_w, n_pairs=n_p, pairs=pairs[:n_p])
+    return out, c, ok
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_execute_async_random_plans_gpu(orc, seed):
+    """tre_execute_async on random plans (most sizes run with no read-back;
+    the others through tre_execute): counts from device memory, pair lists
+    and key sets bit for bit against the oracle, values within the
+    tolerance."""
+    rng = np.random.default_rng(8100 + seed)
+    e, upper, ext, til = random_plan(rng)
+    u_lab, v_lab, _ = split_einsum(e)
+    U = workloads.random_relation(rng, u_lab, upper, ext, til, "f32", keep=0.6, zero_frac=0.3)
+    V = workloads.random_relation(rng, v_lab, upper, ext, til, "f32", keep=0.6, zero_frac=0.3)
+    spec = workloads.spec(e, upper, ext, til, "f32")
+    if len(U["keys"]) == 0 or len(V["keys"]) == 0:
+        return
+    out, c, ok = _execute_async(spec, U, V, validate=bool(seed % 2))
+    say("execute async", seed, e, upper, til, len(U["keys"]), len(V["keys"]), c, ok)
+    assert c[2] == 0 and c[3] == 0
+    ref = orc.run(orc_plan(orc, spec), U, V)
+    check(out, ref, "f32")
+
+
+def test_execute_async_chain_gpu(orc):
+    """The 4096-vertex chain with no host wait: E1 asynchronously, then E2 on
+    E1's output buffers with U's count taken from E1's device counts; both
+    against the synchronous calls (bit for bit: the bounds are the counts
+    here) and E2 against the oracle on E1's output."""
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    w = workloads.config(1, "small")
+    p1 = tre.Plan.from_spec(w["E1"], validate=False)
+    p2 = tre.Plan.from_spec(w["E2"], validate=False)
+    xk, xt = to_dev(w["X"])
+    yk, yt = to_dev(w["Y"])
+    zk, zt = to_dev(w["Z"])
+    n_x, n_y = len(w["X"]["keys"]), len(w["Y"]["keys"])
+    ws1 = tre.alloc_workspace(p1.workspace_bytes(n_x, n_y, n_y))
+    pb1, kb1, ok1 = tre.output_bounds(p1, n_x, n_y, ws1.numel())
+    assert ok1
+    t_k = torch.empty((kb1, p1.key_arity[2]), dtype=torch.int32, device="cuda")
+    t_t = torch.empty((kb1, p1.tile_elems[2]), dtype=torch.float32, device="cuda")
+    c1 = torch.zeros(4, dtype=torch.int64, device="cuda")
+    ws2 = tre.alloc_workspace(p2.workspace_bytes(kb1, 1, kb1))
+    pb2, kb2, ok2 = tre.output_bounds(p2, kb1, 1, ws2.numel())
+    assert ok2 and kb2 == kb1
+    o_k = torch.empty((kb2, p2.key_arity[2]), dtype=torch.int32, device="cuda")
+    o_t = torch.empty((kb2, p2.tile_elems[2]), dtype=torch.float32, device="cuda")
+    c2 = torch.zeros(4, dtype=torch.int64, device="cuda")
+    for _ in range(3):  # back to back, no host wait
+        tre.execute_async(p1, xk, xt, yk, yt, t_k, t_t, ws1, c1)
+        tre.execute_async(p2, t_k, t_t, zk, zt, o_k, o_t, ws2, c2, n_u=kb1, n_u_dev=c1[1:2])
+    torch.cuda.synchronize()
+    cc1, cc2 = c1.cpu().tolist(), c2.cpu().tolist()
+    say("chain counts", cc1, cc2)
+    assert cc1[2] == 0 and cc2[2] == 0 and cc2[0] == cc2[1] == cc1[1]
+    n_t = cc1[1]
+    # synchronous reference on the same inputs
+    s1 = tre.einsum(p1, xk, xt, yk, yt)
+    assert torch.equal(s1.w_keys, t_k[:n_t]) and torch.equal(s1.w_tiles, t_t[:n_t])
+    s2 = tre.einsum(p2, s1.w_keys, s1.w_tiles, zk, zt)
+    assert torch.equal(s2.w_keys, o_k[:n_t]) and torch.equal(s2.w_tiles, o_t[:n_t])
+    T = {"keys": s1.w_keys.cpu().numpy(), "tiles": s1.w_tiles.cpu().numpy(), "dtype": "f32"}
+    ref = orc.run(orc_plan(orc, w["E2"]), T, w["Z"])
+    assert np.array_equal(o_k[:n_t].cpu().numpy().reshape(ref.wkeys.shape), ref.wkeys)
+    assert_values(o_t[:n_t].cpu().numpy(), ref.acc, ref.mag, "f32", "E2 async")
+
+
+def test_execute_async_errors_gpu():
+    """Errors of the asynchronous call: key errors and pairs beyond the
+    workspace come back in the device counts ([2]; [0] the pairs needed);
+    output capacity below the bounds and a device-side U count on a plan
+    that cannot take one are host errors; sizes beyond the device-count
+    launches run synchronously and still fill the counts."""
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    rng = np.random.default_rng(6)
+    e, upper, ext, til = "ij,jk->ik", "ijk", {"i": 64, "j": 64, "k": 64}, {"i": 8, "j": 8, "k": 8}
+    U = workloads.random_relation(rng, "ij", upper, ext, til, "f32", keep=0.3, zero_frac=0.0)
+    V = workloads.random_relation(rng, "jk", upper, ext, til, "f32", keep=0.3, zero_frac=0.0)
+    spec = workloads.spec(e, upper, ext, til, "f32")
+    out, c, ok = _execute_async(spec, U, V)
+    assert ok and c[2] == 0
+    n_pairs = c[0]
+    bad = dict(U)
+    bad["keys"] = np.ascontiguousarray(U["keys"][::-1])
+    bad["tiles"] = np.ascontiguousarray(U["tiles"][::-1])
+    _, c2, _ = _execute_async(spec, bad, V)
+    assert c2[2] == tre.tre.STATUS_CODE["TRE_E_UNSORTED"]
+    _, c3, _ = _execute_async(spec, U, V, max_pairs=n_pairs // 2)
+    assert c3[2] == tre.tre.STATUS_CODE["TRE_E_WORKSPACE"] and c3[0] == n_pairs
+    with pytest.raises(tre.TreError) as err:
+        _execute_async(spec, U, V, w_cap=1)
+    assert err.value.status == "TRE_E_CAPACITY"
+    plan = tre.Plan.from_spec(spec)
+    uk, ut = to_dev(U)
+    vk, vt = to_dev(V)
+    ws = tre.alloc_workspace(plan.workspace_bytes(len(uk), len(vk), len(uk) * len(vk)))
+    n_dev = torch.tensor([len(uk)], dtype=torch.int64, device="cuda")
+    counts = torch.zeros(4, dtype=torch.int64, device="cuda")
+    big = torch.empty((4096, 64), dtype=torch.float32, device="cuda")
+    bigk = torch.empty((4096, 2), dtype=torch.int32, device="cuda")
+    with pytest.raises(tre.TreError) as err:
+        tre.execute_async(plan, uk, ut, vk, vt, bigk, big, ws, counts, n_u_dev=n_dev)
+    assert err.value.status == "TRE_E_ARG"
+    # more than 4,096 output keys cut into units: synchronous, counts filled
+    ext2, til2 = {"i": 1 << 14, "k": 1 << 14, "a": 3}, {"i": 1, "k": 1}
+    U2 = _rel(rng, np.sort(rng.choice(1 << 14, 100, replace=False)), 3)
+    V2 = _rel(rng, np.sort(rng.choice(1 << 14, 100, replace=False)), 3)
+    spec2 = workloads.spec("ia,ka->ik", "ik", ext2, til2, "f32")
+    out2, c4, ok2 = _execute_async(spec2, U2, V2)
+    assert not ok2 and c4[2] == 0 and c4[0] == 10000 and c4[1] == 10000
