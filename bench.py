@@ -135,7 +135,8 @@ class Stage:
         the counts land in self.counts.  Returns the output buffers (rows up
         to the key bound; the first counts[1] are the output)."""
         self.tre.execute_async(self.plan, uk, ut, vk, vt, self.a_keys if self.plan.key_arity[2] else None,
-                               self.a_tiles, self.ws, self.counts, n_u=self.async_n_u, n_u_dev=n_u_dev, timing=timing)
+                               self.a_tiles, self.ws, self.counts, pairs_out=self.pairs_out, n_u=self.async_n_u,
+                               n_u_dev=n_u_dev, timing=timing)
         return self.a_keys, self.a_tiles
 
     def check_async(self):
@@ -303,7 +304,7 @@ class GnnChain:
         # with no stack between the EinSums and counts that the device-count
         # launches cover, the whole chain is enqueued with no host wait:
         # E2 takes U's count from E1's counts in device memory
-        self.async_ok = (ASYNC and self.stack == 1 and not self.bf and self.e1.prepare_async()
+        self.async_ok = (ASYNC and self.stack == 1 and self.e1.prepare_async()
                          and self.e2.prepare_async(n_u_bound=self.e1.async_keys_bound))
         torch.cuda.synchronize()
 

@@ -286,8 +286,8 @@ void join_timing(tre_timing* timing, int32_t path) {
 
 // tre_contract's launches, for the join's counts n_pairs and n_w.  With
 // `dev` those are upper bounds and every kernel reads the join's counts from
-// the workspace header (the caller has checked that the bounds need no
-// pacing, no U ranges, and a one-workgroup unit table or one unit per key).
+// the workspace header (the caller has checked that the bounds need no U
+// ranges and take a one-workgroup unit table or one unit per key).
 tre_status contract_enqueue(tre_plan_t plan, const tre_join_result* jr, int64_t n_pairs, int64_t n_w,
                             const void* u_tiles, const void* v_tiles, int32_t* w_keys, void* w_out,
                             int32_t* pairs_out, hipStream_t s, tre_timing* timing, bool dev = false) {
@@ -319,7 +319,7 @@ tre_status contract_enqueue(tre_plan_t plan, const tre_join_result* jr, int64_t 
     }
     tm.mark(s);
     const int64_t slots = (p.kclass == KC_GEMM && p.fast) ? gemm_paced_slots(p) : 0;
-    const int32_t pace = dev ? 0 : choose_pacing(p, jr->n_u, n_pairs, n_w, slots);
+    const int32_t pace = choose_pacing(p, jr->n_u, n_pairs, n_w, slots);
     const int32_t R = (pace || dev) ? 0 : choose_u_ranges(p, L, jr->n_u, n_pairs, n_w);
     const int64_t p_unit = (R > 1 || pace) ? n_pairs : choose_unit(p, L, n_pairs, n_w);
     hipError_t e;
@@ -384,7 +384,8 @@ tre_status contract_enqueue(tre_plan_t plan, const tre_join_result* jr, int64_t 
 // Upper bounds on a join's pair and output key counts, from the sizes alone
 // (exact when the host knows them), and whether the contraction can be
 // enqueued on them with the counts read on the device: no pacing and no U
-// ranges at the bounds, and a one-workgroup unit table or one unit per key.
+// ranges at the bounds, and a one-workgroup unit table or one unit per key
+// (the paced persistent grid takes one unit per key and reads their count).
 struct AsyncBounds {
     int64_t pairs = 0, keys = 0;
     bool ok = false;
@@ -406,8 +407,11 @@ AsyncBounds async_bounds(const Plan& p, int64_t n_u, int64_t n_v, int64_t max_pa
     }
     const Layout L = make_layout(p, n_u, n_v, max_pairs);
     const int64_t slots = (p.kclass == KC_GEMM && p.fast) ? gemm_paced_slots(p) : 0;
-    if (choose_pacing(p, n_u, b.pairs, b.keys, slots) != 0 || choose_u_ranges(p, L, n_u, b.pairs, b.keys) != 0)
+    if (choose_pacing(p, n_u, b.pairs, b.keys, slots) != 0) {
+        b.ok = true;  // one unit per key; the persistent grid reads the unit count on the device
         return b;
+    }
+    if (choose_u_ranges(p, L, n_u, b.pairs, b.keys) != 0) return b;
     const int64_t p_unit = choose_unit(p, L, b.pairs, b.keys);
     b.ok = b.keys <= kAsyncMaxKeys || p_unit >= b.pairs;
     return b;
