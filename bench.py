@@ -309,7 +309,10 @@ class GnnChain:
         torch.cuda.synchronize()
 
     def step(self, timing=None):
-        """E1's output keys are known once its join is done, so E2's join (and
+        """Without a stack, both EinSums go through tre_execute_async, back to
+        back on one stream with no host wait (E2 takes U's tuple count from
+        E1's device counts).  Otherwise E1's output keys are known once its
+        join is done, so E2's join (and
         the key-only stack of the per-vertex rows) runs on a second stream
         while E1's contraction runs; the cast and E2's contraction follow on
         the first.  The synchronous phase pass, a stack that has to move
