@@ -37,6 +37,9 @@ __device__ inline float ld_f(const uint16_t* p) { return __uint_as_float(uint32_
 
 // ---------------------------------------------------------------- tables
 
+// off[t] < 0: the plan's contraction kernel does not read table t (the
+// GEMM class reads the A/B/W tables, the vector class the E/K ones, the
+// 128x128 path none), so it is not written.
 struct TableSet {
     Dims d[T_COUNT];
     int64_t off[T_COUNT];
@@ -44,6 +47,7 @@ struct TableSet {
 
 __global__ void k_tables(TableSet ts, int32_t* __restrict__ out) {
     const int t = blockIdx.y;
+    if (ts.off[t] < 0) return;
     const Dims& d = ts.d[t];
     int64_t cnt = 1;
     for (int i = 0; i < d.n; i++) cnt *= d.size[i];
@@ -157,6 +161,7 @@ __global__ __launch_bounds__(kOrderBins) void k_order_units(Unit* __restrict__ u
 constexpr int kUnitsThreads = kOrderBins;
 constexpr int kUnitsPer = kOrderMax / kUnitsThreads;
 constexpr int64_t kUnitsTableMax = 16384;
+static_assert(kUnitsTableMax < (1 << 16) && T_COUNT * kMaxDims <= kUnitsThreads, "table set-up in k_units_small");
 
 // part_off[s]: the first partial slot of key s (n_w + 1 entries; k_reduce
 // sums slots part_off[s] .. part_off[s + 1] - 1 of each split key).
@@ -178,22 +183,49 @@ __global__ __launch_bounds__(kUnitsThreads) void k_units_small(const int32_t* __
         constexpr int kWords = int(sizeof(TableSet) / sizeof(int32_t));
         static_assert(sizeof(TableSet) % sizeof(int64_t) == 0, "TableSet words");
         __shared__ int64_t s_ts_raw[sizeof(TableSet) / sizeof(int64_t)];
+        __shared__ uint32_t s_magic[T_COUNT][kMaxDims];
+        __shared__ int32_t s_first[T_COUNT + 1];
         for (int i = t; i < kWords; i += kUnitsThreads)
             reinterpret_cast<int32_t*>(s_ts_raw)[i] = reinterpret_cast<const int32_t*>(&ts)[i];
         __syncthreads();
         const TableSet& s_ts = *reinterpret_cast<const TableSet*>(s_ts_raw);
-        for (int k = 0; k < T_COUNT; k++) {
-            const Dims& d = s_ts.d[k];
-            int32_t c = 1;
-            for (int i = 0; i < d.n; i++) c *= d.size[i];
-            for (int32_t x = t; x < c; x += kUnitsThreads) {
-                int32_t rem = x, o = 0;
-                for (int i = d.n - 1; i >= 0; i--) {
-                    o += (rem % d.size[i]) * d.stride[i];
-                    rem /= d.size[i];
-                }
-                tables[s_ts.off[k] + x] = o;
+        // Every used table holds at most kUnitsTableMax < 2^16 entries, so
+        // an index and every size are below 2^16, and x / d = umulhi(x, m)
+        // with m = ceil(2^32 / d) exactly (x * (m d - 2^32) < 2^32); m = 0
+        // stands for d <= 1.
+        if (t < T_COUNT * kMaxDims) {
+            const int k = t / kMaxDims, i = t % kMaxDims;
+            const uint32_t d = i < s_ts.d[k].n ? uint32_t(s_ts.d[k].size[i]) : 1u;
+            s_magic[k][i] = d > 1 ? 0xffffffffu / d + 1u : 0u;
+        }
+        if (t == 0) {
+            // the used tables' entries, numbered one after another
+            int32_t f = 0;
+            for (int k = 0; k < T_COUNT; k++) {
+                s_first[k] = f;
+                if (s_ts.off[k] < 0) continue;
+                int32_t c = 1;
+                for (int i = 0; i < s_ts.d[k].n; i++) c *= s_ts.d[k].size[i];
+                f += c;
             }
+            s_first[T_COUNT] = f;
+        }
+        __syncthreads();
+        const int32_t total = s_first[T_COUNT];
+        for (int32_t x = t; x < total; x += kUnitsThreads) {
+            int k = 0;
+            while (x >= s_first[k + 1]) k++;
+            const Dims& d = s_ts.d[k];
+            const int32_t xi = x - s_first[k];
+            uint32_t rem = uint32_t(xi);
+            int32_t o = 0;
+            for (int i = d.n - 1; i >= 0; i--) {
+                const uint32_t m = s_magic[k][i];
+                const uint32_t q = m ? __umulhi(rem, m) : rem;
+                o += int32_t(rem - q * uint32_t(d.size[i])) * d.stride[i];
+                rem = q;
+            }
+            tables[s_ts.off[k] + xi] = o;
         }
     }
     int32_t nu[kUnitsPer], a0[kUnitsPer], su = 0, sp = 0, ss = 0;
@@ -817,13 +849,22 @@ hipError_t gemm_dispatch(const Plan& p, const GemmArgs& g, dim3 grid, int64_t n_
 
 namespace {
 
+// Whether the plan's contraction kernel reads offset table t.
+bool table_used(const Plan& p, int t) {
+    if (p.kclass == KC_VEC) return t >= T_EU;
+    return !p.fast && t < T_EU;
+}
+
+// The tables the contraction reads (the others marked off = -1), their
+// largest and total entry counts.
 TableSet table_set(const Plan& p, int64_t* largest, int64_t* total) {
     TableSet ts{};
-    *largest = 1;
+    *largest = 0;
     *total = 0;
     for (int t = 0; t < T_COUNT; t++) {
         ts.d[t] = p.dims[t];
-        ts.off[t] = p.table_off[t];
+        ts.off[t] = table_used(p, t) ? p.table_off[t] : -1;
+        if (ts.off[t] < 0) continue;
         *largest = std::max<int64_t>(*largest, p.dims[t].count());
         *total += p.dims[t].count();
     }
@@ -835,6 +876,7 @@ TableSet table_set(const Plan& p, int64_t* largest, int64_t* total) {
 hipError_t launch_tables(const Plan& p, int32_t* tables, hipStream_t s) {
     int64_t mx, total;
     const TableSet ts = table_set(p, &mx, &total);
+    if (total == 0) return hipSuccess;
     const unsigned gx = unsigned(std::min<int64_t>((mx + kThreads - 1) / kThreads, 1024));
     k_tables<<<dim3(gx, T_COUNT), kThreads, 0, s>>>(ts, tables);
     return hipGetLastError();
@@ -876,8 +918,8 @@ hipError_t launch_units(const Plan& p, const Layout& L, char* ws, int64_t n_pair
         // the tables too, when small (one launch for both)
         int64_t mx, total;
         const TableSet ts = table_set(p, &mx, &total);
-        const bool with_tables = total <= kUnitsTableMax;
-        if (!with_tables && (e = launch_tables(p, tables, s)) != hipSuccess) return e;
+        const bool with_tables = total > 0 && total <= kUnitsTableMax;
+        if (total > kUnitsTableMax && (e = launch_tables(p, tables, s)) != hipSuccess) return e;
         k_units_small<<<1, kUnitsThreads, 0, s>>>(seg_start, n_w, std::max<int64_t>(p_unit, 1),
                                                    longest_first && p.kclass == KC_GEMM ? 1 : 0,
                                                    reinterpret_cast<Unit*>(ws + L.unit_desc),
