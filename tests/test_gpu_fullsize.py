@@ -115,7 +115,7 @@ def sampled_check(orc, spec, U, V, out, S, u_tiles_host=True, pairs=None):
     gk = out.w_keys.cpu().numpy().reshape(out.n_w, -1)
     index = {tuple(r): i for i, r in enumerate(gk.tolist())}
     rows = [index[tuple(r)] for r in S.tolist()]
-    got = out.w_tiles[rows].cpu().numpy()
+    got = out.w_tiles[rows].float().cpu().numpy()  # (bf16 outputs upcast exactly)
     f = assert_values(got, acc, mag, spec["dtype"], "sampled keys")
     say(f"sampled keys: {f}")
     return f["mag_rel"]

@@ -180,11 +180,13 @@ def torch_f32():
     return torch.float32
 
 
-def test_paced_rounds_gpu(orc):
+@pytest.mark.parametrize("dtype,w_bf16", [("bf16", False), ("bf16", True), ("f32", False)])
+def test_paced_rounds_gpu(orc, dtype, w_bf16):
     """More keys than resident workgroups (512 on 256 CUs): the paced kernel
-    deals whole keys in rounds, the last one partial.  Each key is still
-    summed by one workgroup in pair order, so the result equals the
-    one-unit-per-key launch bit for bit, and sampled keys match the oracle."""
+    deals whole keys in rounds, the last one partial; bf16 and fp32 inputs,
+    and bf16 output.  Each key is still summed by one workgroup in pair
+    order, so the result equals the one-unit-per-key launch bit for bit, and
+    sampled keys match the oracle."""
     import torch
 
     from test_gpu_fullsize import sampled_check
@@ -193,17 +195,18 @@ def test_paced_rounds_gpu(orc):
     nk = 512 * 3 + 77
     ext, til = {"i": 128, "j": 128 * 3, "k": 128 * nk}, {"j": 128, "k": 128}
     rng = np.random.default_rng(4242)
-    U = workloads.random_relation(rng, "ij", upper, ext, til, "bf16", keep=1.0)
-    V = workloads.random_relation(rng, "jk", upper, ext, til, "bf16", keep=0.7)
-    spec = workloads.spec(e, upper, ext, til, "bf16")
-    say("paced rounds", len(U["keys"]), len(V["keys"]))
-    _, paced = gpu_run(spec, U, V, pace_windows=2)
-    _, whole = gpu_run(spec, U, V, pace_windows=-1, u_ranges=-1, max_pairs_per_unit=1 << 20)
+    U = workloads.random_relation(rng, "ij", upper, ext, til, dtype, keep=1.0)
+    V = workloads.random_relation(rng, "jk", upper, ext, til, dtype, keep=0.7)
+    spec = workloads.spec(e, upper, ext, til, dtype)
+    say("paced rounds", dtype, w_bf16, len(U["keys"]), len(V["keys"]))
+    _, paced = gpu_run(spec, U, V, pace_windows=2, w_bf16=w_bf16)
+    _, whole = gpu_run(spec, U, V, pace_windows=-1, u_ranges=-1, max_pairs_per_unit=1 << 20, w_bf16=w_bf16)
     torch.cuda.synchronize()
     assert 3 * 512 < paced.n_w < 4 * 512, paced.n_w
     assert paced.n_w == whole.n_w and torch.equal(paced.w_keys, whole.w_keys)
     assert torch.equal(paced.pairs, whole.pairs)
-    assert torch.equal(paced.w_tiles.view(torch.int32), whole.w_tiles.view(torch.int32)), "paced result differs"
+    assert torch.equal(paced.w_tiles.view(torch.int16 if w_bf16 else torch.int32),
+                       whole.w_tiles.view(torch.int16 if w_bf16 else torch.int32)), "paced result differs"
     wk = paced.w_keys.cpu().numpy().reshape(paced.n_w, -1)
     S = wk[np.sort(rng.choice(paced.n_w, 12, replace=False))]
     sampled_check(orc, spec, U, V, paced, S, pairs=paced.pairs.cpu().numpy())
