@@ -304,19 +304,48 @@ __global__ __launch_bounds__(kUnitsThreads) void k_units_small(const int32_t* __
     if (!in_lds) return;
     // longest first (unit lengths capped at kOrderBins - 1; order within a
     // length class is free: a unit's sum does not depend on when it runs)
+    // (units mostly share one or two lengths, and LDS atomics on one
+    // address serialise: the lanes of a wavefront with the leading lane's
+    // length take one atomic together, twice; any lanes left take one each)
     auto bin = [](const Unit& u) { return kOrderBins - 1 - min(u.p1 - u.p0, kOrderBins - 1); };
+    const int lane = t & 63;
+    const uint64_t below = (uint64_t(1) << lane) - 1;
+    // counting pass (place false): adds the lane to its bin's count;
+    // placing pass: returns the lane's slot from its bin's running start
+    auto wave_rank = [&](bool valid, int b, bool place) {
+        uint64_t todo = __ballot(valid);
+        int32_t rank = 0;
+        for (int round = 0; round < 2 && todo; round++) {
+            const int leader = __ffsll((unsigned long long)todo) - 1;
+            const int lb = __shfl(b, leader, 64);
+            const uint64_t m = __ballot(valid && b == lb);
+            int32_t base = 0;
+            if (lane == leader) base = atomicAdd(&cnt[lb], __popcll(m));
+            base = __shfl(base, leader, 64);
+            if (valid && b == lb) rank = base + __popcll(m & below);
+            todo &= ~m;
+        }
+        if ((todo >> lane) & 1) rank = atomicAdd(&cnt[b], 1);
+        return place ? rank : 0;
+    };
     cnt[t] = 0;
     __syncthreads();
-    for (int i = t; i < n_units; i += kUnitsThreads) atomicAdd(&cnt[bin(buf[i])], 1);
+    for (int i0 = t - lane; i0 < n_units; i0 += kUnitsThreads) {
+        const int i = i0 + lane;
+        (void)wave_rank(i < n_units, i < n_units ? bin(buf[i]) : 0, false);
+    }
     __syncthreads();
     int32_t total;
     const int32_t start = block_scan_excl<kUnitsThreads>(cnt[t], wsum, &total);
     __syncthreads();
     cnt[t] = start;
     __syncthreads();
-    for (int i = t; i < n_units; i += kUnitsThreads) {
-        const Unit u = buf[i];
-        units[atomicAdd(&cnt[bin(u)], 1)] = u;
+    for (int i0 = t - lane; i0 < n_units; i0 += kUnitsThreads) {
+        const int i = i0 + lane;
+        const bool valid = i < n_units;
+        const Unit u = valid ? buf[i] : Unit{};
+        const int32_t r = wave_rank(valid, valid ? bin(u) : 0, true);
+        if (valid) units[r] = u;
     }
 }
 
