@@ -321,7 +321,10 @@ tre_status contract_enqueue(tre_plan_t plan, const tre_join_result* jr, int64_t 
     const int64_t slots = (p.kclass == KC_GEMM && p.fast) ? gemm_paced_slots(p) : 0;
     const int32_t pace = choose_pacing(p, jr->n_u, n_pairs, n_w, slots);
     const int32_t R = (pace || dev) ? 0 : choose_u_ranges(p, L, jr->n_u, n_pairs, n_w);
-    const int64_t p_unit = (R > 1 || pace) ? n_pairs : choose_unit(p, L, n_pairs, n_w);
+    // (a keyless one-tuple V with W keyed by U: one pair per key, nothing
+    // to cut and no partial tiles to sum)
+    const bool one_pair_keys = jr->n_v <= 1 && keyed_by_u(p);
+    const int64_t p_unit = (R > 1 || pace || one_pair_keys) ? n_pairs : choose_unit(p, L, n_pairs, n_w);
     hipError_t e;
     // (launch_units writes the tile offset tables itself)
     if (R > 1) {
