@@ -42,6 +42,7 @@ PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}
 METRIC = "effective tile GFLOP/s + join/reduce HBM GB/s per EinSum, 1 MI355X"
 PLAN_OPTIONS = {}  # extra tre_options for every EinSum (set from the command line)
 WARMUP_MIN_S = 0.25  # warm-up continues past --warmup steps until this much wall time has run
+MIN_TIMED_S, MAX_CFG_STEPS = 0.02, 100  # timed work of a short non-headline workload (steps capped)
 ASYNC = True  # workloads whose counts the device-count launches cover run tre_execute_async (--sync: never)
 WARMUP_MAX_STEPS = 4000
 SETTLE_S, SETTLE_S_PER_GIB = 0.5, 0.03  # pause after a workload's inputs are built
@@ -1089,8 +1090,7 @@ def measure(W, args, torch, tre, config, cpu_budget_s):
     # W warm-up steps, and for short steps more of them until about a
     # quarter of a second has run, so the clocks have ramped before the
     # timed steps (a 0.15 ms step measured 10-20% slower in its first
-    # hundred repetitions); the last warm-up step passes the timed steps'
-    # timing too, so their events and launch path are warm as well
+    # hundred repetitions)
     t_warm = time.perf_counter()
     n_warm = 0
     while n_warm < args.warmup or (args.warmup > 0 and time.perf_counter() - t_warm < WARMUP_MIN_S
@@ -1099,21 +1099,38 @@ def measure(W, args, torch, tre, config, cpu_budget_s):
         n_warm += 1
         if n_warm % 32 == 0:
             torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    warm_s = time.perf_counter() - t_warm
+    # the headline times exactly --steps steps; a workload of short steps
+    # times more of them (about MIN_TIMED_S of work, at most MAX_CFG_STEPS), so
+    # that one slow step does not carry its mean
+    steps = args.steps
+    if config != HEADLINE and n_warm > 0:
+        steps = max(steps, min(MAX_CFG_STEPS, int(MIN_TIMED_S / max(warm_s / n_warm, 1e-6))))
     if args.warmup > 0:
-        tm = tre.Timing()
-        tm.deferred = 1
-        W.step(timing=tm)
-        tm.read()
-        n_warm += 1
+        # as many warm-up steps with the timed steps' deferred timing, read
+        # afterwards, so the library's event pool holds the events the timed
+        # steps take (events created inside the timed region once coincided
+        # with one step running 15x slower)
+        warm_t = []
+        for _ in range(steps):
+            tm = tre.Timing()
+            tm.deferred = 1
+            W.step(timing=tm)
+            warm_t.append(tm)
+        torch.cuda.synchronize()
+        for tm in warm_t:
+            tm.read()
+        n_warm += steps
     torch.cuda.synchronize()
     stages = W.stages()
     dom = stages[0]
     timings = []
-    log(f"[bench] config {config}: timing {args.steps} steps")
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    log(f"[bench] config {config}: timing {steps} steps")
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     t0 = time.perf_counter()
     evs[0].record()
-    for i in range(args.steps):
+    for i in range(steps):
         tm = tre.Timing()
         tm.deferred = 1
         W.step(timing=tm)
@@ -1123,8 +1140,8 @@ def measure(W, args, torch, tre, config, cpu_budget_s):
     wall = time.perf_counter() - t0
     if hasattr(W, "check_async"):
         W.check_async()  # the asynchronous steps' counts and status, read after the timed region
-    per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
-    ms_step = evs[0].elapsed_time(evs[-1]) / args.steps
+    per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(steps)]
+    ms_step = evs[0].elapsed_time(evs[-1]) / steps
     for tm in timings:
         tm.read()
     contract_ms = float(np.mean([t.contract_ms for t in timings]))
@@ -1175,7 +1192,7 @@ def measure(W, args, torch, tre, config, cpu_budget_s):
         cpu = W.oracle_sample(oracle, cpu_budget_s)
         cpu.pop("seconds", None)
         cpu["host"] = host_facts()
-    rep = {"config": config, "workload": W.describe(), "dtype": dtype, "steps": args.steps, "warmup": args.warmup,
+    rep = {"config": config, "workload": W.describe(), "dtype": dtype, "steps": steps, "warmup": args.warmup,
            "warmup_steps_run": n_warm,
            "host_waits": "none (tre_execute_async)" if getattr(W, "async_ok", False) else "one count read-back per EinSum",
            "ms_per_step": ms_step, "ms_per_step_median": float(np.median(per_step)),
