@@ -186,3 +186,33 @@ def test_binding_structs_match_the_header(tre, tmp_path):
         assert got[(cname, "size")] == ctypes.sizeof(cls), cname
         for f, _ in cls._fields_:
             assert got[(cname, f)] == getattr(cls, f).offset, (cname, f)
+
+
+def test_output_bounds_closed_forms(tre):
+    """tre_output_bounds (host only) against the bounds it promises: one pair
+    per V tuple when U's key is the join labels, the cross product
+    otherwise, the pair capacity of the workspace, W's key space, n_u for a
+    keyless one-tuple V with W keyed by U, zero pairs for an empty side, and
+    TRE_E_WORKSPACE below the smallest workspace."""
+    ws_of = lambda p, n_u, n_v, mp: p.workspace_bytes(n_u, n_v, mp)  # noqa: E731
+    # U keyed (J) = the join labels: a V tuple meets at most one U tuple
+    a = tre.Plan("ij,jk->ki", "jk", {"i": 64, "j": 64 * 8, "k": 64 * 16}, {"j": 64, "k": 64})
+    assert tre.output_bounds(a, 8, 50, ws_of(a, 8, 50, 1000)) == (50, 16, True)  # keys: 16 K blocks
+    # a workspace sized for 20 pairs caps the pair bound at its capacity
+    ws20 = ws_of(a, 8, 50, 20)
+    pb, kb, ok = tre.output_bounds(a, 8, 50, ws20)
+    assert 20 <= pb <= 50 and kb == min(pb, 16) and ok
+    assert pb == 50 or ws_of(a, 8, 50, pb + 1) > ws20
+    # neither key is made of join labels only: the cross product
+    b = tre.Plan("ij,jk->ik", "ijk", {"i": 64 * 3, "j": 64 * 4, "k": 64 * 5}, {"i": 64, "j": 64, "k": 64})
+    assert tre.output_bounds(b, 5, 7, ws_of(b, 5, 7, 1000)) == (35, 15, True)  # keys: 3 x 5 (I, K) blocks
+    assert tre.output_bounds(b, 5, 2, ws_of(b, 5, 2, 1000)) == (10, 10, True)
+    # keyless one-tuple V, W keyed by U: one pair and one key per U tuple
+    c = tre.Plan("ij,jk->ik", "i", {"i": 64 * 100, "j": 32, "k": 16}, {"i": 64})
+    assert tre.output_bounds(c, 37, 1, ws_of(c, 37, 1, 37)) == (37, 37, True)
+    # an empty side: nothing to bound
+    assert tre.output_bounds(a, 0, 50, ws_of(a, 0, 50, 0)) == (0, 0, True)
+    assert tre.output_bounds(b, 5, 0, ws_of(b, 5, 0, 0)) == (0, 0, True)
+    with pytest.raises(tre.TreError) as e:
+        tre.output_bounds(a, 8, 50, ws_of(a, 8, 50, 0) - 1)
+    assert e.value.status == "TRE_E_WORKSPACE"
