@@ -634,7 +634,10 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs g) {
 // the same scalar for the whole group) run contiguously in aligned groups; a
 // unit needing fewer than 256 threads shares its workgroup with other units.
 // The contracted-index tables sit in LDS; for K <= 2 the pair loop is unrolled
-// by four so four tiles are in flight per thread.
+// by four so four tiles are in flight per thread.  When several units share a
+// workgroup (SPAN), their pairs are consecutive, and the workgroup first
+// copies the pair indices of that span into LDS (up to kVecSpan of them), so
+// the tile loads of a group of pairs wait for no index load from memory.
 
 struct VecArgs {
     const void* U;
@@ -674,9 +677,12 @@ __device__ inline void load_vec(const T* p, float (&x)[EPT]) {
     }
 }
 
-template <typename T, int EPT, bool VB, int PU>
+constexpr int kVecSpan = 512;
+
+template <typename T, int EPT, bool VB, int PU, bool SPAN>
 __global__ __launch_bounds__(kThreads) void k_vec(VecArgs a) {
     __shared__ int32_t sKU[kVecMaxK], sKV[kVecMaxK];
+    __shared__ int32_t sPU[SPAN ? kVecSpan : 1], sPV[SPAN ? kVecSpan : 1];
     const bool lds_tables = a.K <= kVecMaxK;
     if (lds_tables) {
         for (int k = threadIdx.x; k < a.K; k += kThreads) {
@@ -688,7 +694,23 @@ __global__ __launch_bounds__(kThreads) void k_vec(VecArgs a) {
     const int64_t unit_id = int64_t(blockIdx.x) * a.upb + (a.upb > 1 ? threadIdx.x / a.tpu : 0);
     const int64_t ti = a.upb > 1 ? threadIdx.x % a.tpu : int64_t(blockIdx.y) * kThreads + threadIdx.x;
     const int64_t e0 = ti * EPT;
-    if (unit_id >= a.hdr->n_units || e0 >= a.w_elems) return;
+    const int64_t n_units = a.hdr->n_units;
+    int32_t s0 = 0, s1 = 0;  // the staged span of pairs (empty: none staged)
+    if constexpr (SPAN) {
+        // (every thread reaches the barrier: the tests below are uniform
+        // over the workgroup)
+        const int64_t u0 = int64_t(blockIdx.x) * a.upb;
+        if (u0 >= n_units) return;
+        s0 = a.units[u0].p0;
+        s1 = a.units[min<int64_t>(u0 + a.upb, n_units) - 1].p1;
+        if (s1 < s0 || s1 - s0 > kVecSpan) s1 = s0;
+        for (int i = threadIdx.x; i < s1 - s0; i += kThreads) {
+            sPU[i] = a.pu[s0 + i];
+            sPV[i] = a.pv[s0 + i];
+        }
+        __syncthreads();
+    }
+    if (unit_id >= n_units || e0 >= a.w_elems) return;
     const Unit un = a.units[unit_id];
     const T* U = reinterpret_cast<const T*>(a.U);
     const T* V = reinterpret_cast<const T*>(a.V);
@@ -712,27 +734,34 @@ __global__ __launch_bounds__(kThreads) void k_vec(VecArgs a) {
             for (int i = 0; i < EPT; i++) acc[i] = fmaf(x[i], y[i], acc[i]);
         }
     };
-    int p = un.p0;
-    if constexpr (PU > 1) {
-        for (; p + PU <= un.p1; p += PU) {
-            const T* ub[PU];
-            const T* vb[PU];
+    // the unit's pairs, their indices read through get_u / get_v
+    auto run_pairs = [&](auto get_u, auto get_v) {
+        int p = un.p0;
+        if constexpr (PU > 1) {
+            for (; p + PU <= un.p1; p += PU) {
+                const T* ub[PU];
+                const T* vb[PU];
 #pragma unroll
-            for (int j = 0; j < PU; j++) {
-                ub[j] = U + int64_t(a.pu[p + j]) * a.u_elems + eu;
-                vb[j] = V + int64_t(a.pv[p + j]) * a.v_elems + ev;
+                for (int j = 0; j < PU; j++) {
+                    ub[j] = U + int64_t(get_u(p + j)) * a.u_elems + eu;
+                    vb[j] = V + int64_t(get_v(p + j)) * a.v_elems + ev;
+                }
+                for (int k = 0; k < a.K; k++)
+#pragma unroll
+                    for (int j = 0; j < PU; j++) pair_step(ub[j], vb[j], k);
             }
-            for (int k = 0; k < a.K; k++)
-#pragma unroll
-                for (int j = 0; j < PU; j++) pair_step(ub[j], vb[j], k);
         }
-    }
-    for (; p < un.p1; p++) {
-        const T* ub = U + int64_t(a.pu[p]) * a.u_elems + eu;
-        const T* vb = V + int64_t(a.pv[p]) * a.v_elems + ev;
+        for (; p < un.p1; p++) {
+            const T* ub = U + int64_t(get_u(p)) * a.u_elems + eu;
+            const T* vb = V + int64_t(get_v(p)) * a.v_elems + ev;
 #pragma unroll 4
-        for (int k = 0; k < a.K; k++) pair_step(ub, vb, k);
-    }
+            for (int k = 0; k < a.K; k++) pair_step(ub, vb, k);
+        }
+    };
+    if (SPAN && un.p0 >= s0 && un.p1 <= s1)
+        run_pairs([&](int q) { return sPU[q - s0]; }, [&](int q) { return sPV[q - s0]; });
+    else
+        run_pairs([&](int q) { return a.pu[q]; }, [&](int q) { return a.pv[q]; });
     if (a.w_bf16 && un.slot < 0) {
         uint16_t* o = reinterpret_cast<uint16_t*>(a.W) + int64_t(un.seg) * a.w_elems + e0;
         if constexpr (EPT % 4 == 0) {
@@ -761,14 +790,19 @@ __global__ __launch_bounds__(kThreads) void k_vec(VecArgs a) {
     }
 }
 
-template <typename T, int EPT>
-hipError_t vec_dispatch(const Plan& p, const VecArgs& a, dim3 grid, hipStream_t s) {
+template <typename T, int EPT, bool SPAN>
+hipError_t vec_dispatch_s(const Plan& p, const VecArgs& a, dim3 grid, hipStream_t s) {
     const bool pu4 = p.nK <= 2;
     const dim3 block{unsigned(kThreads)};
-    if (p.vec_vbcast) return pu4 ? launch_k(k_vec<T, EPT, true, 4>, grid, block, 0, s, a)
-                                 : launch_k(k_vec<T, EPT, true, 1>, grid, block, 0, s, a);
-    return pu4 ? launch_k(k_vec<T, EPT, false, 4>, grid, block, 0, s, a)
-               : launch_k(k_vec<T, EPT, false, 1>, grid, block, 0, s, a);
+    if (p.vec_vbcast) return pu4 ? launch_k(k_vec<T, EPT, true, 4, SPAN>, grid, block, 0, s, a)
+                                 : launch_k(k_vec<T, EPT, true, 1, SPAN>, grid, block, 0, s, a);
+    return pu4 ? launch_k(k_vec<T, EPT, false, 4, SPAN>, grid, block, 0, s, a)
+               : launch_k(k_vec<T, EPT, false, 1, SPAN>, grid, block, 0, s, a);
+}
+
+template <typename T, int EPT>
+hipError_t vec_dispatch(const Plan& p, const VecArgs& a, dim3 grid, hipStream_t s) {
+    return a.upb > 1 ? vec_dispatch_s<T, EPT, true>(p, a, grid, s) : vec_dispatch_s<T, EPT, false>(p, a, grid, s);
 }
 
 // ---------------------------------------------------------------- reduce
