@@ -27,6 +27,7 @@ With --config N only that workload runs (no configs list).
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import os
 import sys
@@ -1107,37 +1108,44 @@ def measure(W, args, torch, tre, config, cpu_budget_s):
     steps = args.steps
     if config != HEADLINE and n_warm > 0:
         steps = max(steps, min(MAX_CFG_STEPS, int(MIN_TIMED_S / max(warm_s / n_warm, 1e-6))))
-    if args.warmup > 0:
-        # as many warm-up steps with the timed steps' deferred timing, read
-        # afterwards, so the library's event pool holds the events the timed
-        # steps take (events created inside the timed region once coincided
-        # with one step running 15x slower)
-        warm_t = []
-        for _ in range(steps):
+    # no garbage collection pass from here to the end of the timed region
+    # (as timeit does: a full pass once stalled a 0.67 ms step for 35 ms);
+    # the warm-up steps below run after the explicit one
+    gc.collect()
+    gc.disable()
+    try:
+        if args.warmup > 0:
+            # as many warm-up steps with the timed steps' deferred timing,
+            # read afterwards, so the library's event pool already holds the
+            # events the timed steps take
+            warm_t = []
+            for _ in range(steps):
+                tm = tre.Timing()
+                tm.deferred = 1
+                W.step(timing=tm)
+                warm_t.append(tm)
+            torch.cuda.synchronize()
+            for tm in warm_t:
+                tm.read()
+            n_warm += steps
+        torch.cuda.synchronize()
+        stages = W.stages()
+        dom = stages[0]
+        timings = []
+        log(f"[bench] config {config}: timing {steps} steps")
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        t0 = time.perf_counter()
+        evs[0].record()
+        for i in range(steps):
             tm = tre.Timing()
             tm.deferred = 1
             W.step(timing=tm)
-            warm_t.append(tm)
+            evs[i + 1].record()
+            timings.append(tm)
         torch.cuda.synchronize()
-        for tm in warm_t:
-            tm.read()
-        n_warm += steps
-    torch.cuda.synchronize()
-    stages = W.stages()
-    dom = stages[0]
-    timings = []
-    log(f"[bench] config {config}: timing {steps} steps")
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
-    t0 = time.perf_counter()
-    evs[0].record()
-    for i in range(steps):
-        tm = tre.Timing()
-        tm.deferred = 1
-        W.step(timing=tm)
-        evs[i + 1].record()
-        timings.append(tm)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+        wall = time.perf_counter() - t0
+    finally:
+        gc.enable()
     if hasattr(W, "check_async"):
         W.check_async()  # the asynchronous steps' counts and status, read after the timed region
     per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(steps)]
