@@ -1102,11 +1102,12 @@ def measure(W, args, torch, tre, config, cpu_budget_s):
             torch.cuda.synchronize()
     torch.cuda.synchronize()
     warm_s = time.perf_counter() - t_warm
-    # the headline times exactly --steps steps; a workload of short steps
-    # times more of them (about MIN_TIMED_S of work, at most MAX_CFG_STEPS), so
-    # that one slow step does not carry its mean
+    # the headline (and a workload chosen with --config) times exactly
+    # --steps steps; in the all-workload run, a workload of short steps times
+    # more of them (about MIN_TIMED_S of work, at most MAX_CFG_STEPS), so that
+    # one slow step does not carry its mean
     steps = args.steps
-    if config != HEADLINE and n_warm > 0:
+    if config != HEADLINE and args.config is None and n_warm > 0:
         steps = max(steps, min(MAX_CFG_STEPS, int(MIN_TIMED_S / max(warm_s / n_warm, 1e-6))))
     # no garbage collection pass from here to the end of the timed region
     # (as timeit does: a full pass once stalled a 0.67 ms step for 35 ms);
