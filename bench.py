@@ -1107,7 +1107,7 @@ def measure(W, args, torch, tre, config, cpu_budget_s):
     # more of them (about MIN_TIMED_S of work, at most MAX_CFG_STEPS), so that
     # one slow step does not carry its mean
     steps = args.steps
-    if config != HEADLINE and args.config is None and n_warm > 0:
+    if config != HEADLINE and not args.config and n_warm > 0:
         steps = max(steps, min(MAX_CFG_STEPS, int(MIN_TIMED_S / max(warm_s / n_warm, 1e-6))))
     # no garbage collection pass from here to the end of the timed region
     # (as timeit does: a full pass once stalled a 0.67 ms step for 35 ms);
