@@ -637,7 +637,8 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs g) {
 // by four so four tiles are in flight per thread.  When several units share a
 // workgroup (SPAN), their pairs are consecutive, and the workgroup first
 // copies the pair indices of that span into LDS (up to kVecSpan of them), so
-// the tile loads of a group of pairs wait for no index load from memory.
+// the tile loads of a group of pairs wait for no index load from memory;
+// when a pair's V factor is one scalar (y_scalar), its value is staged too.
 
 struct VecArgs {
     const void* U;
@@ -654,6 +655,7 @@ struct VecArgs {
     float* W;  // bf16 bits when w_bf16 (partials stay fp32)
     float* partials;
     int32_t w_bf16;
+    int32_t y_scalar;  // V broadcast, K = 1 and one-element V tiles: a pair's factor is V[pv]
 };
 
 constexpr int kVecMaxK = 2048;
@@ -683,6 +685,7 @@ template <typename T, int EPT, bool VB, int PU, bool SPAN>
 __global__ __launch_bounds__(kThreads) void k_vec(VecArgs a) {
     __shared__ int32_t sKU[kVecMaxK], sKV[kVecMaxK];
     __shared__ int32_t sPU[SPAN ? kVecSpan : 1], sPV[SPAN ? kVecSpan : 1];
+    __shared__ float sY[SPAN && VB ? kVecSpan : 1];
     const bool lds_tables = a.K <= kVecMaxK;
     if (lds_tables) {
         for (int k = threadIdx.x; k < a.K; k += kThreads) {
@@ -705,8 +708,11 @@ __global__ __launch_bounds__(kThreads) void k_vec(VecArgs a) {
         s1 = a.units[min<int64_t>(u0 + a.upb, n_units) - 1].p1;
         if (s1 < s0 || s1 - s0 > kVecSpan) s1 = s0;
         for (int i = threadIdx.x; i < s1 - s0; i += kThreads) {
+            const int32_t v = a.pv[s0 + i];
             sPU[i] = a.pu[s0 + i];
-            sPV[i] = a.pv[s0 + i];
+            sPV[i] = v;
+            if constexpr (VB)
+                if (a.y_scalar) sY[i] = ld_f(reinterpret_cast<const T*>(a.V) + v);
         }
         __syncthreads();
     }
@@ -758,10 +764,37 @@ __global__ __launch_bounds__(kThreads) void k_vec(VecArgs a) {
             for (int k = 0; k < a.K; k++) pair_step(ub, vb, k);
         }
     };
-    if (SPAN && un.p0 >= s0 && un.p1 <= s1)
+    const bool staged = SPAN && un.p0 >= s0 && un.p1 <= s1;
+    if (VB && staged && a.y_scalar) {
+        // the staged factors: only the U tiles are loaded (same order of
+        // the sums as pair_step's)
+        const int32_t ku0 = kU[0];
+        int p = un.p0;
+        if constexpr (PU > 1) {
+            for (; p + PU <= un.p1; p += PU) {
+                float x[PU][EPT];
+#pragma unroll
+                for (int j = 0; j < PU; j++) load_vec<T, EPT>(U + int64_t(sPU[p + j - s0]) * a.u_elems + eu + ku0, x[j]);
+#pragma unroll
+                for (int j = 0; j < PU; j++) {
+                    const float y = sY[p + j - s0];
+#pragma unroll
+                    for (int i = 0; i < EPT; i++) acc[i] = fmaf(x[j][i], y, acc[i]);
+                }
+            }
+        }
+        for (; p < un.p1; p++) {
+            float x[EPT];
+            load_vec<T, EPT>(U + int64_t(sPU[p - s0]) * a.u_elems + eu + ku0, x);
+            const float y = sY[p - s0];
+#pragma unroll
+            for (int i = 0; i < EPT; i++) acc[i] = fmaf(x[i], y, acc[i]);
+        }
+    } else if (staged) {
         run_pairs([&](int q) { return sPU[q - s0]; }, [&](int q) { return sPV[q - s0]; });
-    else
+    } else {
         run_pairs([&](int q) { return a.pu[q]; }, [&](int q) { return a.pv[q]; });
+    }
     if (a.w_bf16 && un.slot < 0) {
         uint16_t* o = reinterpret_cast<uint16_t*>(a.W) + int64_t(un.seg) * a.w_elems + e0;
         if constexpr (EPT % 4 == 0) {
@@ -1099,6 +1132,7 @@ hipError_t launch_contract(const Plan& p, const Layout& L, char* ws, const void*
     a.W = w_tiles;
     a.partials = parts;
     a.w_bf16 = p.opt.w_bf16;
+    a.y_scalar = p.vec_vbcast && p.nK == 1 && a.v_elems == 1;
     const int ept = p.vec_ept;
     const int64_t threads = (p.tile_elems[2] + ept - 1) / ept;
     dim3 grid;
