@@ -400,23 +400,24 @@ __global__ void k_dense(const int32_t* __restrict__ okeys, int64_t n_o, int ro, 
     const int64_t o = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (o >= n_o) return;
     if (o == 0) hdr->n_pairs = n_o;
-    if (VO && dout.n == 1 && wd.n == 1 && wd.src[0] == 1) {
-        // one join label and W keyed by one label of V (the outer relation,
-        // whose keys okeys are): the pair's join key, its W key and the
+    if (dout.n == 1 && wd.n == 1 && wd.src[0] == (VO ? 1 : 0)) {
+        // one join label and W keyed by one label of the outer relation
+        // (whose keys okeys are): the pair's join key, its W key and the
         // previous pair's W key are loaded at once (the general path below
         // waits for each in turn)
         const int32_t* row = okeys + o * ro;
         const int32_t jk = row[dout.pos[0]];
         const KT k = KT(uint32_t(row[wd.pos[0]]));
         const KT kp = o > 0 ? KT(uint32_t(row[wd.pos[0] - ro])) : k;
-        const int64_t u = min(max(jk, 0), ir.r[0] - 1);
+        const int64_t in = min(max(jk, 0), ir.r[0] - 1);
+        const int64_t u = VO ? in : o, v = VO ? o : in;
         wk[o] = k;
         if (uv) {
-            uv[o] = (uint64_t(uint32_t(u)) << 32) | uint64_t(uint32_t(o));
+            uv[o] = (uint64_t(uint32_t(u)) << 32) | uint64_t(uint32_t(v));
             return;
         }
         pu[o] = int32_t(u);
-        pv[o] = int32_t(o);
+        pv[o] = int32_t(v);
         if (first && uint64_t(k) < uint64_t(nk) && (o == 0 || kp != k)) first[k] = int32_t(o + 1);
         return;
     }
