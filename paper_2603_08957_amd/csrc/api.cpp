@@ -192,10 +192,9 @@ tre_status join_enqueue(tre_plan_t plan, const int32_t* u_keys, int64_t n_u, con
     if (e != hipSuccess) return dev_fail(e, "header");
     WsHeader* hdr = reinterpret_cast<WsHeader*>(w + L.hdr);
     if (p.opt.validate_keys) {
-        if ((e = launch_validate(u_keys, n_u, p.nk[0], p.radix[0], &hdr->err_u, s, n_u_dev)) != hipSuccess)
-            return dev_fail(e, "validate U");
-        if ((e = launch_validate(v_keys, n_v, p.nk[1], p.radix[1], &hdr->err_v, s)) != hipSuccess)
-            return dev_fail(e, "validate V");
+        const ValJob jobs[2] = {{u_keys, n_u, p.nk[0], p.radix[0], &hdr->err_u, n_u_dev},
+                                {v_keys, n_v, p.nk[1], p.radix[1], &hdr->err_v, nullptr}};
+        if ((e = launch_validate(jobs, 2, s)) != hipSuccess) return dev_fail(e, "validate");
     }
     if (n_u > 0 && n_v == 1 && keyed_by_u(p)) {
         // one pair and one group per U tuple: nothing to count

@@ -958,10 +958,12 @@ tre_status tre_execute3(const char* einsum, const char* upper, const int64_t* ex
         if (timing) std::memset(timing, 0, sizeof(*timing));
         return TRE_OK;
     }
-    if ((e = launch_validate(u_keys, n_u, d.ru, d.radix_u, &hdr->err_u, s)) != hipSuccess ||
-        (e = launch_validate(p_keys, n_p, 1, &d.radix_p, &hdr->err_p, s)) != hipSuccess ||
-        (e = launch_validate(q_keys, n_q, 1, &d.radix_q, &hdr->err_q, s)) != hipSuccess)
-        return dev_fail(e, "validate");
+    {
+        const ValJob jobs[3] = {{u_keys, n_u, d.ru, d.radix_u, &hdr->err_u, nullptr},
+                                {p_keys, n_p, 1, &d.radix_p, &hdr->err_p, nullptr},
+                                {q_keys, n_q, 1, &d.radix_q, &hdr->err_q, nullptr}};
+        if ((e = launch_validate(jobs, 3, s)) != hipSuccess) return dev_fail(e, "validate");
+    }
     int32_t* flag = static_cast<int32_t*>(at(L.flag));
     int32_t* pos = static_cast<int32_t*>(at(L.pos));
     int32_t* ip = static_cast<int32_t*>(at(L.ip));

@@ -55,15 +55,34 @@ __device__ inline uint64_t pack_row(const int32_t* row, const KeyDesc& d) {
 }
 
 // (dn: the tuple count on the device, at most n; null: n)
-__global__ void k_validate(const int32_t* __restrict__ keys, int64_t n, int r, Radix rad, int32_t* err,
-                           const int64_t* __restrict__ dn) {
-    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (dn) n = min(n, *dn);
+// Key validation of up to kValJobs relations in one launch: job j's rows take
+// blocks block0[j] .. block0[j + 1] - 1.  Per row: every attribute inside its
+// radix (flag 4), and strictly above the previous row (1: below, 2: equal).
+constexpr int kValJobs = 3;
+struct ValSet {
+    int32_t n_jobs;
+    const int32_t* keys[kValJobs];
+    int64_t n[kValJobs];
+    int32_t r[kValJobs];
+    int32_t* err[kValJobs];
+    const int64_t* dn[kValJobs];  // optional device row count (n is then a bound)
+    int64_t block0[kValJobs + 1];
+    Radix rad[kValJobs];
+};
+
+__global__ void k_validate(ValSet vs) {
+    const int64_t b = blockIdx.x;
+    int j = 0;
+    while (j + 1 < vs.n_jobs && b >= vs.block0[j + 1]) j++;
+    const int64_t i = (b - vs.block0[j]) * blockDim.x + threadIdx.x;
+    int64_t n = vs.n[j];
+    if (vs.dn[j]) n = min(n, *vs.dn[j]);
     if (i >= n) return;
+    const int r = vs.r[j];
     int flags = 0;
-    const int32_t* row = keys + i * r;
+    const int32_t* row = vs.keys[j] + i * r;
     for (int a = 0; a < r; a++)
-        if (row[a] < 0 || row[a] >= rad.r[a]) flags |= 4;
+        if (row[a] < 0 || row[a] >= vs.rad[j].r[a]) flags |= 4;
     if (i > 0) {
         const int32_t* prev = row - r;
         int c = 0;
@@ -71,7 +90,7 @@ __global__ void k_validate(const int32_t* __restrict__ keys, int64_t n, int r, R
         if (c == 0) flags |= 2;
         if (c > 0) flags |= 1;
     }
-    if (flags) atomicOr(err, flags);
+    if (flags) atomicOr(vs.err[j], flags);
 }
 
 __global__ void k_pack_join(const int32_t* __restrict__ keys, int64_t n, int r, KeyDesc d, uint64_t* __restrict__ out,
@@ -802,13 +821,34 @@ KeyDesc desc_v(const Plan& p) {
 
 }  // namespace
 
+hipError_t launch_validate(const ValJob* jobs, int n_jobs, hipStream_t s) {
+    ValSet vs{};
+    int64_t blocks = 0;
+    for (int k = 0; k < n_jobs; k++) {
+        const ValJob& jb = jobs[k];
+        if (jb.n <= 0 || jb.r == 0) continue;  // r == 0: at most one tuple, checked on the host
+        if (vs.n_jobs == kValJobs || jb.r > 26) return hipErrorInvalidValue;
+        const int j = vs.n_jobs++;
+        vs.keys[j] = jb.keys;
+        vs.n[j] = jb.n;
+        vs.r[j] = jb.r;
+        vs.err[j] = jb.err;
+        vs.dn[j] = jb.dn;
+        for (int a = 0; a < jb.r; a++) vs.rad[j].r[a] = jb.radix[a];
+        vs.block0[j] = blocks;
+        blocks += blocks_for(jb.n);
+    }
+    if (vs.n_jobs == 0) return hipSuccess;
+    vs.block0[vs.n_jobs] = blocks;
+    if (blocks > int64_t(0x7fffffff)) return hipErrorInvalidConfiguration;
+    k_validate<<<dim3(unsigned(blocks)), kThreads, 0, s>>>(vs);
+    return hipGetLastError();
+}
+
 hipError_t launch_validate(const int32_t* keys, int64_t n, int r, const int32_t* radix, int32_t* err_flag,
                            hipStream_t s, const int64_t* dn) {
-    if (n <= 0 || r == 0) return hipSuccess;  // r == 0: at most one tuple, checked on the host
-    Radix rad{};
-    for (int a = 0; a < r; a++) rad.r[a] = radix[a];
-    k_validate<<<blocks_for(n), kThreads, 0, s>>>(keys, n, r, rad, err_flag, dn);
-    return hipGetLastError();
+    const ValJob jb{keys, n, r, radix, err_flag, dn};
+    return launch_validate(&jb, 1, s);
 }
 
 hipError_t launch_join(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,

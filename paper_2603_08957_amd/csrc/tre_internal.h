@@ -188,6 +188,17 @@ hipError_t radix_sort_u32_pairs(uint32_t* keys, uint64_t* vals, uint32_t* keys_a
 // join.hip
 hipError_t launch_validate(const int32_t* keys, int64_t n, int r, const int32_t* radix, int32_t* err_flag,
                            hipStream_t s, const int64_t* dn = nullptr);
+// several relations (at most three) in one launch; jobs with no rows or no
+// key attributes are skipped
+struct ValJob {
+    const int32_t* keys;
+    int64_t n;
+    int r;
+    const int32_t* radix;  // host, r entries
+    int32_t* err;          // device flag word (bits 1 unsorted, 2 duplicate, 4 range)
+    const int64_t* dn;     // optional device row count
+};
+hipError_t launch_validate(const ValJob* jobs, int n_jobs, hipStream_t s);
 hipError_t launch_join(const Plan& p, const Layout& L, char* ws, const int32_t* u_keys, const int32_t* v_keys,
                        hipStream_t s, int stage);
 // A V-driven join where U's key is the join labels and U holds every key of
