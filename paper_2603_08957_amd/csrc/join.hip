@@ -1071,7 +1071,7 @@ bool u_dense(const Plan& p, int64_t n_v) {
 }
 
 bool v_dense(const Plan& p, int64_t n_u) {
-    if (!(p.v_outer && p.nk[0] == p.n_join && p.nk[0] > 0)) return false;
+    if (!(p.nk[0] == p.n_join && p.nk[0] > 0) || (!p.v_outer && p.v_needs_sort)) return false;
     int64_t space = 1;
     for (int i = 0; i < p.nk[0]; i++) {
         space *= p.radix[0][i];

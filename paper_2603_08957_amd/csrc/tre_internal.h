@@ -203,7 +203,9 @@ hipError_t launch_join(const Plan& p, const Layout& L, char* ws, const int32_t* 
                        hipStream_t s, int stage);
 // A V-driven join where U's key is the join labels and U holds every key of
 // that key space: U's index is the join key itself, one pair per V tuple,
-// written by the GROUP BY stage (the pair count is n_v, known on the host)
+// written by the GROUP BY stage (the pair count is n_v, known on the host).
+// Taken when V drives the plan's join, and also when U does but V's key
+// starts with the join labels: V's order is then (u, v) order as well.
 bool v_dense(const Plan& p, int64_t n_u);
 // The same with U driving: V's key is the join labels and V holds every key of
 // that key space (one pair per U tuple, the pair count n_u known on the host)

@@ -870,6 +870,39 @@ def test_u_dense_join_gpu(orc, idx, validate):
     check(out, orc.run(orc_plan(orc, spec), U, V), dtype)
 
 
+V_DENSE_PLANS = [
+    # (einsum, upper, extents, tiles, dtype): joins over a U that holds every
+    # key of its key space (U's key is the join labels) driven by V, also for
+    # plans whose join U drives but whose V key starts with the join labels
+    # (V's order is then (u, v) order), with and without the GROUP BY sort
+    ("ij,jk->ki", "jk", {"i": 16, "j": 32, "k": 24}, {"j": 4, "k": 4}, "f32"),     # the bf16 chain's E1 form: sorted
+    ("ij,jk->ki", "jk", {"i": 8, "j": 24, "k": 40}, {"j": 4, "k": 4}, "bf16"),
+    ("ij,kj->ki", "jk", {"i": 16, "j": 32, "k": 24}, {"j": 4, "k": 4}, "f32"),     # V keyed (K, J): V drives
+    ("j,jk->jk", "jk", {"j": 30, "k": 20}, {"j": 1, "k": 1}, "f32"),               # W keyed as V: no sort
+]
+
+
+@pytest.mark.parametrize("idx", range(len(V_DENSE_PLANS)))
+@pytest.mark.parametrize("validate", [True, False])
+def test_v_dense_join_gpu(orc, idx, validate):
+    """V-driven joins over a complete U (U's index is the join key itself),
+    with the one-workgroup join switched off so the dense pass runs: pairs,
+    keys and values against the oracle."""
+    import paper_2603_08957_amd as tre
+
+    e, upper, ext, til, dtype = V_DENSE_PLANS[idx]
+    rng = np.random.default_rng(760 + idx)
+    u_lab, v_lab, _ = split_einsum(e)
+    U = workloads.random_relation(rng, u_lab, upper, ext, til, dtype, keep=1.0, zero_frac=0.05)
+    V = workloads.random_relation(rng, v_lab, upper, ext, til, dtype, keep=0.4, zero_frac=0.05)
+    spec = workloads.spec(e, upper, ext, til, dtype)
+    plan = tre.Plan.from_spec(spec, validate=validate, small_join=-1)
+    say("v dense", idx, validate, e, plan.join_outer, len(U["keys"]), len(V["keys"]))
+    out = tre.einsum(plan, *to_dev(U), *to_dev(V), want_pairs=True, timing=True)
+    assert out.timing["join_path"] == "v_driven_dense", out.timing
+    check(out, orc.run(orc_plan(orc, spec), U, V), dtype)
+
+
 # ------------------------------------------------------------ tre_execute
 
 def _execute(spec, U, V, w_cap=None, max_pairs=None, **plan_kw):
