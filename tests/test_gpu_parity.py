@@ -1255,3 +1255,30 @@ def test_execute_async_errors_gpu():
     spec2 = workloads.spec("ia,ka->ik", "ik", ext2, til2, "f32")
     out2, c4, ok2 = _execute_async(spec2, U2, V2)
     assert not ok2 and c4[2] == 0 and c4[0] == 10000 and c4[1] == 10000
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("keep,pmax", [(0.01, 1000), (0.2, 1000), (0.2, 0)])
+def test_vec_staged_span_gpu(orc, dtype, keep, pmax):
+    """Vector class with many units per workgroup (16-element W tiles: 64
+    units per workgroup in fp32, 128 in bf16): a workgroup stages its units'
+    pair indices (and, V being scalar tiles, each pair's factor) in LDS when
+    their span holds at most 512 pairs, and reads them from memory when it
+    does not.  One unit per key (pmax 1000) with about 3 pairs per key
+    (keep 0.01) stages; with about 60 (keep 0.2) it does not; the default
+    unit length (pmax 0) cuts those keys into short units, staged, with
+    partial tiles summed afterwards.  All against the oracle."""
+    import paper_2603_08957_amd as tre
+
+    e, upper = "ij,kj->ki", "jk"
+    ext, til = {"i": 16, "j": 300, "k": 900}, {"j": 1, "k": 1}
+    rng = np.random.default_rng(7100 + int(keep * 100) + 7 * (dtype == "bf16") + (pmax > 0))
+    U = workloads.random_relation(rng, "ij", upper, ext, til, dtype, keep=1.0, zero_frac=0.05)
+    V = workloads.random_relation(rng, "kj", upper, ext, til, dtype, keep=keep, zero_frac=0.05)
+    spec = workloads.spec(e, upper, ext, til, dtype)
+    plan = tre.Plan.from_spec(spec, max_pairs_per_unit=pmax)
+    assert plan.kernel_class == "vec"
+    say("vec staged span", dtype, keep, pmax, len(U["keys"]), len(V["keys"]))
+    out = tre.einsum(plan, *to_dev(U), *to_dev(V), want_pairs=True, timing=True)
+    assert out.timing["contract_path"] == "vec", out.timing
+    check(out, orc.run(orc_plan(orc, spec), U, V), dtype)
