@@ -6,8 +6,12 @@ A step is one pass of the whole hot path over one batch of synthetic input
 that is already resident in HBM: for the default workload (the bf16 GNN
 message-passing chain (X.Y)^T.Z on a 262,144-vertex power-law graph with
 128x128 tiles) that is E1 = join X with Y on J + tile contraction + group by
-K, the fp32 -> bf16 cast of T, and E2 = cross product of T with Z + tile
-contraction.  Prints one JSON line:
+K, writing T in bf16 (its fp32 sums rounded in the contraction), and E2 =
+cross product of T with Z + tile contraction; workloads 1-3 enqueue their
+steps through tre_execute_async (no host wait inside a step).  Warm-up runs
+at least a quarter of a second, then as many steps with the timed steps'
+deferred timing; Python's garbage collector is off from there to the end
+of the timed region.  Prints one JSON line:
 
   value       effective tile GFLOP/s of the step = sum over EinSums of
               (matched pairs x dense tile flops per pair) / step time
