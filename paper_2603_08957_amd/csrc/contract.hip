@@ -634,11 +634,13 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs g) {
 // the same scalar for the whole group) run contiguously in aligned groups; a
 // unit needing fewer than 256 threads shares its workgroup with other units.
 // The contracted-index tables sit in LDS; for K <= 2 the pair loop is unrolled
-// by four so four tiles are in flight per thread.  When several units share a
-// workgroup (SPAN), their pairs are consecutive, and the workgroup first
-// copies the pair indices of that span into LDS (up to kVecSpan of them), so
-// the tile loads of a group of pairs wait for no index load from memory;
-// when a pair's V factor is one scalar (y_scalar), its value is staged too.
+// by four so four tiles are in flight per thread.  A workgroup first copies
+// the pair indices of its units' span into LDS (their pairs are consecutive;
+// up to kVecSpan of them), so the tile loads of a group of pairs wait for no
+// index load from memory; when a pair's V factor is one scalar (y_scalar),
+// its value is staged too and only the U tiles are loaded per pair (the
+// attention projections, one unit of about 38 pairs per workgroup: 0.131 ->
+// 0.082 ms each).
 
 struct VecArgs {
     const void* U;
@@ -681,11 +683,11 @@ __device__ inline void load_vec(const T* p, float (&x)[EPT]) {
 
 constexpr int kVecSpan = 512;
 
-template <typename T, int EPT, bool VB, int PU, bool SPAN>
+template <typename T, int EPT, bool VB, int PU>
 __global__ __launch_bounds__(kThreads) void k_vec(VecArgs a) {
     __shared__ int32_t sKU[kVecMaxK], sKV[kVecMaxK];
-    __shared__ int32_t sPU[SPAN ? kVecSpan : 1], sPV[SPAN ? kVecSpan : 1];
-    __shared__ float sY[SPAN && VB ? kVecSpan : 1];
+    __shared__ int32_t sPU[kVecSpan], sPV[kVecSpan];
+    __shared__ float sY[VB ? kVecSpan : 1];
     const bool lds_tables = a.K <= kVecMaxK;
     if (lds_tables) {
         for (int k = threadIdx.x; k < a.K; k += kThreads) {
@@ -698,24 +700,21 @@ __global__ __launch_bounds__(kThreads) void k_vec(VecArgs a) {
     const int64_t ti = a.upb > 1 ? threadIdx.x % a.tpu : int64_t(blockIdx.y) * kThreads + threadIdx.x;
     const int64_t e0 = ti * EPT;
     const int64_t n_units = a.hdr->n_units;
-    int32_t s0 = 0, s1 = 0;  // the staged span of pairs (empty: none staged)
-    if constexpr (SPAN) {
-        // (every thread reaches the barrier: the tests below are uniform
-        // over the workgroup)
-        const int64_t u0 = int64_t(blockIdx.x) * a.upb;
-        if (u0 >= n_units) return;
-        s0 = a.units[u0].p0;
-        s1 = a.units[min<int64_t>(u0 + a.upb, n_units) - 1].p1;
-        if (s1 < s0 || s1 - s0 > kVecSpan) s1 = s0;
-        for (int i = threadIdx.x; i < s1 - s0; i += kThreads) {
-            const int32_t v = a.pv[s0 + i];
-            sPU[i] = a.pu[s0 + i];
-            sPV[i] = v;
-            if constexpr (VB)
-                if (a.y_scalar) sY[i] = ld_f(reinterpret_cast<const T*>(a.V) + v);
-        }
-        __syncthreads();
+    // the staged span of pairs (empty: none staged); every thread reaches
+    // the barrier (the tests before it are uniform over the workgroup)
+    const int64_t u0 = int64_t(blockIdx.x) * a.upb;
+    if (u0 >= n_units) return;
+    const int32_t s0 = a.units[u0].p0;
+    int32_t s1 = a.units[min<int64_t>(u0 + a.upb, n_units) - 1].p1;
+    if (s1 < s0 || s1 - s0 > kVecSpan) s1 = s0;
+    for (int i = threadIdx.x; i < s1 - s0; i += kThreads) {
+        const int32_t v = a.pv[s0 + i];
+        sPU[i] = a.pu[s0 + i];
+        sPV[i] = v;
+        if constexpr (VB)
+            if (a.y_scalar) sY[i] = ld_f(reinterpret_cast<const T*>(a.V) + v);
     }
+    __syncthreads();
     if (unit_id >= n_units || e0 >= a.w_elems) return;
     const Unit un = a.units[unit_id];
     const T* U = reinterpret_cast<const T*>(a.U);
@@ -764,7 +763,7 @@ __global__ __launch_bounds__(kThreads) void k_vec(VecArgs a) {
             for (int k = 0; k < a.K; k++) pair_step(ub, vb, k);
         }
     };
-    const bool staged = SPAN && un.p0 >= s0 && un.p1 <= s1;
+    const bool staged = un.p0 >= s0 && un.p1 <= s1;
     if (VB && staged && a.y_scalar) {
         // the staged factors: only the U tiles are loaded (same order of
         // the sums as pair_step's)
@@ -823,19 +822,14 @@ __global__ __launch_bounds__(kThreads) void k_vec(VecArgs a) {
     }
 }
 
-template <typename T, int EPT, bool SPAN>
-hipError_t vec_dispatch_s(const Plan& p, const VecArgs& a, dim3 grid, hipStream_t s) {
-    const bool pu4 = p.nK <= 2;
-    const dim3 block{unsigned(kThreads)};
-    if (p.vec_vbcast) return pu4 ? launch_k(k_vec<T, EPT, true, 4, SPAN>, grid, block, 0, s, a)
-                                 : launch_k(k_vec<T, EPT, true, 1, SPAN>, grid, block, 0, s, a);
-    return pu4 ? launch_k(k_vec<T, EPT, false, 4, SPAN>, grid, block, 0, s, a)
-               : launch_k(k_vec<T, EPT, false, 1, SPAN>, grid, block, 0, s, a);
-}
-
 template <typename T, int EPT>
 hipError_t vec_dispatch(const Plan& p, const VecArgs& a, dim3 grid, hipStream_t s) {
-    return a.upb > 1 ? vec_dispatch_s<T, EPT, true>(p, a, grid, s) : vec_dispatch_s<T, EPT, false>(p, a, grid, s);
+    const bool pu4 = p.nK <= 2;
+    const dim3 block{unsigned(kThreads)};
+    if (p.vec_vbcast) return pu4 ? launch_k(k_vec<T, EPT, true, 4>, grid, block, 0, s, a)
+                                 : launch_k(k_vec<T, EPT, true, 1>, grid, block, 0, s, a);
+    return pu4 ? launch_k(k_vec<T, EPT, false, 4>, grid, block, 0, s, a)
+               : launch_k(k_vec<T, EPT, false, 1>, grid, block, 0, s, a);
 }
 
 // ---------------------------------------------------------------- reduce
