@@ -843,8 +843,9 @@ __global__ __launch_bounds__(kThreads) void k_reduce(const int32_t* __restrict__
     if (x >= hdr->n_split) return;
     const int32_t s = split[x];
     const int32_t first = poff[s], cnt = poff[s + 1] - poff[s];
-    if (w_elems % 4 == 0 && !w_bf16) {
+    if (w_elems % 4 == 0) {
         // 16-byte lanes; partials are read once, so they bypass L2 retention
+        // (a bf16 W takes the four sums of a lane as one 8-byte store)
         const int64_t q = w_elems / 4;
         for (int64_t e = int64_t(blockIdx.y) * kThreads + threadIdx.x; e < q; e += int64_t(gridDim.y) * kThreads) {
             const f32x4* src = reinterpret_cast<const f32x4*>(parts) + int64_t(first) * q + e;
@@ -859,7 +860,13 @@ __global__ __launch_bounds__(kThreads) void k_reduce(const int32_t* __restrict__
                 for (int i = 0; i < kReduceBatch; i++) acc += v[i];
             }
             for (; j < cnt; j++) acc += __builtin_nontemporal_load(src + int64_t(j) * q);
-            reinterpret_cast<f32x4*>(W)[int64_t(s) * q + e] = acc;
+            if (w_bf16) {
+                const uint32_t lo = uint32_t(f32_to_bf16_rne(acc[0])) | (uint32_t(f32_to_bf16_rne(acc[1])) << 16);
+                const uint32_t hi = uint32_t(f32_to_bf16_rne(acc[2])) | (uint32_t(f32_to_bf16_rne(acc[3])) << 16);
+                reinterpret_cast<uint2*>(W)[int64_t(s) * q + e] = make_uint2(lo, hi);
+            } else {
+                reinterpret_cast<f32x4*>(W)[int64_t(s) * q + e] = acc;
+            }
         }
         return;
     }
