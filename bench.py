@@ -88,11 +88,13 @@ class Stage:
         algorithmic HBM rates: the join reads the int32 keys once and writes
         the (u, v) pair list and the segment table once; the contraction
         reads every input tuple once and writes every output tile once; the
-        reduction reads and writes partial tiles of split keys only."""
+        reduction reads the partial tiles of split keys once (always fp32)
+        and writes their W tiles once (in W's dtype)."""
         t = self.record
         jb = 4 * (self.n_u * self.plan.key_arity[0] + self.n_v * self.plan.key_arity[1]) + 8 * self.n_pairs \
             + 12 * self.n_w
-        rb = (t.n_partials + t.n_split_segments) * self.tile_bytes(2) if t.n_split_segments else 0
+        rb = (t.n_partials * 4 * self.plan.tile_elems[2] + t.n_split_segments * self.tile_bytes(2)
+              if t.n_split_segments else 0)
         gbs = lambda b, ms: (b / (ms * 1e-3) / 1e9) if ms > 0 else None  # noqa: E731
         return {"join_ms": t.join_ms, "join_alg_bytes": jb, "join_GBs": gbs(jb, t.join_ms),
                 "contract_ms": t.contract_ms, "contract_alg_bytes": self.alg_bytes(),
