@@ -437,6 +437,8 @@ __device__ inline void run_unit(const FastArgs& g, const Unit& un, int m0, int n
     // (its LDS may be handed to another workgroup)
     __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
 
+    // non-temporal stores: an output block is written once per launch, and
+    // keeping its lines out of L2 leaves room for the reused operand's tiles
 #pragma unroll
     for (int i = 0; i < 2; i++)
 #pragma unroll
@@ -445,8 +447,8 @@ __device__ inline void run_unit(const FastArgs& g, const Unit& un, int m0, int n
 #pragma unroll
             for (int r = 0; r < 16; r++) {
                 const int m = m0 + wm * 64 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-                if (out16) out16[int64_t(m) * g.ldw + n] = f32_to_bf16_rne(acc[i][j][r]);
-                else out[int64_t(m) * g.ldw + n] = acc[i][j][r];
+                if (out16) __builtin_nontemporal_store(f32_to_bf16_rne(acc[i][j][r]), out16 + int64_t(m) * g.ldw + n);
+                else __builtin_nontemporal_store(acc[i][j][r], out + int64_t(m) * g.ldw + n);
             }
         }
 }
