@@ -75,9 +75,11 @@ int32_t choose_pacing(const Plan& p, int64_t n_u, int64_t n_pairs, int64_t n_w, 
         const int64_t u_bytes = n_u * p.tile_elems[0] * (p.dtype == TRE_BF16 ? 2 : 4);
         const int64_t reuse = n_pairs / n_u;
         if (u_bytes <= (int64_t(16) << 20) || reuse < 64 || n_w < slots) return 0;
-        // ~4 MB of U per window: measured best on the 262,144-vertex chain
-        // (2 MB windows wait more often, 8 MB windows miss L2)
-        W = (u_bytes + (int64_t(4) << 20) - 1) >> 22;
+        // ~5.5 MB of U per window: measured best on the 262,144-vertex chain
+        // (12 windows of its 64 MB; 16 or 10 windows are 0.5% slower, 8 and
+        // 24 windows 1-3%: small windows wait more often, large ones miss L2)
+        constexpr int64_t kWindowBytes = int64_t(11) << 19;
+        W = (u_bytes + kWindowBytes - 1) / kWindowBytes;
     }
     W = std::max<int64_t>(1, std::min<int64_t>({W, n_u, 256}));
     const int64_t n_wg = std::min(n_w, slots);
