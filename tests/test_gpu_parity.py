@@ -228,6 +228,41 @@ def test_split_segments_gpu(orc, pmax):
     check(out, ref, "f32")
 
 
+W_BF16_SPLIT = [
+    # (einsum, upper, extents, tiles, plan options): bf16 inputs, keys cut
+    # into several units, W written in bf16 by the segmented sum
+    ("ik,kj->ij", "ijk", {"i": 256, "j": 256, "k": 1024}, {"i": 128, "j": 128, "k": 128}, {"max_pairs_per_unit": 3}),
+    ("ik,kj->ij", "ijk", {"i": 256, "j": 256, "k": 1024}, {"i": 128, "j": 128, "k": 128}, {"u_ranges": 2}),
+    ("ij,jk->ki", "jk", {"i": 64, "j": 300, "k": 40}, {"j": 1, "k": 1}, {"max_pairs_per_unit": 3}),  # 64-element W tiles
+    ("ij,jk->ki", "jk", {"i": 6, "j": 300, "k": 40}, {"j": 1, "k": 1}, {"max_pairs_per_unit": 3}),   # 6-element W tiles
+]
+
+
+@pytest.mark.parametrize("idx", range(len(W_BF16_SPLIT)))
+def test_split_segments_bf16_w_gpu(orc, idx):
+    """Keys cut into several units with W written in bf16: the partial tiles
+    (fp32) are summed in unit order and rounded once, four elements per lane
+    when a W tile holds a multiple of 4 elements and one otherwise; keys,
+    pairs and the upcast values against the oracle (Sec. 5, the GROUP BY
+    sum of the matched tile products)."""
+    import torch
+
+    import paper_2603_08957_amd as tre
+
+    e, upper, ext, til, opts = W_BF16_SPLIT[idx]
+    rng = np.random.default_rng(940 + idx)
+    u_lab, v_lab, _ = split_einsum(e)
+    U = workloads.random_relation(rng, u_lab, upper, ext, til, "bf16", keep=0.9)
+    V = workloads.random_relation(rng, v_lab, upper, ext, til, "bf16", keep=0.9)
+    spec = workloads.spec(e, upper, ext, til, "bf16")
+    plan = tre.Plan.from_spec(spec, w_bf16=True, **opts)
+    say("split bf16 W", idx, e, opts, plan.kernel_class, len(U["keys"]), len(V["keys"]))
+    out = tre.einsum(plan, *to_dev(U), *to_dev(V), want_pairs=True, timing=True)
+    assert out.w_tiles.dtype == torch.bfloat16
+    assert out.timing["n_split_segments"] > 0, out.timing
+    check(out, orc.run(orc_plan(orc, spec), U, V), "bf16")
+
+
 @pytest.mark.parametrize("c", [1, 2, 3, 4, 5])
 def test_small_configs_gpu(orc, c):
     """Scaled-down twins of the five workloads, every EinSum of each."""
